@@ -1,0 +1,184 @@
+"""UniSVQ fp64 CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+Thin ctypes wrapper around ``oracle.c``: a plain, slow, obviously correct
+implementation of the UniSVQ inference product (Sec. 3.1 Eq. 4 decode, Sec.
+3.2.3 Eq. 8 stacking along the input dimension, Sec. 2.1 Eq. 1 product) and of
+the packed byte format.  Only ``tests/``, the smoke check and the benchmark's
+CPU-baseline leg may import this package; the product path never does.  It
+shares no code with the HIP library.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile oracle.c into liboracle.so with the host C compiler (gcc)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-pthread",
+                               _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    i64, p = ctypes.c_int64, ctypes.c_void_p
+    lib.oracle_half_to_double.argtypes = [ctypes.c_uint16]
+    lib.oracle_half_to_double.restype = ctypes.c_double
+    lib.oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
+    lib.oracle_bf16_to_double.restype = ctypes.c_double
+    lib.oracle_half_array_to_double.argtypes = [p, p, i64]
+    lib.oracle_half_array_to_double.restype = None
+    lib.oracle_bf16_array_to_double.argtypes = [p, p, i64]
+    lib.oracle_bf16_array_to_double.restype = None
+    lib.oracle_packed_bytes.argtypes = [i64, i64]
+    lib.oracle_packed_bytes.restype = i64
+    lib.oracle_pack.argtypes = [i64, i64, p, p, p, p]
+    lib.oracle_pack.restype = i64
+    lib.oracle_unpack.argtypes = [i64, i64, p, p, p, p]
+    lib.oracle_unpack.restype = ctypes.c_int
+    lib.oracle_decode.argtypes = [i64, i64, p, p, p, p]
+    lib.oracle_decode.restype = ctypes.c_int
+    lib.oracle_decode_packed_rows.argtypes = [i64, i64, p, i64, i64, p]
+    lib.oracle_decode_packed_rows.restype = ctypes.c_int
+    lib.oracle_matmul_rows.argtypes = [i64, i64, p, i64, p, i64, p, p, ctypes.c_int]
+    lib.oracle_matmul_rows.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"], "oracle arrays must be C-contiguous"
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _bits16(a: np.ndarray) -> np.ndarray:
+    """fp16 / bf16-bit arrays are passed as raw uint16 bits."""
+    if a.dtype == np.float16:
+        return np.ascontiguousarray(a).view(np.uint16)
+    assert a.dtype == np.uint16, a.dtype
+    return np.ascontiguousarray(a)
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _check(rc: int, what: str) -> int:
+    if rc < 0:
+        raise OracleError(f"{what} failed with status {rc}")
+    return rc
+
+
+def half_to_double(bits: np.ndarray) -> np.ndarray:
+    lib = _load()
+    b = np.ascontiguousarray(bits, dtype=np.uint16)
+    out = np.empty(b.shape, dtype=np.float64)
+    lib.oracle_half_array_to_double(_ptr(b), _ptr(out), b.size)
+    return out
+
+
+def bf16_to_double(bits: np.ndarray) -> np.ndarray:
+    lib = _load()
+    b = np.ascontiguousarray(bits, dtype=np.uint16)
+    out = np.empty(b.shape, dtype=np.float64)
+    lib.oracle_bf16_array_to_double(_ptr(b), _ptr(out), b.size)
+    return out
+
+
+def packed_bytes(N: int, K: int) -> int:
+    return _check(_load().oracle_packed_bytes(N, K), "packed_bytes")
+
+
+def pack(Q: np.ndarray, A: np.ndarray, B: np.ndarray):
+    """Pack canonical arrays; returns (packed uint8 bytes, number of codes > 3)."""
+    lib = _load()
+    N, K = Q.shape
+    Q = np.ascontiguousarray(Q, dtype=np.uint8)
+    Ab, Bb = _bits16(A), _bits16(B)
+    assert Ab.shape == (N, K // 128, 4, 4) and Bb.shape == (N, K // 128, 4)
+    out = np.empty(packed_bytes(N, K), dtype=np.uint8)
+    bad = _check(lib.oracle_pack(N, K, _ptr(Q), _ptr(Ab), _ptr(Bb), _ptr(out)), "pack")
+    return out, int(bad)
+
+
+def unpack(packed: np.ndarray, N: int, K: int):
+    """Inverse of pack: returns (Q uint8, A fp16, B fp16)."""
+    lib = _load()
+    packed = np.ascontiguousarray(packed, dtype=np.uint8)
+    assert packed.size == packed_bytes(N, K)
+    Q = np.empty((N, K), dtype=np.uint8)
+    A = np.empty((N, K // 128, 4, 4), dtype=np.uint16)
+    B = np.empty((N, K // 128, 4), dtype=np.uint16)
+    _check(lib.oracle_unpack(N, K, _ptr(packed), _ptr(Q), _ptr(A), _ptr(B)), "unpack")
+    return Q, A.view(np.float16), B.view(np.float16)
+
+
+def decode(Q: np.ndarray, A: np.ndarray, B: np.ndarray) -> np.ndarray:
+    """fp64 dequantised weights W_hat [N][K] from canonical arrays."""
+    lib = _load()
+    N, K = Q.shape
+    Q = np.ascontiguousarray(Q, dtype=np.uint8)
+    Ab, Bb = _bits16(A), _bits16(B)
+    W = np.empty((N, K), dtype=np.float64)
+    _check(lib.oracle_decode(N, K, _ptr(Q), _ptr(Ab), _ptr(Bb), _ptr(W)), "decode")
+    return W
+
+
+def decode_packed_rows(packed: np.ndarray, N: int, K: int, r0: int, r1: int) -> np.ndarray:
+    lib = _load()
+    packed = np.ascontiguousarray(packed, dtype=np.uint8)
+    W = np.empty((r1 - r0, K), dtype=np.float64)
+    _check(lib.oracle_decode_packed_rows(N, K, _ptr(packed), r0, r1, _ptr(W)), "decode_packed_rows")
+    return W
+
+
+def default_threads() -> int:
+    try:
+        return max(1, len(os.sched_getaffinity(0)))
+    except AttributeError:  # pragma: no cover
+        return os.cpu_count() or 1
+
+
+def matmul(packed: np.ndarray, N: int, K: int, X: np.ndarray, rows=None, threads: int | None = None):
+    """Y = X * W_hat^T in fp64 from packed bytes.
+
+    X is [M][K] (any float dtype; converted exactly to fp64).  With ``rows``
+    given, only those output columns are computed and Y is [M][len(rows)].
+    """
+    lib = _load()
+    packed = np.ascontiguousarray(packed, dtype=np.uint8)
+    assert packed.size == packed_bytes(N, K)
+    X = np.ascontiguousarray(X, dtype=np.float64)
+    if X.ndim == 1:
+        X = X[None, :]
+    M = X.shape[0]
+    assert X.shape[1] == K
+    if threads is None:
+        threads = default_threads()
+    if rows is None:
+        Y = np.empty((M, N), dtype=np.float64)
+        _check(lib.oracle_matmul_rows(N, K, _ptr(packed), M, _ptr(X), N, None, _ptr(Y), threads),
+               "matmul")
+    else:
+        r = np.ascontiguousarray(rows, dtype=np.int64)
+        Y = np.empty((M, r.size), dtype=np.float64)
+        _check(lib.oracle_matmul_rows(N, K, _ptr(packed), M, _ptr(X), r.size, _ptr(r), _ptr(Y),
+                                      threads), "matmul_rows")
+    return Y

@@ -1,0 +1,328 @@
+/*
+ * UniSVQ reference oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Plain, slow, obviously-correct CPU implementation (fp64) of what the
+ * UniSVQ inference path computes.  Only tests/, the smoke check and the
+ * CPU-baseline leg of the benchmark may load this code; the product library
+ * never does.  It shares no code, header, table or helper with the HIP path:
+ * the packed byte format is re-implemented here from its written definition
+ * (the format block in include/unisvq.h, restated below).
+ *
+ * What is computed (paper: "UniSVQ: 2-bit Unified Scalar-Vector
+ * Quantization"):
+ *   - Each weight vector of d = 4 consecutive input columns of one output row
+ *     is rebuilt as an affine image of its integer lattice point,
+ *     w_hat = A * q + B, q in {0,1,2,3}^4                      (Sec. 3.1, Eq. 4)
+ *   - The dequantised matrix is the stack of those vectors along the input
+ *     dimension; vector i covers input columns 4i..4i+3          (Sec. 3.2.3, Eq. 8)
+ *   - The layer output is Y = X * W_hat^T                       (Sec. 2.1, Eq. 1)
+ *   - Codes are the unsigned integers 0..2^bits-1; the centring constant of
+ *     the initialisation lives in B                              (Sec. 3.2.2, Eq. 6; App. A.1)
+ *   - One (A, B) pair is held per (output row, 128-column group); the paper's
+ *     one-pair-per-matrix setting (Sec. 4.2) is the special case where all
+ *     pairs are equal.
+ *
+ * Packed format (restated from its definition; byte offsets little endian):
+ *   N % 16 == 0, K % 128 == 0.  Row block rb (rows 16rb..16rb+15) occupies
+ *   (K/128)*1152 consecutive bytes starting at rb*(K/128)*1152.  Inside it the
+ *   groups g = 0..K/128-1 are taken in pairs: packet p holds groups 2p, 2p+1
+ *   (2304 bytes) and, when K/128 is odd, a final half packet holds the last
+ *   group (1152 bytes).  Slot s = 0..63 stands for row r = 16rb + s/4 and
+ *   component b = s%4.
+ *     full packet at offset P:
+ *       P +       16s + 8j : 8-byte code field F(r, 2p+j, b)      j = 0,1
+ *       P + 1024 + 16s + 8j : A[r][2p+j][a][b], a = 0..3 (fp16 each)
+ *       P + 2048 +  4s + 2j : B[r][2p+j][b] (fp16)
+ *     half packet at offset P (group g):
+ *       P +        8s : F(r, g, b);  P + 512 + 8s : A[r][g][0..3][b];
+ *       P + 1024 + 2s : B[r][g][b]
+ *   Code field F(r, g, b) is a 64-bit little-endian word whose bits 2v, 2v+1
+ *   hold Q[r][128g + 4v + b], v = 0..31.
+ *
+ * Canonical (unpacked) arrays:
+ *   Q uint8  [N][K]           codes, valid values 0..3
+ *   A fp16   [N][K/128][4][4] A[r][g][a][b] multiplies q_b into output a
+ *   B fp16   [N][K/128][4]
+ *   X double [M][K], Y double [M][N]
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define OR_D 4
+#define OR_G 128
+#define OR_ROWBLOCK 16
+#define OR_GROUP_BYTES_PER_BLOCK 1152 /* 16 rows * (32 code bytes + 40 affine bytes) */
+
+enum { OR_OK = 0, OR_EINVAL = -1, OR_ESHAPE = -2 };
+
+/* ---- scalar conversions, written from the IEEE-754 / bfloat16 definitions ---- */
+
+/* binary16: 1 sign bit, 5 exponent bits (bias 15), 10 fraction bits. */
+double oracle_half_to_double(uint16_t h) {
+    int sign = (h >> 15) & 1;
+    int e = (h >> 10) & 0x1f;
+    int f = h & 0x3ff;
+    double v;
+    if (e == 0)
+        v = ldexp((double)f, -24); /* subnormal: f * 2^-14 * 2^-10 */
+    else if (e == 31)
+        v = f ? NAN : INFINITY;
+    else
+        v = ldexp((double)(1024 + f), e - 25); /* (1 + f/1024) * 2^(e-15) */
+    return sign ? -v : v;
+}
+
+/* bfloat16: the upper 16 bits of a binary32. */
+double oracle_bf16_to_double(uint16_t h) {
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+void oracle_half_array_to_double(const uint16_t* h, double* out, int64_t n) {
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_half_to_double(h[i]);
+}
+
+void oracle_bf16_array_to_double(const uint16_t* h, double* out, int64_t n) {
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_bf16_to_double(h[i]);
+}
+
+/* ---- packed format ---- */
+
+static int shape_ok(int64_t N, int64_t K) {
+    return N > 0 && K > 0 && N % OR_ROWBLOCK == 0 && K % OR_G == 0;
+}
+
+int64_t oracle_packed_bytes(int64_t N, int64_t K) {
+    if (!shape_ok(N, K)) return OR_ESHAPE;
+    return (N / OR_ROWBLOCK) * (K / OR_G) * OR_GROUP_BYTES_PER_BLOCK;
+}
+
+/* Where the three parts of group g of row block rb live, and at what stride
+ * per slot.  Returns byte offsets of slot 0. */
+typedef struct {
+    int64_t code, a, b;   /* offsets of slot 0 */
+    int64_t code_stride;  /* bytes between slots in the code area */
+    int64_t a_stride;     /* bytes between slots in the A area */
+    int64_t b_stride;     /* bytes between slots in the B area */
+} group_place;
+
+static group_place place_group(int64_t K, int64_t rb, int64_t g) {
+    int64_t groups = K / OR_G;
+    int64_t base = rb * groups * OR_GROUP_BYTES_PER_BLOCK;
+    int64_t p = g / 2, j = g % 2;
+    int64_t pkt = base + p * 2 * OR_GROUP_BYTES_PER_BLOCK;
+    group_place gp;
+    int half = (groups % 2 == 1) && (g == groups - 1);
+    if (!half) {
+        gp.code = pkt + 8 * j;
+        gp.a = pkt + 1024 + 8 * j;
+        gp.b = pkt + 2048 + 2 * j;
+        gp.code_stride = 16;
+        gp.a_stride = 16;
+        gp.b_stride = 4;
+    } else {
+        gp.code = pkt;
+        gp.a = pkt + 512;
+        gp.b = pkt + 1024;
+        gp.code_stride = 8;
+        gp.a_stride = 8;
+        gp.b_stride = 2;
+    }
+    return gp;
+}
+
+static void put_u16(uint8_t* p, uint16_t v) { p[0] = (uint8_t)(v & 0xff); p[1] = (uint8_t)(v >> 8); }
+static uint16_t get_u16(const uint8_t* p) { return (uint16_t)(p[0] | (p[1] << 8)); }
+
+/* Pack canonical arrays into the packed byte format.  Returns the number of
+ * codes outside 0..3 (their low two bits are stored), or a negative error. */
+int64_t oracle_pack(int64_t N, int64_t K, const uint8_t* Q, const uint16_t* A, const uint16_t* B,
+                    uint8_t* out) {
+    if (!Q || !A || !B || !out) return OR_EINVAL;
+    if (!shape_ok(N, K)) return OR_ESHAPE;
+    int64_t groups = K / OR_G, bad = 0;
+    memset(out, 0, (size_t)oracle_packed_bytes(N, K));
+    for (int64_t r = 0; r < N; ++r) {
+        int64_t rb = r / OR_ROWBLOCK, rl = r % OR_ROWBLOCK;
+        for (int64_t g = 0; g < groups; ++g) {
+            group_place gp = place_group(K, rb, g);
+            for (int b = 0; b < OR_D; ++b) {
+                int64_t s = rl * 4 + b;
+                uint8_t* field = out + gp.code + s * gp.code_stride;
+                for (int v = 0; v < 32; ++v) {
+                    uint8_t q = Q[r * K + g * OR_G + 4 * v + b];
+                    if (q > 3) ++bad;
+                    int bit = 2 * v;
+                    field[bit / 8] |= (uint8_t)((q & 3) << (bit % 8));
+                }
+                uint8_t* acol = out + gp.a + s * gp.a_stride;
+                for (int a = 0; a < OR_D; ++a)
+                    put_u16(acol + 2 * a, A[((r * groups + g) * OR_D + a) * OR_D + b]);
+                put_u16(out + gp.b + s * gp.b_stride, B[(r * groups + g) * OR_D + b]);
+            }
+        }
+    }
+    return bad;
+}
+
+/* Read back row r's codes and affine parameters from packed bytes. */
+static void unpack_row(int64_t K, const uint8_t* packed, int64_t r, uint8_t* q_row,
+                       uint16_t* a_row, uint16_t* b_row) {
+    int64_t groups = K / OR_G, rb = r / OR_ROWBLOCK, rl = r % OR_ROWBLOCK;
+    for (int64_t g = 0; g < groups; ++g) {
+        group_place gp = place_group(K, rb, g);
+        for (int b = 0; b < OR_D; ++b) {
+            int64_t s = rl * 4 + b;
+            const uint8_t* field = packed + gp.code + s * gp.code_stride;
+            for (int v = 0; v < 32; ++v) {
+                int bit = 2 * v;
+                q_row[g * OR_G + 4 * v + b] = (uint8_t)((field[bit / 8] >> (bit % 8)) & 3);
+            }
+            const uint8_t* acol = packed + gp.a + s * gp.a_stride;
+            for (int a = 0; a < OR_D; ++a) a_row[(g * OR_D + a) * OR_D + b] = get_u16(acol + 2 * a);
+            b_row[g * OR_D + b] = get_u16(packed + gp.b + s * gp.b_stride);
+        }
+    }
+}
+
+int oracle_unpack(int64_t N, int64_t K, const uint8_t* packed, uint8_t* Q, uint16_t* A, uint16_t* B) {
+    if (!packed || !Q || !A || !B) return OR_EINVAL;
+    if (!shape_ok(N, K)) return OR_ESHAPE;
+    int64_t groups = K / OR_G;
+    for (int64_t r = 0; r < N; ++r)
+        unpack_row(K, packed, r, Q + r * K, A + r * groups * 16, B + r * groups * 4);
+    return OR_OK;
+}
+
+/* ---- decode (Eq. 4 applied along the input dimension as in Eq. 8) ---- */
+
+/* One row: w[k] for k = 4v + a is sum_b A[g][a][b] * q[4v + b] + B[g][a],
+ * g = (4v) / 128.  Every product is an fp16 value times a small integer, so the
+ * fp64 result is exact. */
+static void decode_row(int64_t K, const uint8_t* q_row, const uint16_t* a_row, const uint16_t* b_row,
+                       double* w) {
+    for (int64_t v = 0; v < K / OR_D; ++v) {
+        int64_t g = (OR_D * v) / OR_G;
+        for (int a = 0; a < OR_D; ++a) {
+            double acc = oracle_half_to_double(b_row[g * OR_D + a]);
+            for (int b = 0; b < OR_D; ++b)
+                acc += oracle_half_to_double(a_row[(g * OR_D + a) * OR_D + b]) * (double)q_row[OR_D * v + b];
+            w[OR_D * v + a] = acc;
+        }
+    }
+}
+
+/* Decode from canonical arrays (no packing involved).  W is [N][K] fp64.
+ * Codes are used as given (values above 3 are not masked). */
+int oracle_decode(int64_t N, int64_t K, const uint8_t* Q, const uint16_t* A, const uint16_t* B,
+                  double* W) {
+    if (!Q || !A || !B || !W) return OR_EINVAL;
+    if (N <= 0 || K <= 0 || K % OR_G) return OR_ESHAPE;
+    int64_t groups = K / OR_G;
+    for (int64_t r = 0; r < N; ++r)
+        decode_row(K, Q + r * K, A + r * groups * 16, B + r * groups * 4, W + r * K);
+    return OR_OK;
+}
+
+/* Decode rows [r0, r1) straight from packed bytes into W [(r1-r0)][K]. */
+int oracle_decode_packed_rows(int64_t N, int64_t K, const uint8_t* packed, int64_t r0, int64_t r1,
+                              double* W) {
+    if (!packed || !W) return OR_EINVAL;
+    if (!shape_ok(N, K) || r0 < 0 || r1 > N || r0 > r1) return OR_ESHAPE;
+    int64_t groups = K / OR_G;
+    uint8_t* q = malloc((size_t)K);
+    uint16_t* a = malloc((size_t)groups * 16 * sizeof(uint16_t));
+    uint16_t* b = malloc((size_t)groups * 4 * sizeof(uint16_t));
+    if (!q || !a || !b) { free(q); free(a); free(b); return OR_EINVAL; }
+    for (int64_t r = r0; r < r1; ++r) {
+        unpack_row(K, packed, r, q, a, b);
+        decode_row(K, q, a, b, W + (r - r0) * K);
+    }
+    free(q); free(a); free(b);
+    return OR_OK;
+}
+
+/* ---- product Y = X * W_hat^T (Eq. 1), rows of W decoded one at a time ---- */
+
+typedef struct {
+    int64_t N, K, M, nrows;
+    const uint8_t* packed;
+    const double* X;
+    const int64_t* rows; /* NULL: all rows in order */
+    double* Y;           /* [M][nrows] */
+    int64_t first, last; /* index range into the row list for this worker */
+    int status;
+} mm_job;
+
+static void* mm_worker(void* arg) {
+    mm_job* j = (mm_job*)arg;
+    int64_t K = j->K, groups = K / OR_G;
+    uint8_t* q = malloc((size_t)K);
+    uint16_t* a = malloc((size_t)groups * 16 * sizeof(uint16_t));
+    uint16_t* b = malloc((size_t)groups * 4 * sizeof(uint16_t));
+    double* w = malloc((size_t)K * sizeof(double));
+    if (!q || !a || !b || !w) { j->status = OR_EINVAL; goto done; }
+    for (int64_t i = j->first; i < j->last; ++i) {
+        int64_t r = j->rows ? j->rows[i] : i;
+        unpack_row(K, j->packed, r, q, a, b);
+        decode_row(K, q, a, b, w);
+        for (int64_t t = 0; t < j->M; ++t) {
+            const double* x = j->X + t * K;
+            double acc = 0.0;
+            for (int64_t k = 0; k < K; ++k) acc += x[k] * w[k];
+            j->Y[t * j->nrows + i] = acc;
+        }
+    }
+    j->status = OR_OK;
+done:
+    free(q); free(a); free(b); free(w);
+    return NULL;
+}
+
+/* Y[t][i] = sum_k X[t][k] * W_hat[rows[i]][k] for the listed rows (all rows
+ * when rows == NULL, then nrows must equal N).  Work is split over `threads`
+ * POSIX threads by output row; each Y element is one plain sequential sum. */
+int oracle_matmul_rows(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const double* X,
+                       int64_t nrows, const int64_t* rows, double* Y, int threads) {
+    if (!packed || !X || !Y) return OR_EINVAL;
+    if (!shape_ok(N, K) || M < 0 || nrows < 0) return OR_ESHAPE;
+    if (!rows && nrows != N) return OR_ESHAPE;
+    if (rows)
+        for (int64_t i = 0; i < nrows; ++i)
+            if (rows[i] < 0 || rows[i] >= N) return OR_EINVAL;
+    if (M == 0 || nrows == 0) return OR_OK;
+    if (threads < 1) threads = 1;
+    if (threads > nrows) threads = (int)nrows;
+    mm_job* jobs = calloc((size_t)threads, sizeof(mm_job));
+    pthread_t* tids = calloc((size_t)threads, sizeof(pthread_t));
+    if (!jobs || !tids) { free(jobs); free(tids); return OR_EINVAL; }
+    int64_t per = (nrows + threads - 1) / threads;
+    int status = OR_OK;
+    for (int t = 0; t < threads; ++t) {
+        mm_job* j = &jobs[t];
+        j->N = N; j->K = K; j->M = M; j->nrows = nrows;
+        j->packed = packed; j->X = X; j->rows = rows; j->Y = Y;
+        j->first = t * per;
+        j->last = (t + 1) * per < nrows ? (t + 1) * per : nrows;
+        if (j->first > j->last) j->first = j->last;
+        if (threads == 1) mm_worker(j);
+        else if (pthread_create(&tids[t], NULL, mm_worker, j) != 0) { mm_worker(j); tids[t] = 0; }
+    }
+    if (threads > 1)
+        for (int t = 0; t < threads; ++t)
+            if (tids[t]) pthread_join(tids[t], NULL);
+    for (int t = 0; t < threads; ++t)
+        if (jobs[t].status != OR_OK) status = jobs[t].status;
+    free(jobs); free(tids);
+    return status;
+}
+
+int oracle_matmul(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const double* X, double* Y,
+                  int threads) {
+    return oracle_matmul_rows(N, K, packed, M, X, N, NULL, Y, threads);
+}

@@ -1,0 +1,316 @@
+"""Pins for the fp64 oracle: each test checks it against something other than
+itself -- values worked out by hand, closed forms of the paper, special cases
+that reduce to a textbook routine, or exact rational arithmetic.
+
+Paper passages: Sec. 2.1 Eq. 1 (Y = X W^T), Sec. 2.2 Eq. 2 (scalar
+quantisation), Sec. 3.1 Eq. 4 (affine lattice decode), Sec. 3.2.2 Eq. 6 and
+App. A.1 (initialisation and the codebook moments), Sec. 3.2.3 Eq. 8/9
+(stacking along the input dimension and the activation-side fold), App. A.2
+(the D4 generator matrix).
+"""
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rand_params(rng, N, K, a_std=0.02, b_std=0.01):
+    Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+    A = (rng.standard_normal((N, K // 128, 4, 4)) * a_std).astype(np.float16)
+    B = (rng.standard_normal((N, K // 128, 4)) * b_std).astype(np.float16)
+    return Q, A, B
+
+
+# ---------------------------------------------------------------- conversions
+
+def test_half_to_double_all_bit_patterns():
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    got = oracle.half_to_double(bits)
+    ref = bits.view(np.float16).astype(np.float64)  # numpy's IEEE binary16
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+
+
+def test_bf16_to_double_matches_torch():
+    torch = pytest.importorskip("torch")
+    bits = np.arange(0, 65536, 7, dtype=np.uint32).astype(np.uint16)
+    got = oracle.bf16_to_double(bits)
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).double().numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+
+
+# ---------------------------------------------------------------- golden decode
+
+def test_golden_d4_generator_decode():
+    """Hand-worked decodes with the integer D4 generator of App. A.2.
+
+    A is not symmetric, so applying q^T A instead of A q, or swapping the
+    component order of a vector, changes the expected values."""
+    g = json.load(open(os.path.join(GOLD, "d4_decode.json")))
+    N, K = 1, 128
+    Q = np.zeros((N, K), np.uint8)
+    for e in g["vectors"]:
+        Q[0, 4 * e["v"]:4 * e["v"] + 4] = e["q"]
+    A = np.array(g["A"], np.float16).reshape(1, 1, 4, 4)
+    B = np.array(g["B"], np.float16).reshape(1, 1, 4)
+    W = oracle.decode(Q, A, B)
+    for e in g["vectors"]:
+        assert W[0, 4 * e["v"]:4 * e["v"] + 4].tolist() == e["w"], e
+    # untouched vectors (code 0) decode to B
+    untouched = [v for v in range(32) if v not in {e["v"] for e in g["vectors"]}]
+    for v in untouched:
+        assert W[0, 4 * v:4 * v + 4].tolist() == g["B"]
+    # and through the packed path, 16 rows (row 0 carries the fixture)
+    Q16 = np.zeros((16, K), np.uint8); Q16[0] = Q[0]
+    A16 = np.zeros((16, 1, 4, 4), np.float16); A16[0] = A[0]
+    B16 = np.zeros((16, 1, 4), np.float16); B16[0] = B[0]
+    packed, bad = oracle.pack(Q16, A16, B16)
+    assert bad == 0
+    X = np.zeros((1, K)); X[0, 20:24] = 1.0
+    Y = oracle.matmul(packed, 16, K, X)
+    assert Y[0, 0] == g["x_picks_vector_5"]["y"]
+
+
+# ---------------------------------------------------------------- special cases
+
+def _nice_scales(rng, shape):
+    """fp16 scales with at most 9 significant bits, so s*z (z <= 3) is exact in fp16."""
+    m = rng.integers(64, 256, size=shape) | 1
+    e = rng.integers(9, 13, size=shape)
+    return (m * np.exp2(-e.astype(np.float64))).astype(np.float16)
+
+
+def test_scalar_quantisation_special_case():
+    """A = s I, B = -s z 1 turns the decode into the scalar dequantiser of Eq. 2:
+    Phi_SQ(w) = s (clamp(round(w/s) + z, 0, 3) - z), per (row, group)."""
+    rng = np.random.default_rng(11)
+    N, K = 32, 384
+    w = rng.standard_normal((N, K)) * 0.05
+    s = _nice_scales(rng, (N, K // 128))
+    z = rng.integers(1, 3, size=(N, K // 128))  # integer zero points 1 or 2
+    s_col = np.repeat(s.astype(np.float64), 128, axis=1)
+    z_col = np.repeat(z, 128, axis=1)
+    codes = np.clip(np.round(w / s_col) + z_col, 0, 3)
+    phi_sq = s_col * (codes - z_col)  # Eq. 2, computed from w directly
+    A = np.zeros((N, K // 128, 4, 4), np.float16)
+    for a in range(4):
+        A[:, :, a, a] = s
+    B = np.repeat((-(s.astype(np.float64)) * z)[..., None], 4, axis=2).astype(np.float16)
+    assert np.array_equal(B.astype(np.float64)[..., 0], -(s.astype(np.float64)) * z)  # exact
+    W = oracle.decode(codes.astype(np.uint8), A, B)
+    assert np.array_equal(W, phi_sq)
+    packed, _ = oracle.pack(codes.astype(np.uint8), A, B)
+    assert np.array_equal(oracle.decode_packed_rows(packed, N, K, 0, N), phi_sq)
+
+
+def test_identity_transform_is_plain_integer_matmul():
+    """A = I, B = 0: W_hat = Q, so Y = X Q^T (a library matmul on the codes)."""
+    rng = np.random.default_rng(5)
+    N, K, M = 48, 640, 3  # 5 groups: exercises the half packet
+    Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+    A = np.zeros((N, K // 128, 4, 4), np.float16)
+    for a in range(4):
+        A[:, :, a, a] = 1.0
+    B = np.zeros((N, K // 128, 4), np.float16)
+    X = rng.integers(-8, 9, size=(M, K)).astype(np.float64)
+    packed, _ = oracle.pack(Q, A, B)
+    Y = oracle.matmul(packed, N, K, X, threads=3)
+    assert np.array_equal(Y, X @ Q.T.astype(np.float64))
+
+
+# ---------------------------------------------------------------- closed forms
+
+def _all_codes_row(A_g, B_g):
+    """One row whose 8 groups enumerate all 256 code tuples, all groups sharing (A_g, B_g)."""
+    K = 1024
+    c = np.arange(256)
+    q = np.stack([(c >> (2 * b)) & 3 for b in range(4)], axis=1)  # tuple of code c
+    Q = q.reshape(1, K).astype(np.uint8)
+    A = np.broadcast_to(A_g, (1, 8, 4, 4)).astype(np.float16)
+    B = np.broadcast_to(B_g, (1, 8, 4)).astype(np.float16)
+    return Q, A, B
+
+
+def test_codebook_moments_closed_form():
+    """Over the full code grid: mean = A (1.5 * 1) + B, covariance = 1.25 A A^T,
+    since each code is uniform on {0..3} with mean 3/2 and variance 15/12
+    (App. A.1).  A A^T differs from A^T A for a general A, so a transposed A
+    fails this."""
+    rng = np.random.default_rng(3)
+    for _ in range(5):
+        A_g = (rng.standard_normal((4, 4)) * 0.3).astype(np.float16)
+        B_g = (rng.standard_normal(4) * 0.1).astype(np.float16)
+        Q, A, B = _all_codes_row(A_g, B_g)
+        code_words = oracle.decode(Q, A, B).reshape(256, 4)
+        Af, Bf = A_g.astype(np.float64), B_g.astype(np.float64)
+        mean = code_words.mean(axis=0)
+        cov = (code_words - mean).T @ (code_words - mean) / 256.0
+        np.testing.assert_allclose(mean, 1.5 * Af.sum(axis=1) + Bf, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(cov, 1.25 * Af @ Af.T, rtol=0, atol=1e-12)
+
+
+def test_paper_initialisation_gives_centred_unit_grid():
+    """Eq. 6 with b = 1.5, s = sqrt(12/15) and G orthogonal: mean 0 and
+    covariance I (App. A.1), up to the fp16 rounding of A and B."""
+    stats = pytest.importorskip("scipy.stats")
+    G = stats.ortho_group.rvs(4, random_state=7)
+    s = np.sqrt(12.0 / 15.0)
+    A_g = (s * G).astype(np.float16)
+    B_g = (-1.5 * s * G @ np.ones(4)).astype(np.float16)
+    Q, A, B = _all_codes_row(A_g, B_g)
+    cw = oracle.decode(Q, A, B).reshape(256, 4)
+    np.testing.assert_allclose(cw.mean(axis=0), 0.0, atol=4e-3)
+    cov = np.cov(cw.T, bias=True)
+    np.testing.assert_allclose(cov, np.eye(4), atol=4e-3)
+
+
+def test_fold_identity_for_row_shared_affine():
+    """Eq. 9: with (A, B) shared by all rows of a group,
+    Y = sum_i (X_i A) W_int,i^T + sum_i (X_i B) 1^T  -- activations folded first."""
+    rng = np.random.default_rng(9)
+    N, K, M = 32, 512, 4
+    Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+    A_grp = (rng.standard_normal((K // 128, 4, 4)) * 0.05).astype(np.float16)
+    B_grp = (rng.standard_normal((K // 128, 4)) * 0.02).astype(np.float16)
+    A = np.broadcast_to(A_grp, (N,) + A_grp.shape).copy()
+    B = np.broadcast_to(B_grp, (N,) + B_grp.shape).copy()
+    X = rng.standard_normal((M, K))
+    packed, _ = oracle.pack(Q, A, B)
+    Y = oracle.matmul(packed, N, K, X)
+    Xv = X.reshape(M, K // 4, 4)  # X_i: tokens x d, one per vector i
+    g_of_v = np.arange(K // 4) // 32
+    XA = np.einsum("tva,vab->tvb", Xv, A_grp.astype(np.float64)[g_of_v])  # X_i A
+    XB = np.einsum("tva,va->t", Xv, B_grp.astype(np.float64)[g_of_v])     # sum_i X_i B
+    Y_fold = XA.reshape(M, K) @ Q.T.astype(np.float64) + XB[:, None]
+    np.testing.assert_allclose(Y, Y_fold, rtol=1e-12, atol=1e-12)
+
+
+def test_linearity_in_x_and_additivity_in_b():
+    rng = np.random.default_rng(21)
+    N, K, M = 32, 384, 2
+    Q, A, B = _rand_params(rng, N, K)
+    X1, X2 = rng.standard_normal((M, K)), rng.standard_normal((M, K))
+    pk, _ = oracle.pack(Q, A, B)
+    Y1, Y2 = oracle.matmul(pk, N, K, X1), oracle.matmul(pk, N, K, X2)
+    Y12 = oracle.matmul(pk, N, K, 2.0 * X1 - 0.5 * X2)
+    np.testing.assert_allclose(Y12, 2.0 * Y1 - 0.5 * Y2, rtol=1e-12, atol=1e-12)
+    # additivity in B: Y(A, B) = Y(A, 0) + Y(0, B) with Y(0, B)[t][r] = sum_g B[r][g] . Xbar[t][g]
+    zA, zB = np.zeros_like(A), np.zeros_like(B)
+    Y_A0 = oracle.matmul(oracle.pack(Q, A, zB)[0], N, K, X1)
+    Y_0B = oracle.matmul(oracle.pack(Q, zA, B)[0], N, K, X1)
+    Xbar = X1.reshape(M, K // 128, 32, 4).sum(axis=2)  # [t][g][a]
+    np.testing.assert_allclose(Y_0B, np.einsum("rga,tga->tr", B.astype(np.float64), Xbar),
+                               rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(Y1, Y_A0 + Y_0B, rtol=1e-12, atol=1e-12)
+    # linear in A: doubling A (exact in fp16) doubles Y(A, 0)
+    Y_2A = oracle.matmul(oracle.pack(Q, (2 * A.astype(np.float32)).astype(np.float16), zB)[0], N, K, X1)
+    np.testing.assert_array_equal(Y_2A, 2.0 * Y_A0)
+
+
+def test_exact_rational_brute_force():
+    """Exact rationals on tiny inputs: the fp64 decode is exact (each product is
+    an fp16 value times an integer <= 3; 4 of them plus B fit in 53 bits) and Y
+    differs from the exact value only by the rounding of one K-term sum."""
+    rng = np.random.default_rng(1)
+    N, K, M = 16, 256, 2
+    Q, A, B = _rand_params(rng, N, K, a_std=0.5, b_std=0.5)
+    X = rng.standard_normal((M, K)).astype(np.float16)
+    pk, _ = oracle.pack(Q, A, B)
+    Y = oracle.matmul(pk, N, K, X.astype(np.float64))
+    W = oracle.decode(Q, A, B)
+    Af = [[[[Fraction(float(A[r, g, a, b])) for b in range(4)] for a in range(4)]
+           for g in range(K // 128)] for r in range(N)]
+    for r in range(0, N, 5):
+        w_exact = []
+        for k in range(K):
+            v, a = divmod(k, 4)
+            g = 4 * v // 128
+            w = Fraction(float(B[r, g, a])) + sum(Af[r][g][a][b] * int(Q[r, 4 * v + b]) for b in range(4))
+            w_exact.append(w)
+            assert Fraction(W[r, k]) == w  # exact decode
+        for t in range(M):
+            y = sum(Fraction(float(X[t, k])) * w_exact[k] for k in range(K))
+            scale = sum(abs(Fraction(float(X[t, k])) * w_exact[k]) for k in range(K))
+            assert abs(Fraction(Y[t, r]) - y) <= scale * Fraction(K, 2 ** 52)
+
+
+# ---------------------------------------------------------------- packed format
+
+def test_packed_size_is_4p5_bits_per_weight():
+    """2-bit codes plus one 40-byte (A, B) set per 128 weights of a row (Sec. 3.1:
+    (4*4+4)*2 bytes per set)."""
+    for N, K in [(16, 128), (4096, 4096), (11008, 4096), (4096, 11008), (1024, 8192)]:
+        assert oracle.packed_bytes(N, K) == N * K // 4 + N * (K // 128) * 40
+    for N, K in [(15, 128), (16, 100), (0, 128)]:
+        with pytest.raises(oracle.OracleError):
+            oracle.packed_bytes(N, K)
+
+
+def test_packed_byte_positions_worked_by_hand():
+    g = json.load(open(os.path.join(GOLD, "pack_positions.json")))
+    for c in g["cases"]:
+        N, K = c["N"], c["K"]
+        Q = np.zeros((N, K), np.uint8)
+        A = np.zeros((N, K // 128, 4, 4), np.uint16)
+        B = np.zeros((N, K // 128, 4), np.uint16)
+        if c["set"] == "Q":
+            Q[tuple(c["index"])] = c["value"]
+        elif c["set"] == "A":
+            A[tuple(c["index"])] = c["bits"]
+        else:
+            B[tuple(c["index"])] = c["bits"]
+        packed, bad = oracle.pack(Q, A, B)
+        assert bad == 0
+        expect = np.zeros_like(packed)
+        for off, val in c["bytes"].items():
+            expect[int(off)] = val
+        nz = np.nonzero(packed != expect)[0]
+        assert nz.size == 0, (c, nz[:8], packed[nz[:8]])
+
+
+@pytest.mark.parametrize("N,K", [(16, 128), (16, 256), (48, 384), (32, 1152)])
+def test_pack_unpack_round_trip(N, K):
+    rng = np.random.default_rng(N * 7 + K)
+    Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+    A = rng.integers(0, 65536, size=(N, K // 128, 4, 4), dtype=np.uint32).astype(np.uint16)
+    B = rng.integers(0, 65536, size=(N, K // 128, 4), dtype=np.uint32).astype(np.uint16)
+    packed, bad = oracle.pack(Q, A, B)
+    assert bad == 0
+    Q2, A2, B2 = oracle.unpack(packed, N, K)
+    assert np.array_equal(Q2, Q)
+    assert np.array_equal(A2.view(np.uint16), A) and np.array_equal(B2.view(np.uint16), B)
+    # every byte is used exactly: distinct inputs give distinct images
+    Q[0, 0] ^= 1
+    assert not np.array_equal(oracle.pack(Q, A, B)[0], packed)
+
+
+def test_pack_counts_out_of_range_codes():
+    N, K = 16, 256
+    Q = np.zeros((N, K), np.uint8)
+    Q[3, 7] = 4; Q[15, 200] = 255; Q[0, 0] = 3
+    A = np.zeros((N, 2, 4, 4), np.float16); B = np.zeros((N, 2, 4), np.float16)
+    _, bad = oracle.pack(Q, A, B)
+    assert bad == 2
+
+
+def test_row_subset_matches_full_product():
+    rng = np.random.default_rng(4)
+    N, K, M = 64, 384, 3
+    Q, A, B = _rand_params(rng, N, K)
+    pk, _ = oracle.pack(Q, A, B)
+    X = rng.standard_normal((M, K))
+    Y = oracle.matmul(pk, N, K, X, threads=4)
+    rows = [63, 0, 17, 17, 40]
+    Ys = oracle.matmul(pk, N, K, X, rows=rows, threads=2)
+    assert np.array_equal(Ys, Y[:, rows])
+    # single-threaded and multi-threaded agree bit for bit (each sum is sequential)
+    assert np.array_equal(Y, oracle.matmul(pk, N, K, X, threads=1))
