@@ -1,0 +1,146 @@
+/*
+ * unisvq.h -- C ABI of libunisvq, the MI355X (gfx950) inference path of
+ * UniSVQ 2-bit affine-lattice quantised linear layers.
+ *
+ * The operation (paper "UniSVQ: 2-bit Unified Scalar-Vector Quantization"):
+ *   A weight matrix W (N output features x K input features) is stored as
+ *   integer codes q in {0,1,2,3}.  Every d = 4 consecutive input columns of
+ *   one output row form a vector, rebuilt as an affine image of its lattice
+ *   point:   w_hat = A q + B,  A in R^{4x4}, B in R^4          (Sec. 3.1, Eq. 4)
+ *   Vector i of a row covers input columns 4i..4i+3           (Sec. 3.2.3, Eq. 8)
+ *   and the layer output is  Y = X W_hat^T                     (Sec. 2.1, Eq. 1)
+ *   The affine map commutes with the matrix product (Sec. 3.1, Eq. 9), so the
+ *   kernels never materialise W_hat in memory.
+ *   Granularity: one (A, B) pair per (output row, group of 128 input
+ *   columns), stored as fp16 -- 40 bytes per set (Sec. 3.1).  The paper's
+ *   one-pair-per-matrix setting (Sec. 4.2) is the special case where all
+ *   pairs are equal.
+ *
+ * Conventions shared by every entry point
+ *   - Pointers named "device" are device memory owned by the caller; the
+ *     library never allocates, frees or keeps them.  Host pointers are named.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *     work is enqueued asynchronously on it; no call synchronises.
+ *   - Returns UNISVQ_OK (0) or a negative unisvq_status.  Argument errors are
+ *     detected on the host before anything is enqueued (so they can be tested
+ *     without a GPU).  A failed launch returns UNISVQ_EHIP.  Faults inside a
+ *     kernel surface at the caller's next synchronisation.
+ *   - Outputs are overwritten, never accumulated into.
+ *   - Thread-safe: no global mutable state besides a once-per-process,
+ *     per-device kernel attribute set-up.
+ *   - Shapes: N % 16 == 0, K % 128 == 0, N >= 16, K >= 128, M >= 1.
+ *
+ * ---------------------------------------------------------------------------
+ * Packed weight format, version 1 (bytes little endian)
+ *   Canonical inputs: Q uint8 [N][K] (values 0..3); A fp16 [N][K/128][4][4],
+ *   A[r][g][a][b] multiplies q_b into output component a; B fp16 [N][K/128][4].
+ *   Total size N*K/4 + N*(K/128)*40 bytes (4.5 bits per weight), no padding.
+ *
+ *   Row block rb (rows 16rb..16rb+15) occupies (K/128)*1152 consecutive bytes
+ *   starting at rb*(K/128)*1152.  Within it, groups g = 0..K/128-1 are taken
+ *   in pairs: packet p holds groups 2p and 2p+1 (2304 bytes, at p*2304); when
+ *   K/128 is odd a final half packet holds the last group (1152 bytes).
+ *   Slot s = 0..63 of a packet stands for row r = 16rb + s/4 and component
+ *   b = s%4.
+ *     full packet at offset P, j = 0 for group 2p, j = 1 for group 2p+1:
+ *       P +        16s + 8j   8-byte code field F(r, 2p+j, b)
+ *       P + 1024 + 16s + 8j   A[r][2p+j][a][b] for a = 0..3, fp16 each
+ *       P + 2048 +  4s + 2j   B[r][2p+j][b], fp16
+ *     half packet at offset P (group g):
+ *       P +        8s         F(r, g, b)
+ *       P +  512 + 8s         A[r][g][0..3][b]
+ *       P + 1024 + 2s         B[r][g][b]
+ *   Code field F(r, g, b): 64-bit little-endian word whose bits 2v, 2v+1 hold
+ *   Q[r][128g + 4v + b], v = 0..31 (component b of the group's 32 vectors).
+ *
+ *   One packet slot is exactly the data one lane of a 64-lane wavefront
+ *   consumes, so every load of the matrix-vector kernel is a fully coalesced
+ *   16-byte-per-lane read.
+ * ---------------------------------------------------------------------------
+ */
+#ifndef UNISVQ_H
+#define UNISVQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define UNISVQ_FORMAT_VERSION 1
+#define UNISVQ_GROUP 128   /* input columns per (A, B) set */
+#define UNISVQ_DIM 4       /* vector dimension d */
+#define UNISVQ_ROW_BLOCK 16
+
+typedef enum {
+    UNISVQ_OK = 0,
+    UNISVQ_EINVAL = -1,     /* null pointer, M < 1, unknown dtype value */
+    UNISVQ_ESHAPE = -2,     /* N % 16 != 0, K % 128 != 0, N < 16 or K < 128 */
+    UNISVQ_EUNSUP = -3,     /* valid but unsupported combination (dtype pair, M too large for gemv) */
+    UNISVQ_EALIGN = -4,     /* a pointer lacks the alignment stated for it */
+    UNISVQ_EHIP = -5,       /* the HIP runtime reported an error at launch */
+    UNISVQ_EWORKSPACE = -6  /* workspace smaller than unisvq_gemm_workspace_bytes() */
+} unisvq_status;
+
+typedef enum {
+    UNISVQ_F16 = 0,   /* IEEE binary16 */
+    UNISVQ_BF16 = 1,  /* bfloat16 */
+    UNISVQ_F32 = 2    /* IEEE binary32 (outputs only) */
+} unisvq_dtype;
+
+/* Library and format version (UNISVQ_FORMAT_VERSION). */
+int unisvq_version(void);
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* unisvq_status_string(int status);
+
+/* Bytes of the packed buffer for an N x K matrix (format block above);
+ * 0 when the shape is invalid.  Host-only, no GPU needed. */
+size_t unisvq_packed_bytes(int64_t N, int64_t K);
+
+/* Pack canonical codes and affine parameters into the packed format.
+ *   codes     device uint8  [N][K], values 0..3 (Sec. 3.2.2: unsigned codes,
+ *             the centring constant lives in B)
+ *   A         device fp16 bits [N][K/128][4][4]
+ *   B         device fp16 bits [N][K/128][4]
+ *   packed    device, unisvq_packed_bytes(N, K) bytes, 16-byte aligned
+ *   bad_codes device int32 or NULL: if given, the number of codes above 3 is
+ *             ADDED to *bad_codes (the caller zeroes it); such codes are stored
+ *             modulo 4.
+ * A bit-exact permutation: values are never converted or rounded. */
+int unisvq_pack(int64_t N, int64_t K, const uint8_t* codes, const uint16_t* A, const uint16_t* B,
+                void* packed, int32_t* bad_codes, void* stream);
+
+/* Exact inverse of unisvq_pack (codes come back in 0..3).  All device. */
+int unisvq_unpack(int64_t N, int64_t K, const void* packed, uint8_t* codes, uint16_t* A, uint16_t* B,
+                  void* stream);
+
+/* Decode-phase product y = x * W_hat^T for a few tokens (Eq. 1 with Eq. 4/8).
+ *   packed  device, packed N x K matrix, 16-byte aligned
+ *   x       device [M][K] row-major, dtype x_dtype (F16 or BF16), 16-byte aligned
+ *   y       device [M][N] row-major, dtype y_dtype (F16, BF16 or F32)
+ *   M       1..4 tokens (UNISVQ_EUNSUP above that; use unisvq_gemm)
+ * Per (row, group) the kernel contracts the activations with the integer
+ * codes on the matrix cores and applies A and B to that small result
+ * (the affine map commutes with the product, Sec. 3.1), accumulating in fp32
+ * and rounding once to y_dtype. */
+int unisvq_gemv(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype,
+                void* y, int y_dtype, void* stream);
+
+/* Workspace the GEMM needs for this problem (currently always 0). */
+size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M);
+
+/* Prefill product y = x * W_hat^T for any M >= 1 (Eq. 1 with Eq. 4/8).
+ * Arguments as unisvq_gemv; x_dtype F16 or BF16, y_dtype F16, BF16 or F32.
+ * Decodes weight tiles into LDS (each vector A q + B in fp32, rounded once to
+ * the activation dtype) and multiplies them on the matrix cores with fp32
+ * accumulation.  workspace may be NULL when the required size is 0. */
+int unisvq_gemm(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype,
+                void* y, int y_dtype, void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UNISVQ_H */

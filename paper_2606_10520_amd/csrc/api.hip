@@ -1,0 +1,101 @@
+// C entry points of libunisvq: argument validation (host only, before any
+// HIP call) and dispatch to the kernels.
+#include <cstring>
+
+#include "common.hpp"
+
+namespace {
+
+bool shape_ok(int64_t N, int64_t K) {
+    return N >= unisvq::kRowBlock && K >= unisvq::kGroup && N % unisvq::kRowBlock == 0 &&
+           K % unisvq::kGroup == 0 && N <= (int64_t{1} << 31) - 1 && K <= (int64_t{1} << 31) - 1;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+bool x_dtype_ok(int t) { return t == UNISVQ_F16 || t == UNISVQ_BF16; }
+bool y_dtype_ok(int t) { return t == UNISVQ_F16 || t == UNISVQ_BF16 || t == UNISVQ_F32; }
+
+// Common checks of the two product entry points.
+int check_product(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype,
+                  const void* y, int y_dtype) {
+    if (!packed || !x || !y) return UNISVQ_EINVAL;
+    if (M < 1 || M > (int64_t{1} << 31) - 1) return UNISVQ_EINVAL;
+    if (!x_dtype_ok(x_dtype) || !y_dtype_ok(y_dtype)) return UNISVQ_EINVAL;
+    if (!shape_ok(N, K)) return UNISVQ_ESHAPE;
+    if (!aligned(packed, 16) || !aligned(x, 16)) return UNISVQ_EALIGN;
+    if (!aligned(y, y_dtype == UNISVQ_F32 ? 4 : 2)) return UNISVQ_EALIGN;
+    return UNISVQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int unisvq_version(void) { return UNISVQ_FORMAT_VERSION; }
+
+const char* unisvq_status_string(int status) {
+    switch (status) {
+        case UNISVQ_OK: return "ok";
+        case UNISVQ_EINVAL: return "invalid argument";
+        case UNISVQ_ESHAPE: return "invalid shape (need N % 16 == 0, K % 128 == 0)";
+        case UNISVQ_EUNSUP: return "unsupported configuration";
+        case UNISVQ_EALIGN: return "misaligned pointer";
+        case UNISVQ_EHIP: return "HIP runtime error";
+        case UNISVQ_EWORKSPACE: return "workspace too small";
+        default: return "unknown status";
+    }
+}
+
+size_t unisvq_packed_bytes(int64_t N, int64_t K) {
+    if (!shape_ok(N, K)) return 0;
+    return static_cast<size_t>(N / unisvq::kRowBlock) * static_cast<size_t>(K / unisvq::kGroup) *
+           unisvq::kGroupBlockBytes;
+}
+
+int unisvq_pack(int64_t N, int64_t K, const uint8_t* codes, const uint16_t* A, const uint16_t* B,
+                void* packed, int32_t* bad_codes, void* stream) {
+    if (!codes || !A || !B || !packed) return UNISVQ_EINVAL;
+    if (!shape_ok(N, K)) return UNISVQ_ESHAPE;
+    if (!aligned(packed, 16) || !aligned(A, 2) || !aligned(B, 2) || (bad_codes && !aligned(bad_codes, 4)))
+        return UNISVQ_EALIGN;
+    const hipError_t e = unisvq::launch_pack(N, K, codes, A, B, static_cast<uint8_t*>(packed), bad_codes,
+                                             static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+}
+
+int unisvq_unpack(int64_t N, int64_t K, const void* packed, uint8_t* codes, uint16_t* A, uint16_t* B,
+                  void* stream) {
+    if (!codes || !A || !B || !packed) return UNISVQ_EINVAL;
+    if (!shape_ok(N, K)) return UNISVQ_ESHAPE;
+    if (!aligned(packed, 16) || !aligned(A, 2) || !aligned(B, 2)) return UNISVQ_EALIGN;
+    const hipError_t e = unisvq::launch_unpack(N, K, static_cast<const uint8_t*>(packed), codes, A, B,
+                                               static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+}
+
+int unisvq_gemv(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype,
+                void* y, int y_dtype, void* stream) {
+    const int st = check_product(N, K, packed, M, x, x_dtype, y, y_dtype);
+    if (st != UNISVQ_OK) return st;
+    if (M > 4) return UNISVQ_EUNSUP;
+    return unisvq::launch_gemv(N, K, static_cast<const uint8_t*>(packed), M, x, x_dtype, y, y_dtype,
+                               static_cast<hipStream_t>(stream));
+}
+
+size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M) {
+    (void)N; (void)K; (void)M;
+    return 0;
+}
+
+int unisvq_gemm(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype,
+                void* y, int y_dtype, void* workspace, size_t workspace_bytes, void* stream) {
+    const int st = check_product(N, K, packed, M, x, x_dtype, y, y_dtype);
+    if (st != UNISVQ_OK) return st;
+    if (workspace_bytes < unisvq_gemm_workspace_bytes(N, K, M)) return UNISVQ_EWORKSPACE;
+    (void)workspace;
+    return unisvq::launch_gemm(N, K, static_cast<const uint8_t*>(packed), M, x, x_dtype, y, y_dtype,
+                               static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

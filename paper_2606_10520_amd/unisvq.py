@@ -1,0 +1,178 @@
+"""ctypes binding of libunisvq (argument marshalling only).
+
+Every function takes torch tensors that already live on the GPU, passes their
+device pointers and the current HIP stream to the C ABI declared in
+``include/unisvq.h``, and raises on a non-zero status.  All compute happens in
+the library's HIP kernels; there is no host or PyTorch fallback.  If the
+library has not been built the first call raises ``UniSVQLibraryMissing``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libunisvq.so")
+
+F16, BF16, F32 = 0, 1, 2
+GROUP, DIM, ROW_BLOCK = 128, 4, 16
+
+STATUS = {0: "UNISVQ_OK", -1: "UNISVQ_EINVAL", -2: "UNISVQ_ESHAPE", -3: "UNISVQ_EUNSUP",
+          -4: "UNISVQ_EALIGN", -5: "UNISVQ_EHIP", -6: "UNISVQ_EWORKSPACE"}
+
+EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "unisvq_pack",
+           "unisvq_unpack", "unisvq_gemv", "unisvq_gemm_workspace_bytes", "unisvq_gemm")
+
+
+class UniSVQLibraryMissing(RuntimeError):
+    pass
+
+
+class UniSVQError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn} returned {STATUS.get(status, status)}: {_status_string(status)}")
+
+
+_lib = None
+
+
+def load():
+    """Load libunisvq.so (once) and declare its C signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise UniSVQLibraryMissing(
+            f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = ctypes.CDLL(LIB_PATH)
+    i64, p, i32, sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    lib.unisvq_version.argtypes = []
+    lib.unisvq_version.restype = i32
+    lib.unisvq_status_string.argtypes = [i32]
+    lib.unisvq_status_string.restype = ctypes.c_char_p
+    lib.unisvq_packed_bytes.argtypes = [i64, i64]
+    lib.unisvq_packed_bytes.restype = sz
+    lib.unisvq_pack.argtypes = [i64, i64, p, p, p, p, p, p]
+    lib.unisvq_pack.restype = i32
+    lib.unisvq_unpack.argtypes = [i64, i64, p, p, p, p, p]
+    lib.unisvq_unpack.restype = i32
+    lib.unisvq_gemv.argtypes = [i64, i64, p, i64, p, i32, p, i32, p]
+    lib.unisvq_gemv.restype = i32
+    lib.unisvq_gemm_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.unisvq_gemm_workspace_bytes.restype = sz
+    lib.unisvq_gemm.argtypes = [i64, i64, p, i64, p, i32, p, i32, p, sz, p]
+    lib.unisvq_gemm.restype = i32
+    _lib = lib
+    return lib
+
+
+def _status_string(status: int) -> str:
+    try:
+        return load().unisvq_status_string(status).decode()
+    except UniSVQLibraryMissing:  # pragma: no cover
+        return "?"
+
+
+def _check(fn: str, status: int) -> None:
+    if status != 0:
+        raise UniSVQError(fn, status)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None) -> int:
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    codes = {torch.float16: F16, torch.bfloat16: BF16, torch.float32: F32}
+    if t not in codes:
+        raise TypeError(f"unsupported dtype {t}")
+    return codes[t]
+
+
+def _need_cuda(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise ValueError("libunisvq takes device tensors only")
+
+
+def version() -> int:
+    return load().unisvq_version()
+
+
+def packed_bytes(N: int, K: int) -> int:
+    return load().unisvq_packed_bytes(N, K)
+
+
+def pack(codes, A, B, out=None, bad_codes=None, stream=None):
+    """codes uint8 [N][K]; A fp16 [N][K/128][4][4]; B fp16 [N][K/128][4] -> packed uint8 bytes."""
+    torch = _torch()
+    _need_cuda(codes, A, B, out, bad_codes)
+    N, K = codes.shape
+    if out is None:
+        out = torch.empty(packed_bytes(N, K), dtype=torch.uint8, device=codes.device)
+    _check("unisvq_pack", load().unisvq_pack(N, K, _ptr(codes.contiguous()), _ptr(A.contiguous()),
+                                             _ptr(B.contiguous()), _ptr(out), _ptr(bad_codes),
+                                             _stream(stream)))
+    return out
+
+
+def unpack(packed, N: int, K: int, stream=None):
+    """Inverse of pack: returns (codes uint8, A fp16, B fp16) device tensors."""
+    torch = _torch()
+    _need_cuda(packed)
+    dev = packed.device
+    codes = torch.empty((N, K), dtype=torch.uint8, device=dev)
+    A = torch.empty((N, K // GROUP, DIM, DIM), dtype=torch.float16, device=dev)
+    B = torch.empty((N, K // GROUP, DIM), dtype=torch.float16, device=dev)
+    _check("unisvq_unpack", load().unisvq_unpack(N, K, _ptr(packed), _ptr(codes), _ptr(A), _ptr(B),
+                                                 _stream(stream)))
+    return codes, A, B
+
+
+def _product(fn_name, N, K, packed, x, out, out_dtype, stream, extra=()):
+    torch = _torch()
+    _need_cuda(packed, x, out)
+    x2 = x if x.dim() == 2 else x.reshape(-1, K)
+    if not x2.is_contiguous():
+        raise ValueError("x must be contiguous")
+    M = x2.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=out_dtype or x.dtype, device=x.device)
+    fn = getattr(load(), fn_name)
+    _check(fn_name, fn(N, K, _ptr(packed), M, _ptr(x2), _dtype_code(x2.dtype), _ptr(out),
+                       _dtype_code(out.dtype), *extra, _stream(stream)))
+    return out
+
+
+def gemv(packed, N: int, K: int, x, out=None, out_dtype=None, stream=None):
+    """y[M][N] = x[M][K] . W_hat^T for 1 <= M <= 4 (decode-phase kernel)."""
+    return _product("unisvq_gemv", N, K, packed, x, out, out_dtype, stream)
+
+
+def gemm_workspace_bytes(N: int, K: int, M: int) -> int:
+    return load().unisvq_gemm_workspace_bytes(N, K, M)
+
+
+def gemm(packed, N: int, K: int, x, out=None, out_dtype=None, workspace=None, stream=None):
+    """y[M][N] = x[M][K] . W_hat^T for any M (prefill kernel)."""
+    M = x.numel() // K
+    need = gemm_workspace_bytes(N, K, M)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if need and workspace is None:
+        workspace = _torch().empty(need, dtype=_torch().uint8, device=x.device)
+        ws_bytes = need
+    return _product("unisvq_gemm", N, K, packed, x, out, out_dtype, stream,
+                    extra=(_ptr(workspace), ws_bytes))

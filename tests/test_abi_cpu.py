@@ -1,0 +1,106 @@
+"""Host-only checks of the C ABI: the library loads, exports every function
+declared in include/unisvq.h, and rejects bad arguments before any HIP call
+(every call here fails validation, so no kernel is ever launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_10520_amd.unisvq as u
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "unisvq.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(u.LIB_PATH), reason="libunisvq.so not built")
+
+OK, EINVAL, ESHAPE, EUNSUP, EALIGN, EHIP, EWS = 0, -1, -2, -3, -4, -5, -6
+GOOD = 0x10000  # 16-byte aligned stand-in address; never dereferenced (validation fails first)
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(unisvq_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_documented_entry_points():
+    assert set(header_functions()) == set(u.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(u.LIB_PATH)
+    for name in header_functions():
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings():
+    lib = u.load()
+    assert lib.unisvq_version() == 1
+    for st in (OK, EINVAL, ESHAPE, EUNSUP, EALIGN, EHIP, EWS):
+        assert lib.unisvq_status_string(st)
+    assert lib.unisvq_status_string(12345) == b"unknown status"
+
+
+@pytest.mark.parametrize("N,K,expect", [
+    (16, 128, 1152), (4096, 4096, 4096 * 4096 // 4 + 4096 * 32 * 40), (11008, 4096, 25_362_432),
+    (15, 128, 0), (16, 100, 0), (0, 128, 0), (16, 0, 0), (-16, 128, 0),
+])
+def test_packed_bytes(N, K, expect):
+    assert u.load().unisvq_packed_bytes(N, K) == expect
+
+
+def test_pack_validation():
+    lib = u.load()
+    assert lib.unisvq_pack(16, 128, None, GOOD, GOOD, GOOD, None, None) == EINVAL
+    assert lib.unisvq_pack(16, 128, GOOD, GOOD, GOOD, None, None, None) == EINVAL
+    assert lib.unisvq_pack(17, 128, GOOD, GOOD, GOOD, GOOD, None, None) == ESHAPE
+    assert lib.unisvq_pack(16, 130, GOOD, GOOD, GOOD, GOOD, None, None) == ESHAPE
+    assert lib.unisvq_pack(16, 128, GOOD, GOOD, GOOD, GOOD + 8, None, None) == EALIGN
+    assert lib.unisvq_pack(16, 128, GOOD, GOOD + 1, GOOD, GOOD, None, None) == EALIGN
+    assert lib.unisvq_pack(16, 128, GOOD, GOOD, GOOD, GOOD, GOOD + 2, None) == EALIGN
+    assert lib.unisvq_unpack(16, 128, None, GOOD, GOOD, GOOD, None) == EINVAL
+    assert lib.unisvq_unpack(32, 64, GOOD, GOOD, GOOD, GOOD, None) == ESHAPE
+    assert lib.unisvq_unpack(16, 128, GOOD + 4, GOOD, GOOD, GOOD, None) == EALIGN
+
+
+@pytest.mark.parametrize("fn", ["gemv", "gemm"])
+def test_product_validation(fn):
+    lib = u.load()
+
+    def call(N=64, K=256, packed=GOOD, M=1, x=GOOD, xt=u.F16, y=GOOD, yt=u.F16, ws_bytes=0):
+        if fn == "gemv":
+            return lib.unisvq_gemv(N, K, packed, M, x, xt, y, yt, None)
+        return lib.unisvq_gemm(N, K, packed, M, x, xt, y, yt, None, ws_bytes, None)
+
+    assert call(packed=None) == EINVAL
+    assert call(x=None) == EINVAL
+    assert call(y=None) == EINVAL
+    assert call(M=0) == EINVAL
+    assert call(M=-3) == EINVAL
+    assert call(xt=u.F32) == EINVAL  # activations must be fp16 or bf16
+    assert call(xt=7) == EINVAL
+    assert call(yt=9) == EINVAL
+    assert call(N=8) == ESHAPE
+    assert call(N=40) == ESHAPE
+    assert call(K=200) == ESHAPE
+    assert call(K=64) == ESHAPE
+    assert call(packed=GOOD + 8) == EALIGN
+    assert call(x=GOOD + 2) == EALIGN
+    assert call(y=GOOD + 1) == EALIGN
+    assert call(y=GOOD + 2, yt=u.F32) == EALIGN
+    if fn == "gemv":
+        # more tokens than the matrix-vector kernel takes; checked before launch
+        assert call(M=5, packed=None) == EINVAL
+        assert lib.unisvq_gemv(64, 256, GOOD, 5, GOOD, u.F16, GOOD, u.F16, None) == EUNSUP
+
+
+def test_gemm_workspace_is_zero():
+    assert u.load().unisvq_gemm_workspace_bytes(4096, 4096, 2048) == 0
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(u, "_lib", None)
+    monkeypatch.setattr(u, "LIB_PATH", str(tmp_path / "libunisvq.so"))
+    with pytest.raises(u.UniSVQLibraryMissing):
+        u.load()

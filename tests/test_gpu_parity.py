@@ -1,0 +1,261 @@
+"""GPU parity: libunisvq (HIP, gfx950) against the fp64 oracle.
+
+Bars: packed bytes, unpacked codes and parameters bit-exact; products within
+max|dy| / max|y| <= 2e-3 for fp16 outputs (the stated bar), tighter where the
+arithmetic allows it (fp32 outputs); integer-valued inputs (the D4 generator
+of App. A.2) bit-exact, since every partial sum is an integer below 2^24.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_10520_amd import workloads as wl
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+u = None
+
+
+@pytest.fixture(scope="module", autouse=True)
+def lib():
+    global u
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_10520_amd.unisvq as mod
+    mod.load()  # raises if the library is missing: no fallback
+    u = mod
+    yield mod
+
+
+DEV = "cuda:0"
+
+
+def dev_u16_as_half(a: np.ndarray):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.float16).to(DEV)
+
+
+def dev_x(bits: np.ndarray, dtype: str):
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.view(torch.float16 if dtype == "f16" else torch.bfloat16).to(DEV)
+
+
+def x_as_f64(bits: np.ndarray, dtype: str) -> np.ndarray:
+    return oracle.half_to_double(bits) if dtype == "f16" else oracle.bf16_to_double(bits)
+
+
+def upload_pack(Q, A, B):
+    pk = u.pack(torch.from_numpy(Q).to(DEV), dev_u16_as_half(A), dev_u16_as_half(B))
+    torch.cuda.synchronize()
+    return pk
+
+
+def rel_err(y: np.ndarray, ref: np.ndarray) -> float:
+    return float(np.abs(y.astype(np.float64) - ref).max() / max(np.abs(ref).max(), 1e-300))
+
+
+# --------------------------------------------------------------------- packing
+
+@pytest.mark.parametrize("N,K", [(16, 128), (16, 256), (48, 384), (64, 1152), (4096, 4096), (1024, 11008)])
+def test_pack_bit_exact(N, K):
+    Q, A, B = wl.gen_weights(N, K, seed=N + K)
+    ref, bad = oracle.pack(Q, A, B)
+    assert bad == 0
+    pk = upload_pack(Q, A, B)
+    assert pk.numel() == ref.size == u.packed_bytes(N, K)
+    got = pk.cpu().numpy()
+    diff = np.nonzero(got != ref)[0]
+    assert diff.size == 0, f"{diff.size} bytes differ, first at {diff[:5]}"
+
+
+@pytest.mark.parametrize("N,K", [(16, 128), (32, 640), (4096, 4096)])
+def test_unpack_inverts_pack(N, K):
+    rng = np.random.default_rng(K)
+    Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+    A = rng.integers(0, 65536, size=(N, K // 128, 4, 4), dtype=np.uint32).astype(np.uint16)
+    B = rng.integers(0, 65536, size=(N, K // 128, 4), dtype=np.uint32).astype(np.uint16)
+    pk = upload_pack(Q, A, B)
+    q2, a2, b2 = u.unpack(pk, N, K)
+    torch.cuda.synchronize()
+    assert np.array_equal(q2.cpu().numpy(), Q)
+    assert np.array_equal(a2.cpu().view(torch.int16).numpy().view(np.uint16), A)
+    assert np.array_equal(b2.cpu().view(torch.int16).numpy().view(np.uint16), B)
+    # and the oracle's unpacker reads the GPU's bytes identically
+    q3, a3, b3 = oracle.unpack(pk.cpu().numpy(), N, K)
+    assert np.array_equal(q3, Q) and np.array_equal(a3.view(np.uint16), A)
+
+
+def test_pack_counts_bad_codes():
+    N, K = 32, 256
+    Q = np.zeros((N, K), np.uint8)
+    Q[0, 0], Q[5, 100], Q[31, 255] = 4, 200, 3
+    A = np.zeros((N, 2, 4, 4), np.float16); B = np.zeros((N, 2, 4), np.float16)
+    bad = torch.zeros(1, dtype=torch.int32, device=DEV)
+    pk = u.pack(torch.from_numpy(Q).to(DEV), dev_u16_as_half(A), dev_u16_as_half(B), bad_codes=bad)
+    torch.cuda.synchronize()
+    assert int(bad.item()) == 2
+    ref, nbad = oracle.pack(Q, A, B)
+    assert nbad == 2 and np.array_equal(pk.cpu().numpy(), ref)
+
+
+# --------------------------------------------------------------------- products
+
+def run_product(fn, N, K, M, dtype="f16", out=torch.float32, seed=0, outliers=False):
+    Q, A, B = wl.gen_weights(N, K, seed=seed)
+    xb = wl.gen_activations(M, K, seed=wl.activation_seed(seed, M), dtype=dtype, outliers=outliers)
+    ref_pk, _ = oracle.pack(Q, A, B)
+    pk = upload_pack(Q, A, B)
+    y = getattr(u, fn)(pk, N, K, dev_x(xb, dtype), out_dtype=out)
+    torch.cuda.synchronize()
+    return y, ref_pk, xb
+
+
+@pytest.mark.parametrize("N,K,M", [
+    (16, 128, 1), (16, 384, 1), (64, 1152, 1), (256, 4096, 1), (48, 640, 2), (32, 256, 3), (64, 512, 4),
+    (1024, 8192, 1),
+])
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_gemv_small_shapes_full_parity(N, K, M, dtype):
+    y, pk, xb = run_product("gemv", N, K, M, dtype)
+    ref = oracle.matmul(pk, N, K, x_as_f64(xb, dtype))
+    assert rel_err(y.cpu().numpy(), ref) <= 1e-5
+
+
+@pytest.mark.parametrize("layer", wl.LLAMA7B, ids=lambda l: l.name)
+def test_gemv_llama7b_m1_full_parity_fp16_out(layer):
+    """The 7B decode set at its real shapes, fp16 outputs, every element."""
+    seed = wl.LLAMA7B.index(layer)
+    y, pk, xb = run_product("gemv", layer.N, layer.K, 1, "f16", out=torch.float16, seed=seed)
+    ref = oracle.matmul(pk, layer.N, layer.K, x_as_f64(xb, "f16"))
+    assert rel_err(y.cpu().numpy(), ref) <= 2e-3
+    # fp16 rounding is the only loss: compare to the correctly rounded value
+    np.testing.assert_array_less(np.abs(y.cpu().numpy().astype(np.float64) - ref),
+                                 np.abs(ref) * 2.0 ** -10 + 1e-4 * np.abs(ref).max())
+
+
+@pytest.mark.parametrize("layer", [wl.LLAMA70B[1], wl.LLAMA70B[0], wl.LLAMA70B[6]], ids=lambda l: l.name)
+def test_gemv_llama70b_m1_sampled_rows(layer):
+    y, pk, xb = run_product("gemv", layer.N, layer.K, 1, "f16", seed=10 + layer.N % 7)
+    rows = np.random.default_rng(0).choice(layer.N, 256, replace=False)
+    rows[:2] = [0, layer.N - 1]
+    ref = oracle.matmul(pk, layer.N, layer.K, x_as_f64(xb, "f16"), rows=rows)
+    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 1e-5
+
+
+@pytest.mark.parametrize("M", [1, 2, 3, 4])
+def test_gemv_outlier_activations(M):
+    y, pk, xb = run_product("gemv", 4096, 4096, M, "f16", out=torch.float16, seed=3, outliers=True)
+    ref = oracle.matmul(pk, 4096, 4096, x_as_f64(xb, "f16"))
+    assert rel_err(y.cpu().numpy(), ref) <= 2e-3
+
+
+@pytest.mark.parametrize("N,K,M", [
+    (16, 128, 1), (64, 384, 63), (64, 256, 64), (80, 640, 65), (128, 1152, 130), (256, 4096, 7),
+])
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_gemm_small_shapes_full_parity(N, K, M, dtype):
+    y, pk, xb = run_product("gemm", N, K, M, dtype)
+    ref = oracle.matmul(pk, N, K, x_as_f64(xb, dtype))
+    # fp16: the decoded weight is rounded once to fp16; bf16: carried as hi + lo
+    assert rel_err(y.cpu().numpy(), ref) <= (5e-4 if dtype == "f16" else 2e-5)
+
+
+@pytest.mark.parametrize("layer", wl.PREFILL7B, ids=lambda l: l.name)
+def test_gemm_prefill_m2048_sampled_rows(layer):
+    """Prefill at its real size (M = 2048, bf16 activations), checked on 64 rows."""
+    y, pk, xb = run_product("gemm", layer.N, layer.K, 2048, "bf16", out=torch.float32, seed=20)
+    rows = np.random.default_rng(1).choice(layer.N, 64, replace=False)
+    rows[:2] = [0, layer.N - 1]
+    ref = oracle.matmul(pk, layer.N, layer.K, x_as_f64(xb, "bf16"), rows=rows)
+    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 2e-5
+
+
+# --------------------------------------------------------------------- exactness
+
+def d4_inputs(N, K, M, seed):
+    """Integer-valued inputs: A = the D4 generator of App. A.2 (every group), B and
+    x small integers.  Every decoded weight is an integer of magnitude <= 8 and
+    every partial sum of the product an integer below 2^24."""
+    rng = np.random.default_rng(seed)
+    D4 = np.array([[1, -1, 0, 0], [0, 1, -1, 0], [0, 0, 1, -1], [0, 0, 1, 1]], np.float16)
+    Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+    A = np.broadcast_to(D4, (N, K // 128, 4, 4)).copy()
+    B = rng.integers(-2, 3, size=(N, K // 128, 4)).astype(np.float16)
+    X = rng.integers(-4, 5, size=(M, K)).astype(np.float16)
+    return Q, A, B, X
+
+
+@pytest.mark.parametrize("fn,M", [("gemv", 1), ("gemv", 4), ("gemm", 33)])
+def test_integer_inputs_bit_exact(fn, M):
+    N, K = 512, 4096
+    Q, A, B, X = d4_inputs(N, K, M, seed=M)
+    pk_ref, _ = oracle.pack(Q, A, B)
+    pk = upload_pack(Q, A, B)
+    x = torch.from_numpy(X).to(DEV)
+    y32 = getattr(u, fn)(pk, N, K, x, out_dtype=torch.float32)
+    y16 = getattr(u, fn)(pk, N, K, x, out_dtype=torch.float16)
+    torch.cuda.synchronize()
+    ref = oracle.matmul(pk_ref, N, K, X.astype(np.float64))
+    assert np.abs(ref).max() < 2 ** 24 and np.array_equal(ref, np.round(ref))
+    assert np.array_equal(y32.cpu().numpy().astype(np.float64), ref)
+    assert np.array_equal(y16.cpu().numpy(), ref.astype(np.float16))  # one RNE rounding
+
+
+def test_identity_transform_is_integer_matmul_on_gpu():
+    """A = I, B = 0 (the scalar special case with unit scale): y = x Q^T."""
+    N, K, M = 256, 1024, 2
+    rng = np.random.default_rng(8)
+    Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+    A = np.zeros((N, K // 128, 4, 4), np.float16)
+    for a in range(4):
+        A[:, :, a, a] = 1
+    B = np.zeros((N, K // 128, 4), np.float16)
+    X = rng.integers(-8, 9, size=(M, K)).astype(np.float16)
+    pk = upload_pack(Q, A, B)
+    for fn in ("gemv", "gemm"):
+        y = getattr(u, fn)(pk, N, K, torch.from_numpy(X).to(DEV), out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        assert np.array_equal(y.cpu().numpy().astype(np.float64), X.astype(np.float64) @ Q.T.astype(np.float64))
+
+
+# --------------------------------------------------------------------- edge behaviour
+
+def test_output_is_overwritten_and_guard_bytes_untouched():
+    N, K, M = 256, 1152, 3
+    Q, A, B = wl.gen_weights(N, K, seed=4)
+    pk = upload_pack(Q, A, B)
+    xb = wl.gen_activations(M, K, seed=5)
+    x = dev_x(xb, "f16")
+    for fn in ("gemv", "gemm"):
+        buf = torch.full((M * N + 2 * 64,), 12345.0, dtype=torch.float32, device=DEV)
+        out = buf[64:64 + M * N].view(M, N)
+        getattr(u, fn)(pk, N, K, x, out=out)
+        torch.cuda.synchronize()
+        b = buf.cpu().numpy()
+        assert np.all(b[:64] == 12345.0) and np.all(b[64 + M * N:] == 12345.0)
+        ref = oracle.matmul(oracle.pack(Q, A, B)[0], N, K, x_as_f64(xb, "f16"))
+        assert rel_err(out.cpu().numpy(), ref) <= 5e-4
+
+
+def test_repeatable_and_linear_in_x():
+    N, K = 1024, 4096
+    Q, A, B = wl.gen_weights(N, K, seed=6)
+    pk = upload_pack(Q, A, B)
+    rng = np.random.default_rng(2)
+    X = rng.integers(-4, 5, size=(2, K)).astype(np.float16)
+    x = torch.from_numpy(X).to(DEV)
+    y1 = u.gemv(pk, N, K, x, out_dtype=torch.float32)
+    y2 = u.gemv(pk, N, K, x, out_dtype=torch.float32)
+    x2 = torch.from_numpy((2 * X).astype(np.float16)).to(DEV)
+    y3 = u.gemv(pk, N, K, x2, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)          # no atomics: bit-identical reruns
+    assert torch.equal(y3, 2 * y1)      # scaling x by 2 is exact end to end
+
+
+def test_gemv_rejects_more_than_four_tokens():
+    pk = torch.zeros(u.packed_bytes(64, 256), dtype=torch.uint8, device=DEV)
+    x = torch.zeros((5, 256), dtype=torch.float16, device=DEV)
+    with pytest.raises(u.UniSVQError) as e:
+        u.gemv(pk, 64, 256, x)
+    assert e.value.status == -3
