@@ -1,0 +1,290 @@
+#!/usr/bin/env python3
+"""Benchmark of the UniSVQ 2-bit affine-lattice product on one MI355X.
+
+Default workload: the LLaMA-7B decoder linears at M = 1 token (q/k/v/o
+4096x4096, gate/up 11008x4096, down 4096x11008), 2-bit codes in d = 4
+vectors along K with one fp16 (A, B) set per (row, 128-column group), fp16
+activations.  One step = one pass of the seven linears through unisvq_gemv,
+launched back to back on one stream.  Weights, activations and outputs are
+resident in HBM before timing starts; the step rotates over enough copies of
+the layer set (> 512 MB) that the 256 MB Infinity Cache cannot serve them.
+
+Prints one JSON line.  value = algorithmic bytes per step / time per step
+(codes N*K/4 + affine N*(K/128)*40 + activations + outputs; dense fp16
+weights are never counted).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2606_10520_amd import workloads as wl  # noqa: E402
+
+PEAK_HBM_GBS = 8000.0      # MI355X HBM3E, datasheet
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16/fp16 matrix, datasheet
+MALL_BYTES = 256 << 20
+METRIC = "2-bit GEMV achieved HBM GB/s (% peak) + µs/layer at 7B shapes, M=1"
+
+
+def algorithmic_bytes(N: int, K: int, M: int, x_bytes: int = 2, y_bytes: int = 2) -> int:
+    return N * K // 4 + N * (K // 128) * 40 + M * K * x_bytes + M * N * y_bytes
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--workload", default="llama7b_decode_m1",
+                   choices=["llama7b_decode_m1", "layer4096_m1", "llama70b_decode_m1",
+                            "llama70b_decode_m16", "llama7b_smallbatch_m4", "llama7b_smallbatch_m16",
+                            "llama7b_smallbatch_m64", "llama7b_prefill_m2048"])
+    p.add_argument("--schedule", default="decoder", choices=["decoder", "per_layer", "single"],
+                   help="decoder: q/k/v in one batched launch, o, gate/up in one batched launch, down "
+                        "(how a decode step runs them); per_layer: one launch per linear; single: all "
+                        "linears in one batched launch")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU work of the oracle sample")
+    p.add_argument("--no-launch-events", action="store_true",
+                   help="skip the per-launch event pass (roofline fields become null)")
+    return p.parse_args()
+
+
+def workload_spec(name: str):
+    """(layers, M, activation dtype, outliers, kernel)"""
+    if name == "llama7b_decode_m1":
+        return wl.LLAMA7B, 1, "f16", False, "gemv"
+    if name == "layer4096_m1":
+        return (wl.Layer("layer", 4096, 4096),), 1, "f16", False, "gemv"
+    if name == "llama70b_decode_m1":
+        return wl.LLAMA70B, 1, "f16", False, "gemv"
+    if name == "llama70b_decode_m16":
+        return wl.LLAMA70B, 16, "f16", False, "gemm"
+    if name.startswith("llama7b_smallbatch_m"):
+        M = int(name.rsplit("m", 1)[1])
+        return wl.LLAMA7B, M, "f16", True, ("gemv" if M <= 4 else "gemm")
+    if name == "llama7b_prefill_m2048":
+        return wl.PREFILL7B, 2048, "bf16", False, "gemm"
+    raise ValueError(name)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
+              "this build has no multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2606_10520_amd.unisvq as u
+
+    u.load()  # fails loudly if libunisvq.so is missing
+    dev = torch.device("cuda:0")
+    layers, M, xdt, outliers, kernel = workload_spec(args.workload)
+    tdt = torch.float16 if xdt == "f16" else torch.bfloat16
+
+    # ---- inputs: canonical arrays drawn on the host, packed on the GPU
+    canon = []
+    for li, L in enumerate(layers):
+        Q, A, B = wl.gen_weights(L.N, L.K, seed=li)
+        xb = wl.gen_activations(M, L.K, seed=wl.activation_seed(li, M), dtype=xdt, outliers=outliers)
+        canon.append((Q, A, B, xb))
+    set_bytes = sum(algorithmic_bytes(L.N, L.K, M) for L in layers)
+    set_packed = sum(u.packed_bytes(L.N, L.K) for L in layers)
+    copies = max(2, -(-2 * MALL_BYTES // set_packed) + 1)
+
+    packed0 = []
+    for (Q, A, B, _), L in zip(canon, layers):
+        pk = u.pack(torch.from_numpy(Q).to(dev),
+                    torch.from_numpy(A.view(np.int16)).view(torch.float16).to(dev),
+                    torch.from_numpy(B.view(np.int16)).view(torch.float16).to(dev))
+        packed0.append(pk)
+    sets = []
+    for c in range(copies):
+        s = []
+        for li, L in enumerate(layers):
+            pk = packed0[li] if c == 0 else packed0[li].clone()
+            x = torch.from_numpy(canon[li][3].view(np.int16)).view(tdt).to(dev)
+            y = torch.empty((M, L.N), dtype=torch.float16, device=dev)
+            s.append((L, pk, x, y))
+        sets.append(s)
+    torch.cuda.synchronize()
+
+    lib = u.load()
+    xcode = u.F16 if xdt == "f16" else u.BF16
+    names = [L.name for L in layers]
+    sched = args.schedule if kernel == "gemv" else "per_layer"
+    if sched == "decoder" and {"q", "k", "v", "o", "gate", "up", "down"} <= set(names):
+        groups_ = [["q", "k", "v"], ["o"], ["gate", "up"], ["down"]]
+    elif sched == "single":
+        groups_ = [names]
+    else:
+        sched = "per_layer"
+        groups_ = [[n] for n in names]
+    calls = []  # per copy: list of (label, ctypes problem array or single tuple)
+    for s_ in sets:
+        by = {L.name: (L, pk, x, y) for (L, pk, x, y) in s_}
+        cc = []
+        for grp in groups_:
+            if len(grp) == 1 or kernel != "gemv":
+                cc.append(("+".join(grp), by[grp[0]]))
+            else:
+                arr = (u.GemvProblem * len(grp))()
+                for i, n in enumerate(grp):
+                    L, pk, x, y = by[n]
+                    arr[i] = u.GemvProblem(L.N, L.K, pk.data_ptr(), x.data_ptr(), y.data_ptr())
+                cc.append(("+".join(grp), arr))
+        calls.append(cc)
+
+    def launch(item, sptr):
+        if isinstance(item, tuple):
+            L, pk, x, y = item
+            if kernel == "gemv":
+                return lib.unisvq_gemv(L.N, L.K, pk.data_ptr(), M, x.data_ptr(), xcode, y.data_ptr(), u.F16, sptr)
+            return lib.unisvq_gemm(L.N, L.K, pk.data_ptr(), M, x.data_ptr(), xcode, y.data_ptr(), u.F16,
+                                   None, 0, sptr)
+        return lib.unisvq_gemv_batched(item, len(item), M, xcode, u.F16, sptr)
+
+    def run_step(i, sptr):
+        for _, item in calls[i % copies]:
+            st = launch(item, sptr)
+            if st != 0:
+                raise RuntimeError(f"{kernel} failed with status {st}")
+
+    stream = torch.cuda.current_stream()
+    for i in range(args.warmup):
+        run_step(i, stream.cuda_stream)
+    torch.cuda.synchronize()
+
+    # ---- the step sequence for all buffer copies, captured once in a HIP graph
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        cap = torch.cuda.current_stream().cuda_stream
+        for c in range(copies):
+            run_step(c, cap)
+    torch.cuda.synchronize()
+    graph.replay()  # one untimed replay
+    torch.cuda.synchronize()
+
+    # ---- timed region: K steps = ceil(K / copies) graph replays
+    replays = max(1, -(-args.steps // copies))
+    steps_done = replays * copies
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(replays):
+        graph.replay()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / steps_done
+    value_gbs = set_bytes / (ms_per_step * 1e-3) / 1e9
+
+    # ---- per-launch durations: HIP events on the launch stream around each
+    # launch.  A spin kernel first lets the host queue a chunk of launches ahead
+    # of the GPU, so an interval brackets GPU work rather than host latency.
+    per_layer_us = {}
+    roofline = None
+    if not args.no_launch_events:
+        ev = []
+        chunk = 8
+        for c0 in range(0, args.steps, chunk):
+            torch.cuda.synchronize()
+            torch.cuda._sleep(20_000_000)  # ~8 ms of spinning at 2.4 GHz
+            for i in range(c0, min(args.steps, c0 + chunk)):
+                for label, item in calls[i % copies]:
+                    a = torch.cuda.Event(enable_timing=True)
+                    b = torch.cuda.Event(enable_timing=True)
+                    a.record(stream)
+                    launch(item, stream.cuda_stream)
+                    b.record(stream)
+                    ev.append((label, a, b))
+        torch.cuda.synchronize()
+        durs = {}
+        for name, a, b in ev:
+            durs.setdefault(name, []).append(a.elapsed_time(b) * 1e3)
+        per_layer_us = {k: float(np.mean(v)) for k, v in durs.items()}
+        launches = len(ev)
+        total_us = sum(sum(v) for v in durs.values())
+        n_steps_ev = launches // len(groups_)
+        bytes_per_launch = set_bytes * n_steps_ev / launches
+        avg_us = total_us / launches
+        if kernel == "gemv":
+            ach = bytes_per_launch / (avg_us * 1e-6) / 1e9
+            roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                        "kernel": "gemv_kernel", "avg_launch_us": round(avg_us, 3),
+                        "bytes_per_launch": int(bytes_per_launch)}
+        else:
+            flops = sum(2 * M * L.N * L.K for L in layers) * n_steps_ev / launches
+            ach = flops / (avg_us * 1e-6) / 1e12
+            roofline = {"bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS,
+                        "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                        "kernel": "gemm_kernel", "avg_launch_us": round(avg_us, 3)}
+
+    # ---- CPU baseline: the fp64 oracle on the host cores, bounded sample
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = oracle.default_threads()
+        packed_h = [oracle.pack(Q, A, B)[0] for (Q, A, B, _) in canon]
+        xs = [oracle.half_to_double(xb) if xdt == "f16" else oracle.bf16_to_double(xb) for (_, _, _, xb) in canon]
+        rows_frac = 1.0
+        if M > 16:  # prefill: a bounded slice of output rows per layer
+            rows_frac = 1.0 / 64
+        done_bytes, t_cpu, passes = 0.0, 0.0, 0
+        while t_cpu < args.cpu_seconds or passes == 0:
+            for li, L in enumerate(layers):
+                nrows = max(16, int(L.N * rows_frac))
+                rows = None if nrows >= L.N else np.arange(nrows)
+                s0 = time.perf_counter()
+                oracle.matmul(packed_h[li], L.N, L.K, xs[li], rows=rows, threads=threads)
+                t_cpu += time.perf_counter() - s0
+                done_bytes += algorithmic_bytes(L.N, L.K, M) * (nrows / L.N)
+            passes += 1
+        cpu = {"value": round(done_bytes / t_cpu / 1e9, 3), "unit": "GB/s", "cores": threads,
+               "kind": "oracle",
+               "sample": f"{passes} pass(es) over the {args.workload} layer set"
+                         + ("" if rows_frac == 1.0 else f" (1/{int(1 / rows_frac)} of output rows)")
+                         + f", fp64 C oracle, {threads} threads, {t_cpu:.1f} s"}
+
+    if kernel == "gemv":
+        metric, value, unit = METRIC, value_gbs, "GB/s"
+    else:
+        flops = sum(2 * M * L.N * L.K for L in layers)
+        metric, value, unit = "unisvq_gemm effective TFLOP/s (2MNK)", flops / (ms_per_step * 1e-3) / 1e12, "TFLOP/s"
+    out = {
+        "metric": metric,
+        "value": round(value, 2),
+        "unit": unit,
+        "n_gpus": 1,
+        "steps": steps_done,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16" if xdt == "f16" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "layers": {L.name: [L.N, L.K] for L in layers}, "M": M,
+                   "d": 4, "bits": 2, "group": 128, "kernel": kernel, "schedule": sched,
+                   "launches_per_step": len(groups_), "buffer_copies": copies,
+                   "set_bytes": set_bytes},
+        "pct_peak_hbm": round(100 * value_gbs / PEAK_HBM_GBS, 2) if kernel == "gemv" else None,
+        "us_per_launch": {k: round(v, 3) for k, v in per_layer_us.items()},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

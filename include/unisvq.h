@@ -128,6 +128,27 @@ int unisvq_unpack(int64_t N, int64_t K, const void* packed, uint8_t* codes, uint
 int unisvq_gemv(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype,
                 void* y, int y_dtype, void* stream);
 
+/* One product of a batched decode-phase call. */
+typedef struct {
+    int64_t N, K;        /* shape of this weight matrix (N % 16 == 0, K % 128 == 0) */
+    const void* packed;  /* device, packed N x K matrix, 16-byte aligned */
+    const void* x;       /* device [M][K], 16-byte aligned */
+    void* y;             /* device [M][N] */
+} unisvq_gemv_problem;
+
+#define UNISVQ_MAX_BATCH 8
+
+/* Several independent decode-phase products y_i = x_i * W_hat_i^T in one
+ * launch (same M, x_dtype and y_dtype for all).  A decoder layer's query,
+ * key and value projections, or its gate and up projections, read the same
+ * activations and are independent -- one launch serves them all, which at
+ * batch 1 saves a kernel launch per extra matrix.
+ *   problems  HOST array of `count` descriptors (1..UNISVQ_MAX_BATCH); read
+ *             before the call returns, so the caller may reuse it at once
+ *   others    as unisvq_gemv.  Every descriptor is validated before launch. */
+int unisvq_gemv_batched(const unisvq_gemv_problem* problems, int count, int64_t M, int x_dtype,
+                        int y_dtype, void* stream);
+
 /* Workspace the GEMM needs for this problem (currently always 0). */
 size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M);
 

@@ -24,6 +24,8 @@ int check_product(int64_t N, int64_t K, const void* packed, int64_t M, const voi
     if (!x_dtype_ok(x_dtype) || !y_dtype_ok(y_dtype)) return UNISVQ_EINVAL;
     if (!shape_ok(N, K)) return UNISVQ_ESHAPE;
     if (!aligned(packed, 16) || !aligned(x, 16)) return UNISVQ_EALIGN;
+    // the kernels address the packed matrix with 32-bit buffer offsets
+    if (static_cast<int64_t>(unisvq_packed_bytes(N, K)) > unisvq::kMaxBufferBytes) return UNISVQ_EUNSUP;
     if (!aligned(y, y_dtype == UNISVQ_F32 ? 4 : 2)) return UNISVQ_EALIGN;
     return UNISVQ_OK;
 }
@@ -81,6 +83,22 @@ int unisvq_gemv(int64_t N, int64_t K, const void* packed, int64_t M, const void*
     if (M > 4) return UNISVQ_EUNSUP;
     return unisvq::launch_gemv(N, K, static_cast<const uint8_t*>(packed), M, x, x_dtype, y, y_dtype,
                                static_cast<hipStream_t>(stream));
+}
+
+int unisvq_gemv_batched(const unisvq_gemv_problem* problems, int count, int64_t M, int x_dtype,
+                        int y_dtype, void* stream) {
+    if (!problems || count < 1) return UNISVQ_EINVAL;
+    if (count > UNISVQ_MAX_BATCH) return UNISVQ_EUNSUP;
+    unisvq::GemvProblem probs[UNISVQ_MAX_BATCH];
+    for (int i = 0; i < count; ++i) {
+        const unisvq_gemv_problem& q = problems[i];
+        const int st = check_product(q.N, q.K, q.packed, M, q.x, x_dtype, q.y, y_dtype);
+        if (st != UNISVQ_OK) return st;
+        probs[i] = unisvq::GemvProblem{static_cast<const uint8_t*>(q.packed), q.x, q.y,
+                                       static_cast<int>(q.N), static_cast<int>(q.K), 0};
+    }
+    if (M > 4) return UNISVQ_EUNSUP;
+    return unisvq::launch_gemv_batch(probs, count, M, x_dtype, y_dtype, static_cast<hipStream_t>(stream));
 }
 
 size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M) {

@@ -16,6 +16,35 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+
+// Raw buffer access: a resource descriptor carries the buffer's size, and the
+// hardware returns zeros for any read beyond it instead of faulting, so loads
+// need no guarding branches (which would also serialise the wait counters).
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), static_cast<short>(0),
+                                             static_cast<int>(bytes), 0x00020000);
+}
+__device__ inline uint4 ld128(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    const i32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    return uint4{static_cast<uint32_t>(v.x), static_cast<uint32_t>(v.y), static_cast<uint32_t>(v.z),
+                 static_cast<uint32_t>(v.w)};
+}
+__device__ inline uint2 ld64(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    const i32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+    return uint2{static_cast<uint32_t>(v.x), static_cast<uint32_t>(v.y)};
+}
+__device__ inline uint32_t ld32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+__device__ inline uint32_t ld16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+}
+
+// Largest buffer a 32-bit buffer offset addresses.
+constexpr int64_t kMaxBufferBytes = (int64_t{1} << 31) - 1;
+
 // Packed format v1 geometry (see the format block in unisvq.h).
 constexpr int kGroup = 128;            // input columns per (A, B) set
 constexpr int kRowBlock = 16;          // rows per row block
@@ -32,8 +61,20 @@ hipError_t launch_pack(int64_t N, int64_t K, const uint8_t* codes, const uint16_
 hipError_t launch_unpack(int64_t N, int64_t K, const uint8_t* packed, uint8_t* codes,
                          uint16_t* A, uint16_t* B, hipStream_t s);
 
+// One problem of a (possibly batched) matrix-vector launch.
+struct GemvProblem {
+    const uint8_t* packed;
+    const void* x;
+    void* y;
+    int N, K;
+    int rb_begin;  // first workgroup index of this problem (set by the launcher)
+};
+constexpr int kMaxBatch = 8;
+
 // Matrix-vector path: returns UNISVQ_EUNSUP if the shape does not fit the
 // kernel (LDS budget), else maps the launch result to a status.
+int launch_gemv_batch(const GemvProblem* probs, int count, int64_t M, int x_dtype, int y_dtype,
+                      hipStream_t s);
 int launch_gemv(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x,
                 int x_dtype, void* y, int y_dtype, hipStream_t s);
 int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x,

@@ -22,14 +22,21 @@
 //   B[r][g][b], which is exactly that lane's affine slot.
 // The dequantised weights never leave registers (they are never formed).
 //
-// Work split: one workgroup per 16-row block; its WAVES wavefronts split the
-// packets along K; partial sums meet in LDS.  Activations for the whole K
-// range are staged in LDS once per workgroup in matrix-core operand order.
+// Schedule.  One workgroup per 16-row block of one problem (several
+// independent problems may share a launch); its WAVES wavefronts split the
+// block's packets along K into contiguous runs.  Each workgroup first loads
+// its activations, then issues the wavefronts' packet loads, and stages the
+// activations into LDS in operand order -- with the per-group sums xbar
+// formed by DPP row reductions -- while the packet data is still in flight.
+// The main loop consumes packets as they arrive (PF loads in flight per
+// wavefront), running four independent matrix-core chains per packet.
+// Partial row sums meet in LDS at the end.
 #include <atomic>
 
 #include "common.hpp"
 
 namespace unisvq {
+
 namespace {
 
 template <typename XT>
@@ -63,10 +70,10 @@ struct XOps<__bf16> {
 // four SrcB operands.  Operand n holds vectors 4n+0, 4n+2, 4n+1, 4n+3 (the
 // nibble order the e2m1 converter produces); the activation operand uses the
 // same slot order.
-template <typename XT, int N>
+template <typename XT, int SEL>
 __device__ inline typename XOps<XT>::vec4 code_operand(uint32_t e, uint32_t o) {
-    auto lo = XOps<XT>::template cvt2<N>(e);
-    auto hi = XOps<XT>::template cvt2<N>(o);
+    auto lo = XOps<XT>::template cvt2<SEL>(e);
+    auto hi = XOps<XT>::template cvt2<SEL>(o);
     return __builtin_shufflevector(lo, hi, 0, 1, 2, 3);
 }
 
@@ -91,153 +98,304 @@ __device__ inline float h2f(uint32_t bits16) {
     return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(bits16)));
 }
 
-// Contract one group: codes (two words = the lane's 64-bit field), A column,
-// B value; adds the group's contribution for every token into acc.
+template <int CTRL>
+__device__ inline float dpp(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                                 0xf, 0xf, true));
+}
+
+// Inclusive sum over the 16 lanes of a DPP row; lane 15 of the row ends
+// with the row total.
+__device__ inline float row16_sum_to_last(float v) {
+    v += dpp<0x111>(v);  // row_shr:1
+    v += dpp<0x112>(v);  // row_shr:2
+    v += dpp<0x114>(v);  // row_shr:4
+    v += dpp<0x118>(v);  // row_shr:8
+    return v;
+}
+
+// Sum over the 4 lanes of a quad, result in every lane of the quad.
+__device__ inline float quad_sum(float v) {
+    v += dpp<0xB1>(v);  // quad_perm [1,0,3,2]
+    v += dpp<0x4E>(v);  // quad_perm [2,3,0,1]
+    return v;
+}
+
+}  // namespace
+
+struct GemvBatch {
+    GemvProblem p[kMaxBatch];
+    int count;
+    int M;
+    int y_dtype;
+};
+
+namespace {
+
+// A buffer offset past the end of every buffer the kernels address: the load
+// returns zeros and generates no memory traffic.
+constexpr uint32_t kOutOfRange = 0x80000000u;
+
+// One 16-byte activation chunk: vectors 2*q16 and 2*q16+1 of group g, token t.
+template <typename XT>
+__device__ inline void stage_chunk(const uint4& raw, int t, int g, int q16, int groups, XT* xs, float* xbar) {
+    const int vbase = 2 * q16;
+    uint16_t* line = reinterpret_cast<uint16_t*>(xs) + (static_cast<size_t>(t) * groups + g) * 128;
+    const uint16_t* v16 = reinterpret_cast<const uint16_t*>(&raw);
+    float part[4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+        line[a * 32 + operand_slot(vbase)] = v16[a];
+        line[a * 32 + operand_slot(vbase + 1)] = v16[4 + a];
+        part[a] = static_cast<float>(__builtin_bit_cast(XT, v16[a])) +
+                  static_cast<float>(__builtin_bit_cast(XT, v16[4 + a]));
+    }
+    // The 16 lanes of a DPP row hold the 16 chunks of one group.
+#pragma unroll
+    for (int a = 0; a < 4; ++a) part[a] = row16_sum_to_last(part[a]);
+    if (q16 == 15) {
+        float* xb = xbar + (static_cast<size_t>(t) * groups + g) * 4;
+#pragma unroll
+        for (int a = 0; a < 4; ++a) xb[a] = part[a];
+    }
+}
+
 template <typename XT, int MT>
-__device__ inline void group_step(uint32_t w0, uint32_t w1, uint32_t a01, uint32_t a23, uint32_t bbits,
-                                  const XT* __restrict__ xs_g, const float* __restrict__ xbar_g,
-                                  int xs_tok_stride, int xbar_tok_stride, int M, int lane,
-                                  typename XOps<XT>::vec4 (&xop)[8], float (&acc)[MT]) {
+__device__ inline void epilogue(const f32x4& d, uint32_t a01, uint32_t a23, uint32_t bbits, float xb,
+                                float& acc) {
+    float r = acc;
+    r = __builtin_fmaf(h2f(a01 & 0xffffu), d[0], r);
+    r = __builtin_fmaf(h2f(a01 >> 16), d[1], r);
+    r = __builtin_fmaf(h2f(a23 & 0xffffu), d[2], r);
+    r = __builtin_fmaf(h2f(a23 >> 16), d[3], r);
+    acc = __builtin_fmaf(h2f(bbits), xb, r);
+}
+
+// One full packet: groups g and g+1 of the row block, both contracted with
+// interleaved, independent matrix-core chains.
+// x0 / x1 hold the activation operand; only lanes 0..3 are ever written
+// (the other lanes keep zeros -- the broadcast ignores them).
+template <typename XT, int MT>
+__device__ inline void packet_step(const uint4& c, const uint4& a, uint32_t bw, int g, const XT* xs,
+                                   const float* xbar, int groups, int M, int lane, float (&acc)[MT],
+                                   typename XOps<XT>::vec4 (&x0)[8], typename XOps<XT>::vec4 (&x1)[8]) {
     typedef typename XOps<XT>::vec4 vec4;
-    vec4 cop[8];
-    word_operands<XT>(w0, cop);
-    word_operands<XT>(w1, cop + 4);
-    const float A0 = h2f(a01 & 0xffffu), A1 = h2f(a01 >> 16);
-    const float A2 = h2f(a23 & 0xffffu), A3 = h2f(a23 >> 16);
-    const float Bv = h2f(bbits);
+    vec4 cop0[8], cop1[8];
+    word_operands<XT>(c.x, cop0);
+    word_operands<XT>(c.y, cop0 + 4);
+    word_operands<XT>(c.z, cop1);
+    word_operands<XT>(c.w, cop1 + 4);
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
         if (t < M) {
             if (lane < 4) {
-                const vec4* src = reinterpret_cast<const vec4*>(xs_g + t * xs_tok_stride + lane * 32);
+                const vec4* s0 = reinterpret_cast<const vec4*>(xs + ((static_cast<size_t>(t) * groups + g) * 4 + lane) * 32);
+                const vec4* s1 = s0 + 32;  // next group: 128 elements further
 #pragma unroll
-                for (int s = 0; s < 8; ++s) xop[s] = src[s];
+                for (int s = 0; s < 8; ++s) { x0[s] = s0[s]; x1[s] = s1[s]; }
             }
-            f32x4 d = {0.f, 0.f, 0.f, 0.f};
+            f32x4 d0a = {0.f, 0.f, 0.f, 0.f}, d0b = d0a, d1a = d0a, d1b = d0a;
 #pragma unroll
-            for (int s = 0; s < 8; ++s) d = XOps<XT>::mfma(xop[s], cop[s], d);
-            const float xb = xbar_g[t * xbar_tok_stride + (lane & 3)];
-            float r = acc[t];
-            r = __builtin_fmaf(A0, d[0], r);
-            r = __builtin_fmaf(A1, d[1], r);
-            r = __builtin_fmaf(A2, d[2], r);
-            r = __builtin_fmaf(A3, d[3], r);
-            acc[t] = __builtin_fmaf(Bv, xb, r);
+            for (int s = 0; s < 8; s += 2) {
+                d0a = XOps<XT>::mfma(x0[s], cop0[s], d0a);
+                d1a = XOps<XT>::mfma(x1[s], cop1[s], d1a);
+                d0b = XOps<XT>::mfma(x0[s + 1], cop0[s + 1], d0b);
+                d1b = XOps<XT>::mfma(x1[s + 1], cop1[s + 1], d1b);
+            }
+            const float* xb = xbar + (static_cast<size_t>(t) * groups + g) * 4 + (lane & 3);
+            epilogue<XT, MT>(d0a + d0b, a.x, a.y, bw & 0xffffu, xb[0], acc[t]);
+            epilogue<XT, MT>(d1a + d1b, a.z, a.w, bw >> 16, xb[4], acc[t]);
         }
     }
 }
 
-template <typename XT, int WAVES, int MT, int PF>
-__global__ __launch_bounds__(WAVES * 64) void gemv_kernel(const uint8_t* __restrict__ packed,
-                                                          const XT* __restrict__ x,
-                                                          void* __restrict__ y, int N, int K, int M,
-                                                          int y_dtype) {
+// The last group of a row block when the group count is odd.
+template <typename XT, int MT>
+__device__ inline void half_step(const uint2& c, const uint2& a, uint32_t bbits, int g, const XT* xs,
+                                 const float* xbar, int groups, int M, int lane, float (&acc)[MT],
+                                 typename XOps<XT>::vec4 (&x0)[8]) {
     typedef typename XOps<XT>::vec4 vec4;
+    vec4 cop[8];
+    word_operands<XT>(c.x, cop);
+    word_operands<XT>(c.y, cop + 4);
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+        if (t < M) {
+            if (lane < 4) {
+                const vec4* s0 = reinterpret_cast<const vec4*>(xs + ((static_cast<size_t>(t) * groups + g) * 4 + lane) * 32);
+#pragma unroll
+                for (int s = 0; s < 8; ++s) x0[s] = s0[s];
+            }
+            f32x4 da = {0.f, 0.f, 0.f, 0.f}, db = da;
+#pragma unroll
+            for (int s = 0; s < 8; s += 2) {
+                da = XOps<XT>::mfma(x0[s], cop[s], da);
+                db = XOps<XT>::mfma(x0[s + 1], cop[s + 1], db);
+            }
+            const float xb = xbar[(static_cast<size_t>(t) * groups + g) * 4 + (lane & 3)];
+            epilogue<XT, MT>(da + db, a.x, a.y, bbits, xb, acc[t]);
+        }
+    }
+}
+
+// Template parameters: WAVES wavefronts per workgroup, MT the largest token
+// count, PF packets in flight per wavefront, NX activation load instructions
+// per wavefront (issued ahead of the packet loads), OCC the minimum
+// wavefronts per SIMD the register allocation must allow.
+template <typename XT, int WAVES, int MT, int PF, int NX, int OCC>
+__global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch batch) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    constexpr int kThreads = WAVES * 64;
+
+    // problem of this workgroup (uniform scalar selection)
+    const int bid = blockIdx.x;
+    const uint8_t* packed = batch.p[0].packed;
+    const XT* x = static_cast<const XT*>(batch.p[0].x);
+    void* y = batch.p[0].y;
+    int N = batch.p[0].N, K = batch.p[0].K, rb0 = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxBatch; ++i) {
+        if (i < batch.count && bid >= batch.p[i].rb_begin) {
+            packed = batch.p[i].packed;
+            x = static_cast<const XT*>(batch.p[i].x);
+            y = batch.p[i].y;
+            N = batch.p[i].N;
+            K = batch.p[i].K;
+            rb0 = batch.p[i].rb_begin;
+        }
+    }
+    const int M = batch.M;
+    const int rb = bid - rb0;
+    (void)kThreads;
     const int groups = K >> 7;
     const int nfull = groups >> 1;
     const bool has_half = (groups & 1) != 0;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int rb = blockIdx.x;
 
-    XT* xs = reinterpret_cast<XT*>(smem);                                     // [M][groups][4][32]
+    XT* xs = reinterpret_cast<XT*>(smem);                                                   // [M][groups][4][32]
     float* xbar = reinterpret_cast<float*>(smem + static_cast<size_t>(M) * groups * 256);  // [M][groups][4]
-    float* red = xbar + M * groups * 4;                                       // [WAVES][MT][16]
+    float* red = xbar + M * groups * 4;                                                     // [WAVES][MT][16]
 
-    const uint8_t* blk = packed + static_cast<size_t>(rb) * groups * kGroupBlockBytes;
+    // This wavefront's run: full packets [p0, p0 + np), i.e. groups
+    // [2 p0, 2 (p0 + np)), plus the trailing half packet for the last wavefront.
     const int per = (nfull + WAVES - 1) / WAVES;
     const int p0 = min(nfull, wave * per);
     const int np = min(nfull, p0 + per) - p0;
+    const bool do_half = has_half && wave == WAVES - 1;
+    const int g0 = 2 * p0;
+    const int ngw = 2 * np + (do_half ? 1 : 0);  // groups this wavefront reads
+    const int gbeg = do_half && np == 0 ? groups - 1 : g0;
 
-    // 1. Issue this wave's first PF packet loads; they do not depend on x.
+    // 1. Activation loads for exactly this wavefront's groups, before the
+    //    packet loads so that staging them waits for nothing else.  Each
+    //    16-byte chunk holds two vectors; 16 consecutive lanes (a DPP row)
+    //    hold one group of one token.  Loads stay outside any branch (a branch
+    //    around a load makes the wait counters drain completely at the join);
+    //    an unneeded load gets an offset past the end of the buffer and returns
+    //    zeros without touching memory.
+    const int chunks_w = M * 16 * ngw;
+    const int nxi = (chunks_w + 63) >> 6;  // load instructions needed (wave-uniform)
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(M) * K * 2u);
+    auto chunk_off = [&](int c) -> uint32_t {  // byte offset of local chunk c in x
+        const int t = MT == 1 ? 0 : c / (16 * ngw);
+        const int lc = c - t * 16 * ngw;
+        return (static_cast<uint32_t>(t) * K + static_cast<uint32_t>(gbeg) * 128 + lc * 8) * 2u;
+    };
+    uint4 xr[NX];
+#pragma unroll
+    for (int i = 0; i < NX; ++i) {
+        const int c = 64 * i + lane;
+        xr[i] = ld128(rx, c < chunks_w ? chunk_off(c) : kOutOfRange);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // keep the activation loads ahead of the packet loads
+
+    // 2. The first PF packets of this wavefront's run.
+    const __amdgpu_buffer_rsrc_t rw =
+        make_rsrc(packed, static_cast<uint32_t>(N / kRowBlock) * groups * kGroupBlockBytes);
+    const uint32_t blk = static_cast<uint32_t>(rb) * groups * kGroupBlockBytes;
     uint4 cbuf[PF], abuf[PF];
     uint32_t bbuf[PF];
-    if (np > 0) {
 #pragma unroll
-        for (int i = 0; i < PF; ++i) {
-            const uint8_t* pk = blk + static_cast<size_t>(p0 + min(i, np - 1)) * kPacketBytes;
-            cbuf[i] = *reinterpret_cast<const uint4*>(pk + 16 * lane);
-            abuf[i] = *reinterpret_cast<const uint4*>(pk + kPacketAffineOff + 16 * lane);
-            bbuf[i] = *reinterpret_cast<const uint32_t*>(pk + kPacketBiasOff + 4 * lane);
+    for (int i = 0; i < PF; ++i) {
+        const uint32_t off = i < np ? blk + static_cast<uint32_t>(p0 + i) * kPacketBytes : kOutOfRange;
+        cbuf[i] = ld128(rw, off + 16 * lane);
+        abuf[i] = ld128(rw, off + kPacketAffineOff + 16 * lane);
+        bbuf[i] = ld32(rw, off + kPacketBiasOff + 4 * lane);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // 3. Stage this wavefront's activations in operand order, with the
+    //    per-(token, group, component) sums.  Only this wavefront reads them,
+    //    so no workgroup barrier is needed -- LDS accesses of one wavefront
+    //    complete in order.
+#pragma unroll
+    for (int i = 0; i < NX; ++i) {
+        const int c = 64 * i + lane;
+        if (c < chunks_w) {
+            const int t = MT == 1 ? 0 : c / (16 * ngw);
+            const int lc = c - t * 16 * ngw;
+            stage_chunk<XT>(xr[i], t, gbeg + (lc >> 4), lc & 15, groups, xs, xbar);
         }
     }
-    const bool do_half = has_half && wave == WAVES - 1;
-    uint2 hc = {0u, 0u}, ha = {0u, 0u};
-    uint32_t hb = 0;
-    if (do_half) {
-        const uint8_t* pk = blk + static_cast<size_t>(nfull) * kPacketBytes;
-        hc = *reinterpret_cast<const uint2*>(pk + 8 * lane);
-        ha = *reinterpret_cast<const uint2*>(pk + kHalfAffineOff + 8 * lane);
-        hb = *reinterpret_cast<const uint16_t*>(pk + kHalfBiasOff + 2 * lane);
-    }
-
-    // 2. Stage activations in operand order and their per-(group, component) sums.
-    const int chunks_per_tok = K >> 3;
-    for (int c = threadIdx.x; c < M * chunks_per_tok; c += WAVES * 64) {
-        const int t = c / chunks_per_tok;
-        const int k0 = (c - t * chunks_per_tok) << 3;
-        const uint4 raw = *reinterpret_cast<const uint4*>(x + static_cast<size_t>(t) * K + k0);
-        const uint16_t* v16 = reinterpret_cast<const uint16_t*>(&raw);
-        const int g = k0 >> 7;
-        const int vbase = (k0 & 127) >> 2;
-        uint16_t* line = reinterpret_cast<uint16_t*>(xs) + (static_cast<size_t>(t) * groups + g) * 128;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int v = vbase + (e >> 2), a = e & 3;
-            line[a * 32 + operand_slot(v)] = v16[e];
+    for (int i = NX; i < nxi; ++i) {  // more than NX instructions: not overlapped with the packets
+        const int c = 64 * i + lane;
+        const uint4 raw = ld128(rx, c < chunks_w ? chunk_off(c) : kOutOfRange);
+        if (c < chunks_w) {
+            const int t = MT == 1 ? 0 : c / (16 * ngw);
+            const int lc = c - t * 16 * ngw;
+            stage_chunk<XT>(raw, t, gbeg + (lc >> 4), lc & 15, groups, xs, xbar);
         }
     }
-    __syncthreads();
-    for (int i = threadIdx.x; i < M * groups * 4; i += WAVES * 64) {
-        const XT* src = xs + static_cast<size_t>(i) * 32;
-        float s = 0.f;
-#pragma unroll
-        for (int v = 0; v < 32; ++v) s += static_cast<float>(src[v]);
-        xbar[i] = s;
-    }
-    __syncthreads();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-    // 3. Main loop over this wave's full packets, PF loads in flight.
+    // 4. Packets.  When the whole run fits the prefetch buffers (np <= PF) it is
+    //    consumed straight from them; otherwise each buffer slot is refilled PF
+    //    packets ahead right after it is consumed.
     float acc[MT];
 #pragma unroll
     for (int t = 0; t < MT; ++t) acc[t] = 0.f;
-    vec4 xop[8];
+    typename XOps<XT>::vec4 x0[8], x1[8];
 #pragma unroll
-    for (int s = 0; s < 8; ++s) xop[s] = vec4{};
-    const int xs_tok = groups * 128;  // elements per token in xs
-    const int xb_tok = groups * 4;
-    for (int i = 0; i < np; i += PF) {
+    for (int s = 0; s < 8; ++s) x0[s] = x1[s] = typename XOps<XT>::vec4{};
+    if (np <= PF) {
 #pragma unroll
-        for (int j = 0; j < PF; ++j) {
-            if (i + j < np) {
-                const uint4 c = cbuf[j], a = abuf[j];
-                const uint32_t bw = bbuf[j];
-                const int nxt = min(i + j + PF, np - 1);
-                const uint8_t* pk = blk + static_cast<size_t>(p0 + nxt) * kPacketBytes;
-                cbuf[j] = *reinterpret_cast<const uint4*>(pk + 16 * lane);
-                abuf[j] = *reinterpret_cast<const uint4*>(pk + kPacketAffineOff + 16 * lane);
-                bbuf[j] = *reinterpret_cast<const uint32_t*>(pk + kPacketBiasOff + 4 * lane);
-                const int g = 2 * (p0 + i + j);
-                group_step<XT, MT>(c.x, c.y, a.x, a.y, bw & 0xffffu, xs + g * 128, xbar + g * 4,
-                                   xs_tok, xb_tok, M, lane, xop, acc);
-                group_step<XT, MT>(c.z, c.w, a.z, a.w, bw >> 16, xs + (g + 1) * 128,
-                                   xbar + (g + 1) * 4, xs_tok, xb_tok, M, lane, xop, acc);
+        for (int j = 0; j < PF; ++j)
+            if (j < np)
+                packet_step<XT, MT>(cbuf[j], abuf[j], bbuf[j], 2 * (p0 + j), xs, xbar, groups, M, lane, acc,
+                                    x0, x1);
+    } else {
+        for (int i = 0; i < np; i += PF) {
+#pragma unroll
+            for (int j = 0; j < PF; ++j) {
+                if (i + j < np)
+                    packet_step<XT, MT>(cbuf[j], abuf[j], bbuf[j], 2 * (p0 + i + j), xs, xbar, groups, M,
+                                        lane, acc, x0, x1);
+                const int nxt = i + j + PF;
+                const uint32_t off =
+                    nxt < np ? blk + static_cast<uint32_t>(p0 + nxt) * kPacketBytes : kOutOfRange;
+                cbuf[j] = ld128(rw, off + 16 * lane);
+                abuf[j] = ld128(rw, off + kPacketAffineOff + 16 * lane);
+                bbuf[j] = ld32(rw, off + kPacketBiasOff + 4 * lane);
             }
         }
     }
+    // The trailing half packet (odd group count) of the last wavefront: loaded
+    // and used here, outside the pipelined part.
     if (do_half) {
-        const int g = groups - 1;
-        group_step<XT, MT>(hc.x, hc.y, ha.x, ha.y, hb, xs + g * 128, xbar + g * 4, xs_tok, xb_tok, M,
-                           lane, xop, acc);
+        const uint32_t hoff = blk + static_cast<uint32_t>(nfull) * kPacketBytes;
+        const uint2 hc = ld64(rw, hoff + 8 * lane);
+        const uint2 ha = ld64(rw, hoff + kHalfAffineOff + 8 * lane);
+        const uint32_t hb = ld16(rw, hoff + kHalfBiasOff + 2 * lane);
+        half_step<XT, MT>(hc, ha, hb, groups - 1, xs, xbar, groups, M, lane, acc, x0);
     }
 
-    // 4. Sum the four component lanes of each row, then the waves.
+    // 5. Sum the four component lanes of each row, then the wavefronts.
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
-        float v = acc[t];
-        v += __shfl_xor(v, 1);
-        v += __shfl_xor(v, 2);
+        const float v = quad_sum(acc[t]);
         if ((lane & 3) == 0) red[(wave * MT + t) * 16 + (lane >> 2)] = v;
     }
     __syncthreads();
@@ -246,68 +404,112 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(const uint8_t* __restr
         float s = 0.f;
 #pragma unroll
         for (int w = 0; w < WAVES; ++w) s += red[(w * MT + t) * 16 + r];
-        store_out(y, static_cast<int64_t>(t) * N + static_cast<int64_t>(rb) * kRowBlock + r, s, y_dtype);
+        store_out(y, static_cast<int64_t>(t) * N + static_cast<int64_t>(rb) * kRowBlock + r, s,
+                  batch.y_dtype);
     }
 }
 
-template <typename XT, int WAVES, int MT>
-size_t gemv_lds_bytes(int K, int M) {
-    const size_t groups = K / kGroup;
-    return static_cast<size_t>(M) * groups * (256 + 16) + static_cast<size_t>(WAVES) * MT * 16 * 4;
-}
-
-constexpr int kPrefetch = 4;
 constexpr size_t kMaxLds = 160 * 1024;
 
-template <typename XT, int WAVES, int MT>
-int launch_cfg(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x, void* y,
-               int y_dtype, hipStream_t s) {
-    const size_t lds = gemv_lds_bytes<XT, WAVES, MT>(static_cast<int>(K), static_cast<int>(M));
+size_t gemv_lds_bytes(int K, int M, int waves, int mt) {
+    const size_t groups = K / kGroup;
+    return static_cast<size_t>(M) * groups * (256 + 16) + static_cast<size_t>(waves) * mt * 16 * 4;
+}
+
+template <typename XT, int WAVES, int MT, int PF, int NX>
+int launch_cfg(const GemvBatch& b, int blocks, int maxK, hipStream_t s) {
+    const size_t lds = gemv_lds_bytes(maxK, b.M, WAVES, MT);
     if (lds > kMaxLds) return UNISVQ_EUNSUP;
     // Raising the dynamic-LDS limit is idempotent; do it once per instantiation.
     static std::atomic<int> attr_done{0};
     if (!attr_done.load(std::memory_order_acquire)) {
-        if (hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_kernel<XT, WAVES, MT, kPrefetch>),
+        if (hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_kernel<XT, WAVES, MT, PF, NX, 1>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize,
                                 static_cast<int>(kMaxLds)) != hipSuccess)
             return UNISVQ_EHIP;
         attr_done.store(1, std::memory_order_release);
     }
-    hipLaunchKernelGGL((gemv_kernel<XT, WAVES, MT, kPrefetch>), dim3(static_cast<unsigned>(N / kRowBlock)), dim3(WAVES * 64), lds, s,
-                       packed, static_cast<const XT*>(x), y, static_cast<int>(N), static_cast<int>(K),
-                       static_cast<int>(M), y_dtype);
+    hipLaunchKernelGGL((gemv_kernel<XT, WAVES, MT, PF, NX, 1>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(WAVES * 64), lds, s, b);
     return hipGetLastError() == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
 }
 
+// Launch geometry for a batch: WAVES wavefronts per 16-row block, PF packets
+// in flight per wavefront, NX activation loads per wavefront issued up front.
+struct GemvPlan {
+    int waves, pf, nx;
+};
+
+GemvPlan plan_gemv(int64_t blocks, int max_groups, int M) {
+    const int packets = max_groups / 2;
+    // Short K: few wavefronts, whole run prefetched.  Long K: more wavefronts
+    // so that every wavefront keeps several packets in flight.
+    GemvPlan p;
+    p.waves = packets <= 16 ? 4 : (packets <= 48 ? 8 : 16);
+    if (M > 1 && p.waves > 8) p.waves = 8;  // register budget of 1024-thread groups
+    while (p.waves > 4 && blocks * p.waves > 16384) p.waves /= 2;
+    const int per = (packets + p.waves - 1) / p.waves;
+    p.pf = per <= 2 ? 2 : 4;
+    const int chunks = M * 16 * (2 * per + (max_groups & 1));
+    const int nxi = (chunks + 63) / 64;
+    p.nx = nxi <= 1 ? 1 : (nxi <= 2 ? 2 : 4);
+    return p;
+}
+
+template <typename XT, int WAVES, int MT, int PF>
+int launch_nx(const GemvBatch& b, int blocks, int maxK, int nx, hipStream_t s) {
+    if (nx == 1) return launch_cfg<XT, WAVES, MT, PF, 1>(b, blocks, maxK, s);
+    if (nx == 2) return launch_cfg<XT, WAVES, MT, PF, 2>(b, blocks, maxK, s);
+    return launch_cfg<XT, WAVES, MT, PF, 4>(b, blocks, maxK, s);
+}
+
+template <typename XT, int WAVES, int MT>
+int launch_pf(const GemvBatch& b, int blocks, int maxK, const GemvPlan& p, hipStream_t s) {
+    if (p.pf == 2) return launch_nx<XT, WAVES, MT, 2>(b, blocks, maxK, p.nx, s);
+    return launch_nx<XT, WAVES, MT, 4>(b, blocks, maxK, p.nx, s);
+}
+
 template <typename XT, int MT>
-int launch_waves(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x, void* y,
-                 int y_dtype, hipStream_t s) {
-    // Enough wavefronts to cover 256 CUs several times over, while keeping
-    // at least two packets per wavefront.
-    const int64_t blocks = N / kRowBlock;
-    const int64_t packets = (K / kGroup) / 2;
-    int waves = 4;
-    while (waves < 16 && blocks * waves < 2048 && packets >= 2 * (waves * 2)) waves *= 2;
-    if (waves == 4) return launch_cfg<XT, 4, MT>(N, K, packed, M, x, y, y_dtype, s);
-    if (waves == 8) return launch_cfg<XT, 8, MT>(N, K, packed, M, x, y, y_dtype, s);
-    return launch_cfg<XT, 16, MT>(N, K, packed, M, x, y, y_dtype, s);
+int launch_waves(const GemvBatch& b, int blocks, int maxK, hipStream_t s) {
+    const GemvPlan p = plan_gemv(blocks, maxK / kGroup, b.M);
+    if (p.waves == 4) return launch_pf<XT, 4, MT>(b, blocks, maxK, p, s);
+    if (MT == 1 && p.waves == 16) return launch_pf<XT, 16, 1>(b, blocks, maxK, p, s);
+    return launch_pf<XT, 8, MT>(b, blocks, maxK, p, s);
 }
 
 template <typename XT>
-int launch_tokens(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x, void* y,
-                  int y_dtype, hipStream_t s) {
-    if (M == 1) return launch_waves<XT, 1>(N, K, packed, M, x, y, y_dtype, s);
-    if (M == 2) return launch_waves<XT, 2>(N, K, packed, M, x, y, y_dtype, s);
-    return launch_waves<XT, 4>(N, K, packed, M, x, y, y_dtype, s);
+int launch_tokens(const GemvBatch& b, int blocks, int maxK, hipStream_t s) {
+    if (b.M == 1) return launch_waves<XT, 1>(b, blocks, maxK, s);
+    if (b.M == 2) return launch_waves<XT, 2>(b, blocks, maxK, s);
+    return launch_waves<XT, 4>(b, blocks, maxK, s);
 }
 
 }  // namespace
 
+int launch_gemv_batch(const GemvProblem* probs, int count, int64_t M, int x_dtype, int y_dtype,
+                      hipStream_t s) {
+    if (M > 4 || count < 1 || count > kMaxBatch) return UNISVQ_EUNSUP;
+    GemvBatch b{};
+    int blocks = 0, maxK = 0, minK = 1 << 30;
+    for (int i = 0; i < count; ++i) {
+        b.p[i] = probs[i];
+        b.p[i].rb_begin = blocks;
+        blocks += probs[i].N / kRowBlock;
+        maxK = probs[i].K > maxK ? probs[i].K : maxK;
+        minK = probs[i].K < minK ? probs[i].K : minK;
+    }
+    b.count = count;
+    b.M = static_cast<int>(M);
+    b.y_dtype = y_dtype;
+    (void)minK;
+    if (x_dtype == UNISVQ_F16) return launch_tokens<_Float16>(b, blocks, maxK, s);
+    return launch_tokens<__bf16>(b, blocks, maxK, s);
+}
+
 int launch_gemv(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x, int x_dtype,
                 void* y, int y_dtype, hipStream_t s) {
-    if (M > 4) return UNISVQ_EUNSUP;
-    if (x_dtype == UNISVQ_F16) return launch_tokens<_Float16>(N, K, packed, M, x, y, y_dtype, s);
-    return launch_tokens<__bf16>(N, K, packed, M, x, y, y_dtype, s);
+    GemvProblem p{packed, x, y, static_cast<int>(N), static_cast<int>(K), 0};
+    return launch_gemv_batch(&p, 1, M, x_dtype, y_dtype, s);
 }
 
 }  // namespace unisvq

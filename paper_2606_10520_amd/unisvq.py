@@ -21,7 +21,15 @@ STATUS = {0: "UNISVQ_OK", -1: "UNISVQ_EINVAL", -2: "UNISVQ_ESHAPE", -3: "UNISVQ_
           -4: "UNISVQ_EALIGN", -5: "UNISVQ_EHIP", -6: "UNISVQ_EWORKSPACE"}
 
 EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "unisvq_pack",
-           "unisvq_unpack", "unisvq_gemv", "unisvq_gemm_workspace_bytes", "unisvq_gemm")
+           "unisvq_unpack", "unisvq_gemv", "unisvq_gemv_batched", "unisvq_gemm_workspace_bytes",
+           "unisvq_gemm")
+MAX_BATCH = 8
+
+
+class GemvProblem(ctypes.Structure):
+    """Mirror of unisvq_gemv_problem."""
+    _fields_ = [("N", ctypes.c_int64), ("K", ctypes.c_int64), ("packed", ctypes.c_void_p),
+                ("x", ctypes.c_void_p), ("y", ctypes.c_void_p)]
 
 
 class UniSVQLibraryMissing(RuntimeError):
@@ -59,6 +67,8 @@ def load():
     lib.unisvq_unpack.restype = i32
     lib.unisvq_gemv.argtypes = [i64, i64, p, i64, p, i32, p, i32, p]
     lib.unisvq_gemv.restype = i32
+    lib.unisvq_gemv_batched.argtypes = [ctypes.POINTER(GemvProblem), i32, i64, i32, i32, p]
+    lib.unisvq_gemv_batched.restype = i32
     lib.unisvq_gemm_workspace_bytes.argtypes = [i64, i64, i64]
     lib.unisvq_gemm_workspace_bytes.restype = sz
     lib.unisvq_gemm.argtypes = [i64, i64, p, i64, p, i32, p, i32, p, sz, p]
@@ -160,6 +170,37 @@ def _product(fn_name, N, K, packed, x, out, out_dtype, stream, extra=()):
 def gemv(packed, N: int, K: int, x, out=None, out_dtype=None, stream=None):
     """y[M][N] = x[M][K] . W_hat^T for 1 <= M <= 4 (decode-phase kernel)."""
     return _product("unisvq_gemv", N, K, packed, x, out, out_dtype, stream)
+
+
+def gemv_batched(problems, out_dtype=None, stream=None):
+    """Several independent decode products in one launch.
+
+    problems: sequence of (packed, N, K, x, out-or-None); all x share M and dtype.
+    Returns the list of outputs."""
+    torch = _torch()
+    if not 1 <= len(problems) <= MAX_BATCH:
+        raise ValueError(f"1..{MAX_BATCH} problems per call")
+    arr = (GemvProblem * len(problems))()
+    outs, M, xdt = [], None, None
+    for i, (packed, N, K, x, out) in enumerate(problems):
+        _need_cuda(packed, x, out)
+        x2 = x if x.dim() == 2 else x.reshape(-1, K)
+        if not x2.is_contiguous():
+            raise ValueError("x must be contiguous")
+        if M is None:
+            M, xdt = x2.shape[0], x2.dtype
+        if x2.shape[0] != M or x2.dtype != xdt:
+            raise ValueError("all problems need the same token count and activation dtype")
+        if out is None:
+            out = torch.empty((M, N), dtype=out_dtype or xdt, device=x.device)
+        outs.append(out)
+        arr[i] = GemvProblem(N, K, packed.data_ptr(), x2.data_ptr(), out.data_ptr())
+    ydt = {o.dtype for o in outs}
+    if len(ydt) != 1:
+        raise ValueError("all outputs need the same dtype")
+    _check("unisvq_gemv_batched", load().unisvq_gemv_batched(arr, len(problems), M, _dtype_code(xdt),
+                                                             _dtype_code(outs[0].dtype), _stream(stream)))
+    return outs
 
 
 def gemm_workspace_bytes(N: int, K: int, M: int) -> int:

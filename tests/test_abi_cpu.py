@@ -95,6 +95,29 @@ def test_product_validation(fn):
         assert lib.unisvq_gemv(64, 256, GOOD, 5, GOOD, u.F16, GOOD, u.F16, None) == EUNSUP
 
 
+def test_batched_validation():
+    lib = u.load()
+    P = u.GemvProblem
+
+    def arr(*ps):
+        a = (P * len(ps))()
+        for i, q in enumerate(ps):
+            a[i] = q
+        return a
+
+    good = P(64, 256, GOOD, GOOD, GOOD)
+    assert lib.unisvq_gemv_batched(None, 1, 1, u.F16, u.F16, None) == EINVAL
+    assert lib.unisvq_gemv_batched(arr(good), 0, 1, u.F16, u.F16, None) == EINVAL
+    assert lib.unisvq_gemv_batched(arr(*[good] * 9), 9, 1, u.F16, u.F16, None) == EUNSUP
+    # any bad descriptor fails the whole call before launch
+    assert lib.unisvq_gemv_batched(arr(good, P(64, 256, None, GOOD, GOOD)), 2, 1, u.F16, u.F16, None) == EINVAL
+    assert lib.unisvq_gemv_batched(arr(good, P(40, 256, GOOD, GOOD, GOOD)), 2, 1, u.F16, u.F16, None) == ESHAPE
+    assert lib.unisvq_gemv_batched(arr(P(64, 256, GOOD + 4, GOOD, GOOD), good), 2, 1, u.F16, u.F16, None) == EALIGN
+    assert lib.unisvq_gemv_batched(arr(good, good), 2, 0, u.F16, u.F16, None) == EINVAL
+    assert lib.unisvq_gemv_batched(arr(good, good), 2, 5, u.F16, u.F16, None) == EUNSUP
+    assert lib.unisvq_gemv_batched(arr(good), 1, 1, u.F32, u.F16, None) == EINVAL
+
+
 def test_gemm_workspace_is_zero():
     assert u.load().unisvq_gemm_workspace_bytes(4096, 4096, 2048) == 0
 

@@ -253,9 +253,61 @@ def test_repeatable_and_linear_in_x():
     assert torch.equal(y3, 2 * y1)      # scaling x by 2 is exact end to end
 
 
+@pytest.mark.parametrize("M", [1, 3])
+def test_gemv_batched_matches_single_calls(M):
+    """q/k/v-style and gate/up-style batches (shared activations, different
+    shapes and K), plus mixed K in one launch."""
+    shapes = [(4096, 4096), (1024, 4096), (1024, 4096), (11008, 4096), (4096, 11008), (16, 384)]
+    probs, refs = [], []
+    for i, (N, K) in enumerate(shapes):
+        Q, A, B = wl.gen_weights(N, K, seed=30 + i)
+        xb = wl.gen_activations(M, K, seed=40 + i)
+        pk = upload_pack(Q, A, B)
+        probs.append((pk, N, K, dev_x(xb, "f16"), None))
+        rows = None if N <= 1024 else np.arange(0, N, 37)
+        refs.append((rows, oracle.matmul(oracle.pack(Q, A, B)[0], N, K, x_as_f64(xb, "f16"), rows=rows)))
+    outs = u.gemv_batched(probs, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    for (pk, N, K, x, _), y, (rows, ref) in zip(probs, outs, refs):
+        # the batched launch may split K differently (it sees more workgroups),
+        # so the fp32 summation order -- not the result's accuracy -- can differ
+        single = u.gemv(pk, N, K, x, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        for out in (y, single):
+            got = out.cpu().numpy() if rows is None else out.cpu().numpy()[:, rows]
+            assert rel_err(got, ref) <= 1e-5
+
+
 def test_gemv_rejects_more_than_four_tokens():
     pk = torch.zeros(u.packed_bytes(64, 256), dtype=torch.uint8, device=DEV)
     x = torch.zeros((5, 256), dtype=torch.float16, device=DEV)
     with pytest.raises(u.UniSVQError) as e:
         u.gemv(pk, 64, 256, x)
     assert e.value.status == -3
+
+
+def test_graph_replays_match_eager():
+    """The launches are capturable in a HIP graph (no allocation, no memset,
+    no synchronisation inside); every replay reproduces the eager result."""
+    N, K = 512, 4096
+    Q, A, B = wl.gen_weights(N, K, seed=12)
+    pk = upload_pack(Q, A, B)
+    x1 = dev_x(wl.gen_activations(1, K, seed=1), "f16")
+    x64 = dev_x(wl.gen_activations(64, K, seed=2), "f16")
+    y1 = torch.empty((1, N), dtype=torch.float16, device=DEV)
+    y64 = torch.empty((64, N), dtype=torch.float32, device=DEV)
+    e1 = u.gemv(pk, N, K, x1).clone()
+    e64 = u.gemm(pk, N, K, x64, out_dtype=torch.float32).clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        u.gemv(pk, N, K, x1, out=y1)
+        u.gemm(pk, N, K, x64, out=y64)
+    for rep in range(4):
+        y1.fill_(7.0); y64.fill_(7.0)           # eager work between replays
+        junk = u.gemv(pk, N, K, x1 * 2)         # and an eager launch of the same kernel
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y1, e1), rep
+        assert torch.equal(y64, e64), rep
+        assert torch.equal(junk, u.gemv(pk, N, K, x1 * 2))
