@@ -51,11 +51,45 @@ def parse():
                    help="decoder: q/k/v in one batched launch, o, gate/up in one batched launch, down "
                         "(how a decode step runs them); per_layer: one launch per linear; single: all "
                         "linears in one batched launch")
+    p.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                   help="only run a plain device-to-device copy of BYTES bytes 10 times (counter calibration)")
+    p.add_argument("--no-schedules", action="store_true",
+                   help="time only the --schedule launch sequence (for profiling runs)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU work of the oracle sample")
     p.add_argument("--no-launch-events", action="store_true",
                    help="skip the per-launch event pass (roofline fields become null)")
     return p.parse_args()
+
+
+def kernel_source_hash(kernel: str) -> str:
+    import hashlib
+    src = os.path.join(ROOT, "paper_2606_10520_amd", "csrc", f"{kernel}.hip")
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str, schedule: str):
+    """HBM bytes per launch from the committed counter summary, if it was taken
+    on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_{schedule}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    d = json.load(open(path))
+    if d.get("source_sha256_16") != kernel_source_hash(kernel):
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def calibrate_copy(nbytes: int):
+    import torch
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(10):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes": nbytes, "launches": 10}), flush=True)
 
 
 def workload_spec(name: str):
@@ -78,6 +112,9 @@ def workload_spec(name: str):
 
 def main():
     args = parse()
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
               "this build has no multi-GPU path.", file=sys.stderr)
@@ -121,28 +158,33 @@ def main():
     lib = u.load()
     xcode = u.F16 if xdt == "f16" else u.BF16
     names = [L.name for L in layers]
-    sched = args.schedule if kernel == "gemv" else "per_layer"
-    if sched == "decoder" and {"q", "k", "v", "o", "gate", "up", "down"} <= set(names):
-        groups_ = [["q", "k", "v"], ["o"], ["gate", "up"], ["down"]]
-    elif sched == "single":
-        groups_ = [names]
-    else:
-        sched = "per_layer"
-        groups_ = [[n] for n in names]
-    calls = []  # per copy: list of (label, ctypes problem array or single tuple)
-    for s_ in sets:
-        by = {L.name: (L, pk, x, y) for (L, pk, x, y) in s_}
-        cc = []
-        for grp in groups_:
-            if len(grp) == 1 or kernel != "gemv":
-                cc.append(("+".join(grp), by[grp[0]]))
-            else:
-                arr = (u.GemvProblem * len(grp))()
-                for i, n in enumerate(grp):
-                    L, pk, x, y = by[n]
-                    arr[i] = u.GemvProblem(L.N, L.K, pk.data_ptr(), x.data_ptr(), y.data_ptr())
-                cc.append(("+".join(grp), arr))
-        calls.append(cc)
+    full_set = {"q", "k", "v", "o", "gate", "up", "down"} <= set(names)
+
+    def schedule_groups(sched):
+        if kernel != "gemv":
+            return "per_layer", [[n] for n in names]
+        if sched == "decoder" and full_set:
+            return "decoder", [["q", "k", "v"], ["o"], ["gate", "up"], ["down"]]
+        if sched == "single" and len(names) <= u.MAX_BATCH:
+            return "single", [names]
+        return "per_layer", [[n] for n in names]
+
+    def build_calls(groups_):
+        calls = []  # per buffer copy: list of (label, single-problem tuple or ctypes problem array)
+        for s_ in sets:
+            by = {L.name: (L, pk, x, y) for (L, pk, x, y) in s_}
+            cc = []
+            for grp in groups_:
+                if len(grp) == 1:
+                    cc.append(("+".join(grp), by[grp[0]]))
+                else:
+                    arr = (u.GemvProblem * len(grp))()
+                    for i, n in enumerate(grp):
+                        L, pk, x, y = by[n]
+                        arr[i] = u.GemvProblem(L.N, L.K, pk.data_ptr(), x.data_ptr(), y.data_ptr())
+                    cc.append(("+".join(grp), arr))
+            calls.append(cc)
+        return calls
 
     def launch(item, sptr):
         if isinstance(item, tuple):
@@ -153,46 +195,59 @@ def main():
                                    None, 0, sptr)
         return lib.unisvq_gemv_batched(item, len(item), M, xcode, u.F16, sptr)
 
-    def run_step(i, sptr):
+    def run_step(calls, i, sptr):
         for _, item in calls[i % copies]:
             st = launch(item, sptr)
             if st != 0:
                 raise RuntimeError(f"{kernel} failed with status {st}")
 
     stream = torch.cuda.current_stream()
-    for i in range(args.warmup):
-        run_step(i, stream.cuda_stream)
-    torch.cuda.synchronize()
 
-    # ---- the step sequence for all buffer copies, captured once in a HIP graph
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        cap = torch.cuda.current_stream().cuda_stream
-        for c in range(copies):
-            run_step(c, cap)
-    torch.cuda.synchronize()
-    graph.replay()  # one untimed replay
-    torch.cuda.synchronize()
+    def time_schedule(calls):
+        """Warm up, capture the steps of all buffer copies in one HIP graph, and
+        time ceil(steps / copies) replays between two events."""
+        for i in range(args.warmup):
+            run_step(calls, i, stream.cuda_stream)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            cap = torch.cuda.current_stream().cuda_stream
+            for c in range(copies):
+                run_step(calls, c, cap)
+        torch.cuda.synchronize()
+        graph.replay()  # one untimed replay
+        torch.cuda.synchronize()
+        replays = max(1, -(-args.steps // copies))
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(replays):
+            graph.replay()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / (replays * copies), replays * copies
 
-    # ---- timed region: K steps = ceil(K / copies) graph replays
-    replays = max(1, -(-args.steps // copies))
-    steps_done = replays * copies
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0.record(stream)
-    for _ in range(replays):
-        graph.replay()
-    t1.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = t0.elapsed_time(t1) / steps_done
+    sched, groups_ = schedule_groups(args.schedule)
+    calls = build_calls(groups_)
+    ms_per_step, steps_done = time_schedule(calls)
     value_gbs = set_bytes / (ms_per_step * 1e-3) / 1e9
 
-    # ---- per-launch durations: HIP events on the launch stream around each
+    # the other launch schedules of the same step, for context
+    schedules = {}
+    if kernel == "gemv" and not args.no_schedules:
+        for other in ("per_layer", "decoder", "single"):
+            oname, ogroups = schedule_groups(other)
+            if oname != other:
+                continue
+            oms = ms_per_step if oname == sched else time_schedule(build_calls(ogroups))[0]
+            schedules[oname] = {"launches_per_step": len(ogroups), "ms_per_step": round(oms, 5),
+                                "GB_per_s": round(set_bytes / (oms * 1e-3) / 1e9, 1)}
+
+    # ---- per-launch breakdown: HIP events on the launch stream around each
     # launch.  A spin kernel first lets the host queue a chunk of launches ahead
-    # of the GPU, so an interval brackets GPU work rather than host latency.
+    # of the GPU, so an interval brackets GPU work rather than host latency;
+    # each interval still includes one dispatch and two marker packets.
     per_layer_us = {}
-    roofline = None
     if not args.no_launch_events:
         ev = []
         chunk = 8
@@ -212,23 +267,29 @@ def main():
         for name, a, b in ev:
             durs.setdefault(name, []).append(a.elapsed_time(b) * 1e3)
         per_layer_us = {k: float(np.mean(v)) for k, v in durs.items()}
-        launches = len(ev)
-        total_us = sum(sum(v) for v in durs.values())
-        n_steps_ev = launches // len(groups_)
-        bytes_per_launch = set_bytes * n_steps_ev / launches
-        avg_us = total_us / launches
-        if kernel == "gemv":
-            ach = bytes_per_launch / (avg_us * 1e-6) / 1e9
-            roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                        "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
-                        "kernel": "gemv_kernel", "avg_launch_us": round(avg_us, 3),
-                        "bytes_per_launch": int(bytes_per_launch)}
-        else:
-            flops = sum(2 * M * L.N * L.K for L in layers) * n_steps_ev / launches
-            ach = flops / (avg_us * 1e-6) / 1e12
-            roofline = {"bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS,
-                        "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None,
-                        "kernel": "gemm_kernel", "avg_launch_us": round(avg_us, 3)}
+
+    # The roofline's launch duration comes from the timed region itself: the
+    # graph-timed step divided by its launches (events around single launches
+    # would add two marker packets and a dispatch to every interval).
+    launches_per_step = len(groups_)
+    avg_us = ms_per_step * 1e3 / launches_per_step
+    bytes_per_launch = set_bytes / launches_per_step
+    if kernel == "gemv":
+        ach = bytes_per_launch / (avg_us * 1e-6) / 1e9
+        traffic = measured_traffic("gemv", args.workload, sched)
+        roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": round(ach / PEAK_HBM_GBS, 4),
+                    "traffic": None if traffic is None else int(traffic),
+                    "kernel": "gemv_kernel", "avg_launch_us": round(avg_us, 3),
+                    "bytes_per_launch": int(bytes_per_launch)}
+    else:
+        flops = sum(2 * M * L.N * L.K for L in layers) / launches_per_step
+        ach = flops / (avg_us * 1e-6) / 1e12
+        traffic = measured_traffic("gemm", args.workload, sched)
+        roofline = {"bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                    "traffic": None if traffic is None else int(traffic),
+                    "kernel": "gemm_kernel", "avg_launch_us": round(avg_us, 3)}
 
     # ---- CPU baseline: the fp64 oracle on the host cores, bounded sample
     cpu = None
@@ -279,7 +340,8 @@ def main():
                    "launches_per_step": len(groups_), "buffer_copies": copies,
                    "set_bytes": set_bytes},
         "pct_peak_hbm": round(100 * value_gbs / PEAK_HBM_GBS, 2) if kernel == "gemv" else None,
-        "us_per_launch": {k: round(v, 3) for k, v in per_layer_us.items()},
+        "event_us_per_launch": {k: round(v, 3) for k, v in per_layer_us.items()},
+        "schedules": schedules,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
