@@ -149,14 +149,25 @@ typedef struct {
 int unisvq_gemv_batched(const unisvq_gemv_problem* problems, int count, int64_t M, int x_dtype,
                         int y_dtype, void* stream);
 
-/* Workspace the GEMM needs for this problem (currently always 0). */
+/* Workspace unisvq_gemm needs for bf16 activations: an fp16 copy of x
+ * (M*K*2 bytes rounded up to 256) plus one fp32 scale per token.  fp16
+ * activations need none.  0 for an invalid shape or M < 1. */
 size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M);
 
 /* Prefill product y = x * W_hat^T for any M >= 1 (Eq. 1 with Eq. 4/8).
  * Arguments as unisvq_gemv; x_dtype F16 or BF16, y_dtype F16, BF16 or F32.
- * Decodes weight tiles into LDS (each vector A q + B in fp32, rounded once to
- * the activation dtype) and multiplies them on the matrix cores with fp32
- * accumulation.  workspace may be NULL when the required size is 0. */
+ * Each workgroup decodes a 128-row x 128-column weight tile at a time into
+ * LDS (every vector A q + B in fp32 from the exact integer codes, rounded
+ * once to fp16) and multiplies it with its tokens on the matrix cores
+ * (fp16 x fp16, fp32 accumulation); decoded weights never reach global
+ * memory.  bf16 activations are first scaled per token by a power of two
+ * into [2^14, 2^15) and stored as fp16 in the workspace -- exact for every
+ * element within 2^28 of its token's largest magnitude -- and the scale is
+ * undone on the fp32 result.
+ *   workspace  device, >= unisvq_gemm_workspace_bytes(N, K, M) bytes,
+ *              16-byte aligned, for BF16 activations (UNISVQ_EWORKSPACE if
+ *              missing or smaller, UNISVQ_EALIGN if misaligned); ignored (may
+ *              be NULL) for F16.  Overwritten; the caller owns it. */
 int unisvq_gemm(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype,
                 void* y, int y_dtype, void* workspace, size_t workspace_bytes, void* stream);
 

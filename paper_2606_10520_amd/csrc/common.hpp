@@ -44,6 +44,9 @@ __device__ inline uint32_t ld16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
 
 // Largest buffer a 32-bit buffer offset addresses.
 constexpr int64_t kMaxBufferBytes = (int64_t{1} << 31) - 1;
+// A buffer offset past the end of every buffer the kernels address (all are
+// below 2^31 bytes): such a load returns zeros.
+constexpr uint32_t kOutOfRange = 0x80000000u;
 
 // Packed format v1 geometry (see the format block in unisvq.h).
 constexpr int kGroup = 128;            // input columns per (A, B) set
@@ -77,8 +80,12 @@ int launch_gemv_batch(const GemvProblem* probs, int count, int64_t M, int x_dtyp
                       hipStream_t s);
 int launch_gemv(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x,
                 int x_dtype, void* y, int y_dtype, hipStream_t s);
+// Prefill path.  bf16 activations need gemm_workspace_bytes(K, M) bytes of
+// 16-byte-aligned device workspace (fp16 copy of x plus one scale per token);
+// fp16 activations need none.
+size_t gemm_workspace_bytes(int64_t K, int64_t M);
 int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x,
-                int x_dtype, void* y, int y_dtype, hipStream_t s);
+                int x_dtype, void* y, int y_dtype, void* workspace, hipStream_t s);
 
 // Output store in the requested dtype (fp32 -> fp16 / bf16 round to nearest even).
 __device__ inline void store_out(void* y, int64_t idx, float v, int y_dtype) {

@@ -132,9 +132,6 @@ struct GemvBatch {
 
 namespace {
 
-// A buffer offset past the end of every buffer the kernels address: the load
-// returns zeros and generates no memory traffic.
-constexpr uint32_t kOutOfRange = 0x80000000u;
 
 // One 16-byte activation chunk: vectors 2*q16 and 2*q16+1 of group g, token t.
 template <typename XT>

@@ -204,13 +204,14 @@ def gemv_batched(problems, out_dtype=None, stream=None):
 
 
 def gemm_workspace_bytes(N: int, K: int, M: int) -> int:
+    """Workspace unisvq_gemm needs for bf16 activations (fp16 needs none)."""
     return load().unisvq_gemm_workspace_bytes(N, K, M)
 
 
 def gemm(packed, N: int, K: int, x, out=None, out_dtype=None, workspace=None, stream=None):
     """y[M][N] = x[M][K] . W_hat^T for any M (prefill kernel)."""
     M = x.numel() // K
-    need = gemm_workspace_bytes(N, K, M)
+    need = gemm_workspace_bytes(N, K, M) if x.dtype == _torch().bfloat16 else 0
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     if need and workspace is None:
         workspace = _torch().empty(need, dtype=_torch().uint8, device=x.device)

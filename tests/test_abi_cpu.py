@@ -118,8 +118,18 @@ def test_batched_validation():
     assert lib.unisvq_gemv_batched(arr(good), 1, 1, u.F32, u.F16, None) == EINVAL
 
 
-def test_gemm_workspace_is_zero():
-    assert u.load().unisvq_gemm_workspace_bytes(4096, 4096, 2048) == 0
+def test_gemm_workspace():
+    lib = u.load()
+    # fp16 copy of the activations (rounded up to 256 bytes) plus one fp32 scale per token
+    assert lib.unisvq_gemm_workspace_bytes(4096, 4096, 2048) == 2048 * 4096 * 2 + 2048 * 4
+    assert lib.unisvq_gemm_workspace_bytes(16, 128, 1) == 256 + 4
+    assert lib.unisvq_gemm_workspace_bytes(15, 128, 1) == 0
+    assert lib.unisvq_gemm_workspace_bytes(16, 128, 0) == 0
+    # bf16 activations need it; fp16 activations do not
+    need = lib.unisvq_gemm_workspace_bytes(64, 256, 4)
+    assert lib.unisvq_gemm(64, 256, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, None, need, None) == EWS
+    assert lib.unisvq_gemm(64, 256, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, GOOD, need - 1, None) == EWS
+    assert lib.unisvq_gemm(64, 256, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, GOOD + 8, need, None) == EALIGN
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):

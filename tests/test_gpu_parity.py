@@ -156,8 +156,10 @@ def test_gemv_outlier_activations(M):
 def test_gemm_small_shapes_full_parity(N, K, M, dtype):
     y, pk, xb = run_product("gemm", N, K, M, dtype)
     ref = oracle.matmul(pk, N, K, x_as_f64(xb, dtype))
-    # fp16: the decoded weight is rounded once to fp16; bf16: carried as hi + lo
-    assert rel_err(y.cpu().numpy(), ref) <= (5e-4 if dtype == "f16" else 2e-5)
+    # The decoded weight is rounded once to fp16 (2^-11 relative); bf16
+    # activations are carried exactly in fp16 after a per-token power-of-two
+    # scale, so both activation types meet the same bar.
+    assert rel_err(y.cpu().numpy(), ref) <= 5e-4
 
 
 @pytest.mark.parametrize("layer", wl.PREFILL7B, ids=lambda l: l.name)
@@ -167,7 +169,31 @@ def test_gemm_prefill_m2048_sampled_rows(layer):
     rows = np.random.default_rng(1).choice(layer.N, 64, replace=False)
     rows[:2] = [0, layer.N - 1]
     ref = oracle.matmul(pk, layer.N, layer.K, x_as_f64(xb, "bf16"), rows=rows)
-    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 2e-5
+    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 5e-4
+
+
+def test_gemm_bf16_extreme_token_scales():
+    """bf16 activations far outside the fp16 range (and far below it) keep
+    full accuracy: each token row is rescaled by a power of two before the
+    fp16 product and scaled back after it.  Checked per token against that
+    token's own output magnitude."""
+    N, K, M = 64, 512, 6
+    Q, A, B = wl.gen_weights(N, K, seed=31)
+    xb = wl.gen_activations(M, K, seed=32, dtype="bf16")
+    x = x_as_f64(xb, "bf16")
+    for t, s in enumerate([1.0, 2.0 ** 40, 2.0 ** -40, 2.0 ** 100, 2.0 ** -100, 3.0e4]):
+        x[t] *= s
+    xb = wl.f64_to_bf16_bits(x)
+    x = x_as_f64(xb, "bf16")
+    pk_ref, _ = oracle.pack(Q, A, B)
+    pk = upload_pack(Q, A, B)
+    y = u.gemm(pk, N, K, dev_x(xb, "bf16"), out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = oracle.matmul(pk_ref, N, K, x)
+    yy = y.cpu().numpy().astype(np.float64)
+    for t in range(M):
+        assert np.isfinite(yy[t]).all(), t
+        assert rel_err(yy[t], ref[t]) <= 5e-4, t
 
 
 # --------------------------------------------------------------------- exactness
