@@ -4,9 +4,9 @@
 // BM tokens x 128 output rows and walks K one 128-column group (one affine
 // parameter set per row, Sec. 3.1) at a time:
 //   * the group's weights are decoded once per workgroup, w_hat = A q + B
-//     (Eq. 4, vectors along K as in Eq. 8), in fp32 (the fp16 parameters
-//     times the exact small-integer codes), rounded once to fp16 and written
-//     to LDS -- decoded weights never reach global memory;
+//     (Eq. 4, vectors along K as in Eq. 8), on the matrix cores in fp32 (the
+//     fp16 parameters times the exact small-integer codes), rounded once to
+//     fp16 and written to LDS -- decoded weights never reach global memory;
 //   * every wavefront owns 16*MI tokens and multiplies them with all 128
 //     decoded rows on v_mfma_f32_16x16x32_f16 (fp32 accumulation); its
 //     activation operands come straight from global memory in the matrix-
@@ -39,114 +39,179 @@ __device__ inline float h2f(uint32_t bits16) {
     return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(bits16)));
 }
 
-// The packet data one thread decodes for one group: row r of the tile,
-// vectors 16*hv .. 16*hv+15 of the group, all four components b.
+// ---------------------------------------------------------------------------
+// Weight decode on the matrix cores.  For one 16-row block and one group,
+// v_mfma_f32_4x4x4_16b computes, per row (one of the 16 blocks) and per
+// 4 consecutive vectors v = 4n .. 4n+3:
+//     D[a][v] = sum_b A[a][b] q[v][b] + B[a]          (Eq. 4)
+// with SrcA lane (row, i) = row i of A, SrcB lane (row, j) = the four codes
+// of vector 4n+j, C = B; the products of fp16 parameters and exact integer
+// codes are exact in fp32.  D lane (row, j) then holds the four weights of
+// vector 4n+j -- four consecutive columns -- which go to LDS as fp16 (one
+// rounding).  Eight instructions decode a 16 x 128 tile.
+
+// Packet data of one row block for lane (beta, j) = packet slot 4 beta + j:
+// exactly what the slot holds, so the loads are fully coalesced.  A full
+// packet covers two groups (jj = 0, 1); a trailing half packet one (jj = 0).
 struct Piece {
-    uint32_t code[4];  // F(r, g, b) bits 32*hv .. 32*hv+31: 16 codes of component b
-    uint2 acol[4];     // A[r][g][0..3][b]
-    uint4 bias;        // the B values of the row's four slots (layout depends on `half`)
-    bool half;         // group stored in a half packet
+    uint4 c;      // F(r, 2p + jj, j): .x/.y for jj = 0, .z/.w for jj = 1
+    uint4 a;      // A[r][2p + jj][0..3][j]: .x/.y for jj = 0, .z/.w for jj = 1
+    uint32_t b;   // B[r][2p + jj][j]: low half jj = 0, high half jj = 1
 };
 
-// g >= groups loads nothing (offsets past the end of the buffer).
-__device__ inline void load_piece(__amdgpu_buffer_rsrc_t rw, uint32_t rowblk, int g, int groups, int beta,
-                                  int hv, Piece& pc) {
-    const int p = g >> 1, j = g & 1;
-    const bool half = (groups & 1) && g == groups - 1;
-    const uint32_t P = g < groups ? rowblk + static_cast<uint32_t>(p) * kPacketBytes : kOutOfRange;
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-        const uint32_t s = 4 * beta + b;
-        const uint32_t co = half ? P + 8 * s + 4 * hv : P + 16 * s + 8 * j + 4 * hv;
-        const uint32_t ao = half ? P + kHalfAffineOff + 8 * s : P + kPacketAffineOff + 16 * s + 8 * j;
-        pc.code[b] = ld32(rw, co);
-        pc.acol[b] = ld64(rw, ao);
+// Packet p of a row block (full, half, or nothing past the last group).
+__device__ inline void load_packet(__amdgpu_buffer_rsrc_t rw, uint32_t rowblk, int p, int groups, int lane,
+                                   Piece& pc) {
+    const bool full = 2 * p + 1 < groups;
+    const bool half = 2 * p + 1 == groups;
+    const uint32_t P = full || half ? rowblk + static_cast<uint32_t>(p) * kPacketBytes : kOutOfRange;
+    if (half) {
+        const uint2 c = ld64(rw, P + 8 * lane);
+        const uint2 a = ld64(rw, P + kHalfAffineOff + 8 * lane);
+        pc.c = uint4{c.x, c.y, 0u, 0u};
+        pc.a = uint4{a.x, a.y, 0u, 0u};
+        pc.b = ld16(rw, P + kHalfBiasOff + 2 * lane);
+    } else {
+        pc.c = ld128(rw, P + 16 * lane);
+        pc.a = ld128(rw, P + kPacketAffineOff + 16 * lane);
+        pc.b = ld32(rw, P + kPacketBiasOff + 4 * lane);
     }
-    // Full packet: 4 bytes per slot (groups 2p, 2p+1); half packet: 2 bytes
-    // per slot (the 16 bytes read cover this row's four slots and whatever
-    // follows them, which is not used).
-    pc.bias = ld128(rw, half ? P + kHalfBiasOff + 8 * beta : P + kPacketBiasOff + 16 * beta);
-    pc.half = half;
 }
 
-// B[r][g][a] from the piece.
-__device__ inline uint32_t piece_bias(const Piece& pc, int a, int j) {
-    const uint32_t w[4] = {pc.bias.x, pc.bias.y, pc.bias.z, pc.bias.w};
-    if (pc.half) return (a & 1) ? w[a >> 1] >> 16 : w[a >> 1] & 0xffffu;
-    return j ? w[a] >> 16 : w[a] & 0xffffu;
+// Value of lane b of this lane's quad.
+template <int B>
+__device__ inline uint32_t quad_lane(uint32_t v) {
+    return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), B * 0x55, 0xf, 0xf, false));
 }
 
-// Decode vectors 4*SEL .. 4*SEL+3 of the piece (16 weights) and store them,
-// in K order, at dst (16 halves).
-template <int SEL>
-__device__ inline void decode4(const Piece& pc, int j, _Float16* dst) {
-    f16x2 qe[4], qo[4];
+// Decode operands prepared from a piece.
+struct DecOps {
+    uint32_t p01[2], p23[2];  // byte n of word h: nibbles (q_0, q_1) / (q_2, q_3) of vector 4(4h+n)+j
+    f16x4 arow;               // A[j][0..3]
+    f32x4 bvec;               // B[0..3]
+};
+
+// Gather, for group 2p + jj, the codes of vectors 4n+j, row j of A and all
+// of B from the four slots of the quad.
+__device__ inline void prepare(const Piece& pc, int j, int jj, DecOps& d) {
+    const uint32_t cl = jj ? pc.c.z : pc.c.x, ch = jj ? pc.c.w : pc.c.y;
+    const uint32_t al = jj ? pc.a.z : pc.a.x, ah = jj ? pc.a.w : pc.a.y;
+    const uint32_t bv = jj ? pc.b >> 16 : pc.b & 0xffffu;
+    const uint32_t cw[2][4] = {{quad_lane<0>(cl), quad_lane<1>(cl), quad_lane<2>(cl), quad_lane<3>(cl)},
+                               {quad_lane<0>(ch), quad_lane<1>(ch), quad_lane<2>(ch), quad_lane<3>(ch)}};
+    const int sh = 2 * j;
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-        // nibble n of e holds vector 2n, nibble n of o vector 2n+1; the fp4
-        // converter turns byte SEL into exact halves (code / 2, scaled by 2)
-        const uint32_t e = pc.code[b] & 0x33333333u;
-        const uint32_t o = (pc.code[b] >> 2) & 0x33333333u;
-        qe[b] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(e, 2.0f, SEL);  // vectors 4SEL, 4SEL+2
-        qo[b] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(o, 2.0f, SEL);  // vectors 4SEL+1, 4SEL+3
+    for (int h = 0; h < 2; ++h) {
+        uint32_t m[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) m[b] = (cw[h][b] >> sh) & 0x03030303u;
+        d.p01[h] = m[0] | (m[1] << 4);
+        d.p23[h] = m[2] | (m[3] << 4);
     }
-    f16x8 out[2];
+    // row j of A: half (j & 1) of word (j >> 1) of every column b
+    const uint32_t lo[4] = {quad_lane<0>(al), quad_lane<1>(al), quad_lane<2>(al), quad_lane<3>(al)};
+    const uint32_t hi[4] = {quad_lane<0>(ah), quad_lane<1>(ah), quad_lane<2>(ah), quad_lane<3>(ah)};
+    uint32_t w[4];
 #pragma unroll
-    for (int vi = 0; vi < 4; ++vi) {
-        float q[4];
+    for (int b = 0; b < 4; ++b) w[b] = j < 2 ? lo[b] : hi[b];
+    const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+    const uint32_t a01 = __builtin_amdgcn_perm(w[1], w[0], sel);
+    const uint32_t a23 = __builtin_amdgcn_perm(w[3], w[2], sel);
+    d.arow = __builtin_bit_cast(f16x4, uint2{a01, a23});
+    d.bvec[0] = h2f(quad_lane<0>(bv));
+    d.bvec[1] = h2f(quad_lane<1>(bv));
+    d.bvec[2] = h2f(quad_lane<2>(bv));
+    d.bvec[3] = h2f(quad_lane<3>(bv));
+}
+
+// Vectors 4N .. 4N+3 of the row block: one matrix-core instruction; lane
+// (beta, j) stores vector 4N+j at dst + 16N + 4j (dst = the lane's row).
+template <int N>
+__device__ inline void decode_vecs(const DecOps& d, _Float16* dst, int j) {
+    const f16x2 lo = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(d.p01[N >> 2], 2.0f, N & 3);
+    const f16x2 hi = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(d.p23[N >> 2], 2.0f, N & 3);
+    const f16x4 q = __builtin_shufflevector(lo, hi, 0, 1, 2, 3);
+    const f32x4 w = __builtin_amdgcn_mfma_f32_4x4x4f16(d.arow, q, d.bvec, 0, 0, 0);
+    f16x4 o;
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            const f16x2 src = (vi & 1) ? qo[b] : qe[b];
-            q[b] = static_cast<float>(vi < 2 ? src.x : src.y);
-        }
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-            float w = h2f(piece_bias(pc, a, j));
-#pragma unroll
-            for (int b = 0; b < 4; ++b) {
-                const uint32_t word = a < 2 ? pc.acol[b].x : pc.acol[b].y;
-                w = __builtin_fmaf(h2f((a & 1) ? word >> 16 : word & 0xffffu), q[b], w);
-            }
-            out[vi >> 1][4 * (vi & 1) + a] = static_cast<_Float16>(w);
-        }
-    }
-    *reinterpret_cast<f16x8*>(dst) = out[0];
-    *reinterpret_cast<f16x8*>(dst + 8) = out[1];
+    for (int a = 0; a < 4; ++a) o[a] = static_cast<_Float16>(w[a]);
+    *reinterpret_cast<f16x4*>(dst + 16 * N + 4 * j) = o;
 }
 
 // One 32-column step of the tile product: MI x kNI matrix-core tiles.
 template <int MI>
-__device__ inline void mma_step(const f16x8 (&xa)[MI], const _Float16* wsrc, f32x4 (&acc)[MI][kNI]) {
-    f16x8 wb[kNI];
-#pragma unroll
-    for (int n = 0; n < kNI; ++n) wb[n] = *reinterpret_cast<const f16x8*>(wsrc + 16 * n * kLdsRow);
+__device__ inline void mma(const f16x8 (&xa)[MI], const f16x8 (&wb)[kNI], f32x4 (&acc)[MI][kNI]) {
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int n = 0; n < kNI; ++n) acc[i][n] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa[i], wb[n], acc[i][n], 0, 0, 0);
+        for (int n = 0; n < kNI; ++n)
+            acc[i][n] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa[i], wb[n], acc[i][n], 0, 0, 0);
+}
+
+__device__ inline void read_w(const _Float16* src, f16x8 (&wb)[kNI]) {
+#pragma unroll
+    for (int n = 0; n < kNI; ++n) wb[n] = *reinterpret_cast<const f16x8*>(src + 16 * n * kLdsRow);
 }
 
 template <int MI>
 __device__ inline void load_x(__amdgpu_buffer_rsrc_t rx, uint32_t off, uint32_t row_step, f16x8 (&xa)[MI]) {
 #pragma unroll
-    for (int i = 0; i < MI; ++i) {
-        const uint4 v = ld128(rx, off + i * row_step);
-        xa[i] = __builtin_bit_cast(f16x8, v);
-    }
+    for (int i = 0; i < MI; ++i) xa[i] = __builtin_bit_cast(f16x8, ld128(rx, off + i * row_step));
 }
 
-// One K step (group g): products of the four 32-column slices of buffer
-// `cur`, with the next group's decode (if any) written to the other buffer.
+// One 32-column slice S of group g: prefetch activations two slices ahead
+// and weights one slice ahead, decode a quarter of the next group (from
+// pieces src, group jj of their packet), multiply.
 template <int MI, int S>
-__device__ inline void group_slice(__amdgpu_buffer_rsrc_t rx, uint32_t xoff, uint32_t row_step, uint32_t next_off,
-                                   f16x8 (&xa)[MI], const _Float16* wsrc, bool decode_next, const Piece& nxt, int jn,
-                                   _Float16* wdst, f32x4 (&acc)[MI][kNI]) {
-    f16x8 xn[MI];
-    load_x<MI>(rx, S < 3 ? xoff + 64 * (S + 1) : next_off, row_step, xn);  // prefetch the next slice
-    mma_step<MI>(xa, wsrc + 32 * S, acc);
-    if (decode_next) decode4<S>(nxt, jn, wdst + 16 * S);
-#pragma unroll
-    for (int i = 0; i < MI; ++i) xa[i] = xn[i];
+__device__ inline void slice(__amdgpu_buffer_rsrc_t rx, uint32_t xnext, uint32_t row_step, f16x8 (&xq)[4][MI],
+                             f16x8 (&wb)[2][kNI], const _Float16* wsrc, bool decode_next, const Piece (&src)[2],
+                             int jj, DecOps (&ops)[2], int j, _Float16* const (&wdst)[2], f32x4 (&acc)[MI][kNI]) {
+    load_x<MI>(rx, xnext, row_step, xq[(S + 2) & 3]);
+    if (S < 3) read_w(wsrc + 32 * (S + 1), wb[(S + 1) & 1]);
+    // (After the last group this decodes zeros into the idle buffer: no
+    // branch in the loop body.)
+    (void)decode_next;
+    {
+        constexpr int r = S >> 1;  // local row block of this wavefront
+        if ((S & 1) == 0) prepare(src[r], j, jj, ops[r]);
+        constexpr int n0 = 4 * (S & 1);
+        decode_vecs<n0 + 0>(ops[r], wdst[r], j);
+        decode_vecs<n0 + 1>(ops[r], wdst[r], j);
+        decode_vecs<n0 + 2>(ops[r], wdst[r], j);
+        decode_vecs<n0 + 3>(ops[r], wdst[r], j);
+    }
+    mma<MI>(xq[S & 3], wb[S & 1], acc);
+}
+
+// Everything a group step needs besides its pieces.
+template <int MI>
+struct GemmState {
+    __amdgpu_buffer_rsrc_t rx;
+    uint32_t xbase, row_step;
+    const _Float16* wlane;
+    _Float16* wrow[2];
+    int groups, j;
+};
+
+// Group g: products of buffer g & 1 (slices 0..3) while group g+1 is decoded
+// from `src` (its group jj) into the other buffer.
+template <int MI>
+__device__ inline void group_step(const GemmState<MI>& st, int g, const Piece (&src)[2], int jj, f16x8 (&xq)[4][MI],
+                                  f32x4 (&acc)[MI][kNI]) {
+    const _Float16* wsrc = st.wlane + (g & 1) * kWBuf;
+    _Float16* const wdst[2] = {st.wrow[0] + ((g + 1) & 1) * kWBuf, st.wrow[1] + ((g + 1) & 1) * kWBuf};
+    const bool decode_next = g + 1 < st.groups;
+    DecOps ops[2];
+    f16x8 wb[2][kNI];
+    read_w(wsrc, wb[0]);
+    // activation slices 2, 3 of this group, 0, 1 of the next (or nothing)
+    const uint32_t xoff = st.xbase + static_cast<uint32_t>(g) * 256u;
+    const uint32_t xn = decode_next ? xoff + 256u : kOutOfRange;
+    slice<MI, 0>(st.rx, xoff + 128u, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
+    slice<MI, 1>(st.rx, xoff + 192u, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
+    slice<MI, 2>(st.rx, xn, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
+    slice<MI, 3>(st.rx, xn + 64u, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
+    __syncthreads();
 }
 
 template <int MI>
@@ -174,20 +239,28 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     const __amdgpu_buffer_rsrc_t rw =
         make_rsrc(packed, static_cast<uint32_t>(N / kRowBlock) * groups * kGroupBlockBytes);
 
-    // Decode role: row rr of the tile, vectors 16*hv .. of each group.
-    const int rr = threadIdx.x >> 1, hv = threadIdx.x & 1;
-    const int r = n0 + rr;
-    const uint32_t rowblk = r < N ? static_cast<uint32_t>(r >> 4) * groups * kGroupBlockBytes : kOutOfRange;
-    const int beta = r & 15;
-    _Float16* wdst = wsh + rr * kLdsRow + 64 * hv;
+    // Decode role: this wavefront decodes local row blocks 2*wave and
+    // 2*wave+1; lane (beta = lane / 4, j = lane % 4) = packet slot `lane`.
+    GemmState<MI> st;
+    const int beta = lane >> 2;
+    st.j = lane & 3;
+    st.groups = groups;
+    uint32_t rowblk[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        const int rb = (n0 >> 4) + 2 * wave + r;
+        rowblk[r] = rb < (N >> 4) ? static_cast<uint32_t>(rb) * groups * kGroupBlockBytes : kOutOfRange;
+        st.wrow[r] = wsh + (16 * (2 * wave + r) + beta) * kLdsRow;
+    }
 
     // Activation operand of tile i, 32-column slice s of group g, lane
     // (m = lane % 16, kb = lane / 16): 8 halves of token tok0 + 16 i + m at
     // column 128 g + 32 s + 8 kb.  Tokens past M read zeros.
-    const uint32_t row_step = 16u * K * 2u;
-    const uint32_t xbase = (static_cast<uint32_t>(tok0 + (lane & 15)) * K + 8 * (lane >> 4)) * 2u;
+    st.rx = rx;
+    st.row_step = 16u * K * 2u;
+    st.xbase = (static_cast<uint32_t>(tok0 + (lane & 15)) * K + 8 * (lane >> 4)) * 2u;
     // Weight operand of tile n: row 16 n + lane % 16, same columns.
-    const _Float16* wlane = wsh + (lane & 15) * kLdsRow + 8 * (lane >> 4);
+    st.wlane = wsh + (lane & 15) * kLdsRow + 8 * (lane >> 4);
 
     f32x4 acc[MI][kNI];
 #pragma unroll
@@ -195,35 +268,49 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
 #pragma unroll
         for (int n = 0; n < kNI; ++n) acc[i][n] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // Prologue: decode group 0 into buffer 0; packet data of group 1 in flight.
-    Piece cur, nxt;
-    load_piece(rw, rowblk, 0, groups, beta, hv, cur);
-    load_piece(rw, rowblk, 1, groups, beta, hv, nxt);
-    decode4<0>(cur, 0, wdst);
-    decode4<1>(cur, 0, wdst + 16);
-    decode4<2>(cur, 0, wdst + 32);
-    decode4<3>(cur, 0, wdst + 48);
-    f16x8 xa[MI];
-    load_x<MI>(rx, xbase, row_step, xa);
+    // Packets two groups ahead of their decode: pa = packet q (groups 2q,
+    // 2q+1), pb = packet q+1, pc = packet q+2 (loaded during group 2q+1).
+    Piece pa[2], pb[2], pc[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        load_packet(rw, rowblk[r], 0, groups, lane, pa[r]);
+        load_packet(rw, rowblk[r], 1, groups, lane, pb[r]);
+    }
+    // Prologue: group 0 into buffer 0.
+    {
+        DecOps ops;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            prepare(pa[r], st.j, 0, ops);
+            decode_vecs<0>(ops, st.wrow[r], st.j);
+            decode_vecs<1>(ops, st.wrow[r], st.j);
+            decode_vecs<2>(ops, st.wrow[r], st.j);
+            decode_vecs<3>(ops, st.wrow[r], st.j);
+            decode_vecs<4>(ops, st.wrow[r], st.j);
+            decode_vecs<5>(ops, st.wrow[r], st.j);
+            decode_vecs<6>(ops, st.wrow[r], st.j);
+            decode_vecs<7>(ops, st.wrow[r], st.j);
+        }
+    }
+    f16x8 xq[4][MI];
+    load_x<MI>(rx, st.xbase, st.row_step, xq[0]);
+    load_x<MI>(rx, st.xbase + 64u, st.row_step, xq[1]);
     __syncthreads();
 
-    for (int g = 0; g < groups; ++g) {
-        const _Float16* wsrc = wlane + (g & 1) * kWBuf;
-        _Float16* wnext = wdst + ((g + 1) & 1) * kWBuf;
-        const bool decode_next = g + 1 < groups;
-        // packet data two groups ahead
-        Piece far;
-        load_piece(rw, rowblk, g + 2, groups, beta, hv, far);
-        const int jn = (g + 1) & 1;
-        const uint32_t xoff = xbase + static_cast<uint32_t>(g) * 256u;
-        const uint32_t next_off = decode_next ? xoff + 256u : kOutOfRange;
-        group_slice<MI, 0>(rx, xoff, row_step, next_off, xa, wsrc, decode_next, nxt, jn, wnext, acc);
-        group_slice<MI, 1>(rx, xoff, row_step, next_off, xa, wsrc, decode_next, nxt, jn, wnext, acc);
-        group_slice<MI, 2>(rx, xoff, row_step, next_off, xa, wsrc, decode_next, nxt, jn, wnext, acc);
-        group_slice<MI, 3>(rx, xoff, row_step, next_off, xa, wsrc, decode_next, nxt, jn, wnext, acc);
-        nxt = far;
-        __syncthreads();
+    int g = 0;
+    for (; g + 1 < groups; g += 2) {
+        const int q = g >> 1;
+        group_step<MI>(st, g, pa, 1, xq, acc);  // decodes group 2q+1 (packet q)
+#pragma unroll
+        for (int r = 0; r < 2; ++r) load_packet(rw, rowblk[r], q + 2, groups, lane, pc[r]);
+        group_step<MI>(st, g + 1, pb, 0, xq, acc);  // decodes group 2q+2 (packet q+1)
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            pa[r] = pb[r];
+            pb[r] = pc[r];
+        }
     }
+    if (g < groups) group_step<MI>(st, g, pa, 1, xq, acc);  // last group (nothing left to decode)
 
     // Epilogue.  D lane layout: output row 16 n + lane % 16, tokens
     // 16 i + 4 (lane / 16) + e.
