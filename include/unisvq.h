@@ -149,10 +149,13 @@ typedef struct {
 int unisvq_gemv_batched(const unisvq_gemv_problem* problems, int count, int64_t M, int x_dtype,
                         int y_dtype, void* stream);
 
-/* Workspace unisvq_gemm needs for bf16 activations: an fp16 copy of x
- * (M*K*2 bytes rounded up to 256) plus one fp32 scale per token.  fp16
- * activations need none.  0 for an invalid shape or M < 1. */
-size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M);
+/* Device workspace unisvq_gemm needs for this product, in bytes (0: none):
+ * for BF16 activations an fp16 copy of x (M*K*2 bytes, rounded up to 256)
+ * and one fp32 scale per token (rounded up to 256); for products with too
+ * few output tiles to fill the GPU (small M), fp32 partial sums of a split
+ * along K (splits*M*N*4 bytes).  0 also for an invalid shape, M < 1 or an
+ * unknown x_dtype.  Host-only, no GPU needed. */
+size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype);
 
 /* Prefill product y = x * W_hat^T for any M >= 1 (Eq. 1 with Eq. 4/8).
  * Arguments as unisvq_gemv; x_dtype F16 or BF16, y_dtype F16, BF16 or F32.
@@ -163,11 +166,13 @@ size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M);
  * memory.  bf16 activations are first scaled per token by a power of two
  * into [2^14, 2^15) and stored as fp16 in the workspace -- exact for every
  * element within 2^28 of its token's largest magnitude -- and the scale is
- * undone on the fp32 result.
- *   workspace  device, >= unisvq_gemm_workspace_bytes(N, K, M) bytes,
- *              16-byte aligned, for BF16 activations (UNISVQ_EWORKSPACE if
- *              missing or smaller, UNISVQ_EALIGN if misaligned); ignored (may
- *              be NULL) for F16.  Overwritten; the caller owns it. */
+ * undone on the fp32 result.  When M is small the K range is split across
+ * workgroups and a second kernel sums the fp32 partials in a fixed order
+ * (results are reproducible run to run).
+ *   workspace  device, >= unisvq_gemm_workspace_bytes(N, K, M, x_dtype)
+ *              bytes, 16-byte aligned (UNISVQ_EWORKSPACE if missing or
+ *              smaller, UNISVQ_EALIGN if misaligned); may be NULL when that
+ *              size is 0.  Overwritten; the caller owns it. */
 int unisvq_gemm(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype,
                 void* y, int y_dtype, void* workspace, size_t workspace_bytes, void* stream);
 

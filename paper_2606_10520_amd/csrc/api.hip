@@ -101,17 +101,18 @@ int unisvq_gemv_batched(const unisvq_gemv_problem* problems, int count, int64_t 
     return unisvq::launch_gemv_batch(probs, count, M, x_dtype, y_dtype, static_cast<hipStream_t>(stream));
 }
 
-size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M) {
-    if (!shape_ok(N, K) || M < 1 || M > (int64_t{1} << 31) - 1) return 0;
-    return unisvq::gemm_workspace_bytes(K, M);
+size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype) {
+    if (!shape_ok(N, K) || M < 1 || M > (int64_t{1} << 31) - 1 || !x_dtype_ok(x_dtype)) return 0;
+    return unisvq::gemm_workspace_bytes(N, K, M, x_dtype);
 }
 
 int unisvq_gemm(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype,
                 void* y, int y_dtype, void* workspace, size_t workspace_bytes, void* stream) {
     const int st = check_product(N, K, packed, M, x, x_dtype, y, y_dtype);
     if (st != UNISVQ_OK) return st;
-    if (x_dtype == UNISVQ_BF16) {
-        if (!workspace || workspace_bytes < unisvq::gemm_workspace_bytes(K, M)) return UNISVQ_EWORKSPACE;
+    const size_t need = unisvq::gemm_workspace_bytes(N, K, M, x_dtype);
+    if (need) {
+        if (!workspace || workspace_bytes < need) return UNISVQ_EWORKSPACE;
         if (!aligned(workspace, 16)) return UNISVQ_EALIGN;
     }
     return unisvq::launch_gemm(N, K, static_cast<const uint8_t*>(packed), M, x, x_dtype, y, y_dtype,

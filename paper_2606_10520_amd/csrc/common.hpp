@@ -80,10 +80,11 @@ int launch_gemv_batch(const GemvProblem* probs, int count, int64_t M, int x_dtyp
                       hipStream_t s);
 int launch_gemv(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x,
                 int x_dtype, void* y, int y_dtype, hipStream_t s);
-// Prefill path.  bf16 activations need gemm_workspace_bytes(K, M) bytes of
-// 16-byte-aligned device workspace (fp16 copy of x plus one scale per token);
-// fp16 activations need none.
-size_t gemm_workspace_bytes(int64_t K, int64_t M);
+// Prefill path.  Device workspace (16-byte aligned) of
+// gemm_workspace_bytes(N, K, M, x_dtype) bytes: for bf16 activations an fp16
+// copy of x plus one scale per token, and for products split along K the
+// fp32 partial sums.  0 means none is needed.
+size_t gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype);
 int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x,
                 int x_dtype, void* y, int y_dtype, void* workspace, hipStream_t s);
 

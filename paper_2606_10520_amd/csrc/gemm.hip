@@ -59,11 +59,13 @@ struct Piece {
     uint32_t b;   // B[r][2p + jj][j]: low half jj = 0, high half jj = 1
 };
 
-// Packet p of a row block (full, half, or nothing past the last group).
-__device__ inline void load_packet(__amdgpu_buffer_rsrc_t rw, uint32_t rowblk, int p, int groups, int lane,
+// Packet p of a row block: full, half (the last group of an odd count), or
+// nothing at or past group `gend` (the end of the range being decoded; a
+// range ends at a packet boundary or at the last group).
+__device__ inline void load_packet(__amdgpu_buffer_rsrc_t rw, uint32_t rowblk, int p, int gend, int lane,
                                    Piece& pc) {
-    const bool full = 2 * p + 1 < groups;
-    const bool half = 2 * p + 1 == groups;
+    const bool full = 2 * p + 1 < gend;
+    const bool half = 2 * p + 1 == gend;
     const uint32_t P = full || half ? rowblk + static_cast<uint32_t>(p) * kPacketBytes : kOutOfRange;
     if (half) {
         const uint2 c = ld64(rw, P + 8 * lane);
@@ -190,7 +192,7 @@ struct GemmState {
     uint32_t xbase, row_step;
     const _Float16* wlane;
     _Float16* wrow[2];
-    int groups, j;
+    int gend, j;  // end of this workgroup's group range
 };
 
 // Group g: products of buffer g & 1 (slices 0..3) while group g+1 is decoded
@@ -200,7 +202,7 @@ __device__ inline void group_step(const GemmState<MI>& st, int g, const Piece (&
                                   f32x4 (&acc)[MI][kNI]) {
     const _Float16* wsrc = st.wlane + (g & 1) * kWBuf;
     _Float16* const wdst[2] = {st.wrow[0] + ((g + 1) & 1) * kWBuf, st.wrow[1] + ((g + 1) & 1) * kWBuf};
-    const bool decode_next = g + 1 < st.groups;
+    const bool decode_next = g + 1 < st.gend;
     DecOps ops[2];
     f16x8 wb[2][kNI];
     read_w(wsrc, wb[0]);
@@ -218,22 +220,29 @@ template <int MI>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restrict__ packed,
                                                         const _Float16* __restrict__ x,
                                                         const float* __restrict__ inv_scale, void* y, int N,
-                                                        int K, int M, int y_dtype, int m_tiles, int n_tiles) {
+                                                        int K, int M, int y_dtype, int m_tiles, int n_tiles,
+                                                        int splits, int gps, float* __restrict__ partial) {
     __shared__ __attribute__((aligned(16))) _Float16 wsh[2 * kWBuf];
     constexpr int BM = kWaves * 16 * MI;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
-    // Tile of this workgroup.  Workgroups are dealt to the 8 XCDs round-robin;
-    // renumbering them so that each XCD gets a contiguous run of tiles makes
-    // the tiles that share activation rows share that XCD's L2.
-    const int T = m_tiles * n_tiles;
+    // Tile of this workgroup: (K split, token tile, row tile), row tile
+    // fastest.  Workgroups are dealt to the 8 XCDs round-robin; renumbering
+    // them so that each XCD gets a contiguous run of tiles makes the tiles
+    // that share activation rows share that XCD's L2.
+    const int T = m_tiles * n_tiles * splits;
     int L = blockIdx.x;
     if ((T & 7) == 0) L = (L & 7) * (T >> 3) + (L >> 3);
-    const int mt = L / n_tiles, nt = L - mt * n_tiles;
+    const int nt = L % n_tiles;
+    const int mt = (L / n_tiles) % m_tiles;
+    const int sp = L / (n_tiles * m_tiles);
     const int n0 = nt * kBN;
     const int tok0 = mt * BM + wave * 16 * MI;
     const int groups = K >> 7;
+    // groups [gb, gend) of this split; gb is even (a packet boundary)
+    const int gb = sp * gps;
+    const int gend = min(groups, gb + gps);
 
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(M) * K * 2u);
     const __amdgpu_buffer_rsrc_t rw =
@@ -244,7 +253,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     GemmState<MI> st;
     const int beta = lane >> 2;
     st.j = lane & 3;
-    st.groups = groups;
+    st.gend = gend;
     uint32_t rowblk[2];
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
@@ -273,10 +282,10 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     Piece pa[2], pb[2], pc[2];
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
-        load_packet(rw, rowblk[r], 0, groups, lane, pa[r]);
-        load_packet(rw, rowblk[r], 1, groups, lane, pb[r]);
+        load_packet(rw, rowblk[r], gb >> 1, gend, lane, pa[r]);
+        load_packet(rw, rowblk[r], (gb >> 1) + 1, gend, lane, pb[r]);
     }
-    // Prologue: group 0 into buffer 0.
+    // Prologue: group gb into buffer gb & 1 (= 0).
     {
         DecOps ops;
 #pragma unroll
@@ -293,16 +302,16 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
         }
     }
     f16x8 xq[4][MI];
-    load_x<MI>(rx, st.xbase, st.row_step, xq[0]);
-    load_x<MI>(rx, st.xbase + 64u, st.row_step, xq[1]);
+    load_x<MI>(rx, st.xbase + static_cast<uint32_t>(gb) * 256u, st.row_step, xq[0]);
+    load_x<MI>(rx, st.xbase + static_cast<uint32_t>(gb) * 256u + 64u, st.row_step, xq[1]);
     __syncthreads();
 
-    int g = 0;
-    for (; g + 1 < groups; g += 2) {
+    int g = gb;
+    for (; g + 1 < gend; g += 2) {
         const int q = g >> 1;
         group_step<MI>(st, g, pa, 1, xq, acc);  // decodes group 2q+1 (packet q)
 #pragma unroll
-        for (int r = 0; r < 2; ++r) load_packet(rw, rowblk[r], q + 2, groups, lane, pc[r]);
+        for (int r = 0; r < 2; ++r) load_packet(rw, rowblk[r], q + 2, gend, lane, pc[r]);
         group_step<MI>(st, g + 1, pb, 0, xq, acc);  // decodes group 2q+2 (packet q+1)
 #pragma unroll
         for (int r = 0; r < 2; ++r) {
@@ -310,10 +319,11 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
             pb[r] = pc[r];
         }
     }
-    if (g < groups) group_step<MI>(st, g, pa, 1, xq, acc);  // last group (nothing left to decode)
+    if (g < gend) group_step<MI>(st, g, pa, 1, xq, acc);  // last group (nothing left to decode)
 
     // Epilogue.  D lane layout: output row 16 n + lane % 16, tokens
-    // 16 i + 4 (lane / 16) + e.
+    // 16 i + 4 (lane / 16) + e.  With a K split the fp32 partial sums go to
+    // partial[split][M][N] and a second kernel adds them up.
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
 #pragma unroll
@@ -324,10 +334,32 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
 #pragma unroll
             for (int n = 0; n < kNI; ++n) {
                 const int row = n0 + 16 * n + (lane & 15);
-                if (row < N) store_out(y, static_cast<int64_t>(t) * N + row, acc[i][n][e] * sc, y_dtype);
+                if (row >= N) continue;
+                if (partial)
+                    partial[(static_cast<int64_t>(sp) * M + t) * N + row] = acc[i][n][e];
+                else
+                    store_out(y, static_cast<int64_t>(t) * N + row, acc[i][n][e] * sc, y_dtype);
             }
         }
     }
+}
+
+// y = (sum over the K splits of the partial sums) * per-token scale, four
+// outputs per thread (N is a multiple of 16).
+__global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ partial, int splits, int M,
+                                                            int N, const float* __restrict__ inv_scale, void* y,
+                                                            int y_dtype) {
+    const int64_t total4 = static_cast<int64_t>(M) * N / 4;
+    const int64_t i4 = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i4 >= total4) return;
+    const f32x4* p = reinterpret_cast<const f32x4*>(partial);
+    f32x4 s = p[i4];
+    for (int k = 1; k < splits; ++k) s += p[k * total4 + i4];
+    const int64_t e0 = 4 * i4;
+    const int t = static_cast<int>(e0 / N);
+    const float sc = inv_scale ? inv_scale[t] : 1.0f;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) store_out(y, e0 + c, s[c] * sc, y_dtype);
 }
 
 // bf16 activations -> fp16 with a power-of-two scale per token (see the top
@@ -375,39 +407,82 @@ __global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restr
     if (threadIdx.x == 0) inv_scale[t] = ldexpf(1.0f, -s);
 }
 
+// Tiling of one product: token tiles of 64 (M <= 128) or 256 tokens, row
+// tiles of 128; when that leaves fewer than 256 workgroups the K range is
+// split (at packet boundaries) until there are about 256.
+struct GemmPlan {
+    int mi, m_tiles, n_tiles, splits, gps;
+};
+
+GemmPlan plan_gemm(int64_t N, int64_t K, int64_t M) {
+    GemmPlan p;
+    p.mi = M > 128 ? 4 : 1;
+    const int64_t bm = kWaves * 16 * p.mi;
+    p.m_tiles = static_cast<int>((M + bm - 1) / bm);
+    p.n_tiles = static_cast<int>((N + kBN - 1) / kBN);
+    const int groups = static_cast<int>(K / kGroup);
+    p.splits = 1;
+    p.gps = groups;
+    const int64_t tiles = static_cast<int64_t>(p.m_tiles) * p.n_tiles;
+    if (tiles < 256 && groups >= 4) {
+        const int packets = (groups + 1) / 2;
+        const int want = static_cast<int>((256 + tiles - 1) / tiles);
+        const int s = want < packets ? want : packets;
+        p.gps = 2 * ((packets + s - 1) / s);
+        p.splits = (groups + p.gps - 1) / p.gps;
+    }
+    return p;
+}
+
+size_t align256(size_t b) { return (b + 255) & ~size_t{255}; }
+
+size_t partial_bytes(int64_t N, int64_t K, int64_t M) {
+    const GemmPlan p = plan_gemm(N, K, M);
+    return p.splits > 1 ? static_cast<size_t>(p.splits) * M * N * 4 : 0;
+}
+
 template <int MI>
-hipError_t launch_tiles(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const _Float16* x,
-                        const float* inv_scale, void* y, int y_dtype, hipStream_t s) {
-    constexpr int BM = kWaves * 16 * MI;
-    const int m_tiles = static_cast<int>((M + BM - 1) / BM);
-    const int n_tiles = static_cast<int>((N + kBN - 1) / kBN);
-    hipLaunchKernelGGL(gemm_kernel<MI>, dim3(static_cast<unsigned>(m_tiles) * n_tiles), dim3(kThreads), 0, s,
-                       packed, x, inv_scale, y, static_cast<int>(N), static_cast<int>(K), static_cast<int>(M),
-                       y_dtype, m_tiles, n_tiles);
+hipError_t launch_tiles(const GemmPlan& p, int64_t N, int64_t K, const uint8_t* packed, int64_t M,
+                        const _Float16* x, const float* inv_scale, void* y, int y_dtype, float* partial,
+                        hipStream_t s) {
+    const unsigned blocks = static_cast<unsigned>(p.m_tiles) * p.n_tiles * p.splits;
+    hipLaunchKernelGGL(gemm_kernel<MI>, dim3(blocks), dim3(kThreads), 0, s, packed, x, inv_scale, y,
+                       static_cast<int>(N), static_cast<int>(K), static_cast<int>(M), y_dtype, p.m_tiles,
+                       p.n_tiles, p.splits, p.gps, p.splits > 1 ? partial : nullptr);
+    if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
+    if (p.splits > 1) {
+        const int64_t total4 = M * N / 4;
+        hipLaunchKernelGGL(reduce_splits_kernel, dim3(static_cast<unsigned>((total4 + 255) / 256)), dim3(256), 0, s,
+                           partial, p.splits, static_cast<int>(M), static_cast<int>(N), inv_scale, y, y_dtype);
+    }
     return hipGetLastError();
 }
 
 }  // namespace
 
-size_t gemm_workspace_bytes(int64_t K, int64_t M) {
-    const size_t xh = (static_cast<size_t>(M) * K * 2 + 255) & ~size_t{255};
-    return xh + static_cast<size_t>(M) * 4;
+size_t gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype) {
+    size_t b = 0;
+    if (x_dtype == UNISVQ_BF16) b += align256(static_cast<size_t>(M) * K * 2) + align256(static_cast<size_t>(M) * 4);
+    return b + partial_bytes(N, K, M);
 }
 
 int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x, int x_dtype,
                 void* y, int y_dtype, void* workspace, hipStream_t s) {
     const _Float16* xh = static_cast<const _Float16*>(x);
     const float* inv = nullptr;
+    uint8_t* ws = static_cast<uint8_t*>(workspace);
     if (x_dtype == UNISVQ_BF16) {
-        _Float16* wxh = static_cast<_Float16*>(workspace);
-        float* winv = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) +
-                                               ((static_cast<size_t>(M) * K * 2 + 255) & ~size_t{255}));
+        _Float16* wxh = reinterpret_cast<_Float16*>(ws);
+        ws += align256(static_cast<size_t>(M) * K * 2);
+        float* winv = reinterpret_cast<float*>(ws);
+        ws += align256(static_cast<size_t>(M) * 4);
         hipLaunchKernelGGL(scale_rows_kernel, dim3(static_cast<unsigned>(M)), dim3(256), 0, s,
                            static_cast<const uint16_t*>(x), static_cast<int>(K), wxh, winv);
         if (hipGetLastError() != hipSuccess) return UNISVQ_EHIP;
         xh = wxh;
         inv = winv;
     }
+    float* partial = reinterpret_cast<float*>(ws);
     // The activation buffer is addressed with 32-bit offsets: slice M.
     const int64_t max_rows = kMaxBufferBytes / (2 * K) / 256 * 256;
     for (int64_t m0 = 0; m0 < M; m0 += max_rows) {
@@ -415,8 +490,9 @@ int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const vo
         const _Float16* xs = xh + m0 * K;
         const float* is = inv ? inv + m0 : nullptr;
         void* ys = static_cast<uint8_t*>(y) + m0 * N * (y_dtype == UNISVQ_F32 ? 4 : 2);
-        const hipError_t e = mc > 128 ? launch_tiles<4>(N, K, packed, mc, xs, is, ys, y_dtype, s)
-                                      : launch_tiles<1>(N, K, packed, mc, xs, is, ys, y_dtype, s);
+        const GemmPlan p = plan_gemm(N, K, mc);
+        const hipError_t e = p.mi == 4 ? launch_tiles<4>(p, N, K, packed, mc, xs, is, ys, y_dtype, partial, s)
+                                       : launch_tiles<1>(p, N, K, packed, mc, xs, is, ys, y_dtype, partial, s);
         if (e != hipSuccess) return UNISVQ_EHIP;
     }
     return UNISVQ_OK;

@@ -69,7 +69,7 @@ def load():
     lib.unisvq_gemv.restype = i32
     lib.unisvq_gemv_batched.argtypes = [ctypes.POINTER(GemvProblem), i32, i64, i32, i32, p]
     lib.unisvq_gemv_batched.restype = i32
-    lib.unisvq_gemm_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.unisvq_gemm_workspace_bytes.argtypes = [i64, i64, i64, i32]
     lib.unisvq_gemm_workspace_bytes.restype = sz
     lib.unisvq_gemm.argtypes = [i64, i64, p, i64, p, i32, p, i32, p, sz, p]
     lib.unisvq_gemm.restype = i32
@@ -203,15 +203,16 @@ def gemv_batched(problems, out_dtype=None, stream=None):
     return outs
 
 
-def gemm_workspace_bytes(N: int, K: int, M: int) -> int:
-    """Workspace unisvq_gemm needs for bf16 activations (fp16 needs none)."""
-    return load().unisvq_gemm_workspace_bytes(N, K, M)
+def gemm_workspace_bytes(N: int, K: int, M: int, x_dtype=None) -> int:
+    """Workspace bytes unisvq_gemm needs (x_dtype: torch dtype, default bf16)."""
+    code = BF16 if x_dtype is None else _dtype_code(x_dtype)
+    return load().unisvq_gemm_workspace_bytes(N, K, M, code)
 
 
 def gemm(packed, N: int, K: int, x, out=None, out_dtype=None, workspace=None, stream=None):
     """y[M][N] = x[M][K] . W_hat^T for any M (prefill kernel)."""
     M = x.numel() // K
-    need = gemm_workspace_bytes(N, K, M) if x.dtype == _torch().bfloat16 else 0
+    need = gemm_workspace_bytes(N, K, M, x.dtype)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     if need and workspace is None:
         workspace = _torch().empty(need, dtype=_torch().uint8, device=x.device)

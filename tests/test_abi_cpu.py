@@ -120,16 +120,26 @@ def test_batched_validation():
 
 def test_gemm_workspace():
     lib = u.load()
-    # fp16 copy of the activations (rounded up to 256 bytes) plus one fp32 scale per token
-    assert lib.unisvq_gemm_workspace_bytes(4096, 4096, 2048) == 2048 * 4096 * 2 + 2048 * 4
-    assert lib.unisvq_gemm_workspace_bytes(16, 128, 1) == 256 + 4
-    assert lib.unisvq_gemm_workspace_bytes(15, 128, 1) == 0
-    assert lib.unisvq_gemm_workspace_bytes(16, 128, 0) == 0
-    # bf16 activations need it; fp16 activations do not
-    need = lib.unisvq_gemm_workspace_bytes(64, 256, 4)
+    ws = lib.unisvq_gemm_workspace_bytes
+    # bf16: fp16 copy of the activations plus one fp32 scale per token (each rounded up to 256 B);
+    # M = 2048 fills the GPU with output tiles, so there is no split along K
+    assert ws(4096, 4096, 2048, u.BF16) == 2048 * 4096 * 2 + 2048 * 4
+    assert ws(4096, 4096, 2048, u.F16) == 0
+    assert ws(16, 128, 1, u.BF16) == 256 + 256
+    assert ws(16, 128, 1, u.F16) == 0
+    assert ws(15, 128, 1, u.BF16) == 0
+    assert ws(16, 128, 0, u.BF16) == 0
+    assert ws(16, 128, 1, u.F32) == 0
+    # a small-M product is split along K: fp32 partials for every split
+    split = ws(64, 1024, 4, u.F16)
+    assert split > 0 and split % (4 * 64 * 4) == 0
+    assert ws(64, 1024, 4, u.BF16) == split + 1024 * 4 * 2 + 256
+    # bf16 activations need it; so does a split product with fp16 activations
+    need = ws(64, 256, 4, u.BF16)
     assert lib.unisvq_gemm(64, 256, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, None, need, None) == EWS
     assert lib.unisvq_gemm(64, 256, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, GOOD, need - 1, None) == EWS
     assert lib.unisvq_gemm(64, 256, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, GOOD + 8, need, None) == EALIGN
+    assert lib.unisvq_gemm(64, 1024, GOOD, 4, GOOD, u.F16, GOOD, u.F16, None, 0, None) == EWS
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):

@@ -172,6 +172,26 @@ def test_gemm_prefill_m2048_sampled_rows(layer):
     assert rel_err(y.cpu().numpy()[:, rows], ref) <= 5e-4
 
 
+@pytest.mark.parametrize("layer", [l for l in wl.LLAMA7B if l.name in ("gate", "down")], ids=lambda l: l.name)
+@pytest.mark.parametrize("M", [16, 64])
+def test_gemm_smallbatch_7b_sampled_rows(layer, M):
+    """Small-batch decode shapes (the product is split along K and the fp32
+    partials summed by a second kernel), outlier activations, 48 rows checked."""
+    Q, A, B = wl.gen_weights(layer.N, layer.K, seed=40 + M)
+    xb = wl.gen_activations(M, layer.K, seed=wl.activation_seed(40, M), dtype="f16", outliers=True)
+    pk_ref, _ = oracle.pack(Q, A, B)
+    pk = upload_pack(Q, A, B)
+    y = u.gemm(pk, layer.N, layer.K, dev_x(xb, "f16"), out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    rows = np.random.default_rng(M).choice(layer.N, 48, replace=False)
+    rows[:2] = [0, layer.N - 1]
+    ref = oracle.matmul(pk_ref, layer.N, layer.K, x_as_f64(xb, "f16"), rows=rows)
+    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 5e-4
+    # the split reduction runs in a fixed order: bit-identical on a rerun
+    y2 = u.gemm(pk, layer.N, layer.K, dev_x(xb, "f16"), out_dtype=torch.float32)
+    assert torch.equal(y, y2)
+
+
 def test_gemm_bf16_extreme_token_scales():
     """bf16 activations far outside the fp16 range (and far below it) keep
     full accuracy: each token row is rescaled by a power of two before the
