@@ -157,6 +157,12 @@ def main():
 
     lib = u.load()
     xcode = u.F16 if xdt == "f16" else u.BF16
+    # GEMM workspace (bf16 activation copy, K-split partials): one buffer
+    # serves every call, since the calls run in order on one stream.
+    ws_bytes = 0
+    if kernel == "gemm":
+        ws_bytes = max(u.gemm_workspace_bytes(L.N, L.K, M, tdt) for L in layers)
+    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
     names = [L.name for L in layers]
     full_set = {"q", "k", "v", "o", "gate", "up", "down"} <= set(names)
 
@@ -192,7 +198,7 @@ def main():
             if kernel == "gemv":
                 return lib.unisvq_gemv(L.N, L.K, pk.data_ptr(), M, x.data_ptr(), xcode, y.data_ptr(), u.F16, sptr)
             return lib.unisvq_gemm(L.N, L.K, pk.data_ptr(), M, x.data_ptr(), xcode, y.data_ptr(), u.F16,
-                                   None, 0, sptr)
+                                   ws.data_ptr(), ws_bytes, sptr)
         return lib.unisvq_gemv_batched(item, len(item), M, xcode, u.F16, sptr)
 
     def run_step(calls, i, sptr):
@@ -231,6 +237,36 @@ def main():
     calls = build_calls(groups_)
     ms_per_step, steps_done = time_schedule(calls)
     value_gbs = set_bytes / (ms_per_step * 1e-3) / 1e9
+
+    # a dense product of the same shapes (random weights, the activation
+    # dtype), timed the same way: the library GEMM the decode would compete with
+    dense = None
+    if kernel == "gemm":
+        wts = [torch.randn(L.K, L.N, device=dev).to(tdt) for L in layers]  # K x N, contiguous
+        xs_d = [torch.from_numpy(canon[li][3].view(np.int16)).view(tdt).to(dev) for li in range(len(layers))]
+        for i in range(3):
+            for x_, w_ in zip(xs_d, wts):
+                torch.matmul(x_, w_)
+        torch.cuda.synchronize()
+        g_d = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_d):
+            outs = [torch.matmul(x_, w_) for x_, w_ in zip(xs_d, wts)]
+        g_d.replay()
+        torch.cuda.synchronize()
+        reps = max(3, args.steps // 4)
+        d0 = torch.cuda.Event(enable_timing=True)
+        d1 = torch.cuda.Event(enable_timing=True)
+        d0.record(stream)
+        for _ in range(reps):
+            g_d.replay()
+        d1.record(stream)
+        torch.cuda.synchronize()
+        dms = d0.elapsed_time(d1) / reps
+        dflops = sum(2 * M * L.N * L.K for L in layers)
+        dense = {"what": f"torch.matmul, dense {'fp16' if xdt == 'f16' else 'bf16'} weights of the same shapes",
+                 "ms_per_step": round(dms, 5), "TFLOP_per_s": round(dflops / (dms * 1e-3) / 1e12, 1),
+                 "unisvq_over_dense_time": round(ms_per_step / dms, 3)}
+        del wts, xs_d, outs, g_d
 
     # the other launch schedules of the same step, for context
     schedules = {}
@@ -282,6 +318,15 @@ def main():
                     "traffic": None if traffic is None else int(traffic),
                     "kernel": "gemv_kernel", "avg_launch_us": round(avg_us, 3),
                     "bytes_per_launch": int(bytes_per_launch)}
+    elif M <= 64:
+        # small batch: still bound by the weight stream
+        ach = bytes_per_launch / (avg_us * 1e-6) / 1e9
+        traffic = measured_traffic("gemm", args.workload, sched)
+        roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": round(ach / PEAK_HBM_GBS, 4),
+                    "traffic": None if traffic is None else int(traffic),
+                    "kernel": "gemm_kernel", "avg_launch_us": round(avg_us, 3),
+                    "bytes_per_launch": int(bytes_per_launch)}
     else:
         flops = sum(2 * M * L.N * L.K for L in layers) / launches_per_step
         ach = flops / (avg_us * 1e-6) / 1e12
@@ -317,8 +362,8 @@ def main():
                          + ("" if rows_frac == 1.0 else f" (1/{int(1 / rows_frac)} of output rows)")
                          + f", fp64 C oracle, {threads} threads, {t_cpu:.1f} s"}
 
-    if kernel == "gemv":
-        metric, value, unit = METRIC, value_gbs, "GB/s"
+    if kernel == "gemv" or M <= 64:
+        metric, value, unit = METRIC if M == 1 else f"2-bit decode achieved HBM GB/s at M={M}", value_gbs, "GB/s"
     else:
         flops = sum(2 * M * L.N * L.K for L in layers)
         metric, value, unit = "unisvq_gemm effective TFLOP/s (2MNK)", flops / (ms_per_step * 1e-3) / 1e12, "TFLOP/s"
@@ -333,13 +378,17 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f16" if xdt == "f16" else "bf16",
+        # arithmetic type of the matrix cores: the GEMM multiplies in fp16
+        # (bf16 activations are carried exactly as scaled fp16)
+        "dtype": "f16" if (xdt == "f16" or kernel == "gemm") else "bf16",
         "data": "synthetic",
         "config": {"workload": args.workload, "layers": {L.name: [L.N, L.K] for L in layers}, "M": M,
+                   "activations": xdt,
                    "d": 4, "bits": 2, "group": 128, "kernel": kernel, "schedule": sched,
                    "launches_per_step": len(groups_), "buffer_copies": copies,
                    "set_bytes": set_bytes},
-        "pct_peak_hbm": round(100 * value_gbs / PEAK_HBM_GBS, 2) if kernel == "gemv" else None,
+        "pct_peak_hbm": round(100 * value_gbs / PEAK_HBM_GBS, 2) if (kernel == "gemv" or M <= 64) else None,
+        "dense_matmul": dense,
         "event_us_per_launch": {k: round(v, 3) for k, v in per_layer_us.items()},
         "schedules": schedules,
         "roofline": roofline,
