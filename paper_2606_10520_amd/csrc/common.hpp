@@ -87,6 +87,11 @@ int launch_gemv(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const vo
 size_t gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype);
 int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x,
                 int x_dtype, void* y, int y_dtype, void* workspace, hipStream_t s);
+// Small-batch kernel (M <= kSkinnyMaxM) on fp16 activations; inv_scale
+// (per token, may be null) multiplies the results.
+constexpr int64_t kSkinnyMaxM = 32;
+hipError_t launch_skinny(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const _Float16* x,
+                         const float* inv_scale, void* y, int y_dtype, hipStream_t s);
 
 // Output store in the requested dtype (fp32 -> fp16 / bf16 round to nearest even).
 __device__ inline void store_out(void* y, int64_t idx, float v, int y_dtype) {

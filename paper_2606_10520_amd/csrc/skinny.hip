@@ -1,0 +1,170 @@
+// Small-batch product y = x * W_hat^T for 4 < M <= 64 tokens on gfx950.
+//
+// Decode dominates nothing here -- the weight stream does -- so the kernel
+// is laid out like the matrix-vector kernel: one workgroup per 16-row block,
+// its wavefronts splitting the block's packets along K in contiguous runs,
+// every packet load a coalesced 16-byte-per-lane read issued well ahead of
+// use, and partial sums meeting once in LDS.  Per group each wavefront
+// decodes its 16 x 128 weight tile on the matrix cores (A q + B exactly in
+// fp32 from the integer codes, Eq. 4; one rounding to fp16) into its own LDS
+// tile and multiplies it with up to 64 tokens on v_mfma_f32_16x16x32_f16
+// (token tiles of 16; activation operands read straight from global memory
+// in the matrix-core layout).  Decoded weights never leave LDS.
+#include "common.hpp"
+#include "decode.hpp"
+
+namespace unisvq {
+namespace {
+
+constexpr int kSRow = kGroup + 8;       // halves per decoded row of a wavefront's tile (16-byte pad)
+constexpr int kSTile = 16 * kSRow;      // halves per wavefront tile (16 rows, one group)
+
+// One group (jj of the piece's packet) of this wavefront's run: decode, read
+// the weight operand back, multiply with the MT token tiles.  xo is the
+// lane's activation offset of the group's first column (or out of range).
+template <int MT>
+__device__ inline void skinny_group(__amdgpu_buffer_rsrc_t rx, uint32_t xo, uint32_t row_step, const Piece& pc,
+                                    int jj, int j, _Float16* wrow, const _Float16* wlane, f32x4 (&acc)[MT]) {
+    f16x8 xa[MT][4];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int s = 0; s < 4; ++s) xa[i][s] = __builtin_bit_cast(f16x8, ld128(rx, xo + i * row_step + 64 * s));
+    DecOps ops;
+    prepare(pc, j, jj, ops);
+    decode_vecs<0>(ops, wrow, j);
+    decode_vecs<1>(ops, wrow, j);
+    decode_vecs<2>(ops, wrow, j);
+    decode_vecs<3>(ops, wrow, j);
+    decode_vecs<4>(ops, wrow, j);
+    decode_vecs<5>(ops, wrow, j);
+    decode_vecs<6>(ops, wrow, j);
+    decode_vecs<7>(ops, wrow, j);
+    f16x8 wb[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) wb[s] = *reinterpret_cast<const f16x8*>(wlane + 32 * s);
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int i = 0; i < MT; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa[i][s], wb[s], acc[i], 0, 0, 0);
+}
+
+// Template parameters: MT token tiles of 16 (M <= 16 MT), WAVES wavefronts
+// per workgroup, PF packets in flight per wavefront.
+template <int MT, int WAVES, int PF>
+__global__ __launch_bounds__(WAVES * 64) void skinny_kernel(const uint8_t* __restrict__ packed,
+                                                           const _Float16* __restrict__ x,
+                                                           const float* __restrict__ inv_scale, void* y, int N,
+                                                           int K, int M, int y_dtype) {
+    __shared__ __attribute__((aligned(16))) _Float16 wtile[WAVES * kSTile];
+    __shared__ float red[WAVES][MT * 16][16];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int rb = blockIdx.x;
+    const int groups = K >> 7;
+    const int nfull = groups >> 1;
+    const bool has_half = (groups & 1) != 0;
+
+    // This wavefront's run of full packets [p0, p0 + np); the last wavefront
+    // also takes the trailing half packet.
+    const int per = (nfull + WAVES - 1) / WAVES;
+    const int p0 = min(nfull, wave * per);
+    const int np = min(nfull, p0 + per) - p0;
+    const bool do_half = has_half && wave == WAVES - 1;
+
+    const __amdgpu_buffer_rsrc_t rw =
+        make_rsrc(packed, static_cast<uint32_t>(N / kRowBlock) * groups * kGroupBlockBytes);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(M) * K * 2u);
+    const uint32_t rowblk = static_cast<uint32_t>(rb) * groups * kGroupBlockBytes;
+    const int gend = 2 * (p0 + np);  // packets at or past this group read nothing
+
+    // Decode role: lane = packet slot (row beta = lane / 4, component j = lane % 4).
+    const int j = lane & 3;
+    _Float16* wrow = wtile + wave * kSTile + (lane >> 2) * kSRow;
+    // Operand roles: weight operand row lane % 16, activation operand token
+    // 16 i + lane % 16, both at columns 8 (lane / 16) + 32 s of the group.
+    const _Float16* wlane = wtile + wave * kSTile + (lane & 15) * kSRow + 8 * (lane >> 4);
+    const uint32_t row_step = 16u * K * 2u;
+    const uint32_t xlane = (static_cast<uint32_t>(lane & 15) * K + 8 * (lane >> 4)) * 2u;
+
+    f32x4 acc[MT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // Packet ring: packet p0 + q lives in ring[q % PF].  Rounds of PF packets
+    // run unconditionally; a packet past the run reads zeros and adds zero.
+    Piece ring[PF];
+#pragma unroll
+    for (int i = 0; i < PF; ++i) load_packet(rw, rowblk, p0 + i, gend, lane, ring[i]);
+    for (int q0 = 0; q0 < np; q0 += PF) {
+#pragma unroll
+        for (int i = 0; i < PF; ++i) {
+            const int q = q0 + i;
+            const uint32_t xo = q < np ? xlane + static_cast<uint32_t>(p0 + q) * 512u : kOutOfRange;
+            skinny_group<MT>(rx, xo, row_step, ring[i], 0, j, wrow, wlane, acc);
+            skinny_group<MT>(rx, q < np ? xo + 256u : kOutOfRange, row_step, ring[i], 1, j, wrow, wlane, acc);
+            load_packet(rw, rowblk, p0 + q + PF, gend, lane, ring[i]);
+        }
+    }
+    if (do_half) {
+        Piece h;
+        load_packet(rw, rowblk, nfull, groups, lane, h);
+        skinny_group<MT>(rx, xlane + static_cast<uint32_t>(nfull) * 512u, row_step, h, 0, j, wrow, wlane, acc);
+    }
+
+    // Partial sums of the wavefronts meet in LDS.  D lane layout: row
+    // lane % 16, tokens 16 i + 4 (lane / 16) + e.
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) red[wave][16 * i + 4 * (lane >> 4) + e][lane & 15] = acc[i][e];
+    __syncthreads();
+    for (int o = threadIdx.x; o < M * 16; o += WAVES * 64) {
+        const int t = o >> 4, r = o & 15;
+        float s = 0.f;
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) s += red[w][t][r];
+        if (inv_scale) s *= inv_scale[t];
+        store_out(y, static_cast<int64_t>(t) * N + static_cast<int64_t>(rb) * kRowBlock + r, s, y_dtype);
+    }
+}
+
+template <int MT, int WAVES, int PF>
+hipError_t launch_cfg(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const _Float16* x,
+                      const float* inv_scale, void* y, int y_dtype, hipStream_t s) {
+    hipLaunchKernelGGL((skinny_kernel<MT, WAVES, PF>), dim3(static_cast<unsigned>(N / kRowBlock)),
+                       dim3(WAVES * 64), 0, s, packed, x, inv_scale, y, static_cast<int>(N),
+                       static_cast<int>(K), static_cast<int>(M), y_dtype);
+    return hipGetLastError();
+}
+
+template <int MT, int WAVES>
+hipError_t launch_pf(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const _Float16* x,
+                     const float* inv_scale, void* y, int y_dtype, hipStream_t s) {
+    // Packets in flight: the whole run when it is short, else 4 or 8.
+    const int64_t packets = K / kGroup / 2;
+    const int64_t per = (packets + WAVES - 1) / WAVES;
+    if (per <= 2) return launch_cfg<MT, WAVES, 2>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
+    if (per <= 4) return launch_cfg<MT, WAVES, 4>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
+    return launch_cfg<MT, WAVES, 8>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
+}
+
+template <int MT>
+hipError_t launch_mt(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const _Float16* x,
+                     const float* inv_scale, void* y, int y_dtype, hipStream_t s) {
+    // Short K: 4 wavefronts; longer K: 8, so that runs stay a few packets long.
+    const int64_t packets = K / kGroup / 2;
+    if (packets <= 16) return launch_pf<MT, 4>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
+    return launch_pf<MT, 8>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
+}
+
+}  // namespace
+
+hipError_t launch_skinny(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const _Float16* x,
+                         const float* inv_scale, void* y, int y_dtype, hipStream_t s) {
+    if (M <= 16) return launch_mt<1>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
+    if (M <= 32) return launch_mt<2>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
+    return launch_mt<4>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
+}
+
+}  // namespace unisvq

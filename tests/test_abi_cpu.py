@@ -130,16 +130,19 @@ def test_gemm_workspace():
     assert ws(15, 128, 1, u.BF16) == 0
     assert ws(16, 128, 0, u.BF16) == 0
     assert ws(16, 128, 1, u.F32) == 0
-    # a small-M product is split along K: fp32 partials for every split
-    split = ws(64, 1024, 4, u.F16)
-    assert split > 0 and split % (4 * 64 * 4) == 0
-    assert ws(64, 1024, 4, u.BF16) == split + 1024 * 4 * 2 + 256
+    # up to 32 tokens the small-batch kernel needs nothing; a 100-token product
+    # with few output tiles is split along K: fp32 partials for every split
+    assert ws(64, 1024, 32, u.F16) == 0
+    assert ws(64, 1024, 33, u.F16) > 0
+    split = ws(64, 1024, 100, u.F16)
+    assert split > 0 and split % (100 * 64 * 4) == 0
+    assert ws(64, 1024, 100, u.BF16) == split + 100 * 1024 * 2 + 512
     # bf16 activations need it; so does a split product with fp16 activations
     need = ws(64, 256, 4, u.BF16)
     assert lib.unisvq_gemm(64, 256, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, None, need, None) == EWS
     assert lib.unisvq_gemm(64, 256, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, GOOD, need - 1, None) == EWS
     assert lib.unisvq_gemm(64, 256, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, GOOD + 8, need, None) == EALIGN
-    assert lib.unisvq_gemm(64, 1024, GOOD, 4, GOOD, u.F16, GOOD, u.F16, None, 0, None) == EWS
+    assert lib.unisvq_gemm(64, 1024, GOOD, 100, GOOD, u.F16, GOOD, u.F16, None, 0, None) == EWS
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
