@@ -42,6 +42,26 @@ __device__ inline uint32_t ld16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
 }
 
+// Streaming variants for data read exactly once (the weight stream of the
+// decode kernels): the non-temporal cache policy keeps it from displacing
+// what is reused (activations, outputs) in L2 and the MALL.
+constexpr int kNonTemporal = 2;
+__device__ inline uint4 ld128_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    const i32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal);
+    return uint4{static_cast<uint32_t>(v.x), static_cast<uint32_t>(v.y), static_cast<uint32_t>(v.z),
+                 static_cast<uint32_t>(v.w)};
+}
+__device__ inline uint2 ld64_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    const i32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kNonTemporal);
+    return uint2{static_cast<uint32_t>(v.x), static_cast<uint32_t>(v.y)};
+}
+__device__ inline uint32_t ld32_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kNonTemporal));
+}
+__device__ inline uint32_t ld16_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, kNonTemporal);
+}
+
 // Largest buffer a 32-bit buffer offset addresses.
 constexpr int64_t kMaxBufferBytes = (int64_t{1} << 31) - 1;
 // A buffer offset past the end of every buffer the kernels address (all are

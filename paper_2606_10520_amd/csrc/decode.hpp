@@ -33,22 +33,24 @@ struct Piece {
 
 // Packet p of a row block: full, half (the last group of an odd count), or
 // nothing at or past group `gend` (the end of the range being decoded; a
-// range ends at a packet boundary or at the last group).
+// range ends at a packet boundary or at the last group).  STREAM selects the
+// non-temporal loads for weights read exactly once.
+template <bool STREAM = false>
 __device__ inline void load_packet(__amdgpu_buffer_rsrc_t rw, uint32_t rowblk, int p, int gend, int lane,
                                    Piece& pc) {
     const bool full = 2 * p + 1 < gend;
     const bool half = 2 * p + 1 == gend;
     const uint32_t P = full || half ? rowblk + static_cast<uint32_t>(p) * kPacketBytes : kOutOfRange;
     if (half) {
-        const uint2 c = ld64(rw, P + 8 * lane);
-        const uint2 a = ld64(rw, P + kHalfAffineOff + 8 * lane);
+        const uint2 c = STREAM ? ld64_stream(rw, P + 8 * lane) : ld64(rw, P + 8 * lane);
+        const uint2 a = STREAM ? ld64_stream(rw, P + kHalfAffineOff + 8 * lane) : ld64(rw, P + kHalfAffineOff + 8 * lane);
         pc.c = uint4{c.x, c.y, 0u, 0u};
         pc.a = uint4{a.x, a.y, 0u, 0u};
-        pc.b = ld16(rw, P + kHalfBiasOff + 2 * lane);
+        pc.b = STREAM ? ld16_stream(rw, P + kHalfBiasOff + 2 * lane) : ld16(rw, P + kHalfBiasOff + 2 * lane);
     } else {
-        pc.c = ld128(rw, P + 16 * lane);
-        pc.a = ld128(rw, P + kPacketAffineOff + 16 * lane);
-        pc.b = ld32(rw, P + kPacketBiasOff + 4 * lane);
+        pc.c = STREAM ? ld128_stream(rw, P + 16 * lane) : ld128(rw, P + 16 * lane);
+        pc.a = STREAM ? ld128_stream(rw, P + kPacketAffineOff + 16 * lane) : ld128(rw, P + kPacketAffineOff + 16 * lane);
+        pc.b = STREAM ? ld32_stream(rw, P + kPacketBiasOff + 4 * lane) : ld32(rw, P + kPacketBiasOff + 4 * lane);
     }
 }
 

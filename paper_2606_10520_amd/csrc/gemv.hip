@@ -316,9 +316,9 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
 #pragma unroll
     for (int i = 0; i < PF; ++i) {
         const uint32_t off = i < np ? blk + static_cast<uint32_t>(p0 + i) * kPacketBytes : kOutOfRange;
-        cbuf[i] = ld128(rw, off + 16 * lane);
-        abuf[i] = ld128(rw, off + kPacketAffineOff + 16 * lane);
-        bbuf[i] = ld32(rw, off + kPacketBiasOff + 4 * lane);
+        cbuf[i] = ld128_stream(rw, off + 16 * lane);
+        abuf[i] = ld128_stream(rw, off + kPacketAffineOff + 16 * lane);
+        bbuf[i] = ld32_stream(rw, off + kPacketBiasOff + 4 * lane);
     }
     __builtin_amdgcn_sched_barrier(0);
 
@@ -373,9 +373,9 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
                 const int nxt = i + j + PF;
                 const uint32_t off =
                     nxt < np ? blk + static_cast<uint32_t>(p0 + nxt) * kPacketBytes : kOutOfRange;
-                cbuf[j] = ld128(rw, off + 16 * lane);
-                abuf[j] = ld128(rw, off + kPacketAffineOff + 16 * lane);
-                bbuf[j] = ld32(rw, off + kPacketBiasOff + 4 * lane);
+                cbuf[j] = ld128_stream(rw, off + 16 * lane);
+                abuf[j] = ld128_stream(rw, off + kPacketAffineOff + 16 * lane);
+                bbuf[j] = ld32_stream(rw, off + kPacketBiasOff + 4 * lane);
             }
         }
     }
@@ -383,9 +383,9 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
     // and used here, outside the pipelined part.
     if (do_half) {
         const uint32_t hoff = blk + static_cast<uint32_t>(nfull) * kPacketBytes;
-        const uint2 hc = ld64(rw, hoff + 8 * lane);
-        const uint2 ha = ld64(rw, hoff + kHalfAffineOff + 8 * lane);
-        const uint32_t hb = ld16(rw, hoff + kHalfBiasOff + 2 * lane);
+        const uint2 hc = ld64_stream(rw, hoff + 8 * lane);
+        const uint2 ha = ld64_stream(rw, hoff + kHalfAffineOff + 8 * lane);
+        const uint32_t hb = ld16_stream(rw, hoff + kHalfBiasOff + 2 * lane);
         half_step<XT, MT>(hc, ha, hb, groups - 1, xs, xbar, groups, M, lane, acc, x0);
     }
 

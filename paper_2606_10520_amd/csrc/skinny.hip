@@ -95,7 +95,7 @@ __global__ __launch_bounds__(WAVES * 64) void skinny_kernel(const uint8_t* __res
     // run unconditionally; a packet past the run reads zeros and adds zero.
     Piece ring[PF];
 #pragma unroll
-    for (int i = 0; i < PF; ++i) load_packet(rw, rowblk, p0 + i, gend, lane, ring[i]);
+    for (int i = 0; i < PF; ++i) load_packet<true>(rw, rowblk, p0 + i, gend, lane, ring[i]);
     for (int q0 = 0; q0 < np; q0 += PF) {
 #pragma unroll
         for (int i = 0; i < PF; ++i) {
@@ -103,12 +103,12 @@ __global__ __launch_bounds__(WAVES * 64) void skinny_kernel(const uint8_t* __res
             const uint32_t xo = q < np ? xlane + static_cast<uint32_t>(p0 + q) * 512u : kOutOfRange;
             skinny_group<MT>(rx, xo, row_step, ring[i], 0, j, wrow, wlane, acc);
             skinny_group<MT>(rx, q < np ? xo + 256u : kOutOfRange, row_step, ring[i], 1, j, wrow, wlane, acc);
-            load_packet(rw, rowblk, p0 + q + PF, gend, lane, ring[i]);
+            load_packet<true>(rw, rowblk, p0 + q + PF, gend, lane, ring[i]);
         }
     }
     if (do_half) {
         Piece h;
-        load_packet(rw, rowblk, nfull, groups, lane, h);
+        load_packet<true>(rw, rowblk, nfull, groups, lane, h);
         skinny_group<MT>(rx, xlane + static_cast<uint32_t>(nfull) * 512u, row_step, h, 0, j, wrow, wlane, acc);
     }
 
