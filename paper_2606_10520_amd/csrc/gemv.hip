@@ -437,12 +437,15 @@ struct GemvPlan {
     int waves, pf, nx;
 };
 
-GemvPlan plan_gemv(int64_t blocks, int max_groups, int M) {
+GemvPlan plan_gemv(int64_t blocks, int min_groups, int max_groups, int M) {
     const int packets = max_groups / 2;
-    // Short K: few wavefronts, whole run prefetched.  Long K: more wavefronts
-    // so that every wavefront keeps several packets in flight.
+    // Short K (in every problem of the batch): 4 wavefronts, whole run
+    // prefetched.  Longer K: 8 wavefronts, or 16 when there are at most 256
+    // workgroups (one per CU), so that the CU still holds enough loads in
+    // flight.  (Measured per shape on MI355X; 16 is slower once there are
+    // several workgroups per CU.)
     GemvPlan p;
-    p.waves = packets <= 16 ? 4 : (packets <= 48 ? 8 : 16);
+    p.waves = min_groups / 2 <= 16 ? 4 : (blocks <= 256 ? 16 : 8);
     if (M > 1 && p.waves > 8) p.waves = 8;  // register budget of 1024-thread groups
     while (p.waves > 4 && blocks * p.waves > 16384) p.waves /= 2;
     const int per = (packets + p.waves - 1) / p.waves;
@@ -467,18 +470,18 @@ int launch_pf(const GemvBatch& b, int blocks, int maxK, const GemvPlan& p, hipSt
 }
 
 template <typename XT, int MT>
-int launch_waves(const GemvBatch& b, int blocks, int maxK, hipStream_t s) {
-    const GemvPlan p = plan_gemv(blocks, maxK / kGroup, b.M);
+int launch_waves(const GemvBatch& b, int blocks, int minK, int maxK, hipStream_t s) {
+    const GemvPlan p = plan_gemv(blocks, minK / kGroup, maxK / kGroup, b.M);
     if (p.waves == 4) return launch_pf<XT, 4, MT>(b, blocks, maxK, p, s);
     if (MT == 1 && p.waves == 16) return launch_pf<XT, 16, 1>(b, blocks, maxK, p, s);
     return launch_pf<XT, 8, MT>(b, blocks, maxK, p, s);
 }
 
 template <typename XT>
-int launch_tokens(const GemvBatch& b, int blocks, int maxK, hipStream_t s) {
-    if (b.M == 1) return launch_waves<XT, 1>(b, blocks, maxK, s);
-    if (b.M == 2) return launch_waves<XT, 2>(b, blocks, maxK, s);
-    return launch_waves<XT, 4>(b, blocks, maxK, s);
+int launch_tokens(const GemvBatch& b, int blocks, int minK, int maxK, hipStream_t s) {
+    if (b.M == 1) return launch_waves<XT, 1>(b, blocks, minK, maxK, s);
+    if (b.M == 2) return launch_waves<XT, 2>(b, blocks, minK, maxK, s);
+    return launch_waves<XT, 4>(b, blocks, minK, maxK, s);
 }
 
 }  // namespace
@@ -498,9 +501,8 @@ int launch_gemv_batch(const GemvProblem* probs, int count, int64_t M, int x_dtyp
     b.count = count;
     b.M = static_cast<int>(M);
     b.y_dtype = y_dtype;
-    (void)minK;
-    if (x_dtype == UNISVQ_F16) return launch_tokens<_Float16>(b, blocks, maxK, s);
-    return launch_tokens<__bf16>(b, blocks, maxK, s);
+    if (x_dtype == UNISVQ_F16) return launch_tokens<_Float16>(b, blocks, minK, maxK, s);
+    return launch_tokens<__bf16>(b, blocks, minK, maxK, s);
 }
 
 int launch_gemv(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x, int x_dtype,
