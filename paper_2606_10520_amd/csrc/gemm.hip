@@ -33,7 +33,7 @@ constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kNI = 8;                // 16-row output tiles per wavefront
 constexpr int kBN = 16 * kNI;         // output rows per workgroup
-constexpr int kLdsRow = kGroup + 8;   // halves per decoded row in LDS (16-byte pad)
+constexpr int kLdsRow = kGroup + 16;  // halves per decoded row in LDS (32-byte pad: no bank conflicts)
 constexpr int kWBuf = kBN * kLdsRow;  // halves per decoded-weight buffer
 
 // One 32-column step of the tile product: MI x kNI matrix-core tiles.
@@ -303,7 +303,7 @@ __global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restr
     if (threadIdx.x == 0) inv_scale[t] = ldexpf(1.0f, -s);
 }
 
-// Tiling of one product: token tiles of 64 (M <= 128) or 256 tokens, row
+// Tiling of one product: token tiles of 64 (M <= 64) or 128 tokens, row
 // tiles of 128; when that leaves fewer than 256 workgroups the K range is
 // split (at packet boundaries) until there are about 256.
 struct GemmPlan {
@@ -312,7 +312,7 @@ struct GemmPlan {
 
 GemmPlan plan_gemm(int64_t N, int64_t K, int64_t M) {
     GemmPlan p;
-    p.mi = M > 128 ? 4 : 1;
+    p.mi = M > 64 ? 2 : 1;
     const int64_t bm = kWaves * 16 * p.mi;
     p.m_tiles = static_cast<int>((M + bm - 1) / bm);
     p.n_tiles = static_cast<int>((N + kBN - 1) / kBN);
@@ -390,7 +390,7 @@ int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const vo
         const float* is = inv ? inv + m0 : nullptr;
         void* ys = static_cast<uint8_t*>(y) + m0 * N * (y_dtype == UNISVQ_F32 ? 4 : 2);
         const GemmPlan p = plan_gemm(N, K, mc);
-        const hipError_t e = p.mi == 4 ? launch_tiles<4>(p, N, K, packed, mc, xs, is, ys, y_dtype, partial, s)
+        const hipError_t e = p.mi == 2 ? launch_tiles<2>(p, N, K, packed, mc, xs, is, ys, y_dtype, partial, s)
                                        : launch_tiles<1>(p, N, K, packed, mc, xs, is, ys, y_dtype, partial, s);
         if (e != hipSuccess) return UNISVQ_EHIP;
     }

@@ -16,7 +16,7 @@
 namespace unisvq {
 namespace {
 
-constexpr int kSRow = kGroup + 8;       // halves per decoded row of a wavefront's tile (16-byte pad)
+constexpr int kSRow = kGroup + 16;      // halves per decoded row of a wavefront's tile (32-byte pad)
 constexpr int kSTile = 16 * kSRow;      // halves per wavefront tile (16 rows, one group)
 
 // One group (jj of the piece's packet) of this wavefront's run: decode, read
