@@ -26,6 +26,8 @@ HIPCC_FLAGS = [
 # about a fifth of the instruction slots moving them.
 EXTRA_FLAGS = {
     "gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "skinny.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "gemv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
 
 
