@@ -342,6 +342,7 @@ template <int MI>
 hipError_t launch_tiles(const GemmPlan& p, int64_t N, int64_t K, const uint8_t* packed, int64_t M,
                         const _Float16* x, const float* inv_scale, void* y, int y_dtype, float* partial,
                         hipStream_t s) {
+    if (p.splits > 1 && partial == nullptr) return hipErrorInvalidValue;  // never launch without the partials
     const unsigned blocks = static_cast<unsigned>(p.m_tiles) * p.n_tiles * p.splits;
     hipLaunchKernelGGL(gemm_kernel<MI>, dim3(blocks), dim3(kThreads), 0, s, packed, x, inv_scale, y,
                        static_cast<int>(N), static_cast<int>(K), static_cast<int>(M), y_dtype, p.m_tiles,
@@ -382,14 +383,22 @@ int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const vo
     if (M <= kSkinnyMaxM)
         return launch_skinny(N, K, packed, M, xh, inv, y, y_dtype, s) == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
     float* partial = reinterpret_cast<float*>(ws);
-    // The activation buffer is addressed with 32-bit offsets: slice M.
+    // The activation buffer is addressed with 32-bit offsets: slice M.  The
+    // workspace was sized for the whole product, which has far more than 256
+    // tiles when it needs slicing; so no slice (the last one may be small)
+    // splits K.
     const int64_t max_rows = kMaxBufferBytes / (2 * K) / 256 * 256;
+    const bool sliced = M > max_rows;
     for (int64_t m0 = 0; m0 < M; m0 += max_rows) {
         const int64_t mc = M - m0 < max_rows ? M - m0 : max_rows;
         const _Float16* xs = xh + m0 * K;
         const float* is = inv ? inv + m0 : nullptr;
         void* ys = static_cast<uint8_t*>(y) + m0 * N * (y_dtype == UNISVQ_F32 ? 4 : 2);
-        const GemmPlan p = plan_gemm(N, K, mc);
+        GemmPlan p = plan_gemm(N, K, mc);
+        if (sliced) {
+            p.splits = 1;
+            p.gps = static_cast<int>(K / kGroup);
+        }
         const hipError_t e = p.mi == 2 ? launch_tiles<2>(p, N, K, packed, mc, xs, is, ys, y_dtype, partial, s)
                                        : launch_tiles<1>(p, N, K, packed, mc, xs, is, ys, y_dtype, partial, s);
         if (e != hipSuccess) return UNISVQ_EHIP;

@@ -332,6 +332,43 @@ def test_gemv_rejects_more_than_four_tokens():
     assert e.value.status == -3
 
 
+def test_gemv_rejects_activations_beyond_lds():
+    """The matrix-vector kernel stages all of x in LDS: 4 tokens x 32768
+    columns do not fit, and the call fails before any launch."""
+    pk = torch.zeros(u.packed_bytes(64, 32768), dtype=torch.uint8, device=DEV)
+    x = torch.zeros((4, 32768), dtype=torch.float16, device=DEV)
+    with pytest.raises(u.UniSVQError) as e:
+        u.gemv(pk, 64, 32768, x)
+    assert e.value.status == -3
+    # the GEMM takes the same product
+    y = u.gemm(pk, 64, 32768, x, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert not torch.any(y)
+
+
+def test_gemm_activations_above_2gib_are_sliced():
+    """x larger than a 32-bit buffer offset reaches (M * K * 2 > 2^31 bytes)
+    is processed in token slices; tokens on both sides of the slice boundary
+    and the last one are checked against the oracle."""
+    N, K, M = 16, 16384, 65600
+    Q, A, B = wl.gen_weights(N, K, seed=50)
+    pk_ref, _ = oracle.pack(Q, A, B)
+    pk = upload_pack(Q, A, B)
+    g = torch.Generator(device=DEV)
+    g.manual_seed(51)
+    x = torch.randn((M, K), generator=g, dtype=torch.float16, device=DEV)
+    assert x.numel() * 2 > 2 ** 31
+    y = u.gemm(pk, N, K, x, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    boundary = (2 ** 31 - 1) // (2 * K) // 256 * 256
+    toks = np.array([0, 1, boundary - 1, boundary, boundary + 1, M - 2, M - 1, 12345])
+    xs = x[torch.from_numpy(toks).to(DEV)].cpu().numpy().view(np.uint16)
+    ref = oracle.matmul(pk_ref, N, K, oracle.half_to_double(xs))
+    got = y[torch.from_numpy(toks).to(DEV)].cpu().numpy()
+    assert rel_err(got, ref) <= 5e-4
+    del x
+
+
 def test_graph_replays_match_eager():
     """The launches are capturable in a HIP graph (no allocation, no memset,
     no synchronisation inside); every replay reproduces the eager result."""
