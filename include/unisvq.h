@@ -172,6 +172,7 @@ size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype)
  * undone on the fp32 result.  When M is small the K range is split across
  * workgroups and a second kernel sums the fp32 partials in a fixed order
  * (results are reproducible run to run).
+ *   BF16 activations need K <= 65536 (UNISVQ_EUNSUP above).
  *   workspace  device, >= unisvq_gemm_workspace_bytes(N, K, M, x_dtype)
  *              bytes, 16-byte aligned (UNISVQ_EWORKSPACE if missing or
  *              smaller, UNISVQ_EALIGN if misaligned); may be NULL when that

@@ -110,6 +110,7 @@ int unisvq_gemm(int64_t N, int64_t K, const void* packed, int64_t M, const void*
                 void* y, int y_dtype, void* workspace, size_t workspace_bytes, void* stream) {
     const int st = check_product(N, K, packed, M, x, x_dtype, y, y_dtype);
     if (st != UNISVQ_OK) return st;
+    if (x_dtype == UNISVQ_BF16 && K > 65536) return UNISVQ_EUNSUP;  // the bf16 pre-pass holds a row in registers
     const size_t need = unisvq::gemm_workspace_bytes(N, K, M, x_dtype);
     if (need) {
         if (!workspace || workspace_bytes < need) return UNISVQ_EWORKSPACE;

@@ -259,7 +259,9 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restr
 }
 
 // bf16 activations -> fp16 with a power-of-two scale per token (see the top
-// of the file).  One workgroup per token row.
+// of the file).  One workgroup per token row; the row is read once and held
+// in registers (CH chunks of 8 values per thread, CH * 2048 >= K).
+template <int CH>
 __global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restrict__ xb, int K,
                                                          _Float16* __restrict__ xh, float* __restrict__ inv_scale) {
     __shared__ float wmax[4];
@@ -268,10 +270,13 @@ __global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restr
     _Float16* out = xh + static_cast<size_t>(t) * K;
     const int chunks = K >> 3;  // 8 values per 16-byte chunk
     auto val = [](uint32_t bits16) { return __builtin_bit_cast(float, bits16 << 16); };
+    uint4 v[CH];
     float mx = 0.f;
-    for (int c = threadIdx.x; c < chunks; c += 256) {
-        const uint4 v = *reinterpret_cast<const uint4*>(row + 8 * c);
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+        const int c = threadIdx.x + 256 * i;
+        v[i] = c < chunks ? *reinterpret_cast<const uint4*>(row + 8 * c) : uint4{0u, 0u, 0u, 0u};
+        const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
 #pragma unroll
         for (int h = 0; h < 4; ++h) {
             mx = fmaxf(mx, fabsf(val(w[h] & 0xffffu)));
@@ -289,9 +294,11 @@ __global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restr
         frexpf(mx, &e);  // mx in [2^(e-1), 2^e)
         s = min(max(15 - e, -126), 126);
     }
-    for (int c = threadIdx.x; c < chunks; c += 256) {
-        const uint4 v = *reinterpret_cast<const uint4*>(row + 8 * c);
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+        const int c = threadIdx.x + 256 * i;
+        if (c >= chunks) break;
+        const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
         f16x8 o;
 #pragma unroll
         for (int h = 0; h < 4; ++h) {
@@ -301,6 +308,19 @@ __global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restr
         *reinterpret_cast<f16x8*>(out + 8 * c) = o;
     }
     if (threadIdx.x == 0) inv_scale[t] = ldexpf(1.0f, -s);
+}
+
+hipError_t launch_scale_rows(int64_t K, int64_t M, const uint16_t* x, _Float16* xh, float* inv, hipStream_t s) {
+    const int64_t per = (K / 8 + 255) / 256;  // chunks per thread
+    const dim3 grid(static_cast<unsigned>(M)), block(256);
+    if (per <= 1) hipLaunchKernelGGL(scale_rows_kernel<1>, grid, block, 0, s, x, static_cast<int>(K), xh, inv);
+    else if (per <= 2) hipLaunchKernelGGL(scale_rows_kernel<2>, grid, block, 0, s, x, static_cast<int>(K), xh, inv);
+    else if (per <= 4) hipLaunchKernelGGL(scale_rows_kernel<4>, grid, block, 0, s, x, static_cast<int>(K), xh, inv);
+    else if (per <= 8) hipLaunchKernelGGL(scale_rows_kernel<8>, grid, block, 0, s, x, static_cast<int>(K), xh, inv);
+    else if (per <= 16) hipLaunchKernelGGL(scale_rows_kernel<16>, grid, block, 0, s, x, static_cast<int>(K), xh, inv);
+    else if (per <= 32) hipLaunchKernelGGL(scale_rows_kernel<32>, grid, block, 0, s, x, static_cast<int>(K), xh, inv);
+    else return hipErrorInvalidValue;  // K > 65536: not supported for bf16 activations
+    return hipGetLastError();
 }
 
 // Tiling of one product: token tiles of 64 (M <= 64) or 128 tokens, row
@@ -374,9 +394,8 @@ int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const vo
         ws += align256(static_cast<size_t>(M) * K * 2);
         float* winv = reinterpret_cast<float*>(ws);
         ws += align256(static_cast<size_t>(M) * 4);
-        hipLaunchKernelGGL(scale_rows_kernel, dim3(static_cast<unsigned>(M)), dim3(256), 0, s,
-                           static_cast<const uint16_t*>(x), static_cast<int>(K), wxh, winv);
-        if (hipGetLastError() != hipSuccess) return UNISVQ_EHIP;
+        if (launch_scale_rows(K, M, static_cast<const uint16_t*>(x), wxh, winv, s) != hipSuccess)
+            return K > 65536 ? UNISVQ_EUNSUP : UNISVQ_EHIP;
         xh = wxh;
         inv = winv;
     }

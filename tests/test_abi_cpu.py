@@ -143,6 +143,8 @@ def test_gemm_workspace():
     assert lib.unisvq_gemm(64, 256, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, GOOD, need - 1, None) == EWS
     assert lib.unisvq_gemm(64, 256, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, GOOD + 8, need, None) == EALIGN
     assert lib.unisvq_gemm(64, 1024, GOOD, 100, GOOD, u.F16, GOOD, u.F16, None, 0, None) == EWS
+    # bf16 activations: K up to 65536
+    assert lib.unisvq_gemm(16, 65664, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, GOOD, 1 << 30, None) == EUNSUP
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
