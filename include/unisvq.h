@@ -121,9 +121,11 @@ int unisvq_unpack(int64_t N, int64_t K, const void* packed, uint8_t* codes, uint
  *   x       device [M][K] row-major, dtype x_dtype (F16 or BF16), 16-byte aligned
  *   y       device [M][N] row-major, dtype y_dtype (F16, BF16 or F32)
  *   M       1..4 tokens (UNISVQ_EUNSUP above that; use unisvq_gemm).  The
- *           kernel stages x in LDS: UNISVQ_EUNSUP also when M * (K / 128) * 272
- *           bytes plus a few KB of working space exceed the 160 KB of LDS
- *           (for M = 4 the limit lies near K = 19000); unisvq_gemm takes any K.
+ *           kernel stages x in LDS: UNISVQ_EUNSUP also when 576 bytes per
+ *           token and 256-column packet, M * ceil(K / 256) * 576, plus up to
+ *           2 KB of working space exceed the 160 KB of LDS (the largest K is
+ *           17920 for M = 4, 36096 for M = 2, 72192 for M = 1);
+ *           unisvq_gemm takes any K.
  * Per (row, group) the kernel contracts the activations with the integer
  * codes on the matrix cores and applies A and B to that small result
  * (the affine map commutes with the product, Sec. 3.1), accumulating in fp32

@@ -12,8 +12,12 @@
 // Matrix-core mapping (v_mfma_f32_4x4x4_16b, 16 independent 4x4x4 blocks):
 //   block beta = lane/4 <-> row 16*rb + beta, column j = lane%4 <-> component b,
 //   k (4 per instruction, 8 instructions per group) <-> vectors of the group.
-//   SrcA = activations x[v][a] -- identical for all 16 blocks, so it is held
-//   only by lanes 0..3 and broadcast to every block (CBSZ = 4, ABID = 0).
+//   SrcA = activations x[v][a] -- identical for all 16 blocks, so one block's
+//   lanes supply it and the broadcast (CBSZ = 4) hands it to every block;
+//   ABID picks the supplying block.  All 16 instructions of a packet (two
+//   groups x 8 steps) therefore take their activation operands from ONE
+//   register pair: lane 4*(8 gi + s) + a holds component a of the four
+//   vectors of step s of group gi, and instruction (gi, s) uses ABID 8 gi + s.
 //   SrcB = codes q[v][b]: lane s of a packet slot already holds component b of
 //   all 32 vectors of its row (packed format v1), converted to exact small
 //   integers with the fp4 (e2m1) converter: a 2-bit code c in the low bits of
@@ -24,13 +28,15 @@
 //
 // Schedule.  One workgroup per 16-row block of one problem (several
 // independent problems may share a launch); its WAVES wavefronts split the
-// block's packets along K into contiguous runs.  Each workgroup first loads
-// its activations, then issues the wavefronts' packet loads, and stages the
-// activations into LDS in operand order -- with the per-group sums xbar
-// formed by DPP row reductions -- while the packet data is still in flight.
-// The main loop consumes packets as they arrive (PF loads in flight per
-// wavefront), running four independent matrix-core chains per packet.
-// Partial row sums meet in LDS at the end.
+// block's packets along K into contiguous runs.  Each wavefront first loads
+// its activations (8 bytes per lane per packet and token: four consecutive
+// vectors per quad), then issues its packet loads, and while those are in
+// flight turns the activations into operand order with a 4x4 transpose
+// inside each quad (DPP), forms the per-group sums xbar with DPP row sums,
+// and parks both in LDS (one 8-byte write per lane per packet).  The main
+// loop consumes packets as they arrive (PF loads in flight per wavefront),
+// one 8-byte LDS read of activations per packet and token, four independent
+// matrix-core chains per packet.  Partial row sums meet in LDS at the end.
 #include <atomic>
 
 #include "common.hpp"
@@ -49,8 +55,15 @@ struct XOps<_Float16> {
     __device__ static inline f16x2 cvt2(uint32_t w) {
         return __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 2.0f, SEL);
     }
+    template <int ABID>
     __device__ static inline f32x4 mfma(vec4 a, vec4 b, f32x4 c) {
-        return __builtin_amdgcn_mfma_f32_4x4x4f16(a, b, c, 4, 0, 0);
+        return __builtin_amdgcn_mfma_f32_4x4x4f16(a, b, c, 4, ABID, 0);
+    }
+    // sum of the four activations of one operand lane, in fp32
+    __device__ static inline float sum4(uint2 w) {
+        const f16x2 one = {static_cast<_Float16>(1.0f), static_cast<_Float16>(1.0f)};
+        const float s = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, w.x), one, 0.0f, false);
+        return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, w.y), one, s, false);
     }
 };
 
@@ -61,8 +74,15 @@ struct XOps<__bf16> {
     __device__ static inline bf16x2 cvt2(uint32_t w) {
         return __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, 2.0f, SEL);
     }
+    template <int ABID>
     __device__ static inline f32x4 mfma(vec4 a, vec4 b, f32x4 c) {
-        return __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(a, b, c, 4, 0, 0);
+        return __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(a, b, c, 4, ABID, 0);
+    }
+    // sum of the four activations of one operand lane, in fp32 (a bf16 value
+    // is the upper half of its fp32 value)
+    __device__ static inline float sum4(uint2 w) {
+        return (__builtin_bit_cast(float, w.x << 16) + __builtin_bit_cast(float, w.x & 0xffff0000u)) +
+               (__builtin_bit_cast(float, w.y << 16) + __builtin_bit_cast(float, w.y & 0xffff0000u));
     }
 };
 
@@ -87,13 +107,6 @@ __device__ inline void word_operands(uint32_t w, typename XOps<XT>::vec4* ops) {
     ops[3] = code_operand<XT, 3>(e, o);
 }
 
-// Position of vector v (0..31 in its group) inside the 32-slot operand
-// order of one (token, group, component) line of the staged activations.
-__device__ inline int operand_slot(int v) {
-    const int j = v & 3;
-    return (v & ~3) | ((j & 1) << 1) | (j >> 1);
-}
-
 __device__ inline float h2f(uint32_t bits16) {
     return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(bits16)));
 }
@@ -104,21 +117,41 @@ __device__ inline float dpp(float v) {
                                                                  0xf, 0xf, true));
 }
 
-// Inclusive sum over the 16 lanes of a DPP row; lane 15 of the row ends
-// with the row total.
-__device__ inline float row16_sum_to_last(float v) {
-    v += dpp<0x111>(v);  // row_shr:1
-    v += dpp<0x112>(v);  // row_shr:2
-    v += dpp<0x114>(v);  // row_shr:4
-    v += dpp<0x118>(v);  // row_shr:8
-    return v;
-}
-
 // Sum over the 4 lanes of a quad, result in every lane of the quad.
 __device__ inline float quad_sum(float v) {
     v += dpp<0xB1>(v);  // quad_perm [1,0,3,2]
     v += dpp<0x4E>(v);  // quad_perm [2,3,0,1]
     return v;
+}
+
+template <int CTRL>
+__device__ inline uint32_t dpp_u32(uint32_t v) {
+    return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), CTRL, 0xf, 0xf, false));
+}
+
+// 4 x 4 transpose of 16-bit elements inside each quad: lane i holds row i
+// (elements 0, 1 in w.x, 2, 3 in w.y); afterwards lane a holds column a
+// (rows 0, 1 in .x, rows 2, 3 in .y).  Two steps: swap the off-diagonal
+// 2 x 2 blocks between lanes i and i ^ 2, then transpose each 2 x 2 block
+// between lanes i and i ^ 1.
+__device__ inline uint2 quad_transpose16(uint2 w, int i) {
+    const bool upper = (i & 2) == 0;
+    const uint32_t t = dpp_u32<0x4E>(upper ? w.y : w.x);  // quad_perm [2,3,0,1]
+    const uint32_t f0 = upper ? w.x : t;
+    const uint32_t f1 = upper ? t : w.y;
+    const uint32_t u0 = dpp_u32<0xB1>(f0);  // quad_perm [1,0,3,2]
+    const uint32_t u1 = dpp_u32<0xB1>(f1);
+    // even lane: (own low half, partner's low half); odd lane: (partner's
+    // high half, own high half)
+    const uint32_t sel = (i & 1) ? 0x03020706u : 0x05040100u;
+    return uint2{__builtin_amdgcn_perm(u0, f0, sel), __builtin_amdgcn_perm(u1, f1, sel)};
+}
+
+// Lane l of a wavefront loads the 4 activations of vector swz(l) of a packet
+// (swz swaps the two low bits: the e2m1 converter delivers a word's codes in
+// the vector order 0, 2, 1, 3 of each step).
+__device__ inline uint32_t operand_vector(int lane) {
+    return static_cast<uint32_t>((lane & ~3) | ((lane & 1) << 1) | ((lane >> 1) & 1));
 }
 
 }  // namespace
@@ -132,32 +165,29 @@ struct GemvBatch {
 
 namespace {
 
+// Activation operands of one (token, packet) in LDS: 64 lanes x 8 bytes, in
+// the operand order of the broadcast A operand.  The per-group sums xbar are
+// kept as the four DPP row sums of the packet, [component][row]: rows 0, 1
+// belong to group 2P, rows 2, 3 to group 2P + 1.
+constexpr int kXsPacketBytes = 64 * 8;
+constexpr int kXbarPacketBytes = 16 * 4;
 
-// One 16-byte activation chunk: vectors 2*q16 and 2*q16+1 of group g, token t.
+// One loaded activation word (lane's vector of packet P, token t) -> operand
+// order in LDS, plus the per-group sums.
 template <typename XT>
-__device__ inline void stage_chunk(const uint4& raw, int t, int g, int q16, int groups, XT* xs, float* xbar) {
-    const int vbase = 2 * q16;
-    uint16_t* line = reinterpret_cast<uint16_t*>(xs) + (static_cast<size_t>(t) * groups + g) * 128;
-    const uint16_t* v16 = reinterpret_cast<const uint16_t*>(&raw);
-    float part[4];
-#pragma unroll
-    for (int a = 0; a < 4; ++a) {
-        line[a * 32 + operand_slot(vbase)] = v16[a];
-        line[a * 32 + operand_slot(vbase + 1)] = v16[4 + a];
-        part[a] = static_cast<float>(__builtin_bit_cast(XT, v16[a])) +
-                  static_cast<float>(__builtin_bit_cast(XT, v16[4 + a]));
-    }
-    // The 16 lanes of a DPP row hold the 16 chunks of one group.
-#pragma unroll
-    for (int a = 0; a < 4; ++a) part[a] = row16_sum_to_last(part[a]);
-    if (q16 == 15) {
-        float* xb = xbar + (static_cast<size_t>(t) * groups + g) * 4;
-#pragma unroll
-        for (int a = 0; a < 4; ++a) xb[a] = part[a];
-    }
+__device__ inline void stage_packet(uint2 raw, int t, int P, int packets, int lane, uint2* xs, float* xbar) {
+    const uint2 op = quad_transpose16(raw, lane & 3);
+    const size_t tp = static_cast<size_t>(t) * packets + P;
+    xs[tp * 64 + lane] = op;
+    // lane 4*(8 gi + s) + a holds component a of the 4 vectors of step s;
+    // the 4 steps of one DPP row sum up in its lanes 12..15
+    float v = XOps<XT>::sum4(op);
+    v += dpp<0x114>(v);  // row_shr:4
+    v += dpp<0x118>(v);  // row_shr:8
+    if ((lane & 15) >= 12) xbar[tp * 16 + (lane & 3) * 4 + (lane >> 4)] = v;
 }
 
-template <typename XT, int MT>
+template <typename XT>
 __device__ inline void epilogue(const f32x4& d, uint32_t a01, uint32_t a23, uint32_t bbits, float xb,
                                 float& acc) {
     float r = acc;
@@ -168,14 +198,28 @@ __device__ inline void epilogue(const f32x4& d, uint32_t a01, uint32_t a23, uint
     acc = __builtin_fmaf(h2f(bbits), xb, r);
 }
 
-// One full packet: groups g and g+1 of the row block, both contracted with
-// interleaved, independent matrix-core chains.
-// x0 / x1 hold the activation operand; only lanes 0..3 are ever written
-// (the other lanes keep zeros -- the broadcast ignores them).
+// Steps S, S+1 of both groups of a packet: four independent chains.
+template <typename XT, int S>
+__device__ inline void chain_steps(typename XOps<XT>::vec4 xo, const typename XOps<XT>::vec4 (&c0)[8],
+                                   const typename XOps<XT>::vec4 (&c1)[8], f32x4& d0a, f32x4& d0b, f32x4& d1a,
+                                   f32x4& d1b) {
+    d0a = XOps<XT>::template mfma<S>(xo, c0[S], d0a);
+    d1a = XOps<XT>::template mfma<8 + S>(xo, c1[S], d1a);
+    d0b = XOps<XT>::template mfma<S + 1>(xo, c0[S + 1], d0b);
+    d1b = XOps<XT>::template mfma<9 + S>(xo, c1[S + 1], d1b);
+}
+
+template <typename XT, int S>
+__device__ inline void chain_steps_half(typename XOps<XT>::vec4 xo, const typename XOps<XT>::vec4 (&c0)[8],
+                                        f32x4& da, f32x4& db) {
+    da = XOps<XT>::template mfma<S>(xo, c0[S], da);
+    db = XOps<XT>::template mfma<S + 1>(xo, c0[S + 1], db);
+}
+
+// One full packet P: groups 2P and 2P+1 of the row block.
 template <typename XT, int MT>
-__device__ inline void packet_step(const uint4& c, const uint4& a, uint32_t bw, int g, const XT* xs,
-                                   const float* xbar, int groups, int M, int lane, float (&acc)[MT],
-                                   typename XOps<XT>::vec4 (&x0)[8], typename XOps<XT>::vec4 (&x1)[8]) {
+__device__ inline void packet_step(const uint4& c, const uint4& a, uint32_t bw, int P, const uint2* xs,
+                                   const float* xbar, int packets, int M, int lane, float (&acc)[MT]) {
     typedef typename XOps<XT>::vec4 vec4;
     vec4 cop0[8], cop1[8];
     word_operands<XT>(c.x, cop0);
@@ -185,32 +229,25 @@ __device__ inline void packet_step(const uint4& c, const uint4& a, uint32_t bw, 
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
         if (t < M) {
-            if (lane < 4) {
-                const vec4* s0 = reinterpret_cast<const vec4*>(xs + ((static_cast<size_t>(t) * groups + g) * 4 + lane) * 32);
-                const vec4* s1 = s0 + 32;  // next group: 128 elements further
-#pragma unroll
-                for (int s = 0; s < 8; ++s) { x0[s] = s0[s]; x1[s] = s1[s]; }
-            }
+            const size_t tp = static_cast<size_t>(t) * packets + P;
+            const vec4 xo = __builtin_bit_cast(vec4, xs[tp * 64 + lane]);
+            const f32x4 xb = *reinterpret_cast<const f32x4*>(xbar + tp * 16 + (lane & 3) * 4);
             f32x4 d0a = {0.f, 0.f, 0.f, 0.f}, d0b = d0a, d1a = d0a, d1b = d0a;
-#pragma unroll
-            for (int s = 0; s < 8; s += 2) {
-                d0a = XOps<XT>::mfma(x0[s], cop0[s], d0a);
-                d1a = XOps<XT>::mfma(x1[s], cop1[s], d1a);
-                d0b = XOps<XT>::mfma(x0[s + 1], cop0[s + 1], d0b);
-                d1b = XOps<XT>::mfma(x1[s + 1], cop1[s + 1], d1b);
-            }
-            const float* xb = xbar + (static_cast<size_t>(t) * groups + g) * 4 + (lane & 3);
-            epilogue<XT, MT>(d0a + d0b, a.x, a.y, bw & 0xffffu, xb[0], acc[t]);
-            epilogue<XT, MT>(d1a + d1b, a.z, a.w, bw >> 16, xb[4], acc[t]);
+            chain_steps<XT, 0>(xo, cop0, cop1, d0a, d0b, d1a, d1b);
+            chain_steps<XT, 2>(xo, cop0, cop1, d0a, d0b, d1a, d1b);
+            chain_steps<XT, 4>(xo, cop0, cop1, d0a, d0b, d1a, d1b);
+            chain_steps<XT, 6>(xo, cop0, cop1, d0a, d0b, d1a, d1b);
+            epilogue<XT>(d0a + d0b, a.x, a.y, bw & 0xffffu, xb[0] + xb[1], acc[t]);
+            epilogue<XT>(d1a + d1b, a.z, a.w, bw >> 16, xb[2] + xb[3], acc[t]);
         }
     }
 }
 
-// The last group of a row block when the group count is odd.
+// The last group of a row block when the group count is odd (packet P,
+// first group only).
 template <typename XT, int MT>
-__device__ inline void half_step(const uint2& c, const uint2& a, uint32_t bbits, int g, const XT* xs,
-                                 const float* xbar, int groups, int M, int lane, float (&acc)[MT],
-                                 typename XOps<XT>::vec4 (&x0)[8]) {
+__device__ inline void half_step(const uint2& c, const uint2& a, uint32_t bbits, int P, const uint2* xs,
+                                 const float* xbar, int packets, int M, int lane, float (&acc)[MT]) {
     typedef typename XOps<XT>::vec4 vec4;
     vec4 cop[8];
     word_operands<XT>(c.x, cop);
@@ -218,19 +255,15 @@ __device__ inline void half_step(const uint2& c, const uint2& a, uint32_t bbits,
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
         if (t < M) {
-            if (lane < 4) {
-                const vec4* s0 = reinterpret_cast<const vec4*>(xs + ((static_cast<size_t>(t) * groups + g) * 4 + lane) * 32);
-#pragma unroll
-                for (int s = 0; s < 8; ++s) x0[s] = s0[s];
-            }
+            const size_t tp = static_cast<size_t>(t) * packets + P;
+            const vec4 xo = __builtin_bit_cast(vec4, xs[tp * 64 + lane]);
+            const f32x4 xb = *reinterpret_cast<const f32x4*>(xbar + tp * 16 + (lane & 3) * 4);
             f32x4 da = {0.f, 0.f, 0.f, 0.f}, db = da;
-#pragma unroll
-            for (int s = 0; s < 8; s += 2) {
-                da = XOps<XT>::mfma(x0[s], cop[s], da);
-                db = XOps<XT>::mfma(x0[s + 1], cop[s + 1], db);
-            }
-            const float xb = xbar[(static_cast<size_t>(t) * groups + g) * 4 + (lane & 3)];
-            epilogue<XT, MT>(da + db, a.x, a.y, bbits, xb, acc[t]);
+            chain_steps_half<XT, 0>(xo, cop, da, db);
+            chain_steps_half<XT, 2>(xo, cop, da, db);
+            chain_steps_half<XT, 4>(xo, cop, da, db);
+            chain_steps_half<XT, 6>(xo, cop, da, db);
+            epilogue<XT>(da + db, a.x, a.y, bbits, xb[0] + xb[1], acc[t]);
         }
     }
 }
@@ -242,7 +275,6 @@ __device__ inline void half_step(const uint2& c, const uint2& a, uint32_t bbits,
 template <typename XT, int WAVES, int MT, int PF, int NX, int OCC>
 __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch batch) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-    constexpr int kThreads = WAVES * 64;
 
     // problem of this workgroup (uniform scalar selection)
     const int bid = blockIdx.x;
@@ -263,48 +295,47 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
     }
     const int M = batch.M;
     const int rb = bid - rb0;
-    (void)kThreads;
     const int groups = K >> 7;
     const int nfull = groups >> 1;
     const bool has_half = (groups & 1) != 0;
+    const int packets = nfull + (has_half ? 1 : 0);  // the half packet counts as one
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
 
-    XT* xs = reinterpret_cast<XT*>(smem);                                                   // [M][groups][4][32]
-    float* xbar = reinterpret_cast<float*>(smem + static_cast<size_t>(M) * groups * 256);  // [M][groups][4]
-    float* red = xbar + M * groups * 4;                                                     // [WAVES][MT][16]
+    uint2* xs = reinterpret_cast<uint2*>(smem);                                                    // [M][packets][64]
+    float* xbar = reinterpret_cast<float*>(smem + static_cast<size_t>(M) * packets * kXsPacketBytes);  // [M][packets][4][4]
+    float* red = xbar + static_cast<size_t>(M) * packets * 16;                                     // [WAVES][MT][16]
 
-    // This wavefront's run: full packets [p0, p0 + np), i.e. groups
-    // [2 p0, 2 (p0 + np)), plus the trailing half packet for the last wavefront.
+    // This wavefront's run: full packets [p0, p0 + np), plus the trailing
+    // half packet (packet nfull) for the last wavefront.
     const int per = (nfull + WAVES - 1) / WAVES;
     const int p0 = min(nfull, wave * per);
     const int np = min(nfull, p0 + per) - p0;
     const bool do_half = has_half && wave == WAVES - 1;
-    const int g0 = 2 * p0;
-    const int ngw = 2 * np + (do_half ? 1 : 0);  // groups this wavefront reads
-    const int gbeg = do_half && np == 0 ? groups - 1 : g0;
+    const int npw = np + (do_half ? 1 : 0);  // packets whose activations this wavefront stages
+    const int pbeg = do_half && np == 0 ? nfull : p0;
 
-    // 1. Activation loads for exactly this wavefront's groups, before the
-    //    packet loads so that staging them waits for nothing else.  Each
-    //    16-byte chunk holds two vectors; 16 consecutive lanes (a DPP row)
-    //    hold one group of one token.  Loads stay outside any branch (a branch
-    //    around a load makes the wait counters drain completely at the join);
-    //    an unneeded load gets an offset past the end of the buffer and returns
-    //    zeros without touching memory.
-    const int chunks_w = M * 16 * ngw;
-    const int nxi = (chunks_w + 63) >> 6;  // load instructions needed (wave-uniform)
+    // 1. Activation loads for exactly this wavefront's packets, before the
+    //    packet loads so that staging them waits for nothing else.  Load c
+    //    covers token c / npw, packet pbeg + c % npw; lane l reads vector
+    //    operand_vector(l) of the packet.  Loads stay outside any branch (a
+    //    branch around a load makes the wait counters drain completely at the
+    //    join); an unneeded load, and the second group of the half packet, get
+    //    an offset past the end of the buffer and return zeros without
+    //    touching memory.
+    const int loads_w = M * npw;
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(M) * K * 2u);
-    auto chunk_off = [&](int c) -> uint32_t {  // byte offset of local chunk c in x
-        const int t = MT == 1 ? 0 : c / (16 * ngw);
-        const int lc = c - t * 16 * ngw;
-        return (static_cast<uint32_t>(t) * K + static_cast<uint32_t>(gbeg) * 128 + lc * 8) * 2u;
+    const uint32_t vlane = operand_vector(lane);
+    auto x_off = [&](int c) -> uint32_t {
+        const int t = MT == 1 || npw == 0 ? 0 : c / npw;
+        const int P = pbeg + (c - t * npw);
+        const uint32_t k = static_cast<uint32_t>(P) * 256u + 4u * vlane;
+        return c < loads_w && k < static_cast<uint32_t>(K) ? (static_cast<uint32_t>(t) * K + k) * 2u
+                                                           : kOutOfRange;
     };
-    uint4 xr[NX];
+    uint2 xr[NX];
 #pragma unroll
-    for (int i = 0; i < NX; ++i) {
-        const int c = 64 * i + lane;
-        xr[i] = ld128(rx, c < chunks_w ? chunk_off(c) : kOutOfRange);
-    }
+    for (int i = 0; i < NX; ++i) xr[i] = ld64(rx, x_off(i));
     __builtin_amdgcn_sched_barrier(0);  // keep the activation loads ahead of the packet loads
 
     // 2. The first PF packets of this wavefront's run.
@@ -323,26 +354,18 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
     __builtin_amdgcn_sched_barrier(0);
 
     // 3. Stage this wavefront's activations in operand order, with the
-    //    per-(token, group, component) sums.  Only this wavefront reads them,
-    //    so no workgroup barrier is needed -- LDS accesses of one wavefront
-    //    complete in order.
+    //    per-group sums.  Only this wavefront reads them, so no workgroup
+    //    barrier is needed -- LDS accesses of one wavefront complete in order.
 #pragma unroll
     for (int i = 0; i < NX; ++i) {
-        const int c = 64 * i + lane;
-        if (c < chunks_w) {
-            const int t = MT == 1 ? 0 : c / (16 * ngw);
-            const int lc = c - t * 16 * ngw;
-            stage_chunk<XT>(xr[i], t, gbeg + (lc >> 4), lc & 15, groups, xs, xbar);
+        if (i < loads_w) {
+            const int t = MT == 1 ? 0 : i / npw;
+            stage_packet<XT>(xr[i], t, pbeg + (i - t * npw), packets, lane, xs, xbar);
         }
     }
-    for (int i = NX; i < nxi; ++i) {  // more than NX instructions: not overlapped with the packets
-        const int c = 64 * i + lane;
-        const uint4 raw = ld128(rx, c < chunks_w ? chunk_off(c) : kOutOfRange);
-        if (c < chunks_w) {
-            const int t = MT == 1 ? 0 : c / (16 * ngw);
-            const int lc = c - t * 16 * ngw;
-            stage_chunk<XT>(raw, t, gbeg + (lc >> 4), lc & 15, groups, xs, xbar);
-        }
+    for (int i = NX; i < loads_w; ++i) {  // more than NX loads: not overlapped with the packets
+        const int t = MT == 1 ? 0 : i / npw;
+        stage_packet<XT>(ld64(rx, x_off(i)), t, pbeg + (i - t * npw), packets, lane, xs, xbar);
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -354,22 +377,17 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
     float acc[MT];
 #pragma unroll
     for (int t = 0; t < MT; ++t) acc[t] = 0.f;
-    typename XOps<XT>::vec4 x0[8], x1[8];
-#pragma unroll
-    for (int s = 0; s < 8; ++s) x0[s] = x1[s] = typename XOps<XT>::vec4{};
     if (np <= PF) {
 #pragma unroll
         for (int j = 0; j < PF; ++j)
             if (j < np)
-                packet_step<XT, MT>(cbuf[j], abuf[j], bbuf[j], 2 * (p0 + j), xs, xbar, groups, M, lane, acc,
-                                    x0, x1);
+                packet_step<XT, MT>(cbuf[j], abuf[j], bbuf[j], p0 + j, xs, xbar, packets, M, lane, acc);
     } else {
         for (int i = 0; i < np; i += PF) {
 #pragma unroll
             for (int j = 0; j < PF; ++j) {
                 if (i + j < np)
-                    packet_step<XT, MT>(cbuf[j], abuf[j], bbuf[j], 2 * (p0 + i + j), xs, xbar, groups, M,
-                                        lane, acc, x0, x1);
+                    packet_step<XT, MT>(cbuf[j], abuf[j], bbuf[j], p0 + i + j, xs, xbar, packets, M, lane, acc);
                 const int nxt = i + j + PF;
                 const uint32_t off =
                     nxt < np ? blk + static_cast<uint32_t>(p0 + nxt) * kPacketBytes : kOutOfRange;
@@ -386,7 +404,7 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
         const uint2 hc = ld64_stream(rw, hoff + 8 * lane);
         const uint2 ha = ld64_stream(rw, hoff + kHalfAffineOff + 8 * lane);
         const uint32_t hb = ld16_stream(rw, hoff + kHalfBiasOff + 2 * lane);
-        half_step<XT, MT>(hc, ha, hb, groups - 1, xs, xbar, groups, M, lane, acc, x0);
+        half_step<XT, MT>(hc, ha, hb, nfull, xs, xbar, packets, M, lane, acc);
     }
 
     // 5. Sum the four component lanes of each row, then the wavefronts.
@@ -409,8 +427,9 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
 constexpr size_t kMaxLds = 160 * 1024;
 
 size_t gemv_lds_bytes(int K, int M, int waves, int mt) {
-    const size_t groups = K / kGroup;
-    return static_cast<size_t>(M) * groups * (256 + 16) + static_cast<size_t>(waves) * mt * 16 * 4;
+    const size_t packets = (K / kGroup + 1) / 2;
+    return static_cast<size_t>(M) * packets * (kXsPacketBytes + kXbarPacketBytes) +
+           static_cast<size_t>(waves) * mt * 16 * 4;
 }
 
 template <typename XT, int WAVES, int MT, int PF, int NX>
@@ -439,20 +458,23 @@ struct GemvPlan {
 
 GemvPlan plan_gemv(int64_t blocks, int min_groups, int max_groups, int M) {
     const int packets = max_groups / 2;
-    // Short K (in every problem of the batch): 4 wavefronts, whole run
-    // prefetched.  Longer K: 8 wavefronts, or 16 when there are at most 256
-    // workgroups (one per CU), so that the CU still holds enough loads in
-    // flight.  (Measured per shape on MI355X; 16 is slower once there are
-    // several workgroups per CU.)
+    // 8 wavefronts per 16-row block; 16 for one token and long K when there
+    // are at most 256 workgroups (one per CU), so that the CU still holds
+    // enough loads in flight.  Two packets in flight per wavefront; four for
+    // one token when even the shortest problem of the batch gives runs of
+    // more than two packets (a longer prefetch is wasted on short runs).
+    // Swept per shape on MI355X: e.g. 4 tokens x 4096 x 4096 6.2 us with 8
+    // wavefronts and 2 in flight, 8.8 us with 4 and 4; one token x 4096 x
+    // 11008 6.8 us with 16 and 4, 7.0 us with 8 and 2; the seven 70B-shaped
+    // products in one launch 72.8 us with 8 and 4, 79.3 us with 4 and 4.
     GemvPlan p;
-    p.waves = min_groups / 2 <= 16 ? 4 : (blocks <= 256 ? 16 : 8);
-    if (M > 1 && p.waves > 8) p.waves = 8;  // register budget of 1024-thread groups
-    while (p.waves > 4 && blocks * p.waves > 16384) p.waves /= 2;
+    p.waves = M == 1 && packets > 16 && blocks <= 256 ? 16 : 8;
     const int per = (packets + p.waves - 1) / p.waves;
-    p.pf = per <= 2 ? 2 : 4;
-    const int chunks = M * 16 * (2 * per + (max_groups & 1));
-    const int nxi = (chunks + 63) / 64;
-    p.nx = nxi <= 1 ? 1 : (nxi <= 2 ? 2 : 4);
+    const int per_min = (min_groups / 2 + p.waves - 1) / p.waves;
+    p.pf = M == 1 && per_min > 2 ? 4 : 2;
+    // one activation load per packet and token (the half packet included)
+    const int loads = M * (per + (max_groups & 1));
+    p.nx = loads <= 1 ? 1 : (loads <= 2 ? 2 : (loads <= 4 ? 4 : 8));
     return p;
 }
 
@@ -460,7 +482,8 @@ template <typename XT, int WAVES, int MT, int PF>
 int launch_nx(const GemvBatch& b, int blocks, int maxK, int nx, hipStream_t s) {
     if (nx == 1) return launch_cfg<XT, WAVES, MT, PF, 1>(b, blocks, maxK, s);
     if (nx == 2) return launch_cfg<XT, WAVES, MT, PF, 2>(b, blocks, maxK, s);
-    return launch_cfg<XT, WAVES, MT, PF, 4>(b, blocks, maxK, s);
+    if (nx == 4) return launch_cfg<XT, WAVES, MT, PF, 4>(b, blocks, maxK, s);
+    return launch_cfg<XT, WAVES, MT, PF, 8>(b, blocks, maxK, s);
 }
 
 template <typename XT, int WAVES, int MT>
@@ -472,7 +495,6 @@ int launch_pf(const GemvBatch& b, int blocks, int maxK, const GemvPlan& p, hipSt
 template <typename XT, int MT>
 int launch_waves(const GemvBatch& b, int blocks, int minK, int maxK, hipStream_t s) {
     const GemvPlan p = plan_gemv(blocks, minK / kGroup, maxK / kGroup, b.M);
-    if (p.waves == 4) return launch_pf<XT, 4, MT>(b, blocks, maxK, p, s);
     if (MT == 1 && p.waves == 16) return launch_pf<XT, 16, 1>(b, blocks, maxK, p, s);
     return launch_pf<XT, 8, MT>(b, blocks, maxK, p, s);
 }

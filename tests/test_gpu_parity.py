@@ -332,18 +332,31 @@ def test_gemv_rejects_more_than_four_tokens():
     assert e.value.status == -3
 
 
-def test_gemv_rejects_activations_beyond_lds():
-    """The matrix-vector kernel stages all of x in LDS: 4 tokens x 32768
-    columns do not fit, and the call fails before any launch."""
-    pk = torch.zeros(u.packed_bytes(64, 32768), dtype=torch.uint8, device=DEV)
-    x = torch.zeros((4, 32768), dtype=torch.float16, device=DEV)
-    with pytest.raises(u.UniSVQError) as e:
-        u.gemv(pk, 64, 32768, x)
-    assert e.value.status == -3
-    # the GEMM takes the same product
-    y = u.gemm(pk, 64, 32768, x, out_dtype=torch.float32)
+@pytest.mark.parametrize("M,K_max", [(4, 17920), (2, 36096), (1, 72192)])
+def test_gemv_lds_limit_boundary(M, K_max):
+    """The matrix-vector kernel stages all of x in LDS (576 bytes per token
+    and 256-column packet): the largest K that fits runs and matches the
+    oracle on sampled rows; the next multiple of 128 fails before any launch,
+    and the GEMM takes that product."""
+    N = 32
+    Q, A, B = wl.gen_weights(N, K_max, seed=5)
+    pk_ref, _ = oracle.pack(Q, A, B)
+    xb = wl.gen_activations(M, K_max, seed=6, dtype="f16")
+    y = u.gemv(upload_pack(Q, A, B), N, K_max, dev_x(xb, "f16"), out_dtype=torch.float32)
     torch.cuda.synchronize()
-    assert not torch.any(y)
+    rows = np.array([0, 17, 31])
+    ref = oracle.matmul(pk_ref, N, K_max, x_as_f64(xb, "f16"), rows=rows)
+    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 1e-5
+
+    K = K_max + 128
+    pk = torch.zeros(u.packed_bytes(N, K), dtype=torch.uint8, device=DEV)
+    xz = torch.zeros((M, K), dtype=torch.float16, device=DEV)
+    with pytest.raises(u.UniSVQError) as e:
+        u.gemv(pk, N, K, xz)
+    assert e.value.status == -3
+    yz = u.gemm(pk, N, K, xz, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert not torch.any(yz)
 
 
 def test_gemm_activations_above_2gib_are_sliced():
