@@ -198,22 +198,19 @@ __device__ inline void epilogue(const f32x4& d, uint32_t a01, uint32_t a23, uint
     acc = __builtin_fmaf(h2f(bbits), xb, r);
 }
 
-// Steps S, S+1 of both groups of a packet: four independent chains.
+// Step S of both groups of a packet: two independent chains (one per
+// group; a dependent matrix-core instruction takes its accumulator straight
+// from the previous one).
 template <typename XT, int S>
-__device__ inline void chain_steps(typename XOps<XT>::vec4 xo, const typename XOps<XT>::vec4 (&c0)[8],
-                                   const typename XOps<XT>::vec4 (&c1)[8], f32x4& d0a, f32x4& d0b, f32x4& d1a,
-                                   f32x4& d1b) {
-    d0a = XOps<XT>::template mfma<S>(xo, c0[S], d0a);
-    d1a = XOps<XT>::template mfma<8 + S>(xo, c1[S], d1a);
-    d0b = XOps<XT>::template mfma<S + 1>(xo, c0[S + 1], d0b);
-    d1b = XOps<XT>::template mfma<9 + S>(xo, c1[S + 1], d1b);
+__device__ inline void chain_step(typename XOps<XT>::vec4 xo, const typename XOps<XT>::vec4 (&c0)[8],
+                                  const typename XOps<XT>::vec4 (&c1)[8], f32x4& d0, f32x4& d1) {
+    d0 = XOps<XT>::template mfma<S>(xo, c0[S], d0);
+    d1 = XOps<XT>::template mfma<8 + S>(xo, c1[S], d1);
 }
 
 template <typename XT, int S>
-__device__ inline void chain_steps_half(typename XOps<XT>::vec4 xo, const typename XOps<XT>::vec4 (&c0)[8],
-                                        f32x4& da, f32x4& db) {
-    da = XOps<XT>::template mfma<S>(xo, c0[S], da);
-    db = XOps<XT>::template mfma<S + 1>(xo, c0[S + 1], db);
+__device__ inline void chain_step_half(typename XOps<XT>::vec4 xo, const typename XOps<XT>::vec4 (&c0)[8], f32x4& d) {
+    d = XOps<XT>::template mfma<S>(xo, c0[S], d);
 }
 
 // One full packet P: groups 2P and 2P+1 of the row block.
@@ -232,13 +229,17 @@ __device__ inline void packet_step(const uint4& c, const uint4& a, uint32_t bw, 
             const size_t tp = static_cast<size_t>(t) * packets + P;
             const vec4 xo = __builtin_bit_cast(vec4, xs[tp * 64 + lane]);
             const f32x4 xb = *reinterpret_cast<const f32x4*>(xbar + tp * 16 + (lane & 3) * 4);
-            f32x4 d0a = {0.f, 0.f, 0.f, 0.f}, d0b = d0a, d1a = d0a, d1b = d0a;
-            chain_steps<XT, 0>(xo, cop0, cop1, d0a, d0b, d1a, d1b);
-            chain_steps<XT, 2>(xo, cop0, cop1, d0a, d0b, d1a, d1b);
-            chain_steps<XT, 4>(xo, cop0, cop1, d0a, d0b, d1a, d1b);
-            chain_steps<XT, 6>(xo, cop0, cop1, d0a, d0b, d1a, d1b);
-            epilogue<XT>(d0a + d0b, a.x, a.y, bw & 0xffffu, xb[0] + xb[1], acc[t]);
-            epilogue<XT>(d1a + d1b, a.z, a.w, bw >> 16, xb[2] + xb[3], acc[t]);
+            f32x4 d0 = {0.f, 0.f, 0.f, 0.f}, d1 = d0;
+            chain_step<XT, 0>(xo, cop0, cop1, d0, d1);
+            chain_step<XT, 1>(xo, cop0, cop1, d0, d1);
+            chain_step<XT, 2>(xo, cop0, cop1, d0, d1);
+            chain_step<XT, 3>(xo, cop0, cop1, d0, d1);
+            chain_step<XT, 4>(xo, cop0, cop1, d0, d1);
+            chain_step<XT, 5>(xo, cop0, cop1, d0, d1);
+            chain_step<XT, 6>(xo, cop0, cop1, d0, d1);
+            chain_step<XT, 7>(xo, cop0, cop1, d0, d1);
+            epilogue<XT>(d0, a.x, a.y, bw & 0xffffu, xb[0] + xb[1], acc[t]);
+            epilogue<XT>(d1, a.z, a.w, bw >> 16, xb[2] + xb[3], acc[t]);
         }
     }
 }
@@ -258,12 +259,16 @@ __device__ inline void half_step(const uint2& c, const uint2& a, uint32_t bbits,
             const size_t tp = static_cast<size_t>(t) * packets + P;
             const vec4 xo = __builtin_bit_cast(vec4, xs[tp * 64 + lane]);
             const f32x4 xb = *reinterpret_cast<const f32x4*>(xbar + tp * 16 + (lane & 3) * 4);
-            f32x4 da = {0.f, 0.f, 0.f, 0.f}, db = da;
-            chain_steps_half<XT, 0>(xo, cop, da, db);
-            chain_steps_half<XT, 2>(xo, cop, da, db);
-            chain_steps_half<XT, 4>(xo, cop, da, db);
-            chain_steps_half<XT, 6>(xo, cop, da, db);
-            epilogue<XT>(da + db, a.x, a.y, bbits, xb[0] + xb[1], acc[t]);
+            f32x4 d = {0.f, 0.f, 0.f, 0.f};
+            chain_step_half<XT, 0>(xo, cop, d);
+            chain_step_half<XT, 1>(xo, cop, d);
+            chain_step_half<XT, 2>(xo, cop, d);
+            chain_step_half<XT, 3>(xo, cop, d);
+            chain_step_half<XT, 4>(xo, cop, d);
+            chain_step_half<XT, 5>(xo, cop, d);
+            chain_step_half<XT, 6>(xo, cop, d);
+            chain_step_half<XT, 7>(xo, cop, d);
+            epilogue<XT>(d, a.x, a.y, bbits, xb[0] + xb[1], acc[t]);
         }
     }
 }
@@ -457,21 +462,23 @@ struct GemvPlan {
 };
 
 GemvPlan plan_gemv(int64_t blocks, int min_groups, int max_groups, int M) {
+    (void)blocks;
     const int packets = max_groups / 2;
-    // 8 wavefronts per 16-row block; 16 for one token and long K when there
-    // are at most 256 workgroups (one per CU), so that the CU still holds
-    // enough loads in flight.  Two packets in flight per wavefront; four for
-    // one token when even the shortest problem of the batch gives runs of
-    // more than two packets (a longer prefetch is wasted on short runs).
-    // Swept per shape on MI355X: e.g. 4 tokens x 4096 x 4096 6.2 us with 8
-    // wavefronts and 2 in flight, 8.8 us with 4 and 4; one token x 4096 x
-    // 11008 6.8 us with 16 and 4, 7.0 us with 8 and 2; the seven 70B-shaped
-    // products in one launch 72.8 us with 8 and 4, 79.3 us with 4 and 4.
+    // 8 wavefronts per 16-row block; 16 for one token when every problem of
+    // the launch has the same, long K (more than 16 packets per row block: a
+    // mix of K sizes leaves the short problems with LDS sized for the long
+    // one).  Two packets in flight per wavefront; four for one token when
+    // the runs are three or four packets long.  Swept per shape on MI355X:
+    // e.g. 4 tokens x 4096 x 4096 6.0 us with 8 wavefronts and 2 in flight,
+    // 8.5 us with 4 and 2; one token x 8192 x 28672 22.2 us with 16 and 2,
+    // 24.6 us with 8 and 4; one token x 4096 x 11008 6.6 us with 16 and 4,
+    // 7.0 us with 16 and 2; the seven 70B-shaped products in one launch
+    // 72.8 us with 8 and 4, 93.8 us with 16 and 2.
     GemvPlan p;
-    p.waves = M == 1 && packets > 16 && blocks <= 256 ? 16 : 8;
+    p.waves = M == 1 && min_groups == max_groups && packets > 16 ? 16 : 8;
     const int per = (packets + p.waves - 1) / p.waves;
     const int per_min = (min_groups / 2 + p.waves - 1) / p.waves;
-    p.pf = M == 1 && per_min > 2 ? 4 : 2;
+    p.pf = M == 1 && per_min > 2 && per_min <= 4 ? 4 : 2;
     // one activation load per packet and token (the half packet included)
     const int loads = M * (per + (max_groups & 1));
     p.nx = loads <= 1 ? 1 : (loads <= 2 ? 2 : (loads <= 4 ? 4 : 8));
