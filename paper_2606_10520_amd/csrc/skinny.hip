@@ -138,24 +138,16 @@ hipError_t launch_cfg(int64_t N, int64_t K, const uint8_t* packed, int64_t M, co
     return hipGetLastError();
 }
 
-template <int MT, int WAVES>
-hipError_t launch_pf(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const _Float16* x,
-                     const float* inv_scale, void* y, int y_dtype, hipStream_t s) {
-    // Packets in flight: the whole run when it is short, else 4 or 8.
-    const int64_t packets = K / kGroup / 2;
-    const int64_t per = (packets + WAVES - 1) / WAVES;
-    if (per <= 2) return launch_cfg<MT, WAVES, 2>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
-    if (per <= 4) return launch_cfg<MT, WAVES, 4>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
-    return launch_cfg<MT, WAVES, 8>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
-}
-
+// 8 wavefronts per 16-row block with 2 packets in flight each, for every
+// shape: swept on MI355X (16 tokens: 4096 x 4096 7.0 us, 4 wavefronts and 4
+// in flight 7.4 us; 4096 x 11008 14.1 us, 8 and 8 18.2 us; deeper prefetch
+// is slower because each activation load then waits behind more packet
+// loads -- the vector-memory counter retires in order).  Two row blocks per
+// workgroup (half the activation reads from L2) gained nothing at 16 tokens.
 template <int MT>
 hipError_t launch_mt(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const _Float16* x,
                      const float* inv_scale, void* y, int y_dtype, hipStream_t s) {
-    // Short K: 4 wavefronts; longer K: 8, so that runs stay a few packets long.
-    const int64_t packets = K / kGroup / 2;
-    if (packets <= 16) return launch_pf<MT, 4>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
-    return launch_pf<MT, 8>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
+    return launch_cfg<MT, 8, 2>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
 }
 
 }  // namespace
@@ -163,8 +155,7 @@ hipError_t launch_mt(int64_t N, int64_t K, const uint8_t* packed, int64_t M, con
 hipError_t launch_skinny(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const _Float16* x,
                          const float* inv_scale, void* y, int y_dtype, hipStream_t s) {
     if (M <= 16) return launch_mt<1>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
-    if (M <= 32) return launch_mt<2>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
-    return launch_mt<4>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
+    return launch_mt<2>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
 }
 
 }  // namespace unisvq
