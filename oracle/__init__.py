@@ -59,6 +59,14 @@ def _load():
     lib.oracle_decode_packed_rows.restype = ctypes.c_int
     lib.oracle_matmul_rows.argtypes = [i64, i64, p, i64, p, i64, p, p, ctypes.c_int]
     lib.oracle_matmul_rows.restype = ctypes.c_int
+    lib.oracle_codes_packed_bytes.argtypes = [i64, i64]
+    lib.oracle_codes_packed_bytes.restype = i64
+    lib.oracle_pack_codes.argtypes = [i64, i64, p, p]
+    lib.oracle_pack_codes.restype = i64
+    lib.oracle_unpack_codes.argtypes = [i64, i64, p, p]
+    lib.oracle_unpack_codes.restype = ctypes.c_int
+    lib.oracle_matmul_shared_rows.argtypes = [i64, i64, p, i64, p, p, i64, p, i64, p, p, ctypes.c_int]
+    lib.oracle_matmul_shared_rows.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -181,4 +189,60 @@ def matmul(packed: np.ndarray, N: int, K: int, X: np.ndarray, rows=None, threads
         Y = np.empty((M, r.size), dtype=np.float64)
         _check(lib.oracle_matmul_rows(N, K, _ptr(packed), M, _ptr(X), r.size, _ptr(r), _ptr(Y),
                                       threads), "matmul_rows")
+    return Y
+
+
+# ------------------------------------------------ row-shared affine parameters
+
+def codes_packed_bytes(N: int, K: int) -> int:
+    """Bytes of the codes-only format: 2 bits per weight, nothing else."""
+    return _check(_load().oracle_codes_packed_bytes(N, K), "codes_packed_bytes")
+
+
+def pack_codes(Q: np.ndarray):
+    """Codes-only packing; returns (packed uint8 bytes, number of codes > 3)."""
+    lib = _load()
+    N, K = Q.shape
+    Q = np.ascontiguousarray(Q, dtype=np.uint8)
+    out = np.empty(codes_packed_bytes(N, K), dtype=np.uint8)
+    bad = _check(lib.oracle_pack_codes(N, K, _ptr(Q), _ptr(out)), "pack_codes")
+    return out, int(bad)
+
+
+def unpack_codes(packed: np.ndarray, N: int, K: int) -> np.ndarray:
+    lib = _load()
+    packed = np.ascontiguousarray(packed, dtype=np.uint8)
+    assert packed.size == codes_packed_bytes(N, K)
+    Q = np.empty((N, K), dtype=np.uint8)
+    _check(lib.oracle_unpack_codes(N, K, _ptr(packed), _ptr(Q)), "unpack_codes")
+    return Q
+
+
+def matmul_shared(packed_codes: np.ndarray, N: int, K: int, As: np.ndarray, Bs: np.ndarray, X: np.ndarray,
+                  rows=None, threads: int | None = None):
+    """Y = X * W_hat^T in fp64 where every row decodes with the shared pairs
+    As [Ga][4][4], Bs [Ga][4] (Ga = 1: one pair for the matrix; Ga = K/128: one
+    per group)."""
+    lib = _load()
+    packed_codes = np.ascontiguousarray(packed_codes, dtype=np.uint8)
+    assert packed_codes.size == codes_packed_bytes(N, K)
+    Ab, Bb = _bits16(As), _bits16(Bs)
+    Ga = Ab.shape[0]
+    assert Ab.shape == (Ga, 4, 4) and Bb.shape == (Ga, 4)
+    X = np.ascontiguousarray(X, dtype=np.float64)
+    if X.ndim == 1:
+        X = X[None, :]
+    M = X.shape[0]
+    assert X.shape[1] == K
+    if threads is None:
+        threads = default_threads()
+    if rows is None:
+        Y = np.empty((M, N), dtype=np.float64)
+        _check(lib.oracle_matmul_shared_rows(N, K, _ptr(packed_codes), Ga, _ptr(Ab), _ptr(Bb), M, _ptr(X), N,
+                                             None, _ptr(Y), threads), "matmul_shared")
+    else:
+        r = np.ascontiguousarray(rows, dtype=np.int64)
+        Y = np.empty((M, r.size), dtype=np.float64)
+        _check(lib.oracle_matmul_shared_rows(N, K, _ptr(packed_codes), Ga, _ptr(Ab), _ptr(Bb), M, _ptr(X),
+                                             r.size, _ptr(r), _ptr(Y), threads), "matmul_shared_rows")
     return Y

@@ -39,6 +39,17 @@
  *   Code field F(r, g, b) is a 64-bit little-endian word whose bits 2v, 2v+1
  *   hold Q[r][128g + 4v + b], v = 0..31.
  *
+ * Codes-only packed format, for affine parameters shared by all rows (the
+ * paper's own setting: one (A, B) per weight matrix, Sec. 3.1 and Sec. 4.2;
+ * or one per 128-column group, shared by the rows):
+ *   Row block rb occupies (K/128)*512 bytes starting at rb*(K/128)*512.
+ *   Packet p (groups 2p, 2p+1) is 1024 bytes: P + 16s + 8j holds F(r, 2p+j, b);
+ *   a final half packet (last group when K/128 is odd) is 512 bytes: P + 8s
+ *   holds F(r, g, b).  Slots and code fields as above.
+ *   Shared parameters: As fp16 [Ga][4][4], Bs fp16 [Ga][4] with Ga = 1 (one
+ *   pair for the matrix) or K/128 (one pair per group); group g uses pair
+ *   (Ga == 1 ? 0 : g).
+ *
  * Canonical (unpacked) arrays:
  *   Q uint8  [N][K]           codes, valid values 0..3
  *   A fp16   [N][K/128][4][4] A[r][g][a][b] multiplies q_b into output a
@@ -199,6 +210,82 @@ int oracle_unpack(int64_t N, int64_t K, const uint8_t* packed, uint8_t* Q, uint1
     return OR_OK;
 }
 
+/* ---- codes-only format (row-shared affine parameters) ---- */
+
+#define OR_CODE_BYTES_PER_BLOCK 512 /* 16 rows * 32 code bytes per group */
+
+int64_t oracle_codes_packed_bytes(int64_t N, int64_t K) {
+    if (!shape_ok(N, K)) return OR_ESHAPE;
+    return (N / OR_ROWBLOCK) * (K / OR_G) * OR_CODE_BYTES_PER_BLOCK;
+}
+
+/* Offset of slot 0's code field of group g of row block rb, and the slot stride. */
+static void place_codes(int64_t K, int64_t rb, int64_t g, int64_t* off, int64_t* stride) {
+    int64_t groups = K / OR_G;
+    int64_t pkt = rb * groups * OR_CODE_BYTES_PER_BLOCK + (g / 2) * 2 * OR_CODE_BYTES_PER_BLOCK;
+    if ((groups % 2 == 1) && (g == groups - 1)) {
+        *off = pkt;
+        *stride = 8;
+    } else {
+        *off = pkt + 8 * (g % 2);
+        *stride = 16;
+    }
+}
+
+int64_t oracle_pack_codes(int64_t N, int64_t K, const uint8_t* Q, uint8_t* out) {
+    if (!Q || !out) return OR_EINVAL;
+    if (!shape_ok(N, K)) return OR_ESHAPE;
+    int64_t groups = K / OR_G, bad = 0;
+    memset(out, 0, (size_t)oracle_codes_packed_bytes(N, K));
+    for (int64_t r = 0; r < N; ++r) {
+        int64_t rb = r / OR_ROWBLOCK, rl = r % OR_ROWBLOCK;
+        for (int64_t g = 0; g < groups; ++g) {
+            int64_t off, stride;
+            place_codes(K, rb, g, &off, &stride);
+            for (int b = 0; b < OR_D; ++b) {
+                uint8_t* field = out + off + (rl * 4 + b) * stride;
+                for (int v = 0; v < 32; ++v) {
+                    uint8_t q = Q[r * K + g * OR_G + 4 * v + b];
+                    if (q > 3) ++bad;
+                    field[(2 * v) / 8] |= (uint8_t)((q & 3) << ((2 * v) % 8));
+                }
+            }
+        }
+    }
+    return bad;
+}
+
+static void unpack_codes_row(int64_t K, const uint8_t* packed, int64_t r, uint8_t* q_row) {
+    int64_t groups = K / OR_G, rb = r / OR_ROWBLOCK, rl = r % OR_ROWBLOCK;
+    for (int64_t g = 0; g < groups; ++g) {
+        int64_t off, stride;
+        place_codes(K, rb, g, &off, &stride);
+        for (int b = 0; b < OR_D; ++b) {
+            const uint8_t* field = packed + off + (rl * 4 + b) * stride;
+            for (int v = 0; v < 32; ++v)
+                q_row[g * OR_G + 4 * v + b] = (uint8_t)((field[(2 * v) / 8] >> ((2 * v) % 8)) & 3);
+        }
+    }
+}
+
+int oracle_unpack_codes(int64_t N, int64_t K, const uint8_t* packed, uint8_t* Q) {
+    if (!packed || !Q) return OR_EINVAL;
+    if (!shape_ok(N, K)) return OR_ESHAPE;
+    for (int64_t r = 0; r < N; ++r) unpack_codes_row(K, packed, r, Q + r * K);
+    return OR_OK;
+}
+
+/* Every row's per-group parameters, replicated from the shared pairs. */
+static void expand_shared(int64_t K, int64_t Ga, const uint16_t* As, const uint16_t* Bs, uint16_t* a_row,
+                          uint16_t* b_row) {
+    int64_t groups = K / OR_G;
+    for (int64_t g = 0; g < groups; ++g) {
+        int64_t src = Ga == 1 ? 0 : g;
+        for (int i = 0; i < 16; ++i) a_row[g * 16 + i] = As[src * 16 + i];
+        for (int i = 0; i < 4; ++i) b_row[g * 4 + i] = Bs[src * 4 + i];
+    }
+}
+
 /* ---- decode (Eq. 4 applied along the input dimension as in Eq. 8) ---- */
 
 /* One row: w[k] for k = 4v + a is sum_b A[g][a][b] * q[4v + b] + B[g][a],
@@ -256,6 +343,8 @@ typedef struct {
     const int64_t* rows; /* NULL: all rows in order */
     double* Y;           /* [M][nrows] */
     int64_t first, last; /* index range into the row list for this worker */
+    const uint16_t *As, *Bs; /* non-NULL: codes-only bytes with row-shared parameters */
+    int64_t Ga;
     int status;
 } mm_job;
 
@@ -267,9 +356,13 @@ static void* mm_worker(void* arg) {
     uint16_t* b = malloc((size_t)groups * 4 * sizeof(uint16_t));
     double* w = malloc((size_t)K * sizeof(double));
     if (!q || !a || !b || !w) { j->status = OR_EINVAL; goto done; }
+    if (j->As) expand_shared(K, j->Ga, j->As, j->Bs, a, b);
     for (int64_t i = j->first; i < j->last; ++i) {
         int64_t r = j->rows ? j->rows[i] : i;
-        unpack_row(K, j->packed, r, q, a, b);
+        if (j->As)
+            unpack_codes_row(K, j->packed, r, q);
+        else
+            unpack_row(K, j->packed, r, q, a, b);
         decode_row(K, q, a, b, w);
         for (int64_t t = 0; t < j->M; ++t) {
             const double* x = j->X + t * K;
@@ -287,8 +380,9 @@ done:
 /* Y[t][i] = sum_k X[t][k] * W_hat[rows[i]][k] for the listed rows (all rows
  * when rows == NULL, then nrows must equal N).  Work is split over `threads`
  * POSIX threads by output row; each Y element is one plain sequential sum. */
-int oracle_matmul_rows(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const double* X,
-                       int64_t nrows, const int64_t* rows, double* Y, int threads) {
+static int matmul_rows(int64_t N, int64_t K, const uint8_t* packed, int64_t Ga, const uint16_t* As,
+                       const uint16_t* Bs, int64_t M, const double* X, int64_t nrows, const int64_t* rows,
+                       double* Y, int threads) {
     if (!packed || !X || !Y) return OR_EINVAL;
     if (!shape_ok(N, K) || M < 0 || nrows < 0) return OR_ESHAPE;
     if (!rows && nrows != N) return OR_ESHAPE;
@@ -307,6 +401,7 @@ int oracle_matmul_rows(int64_t N, int64_t K, const uint8_t* packed, int64_t M, c
         mm_job* j = &jobs[t];
         j->N = N; j->K = K; j->M = M; j->nrows = nrows;
         j->packed = packed; j->X = X; j->rows = rows; j->Y = Y;
+        j->As = As; j->Bs = Bs; j->Ga = Ga;
         j->first = t * per;
         j->last = (t + 1) * per < nrows ? (t + 1) * per : nrows;
         if (j->first > j->last) j->first = j->last;
@@ -322,7 +417,22 @@ int oracle_matmul_rows(int64_t N, int64_t K, const uint8_t* packed, int64_t M, c
     return status;
 }
 
+int oracle_matmul_rows(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const double* X,
+                       int64_t nrows, const int64_t* rows, double* Y, int threads) {
+    return matmul_rows(N, K, packed, 0, NULL, NULL, M, X, nrows, rows, Y, threads);
+}
+
 int oracle_matmul(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const double* X, double* Y,
                   int threads) {
     return oracle_matmul_rows(N, K, packed, M, X, N, NULL, Y, threads);
+}
+
+/* The same product from codes-only bytes and row-shared parameters: every row
+ * decodes with pair (Ga == 1 ? 0 : g) of its group g. */
+int oracle_matmul_shared_rows(int64_t N, int64_t K, const uint8_t* packed_codes, int64_t Ga,
+                              const uint16_t* As, const uint16_t* Bs, int64_t M, const double* X,
+                              int64_t nrows, const int64_t* rows, double* Y, int threads) {
+    if (!As || !Bs) return OR_EINVAL;
+    if (K % OR_G || (Ga != 1 && Ga != K / OR_G)) return OR_ESHAPE;
+    return matmul_rows(N, K, packed_codes, Ga, As, Bs, M, X, nrows, rows, Y, threads);
 }

@@ -314,3 +314,106 @@ def test_row_subset_matches_full_product():
     assert np.array_equal(Ys, Y[:, rows])
     # single-threaded and multi-threaded agree bit for bit (each sum is sequential)
     assert np.array_equal(Y, oracle.matmul(pk, N, K, X, threads=1))
+
+
+# ------------------------------------------- row-shared affine parameters
+# (the paper's own setting: one (A, B) per weight matrix, Sec. 3.1 / Sec. 4.2;
+# or one pair per 128-column group shared by the rows)
+
+def test_codes_packed_size_is_2_bits_per_weight():
+    for N, K in [(16, 128), (4096, 4096), (11008, 4096), (4096, 11008)]:
+        assert oracle.codes_packed_bytes(N, K) == N * K // 4
+    for N, K in [(15, 128), (16, 100), (0, 128)]:
+        with pytest.raises(oracle.OracleError):
+            oracle.codes_packed_bytes(N, K)
+
+
+def test_codes_byte_positions_worked_by_hand():
+    g = json.load(open(os.path.join(GOLD, "codes_positions.json")))
+    for c in g["cases"]:
+        N, K = c["N"], c["K"]
+        Q = np.zeros((N, K), np.uint8)
+        Q[tuple(c["index"])] = c["value"]
+        packed, bad = oracle.pack_codes(Q)
+        assert bad == 0
+        expect = np.zeros_like(packed)
+        for off, val in c["bytes"].items():
+            expect[int(off)] = val
+        nz = np.nonzero(packed != expect)[0]
+        assert nz.size == 0, (c, nz[:8], packed[nz[:8]])
+
+
+@pytest.mark.parametrize("N,K", [(16, 128), (16, 256), (48, 384), (32, 1152)])
+def test_codes_round_trip_and_same_fields_as_full_format(N, K):
+    """Codes-only bytes are the code areas of the full format, packet by packet."""
+    rng = np.random.default_rng(N * 11 + K)
+    Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+    pc, bad = oracle.pack_codes(Q)
+    assert bad == 0
+    assert np.array_equal(oracle.unpack_codes(pc, N, K), Q)
+    A = np.zeros((N, K // 128, 4, 4), np.float16); B = np.zeros((N, K // 128, 4), np.float16)
+    pf, _ = oracle.pack(Q, A, B)
+    groups = K // 128
+    for rb in range(N // 16):
+        for p in range((groups + 1) // 2):
+            half = groups % 2 == 1 and p == groups // 2
+            n = 512 if half else 1024
+            full_off = rb * groups * 1152 + p * 2304
+            code_off = rb * groups * 512 + p * 1024
+            assert np.array_equal(pf[full_off:full_off + n], pc[code_off:code_off + n]), (rb, p)
+    Q[N - 1, K - 1] ^= 2
+    assert not np.array_equal(oracle.pack_codes(Q)[0], pc)
+
+
+@pytest.mark.parametrize("Ga_per_group", [False, True])
+def test_shared_product_equals_replicated_parameters(Ga_per_group):
+    """Row-shared pairs give bit for bit the product of the full format with
+    every row holding copies of them."""
+    rng = np.random.default_rng(31 + Ga_per_group)
+    N, K, M = 32, 384, 3
+    Ga = K // 128 if Ga_per_group else 1
+    Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+    As = (rng.standard_normal((Ga, 4, 4)) * 0.05).astype(np.float16)
+    Bs = (rng.standard_normal((Ga, 4)) * 0.02).astype(np.float16)
+    g_src = np.arange(K // 128) if Ga_per_group else np.zeros(K // 128, np.int64)
+    A = np.broadcast_to(As[g_src], (N, K // 128, 4, 4)).copy()
+    B = np.broadcast_to(Bs[g_src], (N, K // 128, 4)).copy()
+    X = rng.standard_normal((M, K))
+    Y_full = oracle.matmul(oracle.pack(Q, A, B)[0], N, K, X)
+    pc, _ = oracle.pack_codes(Q)
+    assert np.array_equal(oracle.matmul_shared(pc, N, K, As, Bs, X), Y_full)
+    rows = [31, 0, 7]
+    assert np.array_equal(oracle.matmul_shared(pc, N, K, As, Bs, X, rows=rows), Y_full[:, rows])
+
+
+@pytest.mark.parametrize("Ga_per_group", [False, True])
+def test_shared_product_is_the_eq9_fold(Ga_per_group):
+    """Eq. 9 of Sec. 3.2.3: with (A, B) shared by the rows, fold A into the
+    activations (X_i A per vector i) and B into one column term, then multiply
+    by the bare integer codes."""
+    rng = np.random.default_rng(77 + Ga_per_group)
+    N, K, M = 48, 640, 2
+    Ga = K // 128 if Ga_per_group else 1
+    Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+    As = (rng.standard_normal((Ga, 4, 4)) * 0.05).astype(np.float16)
+    Bs = (rng.standard_normal((Ga, 4)) * 0.02).astype(np.float16)
+    X = rng.standard_normal((M, K))
+    Y = oracle.matmul_shared(oracle.pack_codes(Q)[0], N, K, As, Bs, X)
+    g_of_v = (np.arange(K // 4) // 32) if Ga_per_group else np.zeros(K // 4, np.int64)
+    Xv = X.reshape(M, K // 4, 4)
+    XA = np.einsum("tva,vab->tvb", Xv, As.astype(np.float64)[g_of_v])
+    XB = np.einsum("tva,va->t", Xv, Bs.astype(np.float64)[g_of_v])
+    np.testing.assert_allclose(Y, XA.reshape(M, K) @ Q.T.astype(np.float64) + XB[:, None], rtol=1e-12, atol=1e-12)
+
+
+def test_shared_identity_pair_is_integer_matmul():
+    """A = I, B = 0 for the whole matrix: the product of integer activations
+    with the codes, exactly."""
+    rng = np.random.default_rng(5)
+    N, K, M = 16, 256, 2
+    Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+    X = rng.integers(-8, 9, size=(M, K)).astype(np.float64)
+    As = np.eye(4, dtype=np.float16)[None]
+    Bs = np.zeros((1, 4), np.float16)
+    Y = oracle.matmul_shared(oracle.pack_codes(Q)[0], N, K, As, Bs, X)
+    assert np.array_equal(Y, X @ Q.T.astype(np.float64))
