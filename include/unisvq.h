@@ -57,6 +57,25 @@
  *   consumes, so every load of the matrix-vector kernel is a fully coalesced
  *   16-byte-per-lane read.
  * ---------------------------------------------------------------------------
+ * Codes-only format with row-shared affine parameters (the paper's own
+ * setting: one (A, B) pair per weight matrix, Sec. 3.1 and Sec. 4.2; also
+ * one pair per 128-column group shared by all rows)
+ *   affine_groups Ga = 1 (one pair) or K/128 (one per group); group g uses
+ *   pair (Ga == 1 ? 0 : g).  Canonical inputs: Q as above, A fp16 [Ga][4][4],
+ *   B fp16 [Ga][4].
+ *   Codes: format v1 without its A and B areas -- row block rb occupies
+ *   (K/128)*512 bytes at rb*(K/128)*512; packet p (groups 2p, 2p+1) is 1024
+ *   bytes at p*1024 with F(r, 2p+j, b) at P + 16s + 8j; a final half packet
+ *   (odd K/128) is 512 bytes with F(r, g, b) at P + 8s.  N*K/4 bytes (2 bits
+ *   per weight).
+ *   Shared affine block: 80-byte records, one per pair of groups (a single
+ *   record, holding pair 0 for both of its groups, when Ga = 1):
+ *       R*80 + 16b + 8j        A[2R+j][a][b] for a = 0..3, fp16 each
+ *       R*80 + 64 + 4b + 2j    B[2R+j][b], fp16
+ *   a group past the last (odd K/128, Ga = K/128) holds zeros.  Lane
+ *   (beta, b) of a wavefront reads exactly its A column and B values, as from
+ *   a full-format packet.
+ * ---------------------------------------------------------------------------
  */
 #ifndef UNISVQ_H
 #define UNISVQ_H
@@ -181,6 +200,60 @@ size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype)
  *              size is 0.  Overwritten; the caller owns it. */
 int unisvq_gemm(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype,
                 void* y, int y_dtype, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---- Row-shared affine parameters (codes-only format block above) ---- */
+
+/* Bytes of the codes-only buffer for an N x K matrix (N*K/4); 0 when the
+ * shape is invalid.  Host-only. */
+size_t unisvq_codes_bytes(int64_t N, int64_t K);
+
+/* Bytes of the shared affine block: 80 for affine_groups == 1, else
+ * 80*ceil(K/256) for affine_groups == K/128; 0 for any other value or an
+ * invalid K.  Host-only. */
+size_t unisvq_shared_affine_bytes(int64_t K, int64_t affine_groups);
+
+/* Pack codes and row-shared pairs (all device):
+ *   codes          uint8 [N][K], values 0..3
+ *   A, B           fp16 bits [affine_groups][4][4] and [affine_groups][4]
+ *   packed_codes   unisvq_codes_bytes(N, K) bytes, 16-byte aligned
+ *   packed_affine  unisvq_shared_affine_bytes(K, affine_groups) bytes, 16-byte aligned
+ *   bad_codes      as unisvq_pack
+ * UNISVQ_EINVAL when affine_groups is neither 1 nor K/128.  Bit exact. */
+int unisvq_pack_shared(int64_t N, int64_t K, int64_t affine_groups, const uint8_t* codes, const uint16_t* A,
+                       const uint16_t* B, void* packed_codes, void* packed_affine, int32_t* bad_codes,
+                       void* stream);
+
+/* Exact inverse of unisvq_pack_shared.  All device. */
+int unisvq_unpack_shared(int64_t N, int64_t K, int64_t affine_groups, const void* packed_codes,
+                         const void* packed_affine, uint8_t* codes, uint16_t* A, uint16_t* B, void* stream);
+
+/* unisvq_gemv with codes-only weights and row-shared pairs: the same
+ * arithmetic, M and K limits, dtypes and error behaviour; only the 2-bit
+ * codes stream from memory (the shared block is read from cache).
+ * packed_codes and packed_affine 16-byte aligned. */
+int unisvq_gemv_shared(int64_t N, int64_t K, int64_t affine_groups, const void* packed_codes,
+                       const void* packed_affine, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
+                       void* stream);
+
+/* One product of a batched call with row-shared pairs. */
+typedef struct {
+    int64_t N, K, affine_groups;
+    const void* packed_codes;   /* device, 16-byte aligned */
+    const void* packed_affine;  /* device, 16-byte aligned */
+    const void* x;              /* device [M][K], 16-byte aligned */
+    void* y;                    /* device [M][N] */
+} unisvq_gemv_shared_problem;
+
+/* unisvq_gemv_batched for row-shared pairs (each problem has its own). */
+int unisvq_gemv_shared_batched(const unisvq_gemv_shared_problem* problems, int count, int64_t M, int x_dtype,
+                               int y_dtype, void* stream);
+
+/* unisvq_gemm with codes-only weights and row-shared pairs: the same decode
+ * (A q + B exactly in fp32, one rounding to fp16), tiling, K split, bf16
+ * handling and workspace -- size it with unisvq_gemm_workspace_bytes. */
+int unisvq_gemm_shared(int64_t N, int64_t K, int64_t affine_groups, const void* packed_codes,
+                       const void* packed_affine, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
+                       void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -30,6 +30,22 @@ int check_product(int64_t N, int64_t K, const void* packed, int64_t M, const voi
     return UNISVQ_OK;
 }
 
+// Row-shared affine parameters: one pair per matrix or one per group.
+bool affine_groups_ok(int64_t K, int64_t ga) { return ga == 1 || ga == K / unisvq::kGroup; }
+
+int check_shared(int64_t N, int64_t K, int64_t affine_groups, const void* codes, const void* affine, int64_t M,
+                 const void* x, int x_dtype, const void* y, int y_dtype) {
+    if (!codes || !affine || !x || !y) return UNISVQ_EINVAL;
+    if (M < 1 || M > (int64_t{1} << 31) - 1) return UNISVQ_EINVAL;
+    if (!x_dtype_ok(x_dtype) || !y_dtype_ok(y_dtype)) return UNISVQ_EINVAL;
+    if (!shape_ok(N, K)) return UNISVQ_ESHAPE;
+    if (!affine_groups_ok(K, affine_groups)) return UNISVQ_EINVAL;
+    if (!aligned(codes, 16) || !aligned(affine, 16) || !aligned(x, 16)) return UNISVQ_EALIGN;
+    if (static_cast<int64_t>(unisvq_codes_bytes(N, K)) > unisvq::kMaxBufferBytes) return UNISVQ_EUNSUP;
+    if (!aligned(y, y_dtype == UNISVQ_F32 ? 4 : 2)) return UNISVQ_EALIGN;
+    return UNISVQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -118,6 +134,91 @@ int unisvq_gemm(int64_t N, int64_t K, const void* packed, int64_t M, const void*
     }
     return unisvq::launch_gemm(N, K, static_cast<const uint8_t*>(packed), M, x, x_dtype, y, y_dtype,
                                workspace, static_cast<hipStream_t>(stream));
+}
+
+/* ---- row-shared affine parameters ---- */
+
+size_t unisvq_codes_bytes(int64_t N, int64_t K) {
+    if (!shape_ok(N, K)) return 0;
+    return static_cast<size_t>(N / unisvq::kRowBlock) * static_cast<size_t>(K / unisvq::kGroup) *
+           unisvq::kCodeGroupBlockBytes;
+}
+
+size_t unisvq_shared_affine_bytes(int64_t K, int64_t affine_groups) {
+    if (K < unisvq::kGroup || K % unisvq::kGroup || K > (int64_t{1} << 31) - 1) return 0;
+    if (!affine_groups_ok(K, affine_groups)) return 0;
+    const int64_t records = affine_groups == 1 ? 1 : (K / unisvq::kGroup + 1) / 2;
+    return static_cast<size_t>(records) * unisvq::kAffineRecordBytes;
+}
+
+int unisvq_pack_shared(int64_t N, int64_t K, int64_t affine_groups, const uint8_t* codes, const uint16_t* A,
+                       const uint16_t* B, void* packed_codes, void* packed_affine, int32_t* bad_codes,
+                       void* stream) {
+    if (!codes || !A || !B || !packed_codes || !packed_affine) return UNISVQ_EINVAL;
+    if (!shape_ok(N, K)) return UNISVQ_ESHAPE;
+    if (!affine_groups_ok(K, affine_groups)) return UNISVQ_EINVAL;
+    if (!aligned(packed_codes, 16) || !aligned(packed_affine, 16) || !aligned(A, 2) || !aligned(B, 2) ||
+        (bad_codes && !aligned(bad_codes, 4)))
+        return UNISVQ_EALIGN;
+    const hipError_t e = unisvq::launch_pack_shared(N, K, affine_groups, codes, A, B,
+                                                    static_cast<uint8_t*>(packed_codes),
+                                                    static_cast<uint8_t*>(packed_affine), bad_codes,
+                                                    static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+}
+
+int unisvq_unpack_shared(int64_t N, int64_t K, int64_t affine_groups, const void* packed_codes,
+                         const void* packed_affine, uint8_t* codes, uint16_t* A, uint16_t* B, void* stream) {
+    if (!codes || !A || !B || !packed_codes || !packed_affine) return UNISVQ_EINVAL;
+    if (!shape_ok(N, K)) return UNISVQ_ESHAPE;
+    if (!affine_groups_ok(K, affine_groups)) return UNISVQ_EINVAL;
+    if (!aligned(packed_codes, 16) || !aligned(packed_affine, 16) || !aligned(A, 2) || !aligned(B, 2))
+        return UNISVQ_EALIGN;
+    const hipError_t e = unisvq::launch_unpack_shared(N, K, affine_groups, static_cast<const uint8_t*>(packed_codes),
+                                                      static_cast<const uint8_t*>(packed_affine), codes, A, B,
+                                                      static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+}
+
+int unisvq_gemv_shared(int64_t N, int64_t K, int64_t affine_groups, const void* packed_codes,
+                       const void* packed_affine, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
+                       void* stream) {
+    const unisvq_gemv_shared_problem p{N, K, affine_groups, packed_codes, packed_affine, x, y};
+    return unisvq_gemv_shared_batched(&p, 1, M, x_dtype, y_dtype, stream);
+}
+
+int unisvq_gemv_shared_batched(const unisvq_gemv_shared_problem* problems, int count, int64_t M, int x_dtype,
+                               int y_dtype, void* stream) {
+    if (!problems || count < 1) return UNISVQ_EINVAL;
+    if (count > UNISVQ_MAX_BATCH) return UNISVQ_EUNSUP;
+    unisvq::GemvProblem probs[UNISVQ_MAX_BATCH];
+    for (int i = 0; i < count; ++i) {
+        const unisvq_gemv_shared_problem& q = problems[i];
+        const int st = check_shared(q.N, q.K, q.affine_groups, q.packed_codes, q.packed_affine, M, q.x, x_dtype,
+                                    q.y, y_dtype);
+        if (st != UNISVQ_OK) return st;
+        probs[i] = unisvq::GemvProblem{static_cast<const uint8_t*>(q.packed_codes), q.x, q.y,
+                                       static_cast<int>(q.N), static_cast<int>(q.K), 0,
+                                       static_cast<const uint8_t*>(q.packed_affine), q.affine_groups == 1 ? 1 : 0};
+    }
+    if (M > 4) return UNISVQ_EUNSUP;
+    return unisvq::launch_gemv_batch(probs, count, M, x_dtype, y_dtype, static_cast<hipStream_t>(stream));
+}
+
+int unisvq_gemm_shared(int64_t N, int64_t K, int64_t affine_groups, const void* packed_codes,
+                       const void* packed_affine, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+    const int st = check_shared(N, K, affine_groups, packed_codes, packed_affine, M, x, x_dtype, y, y_dtype);
+    if (st != UNISVQ_OK) return st;
+    if (x_dtype == UNISVQ_BF16 && K > 65536) return UNISVQ_EUNSUP;  // the bf16 pre-pass holds a row in registers
+    const size_t need = unisvq::gemm_workspace_bytes(N, K, M, x_dtype);
+    if (need) {
+        if (!workspace || workspace_bytes < need) return UNISVQ_EWORKSPACE;
+        if (!aligned(workspace, 16)) return UNISVQ_EALIGN;
+    }
+    return unisvq::launch_gemm_shared(N, K, static_cast<const uint8_t*>(packed_codes),
+                                      static_cast<const uint8_t*>(packed_affine), affine_groups == 1 ? 1 : 0, M, x,
+                                      x_dtype, y, y_dtype, workspace, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -78,19 +78,34 @@ constexpr int kPacketBiasOff = 2048;   // B values inside a full packet
 constexpr int kHalfAffineOff = 512;
 constexpr int kHalfBiasOff = 1024;
 
+// Codes-only format (affine pairs shared by all rows, held in a separate
+// block of 80-byte records, one per pair of groups; see unisvq.h).
+constexpr int kCodeGroupBlockBytes = 512;  // one group of one row block: 16 rows * 32 B
+constexpr int kCodePacketBytes = 1024;     // two groups
+constexpr int kAffineRecordBytes = 80;     // A columns (64 B) and B values (16 B) of two groups
+constexpr int kRecordBiasOff = 64;
+
 // Launchers (host side).  Each returns the hipError_t of the launch.
 hipError_t launch_pack(int64_t N, int64_t K, const uint8_t* codes, const uint16_t* A,
                        const uint16_t* B, uint8_t* packed, int32_t* bad, hipStream_t s);
 hipError_t launch_unpack(int64_t N, int64_t K, const uint8_t* packed, uint8_t* codes,
                          uint16_t* A, uint16_t* B, hipStream_t s);
+hipError_t launch_pack_shared(int64_t N, int64_t K, int64_t affine_groups, const uint8_t* codes,
+                              const uint16_t* A, const uint16_t* B, uint8_t* packed_codes,
+                              uint8_t* packed_affine, int32_t* bad, hipStream_t s);
+hipError_t launch_unpack_shared(int64_t N, int64_t K, int64_t affine_groups, const uint8_t* packed_codes,
+                                const uint8_t* packed_affine, uint8_t* codes, uint16_t* A, uint16_t* B,
+                                hipStream_t s);
 
 // One problem of a (possibly batched) matrix-vector launch.
 struct GemvProblem {
-    const uint8_t* packed;
+    const uint8_t* packed;   // full format, or codes only when `affine` is set
     const void* x;
     void* y;
     int N, K;
-    int rb_begin;  // first workgroup index of this problem (set by the launcher)
+    int rb_begin;            // first workgroup index of this problem (set by the launcher)
+    const uint8_t* affine;   // shared affine block (codes-only format), else null
+    int affine_one;          // 1: one pair for the whole matrix
 };
 constexpr int kMaxBatch = 8;
 
@@ -107,11 +122,16 @@ int launch_gemv(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const vo
 size_t gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype);
 int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x,
                 int x_dtype, void* y, int y_dtype, void* workspace, hipStream_t s);
+// The same with codes-only weights and a shared affine block.
+int launch_gemm_shared(int64_t N, int64_t K, const uint8_t* packed_codes, const uint8_t* affine,
+                       int affine_one, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
+                       void* workspace, hipStream_t s);
 // Small-batch kernel (M <= kSkinnyMaxM) on fp16 activations; inv_scale
 // (per token, may be null) multiplies the results.
 constexpr int64_t kSkinnyMaxM = 32;
-hipError_t launch_skinny(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const _Float16* x,
-                         const float* inv_scale, void* y, int y_dtype, hipStream_t s);
+hipError_t launch_skinny(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine, int affine_one,
+                         int64_t M, const _Float16* x, const float* inv_scale, void* y, int y_dtype,
+                         hipStream_t s);
 
 // Output store in the requested dtype (fp32 -> fp16 / bf16 round to nearest even).
 __device__ inline void store_out(void* y, int64_t idx, float v, int y_dtype) {

@@ -54,6 +54,31 @@ __device__ inline void load_packet(__amdgpu_buffer_rsrc_t rw, uint32_t rowblk, i
     }
 }
 
+// The same piece from codes-only bytes (row block at `rowblk`, 512 bytes
+// per group) and the shared affine block: lane (beta, j) takes its A column
+// and B values from record p (record 0 for a single pair).  A half packet
+// keeps only its group's parameters.
+template <bool STREAM = false>
+__device__ inline void load_packet_shared(__amdgpu_buffer_rsrc_t rc, __amdgpu_buffer_rsrc_t ra, uint32_t rowblk,
+                                          int p, int gend, int affine_one, int lane, Piece& pc) {
+    const bool full = 2 * p + 1 < gend;
+    const bool half = 2 * p + 1 == gend;
+    const uint32_t P = full || half ? rowblk + static_cast<uint32_t>(p) * kCodePacketBytes : kOutOfRange;
+    const uint32_t R = full || half ? static_cast<uint32_t>(affine_one ? 0 : p) * kAffineRecordBytes : kOutOfRange;
+    const int j = lane & 3;
+    if (half) {
+        const uint2 c = STREAM ? ld64_stream(rc, P + 8 * lane) : ld64(rc, P + 8 * lane);
+        const uint2 a = ld64(ra, R + 16 * j);
+        pc.c = uint4{c.x, c.y, 0u, 0u};
+        pc.a = uint4{a.x, a.y, 0u, 0u};
+        pc.b = ld16(ra, R + kRecordBiasOff + 4 * j);
+    } else {
+        pc.c = STREAM ? ld128_stream(rc, P + 16 * lane) : ld128(rc, P + 16 * lane);
+        pc.a = ld128(ra, R + 16 * j);
+        pc.b = ld32(ra, R + kRecordBiasOff + 4 * j);
+    }
+}
+
 // Value of lane b of this lane's quad.
 template <int B>
 __device__ inline uint32_t quad_lane(uint32_t v) {

@@ -112,8 +112,11 @@ __device__ inline void group_step(const GemmState<MI>& st, int g, const Piece (&
     __syncthreads();
 }
 
-template <int MI>
+// SHARED: codes-only weights, A and B from the shared affine block (one pair
+// for the matrix when affine_one, else one per group); the decode is the same.
+template <int MI, bool SHARED>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restrict__ packed,
+                                                        const uint8_t* __restrict__ affine, int affine_one,
                                                         const _Float16* __restrict__ x,
                                                         const float* __restrict__ inv_scale, void* y, int N,
                                                         int K, int M, int y_dtype, int m_tiles, int n_tiles,
@@ -141,8 +144,17 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     const int gend = min(groups, gb + gps);
 
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(M) * K * 2u);
+    constexpr uint32_t kBlockBytes = SHARED ? kCodeGroupBlockBytes : kGroupBlockBytes;
     const __amdgpu_buffer_rsrc_t rw =
-        make_rsrc(packed, static_cast<uint32_t>(N / kRowBlock) * groups * kGroupBlockBytes);
+        make_rsrc(packed, static_cast<uint32_t>(N / kRowBlock) * groups * kBlockBytes);
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(
+        affine, SHARED ? static_cast<uint32_t>(affine_one ? 1 : (groups + 1) / 2) * kAffineRecordBytes : 0u);
+    auto load = [&](uint32_t rowblk, int p, Piece& pc) {
+        if constexpr (SHARED)
+            load_packet_shared(rw, ra, rowblk, p, gend, affine_one, lane, pc);
+        else
+            load_packet(rw, rowblk, p, gend, lane, pc);
+    };
 
     // Decode role: this wavefront decodes local row blocks 2*wave and
     // 2*wave+1; lane (beta = lane / 4, j = lane % 4) = packet slot `lane`.
@@ -154,7 +166,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
         const int rb = (n0 >> 4) + 2 * wave + r;
-        rowblk[r] = rb < (N >> 4) ? static_cast<uint32_t>(rb) * groups * kGroupBlockBytes : kOutOfRange;
+        rowblk[r] = rb < (N >> 4) ? static_cast<uint32_t>(rb) * groups * kBlockBytes : kOutOfRange;
         st.wrow[r] = wsh + (16 * (2 * wave + r) + beta) * kLdsRow;
     }
 
@@ -178,8 +190,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     Piece pa[2], pb[2], pc[2];
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
-        load_packet(rw, rowblk[r], gb >> 1, gend, lane, pa[r]);
-        load_packet(rw, rowblk[r], (gb >> 1) + 1, gend, lane, pb[r]);
+        load(rowblk[r], gb >> 1, pa[r]);
+        load(rowblk[r], (gb >> 1) + 1, pb[r]);
     }
     // Prologue: group gb into buffer gb & 1 (= 0).
     {
@@ -207,7 +219,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
         const int q = g >> 1;
         group_step<MI>(st, g, pa, 1, xq, acc);  // decodes group 2q+1 (packet q)
 #pragma unroll
-        for (int r = 0; r < 2; ++r) load_packet(rw, rowblk[r], q + 2, gend, lane, pc[r]);
+        for (int r = 0; r < 2; ++r) load(rowblk[r], q + 2, pc[r]);
         group_step<MI>(st, g + 1, pb, 0, xq, acc);  // decodes group 2q+2 (packet q+1)
 #pragma unroll
         for (int r = 0; r < 2; ++r) {
@@ -361,13 +373,14 @@ size_t partial_bytes(int64_t N, int64_t K, int64_t M) {
     return p.splits > 1 ? static_cast<size_t>(p.splits) * M * N * 4 : 0;
 }
 
-template <int MI>
-hipError_t launch_tiles(const GemmPlan& p, int64_t N, int64_t K, const uint8_t* packed, int64_t M,
-                        const _Float16* x, const float* inv_scale, void* y, int y_dtype, float* partial,
-                        hipStream_t s) {
+template <int MI, bool SHARED>
+hipError_t launch_tiles(const GemmPlan& p, int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine,
+                        int affine_one, int64_t M, const _Float16* x, const float* inv_scale, void* y,
+                        int y_dtype, float* partial, hipStream_t s) {
     if (p.splits > 1 && partial == nullptr) return hipErrorInvalidValue;  // never launch without the partials
     const unsigned blocks = static_cast<unsigned>(p.m_tiles) * p.n_tiles * p.splits;
-    hipLaunchKernelGGL(gemm_kernel<MI>, dim3(blocks), dim3(kThreads), 0, s, packed, x, inv_scale, y,
+    hipLaunchKernelGGL((gemm_kernel<MI, SHARED>), dim3(blocks), dim3(kThreads), 0, s, packed, affine, affine_one,
+                       x, inv_scale, y,
                        static_cast<int>(N), static_cast<int>(K), static_cast<int>(M), y_dtype, p.m_tiles,
                        p.n_tiles, p.splits, p.gps, p.splits > 1 ? partial : nullptr);
     if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
@@ -387,8 +400,10 @@ size_t gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype) {
     return b + partial_bytes(N, K, M);
 }
 
-int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x, int x_dtype,
-                void* y, int y_dtype, void* workspace, hipStream_t s) {
+namespace {
+
+int gemm_common(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine, int affine_one, int64_t M,
+                const void* x, int x_dtype, void* y, int y_dtype, void* workspace, hipStream_t s) {
     const _Float16* xh = static_cast<const _Float16*>(x);
     const float* inv = nullptr;
     uint8_t* ws = static_cast<uint8_t*>(workspace);
@@ -403,7 +418,9 @@ int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const vo
         inv = winv;
     }
     if (M <= kSkinnyMaxM)
-        return launch_skinny(N, K, packed, M, xh, inv, y, y_dtype, s) == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+        return launch_skinny(N, K, packed, affine, affine_one, M, xh, inv, y, y_dtype, s) == hipSuccess
+                   ? UNISVQ_OK
+                   : UNISVQ_EHIP;
     float* partial = reinterpret_cast<float*>(ws);
     // The activation buffer is addressed with 32-bit offsets: slice M.  The
     // workspace was sized for the whole product, which has far more than 256
@@ -421,11 +438,29 @@ int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const vo
             p.splits = 1;
             p.gps = static_cast<int>(K / kGroup);
         }
-        const hipError_t e = p.mi == 2 ? launch_tiles<2>(p, N, K, packed, mc, xs, is, ys, y_dtype, partial, s)
-                                       : launch_tiles<1>(p, N, K, packed, mc, xs, is, ys, y_dtype, partial, s);
+        hipError_t e;
+        if (affine)
+            e = p.mi == 2 ? launch_tiles<2, true>(p, N, K, packed, affine, affine_one, mc, xs, is, ys, y_dtype, partial, s)
+                          : launch_tiles<1, true>(p, N, K, packed, affine, affine_one, mc, xs, is, ys, y_dtype, partial, s);
+        else
+            e = p.mi == 2 ? launch_tiles<2, false>(p, N, K, packed, nullptr, 0, mc, xs, is, ys, y_dtype, partial, s)
+                          : launch_tiles<1, false>(p, N, K, packed, nullptr, 0, mc, xs, is, ys, y_dtype, partial, s);
         if (e != hipSuccess) return UNISVQ_EHIP;
     }
     return UNISVQ_OK;
+}
+
+}  // namespace
+
+int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x, int x_dtype,
+                void* y, int y_dtype, void* workspace, hipStream_t s) {
+    return gemm_common(N, K, packed, nullptr, 0, M, x, x_dtype, y, y_dtype, workspace, s);
+}
+
+int launch_gemm_shared(int64_t N, int64_t K, const uint8_t* packed_codes, const uint8_t* affine,
+                       int affine_one, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
+                       void* workspace, hipStream_t s) {
+    return gemm_common(N, K, packed_codes, affine, affine_one, M, x, x_dtype, y, y_dtype, workspace, s);
 }
 
 }  // namespace unisvq

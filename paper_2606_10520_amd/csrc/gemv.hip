@@ -277,7 +277,7 @@ __device__ inline void half_step(const uint2& c, const uint2& a, uint32_t bbits,
 // count, PF packets in flight per wavefront, NX activation load instructions
 // per wavefront (issued ahead of the packet loads), OCC the minimum
 // wavefronts per SIMD the register allocation must allow.
-template <typename XT, int WAVES, int MT, int PF, int NX, int OCC>
+template <typename XT, int WAVES, int MT, int PF, int NX, int OCC, bool SHARED>
 __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch batch) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
@@ -286,7 +286,8 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
     const uint8_t* packed = batch.p[0].packed;
     const XT* x = static_cast<const XT*>(batch.p[0].x);
     void* y = batch.p[0].y;
-    int N = batch.p[0].N, K = batch.p[0].K, rb0 = 0;
+    const uint8_t* affine = batch.p[0].affine;
+    int N = batch.p[0].N, K = batch.p[0].K, rb0 = 0, affine_one = batch.p[0].affine_one;
 #pragma unroll
     for (int i = 1; i < kMaxBatch; ++i) {
         if (i < batch.count && bid >= batch.p[i].rb_begin) {
@@ -296,6 +297,8 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
             N = batch.p[i].N;
             K = batch.p[i].K;
             rb0 = batch.p[i].rb_begin;
+            affine = batch.p[i].affine;
+            affine_one = batch.p[i].affine_one;
         }
     }
     const int M = batch.M;
@@ -343,19 +346,35 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
     for (int i = 0; i < NX; ++i) xr[i] = ld64(rx, x_off(i));
     __builtin_amdgcn_sched_barrier(0);  // keep the activation loads ahead of the packet loads
 
-    // 2. The first PF packets of this wavefront's run.
+    // 2. The first PF packets of this wavefront's run.  With row-shared pairs
+    //    (SHARED) the weights are bare codes and each lane reads its A column
+    //    and B values from the small shared block (cached, the same for every
+    //    row block) instead of the packet.
+    constexpr uint32_t kBlockBytes = SHARED ? kCodeGroupBlockBytes : kGroupBlockBytes;
+    constexpr uint32_t kPktBytes = SHARED ? kCodePacketBytes : kPacketBytes;
     const __amdgpu_buffer_rsrc_t rw =
-        make_rsrc(packed, static_cast<uint32_t>(N / kRowBlock) * groups * kGroupBlockBytes);
-    const uint32_t blk = static_cast<uint32_t>(rb) * groups * kGroupBlockBytes;
+        make_rsrc(packed, static_cast<uint32_t>(N / kRowBlock) * groups * kBlockBytes);
+    const __amdgpu_buffer_rsrc_t ra =
+        make_rsrc(affine, SHARED ? static_cast<uint32_t>(affine_one ? 1 : packets) * kAffineRecordBytes : 0u);
+    const uint32_t blk = static_cast<uint32_t>(rb) * groups * kBlockBytes;
+    const uint32_t jcol = static_cast<uint32_t>(lane & 3);
+    // packet p of the row block (or nothing when !valid)
+    auto load_pkt = [&](int p, bool valid, uint4& c, uint4& a, uint32_t& b) {
+        const uint32_t off = valid ? blk + static_cast<uint32_t>(p) * kPktBytes : kOutOfRange;
+        c = ld128_stream(rw, off + 16 * lane);
+        if constexpr (SHARED) {
+            const uint32_t R = valid ? static_cast<uint32_t>(affine_one ? 0 : p) * kAffineRecordBytes : kOutOfRange;
+            a = ld128(ra, R + 16 * jcol);
+            b = ld32(ra, R + kRecordBiasOff + 4 * jcol);
+        } else {
+            a = ld128_stream(rw, off + kPacketAffineOff + 16 * lane);
+            b = ld32_stream(rw, off + kPacketBiasOff + 4 * lane);
+        }
+    };
     uint4 cbuf[PF], abuf[PF];
     uint32_t bbuf[PF];
 #pragma unroll
-    for (int i = 0; i < PF; ++i) {
-        const uint32_t off = i < np ? blk + static_cast<uint32_t>(p0 + i) * kPacketBytes : kOutOfRange;
-        cbuf[i] = ld128_stream(rw, off + 16 * lane);
-        abuf[i] = ld128_stream(rw, off + kPacketAffineOff + 16 * lane);
-        bbuf[i] = ld32_stream(rw, off + kPacketBiasOff + 4 * lane);
-    }
+    for (int i = 0; i < PF; ++i) load_pkt(p0 + i, i < np, cbuf[i], abuf[i], bbuf[i]);
     __builtin_amdgcn_sched_barrier(0);
 
     // 3. Stage this wavefront's activations in operand order, with the
@@ -394,21 +413,25 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
                 if (i + j < np)
                     packet_step<XT, MT>(cbuf[j], abuf[j], bbuf[j], p0 + i + j, xs, xbar, packets, M, lane, acc);
                 const int nxt = i + j + PF;
-                const uint32_t off =
-                    nxt < np ? blk + static_cast<uint32_t>(p0 + nxt) * kPacketBytes : kOutOfRange;
-                cbuf[j] = ld128_stream(rw, off + 16 * lane);
-                abuf[j] = ld128_stream(rw, off + kPacketAffineOff + 16 * lane);
-                bbuf[j] = ld32_stream(rw, off + kPacketBiasOff + 4 * lane);
+                load_pkt(p0 + nxt, nxt < np, cbuf[j], abuf[j], bbuf[j]);
             }
         }
     }
     // The trailing half packet (odd group count) of the last wavefront: loaded
     // and used here, outside the pipelined part.
     if (do_half) {
-        const uint32_t hoff = blk + static_cast<uint32_t>(nfull) * kPacketBytes;
+        const uint32_t hoff = blk + static_cast<uint32_t>(nfull) * kPktBytes;
         const uint2 hc = ld64_stream(rw, hoff + 8 * lane);
-        const uint2 ha = ld64_stream(rw, hoff + kHalfAffineOff + 8 * lane);
-        const uint32_t hb = ld16_stream(rw, hoff + kHalfBiasOff + 2 * lane);
+        uint2 ha;
+        uint32_t hb;
+        if constexpr (SHARED) {
+            const uint32_t R = static_cast<uint32_t>(affine_one ? 0 : nfull) * kAffineRecordBytes;
+            ha = ld64(ra, R + 16 * jcol);
+            hb = ld16(ra, R + kRecordBiasOff + 4 * jcol);
+        } else {
+            ha = ld64_stream(rw, hoff + kHalfAffineOff + 8 * lane);
+            hb = ld16_stream(rw, hoff + kHalfBiasOff + 2 * lane);
+        }
         half_step<XT, MT>(hc, ha, hb, nfull, xs, xbar, packets, M, lane, acc);
     }
 
@@ -437,20 +460,20 @@ size_t gemv_lds_bytes(int K, int M, int waves, int mt) {
            static_cast<size_t>(waves) * mt * 16 * 4;
 }
 
-template <typename XT, int WAVES, int MT, int PF, int NX>
+template <typename XT, bool SHARED, int WAVES, int MT, int PF, int NX>
 int launch_cfg(const GemvBatch& b, int blocks, int maxK, hipStream_t s) {
     const size_t lds = gemv_lds_bytes(maxK, b.M, WAVES, MT);
     if (lds > kMaxLds) return UNISVQ_EUNSUP;
     // Raising the dynamic-LDS limit is idempotent; do it once per instantiation.
     static std::atomic<int> attr_done{0};
     if (!attr_done.load(std::memory_order_acquire)) {
-        if (hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_kernel<XT, WAVES, MT, PF, NX, 1>),
+        if (hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_kernel<XT, WAVES, MT, PF, NX, 1, SHARED>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize,
                                 static_cast<int>(kMaxLds)) != hipSuccess)
             return UNISVQ_EHIP;
         attr_done.store(1, std::memory_order_release);
     }
-    hipLaunchKernelGGL((gemv_kernel<XT, WAVES, MT, PF, NX, 1>), dim3(static_cast<unsigned>(blocks)),
+    hipLaunchKernelGGL((gemv_kernel<XT, WAVES, MT, PF, NX, 1, SHARED>), dim3(static_cast<unsigned>(blocks)),
                        dim3(WAVES * 64), lds, s, b);
     return hipGetLastError() == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
 }
@@ -485,32 +508,32 @@ GemvPlan plan_gemv(int64_t blocks, int min_groups, int max_groups, int M) {
     return p;
 }
 
-template <typename XT, int WAVES, int MT, int PF>
+template <typename XT, bool SHARED, int WAVES, int MT, int PF>
 int launch_nx(const GemvBatch& b, int blocks, int maxK, int nx, hipStream_t s) {
-    if (nx == 1) return launch_cfg<XT, WAVES, MT, PF, 1>(b, blocks, maxK, s);
-    if (nx == 2) return launch_cfg<XT, WAVES, MT, PF, 2>(b, blocks, maxK, s);
-    if (nx == 4) return launch_cfg<XT, WAVES, MT, PF, 4>(b, blocks, maxK, s);
-    return launch_cfg<XT, WAVES, MT, PF, 8>(b, blocks, maxK, s);
+    if (nx == 1) return launch_cfg<XT, SHARED, WAVES, MT, PF, 1>(b, blocks, maxK, s);
+    if (nx == 2) return launch_cfg<XT, SHARED, WAVES, MT, PF, 2>(b, blocks, maxK, s);
+    if (nx == 4) return launch_cfg<XT, SHARED, WAVES, MT, PF, 4>(b, blocks, maxK, s);
+    return launch_cfg<XT, SHARED, WAVES, MT, PF, 8>(b, blocks, maxK, s);
 }
 
-template <typename XT, int WAVES, int MT>
+template <typename XT, bool SHARED, int WAVES, int MT>
 int launch_pf(const GemvBatch& b, int blocks, int maxK, const GemvPlan& p, hipStream_t s) {
-    if (p.pf == 2) return launch_nx<XT, WAVES, MT, 2>(b, blocks, maxK, p.nx, s);
-    return launch_nx<XT, WAVES, MT, 4>(b, blocks, maxK, p.nx, s);
+    if (p.pf == 2) return launch_nx<XT, SHARED, WAVES, MT, 2>(b, blocks, maxK, p.nx, s);
+    return launch_nx<XT, SHARED, WAVES, MT, 4>(b, blocks, maxK, p.nx, s);
 }
 
-template <typename XT, int MT>
+template <typename XT, bool SHARED, int MT>
 int launch_waves(const GemvBatch& b, int blocks, int minK, int maxK, hipStream_t s) {
     const GemvPlan p = plan_gemv(blocks, minK / kGroup, maxK / kGroup, b.M);
-    if (MT == 1 && p.waves == 16) return launch_pf<XT, 16, 1>(b, blocks, maxK, p, s);
-    return launch_pf<XT, 8, MT>(b, blocks, maxK, p, s);
+    if (MT == 1 && p.waves == 16) return launch_pf<XT, SHARED, 16, 1>(b, blocks, maxK, p, s);
+    return launch_pf<XT, SHARED, 8, MT>(b, blocks, maxK, p, s);
 }
 
-template <typename XT>
+template <typename XT, bool SHARED>
 int launch_tokens(const GemvBatch& b, int blocks, int minK, int maxK, hipStream_t s) {
-    if (b.M == 1) return launch_waves<XT, 1>(b, blocks, minK, maxK, s);
-    if (b.M == 2) return launch_waves<XT, 2>(b, blocks, minK, maxK, s);
-    return launch_waves<XT, 4>(b, blocks, minK, maxK, s);
+    if (b.M == 1) return launch_waves<XT, SHARED, 1>(b, blocks, minK, maxK, s);
+    if (b.M == 2) return launch_waves<XT, SHARED, 2>(b, blocks, minK, maxK, s);
+    return launch_waves<XT, SHARED, 4>(b, blocks, minK, maxK, s);
 }
 
 }  // namespace
@@ -530,13 +553,18 @@ int launch_gemv_batch(const GemvProblem* probs, int count, int64_t M, int x_dtyp
     b.count = count;
     b.M = static_cast<int>(M);
     b.y_dtype = y_dtype;
-    if (x_dtype == UNISVQ_F16) return launch_tokens<_Float16>(b, blocks, minK, maxK, s);
-    return launch_tokens<__bf16>(b, blocks, minK, maxK, s);
+    // every problem of a batch has the same weight format (checked by the caller)
+    const bool shared = probs[0].affine != nullptr;
+    if (x_dtype == UNISVQ_F16)
+        return shared ? launch_tokens<_Float16, true>(b, blocks, minK, maxK, s)
+                      : launch_tokens<_Float16, false>(b, blocks, minK, maxK, s);
+    return shared ? launch_tokens<__bf16, true>(b, blocks, minK, maxK, s)
+                  : launch_tokens<__bf16, false>(b, blocks, minK, maxK, s);
 }
 
 int launch_gemv(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x, int x_dtype,
                 void* y, int y_dtype, hipStream_t s) {
-    GemvProblem p{packed, x, y, static_cast<int>(N), static_cast<int>(K), 0};
+    GemvProblem p{packed, x, y, static_cast<int>(N), static_cast<int>(K), 0, nullptr, 0};
     return launch_gemv_batch(&p, 1, M, x_dtype, y_dtype, s);
 }
 

@@ -51,8 +51,10 @@ __device__ inline void skinny_group(__amdgpu_buffer_rsrc_t rx, uint32_t xo, uint
 
 // Template parameters: MT token tiles of 16 (M <= 16 MT), WAVES wavefronts
 // per workgroup, PF packets in flight per wavefront.
-template <int MT, int WAVES, int PF>
+// SHARED: codes-only weights, A and B from the shared affine block.
+template <int MT, int WAVES, int PF, bool SHARED>
 __global__ __launch_bounds__(WAVES * 64) void skinny_kernel(const uint8_t* __restrict__ packed,
+                                                           const uint8_t* __restrict__ affine, int affine_one,
                                                            const _Float16* __restrict__ x,
                                                            const float* __restrict__ inv_scale, void* y, int N,
                                                            int K, int M, int y_dtype) {
@@ -72,11 +74,20 @@ __global__ __launch_bounds__(WAVES * 64) void skinny_kernel(const uint8_t* __res
     const int np = min(nfull, p0 + per) - p0;
     const bool do_half = has_half && wave == WAVES - 1;
 
+    constexpr uint32_t kBlockBytes = SHARED ? kCodeGroupBlockBytes : kGroupBlockBytes;
     const __amdgpu_buffer_rsrc_t rw =
-        make_rsrc(packed, static_cast<uint32_t>(N / kRowBlock) * groups * kGroupBlockBytes);
+        make_rsrc(packed, static_cast<uint32_t>(N / kRowBlock) * groups * kBlockBytes);
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(
+        affine, SHARED ? static_cast<uint32_t>(affine_one ? 1 : (groups + 1) / 2) * kAffineRecordBytes : 0u);
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(M) * K * 2u);
-    const uint32_t rowblk = static_cast<uint32_t>(rb) * groups * kGroupBlockBytes;
+    const uint32_t rowblk = static_cast<uint32_t>(rb) * groups * kBlockBytes;
     const int gend = 2 * (p0 + np);  // packets at or past this group read nothing
+    auto load = [&](int p, int end, Piece& pc) {
+        if constexpr (SHARED)
+            load_packet_shared<true>(rw, ra, rowblk, p, end, affine_one, lane, pc);
+        else
+            load_packet<true>(rw, rowblk, p, end, lane, pc);
+    };
 
     // Decode role: lane = packet slot (row beta = lane / 4, component j = lane % 4).
     const int j = lane & 3;
@@ -95,7 +106,7 @@ __global__ __launch_bounds__(WAVES * 64) void skinny_kernel(const uint8_t* __res
     // run unconditionally; a packet past the run reads zeros and adds zero.
     Piece ring[PF];
 #pragma unroll
-    for (int i = 0; i < PF; ++i) load_packet<true>(rw, rowblk, p0 + i, gend, lane, ring[i]);
+    for (int i = 0; i < PF; ++i) load(p0 + i, gend, ring[i]);
     for (int q0 = 0; q0 < np; q0 += PF) {
 #pragma unroll
         for (int i = 0; i < PF; ++i) {
@@ -103,12 +114,12 @@ __global__ __launch_bounds__(WAVES * 64) void skinny_kernel(const uint8_t* __res
             const uint32_t xo = q < np ? xlane + static_cast<uint32_t>(p0 + q) * 512u : kOutOfRange;
             skinny_group<MT>(rx, xo, row_step, ring[i], 0, j, wrow, wlane, acc);
             skinny_group<MT>(rx, q < np ? xo + 256u : kOutOfRange, row_step, ring[i], 1, j, wrow, wlane, acc);
-            load_packet<true>(rw, rowblk, p0 + q + PF, gend, lane, ring[i]);
+            load(p0 + q + PF, gend, ring[i]);
         }
     }
     if (do_half) {
         Piece h;
-        load_packet<true>(rw, rowblk, nfull, groups, lane, h);
+        load(nfull, groups, h);
         skinny_group<MT>(rx, xlane + static_cast<uint32_t>(nfull) * 512u, row_step, h, 0, j, wrow, wlane, acc);
     }
 
@@ -129,11 +140,11 @@ __global__ __launch_bounds__(WAVES * 64) void skinny_kernel(const uint8_t* __res
     }
 }
 
-template <int MT, int WAVES, int PF>
-hipError_t launch_cfg(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const _Float16* x,
-                      const float* inv_scale, void* y, int y_dtype, hipStream_t s) {
-    hipLaunchKernelGGL((skinny_kernel<MT, WAVES, PF>), dim3(static_cast<unsigned>(N / kRowBlock)),
-                       dim3(WAVES * 64), 0, s, packed, x, inv_scale, y, static_cast<int>(N),
+template <int MT, int WAVES, int PF, bool SHARED>
+hipError_t launch_cfg(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine, int affine_one,
+                      int64_t M, const _Float16* x, const float* inv_scale, void* y, int y_dtype, hipStream_t s) {
+    hipLaunchKernelGGL((skinny_kernel<MT, WAVES, PF, SHARED>), dim3(static_cast<unsigned>(N / kRowBlock)),
+                       dim3(WAVES * 64), 0, s, packed, affine, affine_one, x, inv_scale, y, static_cast<int>(N),
                        static_cast<int>(K), static_cast<int>(M), y_dtype);
     return hipGetLastError();
 }
@@ -145,17 +156,19 @@ hipError_t launch_cfg(int64_t N, int64_t K, const uint8_t* packed, int64_t M, co
 // loads -- the vector-memory counter retires in order).  Two row blocks per
 // workgroup (half the activation reads from L2) gained nothing at 16 tokens.
 template <int MT>
-hipError_t launch_mt(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const _Float16* x,
-                     const float* inv_scale, void* y, int y_dtype, hipStream_t s) {
-    return launch_cfg<MT, 8, 2>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
+hipError_t launch_mt(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine, int affine_one,
+                     int64_t M, const _Float16* x, const float* inv_scale, void* y, int y_dtype, hipStream_t s) {
+    if (affine) return launch_cfg<MT, 8, 2, true>(N, K, packed, affine, affine_one, M, x, inv_scale, y, y_dtype, s);
+    return launch_cfg<MT, 8, 2, false>(N, K, packed, nullptr, 0, M, x, inv_scale, y, y_dtype, s);
 }
 
 }  // namespace
 
-hipError_t launch_skinny(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const _Float16* x,
-                         const float* inv_scale, void* y, int y_dtype, hipStream_t s) {
-    if (M <= 16) return launch_mt<1>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
-    return launch_mt<2>(N, K, packed, M, x, inv_scale, y, y_dtype, s);
+hipError_t launch_skinny(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine, int affine_one,
+                         int64_t M, const _Float16* x, const float* inv_scale, void* y, int y_dtype,
+                         hipStream_t s) {
+    if (M <= 16) return launch_mt<1>(N, K, packed, affine, affine_one, M, x, inv_scale, y, y_dtype, s);
+    return launch_mt<2>(N, K, packed, affine, affine_one, M, x, inv_scale, y, y_dtype, s);
 }
 
 }  // namespace unisvq

@@ -22,13 +22,21 @@ STATUS = {0: "UNISVQ_OK", -1: "UNISVQ_EINVAL", -2: "UNISVQ_ESHAPE", -3: "UNISVQ_
 
 EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "unisvq_pack",
            "unisvq_unpack", "unisvq_gemv", "unisvq_gemv_batched", "unisvq_gemm_workspace_bytes",
-           "unisvq_gemm")
+           "unisvq_gemm", "unisvq_codes_bytes", "unisvq_shared_affine_bytes", "unisvq_pack_shared",
+           "unisvq_unpack_shared", "unisvq_gemv_shared", "unisvq_gemv_shared_batched", "unisvq_gemm_shared")
 MAX_BATCH = 8
 
 
 class GemvProblem(ctypes.Structure):
     """Mirror of unisvq_gemv_problem."""
     _fields_ = [("N", ctypes.c_int64), ("K", ctypes.c_int64), ("packed", ctypes.c_void_p),
+                ("x", ctypes.c_void_p), ("y", ctypes.c_void_p)]
+
+
+class GemvSharedProblem(ctypes.Structure):
+    """Mirror of unisvq_gemv_shared_problem."""
+    _fields_ = [("N", ctypes.c_int64), ("K", ctypes.c_int64), ("affine_groups", ctypes.c_int64),
+                ("packed_codes", ctypes.c_void_p), ("packed_affine", ctypes.c_void_p),
                 ("x", ctypes.c_void_p), ("y", ctypes.c_void_p)]
 
 
@@ -73,6 +81,20 @@ def load():
     lib.unisvq_gemm_workspace_bytes.restype = sz
     lib.unisvq_gemm.argtypes = [i64, i64, p, i64, p, i32, p, i32, p, sz, p]
     lib.unisvq_gemm.restype = i32
+    lib.unisvq_codes_bytes.argtypes = [i64, i64]
+    lib.unisvq_codes_bytes.restype = sz
+    lib.unisvq_shared_affine_bytes.argtypes = [i64, i64]
+    lib.unisvq_shared_affine_bytes.restype = sz
+    lib.unisvq_pack_shared.argtypes = [i64, i64, i64, p, p, p, p, p, p, p]
+    lib.unisvq_pack_shared.restype = i32
+    lib.unisvq_unpack_shared.argtypes = [i64, i64, i64, p, p, p, p, p, p]
+    lib.unisvq_unpack_shared.restype = i32
+    lib.unisvq_gemv_shared.argtypes = [i64, i64, i64, p, p, i64, p, i32, p, i32, p]
+    lib.unisvq_gemv_shared.restype = i32
+    lib.unisvq_gemv_shared_batched.argtypes = [ctypes.POINTER(GemvSharedProblem), i32, i64, i32, i32, p]
+    lib.unisvq_gemv_shared_batched.restype = i32
+    lib.unisvq_gemm_shared.argtypes = [i64, i64, i64, p, p, i64, p, i32, p, i32, p, sz, p]
+    lib.unisvq_gemm_shared.restype = i32
     _lib = lib
     return lib
 
@@ -219,3 +241,107 @@ def gemm(packed, N: int, K: int, x, out=None, out_dtype=None, workspace=None, st
         ws_bytes = need
     return _product("unisvq_gemm", N, K, packed, x, out, out_dtype, stream,
                     extra=(_ptr(workspace), ws_bytes))
+
+
+# ------------------------------------------------ row-shared affine parameters
+
+def codes_bytes(N: int, K: int) -> int:
+    return load().unisvq_codes_bytes(N, K)
+
+
+def shared_affine_bytes(K: int, affine_groups: int) -> int:
+    return load().unisvq_shared_affine_bytes(K, affine_groups)
+
+
+def pack_shared(codes, A, B, out_codes=None, out_affine=None, bad_codes=None, stream=None):
+    """codes uint8 [N][K]; A fp16 [Ga][4][4]; B fp16 [Ga][4] (Ga = 1 or K/128)
+    -> (packed codes, packed shared affine block), uint8 device tensors."""
+    torch = _torch()
+    _need_cuda(codes, A, B, out_codes, out_affine, bad_codes)
+    N, K = codes.shape
+    Ga = A.shape[0]
+    if out_codes is None:
+        out_codes = torch.empty(codes_bytes(N, K), dtype=torch.uint8, device=codes.device)
+    if out_affine is None:
+        out_affine = torch.empty(max(shared_affine_bytes(K, Ga), 16), dtype=torch.uint8, device=codes.device)
+    _check("unisvq_pack_shared", load().unisvq_pack_shared(
+        N, K, Ga, _ptr(codes.contiguous()), _ptr(A.contiguous()), _ptr(B.contiguous()), _ptr(out_codes),
+        _ptr(out_affine), _ptr(bad_codes), _stream(stream)))
+    return out_codes, out_affine
+
+
+def unpack_shared(packed_codes, packed_affine, N: int, K: int, affine_groups: int, stream=None):
+    """Inverse of pack_shared: (codes uint8 [N][K], A fp16 [Ga][4][4], B fp16 [Ga][4])."""
+    torch = _torch()
+    _need_cuda(packed_codes, packed_affine)
+    dev = packed_codes.device
+    codes = torch.empty((N, K), dtype=torch.uint8, device=dev)
+    A = torch.empty((affine_groups, DIM, DIM), dtype=torch.float16, device=dev)
+    B = torch.empty((affine_groups, DIM), dtype=torch.float16, device=dev)
+    _check("unisvq_unpack_shared", load().unisvq_unpack_shared(
+        N, K, affine_groups, _ptr(packed_codes), _ptr(packed_affine), _ptr(codes), _ptr(A), _ptr(B),
+        _stream(stream)))
+    return codes, A, B
+
+
+def _shared_product(fn_name, N, K, affine_groups, packed_codes, packed_affine, x, out, out_dtype, stream,
+                    extra=()):
+    torch = _torch()
+    _need_cuda(packed_codes, packed_affine, x, out)
+    x2 = x if x.dim() == 2 else x.reshape(-1, K)
+    if not x2.is_contiguous():
+        raise ValueError("x must be contiguous")
+    M = x2.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=out_dtype or x.dtype, device=x.device)
+    fn = getattr(load(), fn_name)
+    _check(fn_name, fn(N, K, affine_groups, _ptr(packed_codes), _ptr(packed_affine), M, _ptr(x2),
+                       _dtype_code(x2.dtype), _ptr(out), _dtype_code(out.dtype), *extra, _stream(stream)))
+    return out
+
+
+def gemv_shared(packed_codes, packed_affine, N: int, K: int, affine_groups: int, x, out=None, out_dtype=None,
+                stream=None):
+    """Decode-phase product with codes-only weights and row-shared pairs (M <= 4)."""
+    return _shared_product("unisvq_gemv_shared", N, K, affine_groups, packed_codes, packed_affine, x, out,
+                           out_dtype, stream)
+
+
+def gemv_shared_batched(problems, out_dtype=None, stream=None):
+    """problems: sequence of (packed_codes, packed_affine, N, K, affine_groups, x, out-or-None)."""
+    torch = _torch()
+    if not 1 <= len(problems) <= MAX_BATCH:
+        raise ValueError(f"1..{MAX_BATCH} problems per call")
+    arr = (GemvSharedProblem * len(problems))()
+    outs, M, xdt = [], None, None
+    for i, (pc, pa, N, K, ga, x, out) in enumerate(problems):
+        _need_cuda(pc, pa, x, out)
+        x2 = x if x.dim() == 2 else x.reshape(-1, K)
+        if not x2.is_contiguous():
+            raise ValueError("x must be contiguous")
+        if M is None:
+            M, xdt = x2.shape[0], x2.dtype
+        if x2.shape[0] != M or x2.dtype != xdt:
+            raise ValueError("all problems need the same token count and activation dtype")
+        if out is None:
+            out = torch.empty((M, N), dtype=out_dtype or xdt, device=x.device)
+        outs.append(out)
+        arr[i] = GemvSharedProblem(N, K, ga, pc.data_ptr(), pa.data_ptr(), x2.data_ptr(), out.data_ptr())
+    if len({o.dtype for o in outs}) != 1:
+        raise ValueError("all outputs need the same dtype")
+    _check("unisvq_gemv_shared_batched", load().unisvq_gemv_shared_batched(
+        arr, len(problems), M, _dtype_code(xdt), _dtype_code(outs[0].dtype), _stream(stream)))
+    return outs
+
+
+def gemm_shared(packed_codes, packed_affine, N: int, K: int, affine_groups: int, x, out=None, out_dtype=None,
+                workspace=None, stream=None):
+    """Prefill product with codes-only weights and row-shared pairs (any M)."""
+    M = x.numel() // K
+    need = gemm_workspace_bytes(N, K, M, x.dtype)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if need and workspace is None:
+        workspace = _torch().empty(need, dtype=_torch().uint8, device=x.device)
+        ws_bytes = need
+    return _shared_product("unisvq_gemm_shared", N, K, affine_groups, packed_codes, packed_affine, x, out,
+                           out_dtype, stream, extra=(_ptr(workspace), ws_bytes))

@@ -13,6 +13,9 @@ vectors of d = 4 consecutive columns):
   X        [M][K]           N(0, 1) in fp64; for the outlier workload 1% of the
                             input channels (chosen without replacement) are
                             scaled by 20; rounded to fp16 or bf16 (RNE)
+  Row-shared pairs (the paper's one pair per matrix, or one per group shared
+  by the rows): Q as above, then A fp16 [Ga][4][4] and B fp16 [Ga][4] drawn
+  the same way, Ga = 1 or K/128.
 Uniform codes match the paper's uniform-code assumption (App. A.1) and
 N(0, 1) activations match the post-Hadamard picture of Sec. 3.2.1; the
 real-model weights and calibration data of the paper are not used.
@@ -74,6 +77,17 @@ def gen_weights(N: int, K: int, seed: int, a_std: float = 0.02, b_std: float = 0
     Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
     A = (rng.standard_normal((N, K // GROUP, D, D)) * a_std).astype(np.float16)
     B = (rng.standard_normal((N, K // GROUP, D)) * b_std).astype(np.float16)
+    return Q, A, B
+
+
+def gen_shared_weights(N: int, K: int, affine_groups: int, seed: int, a_std: float = 0.02, b_std: float = 0.01):
+    """Codes and row-shared affine pairs (Ga = affine_groups = 1 or K/128)."""
+    if K % GROUP or affine_groups not in (1, K // GROUP):
+        raise ValueError("K must be a multiple of 128 and affine_groups 1 or K/128")
+    rng = np.random.default_rng(seed)
+    Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+    A = (rng.standard_normal((affine_groups, D, D)) * a_std).astype(np.float16)
+    B = (rng.standard_normal((affine_groups, D)) * b_std).astype(np.float16)
     return Q, A, B
 
 

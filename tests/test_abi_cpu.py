@@ -152,3 +152,71 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(u, "LIB_PATH", str(tmp_path / "libunisvq.so"))
     with pytest.raises(u.UniSVQLibraryMissing):
         u.load()
+
+
+# ------------------------------------------------ row-shared affine parameters
+
+@pytest.mark.parametrize("N,K,expect", [(16, 128, 512), (4096, 4096, 4096 * 4096 // 4), (11008, 4096, 11_272_192),
+                                        (15, 128, 0), (16, 100, 0), (0, 128, 0)])
+def test_codes_bytes(N, K, expect):
+    assert u.load().unisvq_codes_bytes(N, K) == expect
+
+
+@pytest.mark.parametrize("K,ga,expect", [(128, 1, 80), (128, 1, 80), (4096, 1, 80), (4096, 32, 16 * 80),
+                                         (384, 3, 2 * 80), (11008, 86, 43 * 80), (4096, 2, 0), (4096, 0, 0),
+                                         (100, 1, 0), (0, 1, 0)])
+def test_shared_affine_bytes(K, ga, expect):
+    assert u.load().unisvq_shared_affine_bytes(K, ga) == expect
+
+
+def test_pack_shared_validation():
+    lib = u.load()
+    assert lib.unisvq_pack_shared(16, 256, 1, None, GOOD, GOOD, GOOD, GOOD, None, None) == EINVAL
+    assert lib.unisvq_pack_shared(16, 256, 1, GOOD, GOOD, GOOD, GOOD, None, None, None) == EINVAL
+    assert lib.unisvq_pack_shared(16, 256, 3, GOOD, GOOD, GOOD, GOOD, GOOD, None, None) == EINVAL
+    assert lib.unisvq_pack_shared(17, 256, 1, GOOD, GOOD, GOOD, GOOD, GOOD, None, None) == ESHAPE
+    assert lib.unisvq_pack_shared(16, 256, 2, GOOD, GOOD, GOOD, GOOD + 8, GOOD, None, None) == EALIGN
+    assert lib.unisvq_pack_shared(16, 256, 2, GOOD, GOOD, GOOD, GOOD, GOOD + 4, None, None) == EALIGN
+    assert lib.unisvq_unpack_shared(16, 256, 5, GOOD, GOOD, GOOD, GOOD, GOOD, None) == EINVAL
+    assert lib.unisvq_unpack_shared(16, 250, 1, GOOD, GOOD, GOOD, GOOD, GOOD, None) == ESHAPE
+    assert lib.unisvq_unpack_shared(16, 256, 1, GOOD, GOOD + 2, GOOD, GOOD, GOOD, None) == EALIGN
+
+
+@pytest.mark.parametrize("fn", ["gemv", "gemm"])
+def test_shared_product_validation(fn):
+    lib = u.load()
+
+    def call(N=64, K=256, ga=1, pc=GOOD, pa=GOOD, M=1, x=GOOD, xt=u.F16, y=GOOD, yt=u.F16, ws_bytes=0):
+        if fn == "gemv":
+            return lib.unisvq_gemv_shared(N, K, ga, pc, pa, M, x, xt, y, yt, None)
+        return lib.unisvq_gemm_shared(N, K, ga, pc, pa, M, x, xt, y, yt, None, ws_bytes, None)
+
+    assert call(pc=None) == EINVAL
+    assert call(pa=None) == EINVAL
+    assert call(x=None) == EINVAL
+    assert call(M=0) == EINVAL
+    assert call(ga=3) == EINVAL
+    assert call(ga=0) == EINVAL
+    assert call(xt=u.F32) == EINVAL
+    assert call(N=60) == ESHAPE
+    assert call(K=200) == ESHAPE
+    assert call(pc=GOOD + 8) == EALIGN
+    assert call(pa=GOOD + 8) == EALIGN
+    assert call(y=GOOD + 1) == EALIGN
+    if fn == "gemv":
+        assert call(M=5) == EUNSUP
+    else:
+        # bf16 activations need the workspace; none given
+        assert call(xt=u.BF16, M=64) == EWS
+        assert call(xt=u.BF16, K=65664, M=64) == EUNSUP
+
+
+def test_shared_batched_validation():
+    lib = u.load()
+    arr = (u.GemvSharedProblem * 2)()
+    arr[0] = u.GemvSharedProblem(64, 256, 1, GOOD, GOOD, GOOD, GOOD)
+    arr[1] = u.GemvSharedProblem(64, 256, 5, GOOD, GOOD, GOOD, GOOD)
+    assert lib.unisvq_gemv_shared_batched(arr, 2, 1, u.F16, u.F16, None) == EINVAL
+    assert lib.unisvq_gemv_shared_batched(arr, 0, 1, u.F16, u.F16, None) == EINVAL
+    assert lib.unisvq_gemv_shared_batched(None, 1, 1, u.F16, u.F16, None) == EINVAL
+    assert lib.unisvq_gemv_shared_batched(arr, 9, 1, u.F16, u.F16, None) == EUNSUP

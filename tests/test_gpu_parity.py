@@ -407,3 +407,136 @@ def test_graph_replays_match_eager():
         assert torch.equal(y1, e1), rep
         assert torch.equal(y64, e64), rep
         assert torch.equal(junk, u.gemv(pk, N, K, x1 * 2))
+
+
+# ------------------------------------------- row-shared affine parameters
+
+def upload_shared(Q, A, B):
+    pc, pa = u.pack_shared(torch.from_numpy(Q).to(DEV), dev_u16_as_half(A), dev_u16_as_half(B))
+    torch.cuda.synchronize()
+    return pc, pa
+
+
+def expected_affine_block(A, B, K):
+    """The shared affine block built from its definition in unisvq.h."""
+    Ga, groups = A.shape[0], K // 128
+    recs = 1 if Ga == 1 else (groups + 1) // 2
+    out = np.zeros(recs * 80, np.uint8)
+    Ab, Bb = A.view(np.uint16), B.view(np.uint16)
+    for R in range(recs):
+        for j in range(2):
+            g = 2 * R + j
+            if Ga == 1:
+                src = 0
+            elif g < groups:
+                src = g
+            else:
+                continue
+            for b in range(4):
+                for a in range(4):
+                    off = R * 80 + 16 * b + 8 * j + 2 * a
+                    out[off:off + 2] = np.frombuffer(int(Ab[src, a, b]).to_bytes(2, "little"), np.uint8)
+                off = R * 80 + 64 + 4 * b + 2 * j
+                out[off:off + 2] = np.frombuffer(int(Bb[src, b]).to_bytes(2, "little"), np.uint8)
+    return out
+
+
+@pytest.mark.parametrize("N,K", [(16, 128), (32, 384), (64, 1024), (48, 1152)])
+@pytest.mark.parametrize("per_group", [False, True])
+def test_pack_shared_bit_exact(N, K, per_group):
+    Ga = K // 128 if per_group else 1
+    Q, A, B = wl.gen_shared_weights(N, K, Ga, seed=N + K)
+    pc, pa = upload_shared(Q, A, B)
+    ref, bad = oracle.pack_codes(Q)
+    assert bad == 0 and np.array_equal(pc.cpu().numpy(), ref)
+    assert np.array_equal(pa.cpu().numpy()[:u.shared_affine_bytes(K, Ga)], expected_affine_block(A, B, K))
+    q2, a2, b2 = u.unpack_shared(pc, pa, N, K, Ga)
+    torch.cuda.synchronize()
+    assert np.array_equal(q2.cpu().numpy(), Q)
+    assert np.array_equal(a2.cpu().numpy().view(np.uint16), A.view(np.uint16))
+    assert np.array_equal(b2.cpu().numpy().view(np.uint16), B.view(np.uint16))
+
+
+def run_shared(fn, N, K, M, Ga, dtype="f16", out=torch.float32, seed=0, outliers=False):
+    Q, A, B = wl.gen_shared_weights(N, K, Ga, seed=seed)
+    xb = wl.gen_activations(M, K, seed=wl.activation_seed(seed, M), dtype=dtype, outliers=outliers)
+    pc, pa = upload_shared(Q, A, B)
+    y = getattr(u, fn)(pc, pa, N, K, Ga, dev_x(xb, dtype), out_dtype=out)
+    torch.cuda.synchronize()
+    return y, (Q, A, B), xb
+
+
+@pytest.mark.parametrize("N,K,M", [(16, 128, 1), (32, 384, 1), (64, 1152, 2), (256, 4096, 1), (48, 640, 3),
+                                   (64, 512, 4), (1024, 8192, 1)])
+@pytest.mark.parametrize("per_group", [False, True])
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_gemv_shared_parity(N, K, M, per_group, dtype):
+    Ga = K // 128 if per_group else 1
+    y, (Q, A, B), xb = run_shared("gemv_shared", N, K, M, Ga, dtype, seed=N + M)
+    ref = oracle.matmul_shared(oracle.pack_codes(Q)[0], N, K, A, B, x_as_f64(xb, dtype))
+    assert rel_err(y.cpu().numpy(), ref) <= 1e-5
+
+
+@pytest.mark.parametrize("layer", wl.LLAMA7B[3:], ids=lambda l: l.name)
+def test_gemv_shared_llama7b_one_pair_per_matrix(layer):
+    """The paper's setting at the 7B shapes: one pair per matrix, fp16 outputs."""
+    y, (Q, A, B), xb = run_shared("gemv_shared", layer.N, layer.K, 1, 1, "f16", out=torch.float16, seed=50)
+    rows = np.random.default_rng(2).choice(layer.N, 256, replace=False)
+    rows[:2] = [0, layer.N - 1]
+    ref = oracle.matmul_shared(oracle.pack_codes(Q)[0], layer.N, layer.K, A, B, x_as_f64(xb, "f16"), rows=rows)
+    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 2e-3
+
+
+@pytest.mark.parametrize("fn", ["gemv", "gemm"])
+@pytest.mark.parametrize("per_group", [False, True])
+def test_shared_equals_full_format_with_copied_pairs(fn, per_group):
+    """Codes-only weights with shared pairs give bit for bit what the full
+    format gives when every row holds copies of the pairs (same decode, same
+    accumulation order)."""
+    N, K, M = 128, 1408, (3 if fn == "gemv" else 80)
+    Ga = K // 128 if per_group else 1
+    Q, A, B = wl.gen_shared_weights(N, K, Ga, seed=8)
+    src = np.arange(K // 128) if per_group else np.zeros(K // 128, np.int64)
+    Af = np.broadcast_to(A[src], (N, K // 128, 4, 4)).copy()
+    Bf = np.broadcast_to(B[src], (N, K // 128, 4)).copy()
+    xb = wl.gen_activations(M, K, seed=9, dtype="f16")
+    x = dev_x(xb, "f16")
+    pc, pa = upload_shared(Q, A, B)
+    y_s = getattr(u, fn + "_shared")(pc, pa, N, K, Ga, x, out_dtype=torch.float32)
+    y_f = getattr(u, fn)(upload_pack(Q, Af, Bf), N, K, x, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert torch.equal(y_s, y_f)
+
+
+def test_gemv_shared_batched_matches_single_calls():
+    probs, singles = [], []
+    for i, (N, K, ga) in enumerate([(64, 512, 1), (128, 384, 3), (32, 1024, 8)]):
+        Q, A, B = wl.gen_shared_weights(N, K, ga, seed=60 + i)
+        pc, pa = upload_shared(Q, A, B)
+        x = dev_x(wl.gen_activations(2, K, seed=70 + i, dtype="f16"), "f16")
+        probs.append((pc, pa, N, K, ga, x, None))
+        singles.append(u.gemv_shared(pc, pa, N, K, ga, x, out_dtype=torch.float32))
+    outs = u.gemv_shared_batched(probs, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    for a, b in zip(outs, singles):
+        assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("N,K,M", [(16, 128, 1), (64, 384, 20), (64, 256, 33), (80, 640, 64), (128, 1152, 130),
+                                   (256, 4096, 7)])
+@pytest.mark.parametrize("per_group", [False, True])
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_gemm_shared_parity(N, K, M, per_group, dtype):
+    Ga = K // 128 if per_group else 1
+    y, (Q, A, B), xb = run_shared("gemm_shared", N, K, M, Ga, dtype, seed=N + M + 1)
+    ref = oracle.matmul_shared(oracle.pack_codes(Q)[0], N, K, A, B, x_as_f64(xb, dtype))
+    assert rel_err(y.cpu().numpy(), ref) <= 5e-4
+
+
+def test_gemm_shared_prefill_m2048_sampled_rows():
+    layer = wl.PREFILL7B[0]
+    y, (Q, A, B), xb = run_shared("gemm_shared", layer.N, layer.K, 2048, 1, "bf16", seed=21)
+    rows = np.random.default_rng(3).choice(layer.N, 48, replace=False)
+    rows[:2] = [0, layer.N - 1]
+    ref = oracle.matmul_shared(oracle.pack_codes(Q)[0], layer.N, layer.K, A, B, x_as_f64(xb, "bf16"), rows=rows)
+    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 5e-4
