@@ -34,8 +34,20 @@ MALL_BYTES = 256 << 20
 METRIC = "2-bit GEMV achieved HBM GB/s (% peak) + µs/layer at 7B shapes, M=1"
 
 
-def algorithmic_bytes(N: int, K: int, M: int, x_bytes: int = 2, y_bytes: int = 2) -> int:
-    return N * K // 4 + N * (K // 128) * 40 + M * K * x_bytes + M * N * y_bytes
+def affine_groups(K: int, affine: str) -> int:
+    """Pairs of a row-shared mode: 1 per matrix, or one per 128-column group."""
+    return 1 if affine == "matrix" else K // 128
+
+
+def algorithmic_bytes(N: int, K: int, M: int, x_bytes: int = 2, y_bytes: int = 2, affine: str = "row_group") -> int:
+    """Codes + affine parameters + activations + outputs.  Row-shared pairs
+    are read from their packed block of 80-byte records (one per two groups,
+    a single one for a per-matrix pair)."""
+    if affine == "row_group":
+        par = N * (K // 128) * 40
+    else:
+        par = 80 if affine == "matrix" else 80 * ((K // 128 + 1) // 2)
+    return N * K // 4 + par + M * K * x_bytes + M * N * y_bytes
 
 
 def parse():
@@ -47,6 +59,10 @@ def parse():
                    choices=["llama7b_decode_m1", "layer4096_m1", "llama70b_decode_m1",
                             "llama70b_decode_m16", "llama7b_smallbatch_m4", "llama7b_smallbatch_m16",
                             "llama7b_smallbatch_m64", "llama7b_prefill_m2048"])
+    p.add_argument("--affine", default="row_group", choices=["row_group", "matrix", "group"],
+                   help="row_group: one (A, B) pair per (row, 128-column group), stored with the codes (the "
+                        "default workload); matrix: one pair per weight matrix shared by all rows (the paper's "
+                        "setting), codes-only weights; group: one pair per 128-column group shared by the rows")
     p.add_argument("--schedule", default="decoder", choices=["decoder", "per_layer", "single"],
                    help="decoder: q/k/v in one batched launch, o, gate/up in one batched launch, down "
                         "(how a decode step runs them); per_layer: one launch per linear; single: all "
@@ -70,7 +86,8 @@ def kernel_source_hash(kernel: str) -> str:
 
 def measured_traffic(kernel: str, workload: str, schedule: str):
     """HBM bytes per launch from the committed counter summary, if it was taken
-    on the current kernel source; else None."""
+    on the current kernel source; else None.  (workload carries a suffix for
+    the row-shared modes.)"""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_{schedule}_traffic.json")
     if not os.path.exists(path):
         return None
@@ -127,28 +144,39 @@ def main():
     dev = torch.device("cuda:0")
     layers, M, xdt, outliers, kernel = workload_spec(args.workload)
     tdt = torch.float16 if xdt == "f16" else torch.bfloat16
+    shared = args.affine != "row_group"
+    wname = args.workload if not shared else f"{args.workload}_{args.affine}_shared"
 
     # ---- inputs: canonical arrays drawn on the host, packed on the GPU
     canon = []
     for li, L in enumerate(layers):
-        Q, A, B = wl.gen_weights(L.N, L.K, seed=li)
+        if shared:
+            Q, A, B = wl.gen_shared_weights(L.N, L.K, affine_groups(L.K, args.affine), seed=li)
+        else:
+            Q, A, B = wl.gen_weights(L.N, L.K, seed=li)
         xb = wl.gen_activations(M, L.K, seed=wl.activation_seed(li, M), dtype=xdt, outliers=outliers)
         canon.append((Q, A, B, xb))
-    set_bytes = sum(algorithmic_bytes(L.N, L.K, M) for L in layers)
-    set_packed = sum(u.packed_bytes(L.N, L.K) for L in layers)
+    set_bytes = sum(algorithmic_bytes(L.N, L.K, M, affine=args.affine) for L in layers)
+    set_packed = sum((u.codes_bytes(L.N, L.K) if shared else u.packed_bytes(L.N, L.K)) for L in layers)
     copies = max(2, -(-2 * MALL_BYTES // set_packed) + 1)
+
+    def dev_half(a):
+        return torch.from_numpy(a.view(np.int16)).view(torch.float16).to(dev)
 
     packed0 = []
     for (Q, A, B, _), L in zip(canon, layers):
-        pk = u.pack(torch.from_numpy(Q).to(dev),
-                    torch.from_numpy(A.view(np.int16)).view(torch.float16).to(dev),
-                    torch.from_numpy(B.view(np.int16)).view(torch.float16).to(dev))
-        packed0.append(pk)
+        if shared:
+            packed0.append(u.pack_shared(torch.from_numpy(Q).to(dev), dev_half(A), dev_half(B)))
+        else:
+            packed0.append(u.pack(torch.from_numpy(Q).to(dev), dev_half(A), dev_half(B)))
     sets = []
     for c in range(copies):
         s = []
         for li, L in enumerate(layers):
-            pk = packed0[li] if c == 0 else packed0[li].clone()
+            if shared:
+                pk = packed0[li] if c == 0 else tuple(t.clone() for t in packed0[li])
+            else:
+                pk = packed0[li] if c == 0 else packed0[li].clone()
             x = torch.from_numpy(canon[li][3].view(np.int16)).view(tdt).to(dev)
             y = torch.empty((M, L.N), dtype=torch.float16, device=dev)
             s.append((L, pk, x, y))
@@ -183,6 +211,13 @@ def main():
             for grp in groups_:
                 if len(grp) == 1:
                     cc.append(("+".join(grp), by[grp[0]]))
+                elif shared:
+                    arr = (u.GemvSharedProblem * len(grp))()
+                    for i, n in enumerate(grp):
+                        L, (pc, pa), x, y = by[n]
+                        arr[i] = u.GemvSharedProblem(L.N, L.K, affine_groups(L.K, args.affine), pc.data_ptr(),
+                                                     pa.data_ptr(), x.data_ptr(), y.data_ptr())
+                    cc.append(("+".join(grp), arr))
                 else:
                     arr = (u.GemvProblem * len(grp))()
                     for i, n in enumerate(grp):
@@ -193,6 +228,16 @@ def main():
         return calls
 
     def launch(item, sptr):
+        if isinstance(item, tuple) and shared:
+            L, (pc, pa), x, y = item
+            ga = affine_groups(L.K, args.affine)
+            if kernel == "gemv":
+                return lib.unisvq_gemv_shared(L.N, L.K, ga, pc.data_ptr(), pa.data_ptr(), M, x.data_ptr(), xcode,
+                                              y.data_ptr(), u.F16, sptr)
+            return lib.unisvq_gemm_shared(L.N, L.K, ga, pc.data_ptr(), pa.data_ptr(), M, x.data_ptr(), xcode,
+                                          y.data_ptr(), u.F16, ws.data_ptr(), ws_bytes, sptr)
+        if shared:
+            return lib.unisvq_gemv_shared_batched(item, len(item), M, xcode, u.F16, sptr)
         if isinstance(item, tuple):
             L, pk, x, y = item
             if kernel == "gemv":
@@ -312,7 +357,7 @@ def main():
     bytes_per_launch = set_bytes / launches_per_step
     if kernel == "gemv":
         ach = bytes_per_launch / (avg_us * 1e-6) / 1e9
-        traffic = measured_traffic("gemv", args.workload, sched)
+        traffic = measured_traffic("gemv", wname, sched)
         roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                     "frac": round(ach / PEAK_HBM_GBS, 4),
                     "traffic": None if traffic is None else int(traffic),
@@ -321,7 +366,7 @@ def main():
     elif M <= 64:
         # small batch: still bound by the weight stream
         ach = bytes_per_launch / (avg_us * 1e-6) / 1e9
-        traffic = measured_traffic("gemm", args.workload, sched)
+        traffic = measured_traffic("gemm", wname, sched)
         roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                     "frac": round(ach / PEAK_HBM_GBS, 4),
                     "traffic": None if traffic is None else int(traffic),
@@ -330,7 +375,7 @@ def main():
     else:
         flops = sum(2 * M * L.N * L.K for L in layers) / launches_per_step
         ach = flops / (avg_us * 1e-6) / 1e12
-        traffic = measured_traffic("gemm", args.workload, sched)
+        traffic = measured_traffic("gemm", wname, sched)
         roofline = {"bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS,
                     "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
                     "traffic": None if traffic is None else int(traffic),
@@ -341,7 +386,10 @@ def main():
     if not args.no_cpu_baseline:
         import oracle
         threads = oracle.default_threads()
-        packed_h = [oracle.pack(Q, A, B)[0] for (Q, A, B, _) in canon]
+        if shared:
+            packed_h = [oracle.pack_codes(Q)[0] for (Q, A, B, _) in canon]
+        else:
+            packed_h = [oracle.pack(Q, A, B)[0] for (Q, A, B, _) in canon]
         xs = [oracle.half_to_double(xb) if xdt == "f16" else oracle.bf16_to_double(xb) for (_, _, _, xb) in canon]
         rows_frac = 1.0
         if M > 16:  # prefill: a bounded slice of output rows per layer
@@ -352,9 +400,13 @@ def main():
                 nrows = max(16, int(L.N * rows_frac))
                 rows = None if nrows >= L.N else np.arange(nrows)
                 s0 = time.perf_counter()
-                oracle.matmul(packed_h[li], L.N, L.K, xs[li], rows=rows, threads=threads)
+                if shared:
+                    oracle.matmul_shared(packed_h[li], L.N, L.K, canon[li][1], canon[li][2], xs[li], rows=rows,
+                                         threads=threads)
+                else:
+                    oracle.matmul(packed_h[li], L.N, L.K, xs[li], rows=rows, threads=threads)
                 t_cpu += time.perf_counter() - s0
-                done_bytes += algorithmic_bytes(L.N, L.K, M) * (nrows / L.N)
+                done_bytes += algorithmic_bytes(L.N, L.K, M, affine=args.affine) * (nrows / L.N)
             passes += 1
         cpu = {"value": round(done_bytes / t_cpu / 1e9, 3), "unit": "GB/s", "cores": threads,
                "kind": "oracle",
@@ -363,7 +415,10 @@ def main():
                          + f", fp64 C oracle, {threads} threads, {t_cpu:.1f} s"}
 
     if kernel == "gemv" or M <= 64:
-        metric, value, unit = METRIC if M == 1 else f"2-bit decode achieved HBM GB/s at M={M}", value_gbs, "GB/s"
+        metric = METRIC if (M == 1 and not shared) else f"2-bit decode achieved HBM GB/s at M={M}"
+        if shared:
+            metric += f" (codes-only, one (A, B) pair per {'matrix' if args.affine == 'matrix' else 'group'})"
+        value, unit = value_gbs, "GB/s"
     else:
         flops = sum(2 * M * L.N * L.K for L in layers)
         metric, value, unit = "unisvq_gemm effective TFLOP/s (2MNK)", flops / (ms_per_step * 1e-3) / 1e12, "TFLOP/s"
@@ -383,7 +438,7 @@ def main():
         "dtype": "f16" if (xdt == "f16" or kernel == "gemm") else "bf16",
         "data": "synthetic",
         "config": {"workload": args.workload, "layers": {L.name: [L.N, L.K] for L in layers}, "M": M,
-                   "activations": xdt,
+                   "activations": xdt, "affine": args.affine,
                    "d": 4, "bits": 2, "group": 128, "kernel": kernel, "schedule": sched,
                    "launches_per_step": len(groups_), "buffer_copies": copies,
                    "set_bytes": set_bytes},
