@@ -67,6 +67,8 @@ def _load():
     lib.oracle_unpack_codes.restype = ctypes.c_int
     lib.oracle_matmul_shared_rows.argtypes = [i64, i64, p, i64, p, p, i64, p, i64, p, p, ctypes.c_int]
     lib.oracle_matmul_shared_rows.restype = ctypes.c_int
+    lib.oracle_quantize.argtypes = [i64, i64, p, p, p, i64, p]
+    lib.oracle_quantize.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -246,3 +248,22 @@ def matmul_shared(packed_codes: np.ndarray, N: int, K: int, As: np.ndarray, Bs: 
         _check(lib.oracle_matmul_shared_rows(N, K, _ptr(packed_codes), Ga, _ptr(Ab), _ptr(Bb), M, _ptr(X),
                                              r.size, _ptr(r), _ptr(Y), threads), "matmul_shared_rows")
     return Y
+
+
+# ------------------------------------------------ nearest-codeword quantiser
+
+def quantize(W: np.ndarray, A: np.ndarray, B: np.ndarray, shared: bool = False) -> np.ndarray:
+    """Codes of the nearest codeword A q + B per vector of W (fp32 [N][K]).
+
+    A/B per (row, group) ([N][K/128][4][4] / [N][K/128][4]), or with
+    ``shared`` row-shared ([Ga][4][4] / [Ga][4], Ga = 1 or K/128).  Distances
+    in fp64 with a fixed operation order; ties to the lowest index
+    q0 + 4 q1 + 16 q2 + 64 q3."""
+    lib = _load()
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    N, K = W.shape
+    Ab, Bb = _bits16(A), _bits16(B)
+    Ga = Ab.shape[0] if shared else 0
+    Q = np.empty((N, K), dtype=np.uint8)
+    _check(lib.oracle_quantize(N, K, _ptr(W), _ptr(Ab), _ptr(Bb), Ga, _ptr(Q)), "quantize")
+    return Q

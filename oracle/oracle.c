@@ -286,6 +286,56 @@ static void expand_shared(int64_t K, int64_t Ga, const uint16_t* As, const uint1
     }
 }
 
+/* ---- nearest-codeword quantisation (the quantiser of Sec. 3.2.2 without
+ *      Hessian feedback: each vector takes the affine-lattice point closest
+ *      to it in Euclidean distance) ---- */
+
+/* Squared distance between vector w[0..3] and the codeword A q + B of code
+ * index i (q_b = bits 2b, 2b+1 of i), in fp64 with a fixed operation order:
+ * c_a = B_a + A_a0 q_0 + A_a1 q_1 + A_a2 q_2 + A_a3 q_3 (left to right; each
+ * product of an fp16 value and a small integer is exact), e_a = c_a - w_a,
+ * d = fma(e_a, e_a, d) for a = 0..3 starting from d = 0. */
+static double codeword_dist(const double* A16, const double* B4, const double* w, int i) {
+    double d = 0.0;
+    for (int a = 0; a < OR_D; ++a) {
+        double c = B4[a];
+        for (int b = 0; b < OR_D; ++b) c = c + A16[a * OR_D + b] * (double)((i >> (2 * b)) & 3);
+        double e = c - w[a];
+        d = fma(e, e, d);
+    }
+    return d;
+}
+
+/* W fp32 [N][K]; pairs per (row, group) when Ga == 0 (A [N][K/128][4][4],
+ * B [N][K/128][4]), else row-shared (Ga = 1 or K/128, as the codes-only
+ * format).  Q [N][K] receives, per vector, the codes of the nearest codeword;
+ * ties go to the lowest index sum_b q_b 4^b. */
+int oracle_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, const uint16_t* B, int64_t Ga,
+                    uint8_t* Q) {
+    if (!W || !A || !B || !Q) return OR_EINVAL;
+    if (N <= 0 || K <= 0 || K % OR_G) return OR_ESHAPE;
+    int64_t groups = K / OR_G;
+    if (Ga != 0 && Ga != 1 && Ga != groups) return OR_ESHAPE;
+    for (int64_t r = 0; r < N; ++r) {
+        for (int64_t v = 0; v < K / OR_D; ++v) {
+            int64_t g = (OR_D * v) / OR_G;
+            int64_t set = Ga == 0 ? r * groups + g : (Ga == 1 ? 0 : g);
+            double A16[16], B4[4], w[4];
+            for (int i = 0; i < 16; ++i) A16[i] = oracle_half_to_double(A[set * 16 + i]);
+            for (int i = 0; i < 4; ++i) B4[i] = oracle_half_to_double(B[set * 4 + i]);
+            for (int i = 0; i < 4; ++i) w[i] = (double)W[r * K + OR_D * v + i];
+            int best = 0;
+            double dbest = codeword_dist(A16, B4, w, 0);
+            for (int i = 1; i < 256; ++i) {
+                double d = codeword_dist(A16, B4, w, i);
+                if (d < dbest) { dbest = d; best = i; }
+            }
+            for (int b = 0; b < OR_D; ++b) Q[r * K + OR_D * v + b] = (uint8_t)((best >> (2 * b)) & 3);
+        }
+    }
+    return OR_OK;
+}
+
 /* ---- decode (Eq. 4 applied along the input dimension as in Eq. 8) ---- */
 
 /* One row: w[k] for k = 4v + a is sum_b A[g][a][b] * q[4v + b] + B[g][a],

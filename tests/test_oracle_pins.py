@@ -417,3 +417,81 @@ def test_shared_identity_pair_is_integer_matmul():
     Bs = np.zeros((1, 4), np.float16)
     Y = oracle.matmul_shared(oracle.pack_codes(Q)[0], N, K, As, Bs, X)
     assert np.array_equal(Y, X @ Q.T.astype(np.float64))
+
+
+# ------------------------------------------- nearest-codeword quantiser (Sec. 3.2.2)
+
+def test_quantize_recovers_codes_of_on_grid_weights():
+    """W built as A q + B (exactly representable): the nearest codeword is q."""
+    rng = np.random.default_rng(101)
+    N, K = 16, 256
+    Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+    # A: multiples of 1/8 in [-2, 2] (exact in fp16), full rank with probability one
+    A = (rng.integers(-16, 17, size=(N, K // 128, 4, 4)) / 8).astype(np.float16)
+    B = (rng.integers(-16, 17, size=(N, K // 128, 4)) / 8).astype(np.float16)
+    W = oracle.decode(Q, A, B).astype(np.float32)
+    assert np.array_equal(W.astype(np.float64), oracle.decode(Q, A, B))  # exact on the grid
+    Wv = W.reshape(N, K // 4, 4)
+    got = oracle.quantize(W, A, B)
+    # vectors whose codeword is unique (A of its group nonsingular) must come back exactly
+    det = np.linalg.det(A.astype(np.float64))  # [N][G]
+    ok_vec = np.abs(det[:, (np.arange(K // 4) * 4) // 128]) > 1e-9
+    assert np.array_equal(got.reshape(N, K // 4, 4)[ok_vec], Q.reshape(N, K // 4, 4)[ok_vec])
+    assert ok_vec.mean() > 0.9
+
+
+def test_quantize_scalar_special_case_is_round_to_nearest():
+    """A = s I, B = b 1 (Eq. 2, scalar quantisation on a uniform 4-level grid):
+    per coordinate clamp(round((w - b) / s), 0, 3)."""
+    rng = np.random.default_rng(7)
+    N, K = 32, 384
+    s, b = 0.75, -1.125
+    A = np.zeros((N, K // 128, 4, 4), np.float16)
+    A[..., np.arange(4), np.arange(4)] = s
+    B = np.full((N, K // 128, 4), b, np.float16)
+    W = (rng.standard_normal((N, K)) * 1.5).astype(np.float32)
+    ref = np.clip(np.rint((W.astype(np.float64) - b) / s), 0, 3).astype(np.uint8)
+    assert np.array_equal(oracle.quantize(W, A, B), ref)
+
+
+def test_quantize_ties_go_to_the_lowest_index():
+    """A = I, B = 0 and w exactly between grid points in three coordinates:
+    the codeword with the lowest index q0 + 4 q1 + 16 q2 + 64 q3 wins."""
+    N, K = 16, 128
+    A = np.zeros((N, 1, 4, 4), np.float16)
+    A[..., np.arange(4), np.arange(4)] = 1.0
+    B = np.zeros((N, 1, 4), np.float16)
+    W = np.zeros((N, K), np.float32)
+    W[:, :4] = [0.5, 0.5, 1.5, 2.5]
+    W[:, 4:8] = [3.0, 2.5, 0.25, 1.75]
+    got = oracle.quantize(W, A, B)
+    assert got[0, :4].tolist() == [0, 0, 1, 2]
+    assert got[0, 4:8].tolist() == [3, 2, 0, 2]
+
+
+def test_quantize_no_other_code_is_closer():
+    rng = np.random.default_rng(12)
+    N, K = 16, 256
+    A = (rng.standard_normal((N, K // 128, 4, 4)) * 0.4).astype(np.float16)
+    B = (rng.standard_normal((N, K // 128, 4)) * 0.2).astype(np.float16)
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    Q = oracle.quantize(W, A, B)
+    d_best = ((oracle.decode(Q, A, B) - W.astype(np.float64)) ** 2).reshape(N, K // 4, 4).sum(-1)
+    for _ in range(64):
+        Qo = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+        d_o = ((oracle.decode(Qo, A, B) - W.astype(np.float64)) ** 2).reshape(N, K // 4, 4).sum(-1)
+        assert np.all(d_best <= d_o + 1e-12)
+
+
+@pytest.mark.parametrize("per_group", [False, True])
+def test_quantize_shared_pairs_equal_copied_pairs(per_group):
+    rng = np.random.default_rng(40 + per_group)
+    N, K = 32, 384
+    Ga = K // 128 if per_group else 1
+    As = (rng.standard_normal((Ga, 4, 4)) * 0.4).astype(np.float16)
+    Bs = (rng.standard_normal((Ga, 4)) * 0.2).astype(np.float16)
+    src = np.arange(K // 128) if per_group else np.zeros(K // 128, np.int64)
+    A = np.broadcast_to(As[src], (N, K // 128, 4, 4)).copy()
+    B = np.broadcast_to(Bs[src], (N, K // 128, 4)).copy()
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    assert np.array_equal(oracle.quantize(W, As, Bs, shared=True), oracle.quantize(W, A, B))
