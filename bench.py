@@ -58,7 +58,7 @@ def parse():
     p.add_argument("--workload", default="llama7b_decode_m1",
                    choices=["llama7b_decode_m1", "layer4096_m1", "llama70b_decode_m1",
                             "llama70b_decode_m16", "llama7b_smallbatch_m4", "llama7b_smallbatch_m16",
-                            "llama7b_smallbatch_m64", "llama7b_prefill_m2048"])
+                            "llama7b_smallbatch_m64", "llama7b_prefill_m2048", "quantize_llama7b"])
     p.add_argument("--affine", default="row_group", choices=["row_group", "matrix", "group"],
                    help="row_group: one (A, B) pair per (row, 128-column group), stored with the codes (the "
                         "default workload); matrix: one pair per weight matrix shared by all rows (the paper's "
@@ -127,10 +127,101 @@ def workload_spec(name: str):
     raise ValueError(name)
 
 
+PEAK_FP64_TFLOPS = 78.6   # MI355X fp64 vector, datasheet
+QUANT_FLOP_PER_CANDIDATE = 44  # per component: 4 multiplies, 4 adds, 1 subtract, 1 fma (2)
+
+
+def bench_quantize(args):
+    """Nearest-codeword quantiser over the 7B weight shapes: W ~ N(0, 1) fp32,
+    one pair per (row, group) from the paper's initial grid (Eq. 6: A = s G with
+    G a random orthogonal 4x4 matrix, B = -1.5 s G 1, s = sqrt(12/15), App. A.1),
+    fp16.  Reports vectors per second, the fp64 rate, and the weight SNR."""
+    import torch
+    import paper_2606_10520_amd.unisvq as u
+
+    u.load()
+    dev = torch.device("cuda:0")
+    layers = wl.LLAMA7B
+    rng = np.random.default_rng(0)
+    s = np.sqrt(12.0 / 15.0)
+    data = []
+    for li, L in enumerate(layers):
+        G = np.linalg.qr(rng.standard_normal((L.N * (L.K // 128), 4, 4)))[0]  # random orthogonal per set
+        A = (s * G).astype(np.float16).reshape(L.N, L.K // 128, 4, 4)
+        B = (-1.5 * s * G.sum(axis=2)).astype(np.float16).reshape(L.N, L.K // 128, 4)
+        W = torch.randn(L.N, L.K, device=dev, generator=torch.Generator(device=dev).manual_seed(li))
+        Ad = torch.from_numpy(A.view(np.int16)).view(torch.float16).to(dev)
+        Bd = torch.from_numpy(B.view(np.int16)).view(torch.float16).to(dev)
+        data.append((L, W, Ad, Bd, A, B, torch.empty((L.N, L.K), dtype=torch.uint8, device=dev)))
+    lib = u.load()
+    stream = torch.cuda.current_stream()
+
+    def step():
+        for (L, W, Ad, Bd, _, _, q) in data:
+            st = lib.unisvq_quantize(L.N, L.K, W.data_ptr(), Ad.data_ptr(), Bd.data_ptr(), 0, q.data_ptr(),
+                                     stream.cuda_stream)
+            if st != 0:
+                raise RuntimeError(f"unisvq_quantize failed with status {st}")
+
+    for _ in range(max(1, args.warmup // 10)):
+        step()
+    torch.cuda.synchronize()
+    steps = max(1, args.steps // 20)
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    vecs = sum(L.N * L.K // 4 for L in layers)
+    flops = vecs * 256 * QUANT_FLOP_PER_CANDIDATE
+    ach = flops / (ms * 1e-3) / 1e12
+    # weight SNR of the result, from the oracle's decode of a slice of rows
+    import oracle
+    L, W, _, _, A, B, q = data[0]
+    rows = 64
+    Wh = oracle.decode(q[:rows].cpu().numpy(), A[:rows], B[:rows])
+    W64 = W[:rows].double().cpu().numpy()
+    snr = 10 * np.log10((W64 ** 2).sum() / ((W64 - Wh) ** 2).sum())
+    cpu = None
+    if not args.no_cpu_baseline:
+        Wc = W[:16].cpu().numpy()
+        c0 = time.perf_counter()
+        n = 0
+        while time.perf_counter() - c0 < min(args.cpu_seconds, 5.0) or n == 0:
+            oracle.quantize(Wc, A[:16], B[:16])
+            n += 1
+        dt = time.perf_counter() - c0
+        cpu = {"value": round(n * 16 * L.K / 4 / dt / 1e6, 4), "unit": "Mvectors/s", "cores": 1, "kind": "oracle",
+               "sample": f"{n} pass(es) over 16 rows of {L.N}x{L.K}, fp64 C oracle, one thread, {dt:.1f} s"}
+    out = {
+        "metric": "nearest-codeword quantiser throughput (7B weight shapes)",
+        "value": round(vecs / (ms * 1e-3) / 1e9, 3), "unit": "Gvectors/s", "n_gpus": 1, "steps": steps,
+        "warmup": max(1, args.warmup // 10), "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "quantize_llama7b", "layers": {L.name: [L.N, L.K] for L in layers},
+                   "grid": "Eq. 6 initial grid, one pair per (row, group)", "vectors": vecs},
+        "weight_snr_db": round(float(snr), 2),
+        "roofline": {"bound": "alu", "achieved": round(ach, 1), "peak": PEAK_FP64_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(ach / PEAK_FP64_TFLOPS, 4), "traffic": None, "kernel": "quantize_kernel",
+                     "avg_launch_us": round(ms * 1e3 / len(layers), 3)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
+        return
+    if args.workload == "quantize_llama7b":
+        if args.gpus != 1:
+            print("bench.py measures one GPU only", file=sys.stderr)
+            sys.exit(2)
+        bench_quantize(args)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "

@@ -255,6 +255,23 @@ int unisvq_gemm_shared(int64_t N, int64_t K, int64_t affine_groups, const void* 
                        const void* packed_affine, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
                        void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---- Nearest-codeword quantisation (Sec. 3.2.2, without Hessian feedback) ----
+ * Codes of the affine-lattice point closest to each vector of d = 4
+ * consecutive weights of a row: q* = argmin over the 256 codes q of
+ * ||A q + B - w||^2, where (A, B) is the vector's pair.  The decision is taken
+ * in fp64 with a fixed operation order (c_a = B_a + A_a0 q_0 + ... + A_a3 q_3
+ * left to right, e_a = c_a - w_a, d = fma(e_a, e_a, d) for a = 0..3), and ties
+ * go to the lowest index q_0 + 4 q_1 + 16 q_2 + 64 q_3.
+ *   W              device fp32 [N][K], 16-byte aligned
+ *   A, B           device fp16 bits: affine_groups == 0 -> one pair per (row,
+ *                  group), [N][K/128][4][4] and [N][K/128][4]; affine_groups
+ *                  == 1 or K/128 -> row-shared pairs [affine_groups][4][4] and
+ *                  [affine_groups][4]; any other value: UNISVQ_EINVAL
+ *   codes          device uint8 [N][K] (0..3), 4-byte aligned; pack it with
+ *                  unisvq_pack or unisvq_pack_shared */
+int unisvq_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, const uint16_t* B,
+                    int64_t affine_groups, uint8_t* codes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

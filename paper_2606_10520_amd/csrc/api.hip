@@ -221,4 +221,17 @@ int unisvq_gemm_shared(int64_t N, int64_t K, int64_t affine_groups, const void* 
                                       x_dtype, y, y_dtype, workspace, static_cast<hipStream_t>(stream));
 }
 
+/* ---- nearest-codeword quantisation ---- */
+
+int unisvq_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, const uint16_t* B,
+                    int64_t affine_groups, uint8_t* codes, void* stream) {
+    if (!W || !A || !B || !codes) return UNISVQ_EINVAL;
+    if (!shape_ok(N, K)) return UNISVQ_ESHAPE;
+    if (affine_groups != 0 && !affine_groups_ok(K, affine_groups)) return UNISVQ_EINVAL;
+    if (!aligned(W, 16) || !aligned(A, 2) || !aligned(B, 2) || !aligned(codes, 4)) return UNISVQ_EALIGN;
+    const hipError_t e = unisvq::launch_quantize(N, K, W, A, B, affine_groups, codes,
+                                                 static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+}
+
 }  // extern "C"

@@ -97,6 +97,10 @@ hipError_t launch_unpack_shared(int64_t N, int64_t K, int64_t affine_groups, con
                                 const uint8_t* packed_affine, uint8_t* codes, uint16_t* A, uint16_t* B,
                                 hipStream_t s);
 
+// Nearest-codeword quantisation (codes uint8 [N][K], 4-byte aligned).
+hipError_t launch_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, const uint16_t* B,
+                           int64_t affine_groups, uint8_t* codes, hipStream_t s);
+
 // One problem of a (possibly batched) matrix-vector launch.
 struct GemvProblem {
     const uint8_t* packed;   // full format, or codes only when `affine` is set

@@ -23,7 +23,8 @@ STATUS = {0: "UNISVQ_OK", -1: "UNISVQ_EINVAL", -2: "UNISVQ_ESHAPE", -3: "UNISVQ_
 EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "unisvq_pack",
            "unisvq_unpack", "unisvq_gemv", "unisvq_gemv_batched", "unisvq_gemm_workspace_bytes",
            "unisvq_gemm", "unisvq_codes_bytes", "unisvq_shared_affine_bytes", "unisvq_pack_shared",
-           "unisvq_unpack_shared", "unisvq_gemv_shared", "unisvq_gemv_shared_batched", "unisvq_gemm_shared")
+           "unisvq_unpack_shared", "unisvq_gemv_shared", "unisvq_gemv_shared_batched", "unisvq_gemm_shared",
+           "unisvq_quantize")
 MAX_BATCH = 8
 
 
@@ -95,6 +96,8 @@ def load():
     lib.unisvq_gemv_shared_batched.restype = i32
     lib.unisvq_gemm_shared.argtypes = [i64, i64, i64, p, p, i64, p, i32, p, i32, p, sz, p]
     lib.unisvq_gemm_shared.restype = i32
+    lib.unisvq_quantize.argtypes = [i64, i64, p, p, p, i64, p, p]
+    lib.unisvq_quantize.restype = i32
     _lib = lib
     return lib
 
@@ -345,3 +348,19 @@ def gemm_shared(packed_codes, packed_affine, N: int, K: int, affine_groups: int,
         ws_bytes = need
     return _shared_product("unisvq_gemm_shared", N, K, affine_groups, packed_codes, packed_affine, x, out,
                            out_dtype, stream, extra=(_ptr(workspace), ws_bytes))
+
+
+# ------------------------------------------------ nearest-codeword quantiser
+
+def quantize(W, A, B, affine_groups: int = 0, out=None, stream=None):
+    """Codes uint8 [N][K] of the nearest codeword per vector of W (fp32 [N][K]).
+    affine_groups 0: A/B per (row, group); 1 or K/128: row-shared pairs."""
+    torch = _torch()
+    _need_cuda(W, A, B, out)
+    N, K = W.shape
+    if out is None:
+        out = torch.empty((N, K), dtype=torch.uint8, device=W.device)
+    _check("unisvq_quantize", load().unisvq_quantize(N, K, _ptr(W.contiguous()), _ptr(A.contiguous()),
+                                                     _ptr(B.contiguous()), affine_groups, _ptr(out),
+                                                     _stream(stream)))
+    return out

@@ -220,3 +220,15 @@ def test_shared_batched_validation():
     assert lib.unisvq_gemv_shared_batched(arr, 0, 1, u.F16, u.F16, None) == EINVAL
     assert lib.unisvq_gemv_shared_batched(None, 1, 1, u.F16, u.F16, None) == EINVAL
     assert lib.unisvq_gemv_shared_batched(arr, 9, 1, u.F16, u.F16, None) == EUNSUP
+
+
+def test_quantize_validation():
+    lib = u.load()
+    assert lib.unisvq_quantize(16, 128, None, GOOD, GOOD, 0, GOOD, None) == EINVAL
+    assert lib.unisvq_quantize(16, 128, GOOD, GOOD, GOOD, 0, None, None) == EINVAL
+    assert lib.unisvq_quantize(16, 256, GOOD, GOOD, GOOD, 3, GOOD, None) == EINVAL
+    assert lib.unisvq_quantize(15, 128, GOOD, GOOD, GOOD, 0, GOOD, None) == ESHAPE
+    assert lib.unisvq_quantize(16, 120, GOOD, GOOD, GOOD, 1, GOOD, None) == ESHAPE
+    assert lib.unisvq_quantize(16, 128, GOOD + 4, GOOD, GOOD, 0, GOOD, None) == EALIGN
+    assert lib.unisvq_quantize(16, 128, GOOD, GOOD + 1, GOOD, 0, GOOD, None) == EALIGN
+    assert lib.unisvq_quantize(16, 128, GOOD, GOOD, GOOD, 0, GOOD + 2, None) == EALIGN

@@ -540,3 +540,45 @@ def test_gemm_shared_prefill_m2048_sampled_rows():
     rows[:2] = [0, layer.N - 1]
     ref = oracle.matmul_shared(oracle.pack_codes(Q)[0], layer.N, layer.K, A, B, x_as_f64(xb, "bf16"), rows=rows)
     assert rel_err(y.cpu().numpy()[:, rows], ref) <= 5e-4
+
+
+# ------------------------------------------- nearest-codeword quantiser
+
+def dev_f32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV)
+
+
+@pytest.mark.parametrize("N,K", [(16, 128), (48, 384), (256, 4096)])
+@pytest.mark.parametrize("mode", ["row_group", "matrix", "group"])
+def test_quantize_bit_exact(N, K, mode):
+    """Codes are integers decided by fp64 distances: bit-exact against the oracle."""
+    rng = np.random.default_rng(N + K + len(mode))
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    if mode == "row_group":
+        A = (rng.standard_normal((N, K // 128, 4, 4)) * 0.45).astype(np.float16)
+        B = (rng.standard_normal((N, K // 128, 4)) * 0.3).astype(np.float16)
+        ga = 0
+    else:
+        ga = 1 if mode == "matrix" else K // 128
+        A = (rng.standard_normal((ga, 4, 4)) * 0.45).astype(np.float16)
+        B = (rng.standard_normal((ga, 4)) * 0.3).astype(np.float16)
+    q = u.quantize(dev_f32(W), dev_u16_as_half(A), dev_u16_as_half(B), ga)
+    torch.cuda.synchronize()
+    assert np.array_equal(q.cpu().numpy(), oracle.quantize(W, A, B, shared=ga != 0))
+
+
+def test_quantize_ties_and_grid_points_on_gpu():
+    N, K = 16, 128
+    A = np.zeros((N, 1, 4, 4), np.float16)
+    A[..., np.arange(4), np.arange(4)] = 1.0
+    B = np.zeros((N, 1, 4), np.float16)
+    rng = np.random.default_rng(3)
+    # half-integer and integer coordinates in [-1, 4]: every vector has ties or exact hits
+    W = (rng.integers(-2, 9, size=(N, K)) / 2).astype(np.float32)
+    q = u.quantize(dev_f32(W), dev_u16_as_half(A), dev_u16_as_half(B), 0)
+    torch.cuda.synchronize()
+    ref = oracle.quantize(W, A, B)
+    assert np.array_equal(q.cpu().numpy(), ref)
+    # ties go down: 0.5 -> 0, 1.5 -> 1, 2.5 -> 2, 3.5 -> 3; clamp outside [0, 3]
+    expect = np.clip(np.floor(W.astype(np.float64) - 1e-9 * (W % 1 == 0.5) + 0.5 * (W % 1 != 0.5)), 0, 3)
+    assert np.array_equal(ref, expect.astype(np.uint8))
