@@ -69,6 +69,12 @@ def _load():
     lib.oracle_matmul_shared_rows.restype = ctypes.c_int
     lib.oracle_quantize.argtypes = [i64, i64, p, p, p, i64, p]
     lib.oracle_quantize.restype = ctypes.c_int
+    lib.oracle_hadamard_factor.argtypes = [i64, p]
+    lib.oracle_hadamard_factor.restype = ctypes.c_int
+    lib.oracle_hadamard.argtypes = [i64, p]
+    lib.oracle_hadamard.restype = ctypes.c_int
+    lib.oracle_rht.argtypes = [i64, i64, p, p, ctypes.c_int, p]
+    lib.oracle_rht.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -267,3 +273,33 @@ def quantize(W: np.ndarray, A: np.ndarray, B: np.ndarray, shared: bool = False) 
     Q = np.empty((N, K), dtype=np.uint8)
     _check(lib.oracle_quantize(N, K, _ptr(W), _ptr(Ab), _ptr(Bb), Ga, _ptr(Q)), "quantize")
     return Q
+
+
+# ------------------------------------------------ randomized Hadamard transform
+
+def hadamard_factor(n: int) -> dict:
+    """The construction used for order n: n = 2^k * m (m = 1, or m = q + 1 with
+    q = p^e a prime power = 3 mod 4)."""
+    out = np.zeros(5, dtype=np.int64)
+    _check(_load().oracle_hadamard_factor(n, _ptr(out)), "hadamard_factor")
+    return dict(zip(("k", "m", "q", "p", "e"), (int(v) for v in out)))
+
+
+def hadamard(n: int) -> np.ndarray:
+    """The +-1 Hadamard matrix of order n (int8)."""
+    H = np.empty((n, n), dtype=np.int8)
+    _check(_load().oracle_hadamard(n, _ptr(H)), "hadamard")
+    return H
+
+
+def rht(X: np.ndarray, signs: np.ndarray, mode: str) -> np.ndarray:
+    """mode 'in': (X diag(s)) H / sqrt(n)  (x S_V V);  mode 'out': (X H / sqrt(n)) diag(s)  (y U S_U)."""
+    X = np.ascontiguousarray(X, dtype=np.float64)
+    if X.ndim == 1:
+        X = X[None, :]
+    M, n = X.shape
+    s = np.ascontiguousarray(signs, dtype=np.int8)
+    assert s.shape == (n,)
+    Y = np.empty_like(X)
+    _check(_load().oracle_rht(n, M, _ptr(X), _ptr(s), 0 if mode == "in" else 1, _ptr(Y)), "rht")
+    return Y

@@ -336,6 +336,184 @@ int oracle_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, con
     return OR_OK;
 }
 
+/* ---- randomized Hadamard transform (Sec. 3.2.1, Eq. 5) ----
+ *
+ * The paper rotates W into U S_U W S_V V with random sign diagonals S_U, S_V
+ * and Hadamard matrices U, V; inference undoes it around the product:
+ *     y = x W^T = ((x S_V V) W_rot^T) U S_U     (U, V normalised: H / sqrt(n)).
+ * Hadamard matrix of order n (the paper names no construction; this is the
+ * reading used throughout): n = 2^k * m with the largest k such that m = 1 or
+ * m = q + 1 for a prime power q = p^e, e <= 3, q = 3 (mod 4); then
+ * H_n = H_m (x) H_{2^k} (Kronecker product, index i = i_m * 2^k + i_2) with
+ *   H_{2^k}[i][j] = (-1)^popcount(i & j)          (Sylvester)
+ *   H_m = I + [[0, 1^T], [-1, Qj]]                  (Paley's first construction)
+ * where Qj[a][b] = chi(a - b) over GF(q): elements are the base-p digit
+ * vectors of 0..q-1 read as polynomials over GF(p) modulo the first monic
+ * irreducible polynomial of degree e (coefficient vectors in lexicographic
+ * order, constant term fastest), and chi is the quadratic character. */
+
+typedef struct {
+    int64_t k, m, q, p, e;
+    int64_t f[4];        /* monic irreducible f(x) = x^e + f[e-1] x^(e-1) + ... + f[0] */
+    signed char* chi;    /* chi of every element index, length q (NULL when m == 1) */
+} had_spec;
+
+static int is_prime(int64_t v) {
+    if (v < 2) return 0;
+    for (int64_t d = 2; d * d <= v; ++d) if (v % d == 0) return 0;
+    return 1;
+}
+
+/* element index -> digits (constant term first) */
+static void gf_digits(int64_t x, int64_t p, int64_t e, int64_t* c) {
+    for (int64_t i = 0; i < e; ++i) { c[i] = x % p; x /= p; }
+}
+
+static int64_t gf_index(const int64_t* c, int64_t p, int64_t e) {
+    int64_t x = 0;
+    for (int64_t i = e - 1; i >= 0; --i) x = x * p + c[i];
+    return x;
+}
+
+/* product of two field elements (digit vectors) modulo f */
+static void gf_mul(const int64_t* a, const int64_t* b, const int64_t* f, int64_t p, int64_t e, int64_t* out) {
+    int64_t t[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int64_t i = 0; i < e; ++i)
+        for (int64_t j = 0; j < e; ++j) t[i + j] = (t[i + j] + a[i] * b[j]) % p;
+    /* reduce degrees 2e-2 .. e using x^e = -(f[e-1] x^(e-1) + ... + f[0]) */
+    for (int64_t d = 2 * e - 2; d >= e; --d) {
+        int64_t c = t[d];
+        if (!c) continue;
+        t[d] = 0;
+        for (int64_t i = 0; i < e; ++i) t[d - e + i] = ((t[d - e + i] - c * f[i]) % p + p) % p;
+    }
+    for (int64_t i = 0; i < e; ++i) out[i] = t[i];
+}
+
+/* A monic polynomial of degree 2 or 3 is irreducible iff it has no root. */
+static int poly_has_root(const int64_t* f, int64_t p, int64_t e) {
+    for (int64_t x = 0; x < p; ++x) {
+        int64_t v = 1;  /* leading coefficient */
+        for (int64_t i = e - 1; i >= 0; --i) v = (v * x + f[i]) % p;
+        if (v == 0) return 1;
+    }
+    return 0;
+}
+
+/* Fill spec for order n; returns 0 or OR_ESHAPE when n has no such form. */
+static int had_factor(int64_t n, had_spec* hs) {
+    memset(hs, 0, sizeof(*hs));
+    if (n < 1) return OR_ESHAPE;
+    int64_t k = 0;
+    while ((n >> (k + 1)) << (k + 1) == n) ++k;  /* largest power of two dividing n */
+    for (; k >= 0; --k) {
+        int64_t m = n >> k;
+        if (m == 1) { hs->k = k; hs->m = 1; return OR_OK; }
+        int64_t q = m - 1;
+        if (q % 4 != 3) continue;
+        for (int64_t p = 2; p <= q; ++p) {
+            if (!is_prime(p)) continue;
+            int64_t pe = p, e = 1;
+            while (pe < q && e < 3) { pe *= p; ++e; }
+            if (pe != q) continue;
+            hs->k = k; hs->m = m; hs->q = q; hs->p = p; hs->e = e;
+            if (e > 1) {  /* first monic irreducible polynomial of degree e */
+                int64_t found = 0;
+                for (int64_t idx = 0; idx < q && !found; ++idx) {
+                    gf_digits(idx, p, e, hs->f);
+                    if (!poly_has_root(hs->f, p, e)) found = 1;
+                }
+                if (!found) return OR_ESHAPE;
+            }
+            return OR_OK;
+        }
+    }
+    return OR_ESHAPE;
+}
+
+static int had_build_chi(had_spec* hs) {
+    if (hs->m == 1) return OR_OK;
+    int64_t q = hs->q, p = hs->p, e = hs->e;
+    hs->chi = calloc((size_t)q, 1);
+    if (!hs->chi) return OR_EINVAL;
+    for (int64_t x = 1; x < q; ++x) hs->chi[x] = -1;
+    for (int64_t y = 1; y < q; ++y) {
+        int64_t a[4], sq[4];
+        gf_digits(y, p, e, a);
+        if (e == 1) sq[0] = (a[0] * a[0]) % p;
+        else gf_mul(a, a, hs->f, p, e, sq);
+        hs->chi[gf_index(sq, p, e)] = 1;
+    }
+    return OR_OK;
+}
+
+/* Entry (i, j) of the Paley matrix of order q + 1. */
+static int paley_entry(const had_spec* hs, int64_t i, int64_t j) {
+    if (i == 0) return 1;
+    if (j == 0) return -1;
+    if (i == j) return 1;
+    int64_t a[4], b[4], d[4];
+    gf_digits(i - 1, hs->p, hs->e, a);
+    gf_digits(j - 1, hs->p, hs->e, b);
+    for (int64_t t = 0; t < hs->e; ++t) d[t] = ((a[t] - b[t]) % hs->p + hs->p) % hs->p;
+    return hs->chi[gf_index(d, hs->p, hs->e)];
+}
+
+static int had_entry(const had_spec* hs, int64_t i, int64_t j) {
+    int64_t i2 = i & ((INT64_C(1) << hs->k) - 1), j2 = j & ((INT64_C(1) << hs->k) - 1);
+    int sign = (__builtin_popcountll((unsigned long long)(i2 & j2)) & 1) ? -1 : 1;
+    if (hs->m == 1) return sign;
+    return sign * paley_entry(hs, i >> hs->k, j >> hs->k);
+}
+
+/* Order-n factor description: out[0..4] = k, m, q, p, e (m == 1: pure Sylvester). */
+int oracle_hadamard_factor(int64_t n, int64_t* out) {
+    had_spec hs;
+    int st = had_factor(n, &hs);
+    if (st != OR_OK) return st;
+    out[0] = hs.k; out[1] = hs.m; out[2] = hs.q; out[3] = hs.p; out[4] = hs.e;
+    return OR_OK;
+}
+
+/* The full +-1 matrix (row-major n x n). */
+int oracle_hadamard(int64_t n, signed char* H) {
+    if (!H) return OR_EINVAL;
+    had_spec hs;
+    int st = had_factor(n, &hs);
+    if (st != OR_OK) return st;
+    if ((st = had_build_chi(&hs)) != OR_OK) return st;
+    for (int64_t i = 0; i < n; ++i)
+        for (int64_t j = 0; j < n; ++j) H[i * n + j] = (signed char)had_entry(&hs, i, j);
+    free(hs.chi);
+    return OR_OK;
+}
+
+/* Rows of X [M][n] times the normalised Hadamard matrix, with the sign
+ * vector s (+-1) applied before (mode 0: Y = (X diag(s)) H / sqrt(n), the
+ * input side x S_V V) or after (mode 1: Y = (X H / sqrt(n)) diag(s), the output
+ * side y U S_U).  Plain O(n^2) products, one sequential sum per element. */
+int oracle_rht(int64_t n, int64_t M, const double* X, const signed char* s, int mode, double* Y) {
+    if (!X || !s || !Y) return OR_EINVAL;
+    if (M < 0 || (mode != 0 && mode != 1)) return OR_EINVAL;
+    had_spec hs;
+    int st = had_factor(n, &hs);
+    if (st != OR_OK) return st;
+    if ((st = had_build_chi(&hs)) != OR_OK) return st;
+    double norm = 1.0 / sqrt((double)n);
+    for (int64_t t = 0; t < M; ++t) {
+        for (int64_t j = 0; j < n; ++j) {
+            double acc = 0.0;
+            for (int64_t i = 0; i < n; ++i) {
+                double xv = X[t * n + i] * (mode == 0 ? (double)s[i] : 1.0);
+                acc += xv * (double)had_entry(&hs, i, j);
+            }
+            Y[t * n + j] = acc * norm * (mode == 1 ? (double)s[j] : 1.0);
+        }
+    }
+    free(hs.chi);
+    return OR_OK;
+}
+
 /* ---- decode (Eq. 4 applied along the input dimension as in Eq. 8) ---- */
 
 /* One row: w[k] for k = 4v + a is sum_b A[g][a][b] * q[4v + b] + B[g][a],

@@ -495,3 +495,80 @@ def test_quantize_shared_pairs_equal_copied_pairs(per_group):
     B = np.broadcast_to(Bs[src], (N, K // 128, 4)).copy()
     W = rng.standard_normal((N, K)).astype(np.float32)
     assert np.array_equal(oracle.quantize(W, As, Bs, shared=True), oracle.quantize(W, A, B))
+
+
+# ------------------------------------------- randomized Hadamard transform (Sec. 3.2.1, Eq. 5)
+
+@pytest.mark.parametrize("n", [1, 2, 4, 12, 20, 28, 44, 112, 344, 688])
+def test_hadamard_is_orthogonal(n):
+    H = oracle.hadamard(n).astype(np.int64)
+    assert set(np.unique(H)) <= {-1, 1}
+    assert np.array_equal(H @ H.T, n * np.eye(n, dtype=np.int64))
+
+
+@pytest.mark.parametrize("n", [12, 28, 44, 344])
+def test_paley_part_is_identity_plus_skew(n):
+    H = oracle.hadamard(n).astype(np.int64)
+    assert oracle.hadamard_factor(n)["m"] == n
+    assert np.array_equal(H + H.T, 2 * np.eye(n, dtype=np.int64))
+
+
+def test_paley_order_12_worked_by_hand():
+    g = json.load(open(os.path.join(GOLD, "paley12.json")))
+    H = oracle.hadamard(12)
+    assert H[0].tolist() == g["row0"]
+    assert H[:, 0].tolist() == g["col0"]
+    assert H[1].tolist() == g["row1"]
+
+
+@pytest.mark.parametrize("n", [2, 8, 64, 256])
+def test_power_of_two_is_sylvester(n):
+    linalg = pytest.importorskip("scipy.linalg")
+    assert np.array_equal(oracle.hadamard(n), linalg.hadamard(n).astype(np.int8))
+
+
+def test_kronecker_layout_of_mixed_orders():
+    """n = m * 2^k: H_n = H_m (x) H_{2^k}."""
+    linalg = pytest.importorskip("scipy.linalg")
+    for n, m, k in [(24, 12, 1), (112, 28, 2), (688, 344, 1)]:
+        f = oracle.hadamard_factor(n)
+        assert (f["m"], f["k"]) == (m, k)
+        assert np.array_equal(oracle.hadamard(n), np.kron(oracle.hadamard(m), linalg.hadamard(2 ** k)).astype(np.int8))
+
+
+def test_factor_rule_for_the_layer_sizes():
+    assert oracle.hadamard_factor(4096) == {"k": 12, "m": 1, "q": 0, "p": 0, "e": 0}
+    assert oracle.hadamard_factor(11008) == {"k": 5, "m": 344, "q": 343, "p": 7, "e": 3}
+    assert oracle.hadamard_factor(28672) == {"k": 10, "m": 28, "q": 27, "p": 3, "e": 3}
+    for n in (100, 86, 43):
+        with pytest.raises(oracle.OracleError):
+            oracle.hadamard_factor(n)
+
+
+def test_rht_round_trip_recovers_the_original_product():
+    """Eq. 5: W_rot = U S_U W S_V V; at inference y = ((x S_V V) W_rot^T) U S_U
+    must equal x W^T.  Built with dense numpy products of the oracle's matrices."""
+    rng = np.random.default_rng(55)
+    N, K, M = 24, 28, 3
+    W = rng.standard_normal((N, K))
+    x = rng.standard_normal((M, K))
+    sU = rng.choice(np.array([-1, 1], np.int8), N)
+    sV = rng.choice(np.array([-1, 1], np.int8), K)
+    U = oracle.hadamard(N) / np.sqrt(N)
+    V = oracle.hadamard(K) / np.sqrt(K)
+    W_rot = U @ np.diag(sU) @ W @ np.diag(sV) @ V
+    y_path = oracle.rht(oracle.rht(x, sV, "in") @ W_rot.T, sU, "out")
+    np.testing.assert_allclose(y_path, x @ W.T, rtol=1e-12, atol=1e-12)
+
+
+def test_rht_preserves_norms_and_matches_dense_sylvester():
+    linalg = pytest.importorskip("scipy.linalg")
+    rng = np.random.default_rng(6)
+    n = 256
+    x = rng.standard_normal((2, n))
+    s = rng.choice(np.array([-1, 1], np.int8), n)
+    y = oracle.rht(x, s, "in")
+    np.testing.assert_allclose(np.linalg.norm(y, axis=1), np.linalg.norm(x, axis=1), rtol=1e-13)
+    np.testing.assert_allclose(y, (x * s) @ linalg.hadamard(n) / np.sqrt(n), rtol=1e-12, atol=1e-12)
+    z = oracle.rht(x, s, "out")
+    np.testing.assert_allclose(z, (x @ linalg.hadamard(n) / np.sqrt(n)) * s, rtol=1e-12, atol=1e-12)
