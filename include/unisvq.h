@@ -272,6 +272,30 @@ int unisvq_gemm_shared(int64_t N, int64_t K, int64_t affine_groups, const void* 
 int unisvq_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, const uint16_t* B,
                     int64_t affine_groups, uint8_t* codes, void* stream);
 
+/* ---- Randomized Hadamard transform around the product (Sec. 3.2.1, Eq. 5) ----
+ * The weights are quantised in the rotated basis W_rot = U S_U W S_V V (S_U,
+ * S_V random sign diagonals, U, V Hadamard matrices normalised to be
+ * orthogonal), so a layer computes y = ((x S_V V) W_rot^T) U S_U:
+ *   mode 0 (input side):   y = (x diag(signs)) H_n / sqrt(n)    -> feeds the product
+ *   mode 1 (output side):  y = (x H_n / sqrt(n)) diag(signs)    -> after the product
+ * for M rows of length n.  Hadamard matrix of order n: n = 2^k * m with the
+ * largest k such that m = 1 or m = q + 1 for a prime power q = p^e = 3 (mod 4),
+ * e <= 3; H_n = P_m (x) S_{2^k} (Kronecker; index i = i_m * 2^k + i_2), S the
+ * Sylvester matrix (entry (-1)^popcount(i & j)) and P Paley's first
+ * construction I + [[0, 1^T], [-1, Q]] with Q[a][b] = chi(a - b) over GF(q),
+ * field elements being the base-p digit vectors of their indices taken as
+ * polynomials modulo the first monic irreducible polynomial of degree e
+ * (coefficient vectors counted with the constant term fastest), chi the
+ * quadratic character.  Examples: 4096 = 2^12; 11008 = 2^5 * 344 (q = 7^3);
+ * 28672 = 2^10 * 28 (q = 3^3).  Computed in fp32, rounded once to y_dtype.
+ *   n        1..32768 with such a factorisation (UNISVQ_EUNSUP otherwise)
+ *   M        1..65535 rows
+ *   x        device [M][n], x_dtype F16, BF16 or F32 (aligned to its element)
+ *   signs    device int8 [n], each +1 or -1
+ *   y        device [M][n], y_dtype F16, BF16 or F32; must not overlap x */
+int unisvq_rht(int64_t n, int64_t M, const void* x, int x_dtype, const int8_t* signs, int mode, void* y,
+               int y_dtype, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -499,17 +499,29 @@ int oracle_rht(int64_t n, int64_t M, const double* X, const signed char* s, int 
     int st = had_factor(n, &hs);
     if (st != OR_OK) return st;
     if ((st = had_build_chi(&hs)) != OR_OK) return st;
+    /* the Paley factor as a table (its entries are needed n^2 / m^2 times each) */
+    signed char* P = NULL;
+    if (hs.m > 1) {
+        P = malloc((size_t)(hs.m * hs.m));
+        if (!P) { free(hs.chi); return OR_EINVAL; }
+        for (int64_t a = 0; a < hs.m; ++a)
+            for (int64_t b = 0; b < hs.m; ++b) P[a * hs.m + b] = (signed char)paley_entry(&hs, a, b);
+    }
     double norm = 1.0 / sqrt((double)n);
+    int64_t mask = (INT64_C(1) << hs.k) - 1;
     for (int64_t t = 0; t < M; ++t) {
         for (int64_t j = 0; j < n; ++j) {
             double acc = 0.0;
             for (int64_t i = 0; i < n; ++i) {
                 double xv = X[t * n + i] * (mode == 0 ? (double)s[i] : 1.0);
-                acc += xv * (double)had_entry(&hs, i, j);
+                int h = (__builtin_popcountll((unsigned long long)(i & j & mask)) & 1) ? -1 : 1;
+                if (P) h *= P[(i >> hs.k) * hs.m + (j >> hs.k)];
+                acc += xv * (double)h;
             }
             Y[t * n + j] = acc * norm * (mode == 1 ? (double)s[j] : 1.0);
         }
     }
+    free(P);
     free(hs.chi);
     return OR_OK;
 }

@@ -234,4 +234,21 @@ int unisvq_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, con
     return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
 }
 
+/* ---- randomized Hadamard transform ---- */
+
+int unisvq_rht(int64_t n, int64_t M, const void* x, int x_dtype, const int8_t* signs, int mode, void* y, int y_dtype,
+               void* stream) {
+    if (!x || !signs || !y) return UNISVQ_EINVAL;
+    if (n < 1 || M < 1 || M > 65535 || (mode != 0 && mode != 1)) return UNISVQ_EINVAL;
+    if (!y_dtype_ok(x_dtype) || !y_dtype_ok(y_dtype)) return UNISVQ_EINVAL;  // F16, BF16 or F32 on both sides
+    const size_t xb = x_dtype == UNISVQ_F32 ? 4 : 2, yb = y_dtype == UNISVQ_F32 ? 4 : 2;
+    if (!aligned(x, xb) || !aligned(y, yb)) return UNISVQ_EALIGN;
+    // x and y may not overlap: several workgroups read a row while others write it
+    const uintptr_t x0 = reinterpret_cast<uintptr_t>(x), y0 = reinterpret_cast<uintptr_t>(y);
+    const uintptr_t x1 = x0 + static_cast<uintptr_t>(n * M) * xb, y1 = y0 + static_cast<uintptr_t>(n * M) * yb;
+    if (x0 < y1 && y0 < x1) return UNISVQ_EINVAL;
+    return unisvq::launch_rht(n, M, x, x_dtype, reinterpret_cast<const signed char*>(signs), mode, y, y_dtype,
+                              static_cast<hipStream_t>(stream));
+}
+
 }  // extern "C"

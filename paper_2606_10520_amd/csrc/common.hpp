@@ -101,6 +101,12 @@ hipError_t launch_unpack_shared(int64_t N, int64_t K, int64_t affine_groups, con
 hipError_t launch_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, const uint16_t* B,
                            int64_t affine_groups, uint8_t* codes, hipStream_t s);
 
+// Randomized Hadamard transform of M rows of length n (mode 0: input side,
+// signs first; mode 1: output side, signs last); UNISVQ_EUNSUP when n has no
+// supported Hadamard construction or exceeds the LDS row.
+int launch_rht(int64_t n, int64_t M, const void* x, int x_dtype, const signed char* signs, int mode, void* y,
+               int y_dtype, hipStream_t s);
+
 // One problem of a (possibly batched) matrix-vector launch.
 struct GemvProblem {
     const uint8_t* packed;   // full format, or codes only when `affine` is set

@@ -24,7 +24,7 @@ EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "uni
            "unisvq_unpack", "unisvq_gemv", "unisvq_gemv_batched", "unisvq_gemm_workspace_bytes",
            "unisvq_gemm", "unisvq_codes_bytes", "unisvq_shared_affine_bytes", "unisvq_pack_shared",
            "unisvq_unpack_shared", "unisvq_gemv_shared", "unisvq_gemv_shared_batched", "unisvq_gemm_shared",
-           "unisvq_quantize")
+           "unisvq_quantize", "unisvq_rht")
 MAX_BATCH = 8
 
 
@@ -98,6 +98,8 @@ def load():
     lib.unisvq_gemm_shared.restype = i32
     lib.unisvq_quantize.argtypes = [i64, i64, p, p, p, i64, p, p]
     lib.unisvq_quantize.restype = i32
+    lib.unisvq_rht.argtypes = [i64, i64, p, i32, p, i32, p, i32, p]
+    lib.unisvq_rht.restype = i32
     _lib = lib
     return lib
 
@@ -363,4 +365,23 @@ def quantize(W, A, B, affine_groups: int = 0, out=None, stream=None):
     _check("unisvq_quantize", load().unisvq_quantize(N, K, _ptr(W.contiguous()), _ptr(A.contiguous()),
                                                      _ptr(B.contiguous()), affine_groups, _ptr(out),
                                                      _stream(stream)))
+    return out
+
+
+# ------------------------------------------------ randomized Hadamard transform
+
+def rht(x, signs, mode: str, out=None, out_dtype=None, stream=None):
+    """mode 'in': (x diag(signs)) H / sqrt(n); mode 'out': (x H / sqrt(n)) diag(signs).
+    x [M][n] (fp16, bf16 or fp32), signs int8 [n] (+-1)."""
+    torch = _torch()
+    _need_cuda(x, signs, out)
+    x2 = x if x.dim() == 2 else x.reshape(1, -1)
+    if not x2.is_contiguous():
+        raise ValueError("x must be contiguous")
+    M, n = x2.shape
+    if out is None:
+        out = torch.empty((M, n), dtype=out_dtype or x.dtype, device=x.device)
+    _check("unisvq_rht", load().unisvq_rht(n, M, _ptr(x2), _dtype_code(x2.dtype), _ptr(signs.contiguous()),
+                                           0 if mode == "in" else 1, _ptr(out), _dtype_code(out.dtype),
+                                           _stream(stream)))
     return out

@@ -232,3 +232,18 @@ def test_quantize_validation():
     assert lib.unisvq_quantize(16, 128, GOOD + 4, GOOD, GOOD, 0, GOOD, None) == EALIGN
     assert lib.unisvq_quantize(16, 128, GOOD, GOOD + 1, GOOD, 0, GOOD, None) == EALIGN
     assert lib.unisvq_quantize(16, 128, GOOD, GOOD, GOOD, 0, GOOD + 2, None) == EALIGN
+
+
+def test_rht_validation():
+    lib = u.load()
+    assert lib.unisvq_rht(4096, 1, None, u.F16, GOOD, 0, GOOD + 0x100000, u.F16, None) == EINVAL
+    assert lib.unisvq_rht(4096, 1, GOOD, u.F16, None, 0, GOOD + 0x100000, u.F16, None) == EINVAL
+    assert lib.unisvq_rht(4096, 0, GOOD, u.F16, GOOD, 0, GOOD + 0x100000, u.F16, None) == EINVAL
+    assert lib.unisvq_rht(4096, 1, GOOD, u.F16, GOOD, 2, GOOD + 0x100000, u.F16, None) == EINVAL
+    assert lib.unisvq_rht(4096, 1, GOOD, 7, GOOD, 0, GOOD + 0x100000, u.F16, None) == EINVAL
+    assert lib.unisvq_rht(4096, 1, GOOD, u.F16, GOOD, 0, GOOD + 1000, u.F16, None) == EINVAL  # overlap
+    assert lib.unisvq_rht(4096, 1, GOOD + 1, u.F16, GOOD, 0, GOOD + 0x100000, u.F16, None) == EALIGN
+    assert lib.unisvq_rht(4096, 1, GOOD, u.F16, GOOD, 0, GOOD + 0x100002, u.F32, None) == EALIGN
+    # orders without a supported construction, or beyond the LDS row
+    assert lib.unisvq_rht(100, 1, GOOD, u.F16, GOOD, 0, GOOD + 0x100000, u.F16, None) == EUNSUP
+    assert lib.unisvq_rht(65536, 1, GOOD, u.F16, GOOD, 0, GOOD + 0x100000, u.F16, None) == EUNSUP

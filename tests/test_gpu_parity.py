@@ -582,3 +582,52 @@ def test_quantize_ties_and_grid_points_on_gpu():
     # ties go down: 0.5 -> 0, 1.5 -> 1, 2.5 -> 2, 3.5 -> 3; clamp outside [0, 3]
     expect = np.clip(np.floor(W.astype(np.float64) - 1e-9 * (W % 1 == 0.5) + 0.5 * (W % 1 != 0.5)), 0, 3)
     assert np.array_equal(ref, expect.astype(np.uint8))
+
+
+# ------------------------------------------- randomized Hadamard transform
+
+@pytest.mark.parametrize("n", [256, 4096, 8192, 344, 688, 11008, 28672])
+@pytest.mark.parametrize("mode", ["in", "out"])
+def test_rht_matches_dense_oracle(n, mode):
+    rng = np.random.default_rng(n + len(mode))
+    M = 2
+    x = rng.standard_normal((M, n)).astype(np.float32)
+    s = rng.choice(np.array([-1, 1], np.int8), n)
+    y = u.rht(dev_f32(x), torch.from_numpy(s).to(DEV), mode, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = oracle.rht(x.astype(np.float64), s, mode)
+    # fp32 sums of n terms of unit size: error ~ 2^-24 * log2(n) relative to the entries
+    assert rel_err(y.cpu().numpy(), ref) <= 2e-6
+
+
+@pytest.mark.parametrize("xdt,ydt", [("f16", torch.float16), ("bf16", torch.bfloat16), ("f16", torch.float32)])
+def test_rht_dtypes(xdt, ydt):
+    n, M = 11008, 3
+    xb = wl.gen_activations(M, n, seed=4, dtype=xdt)
+    s = np.random.default_rng(9).choice(np.array([-1, 1], np.int8), n)
+    y = u.rht(dev_x(xb, xdt), torch.from_numpy(s).to(DEV), "in", out_dtype=ydt)
+    torch.cuda.synchronize()
+    ref = oracle.rht(x_as_f64(xb, xdt), s, "in")
+    tol = {torch.float16: 2e-3, torch.bfloat16: 8e-3, torch.float32: 2e-6}[ydt]
+    assert rel_err(y.float().cpu().numpy(), ref) <= tol
+
+
+def test_rotated_layer_end_to_end():
+    """A layer quantised in the rotated basis (Eq. 5): x -> input transform ->
+    2-bit product -> output transform, against the same chain in fp64.  The
+    rotated activations are rounded once to fp16 before the product."""
+    N, K, M = 4096, 11008, 1
+    Q, A, B = wl.gen_weights(N, K, seed=30)
+    pk_ref, _ = oracle.pack(Q, A, B)
+    pk = upload_pack(Q, A, B)
+    rng = np.random.default_rng(31)
+    sU = rng.choice(np.array([-1, 1], np.int8), N)
+    sV = rng.choice(np.array([-1, 1], np.int8), K)
+    xb = wl.gen_activations(M, K, seed=32, dtype="f16")
+    xr = u.rht(dev_x(xb, "f16"), torch.from_numpy(sV).to(DEV), "in", out_dtype=torch.float16)
+    yr = u.gemv(pk, N, K, xr, out_dtype=torch.float32)
+    y = u.rht(yr, torch.from_numpy(sU).to(DEV), "out", out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    x_rot = oracle.rht(x_as_f64(xb, "f16"), sV, "in")
+    ref = oracle.rht(oracle.matmul(pk_ref, N, K, x_rot), sU, "out")
+    assert rel_err(y.cpu().numpy(), ref) <= 2e-3
