@@ -67,6 +67,10 @@ def parse():
                    help="decoder: q/k/v in one batched launch, o, gate/up in one batched launch, down "
                         "(how a decode step runs them); per_layer: one launch per linear; single: all "
                         "linears in one batched launch")
+    p.add_argument("--rht", action="store_true",
+                   help="also time the decoder step of a layer quantised in the rotated basis (Eq. 5): per "
+                        "launch group, one input transform of its activations, the batched product and one "
+                        "output transform of the group's stacked outputs")
     p.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                    help="only run a plain device-to-device copy of BYTES bytes 10 times (counter calibration)")
     p.add_argument("--no-schedules", action="store_true",
@@ -415,6 +419,65 @@ def main():
             schedules[oname] = {"launches_per_step": len(ogroups), "ms_per_step": round(oms, 5),
                                 "GB_per_s": round(set_bytes / (oms * 1e-3) / 1e9, 1)}
 
+    # ---- the rotated layer (Eq. 5): transforms around each launch group
+    rht = None
+    if args.rht and kernel == "gemv" and not shared and full_set:
+        rgroups = [["q", "k", "v"], ["o"], ["gate", "up"], ["down"]]
+        rng = np.random.default_rng(123)
+        rcalls = []
+        for s_ in sets:
+            by = {L.name: (L, pk, x, y) for (L, pk, x, y) in s_}
+            cc = []
+            for grp in rgroups:
+                Ls = [by[n][0] for n in grp]
+                N, K = Ls[0].N, Ls[0].K
+                sV = torch.from_numpy(rng.choice(np.array([-1, 1], np.int8), K)).to(dev)
+                sU = torch.from_numpy(rng.choice(np.array([-1, 1], np.int8), N)).to(dev)
+                xin = by[grp[0]][2]                                   # the group's activations
+                xrot = torch.empty_like(xin)
+                ystk = torch.empty((len(grp) * M, N), dtype=torch.float16, device=dev)
+                yout = torch.empty_like(ystk)
+                arr = (u.GemvProblem * len(grp))()
+                for i, n in enumerate(grp):
+                    L, pk, _, _ = by[n]
+                    arr[i] = u.GemvProblem(L.N, L.K, pk.data_ptr(), xrot.data_ptr(), ystk[i * M:(i + 1) * M].data_ptr())
+                cc.append((K, M, xin, xcode, sV, xrot, arr, len(grp), N, ystk, sU, yout))
+            rcalls.append(cc)
+
+        def rstep(i, sptr):
+            for (K, M_, xin, xc, sV, xrot, arr, cnt, N, ystk, sU, yout) in rcalls[i % copies]:
+                for st in (lib.unisvq_rht(K, M_, xin.data_ptr(), xc, sV.data_ptr(), 0, xrot.data_ptr(), u.F16, sptr),
+                           lib.unisvq_gemv_batched(arr, cnt, M_, u.F16, u.F16, sptr),
+                           lib.unisvq_rht(N, cnt * M_, ystk.data_ptr(), u.F16, sU.data_ptr(), 1, yout.data_ptr(),
+                                          u.F16, sptr)):
+                    if st != 0:
+                        raise RuntimeError(f"rotated step failed with status {st}")
+
+        for i in range(args.warmup):
+            rstep(i, stream.cuda_stream)
+        torch.cuda.synchronize()
+        g_r = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_r):
+            cap = torch.cuda.current_stream().cuda_stream
+            for c in range(copies):
+                rstep(c, cap)
+        g_r.replay()
+        torch.cuda.synchronize()
+        reps = max(1, -(-args.steps // copies))
+        r0 = torch.cuda.Event(enable_timing=True)
+        r1 = torch.cuda.Event(enable_timing=True)
+        r0.record(stream)
+        for _ in range(reps):
+            g_r.replay()
+        r1.record(stream)
+        torch.cuda.synchronize()
+        rms = r0.elapsed_time(r1) / (reps * copies)
+        rht = {"what": "decoder step of a layer quantised in the rotated basis: 4 input transforms, 4 batched "
+                       "products, 4 output transforms (12 launches)",
+               "ms_per_step": round(rms, 5), "over_plain_step": round(rms / ms_per_step, 3),
+               "GB_per_s": round(set_bytes / (rms * 1e-3) / 1e9, 1)}
+        del g_r
+
     # ---- per-launch breakdown: HIP events on the launch stream around each
     # launch.  A spin kernel first lets the host queue a chunk of launches ahead
     # of the GPU, so an interval brackets GPU work rather than host latency;
@@ -537,6 +600,7 @@ def main():
         "dense_matmul": dense,
         "event_us_per_launch": {k: round(v, 3) for k, v in per_layer_us.items()},
         "schedules": schedules,
+        "rotated_layer": rht,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

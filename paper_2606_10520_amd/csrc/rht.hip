@@ -12,10 +12,10 @@
 // first monic irreducible polynomial of degree e, chi the quadratic character).
 //
 // One workgroup per (row, slice of output blocks).  The row goes to LDS in
-// fp32 (signs applied on the input side), the Sylvester factor runs as an
-// in-place fast transform inside each block of 2^k, and the Paley factor, if
-// any, as a dense m x m product for the workgroup's output blocks, with its
-// entries built in LDS from the quadratic character.  fp32 throughout, one
+// fp32 (signs applied on the input side); the Paley factor, if any, runs as a
+// dense product for the workgroup's output blocks with its entries built in
+// LDS from the quadratic character, then the Sylvester factor as an in-place
+// fast transform inside each of those blocks of 2^k.  fp32 throughout, one
 // rounding to the output dtype.
 #include <cmath>
 
@@ -32,17 +32,28 @@ namespace {
 
 constexpr int kRhtThreads = 1024;
 constexpr int kRhtMaxN = 32768;  // fp32 row in LDS
-constexpr int kMaxPaleyBlocks = 8;  // output blocks of the Paley factor per workgroup
 
-template <typename T>
-__device__ inline float to_f32(const void* p, int64_t i) {
-    return static_cast<float>(static_cast<const T*>(p)[i]);
-}
-
-__device__ inline float load_any(const void* p, int64_t i, int dtype) {
-    if (dtype == UNISVQ_F32) return static_cast<const float*>(p)[i];
-    if (dtype == UNISVQ_F16) return to_f32<_Float16>(p, i);
-    return to_f32<__bf16>(p, i);
+// The row into LDS as fp32 (signs applied on the input side): eight
+// independent loads in flight per thread before their LDS writes.
+template <typename XT>
+__device__ inline void load_row(const XT* __restrict__ xr, const signed char* __restrict__ signs, int mode, int n,
+                                float* z, int tid) {
+    constexpr int U = 8;
+    for (int i0 = tid; i0 < n; i0 += kRhtThreads * U) {
+        float v[U];
+        float sg[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * kRhtThreads;
+            v[u] = i < n ? static_cast<float>(xr[i]) : 0.f;
+            sg[u] = (mode == 0 && i < n) ? static_cast<float>(signs[i]) : 1.f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * kRhtThreads;
+            if (i < n) z[i] = v[u] * sg[u];
+        }
+    }
 }
 
 // digits of field element x (constant term first)
@@ -86,42 +97,55 @@ __device__ inline int paley_entry(const signed char* chi, const HadSpec& h, int 
     return chi[gf_index(d, h.p, h.e)];
 }
 
-__global__ __launch_bounds__(kRhtThreads) void rht_kernel(const void* __restrict__ x, int x_dtype,
+// In-place fast Sylvester transform of every block of 2^k consecutive
+// elements of buf[0 .. len): two stages (index bits st, st+1) per pass.
+__device__ inline void sylvester_blocks(float* buf, int len, int k, int tid) {
+    int st = 0;
+    for (; st + 2 <= k; st += 2) {
+        const int l = 1 << st;
+        for (int b = tid; b < len / 4; b += kRhtThreads) {
+            const int base = ((b >> st) << (st + 2)) | (b & (l - 1));  // bits st, st+1 clear
+            const float a0 = buf[base], a1 = buf[base + l], a2 = buf[base + 2 * l], a3 = buf[base + 3 * l];
+            const float b0 = a0 + a1, b1 = a0 - a1, b2 = a2 + a3, b3 = a2 - a3;
+            buf[base] = b0 + b2;
+            buf[base + l] = b1 + b3;
+            buf[base + 2 * l] = b0 - b2;
+            buf[base + 3 * l] = b1 - b3;
+        }
+        __syncthreads();
+    }
+    if (st < k) {  // one stage left
+        const int l = 1 << st;
+        for (int b = tid; b < len / 2; b += kRhtThreads) {
+            const int lo = ((b >> st) << (st + 1)) | (b & (l - 1));  // bit st clear
+            const float u = buf[lo], w = buf[lo + l];
+            buf[lo] = u + w;
+            buf[lo + l] = u - w;
+        }
+        __syncthreads();
+    }
+}
+
+// One workgroup per (row, slice of output blocks [jb0, jb0 + blocks_per_wg)).
+// H = P (x) S factors as (P (x) I)(I (x) S): the Paley factor first, for this
+// workgroup's output blocks only, then the Sylvester transform of just those
+// blocks -- no work is repeated across the workgroups of a row.
+template <typename XT>
+__global__ __launch_bounds__(kRhtThreads) void rht_kernel(const XT* __restrict__ x,
                                                           const signed char* __restrict__ signs, int mode,
                                                           void* __restrict__ y, int y_dtype, int n, HadSpec h,
                                                           int blocks_per_wg, float norm) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-    float* z = reinterpret_cast<float*>(smem);                                // [n]
-    signed char* chi = reinterpret_cast<signed char*>(smem + 4 * n);          // [q]
-    signed char* pcol = chi + (h.q + 15) / 16 * 16;                           // [blocks_per_wg][m]
+    float* z = reinterpret_cast<float*>(smem);  // [n] the row
     const int64_t row = blockIdx.y;
     const int tid = threadIdx.x;
     const int half = 1 << h.k;
 
     // 1. the row, with the signs on the input side
-    for (int i = tid; i < n; i += kRhtThreads) {
-        const float v = load_any(x, row * n + i, x_dtype);
-        z[i] = mode == 0 ? v * static_cast<float>(signs[i]) : v;
-    }
-    // quadratic character: chi[0] = 0, squares +1, the rest -1
-    if (h.m > 1) {
-        for (int i = tid; i < h.q; i += kRhtThreads) chi[i] = i == 0 ? 0 : -1;
-    }
-    __syncthreads();
-    if (h.m > 1) {
-        for (int v = 1 + tid; v < h.q; v += kRhtThreads) chi[gf_square(v, h)] = 1;
-    }
-    // 2. Sylvester factor: in-place fast transform inside every block of 2^k
-    for (int len = 1; len < half; len <<= 1) {
-        for (int b = tid; b < n / 2; b += kRhtThreads) {
-            const int lo = (b / len) * 2 * len + (b % len);  // element with bit `len` clear
-            const float u = z[lo], w = z[lo + len];
-            z[lo] = u + w;
-            z[lo + len] = u - w;
-        }
+    load_row<XT>(x + row * n, signs, mode, n, z, tid);
+    if (h.m == 1) {  // Sylvester only: one workgroup per row
         __syncthreads();
-    }
-    if (h.m == 1) {
+        sylvester_blocks(z, n, h.k, tid);
         for (int j = tid; j < n; j += kRhtThreads) {
             float v = z[j] * norm;
             if (mode == 1) v *= static_cast<float>(signs[j]);
@@ -129,22 +153,42 @@ __global__ __launch_bounds__(kRhtThreads) void rht_kernel(const void* __restrict
         }
         return;
     }
-    // 3. Paley factor for output blocks [jb0, jb1): y[jm][j2] = sum_im P[im][jm] z[im][j2]
     const int jb0 = blockIdx.x * blocks_per_wg;
-    const int jb1 = min(h.m, jb0 + blocks_per_wg);
-    __syncthreads();  // chi complete
-    for (int t = tid; t < (jb1 - jb0) * h.m; t += kRhtThreads) {
-        const int jl = t / h.m, im = t % h.m;
-        pcol[jl * h.m + im] = static_cast<signed char>(paley_entry(chi, h, im, jb0 + jl));
+    const int cnt = min(h.m, jb0 + blocks_per_wg) - jb0;
+    float* pcol = z + n;                                                  // [cnt][m] P[im][jb0 + jl]
+    float* w = pcol + blocks_per_wg * h.m;                                // [cnt][half]
+    signed char* chi = reinterpret_cast<signed char*>(w + blocks_per_wg * half);  // [q]
+    // 2. quadratic character: chi[0] = 0, squares +1, the rest -1
+    for (int i = tid; i < h.q; i += kRhtThreads) chi[i] = i == 0 ? 0 : -1;
+    __syncthreads();
+    for (int v = 1 + tid; v < h.q; v += kRhtThreads) chi[gf_square(v, h)] = 1;
+    __syncthreads();
+    for (int t = tid; t < cnt * h.m; t += kRhtThreads) {
+        const int jl = t / h.m, im = t - jl * h.m;
+        pcol[t] = static_cast<float>(paley_entry(chi, h, im, jb0 + jl));
     }
     __syncthreads();
-    for (int o = tid; o < (jb1 - jb0) * half; o += kRhtThreads) {
-        const int jl = o / half, j2 = o % half;
-        const signed char* pc = pcol + jl * h.m;
-        float acc = 0.f;
-        for (int im = 0; im < h.m; ++im) acc += static_cast<float>(pc[im]) * z[im * half + j2];
-        const int j = (jb0 + jl) * half + j2;
-        float v = acc * norm;
+    // 3. Paley factor: w[jl][i2] = sum_im P[im][jb0 + jl] z[im][i2]
+    for (int o = tid; o < cnt * half; o += kRhtThreads) {
+        const int jl = o >> h.k, i2 = o & (half - 1);
+        const float* pc = pcol + jl * h.m;
+        float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+        int im = 0;
+        for (; im + 4 <= h.m; im += 4) {
+            a0 = __builtin_fmaf(pc[im], z[im * half + i2], a0);
+            a1 = __builtin_fmaf(pc[im + 1], z[(im + 1) * half + i2], a1);
+            a2 = __builtin_fmaf(pc[im + 2], z[(im + 2) * half + i2], a2);
+            a3 = __builtin_fmaf(pc[im + 3], z[(im + 3) * half + i2], a3);
+        }
+        for (; im < h.m; ++im) a0 = __builtin_fmaf(pc[im], z[im * half + i2], a0);
+        w[o] = (a0 + a1) + (a2 + a3);
+    }
+    __syncthreads();
+    // 4. Sylvester factor inside each of this workgroup's blocks
+    sylvester_blocks(w, cnt * half, h.k, tid);
+    for (int o = tid; o < cnt * half; o += kRhtThreads) {
+        const int j = jb0 * half + o;
+        float v = w[o] * norm;
         if (mode == 1) v *= static_cast<float>(signs[j]);
         store_out(y, row * n + j, v, y_dtype);
     }
@@ -215,30 +259,59 @@ bool hadamard_spec(int64_t n, HadSpec* out) {
     return false;
 }
 
-size_t rht_lds_bytes(const HadSpec& h, int n) {
+constexpr size_t kRhtMaxLds = 160 * 1024;
+
+size_t rht_lds_bytes(const HadSpec& h, int n, int per) {
     size_t b = static_cast<size_t>(n) * 4;
-    if (h.m > 1) b += static_cast<size_t>((h.q + 15) / 16 * 16) + static_cast<size_t>(kMaxPaleyBlocks) * h.m;
+    if (h.m > 1)
+        b += static_cast<size_t>(per) * h.m * 4 + static_cast<size_t>(per) * (size_t{1} << h.k) * 4 +
+             static_cast<size_t>(h.q);
     return b;
+}
+
+// Output blocks of the Paley factor per workgroup: at most one output per
+// thread, and few enough blocks that a row spreads over about 32 workgroups
+// or more (the dense factor is bound by LDS reads); fewer when the slice of
+// the Paley matrix would not fit the LDS.
+int rht_blocks_per_wg(const HadSpec& h, int n) {
+    int per = kRhtThreads >> h.k;
+    const int spread = h.m / 32;
+    if (spread >= 1 && per > spread) per = spread;
+    per = per < 1 ? 1 : (per > h.m ? h.m : per);
+    while (per > 1 && rht_lds_bytes(h, n, per) > kRhtMaxLds) per /= 2;
+    return per;
 }
 
 int launch_rht(int64_t n, int64_t M, const void* x, int x_dtype, const signed char* signs, int mode, void* y,
                int y_dtype, hipStream_t s) {
     HadSpec h;
     if (!hadamard_spec(n, &h)) return UNISVQ_EUNSUP;
-    const size_t lds = rht_lds_bytes(h, static_cast<int>(n));
-    if (lds > 160 * 1024) return UNISVQ_EUNSUP;
+    const int per = h.m > 1 ? rht_blocks_per_wg(h, static_cast<int>(n)) : 1;
+    const size_t lds = rht_lds_bytes(h, static_cast<int>(n), per);
+    if (lds > kRhtMaxLds) return UNISVQ_EUNSUP;
     static bool attr_done = false;  // idempotent; racing first calls set the same value
     if (!attr_done) {
-        if (hipFuncSetAttribute(reinterpret_cast<const void*>(&rht_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                160 * 1024) != hipSuccess)
-            return UNISVQ_EHIP;
+        const void* fns[3] = {reinterpret_cast<const void*>(&rht_kernel<_Float16>),
+                              reinterpret_cast<const void*>(&rht_kernel<__bf16>),
+                              reinterpret_cast<const void*>(&rht_kernel<float>)};
+        for (const void* f : fns)
+            if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kRhtMaxLds)) !=
+                hipSuccess)
+                return UNISVQ_EHIP;
         attr_done = true;
     }
-    const int per = h.m > 1 ? (h.m >= 64 ? kMaxPaleyBlocks : 1) : 1;
     const unsigned gx = h.m > 1 ? static_cast<unsigned>((h.m + per - 1) / per) : 1u;
     const float norm = static_cast<float>(1.0 / std::sqrt(static_cast<double>(n)));
-    hipLaunchKernelGGL(rht_kernel, dim3(gx, static_cast<unsigned>(M)), dim3(kRhtThreads), lds, s, x, x_dtype, signs,
-                       mode, y, y_dtype, static_cast<int>(n), h, per, norm);
+    const dim3 grid(gx, static_cast<unsigned>(M));
+    if (x_dtype == UNISVQ_F16)
+        hipLaunchKernelGGL(rht_kernel<_Float16>, grid, dim3(kRhtThreads), lds, s, static_cast<const _Float16*>(x),
+                           signs, mode, y, y_dtype, static_cast<int>(n), h, per, norm);
+    else if (x_dtype == UNISVQ_BF16)
+        hipLaunchKernelGGL(rht_kernel<__bf16>, grid, dim3(kRhtThreads), lds, s, static_cast<const __bf16*>(x), signs,
+                           mode, y, y_dtype, static_cast<int>(n), h, per, norm);
+    else
+        hipLaunchKernelGGL(rht_kernel<float>, grid, dim3(kRhtThreads), lds, s, static_cast<const float*>(x), signs,
+                           mode, y, y_dtype, static_cast<int>(n), h, per, norm);
     return hipGetLastError() == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
 }
 
