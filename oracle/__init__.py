@@ -75,6 +75,23 @@ def _load():
     lib.oracle_hadamard.restype = ctypes.c_int
     lib.oracle_rht.argtypes = [i64, i64, p, p, ctypes.c_int, p]
     lib.oracle_rht.restype = ctypes.c_int
+    ci = ctypes.c_int
+    lib.oracle_var_codes_bytes.argtypes = [i64, i64, ci]
+    lib.oracle_var_codes_bytes.restype = i64
+    lib.oracle_var_pack_codes.argtypes = [i64, i64, ci, ci, p, p]
+    lib.oracle_var_pack_codes.restype = i64
+    lib.oracle_var_unpack_codes.argtypes = [i64, i64, ci, ci, p, p]
+    lib.oracle_var_unpack_codes.restype = ci
+    lib.oracle_var_affine_bytes.argtypes = [i64, i64, ci]
+    lib.oracle_var_affine_bytes.restype = i64
+    lib.oracle_var_pack_affine.argtypes = [i64, i64, ci, p, p, p]
+    lib.oracle_var_pack_affine.restype = ci
+    lib.oracle_var_unpack_affine.argtypes = [i64, i64, ci, p, p, p]
+    lib.oracle_var_unpack_affine.restype = ci
+    lib.oracle_var_decode.argtypes = [i64, i64, ci, p, i64, p, p, p]
+    lib.oracle_var_decode.restype = ci
+    lib.oracle_var_matmul_rows.argtypes = [i64, i64, ci, ci, p, i64, p, p, i64, p, i64, p, p, ci]
+    lib.oracle_var_matmul_rows.restype = ci
     _lib = lib
     return lib
 
@@ -302,4 +319,91 @@ def rht(X: np.ndarray, signs: np.ndarray, mode: str) -> np.ndarray:
     assert s.shape == (n,)
     Y = np.empty_like(X)
     _check(_load().oracle_rht(n, M, _ptr(X), _ptr(s), 0 if mode == "in" else 1, _ptr(Y)), "rht")
+    return Y
+
+
+# ------------------------------------------------ format variants (b = 2, 3; d = 4, 8)
+
+def var_codes_bytes(N: int, K: int, bits: int) -> int:
+    """Bytes of the variant codes-only format: bits per weight, nothing else."""
+    return _check(_load().oracle_var_codes_bytes(N, K, bits), "var_codes_bytes")
+
+
+def var_pack_codes(Q: np.ndarray, bits: int, d: int):
+    """Variant codes-only packing; returns (packed bytes, number of codes >= 2^bits)."""
+    N, K = Q.shape
+    Q = np.ascontiguousarray(Q, dtype=np.uint8)
+    out = np.empty(var_codes_bytes(N, K, bits), dtype=np.uint8)
+    bad = _check(_load().oracle_var_pack_codes(N, K, bits, d, _ptr(Q), _ptr(out)), "var_pack_codes")
+    return out, int(bad)
+
+
+def var_unpack_codes(packed: np.ndarray, N: int, K: int, bits: int, d: int) -> np.ndarray:
+    packed = np.ascontiguousarray(packed, dtype=np.uint8)
+    assert packed.size == var_codes_bytes(N, K, bits)
+    Q = np.empty((N, K), dtype=np.uint8)
+    _check(_load().oracle_var_unpack_codes(N, K, bits, d, _ptr(packed), _ptr(Q)), "var_unpack_codes")
+    return Q
+
+
+def var_affine_bytes(K: int, Ga: int, d: int) -> int:
+    return _check(_load().oracle_var_affine_bytes(K, Ga, d), "var_affine_bytes")
+
+
+def var_pack_affine(As: np.ndarray, Bs: np.ndarray, K: int) -> np.ndarray:
+    """Shared affine block (lane and row views) of As [Ga][d][d], Bs [Ga][d]."""
+    Ab, Bb = _bits16(As), _bits16(Bs)
+    Ga, d = Ab.shape[0], Ab.shape[1]
+    assert Ab.shape == (Ga, d, d) and Bb.shape == (Ga, d)
+    out = np.empty(var_affine_bytes(K, Ga, d), dtype=np.uint8)
+    _check(_load().oracle_var_pack_affine(K, Ga, d, _ptr(Ab), _ptr(Bb), _ptr(out)), "var_pack_affine")
+    return out
+
+
+def var_unpack_affine(block: np.ndarray, K: int, Ga: int, d: int):
+    """Inverse of var_pack_affine (raises if the two views disagree)."""
+    block = np.ascontiguousarray(block, dtype=np.uint8)
+    assert block.size == var_affine_bytes(K, Ga, d)
+    A = np.empty((Ga, d, d), dtype=np.uint16)
+    B = np.empty((Ga, d), dtype=np.uint16)
+    _check(_load().oracle_var_unpack_affine(K, Ga, d, _ptr(block), _ptr(A), _ptr(B)), "var_unpack_affine")
+    return A.view(np.float16), B.view(np.float16)
+
+
+def var_decode(Q: np.ndarray, As: np.ndarray, Bs: np.ndarray) -> np.ndarray:
+    """fp64 W_hat [N][K] from canonical codes and shared pairs As [Ga][d][d], Bs [Ga][d]."""
+    N, K = Q.shape
+    Q = np.ascontiguousarray(Q, dtype=np.uint8)
+    Ab, Bb = _bits16(As), _bits16(Bs)
+    Ga, d = Ab.shape[0], Ab.shape[1]
+    W = np.empty((N, K), dtype=np.float64)
+    _check(_load().oracle_var_decode(N, K, d, _ptr(Q), Ga, _ptr(Ab), _ptr(Bb), _ptr(W)), "var_decode")
+    return W
+
+
+def var_matmul(packed_codes: np.ndarray, N: int, K: int, bits: int, As: np.ndarray, Bs: np.ndarray,
+               X: np.ndarray, rows=None, threads: int | None = None):
+    """Y = X * W_hat^T in fp64 from variant codes-only bytes and shared pairs."""
+    packed_codes = np.ascontiguousarray(packed_codes, dtype=np.uint8)
+    assert packed_codes.size == var_codes_bytes(N, K, bits)
+    Ab, Bb = _bits16(As), _bits16(Bs)
+    Ga, d = Ab.shape[0], Ab.shape[1]
+    assert Ab.shape == (Ga, d, d) and Bb.shape == (Ga, d)
+    X = np.ascontiguousarray(X, dtype=np.float64)
+    if X.ndim == 1:
+        X = X[None, :]
+    M = X.shape[0]
+    assert X.shape[1] == K
+    if threads is None:
+        threads = default_threads()
+    lib = _load()
+    if rows is None:
+        Y = np.empty((M, N), dtype=np.float64)
+        _check(lib.oracle_var_matmul_rows(N, K, bits, d, _ptr(packed_codes), Ga, _ptr(Ab), _ptr(Bb), M, _ptr(X),
+                                          N, None, _ptr(Y), threads), "var_matmul")
+    else:
+        r = np.ascontiguousarray(rows, dtype=np.int64)
+        Y = np.empty((M, r.size), dtype=np.float64)
+        _check(lib.oracle_var_matmul_rows(N, K, bits, d, _ptr(packed_codes), Ga, _ptr(Ab), _ptr(Bb), M, _ptr(X),
+                                          r.size, _ptr(r), _ptr(Y), threads), "var_matmul_rows")
     return Y

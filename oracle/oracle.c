@@ -676,3 +676,305 @@ int oracle_matmul_shared_rows(int64_t N, int64_t K, const uint8_t* packed_codes,
     if (K % OR_G || (Ga != 1 && Ga != K / OR_G)) return OR_ESHAPE;
     return matmul_rows(N, K, packed_codes, Ga, As, Bs, M, X, nrows, rows, Y, threads);
 }
+
+/* ======================================================================
+ * Format variants: b-bit codes (b = 2 or 3; Sec. 5.2.5, bit-width
+ * extensibility: the integer vectors only widen) and d-dimensional vectors
+ * (d = 4 or 8; Sec. 5.2.3, vector dimension), with the pairs shared by all
+ * rows as the paper keeps them (one (A, B) per weight matrix, Sec. 4.2; or
+ * one per 128-column group).  Restated from the definition of the variant
+ * codes-only format (include/unisvq.h, variant format block):
+ *   One group of one row block takes CB = 512 (b = 2) or 768 (b = 3) bytes;
+ *   row block rb starts at rb*(K/128)*CB; packet p (groups 2p, 2p+1) is
+ *   2*CB bytes at p*2*CB, a final half packet (odd K/128) CB bytes.
+ *   Slot s = 0..63: row r = 16rb + s/4, lane index j = s%4.  The slot's 32
+ *   codes of group g are numbered (h, u), h = 0..1, u = 0..15:
+ *     d = 4: Q[r][128g + 4(16h + u) + j]  (vector 16h+u, component j)
+ *     d = 8: Q[r][128g + 8u + 4h + j]     (vector u, component 4h+j)
+ *   Low field (8 bytes): 32-bit word h, bits 2u and 2u+1 = bits 0, 1 of code (h, u).
+ *   High field (b = 3, 4 bytes): bit 8n + 4m + 2h + p = bit 2 of code
+ *     (h, u = 4n + 2m + p), n = 0..3, m, p = 0..1.
+ *   Full packet at P: low field of group 2p+jj at P + 16s + 8jj, high field
+ *   at P + 1024 + 8s + 4jj.  Half packet: low at P + 8s, high at P + 512 + 4s.
+ *   Shared pairs As fp16 [Ga][d][d] (As[a][b] multiplies q_b into component
+ *   a), Bs fp16 [Ga][d], Ga = 1 or K/128; group g uses pair (Ga == 1 ? 0 : g).
+ *   Affine block: records of RB = 160 (d = 4) or 576 (d = 8) bytes, one per
+ *   pair of groups (a single record when Ga = 1); record R serves groups
+ *   2R + jj with pair pi = (Ga == 1 ? 0 : 2R + jj); a group past the last
+ *   holds zeros.  Inside a record (fp16 each):
+ *     lane view, d = 4: As[pi][a][j] at 16j + 8jj + 2a;  Bs[pi][j] at 64 + 4j + 2jj
+ *     lane view, d = 8: As[pi][a][4h+j] at 64j + 32jj + 16h + 2a (a = 0..7);
+ *                       Bs[pi][4h+j] at 256 + 8j + 4jj + 2h
+ *     row view at V = 80 (d = 4) or 288 (d = 8), E = 2(d*d + d):
+ *                       As[pi][a][b] at V + jj*E + 2(d*a + b);  Bs[pi][a] at V + jj*E + 2*d*d + 2a
+ * ====================================================================== */
+
+static int var_ok(int bits, int d) { return (bits == 2 || bits == 3) && (d == 4 || d == 8); }
+
+static int64_t var_group_bytes(int bits) { return bits == 3 ? 768 : 512; }
+
+int64_t oracle_var_codes_bytes(int64_t N, int64_t K, int bits) {
+    if (bits != 2 && bits != 3) return OR_EINVAL;
+    if (!shape_ok(N, K)) return OR_ESHAPE;
+    return (N / OR_ROWBLOCK) * (K / OR_G) * var_group_bytes(bits);
+}
+
+/* Column (within the row) of code (h, u) of lane index j in group g. */
+static int64_t var_column(int d, int64_t g, int h, int u, int j) {
+    if (d == 4) return g * OR_G + 4 * (16 * h + u) + j;
+    return g * OR_G + 8 * u + 4 * h + j;
+}
+
+/* Byte offsets of the low and high fields of slot s, group g, row block rb. */
+static void var_place(int64_t K, int bits, int64_t rb, int64_t g, int s, int64_t* lo, int64_t* hi) {
+    int64_t groups = K / OR_G, cb = var_group_bytes(bits);
+    int64_t P = rb * groups * cb + (g / 2) * 2 * cb;
+    if ((groups % 2 == 1) && (g == groups - 1)) {
+        *lo = P + 8 * s;
+        *hi = P + 512 + 4 * s;
+    } else {
+        *lo = P + 16 * s + 8 * (g % 2);
+        *hi = P + 1024 + 8 * s + 4 * (g % 2);
+    }
+}
+
+/* Bit position of code (h, u) inside the high field. */
+static int var_hi_bit(int h, int u) {
+    int n = u / 4, m = (u / 2) % 2, p = u % 2;
+    return 8 * n + 4 * m + 2 * h + p;
+}
+
+static void set_bit(uint8_t* base, int bit) { base[bit / 8] |= (uint8_t)(1u << (bit % 8)); }
+static int get_bit(const uint8_t* base, int bit) { return (base[bit / 8] >> (bit % 8)) & 1; }
+
+/* Pack Q [N][K] (codes 0..2^bits-1; larger ones are counted and stored
+ * modulo 2^bits).  Returns the count of such codes. */
+int64_t oracle_var_pack_codes(int64_t N, int64_t K, int bits, int d, const uint8_t* Q, uint8_t* out) {
+    if (!Q || !out || !var_ok(bits, d)) return OR_EINVAL;
+    if (!shape_ok(N, K)) return OR_ESHAPE;
+    int64_t groups = K / OR_G, bad = 0;
+    int top = 1 << bits;
+    memset(out, 0, (size_t)oracle_var_codes_bytes(N, K, bits));
+    for (int64_t r = 0; r < N; ++r) {
+        int64_t rb = r / OR_ROWBLOCK, rl = r % OR_ROWBLOCK;
+        for (int64_t g = 0; g < groups; ++g)
+            for (int j = 0; j < 4; ++j) {
+                int s = (int)(rl * 4 + j);
+                int64_t lo, hi;
+                var_place(K, bits, rb, g, s, &lo, &hi);
+                for (int h = 0; h < 2; ++h)
+                    for (int u = 0; u < 16; ++u) {
+                        int q = Q[r * K + var_column(d, g, h, u, j)];
+                        if (q >= top) ++bad;
+                        q %= top;
+                        /* word h of the low field: bits 32h + 2u, 32h + 2u + 1 */
+                        if (q & 1) set_bit(out + lo, 32 * h + 2 * u);
+                        if (q & 2) set_bit(out + lo, 32 * h + 2 * u + 1);
+                        if (bits == 3 && (q & 4)) set_bit(out + hi, var_hi_bit(h, u));
+                    }
+            }
+    }
+    return bad;
+}
+
+static void var_unpack_row(int64_t K, int bits, int d, const uint8_t* packed, int64_t r, uint8_t* q_row) {
+    int64_t groups = K / OR_G, rb = r / OR_ROWBLOCK, rl = r % OR_ROWBLOCK;
+    for (int64_t g = 0; g < groups; ++g)
+        for (int j = 0; j < 4; ++j) {
+            int s = (int)(rl * 4 + j);
+            int64_t lo, hi;
+            var_place(K, bits, rb, g, s, &lo, &hi);
+            for (int h = 0; h < 2; ++h)
+                for (int u = 0; u < 16; ++u) {
+                    int q = get_bit(packed + lo, 32 * h + 2 * u) | (get_bit(packed + lo, 32 * h + 2 * u + 1) << 1);
+                    if (bits == 3) q |= get_bit(packed + hi, var_hi_bit(h, u)) << 2;
+                    q_row[var_column(d, g, h, u, j)] = (uint8_t)q;
+                }
+        }
+}
+
+int oracle_var_unpack_codes(int64_t N, int64_t K, int bits, int d, const uint8_t* packed, uint8_t* Q) {
+    if (!packed || !Q || !var_ok(bits, d)) return OR_EINVAL;
+    if (!shape_ok(N, K)) return OR_ESHAPE;
+    for (int64_t r = 0; r < N; ++r) var_unpack_row(K, bits, d, packed, r, Q + r * K);
+    return OR_OK;
+}
+
+static int64_t var_record_bytes(int d) { return d == 4 ? 160 : 576; }
+
+int64_t oracle_var_affine_bytes(int64_t K, int64_t Ga, int d) {
+    if (d != 4 && d != 8) return OR_EINVAL;
+    if (K <= 0 || K % OR_G) return OR_ESHAPE;
+    if (Ga != 1 && Ga != K / OR_G) return OR_EINVAL;
+    int64_t records = Ga == 1 ? 1 : (K / OR_G + 1) / 2;
+    return records * var_record_bytes(d);
+}
+
+/* Offsets (inside record R) of As[pi][a][b] and Bs[pi][a] in the lane view
+ * and in the row view, for the record's group jj. */
+static int64_t var_lane_a(int d, int jj, int a, int b) {
+    if (d == 4) return 16 * b + 8 * jj + 2 * a;
+    return 64 * (b % 4) + 32 * jj + 16 * (b / 4) + 2 * a;
+}
+static int64_t var_lane_b(int d, int jj, int a) {
+    if (d == 4) return 64 + 4 * a + 2 * jj;
+    return 256 + 8 * (a % 4) + 4 * jj + 2 * (a / 4);
+}
+static int64_t var_row_a(int d, int jj, int a, int b) {
+    int64_t V = d == 4 ? 80 : 288, E = 2 * (d * d + d);
+    return V + jj * E + 2 * (d * a + b);
+}
+static int64_t var_row_b(int d, int jj, int a) {
+    int64_t V = d == 4 ? 80 : 288, E = 2 * (d * d + d);
+    return V + jj * E + 2 * d * d + 2 * a;
+}
+
+int oracle_var_pack_affine(int64_t K, int64_t Ga, int d, const uint16_t* As, const uint16_t* Bs, uint8_t* out) {
+    if (!As || !Bs || !out) return OR_EINVAL;
+    int64_t total = oracle_var_affine_bytes(K, Ga, d);
+    if (total < 0) return (int)total;
+    int64_t groups = K / OR_G, rb = var_record_bytes(d), records = total / rb;
+    memset(out, 0, (size_t)total);
+    for (int64_t R = 0; R < records; ++R)
+        for (int jj = 0; jj < 2; ++jj) {
+            int64_t g = 2 * R + jj;
+            if (Ga != 1 && g >= groups) continue; /* past the last group: zeros */
+            int64_t pi = Ga == 1 ? 0 : g;
+            uint8_t* rec = out + R * rb;
+            for (int a = 0; a < d; ++a) {
+                for (int b = 0; b < d; ++b) {
+                    uint16_t v = As[(pi * d + a) * d + b];
+                    put_u16(rec + var_lane_a(d, jj, a, b), v);
+                    put_u16(rec + var_row_a(d, jj, a, b), v);
+                }
+                put_u16(rec + var_lane_b(d, jj, a), Bs[pi * d + a]);
+                put_u16(rec + var_row_b(d, jj, a), Bs[pi * d + a]);
+            }
+        }
+    return OR_OK;
+}
+
+/* Inverse of oracle_var_pack_affine, read from the lane view; returns
+ * OR_EINVAL if the row view disagrees with it anywhere. */
+int oracle_var_unpack_affine(int64_t K, int64_t Ga, int d, const uint8_t* rec_block, uint16_t* As, uint16_t* Bs) {
+    if (!rec_block || !As || !Bs) return OR_EINVAL;
+    int64_t total = oracle_var_affine_bytes(K, Ga, d);
+    if (total < 0) return (int)total;
+    int64_t rb = var_record_bytes(d);
+    for (int64_t pi = 0; pi < Ga; ++pi) {
+        int64_t R = Ga == 1 ? 0 : pi / 2;
+        int jj = Ga == 1 ? 0 : (int)(pi % 2);
+        const uint8_t* rec = rec_block + R * rb;
+        for (int a = 0; a < d; ++a) {
+            for (int b = 0; b < d; ++b) {
+                uint16_t v = get_u16(rec + var_lane_a(d, jj, a, b));
+                if (v != get_u16(rec + var_row_a(d, jj, a, b))) return OR_EINVAL;
+                As[(pi * d + a) * d + b] = v;
+            }
+            uint16_t v = get_u16(rec + var_lane_b(d, jj, a));
+            if (v != get_u16(rec + var_row_b(d, jj, a))) return OR_EINVAL;
+            Bs[pi * d + a] = v;
+        }
+    }
+    return OR_OK;
+}
+
+/* One row: vector v covers columns d*v .. d*v+d-1 (Eq. 8); component a is
+ * sum_b As[pi][a][b] * q[dv + b] + Bs[pi][a] (Eq. 4), pi the pair of group
+ * g = d*v / 128.  Products of fp16 values and integers below 8 are exact in
+ * fp64, and so is the sum of at most 8 of them plus B. */
+static void var_decode_row(int64_t K, int d, const uint8_t* q_row, int64_t Ga, const uint16_t* As,
+                           const uint16_t* Bs, double* w) {
+    for (int64_t v = 0; v < K / d; ++v) {
+        int64_t g = (d * v) / OR_G, pi = Ga == 1 ? 0 : g;
+        for (int a = 0; a < d; ++a) {
+            double acc = oracle_half_to_double(Bs[pi * d + a]);
+            for (int b = 0; b < d; ++b)
+                acc += oracle_half_to_double(As[(pi * d + a) * d + b]) * (double)q_row[d * v + b];
+            w[d * v + a] = acc;
+        }
+    }
+}
+
+/* Decode canonical codes (no packing); N may be any positive count. */
+int oracle_var_decode(int64_t N, int64_t K, int d, const uint8_t* Q, int64_t Ga, const uint16_t* As,
+                      const uint16_t* Bs, double* W) {
+    if (!Q || !As || !Bs || !W || (d != 4 && d != 8)) return OR_EINVAL;
+    if (N <= 0 || K <= 0 || K % OR_G) return OR_ESHAPE;
+    if (Ga != 1 && Ga != K / OR_G) return OR_EINVAL;
+    for (int64_t r = 0; r < N; ++r) var_decode_row(K, d, Q + r * K, Ga, As, Bs, W + r * K);
+    return OR_OK;
+}
+
+typedef struct {
+    int64_t N, K, M, nrows, Ga;
+    int bits, d;
+    const uint8_t* packed;
+    const uint16_t *As, *Bs;
+    const double* X;
+    const int64_t* rows;
+    double* Y;
+    int64_t first, last;
+    int status;
+} var_job;
+
+static void* var_worker(void* arg) {
+    var_job* j = (var_job*)arg;
+    uint8_t* q = malloc((size_t)j->K);
+    double* w = malloc((size_t)j->K * sizeof(double));
+    if (!q || !w) { j->status = OR_EINVAL; free(q); free(w); return NULL; }
+    for (int64_t i = j->first; i < j->last; ++i) {
+        int64_t r = j->rows ? j->rows[i] : i;
+        var_unpack_row(j->K, j->bits, j->d, j->packed, r, q);
+        var_decode_row(j->K, j->d, q, j->Ga, j->As, j->Bs, w);
+        for (int64_t t = 0; t < j->M; ++t) {
+            const double* x = j->X + t * j->K;
+            double acc = 0.0;
+            for (int64_t k = 0; k < j->K; ++k) acc += x[k] * w[k];
+            j->Y[t * j->nrows + i] = acc;
+        }
+    }
+    j->status = OR_OK;
+    free(q); free(w);
+    return NULL;
+}
+
+/* Y[t][i] = sum_k X[t][k] * W_hat[rows[i]][k] (Eq. 1) from variant codes-only
+ * bytes and the canonical shared pairs; rows == NULL means all N rows. */
+int oracle_var_matmul_rows(int64_t N, int64_t K, int bits, int d, const uint8_t* packed, int64_t Ga,
+                           const uint16_t* As, const uint16_t* Bs, int64_t M, const double* X, int64_t nrows,
+                           const int64_t* rows, double* Y, int threads) {
+    if (!packed || !As || !Bs || !X || !Y || !var_ok(bits, d)) return OR_EINVAL;
+    if (!shape_ok(N, K) || M < 0 || nrows < 0) return OR_ESHAPE;
+    if (Ga != 1 && Ga != K / OR_G) return OR_EINVAL;
+    if (!rows && nrows != N) return OR_ESHAPE;
+    if (rows)
+        for (int64_t i = 0; i < nrows; ++i)
+            if (rows[i] < 0 || rows[i] >= N) return OR_EINVAL;
+    if (M == 0 || nrows == 0) return OR_OK;
+    if (threads < 1) threads = 1;
+    if (threads > nrows) threads = (int)nrows;
+    var_job* jobs = calloc((size_t)threads, sizeof(var_job));
+    pthread_t* tids = calloc((size_t)threads, sizeof(pthread_t));
+    if (!jobs || !tids) { free(jobs); free(tids); return OR_EINVAL; }
+    int64_t per = (nrows + threads - 1) / threads;
+    for (int t = 0; t < threads; ++t) {
+        var_job* j = &jobs[t];
+        j->N = N; j->K = K; j->M = M; j->nrows = nrows; j->Ga = Ga;
+        j->bits = bits; j->d = d; j->packed = packed; j->As = As; j->Bs = Bs;
+        j->X = X; j->rows = rows; j->Y = Y;
+        j->first = t * per;
+        j->last = (t + 1) * per < nrows ? (t + 1) * per : nrows;
+        if (j->first > j->last) j->first = j->last;
+        if (threads == 1) var_worker(j);
+        else if (pthread_create(&tids[t], NULL, var_worker, j) != 0) { var_worker(j); tids[t] = 0; }
+    }
+    int status = OR_OK;
+    if (threads > 1)
+        for (int t = 0; t < threads; ++t)
+            if (tids[t]) pthread_join(tids[t], NULL);
+    for (int t = 0; t < threads; ++t)
+        if (jobs[t].status != OR_OK) status = jobs[t].status;
+    free(jobs); free(tids);
+    return status;
+}

@@ -572,3 +572,233 @@ def test_rht_preserves_norms_and_matches_dense_sylvester():
     np.testing.assert_allclose(y, (x * s) @ linalg.hadamard(n) / np.sqrt(n), rtol=1e-12, atol=1e-12)
     z = oracle.rht(x, s, "out")
     np.testing.assert_allclose(z, (x @ linalg.hadamard(n) / np.sqrt(n)) * s, rtol=1e-12, atol=1e-12)
+
+
+# ---------------------------------------------------------------- format variants
+# b-bit codes, b = 2 or 3 (Sec. 5.2.5: only the integer vectors widen) and
+# d-dimensional vectors, d = 4 or 8 (Sec. 5.2.3), with pairs shared by the
+# rows (one per matrix, Sec. 4.2, or one per 128-column group).
+
+VARIANTS = [(2, 4), (3, 4), (2, 8), (3, 8)]
+
+
+def _var_params(rng, N, K, bits, d, Ga, a_std=0.05, b_std=0.02):
+    Q = rng.integers(0, 1 << bits, size=(N, K), dtype=np.uint8)
+    A = (rng.standard_normal((Ga, d, d)) * a_std).astype(np.float16)
+    B = (rng.standard_normal((Ga, d)) * b_std).astype(np.float16)
+    return Q, A, B
+
+
+def test_var_sizes():
+    for N, K in [(16, 128), (4096, 4096), (11008, 4096)]:
+        assert oracle.var_codes_bytes(N, K, 2) == N * K // 4
+        assert oracle.var_codes_bytes(N, K, 3) == N * K * 3 // 8
+    assert oracle.var_affine_bytes(4096, 1, 4) == 160
+    assert oracle.var_affine_bytes(4096, 1, 8) == 576
+    assert oracle.var_affine_bytes(384, 3, 8) == 2 * 576
+    with pytest.raises(oracle.OracleError):
+        oracle.var_affine_bytes(384, 2, 4)
+    with pytest.raises(oracle.OracleError):
+        oracle.var_codes_bytes(16, 128, 4)
+
+
+def test_var_code_positions_worked_by_hand():
+    g = json.load(open(os.path.join(GOLD, "var_positions.json")))
+    for c in g["codes"]:
+        Q = np.zeros((c["N"], c["K"]), np.uint8)
+        Q[tuple(c["index"])] = c["value"]
+        packed, bad = oracle.var_pack_codes(Q, c["bits"], c["d"])
+        assert bad == 0
+        expect = np.zeros_like(packed)
+        for off, v in c["bytes"].items():
+            expect[int(off)] = v
+        assert np.array_equal(packed, expect), c["work"]
+
+
+def test_var_affine_positions_worked_by_hand():
+    g = json.load(open(os.path.join(GOLD, "var_positions.json")))
+    for c in g["affine"]:
+        d, Ga = c["d"], c["Ga"]
+        A = np.zeros((Ga, d, d), np.uint16)
+        B = np.zeros((Ga, d), np.uint16)
+        target = A if c["param"] == "A" else B
+        target[(c["pair"],) + tuple(c["index"])] = c["bits16"]
+        block = oracle.var_pack_affine(A, B, c["K"])
+        expect = np.zeros_like(block)
+        for off, v in c["bytes"].items():
+            expect[int(off)] = v
+        assert np.array_equal(block, expect), c["work"]
+
+
+@pytest.mark.parametrize("bits,d", VARIANTS)
+@pytest.mark.parametrize("N,K", [(16, 128), (32, 384), (48, 1152)])
+def test_var_round_trip(bits, d, N, K):
+    rng = np.random.default_rng(bits * 100 + d + K)
+    for Ga in (1, K // 128):
+        Q, A, B = _var_params(rng, N, K, bits, d, Ga)
+        packed, bad = oracle.var_pack_codes(Q, bits, d)
+        assert bad == 0
+        assert np.array_equal(oracle.var_unpack_codes(packed, N, K, bits, d), Q)
+        A2, B2 = oracle.var_unpack_affine(oracle.var_pack_affine(A, B, K), K, Ga, d)
+        assert np.array_equal(A2.view(np.uint16), A.view(np.uint16))
+        assert np.array_equal(B2.view(np.uint16), B.view(np.uint16))
+
+
+def test_var_2bit_d4_is_the_codes_only_format():
+    """The variant layout with b = 2, d = 4 is byte for byte the codes-only
+    format (pinned separately by its own hand-worked offsets)."""
+    rng = np.random.default_rng(2)
+    for N, K in [(16, 128), (32, 640)]:
+        Q = rng.integers(0, 4, size=(N, K), dtype=np.uint8)
+        assert np.array_equal(oracle.var_pack_codes(Q, 2, 4)[0], oracle.pack_codes(Q)[0])
+
+
+def test_var_counts_out_of_range_codes():
+    Q = np.zeros((16, 256), np.uint8)
+    Q[3, 7], Q[9, 200], Q[0, 0] = 8, 9, 7
+    _, bad = oracle.var_pack_codes(Q, 3, 8)
+    assert bad == 2
+    _, bad = oracle.var_pack_codes(Q, 2, 4)
+    assert bad == 3
+
+
+def test_var_unpack_affine_rejects_disagreeing_views():
+    A = np.ones((1, 8, 8), np.float16)
+    B = np.ones((1, 8), np.float16)
+    block = oracle.var_pack_affine(A, B, 256)
+    block[300] ^= 1  # one byte of the row view
+    with pytest.raises(oracle.OracleError):
+        oracle.var_unpack_affine(block, 256, 1, 8)
+
+
+@pytest.mark.parametrize("d", [4, 8])
+def test_var_3bit_with_small_codes_equals_2bit(d):
+    """Codes below 4 decode the same whether stored in 2 or 3 bits."""
+    rng = np.random.default_rng(31 + d)
+    N, K, M = 32, 384, 2
+    Q, A, B = _var_params(rng, N, K, 2, d, K // 128)
+    X = rng.standard_normal((M, K))
+    p2, _ = oracle.var_pack_codes(Q, 2, d)
+    p3, _ = oracle.var_pack_codes(Q, 3, d)
+    np.testing.assert_array_equal(oracle.var_matmul(p3, N, K, 3, A, B, X), oracle.var_matmul(p2, N, K, 2, A, B, X))
+
+
+@pytest.mark.parametrize("d", [4, 8])
+def test_var_3bit_is_low_part_plus_four_times_high_bit(d):
+    """q = (q & 3) + 4 (q >> 2) and the decode is linear in q: decoding the
+    3-bit codes equals decoding the low two bits with (A, B) plus the high
+    bits with (4A, 0) (4A is exact in fp16)."""
+    rng = np.random.default_rng(41 + d)
+    N, K, M = 32, 640, 3
+    Q, A, B = _var_params(rng, N, K, 3, d, 1)
+    X = rng.standard_normal((M, K))
+    Y = oracle.var_matmul(oracle.var_pack_codes(Q, 3, d)[0], N, K, 3, A, B, X)
+    Y_lo = oracle.var_matmul(oracle.var_pack_codes(Q & 3, 2, d)[0], N, K, 2, A, B, X)
+    A4 = (4.0 * A.astype(np.float64)).astype(np.float16)
+    assert np.array_equal(A4.astype(np.float64), 4.0 * A.astype(np.float64))
+    Y_hi = oracle.var_matmul(oracle.var_pack_codes(Q >> 2, 2, d)[0], N, K, 2, A4, np.zeros_like(B), X)
+    np.testing.assert_allclose(Y, Y_lo + Y_hi, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("bits", [2, 3])
+def test_var_block_diagonal_d8_equals_d4(bits):
+    """An 8-vector whose A is block diagonal diag(A4, A4) with B = (B4, B4) is
+    two 4-vectors decoded with (A4, B4): the d = 8 product equals the d = 4
+    one (for b = 2 computed by the separately pinned codes-only product)."""
+    rng = np.random.default_rng(50 + bits)
+    N, K, M = 32, 384, 2
+    Ga = K // 128
+    Q, A4, B4 = _var_params(rng, N, K, bits, 4, Ga)
+    A8 = np.zeros((Ga, 8, 8), np.float16)
+    A8[:, :4, :4] = A4
+    A8[:, 4:, 4:] = A4
+    B8 = np.concatenate([B4, B4], axis=1)
+    X = rng.standard_normal((M, K))
+    Y8 = oracle.var_matmul(oracle.var_pack_codes(Q, bits, 8)[0], N, K, bits, A8, B8, X)
+    Y4 = oracle.var_matmul(oracle.var_pack_codes(Q, bits, 4)[0], N, K, bits, A4, B4, X)
+    np.testing.assert_allclose(Y8, Y4, rtol=1e-12, atol=1e-12)
+    if bits == 2:
+        Yc = oracle.matmul_shared(oracle.pack_codes(Q)[0], N, K, A4, B4, X)
+        np.testing.assert_allclose(Y4, Yc, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("bits,d", VARIANTS)
+def test_var_identity_and_scalar_special_cases(bits, d):
+    """A = I, B = 0 gives W_hat = Q (Y = X Q^T, a library matmul); A = s I,
+    B = -s c 1 with c = (2^b - 1)/2 gives the scalar dequantiser of Eq. 2,
+    s (Q - c)."""
+    rng = np.random.default_rng(60 + 10 * bits + d)
+    N, K, M = 32, 384, 2
+    Q = rng.integers(0, 1 << bits, size=(N, K), dtype=np.uint8)
+    pk, _ = oracle.var_pack_codes(Q, bits, d)
+    X = rng.integers(-8, 9, size=(M, K)).astype(np.float64)
+    I = np.eye(d, dtype=np.float16)[None]
+    Y = oracle.var_matmul(pk, N, K, bits, I, np.zeros((1, d), np.float16), X)
+    assert np.array_equal(Y, X @ Q.T.astype(np.float64))
+    s, c = 0.0625, ((1 << bits) - 1) / 2.0
+    W = oracle.var_decode(Q, (s * np.eye(d))[None].astype(np.float16), np.full((1, d), -s * c, np.float16))
+    assert np.array_equal(W, s * (Q.astype(np.float64) - c))
+
+
+@pytest.mark.parametrize("bits,d", [(2, 4), (3, 4), (2, 8)])
+def test_var_codebook_moments_closed_form(bits, d):
+    """Over the full grid of 2^(b d) code tuples (App. A.1 for b bits): mean
+    = c A 1 + B with c = (2^b - 1)/2 and covariance = ((4^b - 1)/12) A A^T."""
+    rng = np.random.default_rng(70 + 10 * bits + d)
+    n = 1 << (bits * d)
+    idx = np.arange(n)
+    q = np.stack([(idx >> (bits * b)) & ((1 << bits) - 1) for b in range(d)], axis=1)
+    Q = q.reshape(1, n * d).astype(np.uint8)
+    A = (rng.standard_normal((1, d, d)) * 0.3).astype(np.float16)
+    B = (rng.standard_normal((1, d)) * 0.1).astype(np.float16)
+    cw = oracle.var_decode(Q, A, B).reshape(n, d)
+    Af, Bf = A[0].astype(np.float64), B[0].astype(np.float64)
+    c, v = ((1 << bits) - 1) / 2.0, ((1 << (2 * bits)) - 1) / 12.0
+    mean = cw.mean(axis=0)
+    np.testing.assert_allclose(mean, c * Af.sum(axis=1) + Bf, rtol=0, atol=1e-11)
+    cov = (cw - mean).T @ (cw - mean) / n
+    np.testing.assert_allclose(cov, v * Af @ Af.T, rtol=0, atol=1e-10)
+
+
+@pytest.mark.parametrize("bits,d", [(3, 4), (2, 8)])
+def test_var_paper_initialisation_gives_centred_unit_grid(bits, d):
+    """Eq. 6 for b bits: A = s G, B = -s c G 1, s = sqrt(12/(4^b - 1)),
+    c = (2^b - 1)/2, G a random orthogonal matrix -> mean 0, covariance I
+    (App. A.1), up to the fp16 rounding of A and B."""
+    stats = pytest.importorskip("scipy.stats")
+    G = stats.ortho_group.rvs(d, random_state=17)
+    s, c = np.sqrt(12.0 / ((1 << (2 * bits)) - 1)), ((1 << bits) - 1) / 2.0
+    A = (s * G)[None].astype(np.float16)
+    B = (-c * s * G @ np.ones(d))[None].astype(np.float16)
+    n = 1 << (bits * d)
+    idx = np.arange(n)
+    q = np.stack([(idx >> (bits * b)) & ((1 << bits) - 1) for b in range(d)], axis=1)
+    cw = oracle.var_decode(q.reshape(1, n * d).astype(np.uint8), A, B).reshape(n, d)
+    np.testing.assert_allclose(cw.mean(axis=0), 0.0, atol=1e-2)
+    np.testing.assert_allclose(np.cov(cw.T, bias=True), np.eye(d), atol=1e-2)
+
+
+@pytest.mark.parametrize("bits,d", VARIANTS)
+def test_var_exact_rational_brute_force(bits, d):
+    """Exact rationals: the decode of every weight is exact and Y is within one
+    K-term summation rounding of the exact product."""
+    rng = np.random.default_rng(80 + 10 * bits + d)
+    N, K, M = 16, 256, 2
+    Ga = K // 128
+    Q, A, B = _var_params(rng, N, K, bits, d, Ga, a_std=0.5, b_std=0.5)
+    X = rng.standard_normal((M, K)).astype(np.float16)
+    Y = oracle.var_matmul(oracle.var_pack_codes(Q, bits, d)[0], N, K, bits, A, B, X.astype(np.float64))
+    Wd = oracle.var_decode(Q, A, B)
+    Af = [[[Fraction(float(A[g, a, b])) for b in range(d)] for a in range(d)] for g in range(Ga)]
+    for r in range(0, N, 7):
+        w_exact = []
+        for k in range(K):
+            v, a = divmod(k, d)
+            g = d * v // 128
+            w = Fraction(float(B[g, a])) + sum(Af[g][a][b] * int(Q[r, d * v + b]) for b in range(d))
+            w_exact.append(w)
+            assert Fraction(Wd[r, k]) == w
+        for t in range(M):
+            y = sum(Fraction(float(X[t, k])) * w_exact[k] for k in range(K))
+            scale = sum(abs(Fraction(float(X[t, k])) * w_exact[k]) for k in range(K))
+            assert abs(Fraction(Y[t, r]) - y) <= scale * Fraction(K, 2 ** 52)
