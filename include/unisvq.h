@@ -76,6 +76,37 @@
  *   (beta, b) of a wavefront reads exactly its A column and B values, as from
  *   a full-format packet.
  * ---------------------------------------------------------------------------
+ * Variant codes-only format: b-bit codes (b = 2 or 3; Sec. 5.2.5, where only
+ * the integer vectors widen) and d-dimensional vectors (d = 4 or 8; Sec.
+ * 5.2.3), with row-shared pairs as the paper keeps them (one per weight
+ * matrix, Sec. 4.2, or one per 128-column group).  Canonical inputs: Q uint8
+ * [N][K] (0..2^b-1); A fp16 [Ga][d][d] (A[a][b] multiplies q_b into output
+ * component a), B fp16 [Ga][d]; Ga = 1 or K/128, group g uses pair (Ga == 1
+ * ? 0 : g).  Vector i of a row covers input columns d*i .. d*i+d-1.
+ *   Codes: a group of a row block takes CB = 512 (b = 2) or 768 (b = 3) bytes;
+ *   row block rb starts at rb*(K/128)*CB; packet p (groups 2p, 2p+1) is 2*CB
+ *   bytes at p*2*CB, a final half packet (odd K/128) CB bytes.  Slot s = 0..63
+ *   stands for row r = 16rb + s/4 and lane index j = s%4; its 32 codes of
+ *   group g are numbered (h, u), h = 0..1, u = 0..15:
+ *     d = 4: Q[r][128g + 4(16h + u) + j]   (vector 16h+u, component j)
+ *     d = 8: Q[r][128g + 8u + 4h + j]      (vector u, component 4h+j)
+ *   Low field (8 bytes): 32-bit word h, bits 2u, 2u+1 = bits 0, 1 of code (h, u).
+ *   High field (b = 3, 4 bytes): bit 8n + 4m + 2h + p = bit 2 of code
+ *   (h, u = 4n + 2m + p).  Full packet at P: low field of group 2p+jj at
+ *   P + 16s + 8jj, high field at P + 1024 + 8s + 4jj; half packet: low at
+ *   P + 8s, high at P + 512 + 4s.  N*K*b/8 bytes.  (b = 2, d = 4 is exactly the
+ *   codes-only format above and is served by the *_shared entry points.)
+ *   Shared affine block: records of RB = 160 (d = 4) or 576 (d = 8) bytes, one
+ *   per pair of groups (a single record when Ga = 1); record R serves groups
+ *   2R + jj with pair pi = (Ga == 1 ? 0 : 2R + jj), zeros for a group past the
+ *   last.  Inside a record, fp16 each:
+ *     lane view (read by the matrix-vector kernel):
+ *       d = 4: A[pi][a][j] at 16j + 8jj + 2a;  B[pi][j] at 64 + 4j + 2jj
+ *       d = 8: A[pi][a][4h+j] at 64j + 32jj + 16h + 2a;  B[pi][4h+j] at 256 + 8j + 4jj + 2h
+ *     row view (read by the tiled product's weight decode), at V = 80 (d = 4)
+ *     or 288 (d = 8), E = 2(d*d + d):
+ *       A[pi][a][b] at V + jj*E + 2(d*a + b);  B[pi][a] at V + jj*E + 2*d*d + 2a
+ * ---------------------------------------------------------------------------
  */
 #ifndef UNISVQ_H
 #define UNISVQ_H
@@ -254,6 +285,66 @@ int unisvq_gemv_shared_batched(const unisvq_gemv_shared_problem* problems, int c
 int unisvq_gemm_shared(int64_t N, int64_t K, int64_t affine_groups, const void* packed_codes,
                        const void* packed_affine, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---- Format variants (variant codes-only format block above) ----
+ * (b, d) = (3, 4), (2, 8) or (3, 8); any other pair is UNISVQ_EUNSUP (b = 2,
+ * d = 4 uses the *_shared entry points). */
+
+/* Bytes of the variant codes for an N x K matrix (N*K*bits/8); 0 for an
+ * invalid shape or an unsupported (bits, d).  Host-only. */
+size_t unisvq_var_codes_bytes(int64_t N, int64_t K, int bits, int d);
+
+/* Bytes of the variant shared affine block: RB for affine_groups == 1, else
+ * RB*ceil(K/256) for affine_groups == K/128 (RB = 160 for d = 4, 576 for
+ * d = 8); 0 for anything else.  Host-only. */
+size_t unisvq_var_affine_bytes(int64_t K, int64_t affine_groups, int bits, int d);
+
+/* Pack codes and row-shared pairs into the variant format (all device):
+ *   codes          uint8 [N][K], values 0..2^bits-1
+ *   A, B           fp16 bits [affine_groups][d][d] and [affine_groups][d]
+ *   packed_codes   unisvq_var_codes_bytes(N, K, bits, d) bytes, 16-byte aligned
+ *   packed_affine  unisvq_var_affine_bytes(K, affine_groups, bits, d) bytes, 16-byte aligned
+ *   bad_codes      as unisvq_pack (codes >= 2^bits counted, stored modulo 2^bits)
+ * UNISVQ_EINVAL when affine_groups is neither 1 nor K/128.  Bit exact. */
+int unisvq_var_pack(int64_t N, int64_t K, int bits, int d, int64_t affine_groups, const uint8_t* codes,
+                    const uint16_t* A, const uint16_t* B, void* packed_codes, void* packed_affine,
+                    int32_t* bad_codes, void* stream);
+
+/* Exact inverse of unisvq_var_pack (A and B read from the lane view).  All device. */
+int unisvq_var_unpack(int64_t N, int64_t K, int bits, int d, int64_t affine_groups, const void* packed_codes,
+                      const void* packed_affine, uint8_t* codes, uint16_t* A, uint16_t* B, void* stream);
+
+/* Decode-phase product with variant weights: the matrix-vector kernel with
+ * T = sum_v x_v q_v^T per (row, group, token) formed on the matrix cores --
+ * for d = 8 as four 4 x 4 quadrants, for 3-bit codes as the low part plus 4
+ * times the high bit (q = lo + 4 hi) accumulated in the same chain -- then
+ * sum A o T + B . xbar in fp32, one rounding to y_dtype.  M 1..4, dtypes,
+ * LDS limit on K and errors as unisvq_gemv; packed_codes, packed_affine and x
+ * 16-byte aligned. */
+int unisvq_var_gemv(int64_t N, int64_t K, int bits, int d, int64_t affine_groups, const void* packed_codes,
+                    const void* packed_affine, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
+                    void* stream);
+
+/* Several independent variant products in one launch (all with the same
+ * bits and d; descriptors as unisvq_gemv_shared_batched, HOST array of
+ * 1..UNISVQ_MAX_BATCH entries). */
+int unisvq_var_gemv_batched(const unisvq_gemv_shared_problem* problems, int count, int bits, int d, int64_t M,
+                            int x_dtype, int y_dtype, void* stream);
+
+/* Device workspace unisvq_var_gemm needs (bytes; 0: none): the bf16 copy of
+ * x as for unisvq_gemm, and fp32 partial sums when the K range is split
+ * (every M goes to the tiled kernel here, so small M splits K).  Host-only. */
+size_t unisvq_var_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype);
+
+/* Prefill product with variant weights, any M: the tiled kernel of
+ * unisvq_gemm with the variant decode (every vector A q + B exactly in fp32
+ * on the matrix cores -- d = 8 as two output halves of two chained 4-column
+ * steps, 3-bit codes as lo + 4 hi -- rounded once to fp16 in LDS).  Dtypes,
+ * bf16 handling, K split and errors as unisvq_gemm; workspace sized by
+ * unisvq_var_gemm_workspace_bytes. */
+int unisvq_var_gemm(int64_t N, int64_t K, int bits, int d, int64_t affine_groups, const void* packed_codes,
+                    const void* packed_affine, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
+                    void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---- Nearest-codeword quantisation (Sec. 3.2.2, without Hessian feedback) ----
  * Codes of the affine-lattice point closest to each vector of d = 4

@@ -46,6 +46,27 @@ int check_shared(int64_t N, int64_t K, int64_t affine_groups, const void* codes,
     return UNISVQ_OK;
 }
 
+// Format variants: (bits, d) = (3, 4), (2, 8), (3, 8).
+bool var_ok(int bits, int d) { return (bits == 2 || bits == 3) && (d == 4 || d == 8) && !(bits == 2 && d == 4); }
+
+int64_t var_codes_size(int64_t N, int64_t K, int bits) {
+    return (N / unisvq::kRowBlock) * (K / unisvq::kGroup) * unisvq::var_group_bytes(bits);
+}
+
+int check_var(int64_t N, int64_t K, int bits, int d, int64_t affine_groups, const void* codes, const void* affine,
+              int64_t M, const void* x, int x_dtype, const void* y, int y_dtype) {
+    if (!codes || !affine || !x || !y) return UNISVQ_EINVAL;
+    if (M < 1 || M > (int64_t{1} << 31) - 1) return UNISVQ_EINVAL;
+    if (!x_dtype_ok(x_dtype) || !y_dtype_ok(y_dtype)) return UNISVQ_EINVAL;
+    if (!var_ok(bits, d)) return UNISVQ_EUNSUP;
+    if (!shape_ok(N, K)) return UNISVQ_ESHAPE;
+    if (!affine_groups_ok(K, affine_groups)) return UNISVQ_EINVAL;
+    if (!aligned(codes, 16) || !aligned(affine, 16) || !aligned(x, 16)) return UNISVQ_EALIGN;
+    if (var_codes_size(N, K, bits) > unisvq::kMaxBufferBytes) return UNISVQ_EUNSUP;
+    if (!aligned(y, y_dtype == UNISVQ_F32 ? 4 : 2)) return UNISVQ_EALIGN;
+    return UNISVQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -219,6 +240,99 @@ int unisvq_gemm_shared(int64_t N, int64_t K, int64_t affine_groups, const void* 
     return unisvq::launch_gemm_shared(N, K, static_cast<const uint8_t*>(packed_codes),
                                       static_cast<const uint8_t*>(packed_affine), affine_groups == 1 ? 1 : 0, M, x,
                                       x_dtype, y, y_dtype, workspace, static_cast<hipStream_t>(stream));
+}
+
+/* ---- format variants ---- */
+
+size_t unisvq_var_codes_bytes(int64_t N, int64_t K, int bits, int d) {
+    if (!shape_ok(N, K) || !var_ok(bits, d)) return 0;
+    return static_cast<size_t>(var_codes_size(N, K, bits));
+}
+
+size_t unisvq_var_affine_bytes(int64_t K, int64_t affine_groups, int bits, int d) {
+    if (K < unisvq::kGroup || K % unisvq::kGroup || K > (int64_t{1} << 31) - 1) return 0;
+    if (!var_ok(bits, d) || !affine_groups_ok(K, affine_groups)) return 0;
+    const int64_t records = affine_groups == 1 ? 1 : (K / unisvq::kGroup + 1) / 2;
+    return static_cast<size_t>(records) * unisvq::var_record_bytes(d);
+}
+
+int unisvq_var_pack(int64_t N, int64_t K, int bits, int d, int64_t affine_groups, const uint8_t* codes,
+                    const uint16_t* A, const uint16_t* B, void* packed_codes, void* packed_affine, int32_t* bad_codes,
+                    void* stream) {
+    if (!codes || !A || !B || !packed_codes || !packed_affine) return UNISVQ_EINVAL;
+    if (!var_ok(bits, d)) return UNISVQ_EUNSUP;
+    if (!shape_ok(N, K)) return UNISVQ_ESHAPE;
+    if (!affine_groups_ok(K, affine_groups)) return UNISVQ_EINVAL;
+    if (!aligned(packed_codes, 16) || !aligned(packed_affine, 16) || !aligned(A, 2) || !aligned(B, 2) ||
+        (bad_codes && !aligned(bad_codes, 4)))
+        return UNISVQ_EALIGN;
+    const hipError_t e = unisvq::launch_var_pack(N, K, bits, d, affine_groups, codes, A, B,
+                                                 static_cast<uint8_t*>(packed_codes),
+                                                 static_cast<uint8_t*>(packed_affine), bad_codes,
+                                                 static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+}
+
+int unisvq_var_unpack(int64_t N, int64_t K, int bits, int d, int64_t affine_groups, const void* packed_codes,
+                      const void* packed_affine, uint8_t* codes, uint16_t* A, uint16_t* B, void* stream) {
+    if (!codes || !A || !B || !packed_codes || !packed_affine) return UNISVQ_EINVAL;
+    if (!var_ok(bits, d)) return UNISVQ_EUNSUP;
+    if (!shape_ok(N, K)) return UNISVQ_ESHAPE;
+    if (!affine_groups_ok(K, affine_groups)) return UNISVQ_EINVAL;
+    if (!aligned(packed_codes, 16) || !aligned(packed_affine, 16) || !aligned(A, 2) || !aligned(B, 2))
+        return UNISVQ_EALIGN;
+    const hipError_t e = unisvq::launch_var_unpack(N, K, bits, d, affine_groups,
+                                                   static_cast<const uint8_t*>(packed_codes),
+                                                   static_cast<const uint8_t*>(packed_affine), codes, A, B,
+                                                   static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+}
+
+int unisvq_var_gemv(int64_t N, int64_t K, int bits, int d, int64_t affine_groups, const void* packed_codes,
+                    const void* packed_affine, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
+                    void* stream) {
+    const unisvq_gemv_shared_problem p{N, K, affine_groups, packed_codes, packed_affine, x, y};
+    return unisvq_var_gemv_batched(&p, 1, bits, d, M, x_dtype, y_dtype, stream);
+}
+
+int unisvq_var_gemv_batched(const unisvq_gemv_shared_problem* problems, int count, int bits, int d, int64_t M,
+                            int x_dtype, int y_dtype, void* stream) {
+    if (!problems || count < 1) return UNISVQ_EINVAL;
+    if (count > UNISVQ_MAX_BATCH) return UNISVQ_EUNSUP;
+    unisvq::GemvProblem probs[UNISVQ_MAX_BATCH];
+    for (int i = 0; i < count; ++i) {
+        const unisvq_gemv_shared_problem& q = problems[i];
+        const int st = check_var(q.N, q.K, bits, d, q.affine_groups, q.packed_codes, q.packed_affine, M, q.x,
+                                 x_dtype, q.y, y_dtype);
+        if (st != UNISVQ_OK) return st;
+        probs[i] = unisvq::GemvProblem{static_cast<const uint8_t*>(q.packed_codes), q.x, q.y,
+                                       static_cast<int>(q.N), static_cast<int>(q.K), 0,
+                                       static_cast<const uint8_t*>(q.packed_affine), q.affine_groups == 1 ? 1 : 0};
+    }
+    if (M > 4) return UNISVQ_EUNSUP;
+    return unisvq::launch_gemv_var_batch(probs, count, M, x_dtype, y_dtype, bits, d,
+                                         static_cast<hipStream_t>(stream));
+}
+
+size_t unisvq_var_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype) {
+    if (!shape_ok(N, K) || M < 1 || M > (int64_t{1} << 31) - 1 || !x_dtype_ok(x_dtype)) return 0;
+    return unisvq::gemm_var_workspace_bytes(N, K, M, x_dtype);
+}
+
+int unisvq_var_gemm(int64_t N, int64_t K, int bits, int d, int64_t affine_groups, const void* packed_codes,
+                    const void* packed_affine, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
+                    void* workspace, size_t workspace_bytes, void* stream) {
+    const int st = check_var(N, K, bits, d, affine_groups, packed_codes, packed_affine, M, x, x_dtype, y, y_dtype);
+    if (st != UNISVQ_OK) return st;
+    if (x_dtype == UNISVQ_BF16 && K > 65536) return UNISVQ_EUNSUP;  // the bf16 pre-pass holds a row in registers
+    const size_t need = unisvq::gemm_var_workspace_bytes(N, K, M, x_dtype);
+    if (need) {
+        if (!workspace || workspace_bytes < need) return UNISVQ_EWORKSPACE;
+        if (!aligned(workspace, 16)) return UNISVQ_EALIGN;
+    }
+    return unisvq::launch_gemm_var(N, K, bits, d, static_cast<const uint8_t*>(packed_codes),
+                                   static_cast<const uint8_t*>(packed_affine), affine_groups == 1 ? 1 : 0, M, x,
+                                   x_dtype, y, y_dtype, workspace, static_cast<hipStream_t>(stream));
 }
 
 /* ---- nearest-codeword quantisation ---- */

@@ -85,6 +85,16 @@ constexpr int kCodePacketBytes = 1024;     // two groups
 constexpr int kAffineRecordBytes = 80;     // A columns (64 B) and B values (16 B) of two groups
 constexpr int kRecordBiasOff = 64;
 
+// Variant codes-only format: b-bit codes (b = 2, 3) and d-dimensional vectors
+// (d = 4, 8) with row-shared pairs (variant format block in unisvq.h).
+constexpr int var_group_bytes(int bits) { return bits == 3 ? 768 : 512; }  // one group of a row block
+constexpr int kVarHiOff = 1024;     // high fields inside a full packet
+constexpr int kVarHalfHiOff = 512;  // high fields inside a half packet
+constexpr int var_record_bytes(int d) { return d == 4 ? 160 : 576; }
+constexpr int kVarBiasOff8 = 256;                                 // lane-view B values, d = 8
+constexpr int var_row_view_off(int d) { return d == 4 ? 80 : 288; }  // row view of a record
+constexpr int var_row_view_group_bytes(int d) { return 2 * (d * d + d); }
+
 // Launchers (host side).  Each returns the hipError_t of the launch.
 hipError_t launch_pack(int64_t N, int64_t K, const uint8_t* codes, const uint16_t* A,
                        const uint16_t* B, uint8_t* packed, int32_t* bad, hipStream_t s);
@@ -96,6 +106,14 @@ hipError_t launch_pack_shared(int64_t N, int64_t K, int64_t affine_groups, const
 hipError_t launch_unpack_shared(int64_t N, int64_t K, int64_t affine_groups, const uint8_t* packed_codes,
                                 const uint8_t* packed_affine, uint8_t* codes, uint16_t* A, uint16_t* B,
                                 hipStream_t s);
+
+// Variant format pack / unpack (codes uint8 [N][K]; A, B fp16 bits [Ga][d][d], [Ga][d]).
+hipError_t launch_var_pack(int64_t N, int64_t K, int bits, int d, int64_t affine_groups, const uint8_t* codes,
+                           const uint16_t* A, const uint16_t* B, uint8_t* packed_codes, uint8_t* packed_affine,
+                           int32_t* bad, hipStream_t s);
+hipError_t launch_var_unpack(int64_t N, int64_t K, int bits, int d, int64_t affine_groups,
+                             const uint8_t* packed_codes, const uint8_t* packed_affine, uint8_t* codes,
+                             uint16_t* A, uint16_t* B, hipStream_t s);
 
 // Nearest-codeword quantisation (codes uint8 [N][K], 4-byte aligned).
 hipError_t launch_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, const uint16_t* B,
@@ -125,6 +143,10 @@ int launch_gemv_batch(const GemvProblem* probs, int count, int64_t M, int x_dtyp
                       hipStream_t s);
 int launch_gemv(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x,
                 int x_dtype, void* y, int y_dtype, hipStream_t s);
+// The same for variant weights (every problem with `bits`-bit codes and
+// d-dimensional vectors, codes-only with its shared affine block).
+int launch_gemv_var_batch(const GemvProblem* probs, int count, int64_t M, int x_dtype, int y_dtype, int bits, int d,
+                          hipStream_t s);
 // Prefill path.  Device workspace (16-byte aligned) of
 // gemm_workspace_bytes(N, K, M, x_dtype) bytes: for bf16 activations an fp16
 // copy of x plus one scale per token, and for products split along K the
@@ -136,6 +158,12 @@ int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const vo
 int launch_gemm_shared(int64_t N, int64_t K, const uint8_t* packed_codes, const uint8_t* affine,
                        int affine_one, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
                        void* workspace, hipStream_t s);
+// Variant weights: every M > 4 goes to the tiled kernel (K split for small
+// M), so the workspace differs from gemm_workspace_bytes.
+size_t gemm_var_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype);
+int launch_gemm_var(int64_t N, int64_t K, int bits, int d, const uint8_t* packed_codes, const uint8_t* affine,
+                    int affine_one, int64_t M, const void* x, int x_dtype, void* y, int y_dtype, void* workspace,
+                    hipStream_t s);
 // Small-batch kernel (M <= kSkinnyMaxM) on fp16 activations; inv_scale
 // (per token, may be null) multiplies the results.
 constexpr int64_t kSkinnyMaxM = 32;

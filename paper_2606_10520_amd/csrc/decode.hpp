@@ -141,3 +141,162 @@ __device__ inline void decode_vecs(const DecOps& d, _Float16* dst, int j) {
 
 }  // namespace
 }  // namespace unisvq
+
+namespace unisvq {
+namespace {
+
+// ---------------------------------------------------------------------------
+// Weight decode for the format variants: b-bit codes (b = 2, 3; Sec. 5.2.5)
+// and d-dimensional vectors (d = 4, 8; Sec. 5.2.3), codes-only with row-shared
+// pairs.  Codes are gathered from the quad exactly as above (for d = 8 code
+// word h of a slot holds component 4h + j, so byte n of the gathered word h
+// holds vector 4n + j, components 4h .. 4h+3); the high bits of 3-bit codes
+// are gathered the same way from the high field, whose layout puts the bit
+// of (word h, vector index 4n + j) at 8n + 4(j >> 1) + 2h + (j & 1).  A and B
+// come from the row view of the group's shared record.
+//   d = 4: one v_mfma_f32_4x4x4_16b per 4 vectors, as above;
+//   d = 8: per 4 vectors and half ah of the output components, two chained
+//          instructions (code components 0..3, then 4..7):
+//          D[a][v] = sum_b A[4 ah + a][b] q[v][b] + B[4 ah + a];
+//   b = 3: q = lo + 4 hi, so each instruction is followed by one with the high
+//          bits (the e2m1 converter with scale 8 gives 0 or 4) into the same
+//          accumulator.
+// All products are exact in fp32; the weight is rounded once to fp16.
+
+// Low and high fields of one slot of a variant packet.
+struct VarPiece {
+    uint4 c;  // low fields: .x/.y group 2p, .z/.w group 2p+1
+    uint2 h;  // high fields (b = 3): .x group 2p, .y group 2p+1
+};
+
+template <int BITS>
+__device__ inline void load_packet_var(__amdgpu_buffer_rsrc_t rc, uint32_t rowblk, int p, int gend, int lane,
+                                       VarPiece& pc) {
+    const bool full = 2 * p + 1 < gend;
+    const bool half = 2 * p + 1 == gend;
+    const uint32_t P =
+        full || half ? rowblk + static_cast<uint32_t>(p) * 2u * var_group_bytes(BITS) : kOutOfRange;
+    if (half) {
+        const uint2 c = ld64(rc, P + 8 * lane);
+        pc.c = uint4{c.x, c.y, 0u, 0u};
+        pc.h = uint2{BITS == 3 ? ld32(rc, P + kVarHalfHiOff + 4 * lane) : 0u, 0u};
+    } else {
+        pc.c = ld128(rc, P + 16 * lane);
+        pc.h = BITS == 3 ? ld64(rc, P + kVarHiOff + 8 * lane) : uint2{0u, 0u};
+    }
+}
+
+// A rows and B of one group, from the row view of its record.
+template <int D>
+struct VarAffine {
+    f16x4 arow[D / 4][D / 4];  // [ah][kb] = A[4 ah + j][4 kb .. 4 kb + 3]
+    f32x4 bvec[D / 4];         // [ah] = B[4 ah .. 4 ah + 3]
+};
+
+// Group gd of the product: record (one pair: 0; else gd / 2), its group gd % 2.
+template <int D>
+__device__ inline void load_var_affine(__amdgpu_buffer_rsrc_t ra, int affine_one, int gd, int j, VarAffine<D>& af) {
+    const uint32_t base = static_cast<uint32_t>(affine_one ? 0 : gd >> 1) * var_record_bytes(D) +
+                          var_row_view_off(D) + static_cast<uint32_t>(gd & 1) * var_row_view_group_bytes(D);
+#pragma unroll
+    for (int ah = 0; ah < D / 4; ++ah) {
+#pragma unroll
+        for (int kb = 0; kb < D / 4; ++kb)
+            af.arow[ah][kb] = __builtin_bit_cast(f16x4, ld64(ra, base + 2u * (D * (4 * ah + j) + 4 * kb)));
+        const uint2 bv = ld64(ra, base + 2u * D * D + 8u * ah);
+        af.bvec[ah] = f32x4{h2f(bv.x & 0xffffu), h2f(bv.x >> 16), h2f(bv.y & 0xffffu), h2f(bv.y >> 16)};
+    }
+}
+
+template <int BITS>
+struct VarDecOps {
+    uint32_t p01[2], p23[2];  // low bits: byte n of word h, nibbles of components (0, 1) / (2, 3) of the word's four
+    uint32_t h01[2], h23[2];  // high bits, same places (b = 3)
+};
+
+template <int BITS>
+__device__ inline void prepare_var(const VarPiece& pc, int j, int jj, VarDecOps<BITS>& d) {
+    const uint32_t cl = jj ? pc.c.z : pc.c.x, ch = jj ? pc.c.w : pc.c.y;
+    const uint32_t cw[2][4] = {{quad_lane<0>(cl), quad_lane<1>(cl), quad_lane<2>(cl), quad_lane<3>(cl)},
+                               {quad_lane<0>(ch), quad_lane<1>(ch), quad_lane<2>(ch), quad_lane<3>(ch)}};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        uint32_t m[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) m[b] = (cw[h][b] >> (2 * j)) & 0x03030303u;
+        d.p01[h] = m[0] | (m[1] << 4);
+        d.p23[h] = m[2] | (m[3] << 4);
+    }
+    if constexpr (BITS == 3) {
+        const uint32_t H = jj ? pc.h.y : pc.h.x;
+        const uint32_t hw[4] = {quad_lane<0>(H), quad_lane<1>(H), quad_lane<2>(H), quad_lane<3>(H)};
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int sh = 4 * (j >> 1) + (j & 1) + 2 * h;
+            uint32_t m[4];
+#pragma unroll
+            for (int b = 0; b < 4; ++b) m[b] = (hw[b] >> sh) & 0x01010101u;
+            d.h01[h] = m[0] | (m[1] << 4);
+            d.h23[h] = m[2] | (m[3] << 4);
+        }
+    }
+}
+
+// Codes of word h, byte n as an operand (low part, or the high part times 4).
+template <int H, int NB>
+__device__ inline f16x4 var_codes(const uint32_t (&p01)[2], const uint32_t (&p23)[2], float scale) {
+    const f16x2 lo = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(p01[H], scale, NB);
+    const f16x2 hi = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(p23[H], scale, NB);
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3);
+}
+
+__device__ inline void store_w4(const f32x4& w, _Float16* dst) {
+    f16x4 o;
+#pragma unroll
+    for (int a = 0; a < 4; ++a) o[a] = static_cast<_Float16>(w[a]);
+    *reinterpret_cast<f16x4*>(dst) = o;
+}
+
+// d = 4: vectors 4N .. 4N+3; lane (beta, j) stores vector 4N+j at dst + 16N + 4j.
+template <int BITS, int N>
+__device__ inline void decode_var4(const VarDecOps<BITS>& d, const VarAffine<4>& af, _Float16* dst, int j) {
+    f32x4 w = __builtin_amdgcn_mfma_f32_4x4x4f16(af.arow[0][0], var_codes<N / 4, N % 4>(d.p01, d.p23, 2.0f),
+                                                 af.bvec[0], 0, 0, 0);
+    if constexpr (BITS == 3)
+        w = __builtin_amdgcn_mfma_f32_4x4x4f16(af.arow[0][0], var_codes<N / 4, N % 4>(d.h01, d.h23, 8.0f), w, 0, 0,
+                                               0);
+    store_w4(w, dst + 16 * N + 4 * j);
+}
+
+// d = 8: vectors 4n .. 4n+3, output components 4 AH .. 4 AH + 3; lane
+// (beta, j) stores them at dst + 8 (4n + j) + 4 AH.
+template <int BITS, int NV, int AH>
+__device__ inline void decode_var8(const VarDecOps<BITS>& d, const VarAffine<8>& af, _Float16* dst, int j) {
+    f32x4 w = __builtin_amdgcn_mfma_f32_4x4x4f16(af.arow[AH][0], var_codes<0, NV>(d.p01, d.p23, 2.0f), af.bvec[AH],
+                                                 0, 0, 0);
+    w = __builtin_amdgcn_mfma_f32_4x4x4f16(af.arow[AH][1], var_codes<1, NV>(d.p01, d.p23, 2.0f), w, 0, 0, 0);
+    if constexpr (BITS == 3) {
+        w = __builtin_amdgcn_mfma_f32_4x4x4f16(af.arow[AH][0], var_codes<0, NV>(d.h01, d.h23, 8.0f), w, 0, 0, 0);
+        w = __builtin_amdgcn_mfma_f32_4x4x4f16(af.arow[AH][1], var_codes<1, NV>(d.h01, d.h23, 8.0f), w, 0, 0, 0);
+    }
+    store_w4(w, dst + 8 * (4 * NV + j) + 4 * AH);
+}
+
+// Half S (0: first half of the vectors, 1: second) of one row block's group.
+template <int BITS, int D, int S>
+__device__ inline void decode_var_half(const VarDecOps<BITS>& d, const VarAffine<D>& af, _Float16* dst, int j) {
+    if constexpr (D == 4) {
+        decode_var4<BITS, 4 * S + 0>(d, af, dst, j);
+        decode_var4<BITS, 4 * S + 1>(d, af, dst, j);
+        decode_var4<BITS, 4 * S + 2>(d, af, dst, j);
+        decode_var4<BITS, 4 * S + 3>(d, af, dst, j);
+    } else {
+        decode_var8<BITS, 2 * S, 0>(d, af, dst, j);
+        decode_var8<BITS, 2 * S, 1>(d, af, dst, j);
+        decode_var8<BITS, 2 * S + 1, 0>(d, af, dst, j);
+        decode_var8<BITS, 2 * S + 1, 1>(d, af, dst, j);
+    }
+}
+
+}  // namespace
+}  // namespace unisvq

@@ -23,6 +23,8 @@
 // carries the same single rounding of w_hat to fp16 (2^-11 relative) as the
 // fp16 path, where bf16 operands would need w_hat split into two bf16 terms
 // and twice the matrix-core work.
+#include <type_traits>
+
 #include "common.hpp"
 #include "decode.hpp"
 
@@ -81,6 +83,23 @@ __device__ inline void slice(__amdgpu_buffer_rsrc_t rx, uint32_t xnext, uint32_t
     mma<MI>(xq[S & 3], wb[S & 1], acc);
 }
 
+// The same for a format variant: the group's A rows and B (af) were loaded
+// at the start of the group step.
+template <int MI, int S, int BITS, int D>
+__device__ inline void slice_var(__amdgpu_buffer_rsrc_t rx, uint32_t xnext, uint32_t row_step, f16x8 (&xq)[4][MI],
+                                 f16x8 (&wb)[2][kNI], const _Float16* wsrc, const VarPiece (&src)[2], int jj,
+                                 VarDecOps<BITS> (&ops)[2], const VarAffine<D>& af, int j,
+                                 _Float16* const (&wdst)[2], f32x4 (&acc)[MI][kNI]) {
+    load_x<MI>(rx, xnext, row_step, xq[(S + 2) & 3]);
+    if (S < 3) read_w(wsrc + 32 * (S + 1), wb[(S + 1) & 1]);
+    {
+        constexpr int r = S >> 1;
+        if ((S & 1) == 0) prepare_var<BITS>(src[r], j, jj, ops[r]);
+        decode_var_half<BITS, D, S & 1>(ops[r], af, wdst[r], j);
+    }
+    mma<MI>(xq[S & 3], wb[S & 1], acc);
+}
+
 // Everything a group step needs besides its pieces.
 template <int MI>
 struct GemmState {
@@ -89,6 +108,8 @@ struct GemmState {
     const _Float16* wlane;
     _Float16* wrow[2];
     int gend, j;  // end of this workgroup's group range
+    __amdgpu_buffer_rsrc_t ra;  // shared affine block (format variants)
+    int affine_one;
 };
 
 // Group g: products of buffer g & 1 (slices 0..3) while group g+1 is decoded
@@ -112,9 +133,32 @@ __device__ inline void group_step(const GemmState<MI>& st, int g, const Piece (&
     __syncthreads();
 }
 
+// group_step for a format variant.
+template <int MI, int BITS, int D>
+__device__ inline void group_step_var(const GemmState<MI>& st, int g, const VarPiece (&src)[2], int jj,
+                                      f16x8 (&xq)[4][MI], f32x4 (&acc)[MI][kNI]) {
+    const _Float16* wsrc = st.wlane + (g & 1) * kWBuf;
+    _Float16* const wdst[2] = {st.wrow[0] + ((g + 1) & 1) * kWBuf, st.wrow[1] + ((g + 1) & 1) * kWBuf};
+    const bool decode_next = g + 1 < st.gend;
+    VarAffine<D> af;
+    load_var_affine<D>(st.ra, st.affine_one, g + 1, st.j, af);
+    VarDecOps<BITS> ops[2];
+    f16x8 wb[2][kNI];
+    read_w(wsrc, wb[0]);
+    const uint32_t xoff = st.xbase + static_cast<uint32_t>(g) * 256u;
+    const uint32_t xn = decode_next ? xoff + 256u : kOutOfRange;
+    slice_var<MI, 0, BITS, D>(st.rx, xoff + 128u, st.row_step, xq, wb, wsrc, src, jj, ops, af, st.j, wdst, acc);
+    slice_var<MI, 1, BITS, D>(st.rx, xoff + 192u, st.row_step, xq, wb, wsrc, src, jj, ops, af, st.j, wdst, acc);
+    slice_var<MI, 2, BITS, D>(st.rx, xn, st.row_step, xq, wb, wsrc, src, jj, ops, af, st.j, wdst, acc);
+    slice_var<MI, 3, BITS, D>(st.rx, xn + 64u, st.row_step, xq, wb, wsrc, src, jj, ops, af, st.j, wdst, acc);
+    __syncthreads();
+}
+
 // SHARED: codes-only weights, A and B from the shared affine block (one pair
 // for the matrix when affine_one, else one per group); the decode is the same.
-template <int MI, bool SHARED>
+// BITS, D: code width and vector dimension; anything but 2, 4 is a format
+// variant (always SHARED, variant layout and records).
+template <int MI, bool SHARED, int BITS = 2, int D = 4>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restrict__ packed,
                                                         const uint8_t* __restrict__ affine, int affine_one,
                                                         const _Float16* __restrict__ x,
@@ -123,6 +167,9 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
                                                         int splits, int gps, float* __restrict__ partial) {
     __shared__ __attribute__((aligned(16))) _Float16 wsh[2 * kWBuf];
     constexpr int BM = kWaves * 16 * MI;
+    constexpr bool kVar = BITS != 2 || D != 4;
+    static_assert(!kVar || SHARED, "format variants keep their pairs in a shared block");
+    typedef typename std::conditional<kVar, VarPiece, Piece>::type PieceT;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
@@ -144,13 +191,17 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     const int gend = min(groups, gb + gps);
 
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(M) * K * 2u);
-    constexpr uint32_t kBlockBytes = SHARED ? kCodeGroupBlockBytes : kGroupBlockBytes;
+    constexpr uint32_t kBlockBytes =
+        kVar ? var_group_bytes(BITS) : (SHARED ? kCodeGroupBlockBytes : kGroupBlockBytes);
+    constexpr uint32_t kRecBytes = kVar ? var_record_bytes(D) : kAffineRecordBytes;
     const __amdgpu_buffer_rsrc_t rw =
         make_rsrc(packed, static_cast<uint32_t>(N / kRowBlock) * groups * kBlockBytes);
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(
-        affine, SHARED ? static_cast<uint32_t>(affine_one ? 1 : (groups + 1) / 2) * kAffineRecordBytes : 0u);
-    auto load = [&](uint32_t rowblk, int p, Piece& pc) {
-        if constexpr (SHARED)
+        affine, SHARED ? static_cast<uint32_t>(affine_one ? 1 : (groups + 1) / 2) * kRecBytes : 0u);
+    auto load = [&](uint32_t rowblk, int p, PieceT& pc) {
+        if constexpr (kVar)
+            load_packet_var<BITS>(rw, rowblk, p, gend, lane, pc);
+        else if constexpr (SHARED)
             load_packet_shared(rw, ra, rowblk, p, gend, affine_one, lane, pc);
         else
             load_packet(rw, rowblk, p, gend, lane, pc);
@@ -162,6 +213,10 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     const int beta = lane >> 2;
     st.j = lane & 3;
     st.gend = gend;
+    if constexpr (kVar) {
+        st.ra = ra;
+        st.affine_one = affine_one;
+    }
     uint32_t rowblk[2];
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
@@ -187,14 +242,24 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
 
     // Packets two groups ahead of their decode: pa = packet q (groups 2q,
     // 2q+1), pb = packet q+1, pc = packet q+2 (loaded during group 2q+1).
-    Piece pa[2], pb[2], pc[2];
+    PieceT pa[2], pb[2], pc[2];
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
         load(rowblk[r], gb >> 1, pa[r]);
         load(rowblk[r], (gb >> 1) + 1, pb[r]);
     }
     // Prologue: group gb into buffer gb & 1 (= 0).
-    {
+    if constexpr (kVar) {
+        VarAffine<D> af;
+        load_var_affine<D>(ra, affine_one, gb, st.j, af);
+        VarDecOps<BITS> ops;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            prepare_var<BITS>(pa[r], st.j, 0, ops);
+            decode_var_half<BITS, D, 0>(ops, af, st.wrow[r], st.j);
+            decode_var_half<BITS, D, 1>(ops, af, st.wrow[r], st.j);
+        }
+    } else {
         DecOps ops;
 #pragma unroll
         for (int r = 0; r < 2; ++r) {
@@ -215,19 +280,35 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     __syncthreads();
 
     int g = gb;
-    for (; g + 1 < gend; g += 2) {
-        const int q = g >> 1;
-        group_step<MI>(st, g, pa, 1, xq, acc);  // decodes group 2q+1 (packet q)
+    if constexpr (kVar) {
+        for (; g + 1 < gend; g += 2) {
+            const int q = g >> 1;
+            group_step_var<MI, BITS, D>(st, g, pa, 1, xq, acc);
 #pragma unroll
-        for (int r = 0; r < 2; ++r) load(rowblk[r], q + 2, pc[r]);
-        group_step<MI>(st, g + 1, pb, 0, xq, acc);  // decodes group 2q+2 (packet q+1)
+            for (int r = 0; r < 2; ++r) load(rowblk[r], q + 2, pc[r]);
+            group_step_var<MI, BITS, D>(st, g + 1, pb, 0, xq, acc);
 #pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            pa[r] = pb[r];
-            pb[r] = pc[r];
+            for (int r = 0; r < 2; ++r) {
+                pa[r] = pb[r];
+                pb[r] = pc[r];
+            }
         }
+        if (g < gend) group_step_var<MI, BITS, D>(st, g, pa, 1, xq, acc);
+    } else {
+        for (; g + 1 < gend; g += 2) {
+            const int q = g >> 1;
+            group_step<MI>(st, g, pa, 1, xq, acc);  // decodes group 2q+1 (packet q)
+#pragma unroll
+            for (int r = 0; r < 2; ++r) load(rowblk[r], q + 2, pc[r]);
+            group_step<MI>(st, g + 1, pb, 0, xq, acc);  // decodes group 2q+2 (packet q+1)
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                pa[r] = pb[r];
+                pb[r] = pc[r];
+            }
+        }
+        if (g < gend) group_step<MI>(st, g, pa, 1, xq, acc);  // last group (nothing left to decode)
     }
-    if (g < gend) group_step<MI>(st, g, pa, 1, xq, acc);  // last group (nothing left to decode)
 
     // Epilogue.  D lane layout: output row 16 n + lane % 16, tokens
     // 16 i + 4 (lane / 16) + e.  With a K split the fp32 partial sums go to
@@ -373,13 +454,13 @@ size_t partial_bytes(int64_t N, int64_t K, int64_t M) {
     return p.splits > 1 ? static_cast<size_t>(p.splits) * M * N * 4 : 0;
 }
 
-template <int MI, bool SHARED>
+template <int MI, bool SHARED, int BITS = 2, int D = 4>
 hipError_t launch_tiles(const GemmPlan& p, int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine,
                         int affine_one, int64_t M, const _Float16* x, const float* inv_scale, void* y,
                         int y_dtype, float* partial, hipStream_t s) {
     if (p.splits > 1 && partial == nullptr) return hipErrorInvalidValue;  // never launch without the partials
     const unsigned blocks = static_cast<unsigned>(p.m_tiles) * p.n_tiles * p.splits;
-    hipLaunchKernelGGL((gemm_kernel<MI, SHARED>), dim3(blocks), dim3(kThreads), 0, s, packed, affine, affine_one,
+    hipLaunchKernelGGL((gemm_kernel<MI, SHARED, BITS, D>), dim3(blocks), dim3(kThreads), 0, s, packed, affine, affine_one,
                        x, inv_scale, y,
                        static_cast<int>(N), static_cast<int>(K), static_cast<int>(M), y_dtype, p.m_tiles,
                        p.n_tiles, p.splits, p.gps, p.splits > 1 ? partial : nullptr);
@@ -400,10 +481,32 @@ size_t gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype) {
     return b + partial_bytes(N, K, M);
 }
 
+size_t gemm_var_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype) {
+    size_t b = 0;
+    if (x_dtype == UNISVQ_BF16) b += align256(static_cast<size_t>(M) * K * 2) + align256(static_cast<size_t>(M) * 4);
+    const GemmPlan p = plan_gemm(N, K, M);
+    return b + (p.splits > 1 ? static_cast<size_t>(p.splits) * M * N * 4 : 0);
+}
+
 namespace {
 
+// Tiles of one (sliced) product for a format variant.
+template <int BITS, int D>
+hipError_t launch_tiles_var(const GemmPlan& p, int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine,
+                            int affine_one, int64_t M, const _Float16* x, const float* inv_scale, void* y,
+                            int y_dtype, float* partial, hipStream_t s) {
+    return p.mi == 2 ? launch_tiles<2, true, BITS, D>(p, N, K, packed, affine, affine_one, M, x, inv_scale, y,
+                                                      y_dtype, partial, s)
+                     : launch_tiles<1, true, BITS, D>(p, N, K, packed, affine, affine_one, M, x, inv_scale, y,
+                                                      y_dtype, partial, s);
+}
+
+// bits, d: 2, 4 for the main formats; a format variant otherwise (every M
+// goes to the tiled kernel).
 int gemm_common(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine, int affine_one, int64_t M,
-                const void* x, int x_dtype, void* y, int y_dtype, void* workspace, hipStream_t s) {
+                const void* x, int x_dtype, void* y, int y_dtype, void* workspace, hipStream_t s, int bits = 2,
+                int d = 4) {
+    const bool var = bits != 2 || d != 4;
     const _Float16* xh = static_cast<const _Float16*>(x);
     const float* inv = nullptr;
     uint8_t* ws = static_cast<uint8_t*>(workspace);
@@ -417,7 +520,7 @@ int gemm_common(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affi
         xh = wxh;
         inv = winv;
     }
-    if (M <= kSkinnyMaxM)
+    if (!var && M <= kSkinnyMaxM)
         return launch_skinny(N, K, packed, affine, affine_one, M, xh, inv, y, y_dtype, s) == hipSuccess
                    ? UNISVQ_OK
                    : UNISVQ_EHIP;
@@ -439,7 +542,15 @@ int gemm_common(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affi
             p.gps = static_cast<int>(K / kGroup);
         }
         hipError_t e;
-        if (affine)
+        if (var && bits == 3 && d == 4)
+            e = launch_tiles_var<3, 4>(p, N, K, packed, affine, affine_one, mc, xs, is, ys, y_dtype, partial, s);
+        else if (var && bits == 2 && d == 8)
+            e = launch_tiles_var<2, 8>(p, N, K, packed, affine, affine_one, mc, xs, is, ys, y_dtype, partial, s);
+        else if (var && bits == 3 && d == 8)
+            e = launch_tiles_var<3, 8>(p, N, K, packed, affine, affine_one, mc, xs, is, ys, y_dtype, partial, s);
+        else if (var)
+            return UNISVQ_EUNSUP;
+        else if (affine)
             e = p.mi == 2 ? launch_tiles<2, true>(p, N, K, packed, affine, affine_one, mc, xs, is, ys, y_dtype, partial, s)
                           : launch_tiles<1, true>(p, N, K, packed, affine, affine_one, mc, xs, is, ys, y_dtype, partial, s);
         else
@@ -461,6 +572,12 @@ int launch_gemm_shared(int64_t N, int64_t K, const uint8_t* packed_codes, const 
                        int affine_one, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
                        void* workspace, hipStream_t s) {
     return gemm_common(N, K, packed_codes, affine, affine_one, M, x, x_dtype, y, y_dtype, workspace, s);
+}
+
+int launch_gemm_var(int64_t N, int64_t K, int bits, int d, const uint8_t* packed_codes, const uint8_t* affine,
+                    int affine_one, int64_t M, const void* x, int x_dtype, void* y, int y_dtype, void* workspace,
+                    hipStream_t s) {
+    return gemm_common(N, K, packed_codes, affine, affine_one, M, x, x_dtype, y, y_dtype, workspace, s, bits, d);
 }
 
 }  // namespace unisvq

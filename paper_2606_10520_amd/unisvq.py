@@ -24,7 +24,11 @@ EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "uni
            "unisvq_unpack", "unisvq_gemv", "unisvq_gemv_batched", "unisvq_gemm_workspace_bytes",
            "unisvq_gemm", "unisvq_codes_bytes", "unisvq_shared_affine_bytes", "unisvq_pack_shared",
            "unisvq_unpack_shared", "unisvq_gemv_shared", "unisvq_gemv_shared_batched", "unisvq_gemm_shared",
-           "unisvq_quantize", "unisvq_rht")
+           "unisvq_quantize", "unisvq_rht", "unisvq_var_codes_bytes", "unisvq_var_affine_bytes",
+           "unisvq_var_pack", "unisvq_var_unpack", "unisvq_var_gemv", "unisvq_var_gemv_batched",
+           "unisvq_var_gemm_workspace_bytes", "unisvq_var_gemm")
+# format variants: (bits, d) pairs served by the unisvq_var_* entry points
+VARIANTS = ((3, 4), (2, 8), (3, 8))
 MAX_BATCH = 8
 
 
@@ -100,6 +104,22 @@ def load():
     lib.unisvq_quantize.restype = i32
     lib.unisvq_rht.argtypes = [i64, i64, p, i32, p, i32, p, i32, p]
     lib.unisvq_rht.restype = i32
+    lib.unisvq_var_codes_bytes.argtypes = [i64, i64, i32, i32]
+    lib.unisvq_var_codes_bytes.restype = sz
+    lib.unisvq_var_affine_bytes.argtypes = [i64, i64, i32, i32]
+    lib.unisvq_var_affine_bytes.restype = sz
+    lib.unisvq_var_pack.argtypes = [i64, i64, i32, i32, i64, p, p, p, p, p, p, p]
+    lib.unisvq_var_pack.restype = i32
+    lib.unisvq_var_unpack.argtypes = [i64, i64, i32, i32, i64, p, p, p, p, p, p]
+    lib.unisvq_var_unpack.restype = i32
+    lib.unisvq_var_gemv.argtypes = [i64, i64, i32, i32, i64, p, p, i64, p, i32, p, i32, p]
+    lib.unisvq_var_gemv.restype = i32
+    lib.unisvq_var_gemv_batched.argtypes = [ctypes.POINTER(GemvSharedProblem), i32, i32, i32, i64, i32, i32, p]
+    lib.unisvq_var_gemv_batched.restype = i32
+    lib.unisvq_var_gemm_workspace_bytes.argtypes = [i64, i64, i64, i32]
+    lib.unisvq_var_gemm_workspace_bytes.restype = sz
+    lib.unisvq_var_gemm.argtypes = [i64, i64, i32, i32, i64, p, p, i64, p, i32, p, i32, p, sz, p]
+    lib.unisvq_var_gemm.restype = i32
     _lib = lib
     return lib
 
@@ -385,3 +405,111 @@ def rht(x, signs, mode: str, out=None, out_dtype=None, stream=None):
                                            0 if mode == "in" else 1, _ptr(out), _dtype_code(out.dtype),
                                            _stream(stream)))
     return out
+
+
+# ------------------------------------------------ format variants (b-bit codes, d-dim vectors)
+
+def var_codes_bytes(N: int, K: int, bits: int, d: int) -> int:
+    return load().unisvq_var_codes_bytes(N, K, bits, d)
+
+
+def var_affine_bytes(K: int, affine_groups: int, bits: int, d: int) -> int:
+    return load().unisvq_var_affine_bytes(K, affine_groups, bits, d)
+
+
+def var_pack(codes, A, B, bits: int, d: int, out_codes=None, out_affine=None, bad_codes=None, stream=None):
+    """codes uint8 [N][K] (0..2^bits-1); A fp16 [Ga][d][d]; B fp16 [Ga][d]
+    -> (packed variant codes, packed shared affine block), uint8 device tensors."""
+    torch = _torch()
+    _need_cuda(codes, A, B, out_codes, out_affine, bad_codes)
+    N, K = codes.shape
+    Ga = A.shape[0]
+    if out_codes is None:
+        out_codes = torch.empty(max(var_codes_bytes(N, K, bits, d), 16), dtype=torch.uint8, device=codes.device)
+    if out_affine is None:
+        out_affine = torch.empty(max(var_affine_bytes(K, Ga, bits, d), 16), dtype=torch.uint8, device=codes.device)
+    _check("unisvq_var_pack", load().unisvq_var_pack(
+        N, K, bits, d, Ga, _ptr(codes.contiguous()), _ptr(A.contiguous()), _ptr(B.contiguous()), _ptr(out_codes),
+        _ptr(out_affine), _ptr(bad_codes), _stream(stream)))
+    return out_codes, out_affine
+
+
+def var_unpack(packed_codes, packed_affine, N: int, K: int, bits: int, d: int, affine_groups: int, stream=None):
+    """Inverse of var_pack: (codes uint8 [N][K], A fp16 [Ga][d][d], B fp16 [Ga][d])."""
+    torch = _torch()
+    _need_cuda(packed_codes, packed_affine)
+    dev = packed_codes.device
+    codes = torch.empty((N, K), dtype=torch.uint8, device=dev)
+    A = torch.empty((affine_groups, d, d), dtype=torch.float16, device=dev)
+    B = torch.empty((affine_groups, d), dtype=torch.float16, device=dev)
+    _check("unisvq_var_unpack", load().unisvq_var_unpack(
+        N, K, bits, d, affine_groups, _ptr(packed_codes), _ptr(packed_affine), _ptr(codes), _ptr(A), _ptr(B),
+        _stream(stream)))
+    return codes, A, B
+
+
+def _var_product(fn_name, N, K, bits, d, affine_groups, packed_codes, packed_affine, x, out, out_dtype, stream,
+                 extra=()):
+    torch = _torch()
+    _need_cuda(packed_codes, packed_affine, x, out)
+    x2 = x if x.dim() == 2 else x.reshape(-1, K)
+    if not x2.is_contiguous():
+        raise ValueError("x must be contiguous")
+    M = x2.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=out_dtype or x.dtype, device=x.device)
+    fn = getattr(load(), fn_name)
+    _check(fn_name, fn(N, K, bits, d, affine_groups, _ptr(packed_codes), _ptr(packed_affine), M, _ptr(x2),
+                       _dtype_code(x2.dtype), _ptr(out), _dtype_code(out.dtype), *extra, _stream(stream)))
+    return out
+
+
+def var_gemv(packed_codes, packed_affine, N: int, K: int, bits: int, d: int, affine_groups: int, x, out=None,
+             out_dtype=None, stream=None):
+    """Decode-phase product with variant weights (M <= 4)."""
+    return _var_product("unisvq_var_gemv", N, K, bits, d, affine_groups, packed_codes, packed_affine, x, out,
+                        out_dtype, stream)
+
+
+def var_gemv_batched(problems, bits: int, d: int, out_dtype=None, stream=None):
+    """problems: list of dicts with packed_codes, packed_affine, N, K, affine_groups, x (same M and dtype), and
+    optionally out; one launch.  Returns the list of outputs."""
+    torch = _torch()
+    if not 1 <= len(problems) <= MAX_BATCH:
+        raise ValueError(f"1..{MAX_BATCH} problems per launch")
+    arr = (GemvSharedProblem * len(problems))()
+    outs = []
+    M = None
+    for i, pr in enumerate(problems):
+        x = pr["x"]
+        _need_cuda(pr["packed_codes"], pr["packed_affine"], x)
+        if M is None:
+            M, xdt = x.shape[0], x.dtype
+        out = pr.get("out")
+        if out is None:
+            out = torch.empty((x.shape[0], pr["N"]), dtype=out_dtype or x.dtype, device=x.device)
+        outs.append(out)
+        arr[i] = GemvSharedProblem(pr["N"], pr["K"], pr["affine_groups"], _ptr(pr["packed_codes"]),
+                                   _ptr(pr["packed_affine"]), _ptr(x), _ptr(out))
+    _check("unisvq_var_gemv_batched", load().unisvq_var_gemv_batched(
+        arr, len(problems), bits, d, M, _dtype_code(xdt), _dtype_code(outs[0].dtype), _stream(stream)))
+    return outs
+
+
+def var_gemm_workspace_bytes(N: int, K: int, M: int, x_dtype=None) -> int:
+    """Workspace bytes unisvq_var_gemm needs (x_dtype: torch dtype, default bf16)."""
+    code = BF16 if x_dtype is None else _dtype_code(x_dtype)
+    return load().unisvq_var_gemm_workspace_bytes(N, K, M, code)
+
+
+def var_gemm(packed_codes, packed_affine, N: int, K: int, bits: int, d: int, affine_groups: int, x, out=None,
+             out_dtype=None, workspace=None, stream=None):
+    """Prefill product with variant weights (any M)."""
+    torch = _torch()
+    M = x.numel() // K
+    need = var_gemm_workspace_bytes(N, K, M, x.dtype)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    wb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    return _var_product("unisvq_var_gemm", N, K, bits, d, affine_groups, packed_codes, packed_affine, x, out,
+                        out_dtype, stream, extra=(_ptr(workspace), wb))

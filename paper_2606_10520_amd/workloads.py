@@ -91,6 +91,18 @@ def gen_shared_weights(N: int, K: int, affine_groups: int, seed: int, a_std: flo
     return Q, A, B
 
 
+def gen_var_weights(N: int, K: int, bits: int, d: int, affine_groups: int, seed: int, a_std: float = 0.02,
+                    b_std: float = 0.01):
+    """Format variants: codes uniform on {0..2^bits-1} and row-shared pairs A [Ga][d][d], B [Ga][d]."""
+    if K % GROUP or affine_groups not in (1, K // GROUP):
+        raise ValueError("K must be a multiple of 128 and affine_groups 1 or K/128")
+    rng = np.random.default_rng(seed)
+    Q = rng.integers(0, 1 << bits, size=(N, K), dtype=np.uint8)
+    A = (rng.standard_normal((affine_groups, d, d)) * a_std).astype(np.float16)
+    B = (rng.standard_normal((affine_groups, d)) * b_std).astype(np.float16)
+    return Q, A, B
+
+
 def gen_activations(M: int, K: int, seed: int, dtype: str = "f16", outliers: bool = False):
     """Activations X [M][K]; returns raw uint16 bits of fp16 or bf16 values."""
     rng = np.random.default_rng(seed)

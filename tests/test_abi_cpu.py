@@ -247,3 +247,86 @@ def test_rht_validation():
     # orders without a supported construction, or beyond the LDS row
     assert lib.unisvq_rht(100, 1, GOOD, u.F16, GOOD, 0, GOOD + 0x100000, u.F16, None) == EUNSUP
     assert lib.unisvq_rht(65536, 1, GOOD, u.F16, GOOD, 0, GOOD + 0x100000, u.F16, None) == EUNSUP
+
+
+# ---- format variants (b-bit codes, d-dimensional vectors) ----
+
+@pytest.mark.parametrize("bits,d,N,K,expect", [
+    (3, 4, 16, 128, 768), (2, 8, 16, 128, 512), (3, 8, 4096, 4096, 4096 * 4096 * 3 // 8),
+    (2, 4, 16, 128, 0), (4, 4, 16, 128, 0), (3, 6, 16, 128, 0), (3, 8, 15, 128, 0), (3, 8, 16, 100, 0)])
+def test_var_codes_bytes(bits, d, N, K, expect):
+    assert u.load().unisvq_var_codes_bytes(N, K, bits, d) == expect
+
+
+@pytest.mark.parametrize("bits,d,K,ga,expect", [
+    (3, 4, 128, 1, 160), (3, 4, 384, 3, 320), (2, 8, 4096, 1, 576), (2, 8, 11008, 86, 43 * 576),
+    (3, 8, 4096, 32, 16 * 576), (2, 4, 4096, 1, 0), (3, 8, 4096, 2, 0), (3, 8, 100, 1, 0)])
+def test_var_affine_bytes(bits, d, K, ga, expect):
+    assert u.load().unisvq_var_affine_bytes(K, ga, bits, d) == expect
+
+
+def test_var_pack_validation():
+    lib = u.load()
+    assert lib.unisvq_var_pack(16, 256, 3, 8, 1, None, GOOD, GOOD, GOOD, GOOD, None, None) == EINVAL
+    assert lib.unisvq_var_pack(16, 256, 2, 4, 1, GOOD, GOOD, GOOD, GOOD, GOOD, None, None) == EUNSUP
+    assert lib.unisvq_var_pack(16, 256, 4, 8, 1, GOOD, GOOD, GOOD, GOOD, GOOD, None, None) == EUNSUP
+    assert lib.unisvq_var_pack(16, 256, 3, 8, 3, GOOD, GOOD, GOOD, GOOD, GOOD, None, None) == EINVAL
+    assert lib.unisvq_var_pack(17, 256, 3, 8, 1, GOOD, GOOD, GOOD, GOOD, GOOD, None, None) == ESHAPE
+    assert lib.unisvq_var_pack(16, 256, 3, 8, 2, GOOD, GOOD, GOOD, GOOD + 8, GOOD, None, None) == EALIGN
+    assert lib.unisvq_var_pack(16, 256, 3, 8, 2, GOOD, GOOD, GOOD, GOOD, GOOD + 4, None, None) == EALIGN
+    assert lib.unisvq_var_unpack(16, 256, 3, 4, 5, GOOD, GOOD, GOOD, GOOD, GOOD, None) == EINVAL
+    assert lib.unisvq_var_unpack(16, 250, 3, 4, 1, GOOD, GOOD, GOOD, GOOD, GOOD, None) == ESHAPE
+    assert lib.unisvq_var_unpack(16, 256, 2, 4, 1, GOOD, GOOD, GOOD, GOOD, GOOD, None) == EUNSUP
+    assert lib.unisvq_var_unpack(16, 256, 3, 4, 1, GOOD, GOOD + 2, GOOD, GOOD, GOOD, None) == EALIGN
+
+
+@pytest.mark.parametrize("fn", ["gemv", "gemm"])
+def test_var_product_validation(fn):
+    lib = u.load()
+
+    def call(N=64, K=256, bits=3, d=8, ga=1, pc=GOOD, pa=GOOD, M=1, x=GOOD, xt=u.F16, y=GOOD, yt=u.F16,
+             ws_bytes=0):
+        if fn == "gemv":
+            return lib.unisvq_var_gemv(N, K, bits, d, ga, pc, pa, M, x, xt, y, yt, None)
+        return lib.unisvq_var_gemm(N, K, bits, d, ga, pc, pa, M, x, xt, y, yt, None, ws_bytes, None)
+
+    assert call(pc=None) == EINVAL
+    assert call(pa=None) == EINVAL
+    assert call(M=0) == EINVAL
+    assert call(ga=3) == EINVAL
+    assert call(xt=u.F32) == EINVAL
+    assert call(bits=2, d=4) == EUNSUP
+    assert call(bits=1) == EUNSUP
+    assert call(d=16) == EUNSUP
+    assert call(N=60) == ESHAPE
+    assert call(K=200) == ESHAPE
+    assert call(pc=GOOD + 8) == EALIGN
+    assert call(pa=GOOD + 8) == EALIGN
+    assert call(y=GOOD + 1) == EALIGN
+    if fn == "gemv":
+        assert call(M=5) == EUNSUP
+    else:
+        assert call(xt=u.BF16, M=64) == EWS
+        assert call(xt=u.BF16, K=65664, M=64) == EUNSUP
+        # every M goes to the tiled kernel: a small product splits K and needs partials
+        assert call(M=8, K=4096) == EWS
+
+
+def test_var_batched_validation():
+    lib = u.load()
+    arr = (u.GemvSharedProblem * 2)()
+    arr[0] = u.GemvSharedProblem(64, 256, 1, GOOD, GOOD, GOOD, GOOD)
+    arr[1] = u.GemvSharedProblem(64, 256, 5, GOOD, GOOD, GOOD, GOOD)
+    assert lib.unisvq_var_gemv_batched(arr, 2, 3, 8, 1, u.F16, u.F16, None) == EINVAL
+    assert lib.unisvq_var_gemv_batched(arr, 1, 2, 4, 1, u.F16, u.F16, None) == EUNSUP
+    assert lib.unisvq_var_gemv_batched(arr, 0, 3, 8, 1, u.F16, u.F16, None) == EINVAL
+    assert lib.unisvq_var_gemv_batched(arr, 9, 3, 8, 1, u.F16, u.F16, None) == EUNSUP
+
+
+def test_var_gemm_workspace():
+    lib = u.load()
+    # bf16 copy of x plus per-token scales, and K-split partials when the tiles cannot fill the GPU
+    assert lib.unisvq_var_gemm_workspace_bytes(4096, 4096, 2048, u.F16) == 0
+    assert lib.unisvq_var_gemm_workspace_bytes(4096, 4096, 2048, u.BF16) == 2048 * 4096 * 2 + 2048 * 4
+    assert lib.unisvq_var_gemm_workspace_bytes(4096, 4096, 16, u.F16) > 0
+    assert lib.unisvq_var_gemm_workspace_bytes(4096, 100, 16, u.F16) == 0
