@@ -39,15 +39,18 @@ def affine_groups(K: int, affine: str) -> int:
     return 1 if affine == "matrix" else K // 128
 
 
-def algorithmic_bytes(N: int, K: int, M: int, x_bytes: int = 2, y_bytes: int = 2, affine: str = "row_group") -> int:
+def algorithmic_bytes(N: int, K: int, M: int, x_bytes: int = 2, y_bytes: int = 2, affine: str = "row_group",
+                      bits: int = 2, d: int = 4) -> int:
     """Codes + affine parameters + activations + outputs.  Row-shared pairs
-    are read from their packed block of 80-byte records (one per two groups,
-    a single one for a per-matrix pair)."""
+    are read from their packed block of records (one per two groups, a single
+    one for a per-matrix pair): 80 bytes for 2-bit d = 4 codes, 160 (d = 4) or
+    576 (d = 8) bytes for the format variants."""
     if affine == "row_group":
         par = N * (K // 128) * 40
     else:
-        par = 80 if affine == "matrix" else 80 * ((K // 128 + 1) // 2)
-    return N * K // 4 + par + M * K * x_bytes + M * N * y_bytes
+        rec = 80 if (bits, d) == (2, 4) else (160 if d == 4 else 576)
+        par = rec if affine == "matrix" else rec * ((K // 128 + 1) // 2)
+    return N * K * bits // 8 + par + M * K * x_bytes + M * N * y_bytes
 
 
 def parse():
@@ -63,6 +66,9 @@ def parse():
                    help="row_group: one (A, B) pair per (row, 128-column group), stored with the codes (the "
                         "default workload); matrix: one pair per weight matrix shared by all rows (the paper's "
                         "setting), codes-only weights; group: one pair per 128-column group shared by the rows")
+    p.add_argument("--format", default="2x4", choices=["2x4", "3x4", "2x8", "3x8"],
+                   help="code bits x vector dimension; the variants (3-bit codes, d = 8) keep row-shared pairs "
+                        "(--affine matrix unless group is given)")
     p.add_argument("--schedule", default="decoder", choices=["decoder", "per_layer", "single"],
                    help="decoder: q/k/v in one batched launch, o, gate/up in one batched launch, down "
                         "(how a decode step runs them); per_layer: one launch per linear; single: all "
@@ -82,10 +88,17 @@ def parse():
     return p.parse_args()
 
 
+# Sources that define each kernel (its translation unit and the headers it is built from).
+KERNEL_SOURCES = {"gemv": ("gemv.hip", "gemv_kernel.hpp", "common.hpp"),
+                  "gemm": ("gemm.hip", "decode.hpp", "common.hpp", "skinny.hip")}
+
+
 def kernel_source_hash(kernel: str) -> str:
     import hashlib
-    src = os.path.join(ROOT, "paper_2606_10520_amd", "csrc", f"{kernel}.hip")
-    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES.get(kernel, (f"{kernel}.hip",)):
+        h.update(open(os.path.join(ROOT, "paper_2606_10520_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(kernel: str, workload: str, schedule: str):
@@ -239,20 +252,29 @@ def main():
     dev = torch.device("cuda:0")
     layers, M, xdt, outliers, kernel = workload_spec(args.workload)
     tdt = torch.float16 if xdt == "f16" else torch.bfloat16
+    bits, dim = (int(v) for v in args.format.split("x"))
+    var = (bits, dim) != (2, 4)
+    if var and args.affine == "row_group":
+        args.affine = "matrix"  # the variants keep their pairs shared by the rows
     shared = args.affine != "row_group"
     wname = args.workload if not shared else f"{args.workload}_{args.affine}_shared"
+    if var:
+        wname += f"_b{bits}d{dim}"
 
     # ---- inputs: canonical arrays drawn on the host, packed on the GPU
     canon = []
     for li, L in enumerate(layers):
-        if shared:
+        if var:
+            Q, A, B = wl.gen_var_weights(L.N, L.K, bits, dim, affine_groups(L.K, args.affine), seed=li)
+        elif shared:
             Q, A, B = wl.gen_shared_weights(L.N, L.K, affine_groups(L.K, args.affine), seed=li)
         else:
             Q, A, B = wl.gen_weights(L.N, L.K, seed=li)
         xb = wl.gen_activations(M, L.K, seed=wl.activation_seed(li, M), dtype=xdt, outliers=outliers)
         canon.append((Q, A, B, xb))
-    set_bytes = sum(algorithmic_bytes(L.N, L.K, M, affine=args.affine) for L in layers)
-    set_packed = sum((u.codes_bytes(L.N, L.K) if shared else u.packed_bytes(L.N, L.K)) for L in layers)
+    set_bytes = sum(algorithmic_bytes(L.N, L.K, M, affine=args.affine, bits=bits, d=dim) for L in layers)
+    set_packed = sum((u.var_codes_bytes(L.N, L.K, bits, dim) if var else
+                      u.codes_bytes(L.N, L.K) if shared else u.packed_bytes(L.N, L.K)) for L in layers)
     copies = max(2, -(-2 * MALL_BYTES // set_packed) + 1)
 
     def dev_half(a):
@@ -260,7 +282,9 @@ def main():
 
     packed0 = []
     for (Q, A, B, _), L in zip(canon, layers):
-        if shared:
+        if var:
+            packed0.append(u.var_pack(torch.from_numpy(Q).to(dev), dev_half(A), dev_half(B), bits, dim))
+        elif shared:
             packed0.append(u.pack_shared(torch.from_numpy(Q).to(dev), dev_half(A), dev_half(B)))
         else:
             packed0.append(u.pack(torch.from_numpy(Q).to(dev), dev_half(A), dev_half(B)))
@@ -284,7 +308,8 @@ def main():
     # serves every call, since the calls run in order on one stream.
     ws_bytes = 0
     if kernel == "gemm":
-        ws_bytes = max(u.gemm_workspace_bytes(L.N, L.K, M, tdt) for L in layers)
+        wsf = u.var_gemm_workspace_bytes if var else u.gemm_workspace_bytes
+        ws_bytes = max(wsf(L.N, L.K, M, tdt) for L in layers)
     ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
     names = [L.name for L in layers]
     full_set = {"q", "k", "v", "o", "gate", "up", "down"} <= set(names)
@@ -323,6 +348,16 @@ def main():
         return calls
 
     def launch(item, sptr):
+        if var:
+            if not isinstance(item, tuple):
+                return lib.unisvq_var_gemv_batched(item, len(item), bits, dim, M, xcode, u.F16, sptr)
+            L, (pc, pa), x, y = item
+            ga = affine_groups(L.K, args.affine)
+            if kernel == "gemv":
+                return lib.unisvq_var_gemv(L.N, L.K, bits, dim, ga, pc.data_ptr(), pa.data_ptr(), M, x.data_ptr(),
+                                           xcode, y.data_ptr(), u.F16, sptr)
+            return lib.unisvq_var_gemm(L.N, L.K, bits, dim, ga, pc.data_ptr(), pa.data_ptr(), M, x.data_ptr(),
+                                       xcode, y.data_ptr(), u.F16, ws.data_ptr(), ws_bytes, sptr)
         if isinstance(item, tuple) and shared:
             L, (pc, pa), x, y = item
             ga = affine_groups(L.K, args.affine)
@@ -540,7 +575,9 @@ def main():
     if not args.no_cpu_baseline:
         import oracle
         threads = oracle.default_threads()
-        if shared:
+        if var:
+            packed_h = [oracle.var_pack_codes(Q, bits, dim)[0] for (Q, A, B, _) in canon]
+        elif shared:
             packed_h = [oracle.pack_codes(Q)[0] for (Q, A, B, _) in canon]
         else:
             packed_h = [oracle.pack(Q, A, B)[0] for (Q, A, B, _) in canon]
@@ -554,13 +591,16 @@ def main():
                 nrows = max(16, int(L.N * rows_frac))
                 rows = None if nrows >= L.N else np.arange(nrows)
                 s0 = time.perf_counter()
-                if shared:
+                if var:
+                    oracle.var_matmul(packed_h[li], L.N, L.K, bits, canon[li][1], canon[li][2], xs[li], rows=rows,
+                                      threads=threads)
+                elif shared:
                     oracle.matmul_shared(packed_h[li], L.N, L.K, canon[li][1], canon[li][2], xs[li], rows=rows,
                                          threads=threads)
                 else:
                     oracle.matmul(packed_h[li], L.N, L.K, xs[li], rows=rows, threads=threads)
                 t_cpu += time.perf_counter() - s0
-                done_bytes += algorithmic_bytes(L.N, L.K, M, affine=args.affine) * (nrows / L.N)
+                done_bytes += algorithmic_bytes(L.N, L.K, M, affine=args.affine, bits=bits, d=dim) * (nrows / L.N)
             passes += 1
         cpu = {"value": round(done_bytes / t_cpu / 1e9, 3), "unit": "GB/s", "cores": threads,
                "kind": "oracle",
@@ -570,12 +610,16 @@ def main():
 
     if kernel == "gemv" or M <= 64:
         metric = METRIC if (M == 1 and not shared) else f"2-bit decode achieved HBM GB/s at M={M}"
+        if var:
+            metric = f"{bits}-bit d={dim} decode achieved HBM GB/s at M={M}"
         if shared:
             metric += f" (codes-only, one (A, B) pair per {'matrix' if args.affine == 'matrix' else 'group'})"
         value, unit = value_gbs, "GB/s"
     else:
         flops = sum(2 * M * L.N * L.K for L in layers)
         metric, value, unit = "unisvq_gemm effective TFLOP/s (2MNK)", flops / (ms_per_step * 1e-3) / 1e12, "TFLOP/s"
+        if var:
+            metric = f"unisvq_var_gemm ({bits}-bit codes, d={dim}) effective TFLOP/s (2MNK)"
     out = {
         "metric": metric,
         "value": round(value, 2),
@@ -593,7 +637,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "layers": {L.name: [L.N, L.K] for L in layers}, "M": M,
                    "activations": xdt, "affine": args.affine,
-                   "d": 4, "bits": 2, "group": 128, "kernel": kernel, "schedule": sched,
+                   "d": dim, "bits": bits, "group": 128, "kernel": kernel, "schedule": sched,
                    "launches_per_step": len(groups_), "buffer_copies": copies,
                    "set_bytes": set_bytes},
         "pct_peak_hbm": round(100 * value_gbs / PEAK_HBM_GBS, 2) if (kernel == "gemv" or M <= 64) else None,
