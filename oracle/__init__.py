@@ -92,6 +92,8 @@ def _load():
     lib.oracle_var_decode.restype = ci
     lib.oracle_var_matmul_rows.argtypes = [i64, i64, ci, ci, p, i64, p, p, i64, p, i64, p, p, ci]
     lib.oracle_var_matmul_rows.restype = ci
+    lib.oracle_ldlq.argtypes = [i64, i64, p, p, p, p, i64, p, p, ci]
+    lib.oracle_ldlq.restype = ci
     _lib = lib
     return lib
 
@@ -407,3 +409,50 @@ def var_matmul(packed_codes: np.ndarray, N: int, K: int, bits: int, As: np.ndarr
         _check(lib.oracle_var_matmul_rows(N, K, bits, d, _ptr(packed_codes), Ga, _ptr(Ab), _ptr(Bb), M, _ptr(X),
                                           r.size, _ptr(r), _ptr(Y), threads), "var_matmul_rows")
     return Y
+
+
+# ------------------------------------------------ LDLQ (Eq. 7)
+
+def regularised(H: np.ndarray, mu: float = 0.01) -> np.ndarray:
+    """H + mu I (the Tikhonov term of Sec. 4.2, mu = 0.01)."""
+    return np.asarray(H, dtype=np.float64) + mu * np.eye(H.shape[0])
+
+
+def ldl_blocks(H: np.ndarray, d: int = 4):
+    """H = U D U^T with U unit upper block triangular (d x d identity blocks on
+    the diagonal) and D block diagonal, from a Cholesky factorisation (library
+    routine) of H with its index order reversed: reversed(H) = C C^T gives
+    H = R R^T with R = reversed(C) upper triangular; U = R diag(R_jj)^-1 and
+    D_j = R_jj R_jj^T.  Returns (U [K][K], D [K/d][d][d])."""
+    H = np.asarray(H, dtype=np.float64)
+    K = H.shape[0]
+    C = np.linalg.cholesky(H[::-1, ::-1])
+    R = C[::-1, ::-1]
+    U = np.empty_like(R)
+    D = np.empty((K // d, d, d))
+    for j in range(K // d):
+        s = slice(d * j, d * (j + 1))
+        Rjj = R[s, s]
+        U[:, s] = np.linalg.solve(Rjj.T, R[:, s].T).T  # R[:, s] Rjj^-1
+        U[s, s] = np.eye(d)  # Rjj Rjj^-1, exactly
+        D[j] = Rjj @ Rjj.T
+    return np.ascontiguousarray(U), D
+
+
+def ldlq(W: np.ndarray, U: np.ndarray, A: np.ndarray, B: np.ndarray, shared: bool = False, threads: int | None = None):
+    """LDLQ codes (Eq. 7) of fp32 W [N][K] with the feedback factor U (fp64
+    [K][K], from ldl_blocks) and pairs as for quantize().  Returns (codes uint8
+    [N][K], errors W - W_hat fp64 [N][K])."""
+    lib = _load()
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    N, K = W.shape
+    U = np.ascontiguousarray(U, dtype=np.float64)
+    assert U.shape == (K, K)
+    Ab, Bb = _bits16(A), _bits16(B)
+    Ga = Ab.shape[0] if shared else 0
+    Q = np.empty((N, K), dtype=np.uint8)
+    E = np.empty((N, K), dtype=np.float64)
+    if threads is None:
+        threads = default_threads()
+    _check(lib.oracle_ldlq(N, K, _ptr(W), _ptr(U), _ptr(Ab), _ptr(Bb), Ga, _ptr(Q), _ptr(E), threads), "ldlq")
+    return Q, E

@@ -978,3 +978,96 @@ int oracle_var_matmul_rows(int64_t N, int64_t K, int bits, int d, const uint8_t*
     free(jobs); free(tids);
     return status;
 }
+
+/* ---- LDLQ: nearest-codeword rounding with Hessian error feedback
+ *      (Sec. 3.2.2, Eq. 7; regularisation of Sec. 4.2) ----
+ * Vectors of d = 4 consecutive columns are rounded left to right.  Before
+ * vector j (columns 4j..4j+3) is rounded, its weights are moved by the errors
+ * of all earlier columns (Eq. 7):
+ *     u_c = W[r][4j+c] + sum_{k < 4j} E[r][k] * U[k][4j+c],
+ *     E[r][k] = W[r][k] - W_hat[r][k],
+ * where the adjustment coefficients are the off-diagonal entries of the
+ * factor of H = U D U^T with U unit upper block triangular (4 x 4 identity
+ * blocks on the diagonal) and D block diagonal -- the orientation for which
+ * the proxy loss tr(E H E^T) splits into independent per-vector terms when
+ * columns run left to right (checked by a pin).  u is rounded to the nearest
+ * codeword with the operation order and tie rule of oracle_quantize.
+ * Arithmetic: the sum is one fma chain in increasing k starting from 0, then
+ * u = W + sum; codewords and E in fp64 (exact: fp16 times a small integer).
+ *   U   fp64 [K][K] row-major; only U[k][c] with k < 4 floor(c / 4) is read
+ *   E   nullable fp64 [N][K]: the errors W - W_hat */
+typedef struct {
+    int64_t N, K, Ga, r0, r1;
+    const float* W;
+    const double* U;
+    const uint16_t *A, *B;
+    uint8_t* Q;
+    double* E;
+    int status;
+} ldlq_job;
+
+static void* ldlq_worker(void* arg) {
+    ldlq_job* jb = (ldlq_job*)arg;
+    int64_t K = jb->K, groups = K / OR_G;
+    double* e = malloc((size_t)K * sizeof(double));
+    if (!e) { jb->status = OR_EINVAL; return NULL; }
+    for (int64_t r = jb->r0; r < jb->r1; ++r) {
+        for (int64_t v = 0; v < K / OR_D; ++v) {
+            int64_t j0 = OR_D * v, g = j0 / OR_G;
+            int64_t set = jb->Ga == 0 ? r * groups + g : (jb->Ga == 1 ? 0 : g);
+            double A16[16], B4[4], u[4];
+            for (int i = 0; i < 16; ++i) A16[i] = oracle_half_to_double(jb->A[set * 16 + i]);
+            for (int i = 0; i < 4; ++i) B4[i] = oracle_half_to_double(jb->B[set * 4 + i]);
+            for (int c = 0; c < OR_D; ++c) {
+                double s = 0.0;
+                for (int64_t k = 0; k < j0; ++k) s = fma(e[k], jb->U[k * K + j0 + c], s);
+                u[c] = (double)jb->W[r * K + j0 + c] + s;
+            }
+            int best = 0;
+            double dbest = codeword_dist(A16, B4, u, 0);
+            for (int i = 1; i < 256; ++i) {
+                double d = codeword_dist(A16, B4, u, i);
+                if (d < dbest) { dbest = d; best = i; }
+            }
+            for (int a = 0; a < OR_D; ++a) {
+                double cw = B4[a];
+                for (int b = 0; b < OR_D; ++b) cw = cw + A16[a * OR_D + b] * (double)((best >> (2 * b)) & 3);
+                e[j0 + a] = (double)jb->W[r * K + j0 + a] - cw;
+                jb->Q[r * K + j0 + a] = (uint8_t)((best >> (2 * a)) & 3);
+            }
+        }
+        if (jb->E) memcpy(jb->E + r * K, e, (size_t)K * sizeof(double));
+    }
+    free(e);
+    jb->status = OR_OK;
+    return NULL;
+}
+
+int oracle_ldlq(int64_t N, int64_t K, const float* W, const double* U, const uint16_t* A, const uint16_t* B,
+                int64_t Ga, uint8_t* Q, double* E, int threads) {
+    if (!W || !U || !A || !B || !Q) return OR_EINVAL;
+    if (N <= 0 || K <= 0 || K % OR_G) return OR_ESHAPE;
+    if (Ga != 0 && Ga != 1 && Ga != K / OR_G) return OR_ESHAPE;
+    if (threads < 1) threads = 1;
+    if (threads > N) threads = (int)N;
+    ldlq_job* jobs = calloc((size_t)threads, sizeof(ldlq_job));
+    pthread_t* tids = calloc((size_t)threads, sizeof(pthread_t));
+    if (!jobs || !tids) { free(jobs); free(tids); return OR_EINVAL; }
+    int64_t per = (N + threads - 1) / threads;
+    for (int t = 0; t < threads; ++t) {
+        ldlq_job* jb = &jobs[t];
+        jb->N = N; jb->K = K; jb->Ga = Ga; jb->W = W; jb->U = U; jb->A = A; jb->B = B; jb->Q = Q; jb->E = E;
+        jb->r0 = t * per < N ? t * per : N;
+        jb->r1 = (t + 1) * per < N ? (t + 1) * per : N;
+        if (threads == 1) ldlq_worker(jb);
+        else if (pthread_create(&tids[t], NULL, ldlq_worker, jb) != 0) { ldlq_worker(jb); tids[t] = 0; }
+    }
+    int status = OR_OK;
+    if (threads > 1)
+        for (int t = 0; t < threads; ++t)
+            if (tids[t]) pthread_join(tids[t], NULL);
+    for (int t = 0; t < threads; ++t)
+        if (jobs[t].status != OR_OK) status = jobs[t].status;
+    free(jobs); free(tids);
+    return status;
+}

@@ -802,3 +802,118 @@ def test_var_exact_rational_brute_force(bits, d):
             y = sum(Fraction(float(X[t, k])) * w_exact[k] for k in range(K))
             scale = sum(abs(Fraction(float(X[t, k])) * w_exact[k]) for k in range(K))
             assert abs(Fraction(Y[t, r]) - y) <= scale * Fraction(K, 2 ** 52)
+
+
+# ---------------------------------------------------------------- LDLQ (Eq. 7)
+# Reading: the adjustment coefficients of Eq. 7 are the off-diagonal entries of
+# U in H = U D U^T (U unit upper block triangular, 4 x 4 identity blocks; D
+# block diagonal); H is regularised by mu I, mu = 0.01 (Sec. 4.2).
+
+def _spd(rng, K, rank=None, corr=0.9):
+    """A correlated SPD matrix: X^T X / S for activations sharing a common
+    component (strong off-diagonal coupling), plus mu I."""
+    S = 2 * K if rank is None else rank
+    Z = rng.standard_normal((S, K))
+    common = rng.standard_normal((S, 1)) * rng.standard_normal((1, K))
+    X = np.sqrt(1 - corr) * Z + np.sqrt(corr) * common
+    return oracle.regularised(X.T @ X / S)
+
+
+def test_ldl_blocks_reconstruct_h():
+    rng = np.random.default_rng(90)
+    K = 256
+    H = _spd(rng, K)
+    U, D = oracle.ldl_blocks(H)
+    Dfull = np.zeros((K, K))
+    for j in range(K // 4):
+        Dfull[4 * j:4 * j + 4, 4 * j:4 * j + 4] = D[j]
+        assert np.allclose(D[j], D[j].T)
+        assert np.all(np.linalg.eigvalsh(D[j]) > 0)
+        np.testing.assert_array_equal(U[4 * j:4 * j + 4, 4 * j:4 * j + 4], np.eye(4))
+        assert np.all(U[4 * j + 4:, 4 * j:4 * j + 4] == 0)  # nothing below the diagonal blocks
+    np.testing.assert_allclose(U @ Dfull @ U.T, H, rtol=0, atol=1e-10 * np.abs(H).max())
+
+
+def _ldlq_case(rng, N, K, shared=False):
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    s = np.sqrt(12.0 / 15.0)
+    if shared:
+        G = np.linalg.qr(rng.standard_normal((4, 4)))[0]
+        A = (s * G)[None].astype(np.float16)
+        B = (-1.5 * s * G @ np.ones(4))[None].astype(np.float16)
+    else:
+        G = np.linalg.qr(rng.standard_normal((N * (K // 128), 4, 4)))[0]
+        A = (s * G).reshape(N, K // 128, 4, 4).astype(np.float16)
+        B = (-1.5 * s * G @ np.ones(4)).reshape(N, K // 128, 4).astype(np.float16)
+    return W, A, B
+
+
+@pytest.mark.parametrize("coupling", ["identity", "block_diagonal"])
+def test_ldlq_without_cross_vector_coupling_is_nearest_codeword(coupling):
+    """No coupling between vectors leaves U = I: no feedback, so LDLQ rounds
+    every vector to its nearest codeword."""
+    rng = np.random.default_rng(91)
+    N, K = 16, 256
+    W, A, B = _ldlq_case(rng, N, K)
+    H = np.eye(K)
+    if coupling == "block_diagonal":
+        for j in range(K // 4):
+            M = rng.standard_normal((4, 4))
+            H[4 * j:4 * j + 4, 4 * j:4 * j + 4] = M @ M.T + np.eye(4)
+    U, _ = oracle.ldl_blocks(H)
+    Q, E = oracle.ldlq(W, U, A, B)
+    assert np.array_equal(Q, oracle.quantize(W, A, B))
+
+
+@pytest.mark.parametrize("shared", [False, True])
+def test_ldlq_decisions_follow_eq7(shared):
+    """Every vector's codes are the nearest codeword to its adjusted target
+    u = W + E (U - I) (Eq. 7, recomputed here with a library matmul), the
+    first vector of a row has no feedback, E = W - W_hat exactly, and the
+    proxy loss splits per vector: tr(E H E^T) = sum_j eta_j D_j eta_j^T with
+    eta = -E U the rounding errors of the steps."""
+    rng = np.random.default_rng(92 + shared)
+    N, K = 16, 384
+    W, A, B = _ldlq_case(rng, N, K, shared)
+    H = _spd(rng, K)
+    U, D = oracle.ldl_blocks(H)
+    Q, E = oracle.ldlq(W, U, A, B, shared=shared)
+    # E is exactly W minus the decoded weights
+    What = oracle.var_decode(Q, A, B) if shared else oracle.decode(Q, A, B)
+    assert np.array_equal(E, W.astype(np.float64) - What)
+    u = W.astype(np.float64) + E @ (U - np.eye(K))
+    # the chosen codeword is the nearest to u (fp64 distances; u recomputed with
+    # a different summation order, so allow a rounding-level slack)
+    cw = What.reshape(N, K // 4, 4)
+    d_chosen = ((cw - u.reshape(N, K // 4, 4)) ** 2).sum(axis=2)
+    g = np.arange(K // 4) * 4 // 128
+    codes = np.arange(256)
+    qgrid = np.stack([(codes >> (2 * b)) & 3 for b in range(4)], axis=1).astype(np.float64)  # [256][4]
+    Af, Bf = A.astype(np.float64), B.astype(np.float64)
+    for r in range(N):
+        for v in range(K // 4):
+            Ag = Af[0] if shared else Af[r, g[v]]
+            Bg = Bf[0] if shared else Bf[r, g[v]]
+            all_cw = qgrid @ Ag.T + Bg
+            d_all = ((all_cw - u[r, 4 * v:4 * v + 4]) ** 2).sum(axis=1)
+            assert d_chosen[r, v] <= d_all.min() + 1e-9
+    assert np.array_equal(Q[:, :4], oracle.quantize(W, A, B, shared=shared)[:, :4])  # no feedback yet
+    eta = -E @ U
+    loss = np.einsum("rk,kl,rl->r", E, H, E)
+    split = sum(np.einsum("ra,ab,rb->r", eta[:, 4 * j:4 * j + 4], D[j], eta[:, 4 * j:4 * j + 4]) for j in range(K // 4))
+    np.testing.assert_allclose(loss, split, rtol=1e-9)
+
+
+def test_ldlq_feedback_lowers_the_proxy_loss():
+    """With strongly coupled columns the error feedback lowers the Hessian
+    proxy loss tr(E H E^T) against plain nearest-codeword rounding (the
+    'Hessian compensation' component of Sec. 5.2.1)."""
+    rng = np.random.default_rng(93)
+    N, K = 32, 512
+    W, A, B = _ldlq_case(rng, N, K)
+    H = _spd(rng, K, corr=0.95)
+    U, _ = oracle.ldl_blocks(H)
+    _, E_ldlq = oracle.ldlq(W, U, A, B)
+    E_rtn = W.astype(np.float64) - oracle.decode(oracle.quantize(W, A, B), A, B)
+    loss = lambda E: float(np.einsum("rk,kl,rl->", E, H, E))
+    assert loss(E_ldlq) < 0.8 * loss(E_rtn), (loss(E_ldlq), loss(E_rtn))
