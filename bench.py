@@ -61,7 +61,7 @@ def parse():
     p.add_argument("--workload", default="llama7b_decode_m1",
                    choices=["llama7b_decode_m1", "layer4096_m1", "llama70b_decode_m1",
                             "llama70b_decode_m16", "llama7b_smallbatch_m4", "llama7b_smallbatch_m16",
-                            "llama7b_smallbatch_m64", "llama7b_prefill_m2048", "quantize_llama7b"])
+                            "llama7b_smallbatch_m64", "llama7b_prefill_m2048", "quantize_llama7b", "ldlq_layer4096"])
     p.add_argument("--affine", default="row_group", choices=["row_group", "matrix", "group"],
                    help="row_group: one (A, B) pair per (row, 128-column group), stored with the codes (the "
                         "default workload); matrix: one pair per weight matrix shared by all rows (the paper's "
@@ -195,15 +195,15 @@ def bench_quantize(args):
     vecs = sum(L.N * L.K // 4 for L in layers)
     flops = vecs * 256 * QUANT_FLOP_PER_CANDIDATE
     ach = flops / (ms * 1e-3) / 1e12
-    # weight SNR of the result, from the oracle's decode of a slice of rows
-    import oracle
-    L, W, _, _, A, B, q = data[0]
+    # weight SNR of the result on a slice of rows, decoded by the library
+    L, W, Ad, Bd, A, B, q = data[0]
     rows = 64
-    Wh = oracle.decode(q[:rows].cpu().numpy(), A[:rows], B[:rows])
+    Wh = decoded_rows(u, q[:rows], Ad[:rows], Bd[:rows])
     W64 = W[:rows].double().cpu().numpy()
     snr = 10 * np.log10((W64 ** 2).sum() / ((W64 - Wh) ** 2).sum())
     cpu = None
     if not args.no_cpu_baseline:
+        import oracle
         Wc = W[:16].cpu().numpy()
         c0 = time.perf_counter()
         n = 0
@@ -229,10 +229,138 @@ def bench_quantize(args):
     print(json.dumps(out), flush=True)
 
 
+def decoded_rows(u, q, Ad, Bd):
+    """W_hat of a few rows (per-(row, group) pairs), decoded by the library:
+    the prefill product with identity activations returns W_hat^T (each
+    decoded weight rounded once to fp16)."""
+    import torch
+    N, K = q.shape
+    pk = u.pack(q.contiguous(), Ad.contiguous(), Bd.contiguous())
+    eye = torch.eye(K, dtype=torch.float16, device=q.device)
+    y = u.gemm(pk, N, K, eye, out_dtype=torch.float32)  # [K][N]
+    return y.t().double().cpu().numpy()
+
+
+def ldl_factor(H, d=4):
+    """H = U D U^T with U unit upper block triangular (the caller's factorisation
+    that unisvq_ldlq takes): Cholesky of H with its index order reversed."""
+    C = np.linalg.cholesky(H[::-1, ::-1])
+    R = np.ascontiguousarray(C[::-1, ::-1])
+    U = np.empty_like(R)
+    for j in range(H.shape[0] // d):
+        sl = slice(d * j, d * (j + 1))
+        U[:, sl] = np.linalg.solve(R[sl, sl].T, R[:, sl].T).T
+        U[sl, sl] = np.eye(d)
+    return U
+
+
+LDLQ_FLOP_PER_FEEDBACK = 2  # one fma per (row, earlier column, column)
+
+
+def bench_ldlq(args):
+    """LDLQ (Eq. 7) on one 4096 x 4096 layer: W ~ N(0, 1) fp32, the paper's
+    initial grid (Eq. 6) with one pair per (row, group), and a synthetic
+    Hessian with coupled columns (X^T X / S, S = 2K activations sharing a
+    common component, + mu I, mu = 0.01, Sec. 4.2) factorised on the host.
+    Reports vectors per second, the fp64 rate, and the Hessian proxy loss
+    tr(E H E^T) against plain nearest-codeword rounding on a slice of rows."""
+    import torch
+    import paper_2606_10520_amd.unisvq as u
+
+    lib = u.load()
+    dev = torch.device("cuda:0")
+    N = K = 4096
+    rng = np.random.default_rng(0)
+    s = np.sqrt(12.0 / 15.0)
+    G = np.linalg.qr(rng.standard_normal((N * (K // 128), 4, 4)))[0]
+    A = (s * G).astype(np.float16).reshape(N, K // 128, 4, 4)
+    B = (-1.5 * s * G.sum(axis=2)).astype(np.float16).reshape(N, K // 128, 4)
+    S = 2 * K
+    X = np.sqrt(0.1) * rng.standard_normal((S, K)) + np.sqrt(0.9) * rng.standard_normal((S, 1)) * rng.standard_normal((1, K))
+    H = X.T @ X / S + 0.01 * np.eye(K)
+    del X
+    U = ldl_factor(H)
+    W = torch.randn(N, K, device=dev, generator=torch.Generator(device=dev).manual_seed(1))
+    Ad = torch.from_numpy(A.view(np.int16)).view(torch.float16).to(dev)
+    Bd = torch.from_numpy(B.view(np.int16)).view(torch.float16).to(dev)
+    Ud = torch.from_numpy(U).to(dev)
+    q = torch.empty((N, K), dtype=torch.uint8, device=dev)
+    ws = torch.empty(u.ldlq_workspace_bytes(N, K), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        st = lib.unisvq_ldlq(N, K, W.data_ptr(), Ud.data_ptr(), Ad.data_ptr(), Bd.data_ptr(), 0, q.data_ptr(),
+                             ws.data_ptr(), ws.numel(), stream.cuda_stream)
+        if st != 0:
+            raise RuntimeError(f"unisvq_ldlq failed with status {st}")
+
+    step()
+    torch.cuda.synchronize()
+    steps = max(1, args.steps // 40)
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    vecs = N * K // 4
+    flops = vecs * 256 * QUANT_FLOP_PER_CANDIDATE + N * (K * K // 2) * LDLQ_FLOP_PER_FEEDBACK
+    ach = flops / (ms * 1e-3) / 1e12
+    # proxy loss on a slice of rows, against plain nearest-codeword rounding
+    rows = 64
+    q_rtn = torch.empty((rows, K), dtype=torch.uint8, device=dev)
+    st = lib.unisvq_quantize(rows, K, W.data_ptr(), Ad.data_ptr(), Bd.data_ptr(), 0, q_rtn.data_ptr(),
+                             stream.cuda_stream)
+    if st != 0:
+        raise RuntimeError(f"unisvq_quantize failed with status {st}")
+    W64 = W[:rows].double().cpu().numpy()
+    E_l = W64 - decoded_rows(u, q[:rows], Ad[:rows], Bd[:rows])
+    E_r = W64 - decoded_rows(u, q_rtn, Ad[:rows], Bd[:rows])
+    loss = lambda E: float(np.einsum("rk,kl,rl->", E, H, E))
+    mse = lambda E: float((E ** 2).mean())
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        Wc = W[:2].cpu().numpy()
+        c0 = time.perf_counter()
+        n = 0
+        while time.perf_counter() - c0 < min(args.cpu_seconds, 5.0) or n == 0:
+            oracle.ldlq(Wc, U, A[:2], B[:2], threads=2)
+            n += 1
+        dt = time.perf_counter() - c0
+        cpu = {"value": round(n * 2 * K / 4 / dt / 1e6, 5), "unit": "Mvectors/s", "cores": 2, "kind": "oracle",
+               "sample": f"{n} pass(es) over 2 rows of {N}x{K}, fp64 C oracle, two threads, {dt:.1f} s"}
+    out = {
+        "metric": "LDLQ quantiser throughput (one 4096x4096 layer, Hessian feedback)",
+        "value": round(vecs / (ms * 1e-3) / 1e6, 2), "unit": "Mvectors/s", "n_gpus": 1, "steps": steps,
+        "warmup": 1, "ms_per_step": round(ms, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "ldlq_layer4096", "N": N, "K": K,
+                   "grid": "Eq. 6 initial grid, one pair per (row, group)",
+                   "hessian": "X^T X / S, S = 2K, X = sqrt(0.1) Z + sqrt(0.9) common component, + 0.01 I",
+                   "launches": 1 + 2 * (K // 128) - 1},
+        "proxy_loss_over_nearest": round(loss(E_l) / loss(E_r), 4),
+        "weight_mse": {"ldlq": round(mse(E_l), 5), "nearest": round(mse(E_r), 5)},
+        "roofline": {"bound": "alu", "achieved": round(ach, 2), "peak": PEAK_FP64_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(ach / PEAK_FP64_TFLOPS, 4), "traffic": None,
+                     "kernel": "ldlq_block_kernel + ldlq_update_kernel", "avg_launch_us": None},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
+        return
+    if args.workload == "ldlq_layer4096":
+        if args.gpus != 1:
+            print(f"bench.py measures one GPU only (asked for --gpus {args.gpus})", file=sys.stderr)
+            sys.exit(2)
+        bench_ldlq(args)
         return
     if args.workload == "quantize_llama7b":
         if args.gpus != 1:

@@ -363,6 +363,31 @@ int unisvq_var_gemm(int64_t N, int64_t K, int bits, int d, int64_t affine_groups
 int unisvq_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, const uint16_t* B,
                     int64_t affine_groups, uint8_t* codes, void* stream);
 
+/* ---- LDLQ: nearest-codeword rounding with Hessian error feedback (Sec. 3.2.2, Eq. 7) ----
+ * Vectors of d = 4 consecutive columns are rounded left to right; before
+ * vector j (columns 4j..4j+3) is rounded its weights are moved by the errors of
+ * all earlier columns,  u_c = W[r][4j+c] + sum_{k < 4j} E[r][k] U[k][4j+c],
+ * E = W - W_hat, and u is rounded with the decision of unisvq_quantize (fp64,
+ * same operation order, ties to the lowest index).  U is the unit upper
+ * block-triangular factor of H = U D U^T (4 x 4 identity blocks on the
+ * diagonal, D block diagonal; H the layer's input Hessian, regularised by
+ * mu I with mu = 0.01 in Sec. 4.2); the caller factorises H.  Each sum is
+ * evaluated as one fma chain in increasing k from 0, then u = W + sum, so the
+ * codes are those of a plain sequential evaluation bit for bit.
+ *   W          device fp32 [N][K], 16-byte aligned
+ *   U          device fp64 [K][K] row-major, 16-byte aligned; only U[k][c] with
+ *              k < 4 floor(c / 4) is read
+ *   A, B       device fp16 bits, pair layouts as unisvq_quantize (affine_groups
+ *              0: per (row, group); 1 or K/128: row-shared)
+ *   codes      device uint8 [N][K] (0..3), 4-byte aligned
+ *   workspace  device, >= unisvq_ldlq_workspace_bytes(N, K) bytes (fp64 running
+ *              feedback and one block of errors), 16-byte aligned; overwritten
+ * Work: K/128 pairs of launches (each block of 128 columns: rounding with
+ * in-block feedback, then the feedback to every later column). */
+size_t unisvq_ldlq_workspace_bytes(int64_t N, int64_t K);
+int unisvq_ldlq(int64_t N, int64_t K, const float* W, const double* U, const uint16_t* A, const uint16_t* B,
+                int64_t affine_groups, uint8_t* codes, void* workspace, size_t workspace_bytes, void* stream);
+
 /* ---- Randomized Hadamard transform around the product (Sec. 3.2.1, Eq. 5) ----
  * The weights are quantised in the rotated basis W_rot = U S_U W S_V V (S_U,
  * S_V random sign diagonals, U, V Hadamard matrices normalised to be

@@ -348,6 +348,27 @@ int unisvq_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, con
     return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
 }
 
+/* ---- LDLQ ---- */
+
+size_t unisvq_ldlq_workspace_bytes(int64_t N, int64_t K) {
+    if (!shape_ok(N, K)) return 0;
+    return unisvq::ldlq_workspace_bytes(N, K);
+}
+
+int unisvq_ldlq(int64_t N, int64_t K, const float* W, const double* U, const uint16_t* A, const uint16_t* B,
+                int64_t affine_groups, uint8_t* codes, void* workspace, size_t workspace_bytes, void* stream) {
+    if (!W || !U || !A || !B || !codes) return UNISVQ_EINVAL;
+    if (!shape_ok(N, K)) return UNISVQ_ESHAPE;
+    if (affine_groups != 0 && !affine_groups_ok(K, affine_groups)) return UNISVQ_EINVAL;
+    if (!aligned(W, 16) || !aligned(U, 16) || !aligned(A, 2) || !aligned(B, 2) || !aligned(codes, 4))
+        return UNISVQ_EALIGN;
+    if (!workspace || workspace_bytes < unisvq::ldlq_workspace_bytes(N, K)) return UNISVQ_EWORKSPACE;
+    if (!aligned(workspace, 16)) return UNISVQ_EALIGN;
+    const hipError_t e = unisvq::launch_ldlq(N, K, W, U, A, B, affine_groups, codes, workspace,
+                                             static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+}
+
 /* ---- randomized Hadamard transform ---- */
 
 int unisvq_rht(int64_t n, int64_t M, const void* x, int x_dtype, const int8_t* signs, int mode, void* y, int y_dtype,

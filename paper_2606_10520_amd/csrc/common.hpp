@@ -119,6 +119,12 @@ hipError_t launch_var_unpack(int64_t N, int64_t K, int bits, int d, int64_t affi
 hipError_t launch_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, const uint16_t* B,
                            int64_t affine_groups, uint8_t* codes, hipStream_t s);
 
+// LDLQ (Eq. 7) with the caller's feedback factor U (fp64 [K][K]); workspace
+// of ldlq_workspace_bytes(N, K) bytes.
+size_t ldlq_workspace_bytes(int64_t N, int64_t K);
+hipError_t launch_ldlq(int64_t N, int64_t K, const float* W, const double* U, const uint16_t* A, const uint16_t* B,
+                       int64_t affine_groups, uint8_t* codes, void* workspace, hipStream_t s);
+
 // Randomized Hadamard transform of M rows of length n (mode 0: input side,
 // signs first; mode 1: output side, signs last); UNISVQ_EUNSUP when n has no
 // supported Hadamard construction or exceeds the LDS row.

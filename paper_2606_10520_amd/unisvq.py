@@ -26,7 +26,7 @@ EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "uni
            "unisvq_unpack_shared", "unisvq_gemv_shared", "unisvq_gemv_shared_batched", "unisvq_gemm_shared",
            "unisvq_quantize", "unisvq_rht", "unisvq_var_codes_bytes", "unisvq_var_affine_bytes",
            "unisvq_var_pack", "unisvq_var_unpack", "unisvq_var_gemv", "unisvq_var_gemv_batched",
-           "unisvq_var_gemm_workspace_bytes", "unisvq_var_gemm")
+           "unisvq_var_gemm_workspace_bytes", "unisvq_var_gemm", "unisvq_ldlq_workspace_bytes", "unisvq_ldlq")
 # format variants: (bits, d) pairs served by the unisvq_var_* entry points
 VARIANTS = ((3, 4), (2, 8), (3, 8))
 MAX_BATCH = 8
@@ -120,6 +120,10 @@ def load():
     lib.unisvq_var_gemm_workspace_bytes.restype = sz
     lib.unisvq_var_gemm.argtypes = [i64, i64, i32, i32, i64, p, p, i64, p, i32, p, i32, p, sz, p]
     lib.unisvq_var_gemm.restype = i32
+    lib.unisvq_ldlq_workspace_bytes.argtypes = [i64, i64]
+    lib.unisvq_ldlq_workspace_bytes.restype = sz
+    lib.unisvq_ldlq.argtypes = [i64, i64, p, p, p, p, i64, p, p, sz, p]
+    lib.unisvq_ldlq.restype = i32
     _lib = lib
     return lib
 
@@ -513,3 +517,28 @@ def var_gemm(packed_codes, packed_affine, N: int, K: int, bits: int, d: int, aff
     wb = workspace.numel() * workspace.element_size() if workspace is not None else 0
     return _var_product("unisvq_var_gemm", N, K, bits, d, affine_groups, packed_codes, packed_affine, x, out,
                         out_dtype, stream, extra=(_ptr(workspace), wb))
+
+
+# ------------------------------------------------ LDLQ (Eq. 7)
+
+def ldlq_workspace_bytes(N: int, K: int) -> int:
+    return load().unisvq_ldlq_workspace_bytes(N, K)
+
+
+def ldlq(W, U, A, B, affine_groups: int = 0, out=None, workspace=None, stream=None):
+    """LDLQ codes of fp32 W [N][K] with the feedback factor U (fp64 [K][K], unit
+    upper block triangular, from H = U D U^T); A/B as quantize().  Returns
+    codes uint8 [N][K]."""
+    torch = _torch()
+    _need_cuda(W, U, A, B, out, workspace)
+    N, K = W.shape
+    if out is None:
+        out = torch.empty((N, K), dtype=torch.uint8, device=W.device)
+    need = ldlq_workspace_bytes(N, K)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=W.device)
+    wb = workspace.numel() * workspace.element_size()
+    _check("unisvq_ldlq", load().unisvq_ldlq(N, K, _ptr(W.contiguous()), _ptr(U.contiguous()), _ptr(A.contiguous()),
+                                              _ptr(B.contiguous()), affine_groups, _ptr(out), _ptr(workspace), wb,
+                                              _stream(stream)))
+    return out

@@ -330,3 +330,20 @@ def test_var_gemm_workspace():
     assert lib.unisvq_var_gemm_workspace_bytes(4096, 4096, 2048, u.BF16) == 2048 * 4096 * 2 + 2048 * 4
     assert lib.unisvq_var_gemm_workspace_bytes(4096, 4096, 16, u.F16) > 0
     assert lib.unisvq_var_gemm_workspace_bytes(4096, 100, 16, u.F16) == 0
+
+
+def test_ldlq_validation():
+    lib = u.load()
+    need = lib.unisvq_ldlq_workspace_bytes(16, 256)
+    assert need == 16 * 256 * 8 + 16 * 128 * 8
+    assert lib.unisvq_ldlq_workspace_bytes(15, 256) == 0
+    assert lib.unisvq_ldlq(16, 256, None, GOOD, GOOD, GOOD, 0, GOOD, GOOD, need, None) == EINVAL
+    assert lib.unisvq_ldlq(16, 256, GOOD, None, GOOD, GOOD, 0, GOOD, GOOD, need, None) == EINVAL
+    assert lib.unisvq_ldlq(16, 256, GOOD, GOOD, GOOD, GOOD, 3, GOOD, GOOD, need, None) == EINVAL
+    assert lib.unisvq_ldlq(16, 200, GOOD, GOOD, GOOD, GOOD, 0, GOOD, GOOD, need, None) == ESHAPE
+    assert lib.unisvq_ldlq(16, 256, GOOD + 4, GOOD, GOOD, GOOD, 0, GOOD, GOOD, need, None) == EALIGN
+    assert lib.unisvq_ldlq(16, 256, GOOD, GOOD + 8, GOOD, GOOD, 0, GOOD, GOOD, need, None) == EALIGN
+    assert lib.unisvq_ldlq(16, 256, GOOD, GOOD, GOOD, GOOD, 0, GOOD + 2, GOOD, need, None) == EALIGN
+    assert lib.unisvq_ldlq(16, 256, GOOD, GOOD, GOOD, GOOD, 0, GOOD, None, need, None) == EWS
+    assert lib.unisvq_ldlq(16, 256, GOOD, GOOD, GOOD, GOOD, 0, GOOD, GOOD, need - 8, None) == EWS
+    assert lib.unisvq_ldlq(16, 256, GOOD, GOOD, GOOD, GOOD, 0, GOOD, GOOD + 8, need, None) == EALIGN
