@@ -6,10 +6,13 @@
 // every packet load a coalesced 16-byte-per-lane read issued well ahead of
 // use, and partial sums meeting once in LDS.  Per group each wavefront
 // decodes its 16 x 128 weight tile on the matrix cores (A q + B exactly in
-// fp32 from the integer codes, Eq. 4; one rounding to fp16) into its own LDS
-// tile and multiplies it with up to 64 tokens on v_mfma_f32_16x16x32_f16
-// (token tiles of 16; activation operands read straight from global memory
-// in the matrix-core layout).  Decoded weights never leave LDS.
+// fp32 from the integer codes, Eq. 4; one rounding to fp16) into one of its
+// two LDS tiles and multiplies it with up to 64 tokens on
+// v_mfma_f32_16x16x32_f16 (token tiles of 16; activation operands read
+// straight from global memory in the matrix-core layout).  The products of
+// each group run one decode behind, so a group's decode overlaps the
+// previous group's LDS reads and matrix-core work.  Decoded weights never
+// leave LDS.
 #include "common.hpp"
 #include "decode.hpp"
 
@@ -22,6 +25,38 @@ constexpr int kSTile = 16 * kSRow;      // halves per wavefront tile (16 rows, o
 // One group (jj of the piece's packet) of this wavefront's run: decode, read
 // the weight operand back, multiply with the MT token tiles.  xo is the
 // lane's activation offset of the group's first column (or out of range).
+// The three stages of one group, for the pipelined loop below: decode the
+// wavefront's 16 x 128 tile into LDS, load the activation operands, multiply.
+template <int MT>
+__device__ inline void sk_decode(const Piece& pc, int jj, int j, _Float16* wrow) {
+    DecOps ops;
+    prepare(pc, j, jj, ops);
+    decode_vecs<0>(ops, wrow, j);
+    decode_vecs<1>(ops, wrow, j);
+    decode_vecs<2>(ops, wrow, j);
+    decode_vecs<3>(ops, wrow, j);
+    decode_vecs<4>(ops, wrow, j);
+    decode_vecs<5>(ops, wrow, j);
+    decode_vecs<6>(ops, wrow, j);
+    decode_vecs<7>(ops, wrow, j);
+}
+template <int MT>
+__device__ inline void sk_load_x(__amdgpu_buffer_rsrc_t rx, uint32_t xo, uint32_t row_step, f16x8 (&xa)[MT][4]) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int s = 0; s < 4; ++s) xa[i][s] = __builtin_bit_cast(f16x8, ld128(rx, xo + i * row_step + 64 * s));
+}
+template <int MT>
+__device__ inline void sk_mma(const _Float16* wlane, const f16x8 (&xa)[MT][4], f32x4 (&acc)[MT]) {
+    f16x8 wb[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) wb[s] = *reinterpret_cast<const f16x8*>(wlane + 32 * s);
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int i = 0; i < MT; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa[i][s], wb[s], acc[i], 0, 0, 0);
+}
 template <int MT>
 __device__ inline void skinny_group(__amdgpu_buffer_rsrc_t rx, uint32_t xo, uint32_t row_step, const Piece& pc,
                                     int jj, int j, _Float16* wrow, const _Float16* wlane, f32x4 (&acc)[MT]) {
@@ -58,7 +93,7 @@ __global__ __launch_bounds__(WAVES * 64) void skinny_kernel(const uint8_t* __res
                                                            const _Float16* __restrict__ x,
                                                            const float* __restrict__ inv_scale, void* y, int N,
                                                            int K, int M, int y_dtype) {
-    __shared__ __attribute__((aligned(16))) _Float16 wtile[WAVES * kSTile];
+    __shared__ __attribute__((aligned(16))) _Float16 wtile[2 * WAVES * kSTile];
     __shared__ float red[WAVES][MT * 16][16];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -107,16 +142,27 @@ __global__ __launch_bounds__(WAVES * 64) void skinny_kernel(const uint8_t* __res
     Piece ring[PF];
 #pragma unroll
     for (int i = 0; i < PF; ++i) load(p0 + i, gend, ring[i]);
+    // two tiles per wavefront: group (q, 0) in tile 0, (q, 1) in tile 1; the
+    // products of each group run one decode behind
+    _Float16* wrow1 = wrow + WAVES * kSTile;
+    const _Float16* wlane1 = wlane + WAVES * kSTile;
+    f16x8 xp[MT][4];
     for (int q0 = 0; q0 < np; q0 += PF) {
 #pragma unroll
         for (int i = 0; i < PF; ++i) {
             const int q = q0 + i;
             const uint32_t xo = q < np ? xlane + static_cast<uint32_t>(p0 + q) * 512u : kOutOfRange;
-            skinny_group<MT>(rx, xo, row_step, ring[i], 0, j, wrow, wlane, acc);
-            skinny_group<MT>(rx, q < np ? xo + 256u : kOutOfRange, row_step, ring[i], 1, j, wrow, wlane, acc);
+            f16x8 x0[MT][4];
+            sk_load_x<MT>(rx, xo, row_step, x0);
+            sk_decode<MT>(ring[i], 0, j, wrow);
+            if (q > 0) sk_mma<MT>(wlane1, xp, acc);
+            sk_load_x<MT>(rx, q < np ? xo + 256u : kOutOfRange, row_step, xp);
+            sk_decode<MT>(ring[i], 1, j, wrow1);
+            sk_mma<MT>(wlane, x0, acc);
             load(p0 + q + PF, gend, ring[i]);
         }
     }
+    if (np > 0) sk_mma<MT>(wlane1, xp, acc);
     if (do_half) {
         Piece h;
         load(nfull, groups, h);
