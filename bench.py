@@ -90,7 +90,12 @@ def parse():
 
 # Sources that define each kernel (its translation unit and the headers it is built from).
 KERNEL_SOURCES = {"gemv": ("gemv.hip", "gemv_kernel.hpp", "common.hpp"),
-                  "gemm": ("gemm.hip", "decode.hpp", "common.hpp", "skinny.hip")}
+                  "gemm": ("gemm.hip", "decode.hpp", "common.hpp"),
+                  "skinny": ("skinny.hip", "decode.hpp", "common.hpp")}
+
+
+# Largest batch the 2x4 product sends to the skinny kernel (kSkinnyMaxM).
+SKINNY_MAX_M = 32
 
 
 def kernel_source_hash(kernel: str) -> str:
@@ -681,13 +686,15 @@ def main():
                     "kernel": "gemv_kernel", "avg_launch_us": round(avg_us, 3),
                     "bytes_per_launch": int(bytes_per_launch)}
     elif M <= 64:
-        # small batch: still bound by the weight stream
+        # small batch: still bound by the weight stream.  The 2x4 format at
+        # M <= 32 runs the skinny kernel, everything else the tiled one.
+        kname = "skinny" if (not var and M <= SKINNY_MAX_M) else "gemm"
         ach = bytes_per_launch / (avg_us * 1e-6) / 1e9
-        traffic = measured_traffic("gemm", wname, sched)
+        traffic = measured_traffic(kname, wname, sched)
         roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                     "frac": round(ach / PEAK_HBM_GBS, 4),
                     "traffic": None if traffic is None else int(traffic),
-                    "kernel": "gemm_kernel", "avg_launch_us": round(avg_us, 3),
+                    "kernel": f"{kname}_kernel", "avg_launch_us": round(avg_us, 3),
                     "bytes_per_launch": int(bytes_per_launch)}
     else:
         flops = sum(2 * M * L.N * L.K for L in layers) / launches_per_step
