@@ -13,10 +13,12 @@
 //
 // One workgroup per (row, slice of output blocks).  The row goes to LDS in
 // fp32 (signs applied on the input side); the Paley factor, if any, runs as a
-// dense product for the workgroup's output blocks with its entries built in
-// LDS from the quadratic character, then the Sylvester factor as an in-place
-// fast transform inside each of those blocks of 2^k.  fp32 throughout, one
-// rounding to the output dtype.
+// dense product for the workgroup's output blocks -- on the matrix cores in
+// fp32 (rht_paley_kernel), or on the vector ALUs when its tables would not fit
+// the LDS (rht_kernel) -- with its entries built in LDS from the quadratic
+// character, then the Sylvester factor as an in-place fast transform inside
+// each of those blocks of 2^k.  fp32 throughout, one rounding to the output
+// dtype.
 #include <cmath>
 
 #include "common.hpp"
@@ -56,11 +58,23 @@ __device__ inline void load_row(const XT* __restrict__ xr, const signed char* __
     }
 }
 
+// x mod p for |x| < 2^22 through the float reciprocal rp = 1/p: the quotient
+// estimate is off by at most one, which one correction either way fixes.
+__device__ inline int mod_p(int x, int p, float rp) {
+    int r = x - static_cast<int>(floorf(static_cast<float>(x) * rp)) * p;
+    r += r < 0 ? p : 0;
+    r -= r >= p ? p : 0;
+    return r;
+}
+
 // digits of field element x (constant term first)
 __device__ inline void gf_digits(int x, int p, int e, int* c) {
+    const float rp = 1.0f / static_cast<float>(p);
     for (int i = 0; i < 3; ++i) {
-        c[i] = i < e ? x % p : 0;
-        x = i < e ? x / p : x;
+        const int r = mod_p(x, p, rp);  // x < q <= 32767
+        c[i] = i < e ? r : 0;
+        // (x - r) / p is an integer: the float quotient rounds to it exactly
+        x = i < e ? static_cast<int>(rintf(static_cast<float>(x - r) * rp)) : x;
     }
 }
 
@@ -71,19 +85,38 @@ __device__ inline int gf_index(const int* c, int p, int e) {
     return x;
 }
 
-// x^2 in GF(p^e) modulo f (e <= 3)
+// x^2 in GF(p^e) modulo f (e <= 3), written out per degree so that no array
+// is indexed at run time.  For e = 1 the square can reach 2^30 and is reduced
+// in 64 bits; for e >= 2, p <= 181 keeps every intermediate below 2^17 in
+// magnitude, within mod_p's range.  With f = x^e + f[e-1] x^(e-1) + ... + f[0],
+// x^e = -(f[e-1] x^(e-1) + ... + f[0]) removes the top coefficients one by one.
 __device__ inline int gf_square(int x, const HadSpec& h) {
-    int a[3], t[5] = {0, 0, 0, 0, 0};
-    gf_digits(x, h.p, h.e, a);
-    for (int i = 0; i < h.e; ++i)
-        for (int j = 0; j < h.e; ++j) t[i + j] = (t[i + j] + a[i] * a[j]) % h.p;
-    for (int d = 2 * h.e - 2; d >= h.e; --d) {
-        const int c = t[d];
-        if (!c) continue;
-        t[d] = 0;
-        for (int i = 0; i < h.e; ++i) t[d - h.e + i] = ((t[d - h.e + i] - c * h.f[i]) % h.p + h.p) % h.p;
+    const int p = h.p;
+    if (h.e == 1) return static_cast<int>(static_cast<int64_t>(x) * x % p);
+    const float rp = 1.0f / static_cast<float>(p);
+    int a[3];
+    gf_digits(x, p, h.e, a);
+    if (h.e == 2) {
+        int t0 = mod_p(a[0] * a[0], p, rp), t1 = mod_p(2 * a[0] * a[1], p, rp);
+        const int t2 = mod_p(a[1] * a[1], p, rp);
+        t0 = mod_p(t0 - t2 * h.f[0], p, rp);
+        t1 = mod_p(t1 - t2 * h.f[1], p, rp);
+        return t0 + p * t1;
     }
-    return gf_index(t, h.p, h.e);
+    int t0 = mod_p(a[0] * a[0], p, rp);
+    int t1 = mod_p(2 * a[0] * a[1], p, rp);
+    int t2 = mod_p(a[1] * a[1] + 2 * a[0] * a[2], p, rp);
+    int t3 = mod_p(2 * a[1] * a[2], p, rp);
+    const int t4 = mod_p(a[2] * a[2], p, rp);
+    // x^4 = x * x^3
+    t1 = mod_p(t1 - t4 * h.f[0], p, rp);
+    t2 = mod_p(t2 - t4 * h.f[1], p, rp);
+    t3 = mod_p(t3 - t4 * h.f[2], p, rp);
+    // x^3
+    t0 = mod_p(t0 - t3 * h.f[0], p, rp);
+    t1 = mod_p(t1 - t3 * h.f[1], p, rp);
+    t2 = mod_p(t2 - t3 * h.f[2], p, rp);
+    return t0 + p * (t1 + p * t2);
 }
 
 __device__ inline int paley_entry(const signed char* chi, const HadSpec& h, int i, int j) {
@@ -93,7 +126,10 @@ __device__ inline int paley_entry(const signed char* chi, const HadSpec& h, int 
     int a[3], b[3], d[3];
     gf_digits(i - 1, h.p, h.e, a);
     gf_digits(j - 1, h.p, h.e, b);
-    for (int t = 0; t < 3; ++t) d[t] = ((a[t] - b[t]) % h.p + h.p) % h.p;
+    for (int t = 0; t < 3; ++t) {
+        d[t] = a[t] - b[t];
+        d[t] += d[t] < 0 ? h.p : 0;
+    }
     return chi[gf_index(d, h.p, h.e)];
 }
 
@@ -194,6 +230,275 @@ __global__ __launch_bounds__(kRhtThreads) void rht_kernel(const XT* __restrict__
     }
 }
 
+// ---------------------------------------------------------------------------
+// Pure Sylvester orders n = 2^k, 2^10 <= n <= 2^15: one workgroup of
+// T = 64 * 2^W threads per row, R = 2^LR elements per thread, k = 6 + W + LR,
+// W <= LR.  Index bits 0..5 live in the lanes, bits 6 .. 6+W-1 in the
+// wavefront number, the top LR bits in the thread's registers:
+//   phase 1: element i = lane | wave << 6 | r << (6 + W); the register bits'
+//            butterflies in registers, then the lane bits' across lanes (DPP
+//            for distances 1 and 2, bpermute for 4 .. 32);
+//   exchange through LDS (written and read in lane order: no bank conflicts);
+//   phase 2: element i = lane | (r mod 2^W) << 6 | (r >> W) << (6 + W) |
+//            wave << (6 + LR), i.e. the wavefront bits now in registers;
+//            their butterflies, then the store straight from registers.
+// Every element takes one butterfly per index bit, (a, b) -> (a + b, a - b),
+// in fp32.
+
+template <int D>
+__device__ inline float lane_xor(float v, int lane) {
+    if constexpr (D == 1)
+        return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xf, 0xf, false));
+    else if constexpr (D == 2)
+        return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E, 0xf, 0xf, false));
+    else
+        return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((lane ^ D) << 2, __builtin_bit_cast(int, v)));
+}
+
+// Butterflies over register-index bit J (registers r and r | 1 << J).
+template <int R, int J>
+__device__ inline void reg_stage(float (&v)[R]) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        if (r & (1 << J)) continue;
+        const float a = v[r], b = v[r | (1 << J)];
+        v[r] = a + b;
+        v[r | (1 << J)] = a - b;
+    }
+}
+
+template <int R, int J0, int J1>
+__device__ inline void reg_stages(float (&v)[R]) {
+    if constexpr (J0 < J1) {
+        reg_stage<R, J0>(v);
+        reg_stages<R, J0 + 1, J1>(v);
+    }
+}
+
+template <int R, int D>
+__device__ inline void lane_stage(float (&v)[R], int lane) {
+    const bool hi = lane & D;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const float p = lane_xor<D>(v[r], lane);
+        v[r] = hi ? p - v[r] : v[r] + p;
+    }
+}
+
+template <typename XT, int W, int LR>
+__global__ __launch_bounds__(64 << W) void fwht_kernel(const XT* __restrict__ x, const signed char* __restrict__ signs,
+                                                       int mode, void* __restrict__ y, int y_dtype, float norm) {
+    constexpr int R = 1 << LR;
+    constexpr int K = 6 + W + LR;
+    constexpr int N = 1 << K;
+    static_assert(W <= LR && R <= 32, "register and wavefront bits");
+    __shared__ float z[N];
+    const int64_t row = blockIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const XT* xr = x + row * N;
+
+    // phase-2 element of register r (its sign is fetched early on the output side)
+    auto idx2 = [&](int r) { return lane | (r & ((1 << W) - 1)) << 6 | (r >> W) << (6 + W) | wave << (6 + LR); };
+    float v[R];
+    signed char so[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int i = lane | wave << 6 | r << (6 + W);
+        v[r] = static_cast<float>(xr[i]);
+        so[r] = mode == 1 ? signs[idx2(r)] : 1;
+    }
+    if (mode == 0) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) v[r] *= static_cast<float>(signs[lane | wave << 6 | r << (6 + W)]);
+    }
+    reg_stages<R, 0, LR>(v);
+    lane_stage<R, 1>(v, lane);
+    lane_stage<R, 2>(v, lane);
+    lane_stage<R, 4>(v, lane);
+    lane_stage<R, 8>(v, lane);
+    lane_stage<R, 16>(v, lane);
+    lane_stage<R, 32>(v, lane);
+    if constexpr (W > 0) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) z[lane | wave << 6 | r << (6 + W)] = v[r];
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < R; ++r) v[r] = z[idx2(r)];
+        reg_stages<R, 0, W>(v);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        store_out(y, row * N + idx2(r), v[r] * norm * static_cast<float>(so[r]), y_dtype);
+}
+
+// ---------------------------------------------------------------------------
+// The Paley factor on the matrix cores.  For a workgroup's cnt <= 16 output
+// blocks, W[jl][i2] = sum_im P[im][jb0 + jl] z[im][i2] is a (16 x m) by
+// (m x 2^k) product, run as v_mfma_f32_16x16x4_f32 steps: A lane (jl, kk) =
+// P[4s + kk][jb0 + jl], B lane (kk, c) = z[4s + kk][16 nt + c] -- fp32
+// operands (the entries of P are 0 and +-1, so every product is exact) and
+// fp32 accumulation.  The 16 wavefronts split the column tiles and, when
+// there are fewer than 16 of them, the k range; partial sums meet in LDS and
+// are added in a fixed order.  P's entries come from digit tables of the
+// field elements and the quadratic character (no division in the entries).
+
+// Packed base-p digits of field element x: for e >= 2 (then p <= 181) one
+// byte per digit, constant term in the low byte; for e = 1 x itself.
+__device__ inline int gf_packed(int x, int p, int e) {
+    if (e == 1) return x;
+    int c[3];
+    gf_digits(x, p, e, c);
+    return c[0] | (c[1] << 8) | (c[2] << 16);
+}
+
+// Index of the field element a - b from packed digits.
+__device__ inline int gf_sub_index(int a, int b, int p, int e) {
+    if (e == 1) {
+        const int d = a - b;
+        return d < 0 ? d + p : d;
+    }
+    int idx = 0;
+#pragma unroll
+    for (int t = 2; t >= 0; --t) {
+        int d = ((a >> (8 * t)) & 0xff) - ((b >> (8 * t)) & 0xff);
+        d += d < 0 ? p : 0;
+        idx = idx * p + d;
+    }
+    return idx;
+}
+
+struct PaleyPlan {
+    int cnt;     // output blocks per workgroup (<= 16)
+    int ntiles;  // 16-column tiles of a block of 2^k
+    int ksplit;  // wavefronts sharing one column tile's k range
+};
+
+__host__ __device__ inline size_t paley_lds_bytes(const HadSpec& h, int n, const PaleyPlan& pl) {
+    const size_t half = size_t{1} << h.k;
+    const size_t hp = pl.ntiles * 16;  // padded block width
+    size_t b = static_cast<size_t>(n) * 4;           // z
+    b += static_cast<size_t>(h.m) * 16 * 4;           // pcol [m][16]
+    b += static_cast<size_t>(pl.cnt) * half * 4;      // w [cnt][half]
+    if (pl.ksplit > 1) b += static_cast<size_t>(pl.ksplit) * pl.cnt * hp * 4;  // partials
+    b += static_cast<size_t>(h.q) * 4 + h.q;          // digits, character
+    return b;
+}
+
+template <typename XT>
+__global__ __launch_bounds__(kRhtThreads) void rht_paley_kernel(const XT* __restrict__ x,
+                                                                const signed char* __restrict__ signs, int mode,
+                                                                void* __restrict__ y, int y_dtype, int n, HadSpec h,
+                                                                PaleyPlan pl, float norm) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    const int half = 1 << h.k;
+    const int m = h.m;
+    const int hp = pl.ntiles * 16;
+    float* z = reinterpret_cast<float*>(smem);                 // [n]
+    float* pcol = z + n;                                        // [m][16]
+    float* w = pcol + m * 16;                                   // [cnt][half]
+    float* part = w + pl.cnt * half;                            // [ksplit][cnt][hp]
+    int* dig = reinterpret_cast<int*>(part + (pl.ksplit > 1 ? pl.ksplit * pl.cnt * hp : 0));  // [q]
+    signed char* chi = reinterpret_cast<signed char*>(dig + h.q);                              // [q]
+    const int64_t row = blockIdx.y;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int jb0 = blockIdx.x * pl.cnt;
+    const int cnt = min(m, jb0 + pl.cnt) - jb0;
+
+    // 1. the row's loads go out first, raw into registers, and land while the
+    //    digit and character tables are built; then the row goes to LDS
+    //    (signs applied on the input side)
+    constexpr int R = kRhtMaxN / kRhtThreads;
+    XT xv[R];
+    signed char sv[R];
+    const XT* xr = x + row * n;
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+        const int i = tid + u * kRhtThreads;
+        if (i < n) {
+            xv[u] = xr[i];
+            sv[u] = mode == 0 ? signs[i] : 1;
+        }
+    }
+    for (int i = tid; i < h.q; i += kRhtThreads) {
+        chi[i] = i == 0 ? 0 : -1;
+        dig[i] = gf_packed(i, h.p, h.e);
+    }
+    __syncthreads();
+    for (int v = 1 + tid; v < h.q; v += kRhtThreads) chi[gf_square(v, h)] = 1;
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+        const int i = tid + u * kRhtThreads;
+        if (i < n) z[i] = static_cast<float>(xv[u]) * static_cast<float>(sv[u]);
+    }
+    __syncthreads();
+    // 2. pcol[im][jl] = P[im][jb0 + jl] (0 past the workgroup's blocks)
+    for (int t = tid; t < m * 16; t += kRhtThreads) {
+        const int im = t >> 4, jl = t & 15;
+        const int j = jb0 + jl;
+        float v = 0.f;
+        if (jl < cnt) {
+            if (im == 0)
+                v = 1.f;
+            else if (j == 0)
+                v = -1.f;
+            else if (im == j)
+                v = 1.f;
+            else
+                v = static_cast<float>(chi[gf_sub_index(dig[im - 1], dig[j - 1], h.p, h.e)]);
+        }
+        pcol[t] = v;
+    }
+    __syncthreads();
+    // 3. the product: work item (column tile nt, k chunk kc)
+    const int ksteps = (m + 3) >> 2;
+    const int per = (ksteps + pl.ksplit - 1) / pl.ksplit;
+    const int r16 = lane & 15, kk = lane >> 4;
+    for (int it = wave; it < pl.ntiles * pl.ksplit; it += kRhtThreads / 64) {
+        const int nt = it % pl.ntiles, kc = it / pl.ntiles;
+        const int s0 = kc * per, s1 = min(ksteps, s0 + per);
+        const int col = 16 * nt + r16;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int s = s0; s < s1; ++s) {
+            const int im = 4 * s + kk;
+            const float a = im < m ? pcol[im * 16 + r16] : 0.f;
+            const float b = (im < m && col < half) ? z[im * half + col] : 0.f;
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+        }
+        // D lane (r16, kk), element e: block 4 kk + e, column col
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int jl = 4 * kk + e;
+            if (jl < pl.cnt && col < half) {
+                if (pl.ksplit > 1)
+                    part[(kc * pl.cnt + jl) * hp + col] = acc[e];
+                else
+                    w[jl * half + col] = acc[e];
+            }
+        }
+    }
+    __syncthreads();
+    if (pl.ksplit > 1) {
+        for (int o = tid; o < pl.cnt * half; o += kRhtThreads) {
+            const int jl = o >> h.k, c = o & (half - 1);
+            float s = part[jl * hp + c];
+            for (int kc = 1; kc < pl.ksplit; ++kc) s += part[(kc * pl.cnt + jl) * hp + c];
+            w[o] = s;
+        }
+        __syncthreads();
+    }
+    // 4. Sylvester factor inside each of this workgroup's blocks
+    sylvester_blocks(w, cnt * half, h.k, tid);
+    for (int o = tid; o < cnt * half; o += kRhtThreads) {
+        const int j = jb0 * half + o;
+        float v = w[o] * norm;
+        if (mode == 1) v *= static_cast<float>(signs[j]);
+        store_out(y, row * n + j, v, y_dtype);
+    }
+}
+
 bool is_prime(int v) {
     if (v < 2) return false;
     for (int d = 2; d * d <= v; ++d)
@@ -282,6 +587,37 @@ int rht_blocks_per_wg(const HadSpec& h, int n) {
     return per;
 }
 
+template <int W, int LR>
+static int launch_fwht(const void* x, int x_dtype, const signed char* signs, int mode, void* y, int y_dtype,
+                       float norm, dim3 grid, hipStream_t s) {
+    const dim3 block(64 << W);
+    if (x_dtype == UNISVQ_F16)
+        hipLaunchKernelGGL((fwht_kernel<_Float16, W, LR>), grid, block, 0, s, static_cast<const _Float16*>(x), signs,
+                           mode, y, y_dtype, norm);
+    else if (x_dtype == UNISVQ_BF16)
+        hipLaunchKernelGGL((fwht_kernel<__bf16, W, LR>), grid, block, 0, s, static_cast<const __bf16*>(x), signs,
+                           mode, y, y_dtype, norm);
+    else
+        hipLaunchKernelGGL((fwht_kernel<float, W, LR>), grid, block, 0, s, static_cast<const float*>(x), signs, mode,
+                           y, y_dtype, norm);
+    return hipGetLastError() == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+}
+
+// Output blocks per workgroup (at most 16, the matrix-core tile height, and
+// at most 512 outputs, so that long blocks spread over more workgroups),
+// 16-column tiles per block, and the k split that gives the 16 wavefronts
+// one (tile, k chunk) item each when there are fewer tiles.
+static PaleyPlan paley_plan(const HadSpec& h) {
+    const int half = 1 << h.k;
+    PaleyPlan pl;
+    pl.ntiles = half >= 16 ? half / 16 : 1;
+    int c = 512 / half;
+    c = c < 1 ? 1 : (c > 16 ? 16 : c);
+    pl.cnt = c < h.m ? c : h.m;
+    pl.ksplit = pl.ntiles >= 16 ? 1 : 16 / pl.ntiles;
+    return pl;
+}
+
 int launch_rht(int64_t n, int64_t M, const void* x, int x_dtype, const signed char* signs, int mode, void* y,
                int y_dtype, hipStream_t s) {
     HadSpec h;
@@ -291,17 +627,54 @@ int launch_rht(int64_t n, int64_t M, const void* x, int x_dtype, const signed ch
     if (lds > kRhtMaxLds) return UNISVQ_EUNSUP;
     static bool attr_done = false;  // idempotent; racing first calls set the same value
     if (!attr_done) {
-        const void* fns[3] = {reinterpret_cast<const void*>(&rht_kernel<_Float16>),
+        const void* fns[6] = {reinterpret_cast<const void*>(&rht_kernel<_Float16>),
                               reinterpret_cast<const void*>(&rht_kernel<__bf16>),
-                              reinterpret_cast<const void*>(&rht_kernel<float>)};
+                              reinterpret_cast<const void*>(&rht_kernel<float>),
+                              reinterpret_cast<const void*>(&rht_paley_kernel<_Float16>),
+                              reinterpret_cast<const void*>(&rht_paley_kernel<__bf16>),
+                              reinterpret_cast<const void*>(&rht_paley_kernel<float>)};
         for (const void* f : fns)
             if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kRhtMaxLds)) !=
                 hipSuccess)
                 return UNISVQ_EHIP;
         attr_done = true;
     }
-    const unsigned gx = h.m > 1 ? static_cast<unsigned>((h.m + per - 1) / per) : 1u;
     const float norm = static_cast<float>(1.0 / std::sqrt(static_cast<double>(n)));
+    if (h.m == 1 && h.k >= 10) {  // 2^10 .. 2^15: registers, lanes and one exchange
+        const dim3 fgrid(static_cast<unsigned>(M));
+        int st = UNISVQ_OK;
+        switch (h.k) {
+            case 10: st = launch_fwht<2, 2>(x, x_dtype, signs, mode, y, y_dtype, norm, fgrid, s); break;
+            case 11: st = launch_fwht<2, 3>(x, x_dtype, signs, mode, y, y_dtype, norm, fgrid, s); break;
+            case 12: st = launch_fwht<3, 3>(x, x_dtype, signs, mode, y, y_dtype, norm, fgrid, s); break;
+            case 13: st = launch_fwht<3, 4>(x, x_dtype, signs, mode, y, y_dtype, norm, fgrid, s); break;
+            case 14: st = launch_fwht<4, 4>(x, x_dtype, signs, mode, y, y_dtype, norm, fgrid, s); break;
+            default: st = launch_fwht<4, 5>(x, x_dtype, signs, mode, y, y_dtype, norm, fgrid, s); break;
+        }
+        return st;
+    }
+    if (h.m > 1) {
+        // matrix-core Paley factor whenever its tables fit the LDS
+        const PaleyPlan pl = paley_plan(h);
+        const size_t plds = paley_lds_bytes(h, static_cast<int>(n), pl);
+        if (plds <= kRhtMaxLds) {
+            const dim3 pgrid(static_cast<unsigned>((h.m + pl.cnt - 1) / pl.cnt), static_cast<unsigned>(M));
+            if (x_dtype == UNISVQ_F16)
+                hipLaunchKernelGGL(rht_paley_kernel<_Float16>, pgrid, dim3(kRhtThreads), plds, s,
+                                   static_cast<const _Float16*>(x), signs, mode, y, y_dtype, static_cast<int>(n), h,
+                                   pl, norm);
+            else if (x_dtype == UNISVQ_BF16)
+                hipLaunchKernelGGL(rht_paley_kernel<__bf16>, pgrid, dim3(kRhtThreads), plds, s,
+                                   static_cast<const __bf16*>(x), signs, mode, y, y_dtype, static_cast<int>(n), h,
+                                   pl, norm);
+            else
+                hipLaunchKernelGGL(rht_paley_kernel<float>, pgrid, dim3(kRhtThreads), plds, s,
+                                   static_cast<const float*>(x), signs, mode, y, y_dtype, static_cast<int>(n), h, pl,
+                                   norm);
+            return hipGetLastError() == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+        }
+    }
+    const unsigned gx = h.m > 1 ? static_cast<unsigned>((h.m + per - 1) / per) : 1u;
     const dim3 grid(gx, static_cast<unsigned>(M));
     if (x_dtype == UNISVQ_F16)
         hipLaunchKernelGGL(rht_kernel<_Float16>, grid, dim3(kRhtThreads), lds, s, static_cast<const _Float16*>(x),

@@ -586,7 +586,12 @@ def test_quantize_ties_and_grid_points_on_gpu():
 
 # ------------------------------------------- randomized Hadamard transform
 
-@pytest.mark.parametrize("n", [256, 4096, 8192, 344, 688, 11008, 28672])
+# Sylvester sizes (256 in LDS passes, 2^10 .. 2^15 in registers and lanes), then Paley orders m = q + 1 with blocks of 2^k: q prime
+# (12, 24, 44, and 284 with a digit above 255), q = 3^3 (28, 28672), q = 7^3 (344 .. 11008, blocks of 1 to 32),
+# q = 11^3 (1332) on the matrix-core factor, and q = 23^3 (12168), whose
+# tables do not fit the LDS, on the vector-ALU factor.
+@pytest.mark.parametrize("n", [256, 1024, 2048, 4096, 8192, 16384, 32768, 12, 24, 28, 44, 284, 344, 688, 1332, 2752, 5504, 11008, 12168,
+                               28672])
 @pytest.mark.parametrize("mode", ["in", "out"])
 def test_rht_matches_dense_oracle(n, mode):
     rng = np.random.default_rng(n + len(mode))
