@@ -35,27 +35,74 @@ namespace {
 constexpr int kRhtThreads = 1024;
 constexpr int kRhtMaxN = 32768;  // fp32 row in LDS
 
-// The row into LDS as fp32 (signs applied on the input side): eight
-// independent loads in flight per thread before their LDS writes.
+// Sign i through a buffer descriptor: reads past the end return zero, so the
+// load needs no guarding branch (a branch would make the wait counters drain
+// at its join).
+__device__ inline float ld_sign(__amdgpu_buffer_rsrc_t r, int i) {
+    return static_cast<float>(static_cast<signed char>(__builtin_amdgcn_raw_buffer_load_b8(r, static_cast<uint32_t>(i), 0, 0)));
+}
+
+// Eight consecutive elements of a row and their signs: raw bits from one or
+// two 16-byte loads and one 8-byte load (wide loads keep the address units'
+// work per element low; a row is read by every workgroup of a Paley launch).
+template <typename XT>
+struct RowChunk {
+    uint4 a, b;  // b used for fp32 only
+    uint2 s;
+};
+
+template <typename XT>
+__device__ inline void fetch_chunk(__amdgpu_buffer_rsrc_t rx, __amdgpu_buffer_rsrc_t rs, int i0, RowChunk<XT>& c) {
+    const uint32_t off = static_cast<uint32_t>(i0) * sizeof(XT);
+    c.a = ld128(rx, off);
+    if constexpr (sizeof(XT) == 4) c.b = ld128(rx, off + 16u);
+    c.s = ld64(rs, static_cast<uint32_t>(i0));
+}
+
+// The chunk's elements as fp32, times their signs on the input side (mode 0),
+// into z[i0 .. i0 + 8) where below n.
+template <typename XT>
+__device__ inline void put_chunk(const RowChunk<XT>& c, int i0, int n, int mode, float* z) {
+    float v[8];
+    if constexpr (sizeof(XT) == 4) {
+        const uint32_t w[8] = {c.a.x, c.a.y, c.a.z, c.a.w, c.b.x, c.b.y, c.b.z, c.b.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = __builtin_bit_cast(float, w[e]);
+    } else {
+        const uint32_t w[4] = {c.a.x, c.a.y, c.a.z, c.a.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            v[e] = static_cast<float>(__builtin_bit_cast(XT, static_cast<uint16_t>(w[e >> 1] >> (16 * (e & 1)))));
+    }
+    if (mode == 0) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const uint32_t sw = e < 4 ? c.s.x : c.s.y;
+            v[e] *= static_cast<float>(static_cast<signed char>((sw >> (8 * (e & 3))) & 0xffu));
+        }
+    }
+    if (i0 + 8 <= n) {
+        *reinterpret_cast<f32x4*>(z + i0) = f32x4{v[0], v[1], v[2], v[3]};
+        *reinterpret_cast<f32x4*>(z + i0 + 4) = f32x4{v[4], v[5], v[6], v[7]};
+    } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            if (i0 + e < n) z[i0 + e] = v[e];
+    }
+}
+
+// The row into LDS as fp32 (signs applied on the input side).
 template <typename XT>
 __device__ inline void load_row(const XT* __restrict__ xr, const signed char* __restrict__ signs, int mode, int n,
                                 float* z, int tid) {
-    constexpr int U = 8;
-    for (int i0 = tid; i0 < n; i0 += kRhtThreads * U) {
-        float v[U];
-        float sg[U];
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(xr, static_cast<uint32_t>(n) * sizeof(XT));
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(signs, static_cast<uint32_t>(n));
+    constexpr int C = kRhtMaxN / (8 * kRhtThreads);
+    RowChunk<XT> c[C];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int i = i0 + u * kRhtThreads;
-            v[u] = i < n ? static_cast<float>(xr[i]) : 0.f;
-            sg[u] = (mode == 0 && i < n) ? static_cast<float>(signs[i]) : 1.f;
-        }
+    for (int u = 0; u < C; ++u) fetch_chunk<XT>(rx, rs, 8 * (tid + u * kRhtThreads), c[u]);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int i = i0 + u * kRhtThreads;
-            if (i < n) z[i] = v[u] * sg[u];
-        }
-    }
+    for (int u = 0; u < C; ++u) put_chunk<XT>(c[u], 8 * (tid + u * kRhtThreads), n, mode, z);
 }
 
 // x mod p for |x| < 2^22 through the float reciprocal rp = 1/p: the quotient
@@ -377,8 +424,9 @@ struct PaleyPlan {
 __host__ __device__ inline size_t paley_lds_bytes(const HadSpec& h, int n, const PaleyPlan& pl) {
     const size_t half = size_t{1} << h.k;
     const size_t hp = pl.ntiles * 16;  // padded block width
-    size_t b = static_cast<size_t>(n) * 4;           // z
-    b += static_cast<size_t>(h.m) * 16 * 4;           // pcol [m][16]
+    const size_t mp = static_cast<size_t>(h.m + 3) / 4 * 4;  // rows padded to whole k steps
+    size_t b = mp * half * 4;                         // z, zero rows past m
+    b += mp * 16 * 4;                                 // pcol [mp][16]
     b += static_cast<size_t>(pl.cnt) * half * 4;      // w [cnt][half]
     if (pl.ksplit > 1) b += static_cast<size_t>(pl.ksplit) * pl.cnt * hp * 4;  // partials
     b += static_cast<size_t>(h.q) * 4 + h.q;          // digits, character
@@ -394,9 +442,10 @@ __global__ __launch_bounds__(kRhtThreads) void rht_paley_kernel(const XT* __rest
     const int half = 1 << h.k;
     const int m = h.m;
     const int hp = pl.ntiles * 16;
-    float* z = reinterpret_cast<float*>(smem);                 // [n]
-    float* pcol = z + n;                                        // [m][16]
-    float* w = pcol + m * 16;                                   // [cnt][half]
+    const int mp = (m + 3) & ~3;                                // rows padded to whole k steps
+    float* z = reinterpret_cast<float*>(smem);                 // [mp][half], zero rows past m
+    float* pcol = z + mp * half;                                // [mp][16], zero rows past m
+    float* w = pcol + mp * 16;                                  // [cnt][half]
     float* part = w + pl.cnt * half;                            // [ksplit][cnt][hp]
     int* dig = reinterpret_cast<int*>(part + (pl.ksplit > 1 ? pl.ksplit * pl.cnt * hp : 0));  // [q]
     signed char* chi = reinterpret_cast<signed char*>(dig + h.q);                              // [q]
@@ -410,18 +459,16 @@ __global__ __launch_bounds__(kRhtThreads) void rht_paley_kernel(const XT* __rest
     // 1. the row's loads go out first, raw into registers, and land while the
     //    digit and character tables are built; then the row goes to LDS
     //    (signs applied on the input side)
-    constexpr int R = kRhtMaxN / kRhtThreads;
-    XT xv[R];
-    signed char sv[R];
-    const XT* xr = x + row * n;
+    constexpr int C = kRhtMaxN / (8 * kRhtThreads);
+    RowChunk<XT> rc[C];
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + row * n, static_cast<uint32_t>(n) * sizeof(XT));
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(signs, static_cast<uint32_t>(n));
 #pragma unroll
-    for (int u = 0; u < R; ++u) {
-        const int i = tid + u * kRhtThreads;
-        if (i < n) {
-            xv[u] = xr[i];
-            sv[u] = mode == 0 ? signs[i] : 1;
-        }
-    }
+    for (int u = 0; u < C; ++u) fetch_chunk<XT>(rx, rs, 8 * (tid + u * kRhtThreads), rc[u]);
+    // output-side signs of this thread's (at most two) outputs
+    float so[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) so[u] = ld_sign(rs, jb0 * half + tid + u * kRhtThreads);
     for (int i = tid; i < h.q; i += kRhtThreads) {
         chi[i] = i == 0 ? 0 : -1;
         dig[i] = gf_packed(i, h.p, h.e);
@@ -429,43 +476,75 @@ __global__ __launch_bounds__(kRhtThreads) void rht_paley_kernel(const XT* __rest
     __syncthreads();
     for (int v = 1 + tid; v < h.q; v += kRhtThreads) chi[gf_square(v, h)] = 1;
 #pragma unroll
-    for (int u = 0; u < R; ++u) {
-        const int i = tid + u * kRhtThreads;
-        if (i < n) z[i] = static_cast<float>(xv[u]) * static_cast<float>(sv[u]);
-    }
+    for (int u = 0; u < C; ++u) put_chunk<XT>(rc[u], 8 * (tid + u * kRhtThreads), n, mode, z);
     __syncthreads();
-    // 2. pcol[im][jl] = P[im][jb0 + jl] (0 past the workgroup's blocks)
-    for (int t = tid; t < m * 16; t += kRhtThreads) {
+    // 2. pcol[im][jl] = P[im][jb0 + jl] (0 past the workgroup's blocks and
+    //    past row m-1); table reads clamped into range and the cases picked
+    //    by selects, so the loop body has no branch
+    for (int t = tid; t < mp * 16; t += kRhtThreads) {
         const int im = t >> 4, jl = t & 15;
         const int j = jb0 + jl;
-        float v = 0.f;
-        if (jl < cnt) {
-            if (im == 0)
-                v = 1.f;
-            else if (j == 0)
-                v = -1.f;
-            else if (im == j)
-                v = 1.f;
-            else
-                v = static_cast<float>(chi[gf_sub_index(dig[im - 1], dig[j - 1], h.p, h.e)]);
-        }
-        pcol[t] = v;
+        const int a = dig[min(max(im - 1, 0), h.q - 1)];
+        const int b = dig[min(max(j - 1, 0), h.q - 1)];
+        const float c = static_cast<float>(chi[gf_sub_index(a, b, h.p, h.e)]);
+        float v = im == j ? 1.f : (j == 0 ? -1.f : c);
+        v = im == 0 ? 1.f : v;
+        pcol[t] = (jl < cnt && im < m) ? v : 0.f;
     }
+    // zero rows of z past m
+    for (int i = n + tid; i < mp * half; i += kRhtThreads) z[i] = 0.f;
     __syncthreads();
-    // 3. the product: work item (column tile nt, k chunk kc)
+    // 3. the product.  Long blocks (fewer than 8 per workgroup, so at most
+    //    256 rows m) on the vector ALUs, one output per thread and pass, four
+    //    fma chains over the padded rows; otherwise on the matrix cores, one
+    //    work item (column tile nt, k chunk kc) per wavefront and pass.
     const int ksteps = (m + 3) >> 2;
     const int per = (ksteps + pl.ksplit - 1) / pl.ksplit;
     const int r16 = lane & 15, kk = lane >> 4;
-    for (int it = wave; it < pl.ntiles * pl.ksplit; it += kRhtThreads / 64) {
+    if (pl.cnt < 8) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int o = tid + u * kRhtThreads;
+            if (o < pl.cnt * half) {
+                const int jl = o >> h.k, i2 = o & (half - 1);
+                float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+                for (int im = 0; im < mp; im += 4) {
+                    a0 = __builtin_fmaf(pcol[im * 16 + jl], z[im * half + i2], a0);
+                    a1 = __builtin_fmaf(pcol[(im + 1) * 16 + jl], z[(im + 1) * half + i2], a1);
+                    a2 = __builtin_fmaf(pcol[(im + 2) * 16 + jl], z[(im + 2) * half + i2], a2);
+                    a3 = __builtin_fmaf(pcol[(im + 3) * 16 + jl], z[(im + 3) * half + i2], a3);
+                }
+                w[o] = (a0 + a1) + (a2 + a3);
+            }
+        }
+    }
+    for (int it = wave; pl.cnt >= 8 && it < pl.ntiles * pl.ksplit; it += kRhtThreads / 64) {
         const int nt = it % pl.ntiles, kc = it / pl.ntiles;
         const int s0 = kc * per, s1 = min(ksteps, s0 + per);
         const int col = 16 * nt + r16;
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        for (int s = s0; s < s1; ++s) {
-            const int im = 4 * s + kk;
-            const float a = im < m ? pcol[im * 16 + r16] : 0.f;
-            const float b = (im < m && col < half) ? z[im * half + col] : 0.f;
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+        // rows past m are zero in both tables; columns past the block
+        // (blocks under 16 wide) read a clamped column and are never stored
+        const int colc = min(col, half - 1);
+        const float* pa = pcol + (4 * s0 + kk) * 16 + r16;
+        const float* pb = z + (4 * s0 + kk) * half + colc;
+        int s = s0;
+        for (; s + 4 <= s1; s += 4) {
+            float a[4], b[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                a[u] = pa[64 * u];
+                b[u] = pb[4 * half * u];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u], b[u], acc, 0, 0, 0);
+            pa += 256;
+            pb += 16 * half;
+        }
+        for (; s < s1; ++s) {
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(*pa, *pb, acc, 0, 0, 0);
+            pa += 64;
+            pb += 4 * half;
         }
         // D lane (r16, kk), element e: block 4 kk + e, column col
 #pragma unroll
@@ -480,7 +559,7 @@ __global__ __launch_bounds__(kRhtThreads) void rht_paley_kernel(const XT* __rest
         }
     }
     __syncthreads();
-    if (pl.ksplit > 1) {
+    if (pl.cnt >= 8 && pl.ksplit > 1) {
         for (int o = tid; o < pl.cnt * half; o += kRhtThreads) {
             const int jl = o >> h.k, c = o & (half - 1);
             float s = part[jl * hp + c];
@@ -491,11 +570,13 @@ __global__ __launch_bounds__(kRhtThreads) void rht_paley_kernel(const XT* __rest
     }
     // 4. Sylvester factor inside each of this workgroup's blocks
     sylvester_blocks(w, cnt * half, h.k, tid);
-    for (int o = tid; o < cnt * half; o += kRhtThreads) {
-        const int j = jb0 * half + o;
-        float v = w[o] * norm;
-        if (mode == 1) v *= static_cast<float>(signs[j]);
-        store_out(y, row * n + j, v, y_dtype);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int o = tid + u * kRhtThreads;
+        if (o < cnt * half) {
+            const float v = w[o] * norm;
+            store_out(y, row * n + jb0 * half + o, mode == 1 ? v * so[u] : v, y_dtype);
+        }
     }
 }
 
@@ -606,7 +687,9 @@ static int launch_fwht(const void* x, int x_dtype, const signed char* signs, int
 // Output blocks per workgroup (at most 16, the matrix-core tile height, and
 // at most 512 outputs, so that long blocks spread over more workgroups),
 // 16-column tiles per block, and the k split that gives the 16 wavefronts
-// one (tile, k chunk) item each when there are fewer tiles.
+// one (tile, k chunk) item each when there are fewer tiles.  With fewer than
+// 8 blocks the matrix-core tile would be mostly idle and the kernel sums on
+// the vector ALUs instead.
 static PaleyPlan paley_plan(const HadSpec& h) {
     const int half = 1 << h.k;
     PaleyPlan pl;
@@ -657,7 +740,7 @@ int launch_rht(int64_t n, int64_t M, const void* x, int x_dtype, const signed ch
         // matrix-core Paley factor whenever its tables fit the LDS
         const PaleyPlan pl = paley_plan(h);
         const size_t plds = paley_lds_bytes(h, static_cast<int>(n), pl);
-        if (plds <= kRhtMaxLds) {
+        if (plds <= kRhtMaxLds && pl.cnt << h.k <= 2 * kRhtThreads) {  // at most two outputs per thread
             const dim3 pgrid(static_cast<unsigned>((h.m + pl.cnt - 1) / pl.cnt), static_cast<unsigned>(M));
             if (x_dtype == UNISVQ_F16)
                 hipLaunchKernelGGL(rht_paley_kernel<_Float16>, pgrid, dim3(kRhtThreads), plds, s,
