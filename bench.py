@@ -16,6 +16,7 @@ weights are never counted).
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -612,39 +613,59 @@ def main():
                 cc.append((K, M, xin, xcode, sV, xrot, arr, len(grp), N, ystk, sU, yout))
             rcalls.append(cc)
 
-        def rstep(i, sptr):
+        def rstep(i, sptr, fused):
             for (K, M_, xin, xc, sV, xrot, arr, cnt, N, ystk, sU, yout) in rcalls[i % copies]:
-                for st in (lib.unisvq_rht(K, M_, xin.data_ptr(), xc, sV.data_ptr(), 0, xrot.data_ptr(), u.F16, sptr),
-                           lib.unisvq_gemv_batched(arr, cnt, M_, u.F16, u.F16, sptr),
-                           lib.unisvq_rht(N, cnt * M_, ystk.data_ptr(), u.F16, sU.data_ptr(), 1, yout.data_ptr(),
-                                          u.F16, sptr)):
+                # fused where the launch has at most 3 row blocks per CU: beyond that
+                # the transform each workgroup repeats outweighs the saved launch
+                if fused and K in (4096, 8192) and N * cnt // 16 <= 768:
+                    # input transform inside the product launch: x enters unrotated
+                    farr = (u.GemvProblem * cnt)()
+                    for j in range(cnt):
+                        farr[j] = u.GemvProblem(arr[j].N, arr[j].K, arr[j].packed, xin.data_ptr(), arr[j].y)
+                    sg = (ctypes.c_void_p * cnt)(*([sV.data_ptr()] * cnt))
+                    calls_ = (lib.unisvq_gemv_rht_batched(farr, cnt, M_, xc, u.F16, sg, sptr),)
+                else:
+                    calls_ = (lib.unisvq_rht(K, M_, xin.data_ptr(), xc, sV.data_ptr(), 0, xrot.data_ptr(), u.F16,
+                                             sptr),
+                              lib.unisvq_gemv_batched(arr, cnt, M_, u.F16, u.F16, sptr))
+                calls_ += (lib.unisvq_rht(N, cnt * M_, ystk.data_ptr(), u.F16, sU.data_ptr(), 1, yout.data_ptr(),
+                                          u.F16, sptr),)
+                for st in calls_:
                     if st != 0:
                         raise RuntimeError(f"rotated step failed with status {st}")
 
-        for i in range(args.warmup):
-            rstep(i, stream.cuda_stream)
-        torch.cuda.synchronize()
-        g_r = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g_r):
-            cap = torch.cuda.current_stream().cuda_stream
-            for c in range(copies):
-                rstep(c, cap)
-        g_r.replay()
-        torch.cuda.synchronize()
-        reps = max(1, -(-args.steps // copies))
-        r0 = torch.cuda.Event(enable_timing=True)
-        r1 = torch.cuda.Event(enable_timing=True)
-        r0.record(stream)
-        for _ in range(reps):
+        def time_rotated(fused):
+            for i in range(args.warmup):
+                rstep(i, stream.cuda_stream, fused)
+            torch.cuda.synchronize()
+            g_r = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_r):
+                cap = torch.cuda.current_stream().cuda_stream
+                for c in range(copies):
+                    rstep(c, cap, fused)
             g_r.replay()
-        r1.record(stream)
-        torch.cuda.synchronize()
-        rms = r0.elapsed_time(r1) / (reps * copies)
+            torch.cuda.synchronize()
+            reps = max(1, -(-args.steps // copies))
+            r0 = torch.cuda.Event(enable_timing=True)
+            r1 = torch.cuda.Event(enable_timing=True)
+            r0.record(stream)
+            for _ in range(reps):
+                g_r.replay()
+            r1.record(stream)
+            torch.cuda.synchronize()
+            del g_r
+            return r0.elapsed_time(r1) / (reps * copies)
+
+        rms = time_rotated(False)
+        fms = time_rotated(True)
         rht = {"what": "decoder step of a layer quantised in the rotated basis: 4 input transforms, 4 batched "
                        "products, 4 output transforms (12 launches)",
                "ms_per_step": round(rms, 5), "over_plain_step": round(rms / ms_per_step, 3),
-               "GB_per_s": round(set_bytes / (rms * 1e-3) / 1e9, 1)}
-        del g_r
+               "GB_per_s": round(set_bytes / (rms * 1e-3) / 1e9, 1),
+               "fused": {"what": "the same step with the input transforms of the q+k+v and o launch groups "
+                                 "inside their products (unisvq_gemv_rht_batched; 10 launches)",
+                         "ms_per_step": round(fms, 5), "over_plain_step": round(fms / ms_per_step, 3),
+                         "GB_per_s": round(set_bytes / (fms * 1e-3) / 1e9, 1)}}
 
     # ---- per-launch breakdown: HIP events on the launch stream around each
     # launch.  A spin kernel first lets the host queue a chunk of launches ahead

@@ -412,6 +412,25 @@ int unisvq_ldlq(int64_t N, int64_t K, const float* W, const double* U, const uin
 int unisvq_rht(int64_t n, int64_t M, const void* x, int x_dtype, const int8_t* signs, int mode, void* y,
                int y_dtype, void* stream);
 
+/* The input side of a rotated layer fused into the decode-phase product
+ * (Eq. 5): y_i = ((x_i diag(signs_i)) H_K / sqrt(K)) W_rot,i^T for each
+ * problem of the batch, with the transformed activations computed inside the
+ * product's own launch (each workgroup transforms the rows in LDS while its
+ * first weight packets are in flight) instead of by a separate unisvq_rht
+ * call.  The transform follows unisvq_rht mode 0 with y_dtype = x_dtype and
+ * the same arithmetic, so the result equals unisvq_rht followed by
+ * unisvq_gemv_batched on its output bit for bit.  The output-side transform
+ * (U S_U) stays a separate unisvq_rht mode 1 call: it needs all N outputs.
+ *   problems  as unisvq_gemv_batched: packed format v1 weights (per (row,
+ *             group) pairs), x in the original basis; every K the same, 4096
+ *             or 8192 (UNISVQ_EUNSUP otherwise)
+ *   signs     HOST array of `count` device pointers, signs[i] = int8 [K] (+-1),
+ *             the input-side signs S_V of problem i
+ *   M         1..4; x_dtype F16 or BF16 (x' is rounded to it); y_dtype as
+ *             unisvq_gemv */
+int unisvq_gemv_rht_batched(const unisvq_gemv_problem* problems, int count, int64_t M, int x_dtype, int y_dtype,
+                            const int8_t* const* signs, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

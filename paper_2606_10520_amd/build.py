@@ -28,6 +28,7 @@ EXTRA_FLAGS = {
     "gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "skinny.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "gemv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "gemv_rht.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
 
 

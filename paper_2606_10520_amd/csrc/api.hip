@@ -138,6 +138,26 @@ int unisvq_gemv_batched(const unisvq_gemv_problem* problems, int count, int64_t 
     return unisvq::launch_gemv_batch(probs, count, M, x_dtype, y_dtype, static_cast<hipStream_t>(stream));
 }
 
+int unisvq_gemv_rht_batched(const unisvq_gemv_problem* problems, int count, int64_t M, int x_dtype, int y_dtype,
+                            const int8_t* const* signs, void* stream) {
+    if (!problems || count < 1 || !signs) return UNISVQ_EINVAL;
+    if (count > UNISVQ_MAX_BATCH) return UNISVQ_EUNSUP;
+    unisvq::GemvProblem probs[UNISVQ_MAX_BATCH];
+    const signed char* sg[UNISVQ_MAX_BATCH];
+    for (int i = 0; i < count; ++i) {
+        const unisvq_gemv_problem& q = problems[i];
+        const int st = check_product(q.N, q.K, q.packed, M, q.x, x_dtype, q.y, y_dtype);
+        if (st != UNISVQ_OK) return st;
+        if (!signs[i]) return UNISVQ_EINVAL;
+        if (q.K != problems[0].K || (q.K != 4096 && q.K != 8192)) return UNISVQ_EUNSUP;
+        probs[i] = unisvq::GemvProblem{static_cast<const uint8_t*>(q.packed), q.x, q.y,
+                                       static_cast<int>(q.N), static_cast<int>(q.K), 0};
+        sg[i] = reinterpret_cast<const signed char*>(signs[i]);
+    }
+    if (M > 4) return UNISVQ_EUNSUP;
+    return unisvq::launch_gemv_rht_batch(probs, count, M, x_dtype, y_dtype, sg, static_cast<hipStream_t>(stream));
+}
+
 size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype) {
     if (!shape_ok(N, K) || M < 1 || M > (int64_t{1} << 31) - 1 || !x_dtype_ok(x_dtype)) return 0;
     return unisvq::gemm_workspace_bytes(N, K, M, x_dtype);

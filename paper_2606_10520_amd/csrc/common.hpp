@@ -151,6 +151,8 @@ int launch_gemv(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const vo
                 int x_dtype, void* y, int y_dtype, hipStream_t s);
 // The same for variant weights (every problem with `bits`-bit codes and
 // d-dimensional vectors, codes-only with its shared affine block).
+int launch_gemv_rht_batch(const GemvProblem* probs, int count, int64_t M, int x_dtype, int y_dtype,
+                          const signed char* const* signs, hipStream_t s);
 int launch_gemv_var_batch(const GemvProblem* probs, int count, int64_t M, int x_dtype, int y_dtype, int bits, int d,
                           hipStream_t s);
 // Prefill path.  Device workspace (16-byte aligned) of

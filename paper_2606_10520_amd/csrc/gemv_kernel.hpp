@@ -44,6 +44,7 @@
 #include <atomic>
 
 #include "common.hpp"
+#include "fwht.hpp"
 
 namespace unisvq {
 
@@ -189,6 +190,10 @@ struct GemvBatch {
     int count;
     int M;
     int y_dtype;
+    // fused input transform (RHT launches only): the signs S_V of each
+    // problem and 1/sqrt(K)
+    const signed char* signs[kMaxBatch];
+    float rht_norm;
 };
 
 namespace {
@@ -439,17 +444,106 @@ __device__ inline void var_packet_step(const LanePacket<BITS, D>& pk, int P, con
     }
 }
 
+// LDS of the matrix-vector kernel: staged operands xs [M][packets][64],
+// per-group sums xbar [M][packets][16], the cross-wavefront sums red
+// [waves][mt][16]; with the fused transform also the transformed rows
+// xt [M][K] (activation type) and the transform's exchange buffer z [K] (fp32),
+// which starts at offset 0 over xs (dead until the staging writes it) and,
+// for a single row, xt too.
+__host__ __device__ inline size_t gemv_lds_bytes(int K, int M, int waves, int mt) {
+    const size_t packets = (K / kGroup + 1) / 2;
+    return static_cast<size_t>(M) * packets * (kXsPacketBytes + kXbarPacketBytes) +
+           static_cast<size_t>(waves) * mt * 16 * 4;
+}
+__host__ __device__ inline size_t gemv_rht_xt_offset(int K, int M, int waves, int mt) {
+    return (gemv_lds_bytes(K, M, waves, mt) + 15) / 16 * 16;
+}
+__host__ __device__ inline size_t gemv_rht_z_offset(int K, int M, int waves, int mt) {
+    // one row: z may overlap xt as well (the row's x' is written after the
+    // last read of z); several rows: the next row's z must not overwrite x'
+    if (M == 1) return 0;
+    const size_t base = gemv_lds_bytes(K, M, waves, mt);
+    return static_cast<size_t>(K) * 4 <= base ? 0 : gemv_rht_xt_offset(K, M, waves, mt) + static_cast<size_t>(M) * K * 2;
+}
+__host__ __device__ inline size_t gemv_rht_lds_bytes(int K, int M, int waves, int mt) {
+    const size_t zo = gemv_rht_z_offset(K, M, waves, mt);
+    const size_t end_xt = gemv_rht_xt_offset(K, M, waves, mt) + static_cast<size_t>(M) * K * 2;
+    const size_t end_z = zo + static_cast<size_t>(K) * 4;
+    return end_xt > end_z ? end_xt : end_z;
+}
+
+// The input-side transform of M <= MT rows of K = 2^KLOG elements on eight
+// wavefronts (512 threads; in a sixteen-wavefront workgroup the other eight
+// wait at the barriers), with the thread layout and the butterfly order of
+// the standalone transform for the same K (W = 3 wavefront bits, KLOG - 9
+// register bits), so x' is the same to the bit: registers hold elements
+// lane | wave << 6 | r << 9, their register and lane bits are done there,
+// one exchange through z puts the wavefront bits into registers, and x' * norm
+// rounded to XT goes to xt[t][..].  xraw: the raw 16-bit activations, sraw:
+// the signs, both loaded by the caller.
+template <typename XT, int KLOG, int MT>
+__device__ inline void rht_prologue(const uint32_t (&xraw)[MT][1 << (KLOG - 9)], const float (&sraw)[1 << (KLOG - 9)],
+                                    int M, int lane, int wave, float norm, float* z, XT* xt) {
+    constexpr int LR = KLOG - 9, R = 1 << LR, K = 1 << KLOG;
+    const bool tw = wave < 8;  // a sixteen-wavefront workgroup's upper half only passes the barriers
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+        if (t < M) {  // uniform
+            float v[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                v[r] = static_cast<float>(__builtin_bit_cast(XT, static_cast<uint16_t>(xraw[t][r]))) * sraw[r];
+            reg_stages<R, 0, LR>(v);
+            lane_stage<R, 1>(v, lane);
+            lane_stage<R, 2>(v, lane);
+            lane_stage<R, 4>(v, lane);
+            lane_stage<R, 8>(v, lane);
+            lane_stage<R, 16>(v, lane);
+            lane_stage<R, 32>(v, lane);
+            if (t > 0) __syncthreads();  // z of the previous row fully read
+            if (tw) {
+#pragma unroll
+                for (int r = 0; r < R; ++r) z[lane | wave << 6 | r << 9] = v[r];
+            }
+            __syncthreads();
+            if (tw) {
+#pragma unroll
+                for (int r = 0; r < R; ++r) v[r] = z[lane | (r & 7) << 6 | (r >> 3) << 9 | wave << (6 + LR)];
+                reg_stages<R, 0, 3>(v);
+            }
+            __syncthreads();  // every read of z done: x' may overwrite it
+            if (tw) {
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    // x' * norm rounded to fp32 first, as the standalone
+                    // transform does: the empty asm keeps the compiler from
+                    // fusing product and conversion into one mixed-precision
+                    // instruction that would round only once
+                    float p = v[r] * norm;
+                    asm volatile("" : "+v"(p));
+                    xt[t * K + (lane | (r & 7) << 6 | (r >> 3) << 9 | wave << (6 + LR))] = static_cast<XT>(p);
+                }
+            }
+        }
+    }
+    __syncthreads();  // xt complete; z dead
+}
+
 // Template parameters: WAVES wavefronts per workgroup, MT the largest token
 // count, PF packets in flight per wavefront, NX activation load instructions
 // per wavefront (issued ahead of the packet loads), OCC the minimum
 // wavefronts per SIMD the register allocation must allow; SHARED: codes-only
 // weights with row-shared pairs; BITS, D: the code width and vector
 // dimension (anything but 2, 4 is a variant, always SHARED).
-template <typename XT, int WAVES, int MT, int PF, int NX, int OCC, bool SHARED, int BITS = 2, int D = 4>
+// RHTK > 0: the activations enter in the original basis and the workgroup
+// first applies the input-side transform x' = (x diag(s)) H / sqrt(K) of
+// Eq. 5 itself, K = 2^RHTK (see rht_prologue).
+template <typename XT, int WAVES, int MT, int PF, int NX, int OCC, bool SHARED, int BITS = 2, int D = 4, int RHTK = 0>
 __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch batch) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     constexpr bool kVar = BITS != 2 || D != 4;
     static_assert(!kVar || SHARED, "format variants keep their pairs in a shared block");
+    static_assert(RHTK == 0 || ((WAVES == 8 || WAVES == 16) && !kVar), "the fused transform runs on eight wavefronts");
 
     // problem of this workgroup (uniform scalar selection)
     const int bid = blockIdx.x;
@@ -458,6 +552,7 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
     void* y = batch.p[0].y;
     const uint8_t* affine = batch.p[0].affine;
     int N = batch.p[0].N, K = batch.p[0].K, rb0 = 0, affine_one = batch.p[0].affine_one;
+    const signed char* sgn = RHTK > 0 ? batch.signs[0] : nullptr;
 #pragma unroll
     for (int i = 1; i < kMaxBatch; ++i) {
         if (i < batch.count && bid >= batch.p[i].rb_begin) {
@@ -469,6 +564,7 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
             rb0 = batch.p[i].rb_begin;
             affine = batch.p[i].affine;
             affine_one = batch.p[i].affine_one;
+            if constexpr (RHTK > 0) sgn = batch.signs[i];
         }
     }
     const int M = batch.M;
@@ -512,8 +608,26 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
                                                            : kOutOfRange;
     };
     uint2 xr[NX];
+    constexpr int kRR = RHTK > 0 ? 1 << (RHTK - 9) : 1;  // transform elements per thread and token
+    uint32_t xraw[RHTK > 0 ? MT : 1][kRR];
+    float sraw[kRR];
+    if constexpr (RHTK > 0) {
+        // the whole rows, for the transform (element lane | wave << 6 | r << 9)
+        const __amdgpu_buffer_rsrc_t rsg = make_rsrc(sgn, static_cast<uint32_t>(K));
 #pragma unroll
-    for (int i = 0; i < NX; ++i) xr[i] = ld64(rx, x_off(i));
+        for (int r = 0; r < kRR; ++r) {
+            const int i = lane | wave << 6 | r << 9;
+            const bool tw = wave < 8;  // the transform's wavefronts
+#pragma unroll
+            for (int t = 0; t < MT; ++t)
+                xraw[t][r] = ld16(rx, t < M && tw ? (static_cast<uint32_t>(t) * K + i) * 2u : kOutOfRange);
+            sraw[r] = static_cast<float>(static_cast<signed char>(
+                __builtin_amdgcn_raw_buffer_load_b8(rsg, tw ? static_cast<uint32_t>(i) : kOutOfRange, 0, 0)));
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NX; ++i) xr[i] = ld64(rx, x_off(i));
+    }
     __builtin_amdgcn_sched_barrier(0);  // keep the activation loads ahead of the packet loads
 
     // 2. The first PF packets of this wavefront's run.  With row-shared pairs
@@ -575,16 +689,32 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
     // 3. Stage this wavefront's activations in operand order, with the
     //    per-group sums.  Only this wavefront reads them, so no workgroup
     //    barrier is needed -- LDS accesses of one wavefront complete in order.
-#pragma unroll
-    for (int i = 0; i < NX; ++i) {
-        if (i < loads_w) {
+    if constexpr (RHTK > 0) {
+        // the transformed rows x' (rounded to the activation type, as a
+        // standalone transform writing XT would) into LDS, then staged from there
+        XT* xt = reinterpret_cast<XT*>(smem + gemv_rht_xt_offset(K, M, WAVES, MT));
+        float* z = reinterpret_cast<float*>(smem + gemv_rht_z_offset(K, M, WAVES, MT));
+        rht_prologue<XT, RHTK, MT>(xraw, sraw, M, lane, wave, batch.rht_norm, z, xt);
+        for (int i = 0; i < loads_w; ++i) {
+            const uint32_t off = x_off(i);
+            const uint2 raw = off < kOutOfRange ? *reinterpret_cast<const uint2*>(
+                                                      reinterpret_cast<const unsigned char*>(xt) + off)
+                                                : uint2{0u, 0u};
             const int t = MT == 1 ? 0 : i / npw;
-            stage_packet<XT>(xr[i], t, pbeg + (i - t * npw), packets, lane, xs, xbar);
+            stage_packet<XT>(raw, t, pbeg + (i - t * npw), packets, lane, xs, xbar);
         }
-    }
-    for (int i = NX; i < loads_w; ++i) {  // more than NX loads: not overlapped with the packets
-        const int t = MT == 1 ? 0 : i / npw;
-        stage_packet<XT>(ld64(rx, x_off(i)), t, pbeg + (i - t * npw), packets, lane, xs, xbar);
+    } else {
+#pragma unroll
+        for (int i = 0; i < NX; ++i) {
+            if (i < loads_w) {
+                const int t = MT == 1 ? 0 : i / npw;
+                stage_packet<XT>(xr[i], t, pbeg + (i - t * npw), packets, lane, xs, xbar);
+            }
+        }
+        for (int i = NX; i < loads_w; ++i) {  // more than NX loads: not overlapped with the packets
+            const int t = MT == 1 ? 0 : i / npw;
+            stage_packet<XT>(ld64(rx, x_off(i)), t, pbeg + (i - t * npw), packets, lane, xs, xbar);
+        }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -685,11 +815,6 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
 
 constexpr size_t kMaxLds = 160 * 1024;
 
-size_t gemv_lds_bytes(int K, int M, int waves, int mt) {
-    const size_t packets = (K / kGroup + 1) / 2;
-    return static_cast<size_t>(M) * packets * (kXsPacketBytes + kXbarPacketBytes) +
-           static_cast<size_t>(waves) * mt * 16 * 4;
-}
 
 template <typename XT, bool SHARED, int WAVES, int MT, int PF, int NX, int BITS = 2, int D = 4>
 int launch_cfg(const GemvBatch& b, int blocks, int maxK, hipStream_t s) {

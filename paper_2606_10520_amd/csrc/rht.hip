@@ -22,6 +22,7 @@
 #include <cmath>
 
 #include "common.hpp"
+#include "fwht.hpp"
 
 namespace unisvq {
 
@@ -291,46 +292,6 @@ __global__ __launch_bounds__(kRhtThreads) void rht_kernel(const XT* __restrict__
 //            their butterflies, then the store straight from registers.
 // Every element takes one butterfly per index bit, (a, b) -> (a + b, a - b),
 // in fp32.
-
-template <int D>
-__device__ inline float lane_xor(float v, int lane) {
-    if constexpr (D == 1)
-        return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xf, 0xf, false));
-    else if constexpr (D == 2)
-        return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E, 0xf, 0xf, false));
-    else
-        return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((lane ^ D) << 2, __builtin_bit_cast(int, v)));
-}
-
-// Butterflies over register-index bit J (registers r and r | 1 << J).
-template <int R, int J>
-__device__ inline void reg_stage(float (&v)[R]) {
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        if (r & (1 << J)) continue;
-        const float a = v[r], b = v[r | (1 << J)];
-        v[r] = a + b;
-        v[r | (1 << J)] = a - b;
-    }
-}
-
-template <int R, int J0, int J1>
-__device__ inline void reg_stages(float (&v)[R]) {
-    if constexpr (J0 < J1) {
-        reg_stage<R, J0>(v);
-        reg_stages<R, J0 + 1, J1>(v);
-    }
-}
-
-template <int R, int D>
-__device__ inline void lane_stage(float (&v)[R], int lane) {
-    const bool hi = lane & D;
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const float p = lane_xor<D>(v[r], lane);
-        v[r] = hi ? p - v[r] : v[r] + p;
-    }
-}
 
 template <typename XT, int W, int LR>
 __global__ __launch_bounds__(64 << W) void fwht_kernel(const XT* __restrict__ x, const signed char* __restrict__ signs,

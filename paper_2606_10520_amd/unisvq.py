@@ -26,7 +26,8 @@ EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "uni
            "unisvq_unpack_shared", "unisvq_gemv_shared", "unisvq_gemv_shared_batched", "unisvq_gemm_shared",
            "unisvq_quantize", "unisvq_rht", "unisvq_var_codes_bytes", "unisvq_var_affine_bytes",
            "unisvq_var_pack", "unisvq_var_unpack", "unisvq_var_gemv", "unisvq_var_gemv_batched",
-           "unisvq_var_gemm_workspace_bytes", "unisvq_var_gemm", "unisvq_ldlq_workspace_bytes", "unisvq_ldlq")
+           "unisvq_var_gemm_workspace_bytes", "unisvq_var_gemm", "unisvq_ldlq_workspace_bytes", "unisvq_ldlq",
+           "unisvq_gemv_rht_batched")
 # format variants: (bits, d) pairs served by the unisvq_var_* entry points
 VARIANTS = ((3, 4), (2, 8), (3, 8))
 MAX_BATCH = 8
@@ -82,6 +83,9 @@ def load():
     lib.unisvq_gemv.restype = i32
     lib.unisvq_gemv_batched.argtypes = [ctypes.POINTER(GemvProblem), i32, i64, i32, i32, p]
     lib.unisvq_gemv_batched.restype = i32
+    lib.unisvq_gemv_rht_batched.argtypes = [ctypes.POINTER(GemvProblem), i32, i64, i32, i32,
+                                            ctypes.POINTER(ctypes.c_void_p), p]
+    lib.unisvq_gemv_rht_batched.restype = i32
     lib.unisvq_gemm_workspace_bytes.argtypes = [i64, i64, i64, i32]
     lib.unisvq_gemm_workspace_bytes.restype = sz
     lib.unisvq_gemm.argtypes = [i64, i64, p, i64, p, i32, p, i32, p, sz, p]
@@ -251,6 +255,42 @@ def gemv_batched(problems, out_dtype=None, stream=None):
         raise ValueError("all outputs need the same dtype")
     _check("unisvq_gemv_batched", load().unisvq_gemv_batched(arr, len(problems), M, _dtype_code(xdt),
                                                              _dtype_code(outs[0].dtype), _stream(stream)))
+    return outs
+
+
+def gemv_rht_batched(problems, out_dtype=None, stream=None):
+    """Decode products of a rotated layer with the input-side transform fused in
+    (Eq. 5): y_i = ((x_i diag(s_i)) H / sqrt(K)) W_rot,i^T.
+
+    problems: sequence of (packed, N, K, x, signs, out-or-None); x in the
+    original basis, signs int8 [K]; every K the same (4096 or 8192).
+    Returns the list of outputs."""
+    torch = _torch()
+    if not 1 <= len(problems) <= MAX_BATCH:
+        raise ValueError(f"1..{MAX_BATCH} problems per call")
+    arr = (GemvProblem * len(problems))()
+    sgn = (ctypes.c_void_p * len(problems))()
+    outs, M, xdt = [], None, None
+    for i, (packed, N, K, x, signs, out) in enumerate(problems):
+        _need_cuda(packed, x, signs, out)
+        x2 = x if x.dim() == 2 else x.reshape(-1, K)
+        if not x2.is_contiguous() or not signs.is_contiguous():
+            raise ValueError("x and signs must be contiguous")
+        if M is None:
+            M, xdt = x2.shape[0], x2.dtype
+        if x2.shape[0] != M or x2.dtype != xdt:
+            raise ValueError("all problems need the same token count and activation dtype")
+        if out is None:
+            out = torch.empty((M, N), dtype=out_dtype or xdt, device=x.device)
+        outs.append(out)
+        arr[i] = GemvProblem(N, K, packed.data_ptr(), x2.data_ptr(), out.data_ptr())
+        sgn[i] = signs.data_ptr()
+    ydt = {o.dtype for o in outs}
+    if len(ydt) != 1:
+        raise ValueError("all outputs need the same dtype")
+    _check("unisvq_gemv_rht_batched", load().unisvq_gemv_rht_batched(arr, len(problems), M, _dtype_code(xdt),
+                                                                     _dtype_code(outs[0].dtype), sgn,
+                                                                     _stream(stream)))
     return outs
 
 

@@ -118,6 +118,41 @@ def test_batched_validation():
     assert lib.unisvq_gemv_batched(arr(good), 1, 1, u.F32, u.F16, None) == EINVAL
 
 
+def test_rht_batched_validation():
+    """The fused input-transform product: descriptors as unisvq_gemv_batched,
+    plus one sign vector per problem and K = 4096 or 8192 for all of them."""
+    import ctypes
+    lib = u.load()
+    P = u.GemvProblem
+
+    def arr(*ps):
+        a = (P * len(ps))()
+        for i, q in enumerate(ps):
+            a[i] = q
+        return a
+
+    def sg(*ptrs):
+        a = (ctypes.c_void_p * len(ptrs))()
+        for i, v in enumerate(ptrs):
+            a[i] = v
+        return a
+
+    good = P(64, 4096, GOOD, GOOD, GOOD)
+    f = lib.unisvq_gemv_rht_batched
+    assert f(None, 1, 1, u.F16, u.F16, sg(GOOD), None) == EINVAL
+    assert f(arr(good), 1, 1, u.F16, u.F16, None, None) == EINVAL
+    assert f(arr(good, good), 2, 1, u.F16, u.F16, sg(GOOD, None), None) == EINVAL
+    assert f(arr(good), 0, 1, u.F16, u.F16, sg(GOOD), None) == EINVAL
+    assert f(arr(*[good] * 9), 9, 1, u.F16, u.F16, sg(*[GOOD] * 9), None) == EUNSUP
+    assert f(arr(P(64, 11008 // 128 * 128, GOOD, GOOD, GOOD)), 1, 1, u.F16, u.F16, sg(GOOD), None) == EUNSUP
+    assert f(arr(P(64, 2048, GOOD, GOOD, GOOD)), 1, 1, u.F16, u.F16, sg(GOOD), None) == EUNSUP
+    assert f(arr(good, P(64, 8192, GOOD, GOOD, GOOD)), 2, 1, u.F16, u.F16, sg(GOOD, GOOD), None) == EUNSUP
+    assert f(arr(good), 1, 5, u.F16, u.F16, sg(GOOD), None) == EUNSUP
+    assert f(arr(P(40, 4096, GOOD, GOOD, GOOD)), 1, 1, u.F16, u.F16, sg(GOOD), None) == ESHAPE
+    assert f(arr(P(64, 4096, GOOD + 4, GOOD, GOOD)), 1, 1, u.F16, u.F16, sg(GOOD), None) == EALIGN
+    assert f(arr(good), 1, 1, u.F32, u.F16, sg(GOOD), None) == EINVAL
+
+
 def test_gemm_workspace():
     lib = u.load()
     ws = lib.unisvq_gemm_workspace_bytes
