@@ -112,11 +112,19 @@ struct GemmState {
     int affine_one;
 };
 
+// Byte strides of the activation operands between 32-column slices: 64 in
+// the row-major [M][K] layout, 1024 in the tiled layout (TX) of the bf16
+// pre-pass, whose 1 KB tiles hold 16 tokens x 32 columns in the operand's
+// lane order; a group is four slices.
+template <bool TX>
+constexpr uint32_t kSliceBytes = TX ? 1024u : 64u;
+
 // Group g: products of buffer g & 1 (slices 0..3) while group g+1 is decoded
 // from `src` (its group jj) into the other buffer.
-template <int MI>
+template <int MI, bool TX = false>
 __device__ inline void group_step(const GemmState<MI>& st, int g, const Piece (&src)[2], int jj, f16x8 (&xq)[4][MI],
                                   f32x4 (&acc)[MI][kNI]) {
+    constexpr uint32_t SL = kSliceBytes<TX>;
     const _Float16* wsrc = st.wlane + (g & 1) * kWBuf;
     _Float16* const wdst[2] = {st.wrow[0] + ((g + 1) & 1) * kWBuf, st.wrow[1] + ((g + 1) & 1) * kWBuf};
     const bool decode_next = g + 1 < st.gend;
@@ -124,12 +132,12 @@ __device__ inline void group_step(const GemmState<MI>& st, int g, const Piece (&
     f16x8 wb[2][kNI];
     read_w(wsrc, wb[0]);
     // activation slices 2, 3 of this group, 0, 1 of the next (or nothing)
-    const uint32_t xoff = st.xbase + static_cast<uint32_t>(g) * 256u;
-    const uint32_t xn = decode_next ? xoff + 256u : kOutOfRange;
-    slice<MI, 0>(st.rx, xoff + 128u, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
-    slice<MI, 1>(st.rx, xoff + 192u, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
+    const uint32_t xoff = st.xbase + static_cast<uint32_t>(g) * (4 * SL);
+    const uint32_t xn = decode_next ? xoff + 4 * SL : kOutOfRange;
+    slice<MI, 0>(st.rx, xoff + 2 * SL, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
+    slice<MI, 1>(st.rx, xoff + 3 * SL, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
     slice<MI, 2>(st.rx, xn, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
-    slice<MI, 3>(st.rx, xn + 64u, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
+    slice<MI, 3>(st.rx, xn + SL, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
     __syncthreads();
 }
 
@@ -158,7 +166,8 @@ __device__ inline void group_step_var(const GemmState<MI>& st, int g, const VarP
 // for the matrix when affine_one, else one per group); the decode is the same.
 // BITS, D: code width and vector dimension; anything but 2, 4 is a format
 // variant (always SHARED, variant layout and records).
-template <int MI, bool SHARED, int BITS = 2, int D = 4>
+// TX: activations in the tiled layout of the bf16 pre-pass (2-bit d = 4 formats).
+template <int MI, bool SHARED, int BITS = 2, int D = 4, bool TX = false>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restrict__ packed,
                                                         const uint8_t* __restrict__ affine, int affine_one,
                                                         const _Float16* __restrict__ x,
@@ -190,7 +199,11 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     const int gb = sp * gps;
     const int gend = min(groups, gb + gps);
 
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(M) * K * 2u);
+    static_assert(!TX || !kVar, "the tiled activation layout serves the 2-bit d = 4 formats");
+    constexpr uint32_t SL = kSliceBytes<TX>;
+    // (the tiled layout pads the tokens to whole 16-token tiles with zeros)
+    const __amdgpu_buffer_rsrc_t rx =
+        make_rsrc(x, static_cast<uint32_t>(TX ? (M + 15) / 16 * 16 : M) * K * 2u);
     constexpr uint32_t kBlockBytes =
         kVar ? var_group_bytes(BITS) : (SHARED ? kCodeGroupBlockBytes : kGroupBlockBytes);
     constexpr uint32_t kRecBytes = kVar ? var_record_bytes(D) : kAffineRecordBytes;
@@ -230,7 +243,11 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     // column 128 g + 32 s + 8 kb.  Tokens past M read zeros.
     st.rx = rx;
     st.row_step = 16u * K * 2u;
-    st.xbase = (static_cast<uint32_t>(tok0 + (lane & 15)) * K + 8 * (lane >> 4)) * 2u;
+    // (tiled: tile (tok0 / 16, slice) at ((tok0 / 16) * (K / 32) + slice) * 1 KB,
+    // lane l's 16 bytes at 16 l; the next token tile is 16 * K * 2 bytes on,
+    // as in the row-major layout)
+    st.xbase = TX ? static_cast<uint32_t>(tok0 / 16) * static_cast<uint32_t>(K / 32) * 1024u + 16u * lane
+                  : (static_cast<uint32_t>(tok0 + (lane & 15)) * K + 8 * (lane >> 4)) * 2u;
     // Weight operand of tile n: row 16 n + lane % 16, same columns.
     st.wlane = wsh + (lane & 15) * kLdsRow + 8 * (lane >> 4);
 
@@ -275,8 +292,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
         }
     }
     f16x8 xq[4][MI];
-    load_x<MI>(rx, st.xbase + static_cast<uint32_t>(gb) * 256u, st.row_step, xq[0]);
-    load_x<MI>(rx, st.xbase + static_cast<uint32_t>(gb) * 256u + 64u, st.row_step, xq[1]);
+    load_x<MI>(rx, st.xbase + static_cast<uint32_t>(gb) * (4 * SL), st.row_step, xq[0]);
+    load_x<MI>(rx, st.xbase + static_cast<uint32_t>(gb) * (4 * SL) + SL, st.row_step, xq[1]);
     __syncthreads();
 
     int g = gb;
@@ -297,17 +314,17 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     } else {
         for (; g + 1 < gend; g += 2) {
             const int q = g >> 1;
-            group_step<MI>(st, g, pa, 1, xq, acc);  // decodes group 2q+1 (packet q)
+            group_step<MI, TX>(st, g, pa, 1, xq, acc);  // decodes group 2q+1 (packet q)
 #pragma unroll
             for (int r = 0; r < 2; ++r) load(rowblk[r], q + 2, pc[r]);
-            group_step<MI>(st, g + 1, pb, 0, xq, acc);  // decodes group 2q+2 (packet q+1)
+            group_step<MI, TX>(st, g + 1, pb, 0, xq, acc);  // decodes group 2q+2 (packet q+1)
 #pragma unroll
             for (int r = 0; r < 2; ++r) {
                 pa[r] = pb[r];
                 pb[r] = pc[r];
             }
         }
-        if (g < gend) group_step<MI>(st, g, pa, 1, xq, acc);  // last group (nothing left to decode)
+        if (g < gend) group_step<MI, TX>(st, g, pa, 1, xq, acc);  // last group (nothing left to decode)
     }
 
     // Epilogue.  D lane layout: output row 16 n + lane % 16, tokens
@@ -354,11 +371,25 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restr
 // bf16 activations -> fp16 with a power-of-two scale per token (see the top
 // of the file).  One workgroup per token row; the row is read once and held
 // in registers (CH chunks of 8 values per thread, CH * 2048 >= K).
-template <int CH>
-__global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restrict__ xb, int K,
+// TILED: the copy goes out in the tiled layout of the prefill kernel (1 KB
+// tiles of 16 tokens x 32 columns in the operand's lane order, chunk c of
+// token t at tile (t / 16, c / 4), lane t % 16 + 16 (c % 4)); the grid then
+// covers the tokens padded to whole tiles, and the padding rows are zeros.
+// The L2 merges the 16-byte pieces that the 16 rows of a tile write.
+template <int CH, bool TILED = false>
+__global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restrict__ xb, int K, int M,
                                                          _Float16* __restrict__ xh, float* __restrict__ inv_scale) {
     __shared__ float wmax[4];
-    const int t = blockIdx.x;
+    int t = blockIdx.x;
+    if constexpr (TILED) {
+        // Workgroups go to the 8 XCDs round-robin.  Renumber them so that the
+        // 16 rows of a token tile run on one XCD: its L2 then merges their
+        // 16-byte pieces into whole lines before anything goes out to HBM.
+        // Blocks of 8 tiles (128 tokens) are renumbered, the rest keep t = b.
+        const int b = t;
+        if (b < static_cast<int>(gridDim.x) / 128 * 128) t = 16 * (8 * ((b >> 3) >> 4) + (b & 7)) + ((b >> 3) & 15);
+    }
+    const bool real = !TILED || t < M;  // uniform
     const uint16_t* row = xb + static_cast<size_t>(t) * K;
     _Float16* out = xh + static_cast<size_t>(t) * K;
     const int chunks = K >> 3;  // 8 values per 16-byte chunk
@@ -368,7 +399,7 @@ __global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restr
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
         const int c = threadIdx.x + 256 * i;
-        v[i] = c < chunks ? *reinterpret_cast<const uint4*>(row + 8 * c) : uint4{0u, 0u, 0u, 0u};
+        v[i] = c < chunks && real ? *reinterpret_cast<const uint4*>(row + 8 * c) : uint4{0u, 0u, 0u, 0u};
         const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
 #pragma unroll
         for (int h = 0; h < 4; ++h) {
@@ -398,20 +429,26 @@ __global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restr
             o[2 * h] = static_cast<_Float16>(ldexpf(val(w[h] & 0xffffu), s));
             o[2 * h + 1] = static_cast<_Float16>(ldexpf(val(w[h] >> 16), s));
         }
-        *reinterpret_cast<f16x8*>(out + 8 * c) = o;
+        if constexpr (TILED)
+            *reinterpret_cast<f16x8*>(xh + (static_cast<size_t>(t >> 4) * (K >> 5) + (c >> 2)) * 512 +
+                                      8 * ((t & 15) + 16 * (c & 3))) = o;
+        else
+            *reinterpret_cast<f16x8*>(out + 8 * c) = o;
     }
-    if (threadIdx.x == 0) inv_scale[t] = ldexpf(1.0f, -s);
+    if (threadIdx.x == 0 && real) inv_scale[t] = ldexpf(1.0f, -s);
 }
 
-hipError_t launch_scale_rows(int64_t K, int64_t M, const uint16_t* x, _Float16* xh, float* inv, hipStream_t s) {
+template <bool TILED>
+hipError_t launch_scale(int64_t K, int64_t M, const uint16_t* x, _Float16* xh, float* inv, hipStream_t s) {
     const int64_t per = (K / 8 + 255) / 256;  // chunks per thread
-    const dim3 grid(static_cast<unsigned>(M)), block(256);
-    if (per <= 1) hipLaunchKernelGGL(scale_rows_kernel<1>, grid, block, 0, s, x, static_cast<int>(K), xh, inv);
-    else if (per <= 2) hipLaunchKernelGGL(scale_rows_kernel<2>, grid, block, 0, s, x, static_cast<int>(K), xh, inv);
-    else if (per <= 4) hipLaunchKernelGGL(scale_rows_kernel<4>, grid, block, 0, s, x, static_cast<int>(K), xh, inv);
-    else if (per <= 8) hipLaunchKernelGGL(scale_rows_kernel<8>, grid, block, 0, s, x, static_cast<int>(K), xh, inv);
-    else if (per <= 16) hipLaunchKernelGGL(scale_rows_kernel<16>, grid, block, 0, s, x, static_cast<int>(K), xh, inv);
-    else if (per <= 32) hipLaunchKernelGGL(scale_rows_kernel<32>, grid, block, 0, s, x, static_cast<int>(K), xh, inv);
+    const dim3 grid(static_cast<unsigned>(TILED ? (M + 15) / 16 * 16 : M)), block(256);
+    const int k = static_cast<int>(K), m = static_cast<int>(M);
+    if (per <= 1) hipLaunchKernelGGL((scale_rows_kernel<1, TILED>), grid, block, 0, s, x, k, m, xh, inv);
+    else if (per <= 2) hipLaunchKernelGGL((scale_rows_kernel<2, TILED>), grid, block, 0, s, x, k, m, xh, inv);
+    else if (per <= 4) hipLaunchKernelGGL((scale_rows_kernel<4, TILED>), grid, block, 0, s, x, k, m, xh, inv);
+    else if (per <= 8) hipLaunchKernelGGL((scale_rows_kernel<8, TILED>), grid, block, 0, s, x, k, m, xh, inv);
+    else if (per <= 16) hipLaunchKernelGGL((scale_rows_kernel<16, TILED>), grid, block, 0, s, x, k, m, xh, inv);
+    else if (per <= 32) hipLaunchKernelGGL((scale_rows_kernel<32, TILED>), grid, block, 0, s, x, k, m, xh, inv);
     else return hipErrorInvalidValue;  // K > 65536: not supported for bf16 activations
     return hipGetLastError();
 }
@@ -454,13 +491,13 @@ size_t partial_bytes(int64_t N, int64_t K, int64_t M) {
     return p.splits > 1 ? static_cast<size_t>(p.splits) * M * N * 4 : 0;
 }
 
-template <int MI, bool SHARED, int BITS = 2, int D = 4>
+template <int MI, bool SHARED, int BITS = 2, int D = 4, bool TX = false>
 hipError_t launch_tiles(const GemmPlan& p, int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine,
                         int affine_one, int64_t M, const _Float16* x, const float* inv_scale, void* y,
                         int y_dtype, float* partial, hipStream_t s) {
     if (p.splits > 1 && partial == nullptr) return hipErrorInvalidValue;  // never launch without the partials
     const unsigned blocks = static_cast<unsigned>(p.m_tiles) * p.n_tiles * p.splits;
-    hipLaunchKernelGGL((gemm_kernel<MI, SHARED, BITS, D>), dim3(blocks), dim3(kThreads), 0, s, packed, affine, affine_one,
+    hipLaunchKernelGGL((gemm_kernel<MI, SHARED, BITS, D, TX>), dim3(blocks), dim3(kThreads), 0, s, packed, affine, affine_one,
                        x, inv_scale, y,
                        static_cast<int>(N), static_cast<int>(K), static_cast<int>(M), y_dtype, p.m_tiles,
                        p.n_tiles, p.splits, p.gps, p.splits > 1 ? partial : nullptr);
@@ -477,7 +514,9 @@ hipError_t launch_tiles(const GemmPlan& p, int64_t N, int64_t K, const uint8_t* 
 
 size_t gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype) {
     size_t b = 0;
-    if (x_dtype == UNISVQ_BF16) b += align256(static_cast<size_t>(M) * K * 2) + align256(static_cast<size_t>(M) * 4);
+    // (above the small-batch range the fp16 copy is tiled: tokens padded to 16)
+    const int64_t mx = M > kSkinnyMaxM ? (M + 15) / 16 * 16 : M;
+    if (x_dtype == UNISVQ_BF16) b += align256(static_cast<size_t>(mx) * K * 2) + align256(static_cast<size_t>(M) * 4);
     return b + partial_bytes(N, K, M);
 }
 
@@ -510,13 +549,17 @@ int gemm_common(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affi
     const _Float16* xh = static_cast<const _Float16*>(x);
     const float* inv = nullptr;
     uint8_t* ws = static_cast<uint8_t*>(workspace);
+    // bf16 activations for the tiled kernel (2-bit d = 4, M above the
+    // small-batch range) go through the pre-pass that writes the tiled layout
+    const bool tiled = x_dtype == UNISVQ_BF16 && !var && M > kSkinnyMaxM;
     if (x_dtype == UNISVQ_BF16) {
         _Float16* wxh = reinterpret_cast<_Float16*>(ws);
-        ws += align256(static_cast<size_t>(M) * K * 2);
+        ws += align256(static_cast<size_t>(tiled ? (M + 15) / 16 * 16 : M) * K * 2);
         float* winv = reinterpret_cast<float*>(ws);
         ws += align256(static_cast<size_t>(M) * 4);
-        if (launch_scale_rows(K, M, static_cast<const uint16_t*>(x), wxh, winv, s) != hipSuccess)
-            return K > 65536 ? UNISVQ_EUNSUP : UNISVQ_EHIP;
+        const hipError_t e = tiled ? launch_scale<true>(K, M, static_cast<const uint16_t*>(x), wxh, winv, s)
+                                   : launch_scale<false>(K, M, static_cast<const uint16_t*>(x), wxh, winv, s);
+        if (e != hipSuccess) return K > 65536 ? UNISVQ_EUNSUP : UNISVQ_EHIP;
         xh = wxh;
         inv = winv;
     }
@@ -550,9 +593,19 @@ int gemm_common(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affi
             e = launch_tiles_var<3, 8>(p, N, K, packed, affine, affine_one, mc, xs, is, ys, y_dtype, partial, s);
         else if (var)
             return UNISVQ_EUNSUP;
+        else if (affine && tiled)
+            e = p.mi == 2 ? launch_tiles<2, true, 2, 4, true>(p, N, K, packed, affine, affine_one, mc, xs, is, ys,
+                                                              y_dtype, partial, s)
+                          : launch_tiles<1, true, 2, 4, true>(p, N, K, packed, affine, affine_one, mc, xs, is, ys,
+                                                              y_dtype, partial, s);
         else if (affine)
             e = p.mi == 2 ? launch_tiles<2, true>(p, N, K, packed, affine, affine_one, mc, xs, is, ys, y_dtype, partial, s)
                           : launch_tiles<1, true>(p, N, K, packed, affine, affine_one, mc, xs, is, ys, y_dtype, partial, s);
+        else if (tiled)
+            e = p.mi == 2 ? launch_tiles<2, false, 2, 4, true>(p, N, K, packed, nullptr, 0, mc, xs, is, ys, y_dtype,
+                                                               partial, s)
+                          : launch_tiles<1, false, 2, 4, true>(p, N, K, packed, nullptr, 0, mc, xs, is, ys, y_dtype,
+                                                               partial, s);
         else
             e = p.mi == 2 ? launch_tiles<2, false>(p, N, K, packed, nullptr, 0, mc, xs, is, ys, y_dtype, partial, s)
                           : launch_tiles<1, false>(p, N, K, packed, nullptr, 0, mc, xs, is, ys, y_dtype, partial, s);

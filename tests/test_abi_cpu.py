@@ -160,6 +160,8 @@ def test_gemm_workspace():
     # M = 2048 fills the GPU with output tiles, so there is no split along K
     assert ws(4096, 4096, 2048, u.BF16) == 2048 * 4096 * 2 + 2048 * 4
     assert ws(4096, 4096, 2048, u.F16) == 0
+    # above the small-batch range the fp16 copy is tiled (16-token tiles): 33 tokens take 48 rows
+    assert ws(64, 256, 33, u.BF16) == 48 * 256 * 2 + 256
     assert ws(16, 128, 1, u.BF16) == 256 + 256
     assert ws(16, 128, 1, u.F16) == 0
     assert ws(15, 128, 1, u.BF16) == 0
@@ -171,7 +173,8 @@ def test_gemm_workspace():
     assert ws(64, 1024, 33, u.F16) > 0
     split = ws(64, 1024, 100, u.F16)
     assert split > 0 and split % (100 * 64 * 4) == 0
-    assert ws(64, 1024, 100, u.BF16) == split + 100 * 1024 * 2 + 512
+    # (the bf16 pre-pass's fp16 copy for the tiled kernel: 100 tokens padded to 112)
+    assert ws(64, 1024, 100, u.BF16) == split + 112 * 1024 * 2 + 512
     # bf16 activations need it; so does a split product with fp16 activations
     need = ws(64, 256, 4, u.BF16)
     assert lib.unisvq_gemm(64, 256, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, None, need, None) == EWS
