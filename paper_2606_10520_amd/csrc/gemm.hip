@@ -371,25 +371,11 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restr
 // bf16 activations -> fp16 with a power-of-two scale per token (see the top
 // of the file).  One workgroup per token row; the row is read once and held
 // in registers (CH chunks of 8 values per thread, CH * 2048 >= K).
-// TILED: the copy goes out in the tiled layout of the prefill kernel (1 KB
-// tiles of 16 tokens x 32 columns in the operand's lane order, chunk c of
-// token t at tile (t / 16, c / 4), lane t % 16 + 16 (c % 4)); the grid then
-// covers the tokens padded to whole tiles, and the padding rows are zeros.
-// The L2 merges the 16-byte pieces that the 16 rows of a tile write.
-template <int CH, bool TILED = false>
-__global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restrict__ xb, int K, int M,
+template <int CH>
+__global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restrict__ xb, int K,
                                                          _Float16* __restrict__ xh, float* __restrict__ inv_scale) {
     __shared__ float wmax[4];
-    int t = blockIdx.x;
-    if constexpr (TILED) {
-        // Workgroups go to the 8 XCDs round-robin.  Renumber them so that the
-        // 16 rows of a token tile run on one XCD: its L2 then merges their
-        // 16-byte pieces into whole lines before anything goes out to HBM.
-        // Blocks of 8 tiles (128 tokens) are renumbered, the rest keep t = b.
-        const int b = t;
-        if (b < static_cast<int>(gridDim.x) / 128 * 128) t = 16 * (8 * ((b >> 3) >> 4) + (b & 7)) + ((b >> 3) & 15);
-    }
-    const bool real = !TILED || t < M;  // uniform
+    const int t = blockIdx.x;
     const uint16_t* row = xb + static_cast<size_t>(t) * K;
     _Float16* out = xh + static_cast<size_t>(t) * K;
     const int chunks = K >> 3;  // 8 values per 16-byte chunk
@@ -399,7 +385,7 @@ __global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restr
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
         const int c = threadIdx.x + 256 * i;
-        v[i] = c < chunks && real ? *reinterpret_cast<const uint4*>(row + 8 * c) : uint4{0u, 0u, 0u, 0u};
+        v[i] = c < chunks ? *reinterpret_cast<const uint4*>(row + 8 * c) : uint4{0u, 0u, 0u, 0u};
         const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
 #pragma unroll
         for (int h = 0; h < 4; ++h) {
@@ -429,27 +415,87 @@ __global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restr
             o[2 * h] = static_cast<_Float16>(ldexpf(val(w[h] & 0xffffu), s));
             o[2 * h + 1] = static_cast<_Float16>(ldexpf(val(w[h] >> 16), s));
         }
-        if constexpr (TILED)
-            *reinterpret_cast<f16x8*>(xh + (static_cast<size_t>(t >> 4) * (K >> 5) + (c >> 2)) * 512 +
-                                      8 * ((t & 15) + 16 * (c & 3))) = o;
-        else
-            *reinterpret_cast<f16x8*>(out + 8 * c) = o;
+        *reinterpret_cast<f16x8*>(out + 8 * c) = o;
     }
-    if (threadIdx.x == 0 && real) inv_scale[t] = ldexpf(1.0f, -s);
+    if (threadIdx.x == 0) inv_scale[t] = ldexpf(1.0f, -s);
+}
+
+// The same pre-pass writing the tiled layout of the prefill kernel: 1 KB
+// tiles of 16 tokens x 32 columns in the operand's lane order (chunk c of
+// token t at tile (t / 16, c / 4), lane t % 16 + 16 (c % 4)), tokens padded
+// to whole tiles with zero rows.  One workgroup per tile (16 wavefronts), so
+// that every store is one whole 1 KB tile: wavefront w converts the
+// 32-column slices w, w + 16, ...; lane l holds chunk l / 16 of the slice
+// for token l % 16, i.e. exactly its place in the tile.  The tile's rows are
+// read twice: once for the token maxima (over the four lanes that share a
+// row by lane shuffles, then over the 16 wavefronts in LDS), then again,
+// from the L2, for the conversion; nothing is held in registers, so any K.
+__global__ __launch_bounds__(1024) void scale_tiles_kernel(const uint16_t* __restrict__ xb, int K, int M,
+                                                           _Float16* __restrict__ xh, float* __restrict__ inv_scale) {
+    __shared__ float wmax[16][16];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int r = lane & 15, q = lane >> 4;
+    const int tile = blockIdx.x, t = 16 * tile + r;
+    const bool real = t < M;
+    const int slices = K >> 5;
+    const uint16_t* row = xb + static_cast<size_t>(real ? t : 0) * K + 8 * q;
+    auto val = [](uint32_t bits16) { return __builtin_bit_cast(float, bits16 << 16); };
+    float mx = 0.f;
+    if (real) {
+#pragma unroll 4
+        for (int sl = w; sl < slices; sl += 16) {
+            const uint4 v = *reinterpret_cast<const uint4*>(row + 32 * sl);
+            const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int h = 0; h < 4; ++h) mx = fmaxf(mx, fmaxf(fabsf(val(wd[h] & 0xffffu)), fabsf(val(wd[h] >> 16))));
+        }
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    if (q == 0) wmax[w][r] = mx;
+    __syncthreads();
+    mx = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) mx = fmaxf(mx, wmax[j][r]);
+    int s = 0;
+    if (mx > 0.f && mx <= 3.4e38f) {
+        int e;
+        frexpf(mx, &e);  // mx in [2^(e-1), 2^e)
+        s = min(max(15 - e, -126), 126);
+    }
+    _Float16* out = xh + static_cast<size_t>(tile) * slices * 512 + 8 * lane;
+#pragma unroll 4
+    for (int sl = w; sl < slices; sl += 16) {
+        const uint4 v = real ? *reinterpret_cast<const uint4*>(row + 32 * sl) : uint4{0u, 0u, 0u, 0u};
+        const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
+        f16x8 o;
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+            o[2 * h] = static_cast<_Float16>(ldexpf(val(wd[h] & 0xffffu), s));
+            o[2 * h + 1] = static_cast<_Float16>(ldexpf(val(wd[h] >> 16), s));
+        }
+        *reinterpret_cast<f16x8*>(out + static_cast<size_t>(sl) * 512) = o;
+    }
+    if (w == 0 && q == 0 && real) inv_scale[t] = ldexpf(1.0f, -s);
 }
 
 template <bool TILED>
 hipError_t launch_scale(int64_t K, int64_t M, const uint16_t* x, _Float16* xh, float* inv, hipStream_t s) {
+    if (K > 65536) return hipErrorInvalidValue;  // not supported for bf16 activations
+    const int k = static_cast<int>(K);
+    if (TILED) {
+        hipLaunchKernelGGL(scale_tiles_kernel, dim3(static_cast<unsigned>((M + 15) / 16)), dim3(1024), 0, s, x, k,
+                           static_cast<int>(M), xh, inv);
+        return hipGetLastError();
+    }
     const int64_t per = (K / 8 + 255) / 256;  // chunks per thread
-    const dim3 grid(static_cast<unsigned>(TILED ? (M + 15) / 16 * 16 : M)), block(256);
-    const int k = static_cast<int>(K), m = static_cast<int>(M);
-    if (per <= 1) hipLaunchKernelGGL((scale_rows_kernel<1, TILED>), grid, block, 0, s, x, k, m, xh, inv);
-    else if (per <= 2) hipLaunchKernelGGL((scale_rows_kernel<2, TILED>), grid, block, 0, s, x, k, m, xh, inv);
-    else if (per <= 4) hipLaunchKernelGGL((scale_rows_kernel<4, TILED>), grid, block, 0, s, x, k, m, xh, inv);
-    else if (per <= 8) hipLaunchKernelGGL((scale_rows_kernel<8, TILED>), grid, block, 0, s, x, k, m, xh, inv);
-    else if (per <= 16) hipLaunchKernelGGL((scale_rows_kernel<16, TILED>), grid, block, 0, s, x, k, m, xh, inv);
-    else if (per <= 32) hipLaunchKernelGGL((scale_rows_kernel<32, TILED>), grid, block, 0, s, x, k, m, xh, inv);
-    else return hipErrorInvalidValue;  // K > 65536: not supported for bf16 activations
+    const dim3 grid(static_cast<unsigned>(M)), block(256);
+    if (per <= 1) hipLaunchKernelGGL(scale_rows_kernel<1>, grid, block, 0, s, x, k, xh, inv);
+    else if (per <= 2) hipLaunchKernelGGL(scale_rows_kernel<2>, grid, block, 0, s, x, k, xh, inv);
+    else if (per <= 4) hipLaunchKernelGGL(scale_rows_kernel<4>, grid, block, 0, s, x, k, xh, inv);
+    else if (per <= 8) hipLaunchKernelGGL(scale_rows_kernel<8>, grid, block, 0, s, x, k, xh, inv);
+    else if (per <= 16) hipLaunchKernelGGL(scale_rows_kernel<16>, grid, block, 0, s, x, k, xh, inv);
+    else hipLaunchKernelGGL(scale_rows_kernel<32>, grid, block, 0, s, x, k, xh, inv);
     return hipGetLastError();
 }
 

@@ -151,6 +151,7 @@ def test_gemv_outlier_activations(M):
 
 @pytest.mark.parametrize("N,K,M", [
     (16, 128, 1), (64, 384, 63), (64, 256, 64), (80, 640, 65), (128, 1152, 130), (256, 4096, 7), (96, 512, 300),
+    (64, 6144, 40), (32, 16384, 48),
 ])
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
 def test_gemm_small_shapes_full_parity(N, K, M, dtype):
