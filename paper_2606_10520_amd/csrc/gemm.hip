@@ -423,19 +423,21 @@ __global__ __launch_bounds__(256) void scale_rows_kernel(const uint16_t* __restr
 // The same pre-pass writing the tiled layout of the prefill kernel: 1 KB
 // tiles of 16 tokens x 32 columns in the operand's lane order (chunk c of
 // token t at tile (t / 16, c / 4), lane t % 16 + 16 (c % 4)), tokens padded
-// to whole tiles with zero rows.  One workgroup per tile (16 wavefronts), so
-// that every store is one whole 1 KB tile: wavefront w converts the
-// 32-column slices w, w + 16, ...; lane l holds chunk l / 16 of the slice
-// for token l % 16, i.e. exactly its place in the tile.  The tile's rows are
-// read twice: once for the token maxima (over the four lanes that share a
-// row by lane shuffles, then over the 16 wavefronts in LDS), then again,
-// from the L2, for the conversion; nothing is held in registers, so any K.
+// to whole tiles with zero rows.  Tokens 0-7 of a tile fill its 128-byte
+// lines 0, 2, 4, 6 and tokens 8-15 lines 1, 3, 5, 7, so one workgroup (16
+// wavefronts) per half tile still stores whole lines: lane l handles token
+// l % 8 of the half, chunk (l / 8) % 4 of slice 2 (w + 16 i) + l / 32.  The
+// half tile's rows are read twice: once for the token maxima (over the eight
+// lanes that share a row by lane shuffles, then over the wavefronts in LDS),
+// then again, from the L2, for the conversion; nothing is held in
+// registers, so any K.
 __global__ __launch_bounds__(1024) void scale_tiles_kernel(const uint16_t* __restrict__ xb, int K, int M,
                                                            _Float16* __restrict__ xh, float* __restrict__ inv_scale) {
-    __shared__ float wmax[16][16];
+    __shared__ float wmax[16][8];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int r = lane & 15, q = lane >> 4;
-    const int tile = blockIdx.x, t = 16 * tile + r;
+    const int r = lane & 7, q = (lane >> 3) & 3, ps = lane >> 5;
+    const int tile = blockIdx.x >> 1, h = blockIdx.x & 1;
+    const int t = 16 * tile + 8 * h + r;
     const bool real = t < M;
     const int slices = K >> 5;
     const uint16_t* row = xb + static_cast<size_t>(real ? t : 0) * K + 8 * q;
@@ -443,16 +445,17 @@ __global__ __launch_bounds__(1024) void scale_tiles_kernel(const uint16_t* __res
     float mx = 0.f;
     if (real) {
 #pragma unroll 4
-        for (int sl = w; sl < slices; sl += 16) {
+        for (int sl = 2 * w + ps; sl < slices; sl += 32) {
             const uint4 v = *reinterpret_cast<const uint4*>(row + 32 * sl);
             const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-            for (int h = 0; h < 4; ++h) mx = fmaxf(mx, fmaxf(fabsf(val(wd[h] & 0xffffu)), fabsf(val(wd[h] >> 16))));
+            for (int e = 0; e < 4; ++e) mx = fmaxf(mx, fmaxf(fabsf(val(wd[e] & 0xffffu)), fabsf(val(wd[e] >> 16))));
         }
     }
+    mx = fmaxf(mx, __shfl_xor(mx, 8));
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    if (q == 0) wmax[w][r] = mx;
+    if (lane < 8) wmax[w][r] = mx;
     __syncthreads();
     mx = 0.f;
 #pragma unroll
@@ -463,20 +466,20 @@ __global__ __launch_bounds__(1024) void scale_tiles_kernel(const uint16_t* __res
         frexpf(mx, &e);  // mx in [2^(e-1), 2^e)
         s = min(max(15 - e, -126), 126);
     }
-    _Float16* out = xh + static_cast<size_t>(tile) * slices * 512 + 8 * lane;
+    _Float16* out = xh + static_cast<size_t>(tile) * slices * 512 + 8 * (8 * h + r + 16 * q);
 #pragma unroll 4
-    for (int sl = w; sl < slices; sl += 16) {
+    for (int sl = 2 * w + ps; sl < slices; sl += 32) {
         const uint4 v = real ? *reinterpret_cast<const uint4*>(row + 32 * sl) : uint4{0u, 0u, 0u, 0u};
         const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
         f16x8 o;
 #pragma unroll
-        for (int h = 0; h < 4; ++h) {
-            o[2 * h] = static_cast<_Float16>(ldexpf(val(wd[h] & 0xffffu), s));
-            o[2 * h + 1] = static_cast<_Float16>(ldexpf(val(wd[h] >> 16), s));
+        for (int e = 0; e < 4; ++e) {
+            o[2 * e] = static_cast<_Float16>(ldexpf(val(wd[e] & 0xffffu), s));
+            o[2 * e + 1] = static_cast<_Float16>(ldexpf(val(wd[e] >> 16), s));
         }
         *reinterpret_cast<f16x8*>(out + static_cast<size_t>(sl) * 512) = o;
     }
-    if (w == 0 && q == 0 && real) inv_scale[t] = ldexpf(1.0f, -s);
+    if (w == 0 && lane < 8 && real) inv_scale[t] = ldexpf(1.0f, -s);
 }
 
 template <bool TILED>
@@ -484,7 +487,7 @@ hipError_t launch_scale(int64_t K, int64_t M, const uint16_t* x, _Float16* xh, f
     if (K > 65536) return hipErrorInvalidValue;  // not supported for bf16 activations
     const int k = static_cast<int>(K);
     if (TILED) {
-        hipLaunchKernelGGL(scale_tiles_kernel, dim3(static_cast<unsigned>((M + 15) / 16)), dim3(1024), 0, s, x, k,
+        hipLaunchKernelGGL(scale_tiles_kernel, dim3(static_cast<unsigned>((M + 15) / 16 * 2)), dim3(1024), 0, s, x, k,
                            static_cast<int>(M), xh, inv);
         return hipGetLastError();
     }
