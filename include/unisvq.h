@@ -205,8 +205,10 @@ int unisvq_gemv_batched(const unisvq_gemv_problem* problems, int count, int64_t 
                         int y_dtype, void* stream);
 
 /* Device workspace unisvq_gemm needs for this product, in bytes (0: none):
- * for BF16 activations an fp16 copy of x (M*K*2 bytes, rounded up to 256)
- * and one fp32 scale per token (rounded up to 256); for products with too
+ * for BF16 activations an fp16 copy of x (M*K*2 bytes, rounded up to 256;
+ * above 32 tokens the copy is kept in 16-token tiles, so M counts rounded up
+ * to a multiple of 16) and one fp32 scale per token (rounded up to 256);
+ * for products with too
  * few output tiles to fill the GPU (small M), fp32 partial sums of a split
  * along K (splits*M*N*4 bytes).  0 also for an invalid shape, M < 1 or an
  * unknown x_dtype.  Host-only, no GPU needed. */
