@@ -63,6 +63,9 @@ def parse():
                    choices=["llama7b_decode_m1", "layer4096_m1", "llama70b_decode_m1",
                             "llama70b_decode_m16", "llama7b_smallbatch_m4", "llama7b_smallbatch_m16",
                             "llama7b_smallbatch_m64", "llama7b_prefill_m2048", "quantize_llama7b", "ldlq_layer4096"])
+    p.add_argument("--fold", action="store_true",
+                   help="with --affine matrix/group and a GEMM workload: the Eq. 9 fold "
+                        "(unisvq_gemm_shared_fold) instead of the decode path")
     p.add_argument("--affine", default="row_group", choices=["row_group", "matrix", "group"],
                    help="row_group: one (A, B) pair per (row, 128-column group), stored with the codes (the "
                         "default workload); matrix: one pair per weight matrix shared by all rows (the paper's "
@@ -391,7 +394,7 @@ def main():
     if var and args.affine == "row_group":
         args.affine = "matrix"  # the variants keep their pairs shared by the rows
     shared = args.affine != "row_group"
-    wname = args.workload if not shared else f"{args.workload}_{args.affine}_shared"
+    wname = args.workload if not shared else f"{args.workload}_{args.affine}_shared" + ("_fold" if args.fold else "")
     if var:
         wname += f"_b{bits}d{dim}"
 
@@ -444,6 +447,8 @@ def main():
     if kernel == "gemm":
         wsf = u.var_gemm_workspace_bytes if var else u.gemm_workspace_bytes
         ws_bytes = max(wsf(L.N, L.K, M, tdt) for L in layers)
+    if args.fold and shared and kernel == "gemm":
+        ws_bytes = max(ws_bytes, max(u.gemm_fold_workspace_bytes(L.N, L.K, M) for L in layers))
     ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
     names = [L.name for L in layers]
     full_set = {"q", "k", "v", "o", "gate", "up", "down"} <= set(names)
@@ -498,6 +503,9 @@ def main():
             if kernel == "gemv":
                 return lib.unisvq_gemv_shared(L.N, L.K, ga, pc.data_ptr(), pa.data_ptr(), M, x.data_ptr(), xcode,
                                               y.data_ptr(), u.F16, sptr)
+            if args.fold:
+                return lib.unisvq_gemm_shared_fold(L.N, L.K, ga, pc.data_ptr(), pa.data_ptr(), M, x.data_ptr(),
+                                                   xcode, y.data_ptr(), u.F16, ws.data_ptr(), ws_bytes, sptr)
             return lib.unisvq_gemm_shared(L.N, L.K, ga, pc.data_ptr(), pa.data_ptr(), M, x.data_ptr(), xcode,
                                           y.data_ptr(), u.F16, ws.data_ptr(), ws_bytes, sptr)
         if shared:

@@ -288,6 +288,34 @@ int unisvq_gemm_shared(int64_t N, int64_t K, int64_t affine_groups, const void* 
                        const void* packed_affine, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
                        void* workspace, size_t workspace_bytes, void* stream);
 
+/* Device workspace unisvq_gemm_shared_fold needs, in bytes: the folded
+ * activations in fp16 (16-token tiles: M rounded up to a multiple of 16,
+ * times K*2, rounded up to 256), one fp32 scale and one fp32 bias term per
+ * token (each array rounded up to 256), and the fp32 partial sums when the
+ * product is split along K (small M).  0 for an invalid shape or M < 1.
+ * Host-only. */
+size_t unisvq_gemm_fold_workspace_bytes(int64_t N, int64_t K, int64_t M);
+
+/* Prefill product with row-shared pairs computed through the fold of Eq. 9
+ * (Sec. 3.2.3): with A, B shared by the rows, y = sum_v (x_v A) q_v +
+ * sum_v x_v B, so a pre-pass forms x'_v = A^T x_v for every 4-column vector
+ * v of x (the pair of v's group; fp32 from the fp16 pair, then a per-token
+ * power-of-two scale into [2^14, 2^15) and one rounding to fp16) and the
+ * per-token bias term c = sum_v x_v . B (fp32, fixed summation order); the
+ * tiled kernel then multiplies x' by the bare 2-bit codes on the matrix cores
+ * (fp16 operands: the codes are exact, fp32 accumulation) and adds c.  No
+ * weight is ever decoded.  The result differs from unisvq_gemm_shared only
+ * in rounding (x' is rounded instead of the decoded weight).
+ *   Arguments as unisvq_gemm_shared; any M >= 1, x_dtype F16 or BF16,
+ *   y_dtype F16, BF16 or F32; (M rounded up to 16) * K * 2 must not exceed
+ *   2^31 - 1 bytes (UNISVQ_EUNSUP otherwise).
+ *   workspace  device, >= unisvq_gemm_fold_workspace_bytes(N, K, M) bytes,
+ *              16-byte aligned (UNISVQ_EWORKSPACE if missing or smaller,
+ *              UNISVQ_EALIGN if misaligned).  Overwritten; the caller owns it. */
+int unisvq_gemm_shared_fold(int64_t N, int64_t K, int64_t affine_groups, const void* packed_codes,
+                            const void* packed_affine, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
 /* ---- Format variants (variant codes-only format block above) ----
  * (b, d) = (3, 4), (2, 8) or (3, 8); any other pair is UNISVQ_EUNSUP (b = 2,
  * d = 4 uses the *_shared entry points). */

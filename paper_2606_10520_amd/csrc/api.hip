@@ -262,6 +262,24 @@ int unisvq_gemm_shared(int64_t N, int64_t K, int64_t affine_groups, const void* 
                                       x_dtype, y, y_dtype, workspace, static_cast<hipStream_t>(stream));
 }
 
+size_t unisvq_gemm_fold_workspace_bytes(int64_t N, int64_t K, int64_t M) {
+    if (!shape_ok(N, K) || M < 1) return 0;
+    return unisvq::gemm_fold_workspace_bytes(N, K, M);
+}
+
+int unisvq_gemm_shared_fold(int64_t N, int64_t K, int64_t affine_groups, const void* packed_codes,
+                            const void* packed_affine, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+    const int st = check_shared(N, K, affine_groups, packed_codes, packed_affine, M, x, x_dtype, y, y_dtype);
+    if (st != UNISVQ_OK) return st;
+    const size_t need = unisvq::gemm_fold_workspace_bytes(N, K, M);
+    if (!workspace || workspace_bytes < need) return UNISVQ_EWORKSPACE;
+    if (!aligned(workspace, 16)) return UNISVQ_EALIGN;
+    return unisvq::launch_gemm_fold(N, K, static_cast<const uint8_t*>(packed_codes),
+                                    static_cast<const uint8_t*>(packed_affine), affine_groups == 1 ? 1 : 0, M, x,
+                                    x_dtype, y, y_dtype, workspace, static_cast<hipStream_t>(stream));
+}
+
 /* ---- format variants ---- */
 
 size_t unisvq_var_codes_bytes(int64_t N, int64_t K, int bits, int d) {

@@ -166,6 +166,12 @@ int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const vo
 int launch_gemm_shared(int64_t N, int64_t K, const uint8_t* packed_codes, const uint8_t* affine,
                        int affine_one, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
                        void* workspace, hipStream_t s);
+// Eq. 9 fold with row-shared pairs (any M): a pre-pass multiplies the
+// activations by A and sums their bias terms, the tiled kernel multiplies by
+// the bare codes.  Workspace of gemm_fold_workspace_bytes(N, K, M) bytes.
+size_t gemm_fold_workspace_bytes(int64_t N, int64_t K, int64_t M);
+int launch_gemm_fold(int64_t N, int64_t K, const uint8_t* packed_codes, const uint8_t* affine, int affine_one,
+                     int64_t M, const void* x, int x_dtype, void* y, int y_dtype, void* workspace, hipStream_t s);
 // Variant weights: every M > 4 goes to the tiled kernel (K split for small
 // M), so the workspace differs from gemm_workspace_bytes.
 size_t gemm_var_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype);

@@ -94,6 +94,9 @@ struct DecOps {
 
 // Gather, for group 2p + jj, the codes of vectors 4n+j, row j of A and all
 // of B from the four slots of the quad.
+// CODES_ONLY (the Eq. 9 fold, where A and B act on the activations): the
+// codes alone.
+template <bool CODES_ONLY = false>
 __device__ inline void prepare(const Piece& pc, int j, int jj, DecOps& d) {
     const uint32_t cl = jj ? pc.c.z : pc.c.x, ch = jj ? pc.c.w : pc.c.y;
     const uint32_t al = jj ? pc.a.z : pc.a.x, ah = jj ? pc.a.w : pc.a.y;
@@ -109,6 +112,7 @@ __device__ inline void prepare(const Piece& pc, int j, int jj, DecOps& d) {
         d.p01[h] = m[0] | (m[1] << 4);
         d.p23[h] = m[2] | (m[3] << 4);
     }
+    if constexpr (CODES_ONLY) return;
     // row j of A: half (j & 1) of word (j >> 1) of every column b
     const uint32_t lo[4] = {quad_lane<0>(al), quad_lane<1>(al), quad_lane<2>(al), quad_lane<3>(al)};
     const uint32_t hi[4] = {quad_lane<0>(ah), quad_lane<1>(ah), quad_lane<2>(ah), quad_lane<3>(ah)};
@@ -127,11 +131,17 @@ __device__ inline void prepare(const Piece& pc, int j, int jj, DecOps& d) {
 
 // Vectors 4N .. 4N+3 of the row block: one matrix-core instruction; lane
 // (beta, j) stores vector 4N+j at dst + 16N + 4j (dst = the lane's row).
-template <int N>
+// CODES_ONLY: the four codes themselves (exact small integers in fp16) are
+// stored as the vector's weights.
+template <int N, bool CODES_ONLY = false>
 __device__ inline void decode_vecs(const DecOps& d, _Float16* dst, int j) {
     const f16x2 lo = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(d.p01[N >> 2], 2.0f, N & 3);
     const f16x2 hi = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(d.p23[N >> 2], 2.0f, N & 3);
     const f16x4 q = __builtin_shufflevector(lo, hi, 0, 1, 2, 3);
+    if constexpr (CODES_ONLY) {
+        *reinterpret_cast<f16x4*>(dst + 16 * N + 4 * j) = q;
+        return;
+    }
     const f32x4 w = __builtin_amdgcn_mfma_f32_4x4x4f16(d.arow, q, d.bvec, 0, 0, 0);
     f16x4 o;
 #pragma unroll

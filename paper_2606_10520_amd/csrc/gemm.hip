@@ -62,7 +62,7 @@ __device__ inline void load_x(__amdgpu_buffer_rsrc_t rx, uint32_t off, uint32_t 
 // One 32-column slice S of group g: prefetch activations two slices ahead
 // and weights one slice ahead, decode a quarter of the next group (from
 // pieces src, group jj of their packet), multiply.
-template <int MI, int S>
+template <int MI, int S, bool FOLD = false>
 __device__ inline void slice(__amdgpu_buffer_rsrc_t rx, uint32_t xnext, uint32_t row_step, f16x8 (&xq)[4][MI],
                              f16x8 (&wb)[2][kNI], const _Float16* wsrc, bool decode_next, const Piece (&src)[2],
                              int jj, DecOps (&ops)[2], int j, _Float16* const (&wdst)[2], f32x4 (&acc)[MI][kNI]) {
@@ -73,12 +73,12 @@ __device__ inline void slice(__amdgpu_buffer_rsrc_t rx, uint32_t xnext, uint32_t
     (void)decode_next;
     {
         constexpr int r = S >> 1;  // local row block of this wavefront
-        if ((S & 1) == 0) prepare(src[r], j, jj, ops[r]);
+        if ((S & 1) == 0) prepare<FOLD>(src[r], j, jj, ops[r]);
         constexpr int n0 = 4 * (S & 1);
-        decode_vecs<n0 + 0>(ops[r], wdst[r], j);
-        decode_vecs<n0 + 1>(ops[r], wdst[r], j);
-        decode_vecs<n0 + 2>(ops[r], wdst[r], j);
-        decode_vecs<n0 + 3>(ops[r], wdst[r], j);
+        decode_vecs<n0 + 0, FOLD>(ops[r], wdst[r], j);
+        decode_vecs<n0 + 1, FOLD>(ops[r], wdst[r], j);
+        decode_vecs<n0 + 2, FOLD>(ops[r], wdst[r], j);
+        decode_vecs<n0 + 3, FOLD>(ops[r], wdst[r], j);
     }
     mma<MI>(xq[S & 3], wb[S & 1], acc);
 }
@@ -121,7 +121,7 @@ constexpr uint32_t kSliceBytes = TX ? 1024u : 64u;
 
 // Group g: products of buffer g & 1 (slices 0..3) while group g+1 is decoded
 // from `src` (its group jj) into the other buffer.
-template <int MI, bool TX = false>
+template <int MI, bool TX = false, bool FOLD = false>
 __device__ inline void group_step(const GemmState<MI>& st, int g, const Piece (&src)[2], int jj, f16x8 (&xq)[4][MI],
                                   f32x4 (&acc)[MI][kNI]) {
     constexpr uint32_t SL = kSliceBytes<TX>;
@@ -134,10 +134,10 @@ __device__ inline void group_step(const GemmState<MI>& st, int g, const Piece (&
     // activation slices 2, 3 of this group, 0, 1 of the next (or nothing)
     const uint32_t xoff = st.xbase + static_cast<uint32_t>(g) * (4 * SL);
     const uint32_t xn = decode_next ? xoff + 4 * SL : kOutOfRange;
-    slice<MI, 0>(st.rx, xoff + 2 * SL, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
-    slice<MI, 1>(st.rx, xoff + 3 * SL, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
-    slice<MI, 2>(st.rx, xn, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
-    slice<MI, 3>(st.rx, xn + SL, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
+    slice<MI, 0, FOLD>(st.rx, xoff + 2 * SL, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
+    slice<MI, 1, FOLD>(st.rx, xoff + 3 * SL, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
+    slice<MI, 2, FOLD>(st.rx, xn, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
+    slice<MI, 3, FOLD>(st.rx, xn + SL, st.row_step, xq, wb, wsrc, decode_next, src, jj, ops, st.j, wdst, acc);
     __syncthreads();
 }
 
@@ -167,14 +167,19 @@ __device__ inline void group_step_var(const GemmState<MI>& st, int g, const VarP
 // BITS, D: code width and vector dimension; anything but 2, 4 is a format
 // variant (always SHARED, variant layout and records).
 // TX: activations in the tiled layout of the bf16 pre-pass (2-bit d = 4 formats).
-template <int MI, bool SHARED, int BITS = 2, int D = 4, bool TX = false>
+// FOLD (with SHARED and TX): the Eq. 9 fold -- the activations were already
+// multiplied by A (fold pre-pass), so the weights are the bare codes, and
+// the per-token bias term sum_v x_v . B is added in the epilogue.
+template <int MI, bool SHARED, int BITS = 2, int D = 4, bool TX = false, bool FOLD = false>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restrict__ packed,
                                                         const uint8_t* __restrict__ affine, int affine_one,
                                                         const _Float16* __restrict__ x,
                                                         const float* __restrict__ inv_scale, void* y, int N,
                                                         int K, int M, int y_dtype, int m_tiles, int n_tiles,
-                                                        int splits, int gps, float* __restrict__ partial) {
+                                                        int splits, int gps, float* __restrict__ partial,
+                                                        const float* __restrict__ bias) {
     __shared__ __attribute__((aligned(16))) _Float16 wsh[2 * kWBuf];
+    static_assert(!FOLD || (SHARED && TX && BITS == 2 && D == 4), "the fold runs on the tiled shared-pair kernel");
     constexpr int BM = kWaves * 16 * MI;
     constexpr bool kVar = BITS != 2 || D != 4;
     static_assert(!kVar || SHARED, "format variants keep their pairs in a shared block");
@@ -210,7 +215,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     const __amdgpu_buffer_rsrc_t rw =
         make_rsrc(packed, static_cast<uint32_t>(N / kRowBlock) * groups * kBlockBytes);
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(
-        affine, SHARED ? static_cast<uint32_t>(affine_one ? 1 : (groups + 1) / 2) * kRecBytes : 0u);
+        affine, SHARED && !FOLD ? static_cast<uint32_t>(affine_one ? 1 : (groups + 1) / 2) * kRecBytes : 0u);
+    // (FOLD: no pair is read -- the record loads fall outside the empty range)
     auto load = [&](uint32_t rowblk, int p, PieceT& pc) {
         if constexpr (kVar)
             load_packet_var<BITS>(rw, rowblk, p, gend, lane, pc);
@@ -280,15 +286,15 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
         DecOps ops;
 #pragma unroll
         for (int r = 0; r < 2; ++r) {
-            prepare(pa[r], st.j, 0, ops);
-            decode_vecs<0>(ops, st.wrow[r], st.j);
-            decode_vecs<1>(ops, st.wrow[r], st.j);
-            decode_vecs<2>(ops, st.wrow[r], st.j);
-            decode_vecs<3>(ops, st.wrow[r], st.j);
-            decode_vecs<4>(ops, st.wrow[r], st.j);
-            decode_vecs<5>(ops, st.wrow[r], st.j);
-            decode_vecs<6>(ops, st.wrow[r], st.j);
-            decode_vecs<7>(ops, st.wrow[r], st.j);
+            prepare<FOLD>(pa[r], st.j, 0, ops);
+            decode_vecs<0, FOLD>(ops, st.wrow[r], st.j);
+            decode_vecs<1, FOLD>(ops, st.wrow[r], st.j);
+            decode_vecs<2, FOLD>(ops, st.wrow[r], st.j);
+            decode_vecs<3, FOLD>(ops, st.wrow[r], st.j);
+            decode_vecs<4, FOLD>(ops, st.wrow[r], st.j);
+            decode_vecs<5, FOLD>(ops, st.wrow[r], st.j);
+            decode_vecs<6, FOLD>(ops, st.wrow[r], st.j);
+            decode_vecs<7, FOLD>(ops, st.wrow[r], st.j);
         }
     }
     f16x8 xq[4][MI];
@@ -314,17 +320,17 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     } else {
         for (; g + 1 < gend; g += 2) {
             const int q = g >> 1;
-            group_step<MI, TX>(st, g, pa, 1, xq, acc);  // decodes group 2q+1 (packet q)
+            group_step<MI, TX, FOLD>(st, g, pa, 1, xq, acc);  // decodes group 2q+1 (packet q)
 #pragma unroll
             for (int r = 0; r < 2; ++r) load(rowblk[r], q + 2, pc[r]);
-            group_step<MI, TX>(st, g + 1, pb, 0, xq, acc);  // decodes group 2q+2 (packet q+1)
+            group_step<MI, TX, FOLD>(st, g + 1, pb, 0, xq, acc);  // decodes group 2q+2 (packet q+1)
 #pragma unroll
             for (int r = 0; r < 2; ++r) {
                 pa[r] = pb[r];
                 pb[r] = pc[r];
             }
         }
-        if (g < gend) group_step<MI, TX>(st, g, pa, 1, xq, acc);  // last group (nothing left to decode)
+        if (g < gend) group_step<MI, TX, FOLD>(st, g, pa, 1, xq, acc);  // last group (nothing left to decode)
     }
 
     // Epilogue.  D lane layout: output row 16 n + lane % 16, tokens
@@ -337,6 +343,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
             const int t = tok0 + 16 * i + 4 * (lane >> 4) + e;
             if (t >= M) continue;
             const float sc = inv_scale ? inv_scale[t] : 1.0f;
+            const float bt = bias ? bias[t] : 0.0f;
 #pragma unroll
             for (int n = 0; n < kNI; ++n) {
                 const int row = n0 + 16 * n + (lane & 15);
@@ -344,7 +351,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
                 if (partial)
                     partial[(static_cast<int64_t>(sp) * M + t) * N + row] = acc[i][n][e];
                 else
-                    store_out(y, static_cast<int64_t>(t) * N + row, acc[i][n][e] * sc, y_dtype);
+                    store_out(y, static_cast<int64_t>(t) * N + row,
+                              bias ? acc[i][n][e] * sc + bt : acc[i][n][e] * sc, y_dtype);
             }
         }
     }
@@ -354,7 +362,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
 // outputs per thread (N is a multiple of 16).
 __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ partial, int splits, int M,
                                                             int N, const float* __restrict__ inv_scale, void* y,
-                                                            int y_dtype) {
+                                                            int y_dtype, const float* __restrict__ bias) {
     const int64_t total4 = static_cast<int64_t>(M) * N / 4;
     const int64_t i4 = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
     if (i4 >= total4) return;
@@ -364,6 +372,12 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restr
     const int64_t e0 = 4 * i4;
     const int t = static_cast<int>(e0 / N);
     const float sc = inv_scale ? inv_scale[t] : 1.0f;
+    if (bias) {
+        const float bt = bias[t];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) store_out(y, e0 + c, s[c] * sc + bt, y_dtype);
+        return;
+    }
 #pragma unroll
     for (int c = 0; c < 4; ++c) store_out(y, e0 + c, s[c] * sc, y_dtype);
 }
@@ -482,6 +496,118 @@ __global__ __launch_bounds__(1024) void scale_tiles_kernel(const uint16_t* __res
     if (w == 0 && lane < 8 && real) inv_scale[t] = ldexpf(1.0f, -s);
 }
 
+// The Eq. 9 fold for row-shared pairs, as a pre-pass of the tiled product:
+// for every vector v (four consecutive columns) of group g the activations
+// become x'_v = A_g^T x_v (x'_b = sum_a A[a][b] x_a, fp32 from the fp16
+// pair), scaled per token by a power of two 2^s so that the token's largest
+// |x'| lies in [2^14, 2^15), rounded to fp16 and written in the tiled layout;
+// the token's bias term c_t = sum_v x_v . B_g is summed in fp32 (in a fixed
+// order: per lane along its slices, lane shuffles, then the wavefronts).
+// The product then multiplies x' by the bare codes:
+//     y = 2^-s (x' Q^T) + c.
+// Same half-tile organisation and two reads of the rows as
+// scale_tiles_kernel; the pair of group g is read from its record (A column
+// b at 16 b + 8 (g % 2), B[a] at 64 + 4 a + 2 (g % 2); record 0 for one pair
+// per matrix).  BF16: x holds bf16 bits, else fp16.
+template <bool BF16>
+__global__ __launch_bounds__(1024) void fold_tiles_kernel(const uint16_t* __restrict__ xb, int K, int M,
+                                                          const uint8_t* __restrict__ affine, int affine_one,
+                                                          _Float16* __restrict__ xh, float* __restrict__ inv_scale,
+                                                          float* __restrict__ bias) {
+    __shared__ float wmax[16][8], wsum[16][8];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int r = lane & 7, q = (lane >> 3) & 3, ps = lane >> 5;
+    const int tile = blockIdx.x >> 1, h = blockIdx.x & 1;
+    const int t = 16 * tile + 8 * h + r;
+    const bool real = t < M;
+    const int slices = K >> 5;
+    const uint16_t* row = xb + static_cast<size_t>(real ? t : 0) * K + 8 * q;
+    auto val = [](uint32_t bits16) -> float {
+        if constexpr (BF16) return __builtin_bit_cast(float, bits16 << 16);
+        else return h2f(bits16);
+    };
+    // the lane's two vectors of slice sl: x' (8 values) and their part of c_t
+    auto fold = [&](int sl, float (&xp)[8], float& cs) {
+        const int g = sl >> 2;  // the same for both slices of a wavefront step
+        const uint8_t* rec = affine + static_cast<size_t>(affine_one ? 0 : g >> 1) * kAffineRecordBytes;
+        const int jj = g & 1;
+        float A[4][4], Bv[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const uint2 col = *reinterpret_cast<const uint2*>(rec + 16 * b + 8 * jj);
+            A[0][b] = h2f(col.x & 0xffffu);
+            A[1][b] = h2f(col.x >> 16);
+            A[2][b] = h2f(col.y & 0xffffu);
+            A[3][b] = h2f(col.y >> 16);
+        }
+#pragma unroll
+        for (int a = 0; a < 4; ++a) Bv[a] = h2f(*reinterpret_cast<const uint16_t*>(rec + kRecordBiasOff + 4 * a + 2 * jj));
+        const uint4 v = real ? *reinterpret_cast<const uint4*>(row + 32 * sl) : uint4{0u, 0u, 0u, 0u};
+        const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
+        float xv[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            xv[2 * e] = val(wd[e] & 0xffffu);
+            xv[2 * e + 1] = val(wd[e] >> 16);
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                float acc = 0.f;
+#pragma unroll
+                for (int a = 0; a < 4; ++a) acc = fmaf(A[a][b], xv[4 * u + a], acc);
+                xp[4 * u + b] = acc;
+            }
+#pragma unroll
+            for (int a = 0; a < 4; ++a) cs = fmaf(Bv[a], xv[4 * u + a], cs);
+        }
+    };
+    float mx = 0.f, cs = 0.f;
+    for (int sl = 2 * w + ps; sl < slices; sl += 32) {
+        float xp[8];
+        fold(sl, xp, cs);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, fabsf(xp[e]));
+    }
+#pragma unroll
+    for (int off = 8; off < 64; off <<= 1) {
+        mx = fmaxf(mx, __shfl_xor(mx, off));
+        cs += __shfl_xor(cs, off);
+    }
+    if (lane < 8) {
+        wmax[w][r] = mx;
+        wsum[w][r] = cs;
+    }
+    __syncthreads();
+    mx = 0.f;
+    cs = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        mx = fmaxf(mx, wmax[j][r]);
+        cs += wsum[j][r];
+    }
+    int s = 0;
+    if (mx > 0.f && mx <= 3.4e38f) {
+        int e;
+        frexpf(mx, &e);  // mx in [2^(e-1), 2^e)
+        s = min(max(15 - e, -126), 126);
+    }
+    _Float16* out = xh + static_cast<size_t>(tile) * slices * 512 + 8 * (8 * h + r + 16 * q);
+    for (int sl = 2 * w + ps; sl < slices; sl += 32) {
+        float xp[8], unused = 0.f;
+        fold(sl, xp, unused);
+        f16x8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = static_cast<_Float16>(ldexpf(xp[e], s));
+        *reinterpret_cast<f16x8*>(out + static_cast<size_t>(sl) * 512) = o;
+    }
+    if (w == 0 && lane < 8 && real) {
+        inv_scale[t] = ldexpf(1.0f, -s);
+        bias[t] = cs;
+    }
+}
+
 template <bool TILED>
 hipError_t launch_scale(int64_t K, int64_t M, const uint16_t* x, _Float16* xh, float* inv, hipStream_t s) {
     if (K > 65536) return hipErrorInvalidValue;  // not supported for bf16 activations
@@ -540,21 +666,21 @@ size_t partial_bytes(int64_t N, int64_t K, int64_t M) {
     return p.splits > 1 ? static_cast<size_t>(p.splits) * M * N * 4 : 0;
 }
 
-template <int MI, bool SHARED, int BITS = 2, int D = 4, bool TX = false>
+template <int MI, bool SHARED, int BITS = 2, int D = 4, bool TX = false, bool FOLD = false>
 hipError_t launch_tiles(const GemmPlan& p, int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine,
                         int affine_one, int64_t M, const _Float16* x, const float* inv_scale, void* y,
-                        int y_dtype, float* partial, hipStream_t s) {
+                        int y_dtype, float* partial, hipStream_t s, const float* bias = nullptr) {
     if (p.splits > 1 && partial == nullptr) return hipErrorInvalidValue;  // never launch without the partials
     const unsigned blocks = static_cast<unsigned>(p.m_tiles) * p.n_tiles * p.splits;
-    hipLaunchKernelGGL((gemm_kernel<MI, SHARED, BITS, D, TX>), dim3(blocks), dim3(kThreads), 0, s, packed, affine, affine_one,
+    hipLaunchKernelGGL((gemm_kernel<MI, SHARED, BITS, D, TX, FOLD>), dim3(blocks), dim3(kThreads), 0, s, packed, affine, affine_one,
                        x, inv_scale, y,
                        static_cast<int>(N), static_cast<int>(K), static_cast<int>(M), y_dtype, p.m_tiles,
-                       p.n_tiles, p.splits, p.gps, p.splits > 1 ? partial : nullptr);
+                       p.n_tiles, p.splits, p.gps, p.splits > 1 ? partial : nullptr, bias);
     if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
     if (p.splits > 1) {
         const int64_t total4 = M * N / 4;
         hipLaunchKernelGGL(reduce_splits_kernel, dim3(static_cast<unsigned>((total4 + 255) / 256)), dim3(256), 0, s,
-                           partial, p.splits, static_cast<int>(M), static_cast<int>(N), inv_scale, y, y_dtype);
+                           partial, p.splits, static_cast<int>(M), static_cast<int>(N), inv_scale, y, y_dtype, bias);
     }
     return hipGetLastError();
 }
@@ -674,6 +800,44 @@ int launch_gemm_shared(int64_t N, int64_t K, const uint8_t* packed_codes, const 
                        int affine_one, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
                        void* workspace, hipStream_t s) {
     return gemm_common(N, K, packed_codes, affine, affine_one, M, x, x_dtype, y, y_dtype, workspace, s);
+}
+
+// Eq. 9 fold (row-shared pairs, any M): workspace = the tiled x' copy
+// (tokens padded to 16), one scale and one bias term per token, and the
+// fp32 partials when the product is split along K.
+size_t gemm_fold_workspace_bytes(int64_t N, int64_t K, int64_t M) {
+    const GemmPlan p = plan_gemm(N, K, M);
+    const size_t part = p.splits > 1 ? static_cast<size_t>(p.splits) * M * N * 4 : 0;
+    return align256(static_cast<size_t>((M + 15) / 16 * 16) * K * 2) + 2 * align256(static_cast<size_t>(M) * 4) + part;
+}
+
+int launch_gemm_fold(int64_t N, int64_t K, const uint8_t* packed_codes, const uint8_t* affine, int affine_one,
+                     int64_t M, const void* x, int x_dtype, void* y, int y_dtype, void* workspace, hipStream_t s) {
+    const int64_t mpad = (M + 15) / 16 * 16;
+    if (mpad * K * 2 > kMaxBufferBytes) return UNISVQ_EUNSUP;  // one 32-bit addressed activation buffer
+    uint8_t* ws = static_cast<uint8_t*>(workspace);
+    _Float16* xh = reinterpret_cast<_Float16*>(ws);
+    ws += align256(static_cast<size_t>(mpad) * K * 2);
+    float* inv = reinterpret_cast<float*>(ws);
+    ws += align256(static_cast<size_t>(M) * 4);
+    float* bias = reinterpret_cast<float*>(ws);
+    ws += align256(static_cast<size_t>(M) * 4);
+    float* partial = reinterpret_cast<float*>(ws);
+    const dim3 grid(static_cast<unsigned>(mpad / 16 * 2)), block(1024);
+    const uint16_t* xb = static_cast<const uint16_t*>(x);
+    const int k = static_cast<int>(K), m = static_cast<int>(M);
+    if (x_dtype == UNISVQ_BF16)
+        hipLaunchKernelGGL(fold_tiles_kernel<true>, grid, block, 0, s, xb, k, m, affine, affine_one, xh, inv, bias);
+    else
+        hipLaunchKernelGGL(fold_tiles_kernel<false>, grid, block, 0, s, xb, k, m, affine, affine_one, xh, inv, bias);
+    if (hipGetLastError() != hipSuccess) return UNISVQ_EHIP;
+    const GemmPlan p = plan_gemm(N, K, M);
+    const hipError_t e =
+        p.mi == 2 ? launch_tiles<2, true, 2, 4, true, true>(p, N, K, packed_codes, affine, affine_one, M, xh, inv, y,
+                                                            y_dtype, partial, s, bias)
+                  : launch_tiles<1, true, 2, 4, true, true>(p, N, K, packed_codes, affine, affine_one, M, xh, inv, y,
+                                                            y_dtype, partial, s, bias);
+    return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
 }
 
 int launch_gemm_var(int64_t N, int64_t K, int bits, int d, const uint8_t* packed_codes, const uint8_t* affine,

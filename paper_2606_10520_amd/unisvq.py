@@ -24,6 +24,7 @@ EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "uni
            "unisvq_unpack", "unisvq_gemv", "unisvq_gemv_batched", "unisvq_gemm_workspace_bytes",
            "unisvq_gemm", "unisvq_codes_bytes", "unisvq_shared_affine_bytes", "unisvq_pack_shared",
            "unisvq_unpack_shared", "unisvq_gemv_shared", "unisvq_gemv_shared_batched", "unisvq_gemm_shared",
+           "unisvq_gemm_fold_workspace_bytes", "unisvq_gemm_shared_fold",
            "unisvq_quantize", "unisvq_rht", "unisvq_var_codes_bytes", "unisvq_var_affine_bytes",
            "unisvq_var_pack", "unisvq_var_unpack", "unisvq_var_gemv", "unisvq_var_gemv_batched",
            "unisvq_var_gemm_workspace_bytes", "unisvq_var_gemm", "unisvq_ldlq_workspace_bytes", "unisvq_ldlq",
@@ -104,6 +105,10 @@ def load():
     lib.unisvq_gemv_shared_batched.restype = i32
     lib.unisvq_gemm_shared.argtypes = [i64, i64, i64, p, p, i64, p, i32, p, i32, p, sz, p]
     lib.unisvq_gemm_shared.restype = i32
+    lib.unisvq_gemm_shared_fold.argtypes = lib.unisvq_gemm_shared.argtypes
+    lib.unisvq_gemm_shared_fold.restype = i32
+    lib.unisvq_gemm_fold_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.unisvq_gemm_fold_workspace_bytes.restype = sz
     lib.unisvq_quantize.argtypes = [i64, i64, p, p, p, i64, p, p]
     lib.unisvq_quantize.restype = i32
     lib.unisvq_rht.argtypes = [i64, i64, p, i32, p, i32, p, i32, p]
@@ -413,6 +418,23 @@ def gemm_shared(packed_codes, packed_affine, N: int, K: int, affine_groups: int,
         workspace = _torch().empty(need, dtype=_torch().uint8, device=x.device)
         ws_bytes = need
     return _shared_product("unisvq_gemm_shared", N, K, affine_groups, packed_codes, packed_affine, x, out,
+                           out_dtype, stream, extra=(_ptr(workspace), ws_bytes))
+
+
+def gemm_fold_workspace_bytes(N: int, K: int, M: int) -> int:
+    return int(load().unisvq_gemm_fold_workspace_bytes(N, K, M))
+
+
+def gemm_shared_fold(packed_codes, packed_affine, N: int, K: int, affine_groups: int, x, out=None,
+                     out_dtype=None, workspace=None, stream=None):
+    """Prefill product with row-shared pairs through the Eq. 9 fold (any M)."""
+    M = x.numel() // K
+    need = gemm_fold_workspace_bytes(N, K, M)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if workspace is None:
+        workspace = _torch().empty(max(need, 1), dtype=_torch().uint8, device=x.device)
+        ws_bytes = need
+    return _shared_product("unisvq_gemm_shared_fold", N, K, affine_groups, packed_codes, packed_affine, x, out,
                            out_dtype, stream, extra=(_ptr(workspace), ws_bytes))
 
 

@@ -385,3 +385,26 @@ def test_ldlq_validation():
     assert lib.unisvq_ldlq(16, 256, GOOD, GOOD, GOOD, GOOD, 0, GOOD, None, need, None) == EWS
     assert lib.unisvq_ldlq(16, 256, GOOD, GOOD, GOOD, GOOD, 0, GOOD, GOOD, need - 8, None) == EWS
     assert lib.unisvq_ldlq(16, 256, GOOD, GOOD, GOOD, GOOD, 0, GOOD, GOOD + 8, need, None) == EALIGN
+
+
+def test_fold_workspace_and_validation():
+    lib = u.load()
+    ws = lib.unisvq_gemm_fold_workspace_bytes
+    # M = 2048 at 4096 x 4096: no K split; tiled copy + scales + bias terms
+    assert ws(4096, 4096, 2048) == 2048 * 4096 * 2 + 2 * 2048 * 4
+    # 33 tokens take 48 rows of the tiled copy; the small product splits K
+    small = ws(64, 1024, 33)
+    assert small > 48 * 1024 * 2 + 2 * 256 and (small - 48 * 1024 * 2 - 2 * 256) % (33 * 64 * 4) == 0
+    assert ws(60, 1024, 1) == 0 and ws(64, 1000, 1) == 0 and ws(64, 1024, 0) == 0
+
+    def call(N=64, K=256, ga=1, M=4, xt=u.F16, wsp=GOOD, ws_bytes=1 << 20):
+        return lib.unisvq_gemm_shared_fold(N, K, ga, GOOD, GOOD, M, GOOD, xt, GOOD, u.F16, wsp, ws_bytes, None)
+
+    assert call(M=0) == EINVAL
+    assert call(ga=3) == EINVAL
+    assert call(xt=u.F32) == EINVAL
+    assert call(N=60) == ESHAPE
+    assert call(K=200) == ESHAPE
+    assert call(wsp=None) == EWS
+    assert call(ws_bytes=ws(64, 256, 4) - 1) == EWS
+    assert call(wsp=GOOD + 4) == EALIGN
