@@ -9,8 +9,8 @@
  *   point:   w_hat = A q + B,  A in R^{4x4}, B in R^4          (Sec. 3.1, Eq. 4)
  *   Vector i of a row covers input columns 4i..4i+3           (Sec. 3.2.3, Eq. 8)
  *   and the layer output is  Y = X W_hat^T                     (Sec. 2.1, Eq. 1)
- *   The affine map commutes with the matrix product (Sec. 3.1, Eq. 9), so the
- *   kernels never materialise W_hat in memory.
+ *   The affine map commutes with the matrix product (Sec. 3.1; Sec. 3.2.3,
+ *   Eq. 9), so the kernels never materialise W_hat in memory.
  *   Granularity: one (A, B) pair per (output row, group of 128 input
  *   columns), stored as fp16 -- 40 bytes per set (Sec. 3.1).  The paper's
  *   one-pair-per-matrix setting (Sec. 4.2) is the special case where all
@@ -26,8 +26,9 @@
  *     without a GPU).  A failed launch returns UNISVQ_EHIP.  Faults inside a
  *     kernel surface at the caller's next synchronisation.
  *   - Outputs are overwritten, never accumulated into.
- *   - Thread-safe: no global mutable state besides a once-per-process,
- *     per-device kernel attribute set-up.
+ *   - Thread-safe: no global mutable state besides the kernels' dynamic-LDS
+ *     limits, raised on first use once per (kernel, device) -- on the device
+ *     current when the call is made.
  *   - Shapes: N % 16 == 0, K % 128 == 0, N >= 16, K >= 128, M >= 1.
  *
  * ---------------------------------------------------------------------------

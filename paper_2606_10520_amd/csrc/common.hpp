@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "unisvq.h"
 
 namespace unisvq {
@@ -184,6 +186,19 @@ constexpr int64_t kSkinnyMaxM = 32;
 hipError_t launch_skinny(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine, int affine_one,
                          int64_t M, const _Float16* x, const float* inv_scale, void* y, int y_dtype,
                          hipStream_t s);
+
+// Raise a kernel's dynamic-LDS limit on the current device, once per
+// (kernel, device): `done` is the calling site's bitmask of devices already
+// set up (devices past 63 are set up on every call).  Returns a status.
+inline int ensure_lds_limit(const void* fn, int bytes, std::atomic<uint64_t>& done) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return UNISVQ_EHIP;
+    const uint64_t bit = dev >= 0 && dev < 64 ? uint64_t{1} << dev : 0;
+    if (bit && (done.load(std::memory_order_acquire) & bit)) return UNISVQ_OK;
+    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) != hipSuccess) return UNISVQ_EHIP;
+    done.fetch_or(bit, std::memory_order_acq_rel);
+    return UNISVQ_OK;
+}
 
 // Output store in the requested dtype (fp32 -> fp16 / bf16 round to nearest even).
 __device__ inline void store_out(void* y, int64_t idx, float v, int y_dtype) {

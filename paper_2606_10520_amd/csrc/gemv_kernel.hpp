@@ -41,8 +41,6 @@
 // matrix-core chains per packet.  Partial row sums meet in LDS at the end.
 #pragma once
 
-#include <atomic>
-
 #include "common.hpp"
 #include "fwht.hpp"
 
@@ -820,15 +818,11 @@ template <typename XT, bool SHARED, int WAVES, int MT, int PF, int NX, int BITS 
 int launch_cfg(const GemvBatch& b, int blocks, int maxK, hipStream_t s) {
     const size_t lds = gemv_lds_bytes(maxK, b.M, WAVES, MT);
     if (lds > kMaxLds) return UNISVQ_EUNSUP;
-    // Raising the dynamic-LDS limit is idempotent; do it once per instantiation.
-    static std::atomic<int> attr_done{0};
-    if (!attr_done.load(std::memory_order_acquire)) {
-        if (hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_kernel<XT, WAVES, MT, PF, NX, 1, SHARED, BITS, D>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize,
-                                static_cast<int>(kMaxLds)) != hipSuccess)
-            return UNISVQ_EHIP;
-        attr_done.store(1, std::memory_order_release);
-    }
+    // the dynamic-LDS limit, raised once per instantiation and device
+    static std::atomic<uint64_t> attr_done{0};
+    const int st = ensure_lds_limit(reinterpret_cast<const void*>(&gemv_kernel<XT, WAVES, MT, PF, NX, 1, SHARED, BITS, D>),
+                                    static_cast<int>(kMaxLds), attr_done);
+    if (st != UNISVQ_OK) return st;
     hipLaunchKernelGGL((gemv_kernel<XT, WAVES, MT, PF, NX, 1, SHARED, BITS, D>), dim3(static_cast<unsigned>(blocks)),
                        dim3(WAVES * 64), lds, s, b);
     return hipGetLastError() == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;

@@ -14,14 +14,10 @@ template <typename XT, int WAVES, int MT, int PF, int KLOG>
 int launch_rht_cfg(const GemvBatch& b, int blocks, hipStream_t s) {
     const size_t lds = gemv_rht_lds_bytes(1 << KLOG, b.M, WAVES, MT);
     if (lds > kMaxLds) return UNISVQ_EUNSUP;
-    static std::atomic<int> attr_done{0};
-    if (!attr_done.load(std::memory_order_acquire)) {
-        if (hipFuncSetAttribute(
-                reinterpret_cast<const void*>(&gemv_kernel<XT, WAVES, MT, PF, 1, 1, false, 2, 4, KLOG>),
-                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kMaxLds)) != hipSuccess)
-            return UNISVQ_EHIP;
-        attr_done.store(1, std::memory_order_release);
-    }
+    static std::atomic<uint64_t> attr_done{0};
+    const int st = ensure_lds_limit(reinterpret_cast<const void*>(&gemv_kernel<XT, WAVES, MT, PF, 1, 1, false, 2, 4, KLOG>),
+                                    static_cast<int>(kMaxLds), attr_done);
+    if (st != UNISVQ_OK) return st;
     hipLaunchKernelGGL((gemv_kernel<XT, WAVES, MT, PF, 1, 1, false, 2, 4, KLOG>), dim3(static_cast<unsigned>(blocks)),
                        dim3(WAVES * 64), lds, s, b);
     return hipGetLastError() == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;

@@ -13,10 +13,9 @@ namespace {
 // up front cover the run when it is short (2) or up to 8 loads.
 template <typename XT, int BITS, int D, int MT>
 int launch_var_mt(const GemvBatch& b, int blocks, int minK, int maxK, hipStream_t s) {
-    const GemvPlan p = plan_gemv(blocks, minK / kGroup, maxK / kGroup, b.M);
+    (void)minK;
     const int per = (maxK / kGroup / 2 + 7) / 8;
     const int loads = b.M * (per + ((maxK / kGroup) & 1));
-    (void)p;
     if (loads <= 2) return launch_cfg<XT, true, 8, MT, 2, 2, BITS, D>(b, blocks, maxK, s);
     return launch_cfg<XT, true, 8, MT, 2, 8, BITS, D>(b, blocks, maxK, s);
 }

@@ -669,19 +669,17 @@ int launch_rht(int64_t n, int64_t M, const void* x, int x_dtype, const signed ch
     const int per = h.m > 1 ? rht_blocks_per_wg(h, static_cast<int>(n)) : 1;
     const size_t lds = rht_lds_bytes(h, static_cast<int>(n), per);
     if (lds > kRhtMaxLds) return UNISVQ_EUNSUP;
-    static bool attr_done = false;  // idempotent; racing first calls set the same value
-    if (!attr_done) {
-        const void* fns[6] = {reinterpret_cast<const void*>(&rht_kernel<_Float16>),
-                              reinterpret_cast<const void*>(&rht_kernel<__bf16>),
-                              reinterpret_cast<const void*>(&rht_kernel<float>),
-                              reinterpret_cast<const void*>(&rht_paley_kernel<_Float16>),
-                              reinterpret_cast<const void*>(&rht_paley_kernel<__bf16>),
-                              reinterpret_cast<const void*>(&rht_paley_kernel<float>)};
-        for (const void* f : fns)
-            if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kRhtMaxLds)) !=
-                hipSuccess)
-                return UNISVQ_EHIP;
-        attr_done = true;
+    // the dynamic-LDS limits, raised once per kernel and device
+    static std::atomic<uint64_t> attr_done[6];
+    const void* fns[6] = {reinterpret_cast<const void*>(&rht_kernel<_Float16>),
+                          reinterpret_cast<const void*>(&rht_kernel<__bf16>),
+                          reinterpret_cast<const void*>(&rht_kernel<float>),
+                          reinterpret_cast<const void*>(&rht_paley_kernel<_Float16>),
+                          reinterpret_cast<const void*>(&rht_paley_kernel<__bf16>),
+                          reinterpret_cast<const void*>(&rht_paley_kernel<float>)};
+    for (int i = 0; i < 6; ++i) {
+        const int st = ensure_lds_limit(fns[i], static_cast<int>(kRhtMaxLds), attr_done[i]);
+        if (st != UNISVQ_OK) return st;
     }
     const float norm = static_cast<float>(1.0 / std::sqrt(static_cast<double>(n)));
     if (h.m == 1 && h.k >= 10) {  // 2^10 .. 2^15: registers, lanes and one exchange

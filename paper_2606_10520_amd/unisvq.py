@@ -178,6 +178,54 @@ def _need_cuda(*ts):
             raise ValueError("libunisvq takes device tensors only")
 
 
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
+def _need_buffer(t, need: int, what: str, exact: bool = False):
+    """A device buffer of at least (exactly, if `exact`) `need` contiguous bytes:
+    the kernels take their address ranges from the shape arguments, so a short
+    or strided tensor would be read or written out of bounds."""
+    if t is None:
+        raise ValueError(f"{what} is required")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    have = _nbytes(t)
+    if (have != need) if exact else (have < need):
+        raise ValueError(f"{what} holds {have} bytes, expected {'' if exact else 'at least '}{need}")
+
+
+def _activations(x, K: int):
+    """x as a contiguous [M][K] fp16/bf16 view (a 1-D x is one or more rows)."""
+    torch = _torch()
+    if x.dim() == 2:
+        if x.shape[1] != K:
+            raise ValueError(f"x has {x.shape[1]} columns, the weights K = {K}")
+        x2 = x
+    else:
+        if x.numel() == 0 or x.numel() % K:
+            raise ValueError(f"x holds {x.numel()} elements, not a multiple of K = {K}")
+        x2 = x.reshape(-1, K)
+    if not x2.is_contiguous():
+        raise ValueError("x must be contiguous")
+    if x2.dtype not in (torch.float16, torch.bfloat16):
+        raise TypeError(f"activations must be fp16 or bf16, got {x2.dtype}")
+    return x2
+
+
+def _output(out, M: int, N: int, out_dtype, like):
+    """The caller's out (checked: contiguous, M*N elements, fp16/bf16/fp32) or a new [M][N] tensor."""
+    torch = _torch()
+    if out is None:
+        return torch.empty((M, N), dtype=out_dtype or like.dtype, device=like.device)
+    _dtype_code(out.dtype)
+    if not out.is_contiguous():
+        raise ValueError("out must be contiguous")
+    if out.numel() != M * N:
+        raise ValueError(f"out holds {out.numel()} elements, the product has M*N = {M * N}")
+    return out
+
+
 def version() -> int:
     return load().unisvq_version()
 
@@ -186,13 +234,26 @@ def packed_bytes(N: int, K: int) -> int:
     return load().unisvq_packed_bytes(N, K)
 
 
+def _canonical(codes, A, B, N: int, K: int, pairs: int, d: int = DIM):
+    """Shapes of canonical codes [N][K] (uint8) and of `pairs` (A, B) pairs (fp16 d x d and d)."""
+    torch = _torch()
+    if codes.dtype != torch.uint8 or tuple(codes.shape) != (N, K):
+        raise ValueError(f"codes must be uint8 [{N}][{K}]")
+    if A.dtype != torch.float16 or A.numel() != pairs * d * d:
+        raise ValueError(f"A must hold {pairs} fp16 {d}x{d} matrices")
+    if B.dtype != torch.float16 or B.numel() != pairs * d:
+        raise ValueError(f"B must hold {pairs} fp16 {d}-vectors")
+
+
 def pack(codes, A, B, out=None, bad_codes=None, stream=None):
     """codes uint8 [N][K]; A fp16 [N][K/128][4][4]; B fp16 [N][K/128][4] -> packed uint8 bytes."""
     torch = _torch()
     _need_cuda(codes, A, B, out, bad_codes)
     N, K = codes.shape
+    _canonical(codes, A, B, N, K, N * (K // GROUP))
     if out is None:
         out = torch.empty(packed_bytes(N, K), dtype=torch.uint8, device=codes.device)
+    _need_buffer(out, packed_bytes(N, K), "out")
     _check("unisvq_pack", load().unisvq_pack(N, K, _ptr(codes.contiguous()), _ptr(A.contiguous()),
                                              _ptr(B.contiguous()), _ptr(out), _ptr(bad_codes),
                                              _stream(stream)))
@@ -203,6 +264,7 @@ def unpack(packed, N: int, K: int, stream=None):
     """Inverse of pack: returns (codes uint8, A fp16, B fp16) device tensors."""
     torch = _torch()
     _need_cuda(packed)
+    _need_buffer(packed, packed_bytes(N, K), "packed", exact=True)
     dev = packed.device
     codes = torch.empty((N, K), dtype=torch.uint8, device=dev)
     A = torch.empty((N, K // GROUP, DIM, DIM), dtype=torch.float16, device=dev)
@@ -213,14 +275,11 @@ def unpack(packed, N: int, K: int, stream=None):
 
 
 def _product(fn_name, N, K, packed, x, out, out_dtype, stream, extra=()):
-    torch = _torch()
     _need_cuda(packed, x, out)
-    x2 = x if x.dim() == 2 else x.reshape(-1, K)
-    if not x2.is_contiguous():
-        raise ValueError("x must be contiguous")
+    _need_buffer(packed, packed_bytes(N, K), "packed", exact=True)
+    x2 = _activations(x, K)
     M = x2.shape[0]
-    if out is None:
-        out = torch.empty((M, N), dtype=out_dtype or x.dtype, device=x.device)
+    out = _output(out, M, N, out_dtype, x2)
     fn = getattr(load(), fn_name)
     _check(fn_name, fn(N, K, _ptr(packed), M, _ptr(x2), _dtype_code(x2.dtype), _ptr(out),
                        _dtype_code(out.dtype), *extra, _stream(stream)))
@@ -244,15 +303,13 @@ def gemv_batched(problems, out_dtype=None, stream=None):
     outs, M, xdt = [], None, None
     for i, (packed, N, K, x, out) in enumerate(problems):
         _need_cuda(packed, x, out)
-        x2 = x if x.dim() == 2 else x.reshape(-1, K)
-        if not x2.is_contiguous():
-            raise ValueError("x must be contiguous")
+        _need_buffer(packed, packed_bytes(N, K), "packed", exact=True)
+        x2 = _activations(x, K)
         if M is None:
             M, xdt = x2.shape[0], x2.dtype
         if x2.shape[0] != M or x2.dtype != xdt:
             raise ValueError("all problems need the same token count and activation dtype")
-        if out is None:
-            out = torch.empty((M, N), dtype=out_dtype or xdt, device=x.device)
+        out = _output(out, M, N, out_dtype, x2)
         outs.append(out)
         arr[i] = GemvProblem(N, K, packed.data_ptr(), x2.data_ptr(), out.data_ptr())
     ydt = {o.dtype for o in outs}
@@ -278,15 +335,14 @@ def gemv_rht_batched(problems, out_dtype=None, stream=None):
     outs, M, xdt = [], None, None
     for i, (packed, N, K, x, signs, out) in enumerate(problems):
         _need_cuda(packed, x, signs, out)
-        x2 = x if x.dim() == 2 else x.reshape(-1, K)
-        if not x2.is_contiguous() or not signs.is_contiguous():
-            raise ValueError("x and signs must be contiguous")
+        _need_buffer(packed, packed_bytes(N, K), "packed", exact=True)
+        _need_buffer(signs, K, "signs", exact=True)
+        x2 = _activations(x, K)
         if M is None:
             M, xdt = x2.shape[0], x2.dtype
         if x2.shape[0] != M or x2.dtype != xdt:
             raise ValueError("all problems need the same token count and activation dtype")
-        if out is None:
-            out = torch.empty((M, N), dtype=out_dtype or xdt, device=x.device)
+        out = _output(out, M, N, out_dtype, x2)
         outs.append(out)
         arr[i] = GemvProblem(N, K, packed.data_ptr(), x2.data_ptr(), out.data_ptr())
         sgn[i] = signs.data_ptr()
@@ -305,14 +361,22 @@ def gemm_workspace_bytes(N: int, K: int, M: int, x_dtype=None) -> int:
     return load().unisvq_gemm_workspace_bytes(N, K, M, code)
 
 
+def _workspace(workspace, need: int, like):
+    """The caller's workspace (contiguous, at least `need` bytes) or a new one; and its size."""
+    torch = _torch()
+    if workspace is None:
+        if not need:
+            return None, 0
+        workspace = torch.empty(need, dtype=torch.uint8, device=like.device)
+    _need_cuda(workspace)
+    _need_buffer(workspace, need, "workspace")
+    return workspace, _nbytes(workspace)
+
+
 def gemm(packed, N: int, K: int, x, out=None, out_dtype=None, workspace=None, stream=None):
     """y[M][N] = x[M][K] . W_hat^T for any M (prefill kernel)."""
-    M = x.numel() // K
-    need = gemm_workspace_bytes(N, K, M, x.dtype)
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    if need and workspace is None:
-        workspace = _torch().empty(need, dtype=_torch().uint8, device=x.device)
-        ws_bytes = need
+    M = _activations(x, K).shape[0]
+    workspace, ws_bytes = _workspace(workspace, gemm_workspace_bytes(N, K, M, x.dtype), x)
     return _product("unisvq_gemm", N, K, packed, x, out, out_dtype, stream,
                     extra=(_ptr(workspace), ws_bytes))
 
@@ -334,10 +398,13 @@ def pack_shared(codes, A, B, out_codes=None, out_affine=None, bad_codes=None, st
     _need_cuda(codes, A, B, out_codes, out_affine, bad_codes)
     N, K = codes.shape
     Ga = A.shape[0]
+    _canonical(codes, A, B, N, K, Ga)
     if out_codes is None:
         out_codes = torch.empty(codes_bytes(N, K), dtype=torch.uint8, device=codes.device)
     if out_affine is None:
         out_affine = torch.empty(max(shared_affine_bytes(K, Ga), 16), dtype=torch.uint8, device=codes.device)
+    _need_buffer(out_codes, codes_bytes(N, K), "out_codes")
+    _need_buffer(out_affine, shared_affine_bytes(K, Ga), "out_affine")
     _check("unisvq_pack_shared", load().unisvq_pack_shared(
         N, K, Ga, _ptr(codes.contiguous()), _ptr(A.contiguous()), _ptr(B.contiguous()), _ptr(out_codes),
         _ptr(out_affine), _ptr(bad_codes), _stream(stream)))
@@ -348,6 +415,8 @@ def unpack_shared(packed_codes, packed_affine, N: int, K: int, affine_groups: in
     """Inverse of pack_shared: (codes uint8 [N][K], A fp16 [Ga][4][4], B fp16 [Ga][4])."""
     torch = _torch()
     _need_cuda(packed_codes, packed_affine)
+    _need_buffer(packed_codes, codes_bytes(N, K), "packed_codes", exact=True)
+    _need_buffer(packed_affine, shared_affine_bytes(K, affine_groups), "packed_affine")
     dev = packed_codes.device
     codes = torch.empty((N, K), dtype=torch.uint8, device=dev)
     A = torch.empty((affine_groups, DIM, DIM), dtype=torch.float16, device=dev)
@@ -358,16 +427,21 @@ def unpack_shared(packed_codes, packed_affine, N: int, K: int, affine_groups: in
     return codes, A, B
 
 
+def _shared_operands(packed_codes, packed_affine, N, K, affine_groups):
+    _need_buffer(packed_codes, codes_bytes(N, K), "packed_codes", exact=True)
+    need = shared_affine_bytes(K, affine_groups)
+    if not need:
+        raise ValueError(f"affine_groups must be 1 or K/128 = {K // GROUP}, got {affine_groups}")
+    _need_buffer(packed_affine, need, "packed_affine")
+
+
 def _shared_product(fn_name, N, K, affine_groups, packed_codes, packed_affine, x, out, out_dtype, stream,
                     extra=()):
-    torch = _torch()
     _need_cuda(packed_codes, packed_affine, x, out)
-    x2 = x if x.dim() == 2 else x.reshape(-1, K)
-    if not x2.is_contiguous():
-        raise ValueError("x must be contiguous")
+    _shared_operands(packed_codes, packed_affine, N, K, affine_groups)
+    x2 = _activations(x, K)
     M = x2.shape[0]
-    if out is None:
-        out = torch.empty((M, N), dtype=out_dtype or x.dtype, device=x.device)
+    out = _output(out, M, N, out_dtype, x2)
     fn = getattr(load(), fn_name)
     _check(fn_name, fn(N, K, affine_groups, _ptr(packed_codes), _ptr(packed_affine), M, _ptr(x2),
                        _dtype_code(x2.dtype), _ptr(out), _dtype_code(out.dtype), *extra, _stream(stream)))
@@ -390,15 +464,13 @@ def gemv_shared_batched(problems, out_dtype=None, stream=None):
     outs, M, xdt = [], None, None
     for i, (pc, pa, N, K, ga, x, out) in enumerate(problems):
         _need_cuda(pc, pa, x, out)
-        x2 = x if x.dim() == 2 else x.reshape(-1, K)
-        if not x2.is_contiguous():
-            raise ValueError("x must be contiguous")
+        _shared_operands(pc, pa, N, K, ga)
+        x2 = _activations(x, K)
         if M is None:
             M, xdt = x2.shape[0], x2.dtype
         if x2.shape[0] != M or x2.dtype != xdt:
             raise ValueError("all problems need the same token count and activation dtype")
-        if out is None:
-            out = torch.empty((M, N), dtype=out_dtype or xdt, device=x.device)
+        out = _output(out, M, N, out_dtype, x2)
         outs.append(out)
         arr[i] = GemvSharedProblem(N, K, ga, pc.data_ptr(), pa.data_ptr(), x2.data_ptr(), out.data_ptr())
     if len({o.dtype for o in outs}) != 1:
@@ -411,12 +483,8 @@ def gemv_shared_batched(problems, out_dtype=None, stream=None):
 def gemm_shared(packed_codes, packed_affine, N: int, K: int, affine_groups: int, x, out=None, out_dtype=None,
                 workspace=None, stream=None):
     """Prefill product with codes-only weights and row-shared pairs (any M)."""
-    M = x.numel() // K
-    need = gemm_workspace_bytes(N, K, M, x.dtype)
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    if need and workspace is None:
-        workspace = _torch().empty(need, dtype=_torch().uint8, device=x.device)
-        ws_bytes = need
+    M = _activations(x, K).shape[0]
+    workspace, ws_bytes = _workspace(workspace, gemm_workspace_bytes(N, K, M, x.dtype), x)
     return _shared_product("unisvq_gemm_shared", N, K, affine_groups, packed_codes, packed_affine, x, out,
                            out_dtype, stream, extra=(_ptr(workspace), ws_bytes))
 
@@ -428,12 +496,8 @@ def gemm_fold_workspace_bytes(N: int, K: int, M: int) -> int:
 def gemm_shared_fold(packed_codes, packed_affine, N: int, K: int, affine_groups: int, x, out=None,
                      out_dtype=None, workspace=None, stream=None):
     """Prefill product with row-shared pairs through the Eq. 9 fold (any M)."""
-    M = x.numel() // K
-    need = gemm_fold_workspace_bytes(N, K, M)
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    if workspace is None:
-        workspace = _torch().empty(max(need, 1), dtype=_torch().uint8, device=x.device)
-        ws_bytes = need
+    M = _activations(x, K).shape[0]
+    workspace, ws_bytes = _workspace(workspace, gemm_fold_workspace_bytes(N, K, M), x)
     return _shared_product("unisvq_gemm_shared_fold", N, K, affine_groups, packed_codes, packed_affine, x, out,
                            out_dtype, stream, extra=(_ptr(workspace), ws_bytes))
 
@@ -446,8 +510,13 @@ def quantize(W, A, B, affine_groups: int = 0, out=None, stream=None):
     torch = _torch()
     _need_cuda(W, A, B, out)
     N, K = W.shape
+    if W.dtype != torch.float32:
+        raise TypeError("W must be fp32")
+    pairs = N * (K // GROUP) if affine_groups == 0 else affine_groups
+    _canonical(torch.empty((N, K), dtype=torch.uint8, device="meta"), A, B, N, K, pairs)
     if out is None:
         out = torch.empty((N, K), dtype=torch.uint8, device=W.device)
+    _need_buffer(out, N * K, "out", exact=True)
     _check("unisvq_quantize", load().unisvq_quantize(N, K, _ptr(W.contiguous()), _ptr(A.contiguous()),
                                                      _ptr(B.contiguous()), affine_groups, _ptr(out),
                                                      _stream(stream)))
@@ -459,14 +528,13 @@ def quantize(W, A, B, affine_groups: int = 0, out=None, stream=None):
 def rht(x, signs, mode: str, out=None, out_dtype=None, stream=None):
     """mode 'in': (x diag(signs)) H / sqrt(n); mode 'out': (x H / sqrt(n)) diag(signs).
     x [M][n] (fp16, bf16 or fp32), signs int8 [n] (+-1)."""
-    torch = _torch()
     _need_cuda(x, signs, out)
     x2 = x if x.dim() == 2 else x.reshape(1, -1)
     if not x2.is_contiguous():
         raise ValueError("x must be contiguous")
     M, n = x2.shape
-    if out is None:
-        out = torch.empty((M, n), dtype=out_dtype or x.dtype, device=x.device)
+    _need_buffer(signs, n, "signs", exact=True)
+    out = _output(out, M, n, out_dtype, x2)
     _check("unisvq_rht", load().unisvq_rht(n, M, _ptr(x2), _dtype_code(x2.dtype), _ptr(signs.contiguous()),
                                            0 if mode == "in" else 1, _ptr(out), _dtype_code(out.dtype),
                                            _stream(stream)))
@@ -490,10 +558,13 @@ def var_pack(codes, A, B, bits: int, d: int, out_codes=None, out_affine=None, ba
     _need_cuda(codes, A, B, out_codes, out_affine, bad_codes)
     N, K = codes.shape
     Ga = A.shape[0]
+    _canonical(codes, A, B, N, K, Ga, d)
     if out_codes is None:
         out_codes = torch.empty(max(var_codes_bytes(N, K, bits, d), 16), dtype=torch.uint8, device=codes.device)
     if out_affine is None:
         out_affine = torch.empty(max(var_affine_bytes(K, Ga, bits, d), 16), dtype=torch.uint8, device=codes.device)
+    _need_buffer(out_codes, var_codes_bytes(N, K, bits, d), "out_codes")
+    _need_buffer(out_affine, var_affine_bytes(K, Ga, bits, d), "out_affine")
     _check("unisvq_var_pack", load().unisvq_var_pack(
         N, K, bits, d, Ga, _ptr(codes.contiguous()), _ptr(A.contiguous()), _ptr(B.contiguous()), _ptr(out_codes),
         _ptr(out_affine), _ptr(bad_codes), _stream(stream)))
@@ -504,6 +575,7 @@ def var_unpack(packed_codes, packed_affine, N: int, K: int, bits: int, d: int, a
     """Inverse of var_pack: (codes uint8 [N][K], A fp16 [Ga][d][d], B fp16 [Ga][d])."""
     torch = _torch()
     _need_cuda(packed_codes, packed_affine)
+    _var_operands(packed_codes, packed_affine, N, K, bits, d, affine_groups)
     dev = packed_codes.device
     codes = torch.empty((N, K), dtype=torch.uint8, device=dev)
     A = torch.empty((affine_groups, d, d), dtype=torch.float16, device=dev)
@@ -514,16 +586,22 @@ def var_unpack(packed_codes, packed_affine, N: int, K: int, bits: int, d: int, a
     return codes, A, B
 
 
+def _var_operands(packed_codes, packed_affine, N, K, bits, d, affine_groups):
+    need_c = var_codes_bytes(N, K, bits, d)
+    need_a = var_affine_bytes(K, affine_groups, bits, d)
+    if not need_c or not need_a:
+        raise ValueError(f"unsupported variant (bits={bits}, d={d}, affine_groups={affine_groups}) or shape")
+    _need_buffer(packed_codes, need_c, "packed_codes")
+    _need_buffer(packed_affine, need_a, "packed_affine")
+
+
 def _var_product(fn_name, N, K, bits, d, affine_groups, packed_codes, packed_affine, x, out, out_dtype, stream,
                  extra=()):
-    torch = _torch()
     _need_cuda(packed_codes, packed_affine, x, out)
-    x2 = x if x.dim() == 2 else x.reshape(-1, K)
-    if not x2.is_contiguous():
-        raise ValueError("x must be contiguous")
+    _var_operands(packed_codes, packed_affine, N, K, bits, d, affine_groups)
+    x2 = _activations(x, K)
     M = x2.shape[0]
-    if out is None:
-        out = torch.empty((M, N), dtype=out_dtype or x.dtype, device=x.device)
+    out = _output(out, M, N, out_dtype, x2)
     fn = getattr(load(), fn_name)
     _check(fn_name, fn(N, K, bits, d, affine_groups, _ptr(packed_codes), _ptr(packed_affine), M, _ptr(x2),
                        _dtype_code(x2.dtype), _ptr(out), _dtype_code(out.dtype), *extra, _stream(stream)))
@@ -547,16 +625,19 @@ def var_gemv_batched(problems, bits: int, d: int, out_dtype=None, stream=None):
     outs = []
     M = None
     for i, pr in enumerate(problems):
-        x = pr["x"]
-        _need_cuda(pr["packed_codes"], pr["packed_affine"], x)
+        _need_cuda(pr["packed_codes"], pr["packed_affine"], pr["x"], pr.get("out"))
+        _var_operands(pr["packed_codes"], pr["packed_affine"], pr["N"], pr["K"], bits, d, pr["affine_groups"])
+        x = _activations(pr["x"], pr["K"])
         if M is None:
             M, xdt = x.shape[0], x.dtype
-        out = pr.get("out")
-        if out is None:
-            out = torch.empty((x.shape[0], pr["N"]), dtype=out_dtype or x.dtype, device=x.device)
+        if x.shape[0] != M or x.dtype != xdt:
+            raise ValueError("all problems need the same token count and activation dtype")
+        out = _output(pr.get("out"), M, pr["N"], out_dtype, x)
         outs.append(out)
         arr[i] = GemvSharedProblem(pr["N"], pr["K"], pr["affine_groups"], _ptr(pr["packed_codes"]),
                                    _ptr(pr["packed_affine"]), _ptr(x), _ptr(out))
+    if len({o.dtype for o in outs}) != 1:
+        raise ValueError("all outputs need the same dtype")
     _check("unisvq_var_gemv_batched", load().unisvq_var_gemv_batched(
         arr, len(problems), bits, d, M, _dtype_code(xdt), _dtype_code(outs[0].dtype), _stream(stream)))
     return outs
@@ -571,12 +652,8 @@ def var_gemm_workspace_bytes(N: int, K: int, M: int, x_dtype=None) -> int:
 def var_gemm(packed_codes, packed_affine, N: int, K: int, bits: int, d: int, affine_groups: int, x, out=None,
              out_dtype=None, workspace=None, stream=None):
     """Prefill product with variant weights (any M)."""
-    torch = _torch()
-    M = x.numel() // K
-    need = var_gemm_workspace_bytes(N, K, M, x.dtype)
-    if workspace is None and need:
-        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
-    wb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    M = _activations(x, K).shape[0]
+    workspace, wb = _workspace(workspace, var_gemm_workspace_bytes(N, K, M, x.dtype), x)
     return _var_product("unisvq_var_gemm", N, K, bits, d, affine_groups, packed_codes, packed_affine, x, out,
                         out_dtype, stream, extra=(_ptr(workspace), wb))
 
@@ -594,12 +671,14 @@ def ldlq(W, U, A, B, affine_groups: int = 0, out=None, workspace=None, stream=No
     torch = _torch()
     _need_cuda(W, U, A, B, out, workspace)
     N, K = W.shape
+    if W.dtype != torch.float32 or U.dtype != torch.float64 or U.numel() != K * K:
+        raise ValueError(f"W must be fp32 [N][K] and U fp64 [{K}][{K}]")
+    pairs = N * (K // GROUP) if affine_groups == 0 else affine_groups
+    _canonical(torch.empty((N, K), dtype=torch.uint8, device="meta"), A, B, N, K, pairs)
     if out is None:
         out = torch.empty((N, K), dtype=torch.uint8, device=W.device)
-    need = ldlq_workspace_bytes(N, K)
-    if workspace is None:
-        workspace = torch.empty(need, dtype=torch.uint8, device=W.device)
-    wb = workspace.numel() * workspace.element_size()
+    _need_buffer(out, N * K, "out", exact=True)
+    workspace, wb = _workspace(workspace, ldlq_workspace_bytes(N, K), W)
     _check("unisvq_ldlq", load().unisvq_ldlq(N, K, _ptr(W.contiguous()), _ptr(U.contiguous()), _ptr(A.contiguous()),
                                               _ptr(B.contiguous()), affine_groups, _ptr(out), _ptr(workspace), wb,
                                               _stream(stream)))

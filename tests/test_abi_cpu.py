@@ -408,3 +408,47 @@ def test_fold_workspace_and_validation():
     assert call(wsp=None) == EWS
     assert call(ws_bytes=ws(64, 256, 4) - 1) == EWS
     assert call(wsp=GOOD + 4) == EALIGN
+
+
+def test_binding_checks_buffers_against_the_shape():
+    """The kernels take their address ranges from N, K and M, so the binding
+    rejects short, strided or mistyped tensors before any call (checked with
+    host tensors: the helpers look only at shape, dtype and layout)."""
+    torch = pytest.importorskip("torch")
+    N, K = 32, 256
+    need = u.packed_bytes(N, K)
+    u._need_buffer(torch.empty(need, dtype=torch.uint8), need, "packed", exact=True)
+    with pytest.raises(ValueError):
+        u._need_buffer(torch.empty(need - 1, dtype=torch.uint8), need, "packed", exact=True)
+    with pytest.raises(ValueError):
+        u._need_buffer(torch.empty(need + 16, dtype=torch.uint8), need, "packed", exact=True)
+    with pytest.raises(ValueError):
+        u._need_buffer(torch.empty(2 * need, dtype=torch.uint8)[::2], need, "packed")
+    with pytest.raises(ValueError):
+        u._need_buffer(None, need, "workspace")
+    # activations: K columns, contiguous, fp16/bf16
+    assert u._activations(torch.empty(3, K, dtype=torch.float16), K).shape == (3, K)
+    assert u._activations(torch.empty(2 * K, dtype=torch.bfloat16), K).shape == (2, K)
+    for bad in (torch.empty(3, K + 128, dtype=torch.float16), torch.empty(K + 1, dtype=torch.float16),
+                torch.empty(K, 3, dtype=torch.float16).t()):
+        with pytest.raises(ValueError):
+            u._activations(bad, K)
+    with pytest.raises(TypeError):
+        u._activations(torch.empty(1, K, dtype=torch.float32), K)
+    # outputs: M*N elements, contiguous, fp16/bf16/fp32
+    like = torch.empty(1, K, dtype=torch.float16)
+    assert u._output(None, 3, N, None, like).shape == (3, N)
+    assert u._output(torch.empty(3 * N, dtype=torch.float32), 3, N, None, like).numel() == 3 * N
+    with pytest.raises(ValueError):
+        u._output(torch.empty(3 * N - 1, dtype=torch.float16), 3, N, None, like)
+    with pytest.raises(ValueError):
+        u._output(torch.empty(N, 3, dtype=torch.float16).t(), 3, N, None, like)
+    with pytest.raises(TypeError):
+        u._output(torch.empty(3 * N, dtype=torch.int32), 3, N, None, like)
+    # canonical codes and pairs
+    q = torch.zeros(N, K, dtype=torch.uint8)
+    u._canonical(q, torch.zeros(N, 2, 4, 4, dtype=torch.float16), torch.zeros(N, 2, 4, dtype=torch.float16),
+                 N, K, N * 2)
+    with pytest.raises(ValueError):
+        u._canonical(q, torch.zeros(N, 2, 4, 4, dtype=torch.float16), torch.zeros(N, 1, 4, dtype=torch.float16),
+                     N, K, N * 2)
