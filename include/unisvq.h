@@ -462,6 +462,26 @@ int unisvq_rht(int64_t n, int64_t M, const void* x, int x_dtype, const int8_t* s
 int unisvq_gemv_rht_batched(const unisvq_gemv_problem* problems, int count, int64_t M, int x_dtype, int y_dtype,
                             const int8_t* const* signs, void* stream);
 
+/* ---- Bandwidth reference (not part of the method) ----
+ * A plain read of `count` device byte ranges in one launch, with the 16-byte
+ * non-temporal loads the decode kernels stream their weights with (32 KB per
+ * workgroup of 512 threads; a thread issues all four of its loads before
+ * using any).  The 32-bit words of all ranges are XOR-folded into *sink (one
+ * atomic per wavefront; XOR does not depend on the order, so the result is
+ * exact and checkable).  Timed over the buffers of a product launch it gives
+ * the read rate those bytes reach in the same launch structure.
+ *   ranges  HOST array of 1..UNISVQ_MAX_BATCH descriptors, read before the
+ *           call returns; each ptr device, 16-byte aligned, bytes a multiple
+ *           of 16 in [0, 2^31) (UNISVQ_EINVAL otherwise)
+ *   sink    device uint32, 4-byte aligned; XOR-accumulated (the caller sets
+ *           its initial value) */
+typedef struct {
+    const void* ptr;
+    int64_t bytes;
+} unisvq_byte_range;
+
+int unisvq_read_bytes(const unisvq_byte_range* ranges, int count, uint32_t* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -424,4 +424,23 @@ int unisvq_rht(int64_t n, int64_t M, const void* x, int x_dtype, const int8_t* s
                               static_cast<hipStream_t>(stream));
 }
 
+/* ---- bandwidth reference ---- */
+
+int unisvq_read_bytes(const unisvq_byte_range* ranges, int count, uint32_t* sink, void* stream) {
+    if (!ranges || !sink || count < 1) return UNISVQ_EINVAL;
+    if (count > UNISVQ_MAX_BATCH) return UNISVQ_EUNSUP;
+    if (!aligned(sink, 4)) return UNISVQ_EALIGN;
+    const uint8_t* ptrs[UNISVQ_MAX_BATCH];
+    int64_t bytes[UNISVQ_MAX_BATCH];
+    for (int i = 0; i < count; ++i) {
+        if (ranges[i].bytes < 0 || ranges[i].bytes % 16 || ranges[i].bytes > unisvq::kMaxBufferBytes)
+            return UNISVQ_EINVAL;
+        if (ranges[i].bytes > 0 && !ranges[i].ptr) return UNISVQ_EINVAL;
+        if (!aligned(ranges[i].ptr, 16)) return UNISVQ_EALIGN;
+        ptrs[i] = static_cast<const uint8_t*>(ranges[i].ptr);
+        bytes[i] = ranges[i].bytes;
+    }
+    return unisvq::launch_read(ptrs, bytes, count, sink, static_cast<hipStream_t>(stream));
+}
+
 }  // extern "C"

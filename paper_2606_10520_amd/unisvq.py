@@ -28,7 +28,7 @@ EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "uni
            "unisvq_quantize", "unisvq_rht", "unisvq_var_codes_bytes", "unisvq_var_affine_bytes",
            "unisvq_var_pack", "unisvq_var_unpack", "unisvq_var_gemv", "unisvq_var_gemv_batched",
            "unisvq_var_gemm_workspace_bytes", "unisvq_var_gemm", "unisvq_ldlq_workspace_bytes", "unisvq_ldlq",
-           "unisvq_gemv_rht_batched")
+           "unisvq_gemv_rht_batched", "unisvq_read_bytes")
 # format variants: (bits, d) pairs served by the unisvq_var_* entry points
 VARIANTS = ((3, 4), (2, 8), (3, 8))
 MAX_BATCH = 8
@@ -45,6 +45,11 @@ class GemvSharedProblem(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int64), ("K", ctypes.c_int64), ("affine_groups", ctypes.c_int64),
                 ("packed_codes", ctypes.c_void_p), ("packed_affine", ctypes.c_void_p),
                 ("x", ctypes.c_void_p), ("y", ctypes.c_void_p)]
+
+
+class ByteRange(ctypes.Structure):
+    """Mirror of unisvq_byte_range."""
+    _fields_ = [("ptr", ctypes.c_void_p), ("bytes", ctypes.c_int64)]
 
 
 class UniSVQLibraryMissing(RuntimeError):
@@ -133,6 +138,8 @@ def load():
     lib.unisvq_ldlq_workspace_bytes.restype = sz
     lib.unisvq_ldlq.argtypes = [i64, i64, p, p, p, p, i64, p, p, sz, p]
     lib.unisvq_ldlq.restype = i32
+    lib.unisvq_read_bytes.argtypes = [ctypes.POINTER(ByteRange), i32, p, p]
+    lib.unisvq_read_bytes.restype = i32
     _lib = lib
     return lib
 
@@ -683,3 +690,20 @@ def ldlq(W, U, A, B, affine_groups: int = 0, out=None, workspace=None, stream=No
                                               _ptr(B.contiguous()), affine_groups, _ptr(out), _ptr(workspace), wb,
                                               _stream(stream)))
     return out
+
+
+# ------------------------------------------------ bandwidth reference
+
+def read_bytes(buffers, sink, stream=None):
+    """Plain read of the given device tensors (contiguous, 16-byte multiples)
+    in one launch; XOR-folds their 32-bit words into sink (int32 [1])."""
+    _need_cuda(sink, *buffers)
+    if not 1 <= len(buffers) <= MAX_BATCH:
+        raise ValueError(f"1..{MAX_BATCH} buffers per call")
+    arr = (ByteRange * len(buffers))()
+    for i, t in enumerate(buffers):
+        if not t.is_contiguous():
+            raise ValueError("buffers must be contiguous")
+        arr[i] = ByteRange(t.data_ptr(), _nbytes(t))
+    _need_buffer(sink, 4, "sink")
+    _check("unisvq_read_bytes", load().unisvq_read_bytes(arr, len(buffers), _ptr(sink), _stream(stream)))

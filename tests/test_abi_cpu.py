@@ -452,3 +452,17 @@ def test_binding_checks_buffers_against_the_shape():
     with pytest.raises(ValueError):
         u._canonical(q, torch.zeros(N, 2, 4, 4, dtype=torch.float16), torch.zeros(N, 1, 4, dtype=torch.float16),
                      N, K, N * 2)
+
+
+def test_read_bytes_validation():
+    lib = u.load()
+    R = u.ByteRange
+    one = (R * 1)(R(GOOD, 4096))
+    assert lib.unisvq_read_bytes(None, 1, GOOD, None) == EINVAL
+    assert lib.unisvq_read_bytes(one, 0, GOOD, None) == EINVAL
+    assert lib.unisvq_read_bytes(one, 1, None, None) == EINVAL
+    assert lib.unisvq_read_bytes(one, 9, GOOD, None) == EUNSUP
+    assert lib.unisvq_read_bytes(one, 1, GOOD + 2, None) == EALIGN
+    for bad in (R(GOOD, 4100), R(GOOD, -16), R(None, 4096), R(GOOD, 2 ** 31)):
+        assert lib.unisvq_read_bytes((R * 1)(bad), 1, GOOD, None) == EINVAL
+    assert lib.unisvq_read_bytes((R * 1)(R(GOOD + 8, 4096)), 1, GOOD, None) == EALIGN

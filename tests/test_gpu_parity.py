@@ -133,15 +133,6 @@ def test_gemv_llama7b_m1_full_parity_fp16_out(layer):
                                  np.abs(ref) * 2.0 ** -10 + 1e-4 * np.abs(ref).max())
 
 
-@pytest.mark.parametrize("layer", [wl.LLAMA70B[1], wl.LLAMA70B[0], wl.LLAMA70B[6]], ids=lambda l: l.name)
-def test_gemv_llama70b_m1_sampled_rows(layer):
-    y, pk, xb = run_product("gemv", layer.N, layer.K, 1, "f16", seed=10 + layer.N % 7)
-    rows = np.random.default_rng(0).choice(layer.N, 256, replace=False)
-    rows[:2] = [0, layer.N - 1]
-    ref = oracle.matmul(pk, layer.N, layer.K, x_as_f64(xb, "f16"), rows=rows)
-    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 1e-5
-
-
 @pytest.mark.parametrize("M", [1, 2, 3, 4])
 def test_gemv_outlier_activations(M):
     y, pk, xb = run_product("gemv", 4096, 4096, M, "f16", out=torch.float16, seed=3, outliers=True)
@@ -161,36 +152,6 @@ def test_gemm_small_shapes_full_parity(N, K, M, dtype):
     # activations are carried exactly in fp16 after a per-token power-of-two
     # scale, so both activation types meet the same bar.
     assert rel_err(y.cpu().numpy(), ref) <= 5e-4
-
-
-@pytest.mark.parametrize("layer", wl.PREFILL7B, ids=lambda l: l.name)
-def test_gemm_prefill_m2048_sampled_rows(layer):
-    """Prefill at its real size (M = 2048, bf16 activations), checked on 64 rows."""
-    y, pk, xb = run_product("gemm", layer.N, layer.K, 2048, "bf16", out=torch.float32, seed=20)
-    rows = np.random.default_rng(1).choice(layer.N, 64, replace=False)
-    rows[:2] = [0, layer.N - 1]
-    ref = oracle.matmul(pk, layer.N, layer.K, x_as_f64(xb, "bf16"), rows=rows)
-    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 5e-4
-
-
-@pytest.mark.parametrize("layer", [l for l in wl.LLAMA7B if l.name in ("gate", "down")], ids=lambda l: l.name)
-@pytest.mark.parametrize("M", [16, 64])
-def test_gemm_smallbatch_7b_sampled_rows(layer, M):
-    """Small-batch decode shapes (the product is split along K and the fp32
-    partials summed by a second kernel), outlier activations, 48 rows checked."""
-    Q, A, B = wl.gen_weights(layer.N, layer.K, seed=40 + M)
-    xb = wl.gen_activations(M, layer.K, seed=wl.activation_seed(40, M), dtype="f16", outliers=True)
-    pk_ref, _ = oracle.pack(Q, A, B)
-    pk = upload_pack(Q, A, B)
-    y = u.gemm(pk, layer.N, layer.K, dev_x(xb, "f16"), out_dtype=torch.float32)
-    torch.cuda.synchronize()
-    rows = np.random.default_rng(M).choice(layer.N, 48, replace=False)
-    rows[:2] = [0, layer.N - 1]
-    ref = oracle.matmul(pk_ref, layer.N, layer.K, x_as_f64(xb, "f16"), rows=rows)
-    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 5e-4
-    # the split reduction runs in a fixed order: bit-identical on a rerun
-    y2 = u.gemm(pk, layer.N, layer.K, dev_x(xb, "f16"), out_dtype=torch.float32)
-    assert torch.equal(y, y2)
 
 
 def test_gemm_bf16_extreme_token_scales():
@@ -480,12 +441,11 @@ def test_gemv_shared_parity(N, K, M, per_group, dtype):
 
 @pytest.mark.parametrize("layer", wl.LLAMA7B[3:], ids=lambda l: l.name)
 def test_gemv_shared_llama7b_one_pair_per_matrix(layer):
-    """The paper's setting at the 7B shapes: one pair per matrix, fp16 outputs."""
+    """The paper's setting at the 7B shapes: one pair per matrix, fp16
+    outputs, every element."""
     y, (Q, A, B), xb = run_shared("gemv_shared", layer.N, layer.K, 1, 1, "f16", out=torch.float16, seed=50)
-    rows = np.random.default_rng(2).choice(layer.N, 256, replace=False)
-    rows[:2] = [0, layer.N - 1]
-    ref = oracle.matmul_shared(oracle.pack_codes(Q)[0], layer.N, layer.K, A, B, x_as_f64(xb, "f16"), rows=rows)
-    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 2e-3
+    ref = oracle.matmul_shared(oracle.pack_codes(Q)[0], layer.N, layer.K, A, B, x_as_f64(xb, "f16"))
+    assert rel_err(y.cpu().numpy(), ref) <= 2e-3
 
 
 @pytest.mark.parametrize("fn", ["gemv", "gemm"])
@@ -532,15 +492,6 @@ def test_gemm_shared_parity(N, K, M, per_group, dtype):
     y, (Q, A, B), xb = run_shared("gemm_shared", N, K, M, Ga, dtype, seed=N + M + 1)
     ref = oracle.matmul_shared(oracle.pack_codes(Q)[0], N, K, A, B, x_as_f64(xb, dtype))
     assert rel_err(y.cpu().numpy(), ref) <= 5e-4
-
-
-def test_gemm_shared_prefill_m2048_sampled_rows():
-    layer = wl.PREFILL7B[0]
-    y, (Q, A, B), xb = run_shared("gemm_shared", layer.N, layer.K, 2048, 1, "bf16", seed=21)
-    rows = np.random.default_rng(3).choice(layer.N, 48, replace=False)
-    rows[:2] = [0, layer.N - 1]
-    ref = oracle.matmul_shared(oracle.pack_codes(Q)[0], layer.N, layer.K, A, B, x_as_f64(xb, "bf16"), rows=rows)
-    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 5e-4
 
 
 # ------------------------------------------- nearest-codeword quantiser
@@ -637,3 +588,23 @@ def test_rotated_layer_end_to_end():
     x_rot = oracle.rht(x_as_f64(xb, "f16"), sV, "in")
     ref = oracle.rht(oracle.matmul(pk_ref, N, K, x_rot), sU, "out")
     assert rel_err(y.cpu().numpy(), ref) <= 2e-3
+
+
+# ------------------------------------------- bandwidth reference
+
+def test_read_bytes_folds_every_word():
+    """The plain-read reference reads every byte it is given: the XOR of all
+    32-bit words of several ranges (one with a partial last workgroup, one
+    empty) matches the host's."""
+    rng = np.random.default_rng(77)
+    sizes = [9_437_184, 32_768 + 48, 0, 16]
+    host = [rng.integers(0, 2 ** 32, size=n // 4, dtype=np.uint64).astype(np.uint32) for n in sizes]
+    bufs = [torch.from_numpy(h.view(np.int32)).to(DEV) for h in host]
+    sink = torch.full((1,), 0x5A5A5A5A, dtype=torch.int32, device=DEV)
+    u.read_bytes(bufs, sink)
+    torch.cuda.synchronize()
+    expect = np.uint32(0x5A5A5A5A)
+    for h in host:
+        if h.size:
+            expect ^= np.bitwise_xor.reduce(h)
+    assert np.uint32(sink.cpu().numpy().view(np.uint32)[0]) == expect

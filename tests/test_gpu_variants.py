@@ -197,10 +197,9 @@ def test_var_gemm_parity(bits, d, N, K, M, per_group, dtype):
 
 
 @pytest.mark.parametrize("bits,d", VARIANTS, ids=VID)
-def test_var_gemm_prefill_m2048_sampled_rows(bits, d):
+def test_var_gemm_prefill_m2048_full_tensor(bits, d):
+    """Prefill (2048 tokens, bf16) at 4096 x 4096, every element."""
     L = wl.PREFILL7B[0]
     y, (Q, A, B), xb = run("var_gemm", L.N, L.K, 2048, bits, d, 1, "bf16", seed=21)
-    rows = np.random.default_rng(3).choice(L.N, 32, replace=False)
-    rows[:2] = [0, L.N - 1]
-    ref = oracle_y(Q, A, B, bits, d, x_as_f64(xb, "bf16"), rows=rows)
-    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 5e-4
+    ref = oracle_y(Q, A, B, bits, d, x_as_f64(xb, "bf16"))
+    assert rel_err(y.cpu().numpy(), ref) <= 5e-4
