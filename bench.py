@@ -1,17 +1,28 @@
 #!/usr/bin/env python3
 """Benchmark of the UniSVQ 2-bit affine-lattice product on one MI355X.
 
-Default workload: the LLaMA-7B decoder linears at M = 1 token (q/k/v/o
-4096x4096, gate/up 11008x4096, down 4096x11008), 2-bit codes in d = 4
-vectors along K with one fp16 (A, B) set per (row, 128-column group), fp16
-activations.  One step = one pass of the seven linears through unisvq_gemv,
-launched back to back on one stream.  Weights, activations and outputs are
-resident in HBM before timing starts; the step rotates over enough copies of
-the layer set (> 512 MB) that the 256 MB Infinity Cache cannot serve them.
+Headline workload: the LLaMA-7B decoder linears at M = 1 token (q/k/v/o
+4096x4096, gate/up 11008x4096, down 4096x11008), 2-bit codes in d = 4 vectors
+along K with one fp16 (A, B) set per (row, 128-column group), fp16
+activations.  One step = one pass of the seven linears in the decoder's launch
+schedule (q+k+v in one batched launch, o, gate+up in one batched launch,
+down).  Weights, activations and outputs are resident in HBM before timing
+starts; the steps rotate over enough copies of the layer set (> 512 MB) that
+the 256 MB Infinity Cache cannot serve them.  The K timed steps are one HIP
+graph of exactly K steps, replayed once between two events.
 
-Prints one JSON line.  value = algorithmic bytes per step / time per step
-(codes N*K/4 + affine N*(K/128)*40 + activations + outputs; dense fp16
-weights are never counted).
+value = algorithmic bytes per step / time per step (codes N*K/4 + affine
+N*(K/128)*40 + activations + outputs; dense fp16 weights are never counted).
+
+The same JSON line carries a sub-record per configured workload ("configs"):
+one 4096x4096 layer at M = 1; the 7B set at M = 4, 16, 64 (outlier
+channels); the 70B set at M = 1 and 16; prefill at M = 2048 (bf16) through
+the decode path and the Eq. 9 fold, with eager and in-graph dense bf16
+products of the same shapes; each with its own roofline, graph-timed
+per-launch durations and, for the bandwidth-bound ones, a plain read of the
+same buffers in the same launch structure ("achievable").
+
+Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -33,6 +44,11 @@ PEAK_HBM_GBS = 8000.0      # MI355X HBM3E, datasheet
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16/fp16 matrix, datasheet
 MALL_BYTES = 256 << 20
 METRIC = "2-bit GEMV achieved HBM GB/s (% peak) + µs/layer at 7B shapes, M=1"
+SUB_WORKLOADS = ("layer4096_m1", "llama7b_smallbatch_m4", "llama7b_smallbatch_m16", "llama7b_smallbatch_m64",
+                 "llama70b_decode_m1", "llama70b_decode_m16", "llama7b_prefill_m2048")
+CONFIG_INDEX = {"layer4096_m1": 0, "llama7b_decode_m1": 1, "llama7b_smallbatch_m4": 2, "llama7b_smallbatch_m16": 2,
+                "llama7b_smallbatch_m64": 2, "llama70b_decode_m1": 3, "llama70b_decode_m16": 3,
+                "llama7b_prefill_m2048": 4}
 
 
 def affine_groups(K: int, affine: str) -> int:
@@ -59,12 +75,12 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--workload", default="llama7b_decode_m1",
-                   choices=["llama7b_decode_m1", "layer4096_m1", "llama70b_decode_m1",
-                            "llama70b_decode_m16", "llama7b_smallbatch_m4", "llama7b_smallbatch_m16",
-                            "llama7b_smallbatch_m64", "llama7b_prefill_m2048", "quantize_llama7b", "ldlq_layer4096"])
+    p.add_argument("--workload", default=None,
+                   choices=["llama7b_decode_m1", *SUB_WORKLOADS, "quantize_llama7b", "ldlq_layer4096"],
+                   help="time this workload only (default: the 7B M = 1 headline plus a sub-record per "
+                        "configured workload)")
     p.add_argument("--fold", action="store_true",
-                   help="with --affine matrix/group and a GEMM workload: the Eq. 9 fold "
+                   help="with --affine matrix/group and a workload above 4 tokens: the Eq. 9 fold "
                         "(unisvq_gemm_shared_fold) instead of the decode path")
     p.add_argument("--affine", default="row_group", choices=["row_group", "matrix", "group"],
                    help="row_group: one (A, B) pair per (row, 128-column group), stored with the codes (the "
@@ -78,17 +94,15 @@ def parse():
                         "(how a decode step runs them); per_layer: one launch per linear; single: all "
                         "linears in one batched launch")
     p.add_argument("--rht", action="store_true",
-                   help="also time the decoder step of a layer quantised in the rotated basis (Eq. 5): per "
-                        "launch group, one input transform of its activations, the batched product and one "
-                        "output transform of the group's stacked outputs")
+                   help="also time the decoder step of a layer quantised in the rotated basis (Eq. 5)")
     p.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                    help="only run a plain device-to-device copy of BYTES bytes 10 times (counter calibration)")
     p.add_argument("--no-schedules", action="store_true",
-                   help="time only the --schedule launch sequence (for profiling runs)")
+                   help="skip the other launch schedules, the per-launch pass and the plain-read line "
+                        "(profiling runs)")
+    p.add_argument("--no-sub", action="store_true", help="skip the per-config sub-records")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU work of the oracle sample")
-    p.add_argument("--no-launch-events", action="store_true",
-                   help="skip the per-launch event pass (roofline fields become null)")
     return p.parse_args()
 
 
@@ -96,10 +110,6 @@ def parse():
 KERNEL_SOURCES = {"gemv": ("gemv.hip", "gemv_kernel.hpp", "common.hpp"),
                   "gemm": ("gemm.hip", "decode.hpp", "common.hpp"),
                   "skinny": ("skinny.hip", "decode.hpp", "common.hpp")}
-
-
-# Largest batch the 2x4 product sends to the skinny kernel (kSkinnyMaxM).
-SKINNY_MAX_M = 32
 
 
 def kernel_source_hash(kernel: str) -> str:
@@ -112,8 +122,7 @@ def kernel_source_hash(kernel: str) -> str:
 
 def measured_traffic(kernel: str, workload: str, schedule: str):
     """HBM bytes per launch from the committed counter summary, if it was taken
-    on the current kernel source; else None.  (workload carries a suffix for
-    the row-shared modes.)"""
+    on the current kernel source; else None."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_{schedule}_traffic.json")
     if not os.path.exists(path):
         return None
@@ -136,21 +145,30 @@ def calibrate_copy(nbytes: int):
 
 
 def workload_spec(name: str):
-    """(layers, M, activation dtype, outliers, kernel)"""
+    """(layers, M, activation dtype, outlier channels)"""
     if name == "llama7b_decode_m1":
-        return wl.LLAMA7B, 1, "f16", False, "gemv"
+        return wl.LLAMA7B, 1, "f16", False
     if name == "layer4096_m1":
-        return (wl.Layer("layer", 4096, 4096),), 1, "f16", False, "gemv"
+        return (wl.Layer("layer", 4096, 4096),), 1, "f16", False
     if name == "llama70b_decode_m1":
-        return wl.LLAMA70B, 1, "f16", False, "gemv"
+        return wl.LLAMA70B, 1, "f16", False
     if name == "llama70b_decode_m16":
-        return wl.LLAMA70B, 16, "f16", False, "gemm"
+        return wl.LLAMA70B, 16, "f16", False
     if name.startswith("llama7b_smallbatch_m"):
-        M = int(name.rsplit("m", 1)[1])
-        return wl.LLAMA7B, M, "f16", True, ("gemv" if M <= 4 else "gemm")
+        return wl.LLAMA7B, int(name.rsplit("m", 1)[1]), "f16", True
     if name == "llama7b_prefill_m2048":
-        return wl.PREFILL7B, 2048, "bf16", False, "gemm"
+        return wl.PREFILL7B, 2048, "bf16", False
     raise ValueError(name)
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 PEAK_FP64_TFLOPS = 78.6   # MI355X fp64 vector, datasheet
@@ -360,457 +378,603 @@ def bench_ldlq(args):
     print(json.dumps(out), flush=True)
 
 
+
+
+# ---------------------------------------------------------------------------
+# Product workloads: packed weight sets, launch schedules, graph timing.
+
+class WeightSet:
+    """A layer set packed on the GPU in one weight format, with enough copies
+    (> 2x the 256 MB Infinity Cache) for every step to stream from HBM."""
+
+    def __init__(self, u, torch, layers, affine="row_group", bits=2, dim=4, keep_host=False):
+        self.u, self.torch = u, torch
+        self.layers, self.affine, self.bits, self.dim = layers, affine, bits, dim
+        self.var = (bits, dim) != (2, 4)
+        self.shared = affine != "row_group"
+        dev = torch.device("cuda:0")
+
+        def dev_half(a):
+            return torch.from_numpy(a.view(np.int16)).view(torch.float16).to(dev)
+
+        self.host = []
+        packed0 = []
+        for li, L in enumerate(layers):
+            if self.var:
+                Q, A, B = wl.gen_var_weights(L.N, L.K, bits, dim, affine_groups(L.K, affine), seed=li)
+                pk = u.var_pack(torch.from_numpy(Q).to(dev), dev_half(A), dev_half(B), bits, dim)
+            elif self.shared:
+                Q, A, B = wl.gen_shared_weights(L.N, L.K, affine_groups(L.K, affine), seed=li)
+                pk = u.pack_shared(torch.from_numpy(Q).to(dev), dev_half(A), dev_half(B))
+            else:
+                Q, A, B = wl.gen_weights(L.N, L.K, seed=li)
+                pk = u.pack(torch.from_numpy(Q).to(dev), dev_half(A), dev_half(B))
+            packed0.append(pk)
+            self.host.append((Q, A, B) if keep_host else None)
+        self.packed_bytes = sum((u.var_codes_bytes(L.N, L.K, bits, dim) if self.var else
+                                 u.codes_bytes(L.N, L.K) if self.shared else u.packed_bytes(L.N, L.K))
+                                for L in layers)
+        self.copies = max(2, -(-2 * MALL_BYTES // self.packed_bytes) + 1)
+        self.packed = [packed0]
+        for _ in range(1, self.copies):
+            self.packed.append([tuple(t.clone() for t in pk) if isinstance(pk, tuple) else pk.clone()
+                                for pk in packed0])
+        torch.cuda.synchronize()
+
+    def weight_buffers(self, c, li):
+        """Device tensors the product streams for layer li of copy c."""
+        pk = self.packed[c][li]
+        return [pk[0]] if isinstance(pk, tuple) else [pk]
+
+
+class Case:
+    """One workload (weight set, token count, activation type) with its launch
+    schedule; x and y per layer and copy."""
+
+    def __init__(self, ws: WeightSet, M: int, xdt: str, outliers: bool, fold: bool = False):
+        u, torch = ws.u, ws.torch
+        self.ws, self.u, self.torch = ws, u, torch
+        self.M, self.xdt, self.outliers, self.fold = M, xdt, outliers, fold
+        self.lib = u.load()
+        self.tdt = torch.float16 if xdt == "f16" else torch.bfloat16
+        self.xcode = u.F16 if xdt == "f16" else u.BF16
+        self.kernel = "gemv" if M <= 4 else "gemm"
+        dev = torch.device("cuda:0")
+        layers = ws.layers
+        self.x_host = [wl.gen_activations(M, L.K, seed=wl.activation_seed(li, M), dtype=xdt, outliers=outliers)
+                       for li, L in enumerate(layers)]
+        self.xs, self.ys = [], []
+        for c in range(ws.copies):
+            self.xs.append([torch.from_numpy(xb.view(np.int16)).view(self.tdt).to(dev) for xb in self.x_host])
+            self.ys.append([torch.empty((M, L.N), dtype=torch.float16, device=dev) for L in layers])
+        self.set_bytes = sum(algorithmic_bytes(L.N, L.K, M, affine=ws.affine, bits=ws.bits, d=ws.dim)
+                             for L in layers)
+        self.flops = sum(2 * M * L.N * L.K for L in layers)
+        ws_bytes = 0
+        if self.kernel == "gemm":
+            for L in layers:
+                if ws.var:
+                    need = u.var_gemm_workspace_bytes(L.N, L.K, M, self.tdt)
+                elif fold:
+                    need = u.gemm_fold_workspace_bytes(L.N, L.K, M)
+                else:
+                    need = u.gemm_workspace_bytes(L.N, L.K, M, self.tdt)
+                ws_bytes = max(ws_bytes, need)
+        # one workspace serves every call: the calls run in order on one stream
+        self.ws_bytes = ws_bytes
+        self.wsbuf = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+        self.names = [L.name for L in layers]
+        # the plain-read reference's sink: one word per wavefront of the largest launch
+        self.sink = torch.zeros(2 * (self.set_bytes // 8192 + 16 * len(layers)), dtype=torch.int32, device=dev)
+        torch.cuda.synchronize()
+
+    # ---- schedules
+    def groups(self, sched):
+        full_set = {"q", "k", "v", "o", "gate", "up", "down"} <= set(self.names)
+        if self.kernel != "gemv":
+            return "per_layer", [[n] for n in self.names]
+        if sched == "decoder" and full_set:
+            return "decoder", [["q", "k", "v"], ["o"], ["gate", "up"], ["down"]]
+        if sched == "single" and len(self.names) <= self.u.MAX_BATCH:
+            return "single", [self.names]
+        return "per_layer", [[n] for n in self.names]
+
+    def calls(self, groups):
+        """Per buffer copy: the step's launches, each (label, [layer indices])."""
+        idx = {n: i for i, n in enumerate(self.names)}
+        return [[("+".join(g), [idx[n] for n in g]) for g in groups] for _ in range(self.ws.copies)]
+
+    def launch(self, c, lis, sptr):
+        u, lib, ws, M = self.u, self.lib, self.ws, self.M
+        Ls = [ws.layers[i] for i in lis]
+        if len(lis) > 1:
+            if ws.shared or ws.var:
+                arr = (u.GemvSharedProblem * len(lis))()
+                for j, li in enumerate(lis):
+                    L, (pc, pa) = ws.layers[li], ws.packed[c][li]
+                    arr[j] = u.GemvSharedProblem(L.N, L.K, affine_groups(L.K, ws.affine), pc.data_ptr(),
+                                                 pa.data_ptr(), self.xs[c][li].data_ptr(), self.ys[c][li].data_ptr())
+                if ws.var:
+                    return lib.unisvq_var_gemv_batched(arr, len(lis), ws.bits, ws.dim, M, self.xcode, u.F16, sptr)
+                return lib.unisvq_gemv_shared_batched(arr, len(lis), M, self.xcode, u.F16, sptr)
+            arr = (u.GemvProblem * len(lis))()
+            for j, li in enumerate(lis):
+                L = ws.layers[li]
+                arr[j] = u.GemvProblem(L.N, L.K, ws.packed[c][li].data_ptr(), self.xs[c][li].data_ptr(),
+                                       self.ys[c][li].data_ptr())
+            return lib.unisvq_gemv_batched(arr, len(lis), M, self.xcode, u.F16, sptr)
+        li = lis[0]
+        L, pk, x, y = Ls[0], ws.packed[c][li], self.xs[c][li].data_ptr(), self.ys[c][li].data_ptr()
+        wsp, wsb = self.wsbuf.data_ptr(), self.ws_bytes
+        if ws.var:
+            pc, pa = pk
+            ga = affine_groups(L.K, ws.affine)
+            if self.kernel == "gemv":
+                return lib.unisvq_var_gemv(L.N, L.K, ws.bits, ws.dim, ga, pc.data_ptr(), pa.data_ptr(), M, x,
+                                           self.xcode, y, u.F16, sptr)
+            return lib.unisvq_var_gemm(L.N, L.K, ws.bits, ws.dim, ga, pc.data_ptr(), pa.data_ptr(), M, x,
+                                       self.xcode, y, u.F16, wsp, wsb, sptr)
+        if ws.shared:
+            pc, pa = pk
+            ga = affine_groups(L.K, ws.affine)
+            if self.kernel == "gemv":
+                return lib.unisvq_gemv_shared(L.N, L.K, ga, pc.data_ptr(), pa.data_ptr(), M, x, self.xcode, y,
+                                              u.F16, sptr)
+            fn = lib.unisvq_gemm_shared_fold if self.fold else lib.unisvq_gemm_shared
+            return fn(L.N, L.K, ga, pc.data_ptr(), pa.data_ptr(), M, x, self.xcode, y, u.F16, wsp, wsb, sptr)
+        if self.kernel == "gemv":
+            return lib.unisvq_gemv(L.N, L.K, pk.data_ptr(), M, x, self.xcode, y, u.F16, sptr)
+        return lib.unisvq_gemm(L.N, L.K, pk.data_ptr(), M, x, self.xcode, y, u.F16, wsp, wsb, sptr)
+
+    def read_only(self, c, lis, sptr):
+        return self.read(c, lis, sptr, 0)
+
+    def read_store(self, c, lis, sptr):
+        return self.read(c, lis, sptr, 1)
+
+    def read(self, c, lis, sptr, store):
+        """The plain-read reference of one launch: the same weight and
+        activation buffers, one launch; with `store` each wavefront also
+        stores one word (about 4 bytes per KB read, of the order of the
+        product's output)."""
+        bufs = []
+        for li in lis:
+            bufs += self.ws.weight_buffers(c, li) + [self.xs[c][li]]
+        arr = (self.u.ByteRange * len(bufs))()
+        for j, t in enumerate(bufs):
+            arr[j] = self.u.ByteRange(t.data_ptr(), (t.numel() * t.element_size()) // 16 * 16)
+        return self.lib.unisvq_read_bytes(arr, len(bufs), store, self.sink.data_ptr(), self.sink.numel(), sptr)
+
+    def run_step(self, calls, i, sptr, fn=None):
+        fn = fn or self.launch
+        for _, lis in calls[i % self.ws.copies]:
+            st = fn(i % self.ws.copies, lis, sptr)
+            if st != 0:
+                raise RuntimeError(f"{self.kernel} launch failed with status {st}")
+
+    def time_steps(self, calls, nsteps, warmup, fn=None):
+        """Warm up eagerly, capture exactly `nsteps` steps (rotating over the
+        copies) in one HIP graph, replay it once untimed and once between two
+        events; returns ms per step."""
+        torch = self.torch
+        stream = torch.cuda.current_stream()
+        for i in range(warmup):
+            self.run_step(calls, i, stream.cuda_stream, fn)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            cap = torch.cuda.current_stream().cuda_stream
+            for i in range(nsteps):
+                self.run_step(calls, i, cap, fn)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        graph.replay()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        del graph
+        return t0.elapsed_time(t1) / nsteps
+
+    def per_launch_us(self, groups, reps):
+        """Graph-timed duration of each launch of the schedule: `reps`
+        back-to-back launches of that launch alone (rotating over the copies)."""
+        out = {}
+        for g in groups:
+            one = self.calls([g])
+            out["+".join(g)] = round(self.time_steps(one, reps, 2) * 1e3, 3)
+        return out
+
+
+def hbm_roofline(kernel_name, bytes_per_step, launches, ms_per_step, traffic=None):
+    avg_us = ms_per_step * 1e3 / launches
+    bpl = bytes_per_step / launches
+    ach = bpl / (avg_us * 1e-6) / 1e9
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None if traffic is None else int(traffic),
+            "kernel": kernel_name, "avg_launch_us": round(avg_us, 3), "bytes_per_launch": int(bpl)}
+
+
+def mfma_roofline(kernel_name, flops_per_step, launches, ms_per_step, traffic=None):
+    avg_us = ms_per_step * 1e3 / launches
+    ach = flops_per_step / launches / (avg_us * 1e-6) / 1e12
+    return {"bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None if traffic is None else int(traffic),
+            "kernel": kernel_name, "avg_launch_us": round(avg_us, 3)}
+
+
+def product_kernel_name(case):
+    if case.kernel == "gemv":
+        return "gemv_kernel"
+    if not case.ws.var and not case.fold and case.M <= SKINNY_MAX_M:
+        return "skinny_kernel"
+    return "gemm_kernel"
+
+
+# Largest batch the 2x4 product sends to the small-batch kernel.
+SKINNY_MAX_M = 32
+
+
+def measure_case(case, sched_name, nsteps, warmup, extras=True, traffic_key=None):
+    """Time one workload: the step (graph of nsteps steps), and optionally the
+    per-launch durations and the plain read of the same buffers."""
+    sched, groups = case.groups(sched_name)
+    calls = case.calls(groups)
+    ms = case.time_steps(calls, nsteps, warmup)
+    rec = {"schedule": sched, "launches_per_step": len(groups), "steps": nsteps, "ms_per_step": round(ms, 5),
+           "buffer_copies": case.ws.copies, "set_bytes": case.set_bytes}
+    kname = product_kernel_name(case)
+    bandwidth_bound = case.M <= 64
+    traffic = None
+    if traffic_key is not None:
+        traffic = measured_traffic(kname.replace("_kernel", ""), traffic_key, sched)
+    if bandwidth_bound:
+        gbs = case.set_bytes / (ms * 1e-3) / 1e9
+        rec.update({"value": round(gbs, 2), "unit": "GB/s", "pct_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2)})
+        rec["roofline"] = hbm_roofline(kname, case.set_bytes, len(groups), ms, traffic)
+    else:
+        tf = case.flops / (ms * 1e-3) / 1e12
+        rec.update({"value": round(tf, 2), "unit": "TFLOP/s"})
+        rec["roofline"] = mfma_roofline(kname, case.flops, len(groups), ms, traffic)
+    if extras:
+        rec["per_launch_us"] = case.per_launch_us(groups, max(8, min(nsteps, 60)))
+        if bandwidth_bound:
+            rms = case.time_steps(calls, nsteps, 2, fn=case.read_only)
+            sms = case.time_steps(calls, nsteps, 2, fn=case.read_store)
+            rec["achievable"] = {
+                "what": "plain read (unisvq_read_bytes) of the same weight and activation buffers, one launch per "
+                        "launch of the schedule; read_only writes nothing, read_and_store also stores one word per "
+                        "wavefront (a kernel that writes any output pays a fixed end-of-launch cost)",
+                "read_only": {"ms_per_step": round(rms, 5), "GB_per_s": round(case.set_bytes / (rms * 1e-3) / 1e9, 1),
+                              "product_over_read_time": round(ms / rms, 4)},
+                "read_and_store": {"ms_per_step": round(sms, 5),
+                                   "GB_per_s": round(case.set_bytes / (sms * 1e-3) / 1e9, 1),
+                                   "product_over_read_time": round(ms / sms, 4)}}
+    return rec, calls, groups
+
+
+def dense_baseline(torch, layers, M, tdt, x_host, reps):
+    """Dense products of the same shapes (random bf16/fp16 weights): torch.matmul
+    (hipBLASLt) eagerly, each shape timed between events, and the same
+    products captured in one graph."""
+    dev = torch.device("cuda:0")
+    wts = [torch.randn(L.K, L.N, device=dev).to(tdt) for L in layers]  # K x N, contiguous
+    xs = [torch.from_numpy(xb.view(np.int16)).view(tdt).to(dev) for xb in x_host]
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        for x_, w_ in zip(xs, wts):
+            torch.matmul(x_, w_)
+    torch.cuda.synchronize()
+    eager_ms = 0.0
+    per = {}
+    for L, x_, w_ in zip(layers, xs, wts):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            torch.matmul(x_, w_)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / reps
+        per[L.name] = round(t * 1e3, 2)
+        eager_ms += t
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        outs = [torch.matmul(x_, w_) for x_, w_ in zip(xs, wts)]
+    g.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    graph_ms = e0.elapsed_time(e1) / reps
+    del outs, g, wts, xs
+    flops = sum(2 * M * L.N * L.K for L in layers)
+    kind = "bf16" if tdt == torch.bfloat16 else "fp16"
+    return {"what": f"torch.matmul (hipBLASLt), dense {kind} weights of the same shapes",
+            "eager": {"ms_per_step": round(eager_ms, 5), "TFLOP_per_s": round(flops / (eager_ms * 1e-3) / 1e12, 1),
+                      "per_shape_us": per},
+            "graph": {"ms_per_step": round(graph_ms, 5), "TFLOP_per_s": round(flops / (graph_ms * 1e-3) / 1e12, 1)}}
+
+
+def rotated_step(case, nsteps, warmup):
+    """Decoder step of a layer quantised in the rotated basis (Eq. 5): per
+    launch group one input transform, the batched product, one output
+    transform of the group's stacked outputs (12 launches); and the same with
+    the input transforms of the q+k+v and o groups inside their products."""
+    torch, u, lib, ws, M = case.torch, case.u, case.lib, case.ws, case.M
+    dev = torch.device("cuda:0")
+    rgroups = [["q", "k", "v"], ["o"], ["gate", "up"], ["down"]]
+    idx = {n: i for i, n in enumerate(case.names)}
+    rng = np.random.default_rng(123)
+    signs = {}
+    for grp in rgroups:
+        L0 = ws.layers[idx[grp[0]]]
+        signs[grp[0]] = (torch.from_numpy(rng.choice(np.array([-1, 1], np.int8), L0.K)).to(dev),
+                         torch.from_numpy(rng.choice(np.array([-1, 1], np.int8), L0.N)).to(dev))
+    bufs = []
+    for c in range(ws.copies):
+        cc = []
+        for grp in rgroups:
+            L0 = ws.layers[idx[grp[0]]]
+            xin = case.xs[c][idx[grp[0]]]
+            cc.append((grp, L0.N, L0.K, xin, torch.empty_like(xin),
+                       torch.empty((len(grp) * M, L0.N), dtype=torch.float16, device=dev),
+                       torch.empty((len(grp) * M, L0.N), dtype=torch.float16, device=dev)))
+        bufs.append(cc)
+
+    def step(i, sptr, fused):
+        c = i % ws.copies
+        for (grp, N, K, xin, xrot, ystk, yout) in bufs[c]:
+            sV, sU = signs[grp[0]]
+            cnt = len(grp)
+            arr = (u.GemvProblem * cnt)()
+            # fused where the launch has at most 3 row blocks per CU: beyond that
+            # the transform each workgroup repeats outweighs the saved launch
+            fuse = fused and K in (4096, 8192) and N * cnt // 16 <= 768
+            for j, n in enumerate(grp):
+                L = ws.layers[idx[n]]
+                arr[j] = u.GemvProblem(L.N, L.K, ws.packed[c][idx[n]].data_ptr(),
+                                       (xin if fuse else xrot).data_ptr(), ystk[j * M:(j + 1) * M].data_ptr())
+            if fuse:
+                sg = (ctypes.c_void_p * cnt)(*([sV.data_ptr()] * cnt))
+                sts = (lib.unisvq_gemv_rht_batched(arr, cnt, M, case.xcode, u.F16, sg, sptr),)
+            else:
+                sts = (lib.unisvq_rht(K, M, xin.data_ptr(), case.xcode, sV.data_ptr(), 0, xrot.data_ptr(), u.F16,
+                                      sptr),
+                       lib.unisvq_gemv_batched(arr, cnt, M, u.F16, u.F16, sptr))
+            sts += (lib.unisvq_rht(N, cnt * M, ystk.data_ptr(), u.F16, sU.data_ptr(), 1, yout.data_ptr(), u.F16,
+                                   sptr),)
+            for st in sts:
+                if st != 0:
+                    raise RuntimeError(f"rotated step failed with status {st}")
+
+    def timed(fused):
+        stream = torch.cuda.current_stream()
+        for i in range(warmup):
+            step(i, stream.cuda_stream, fused)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            cap = torch.cuda.current_stream().cuda_stream
+            for i in range(nsteps):
+                step(i, cap, fused)
+        g.replay()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        del g
+        return e0.elapsed_time(e1) / nsteps
+
+    rms, fms = timed(False), timed(True)
+    return {"what": "decoder step of a layer quantised in the rotated basis: 4 input transforms, 4 batched "
+                    "products, 4 output transforms (12 launches)",
+            "ms_per_step": round(rms, 5), "GB_per_s": round(case.set_bytes / (rms * 1e-3) / 1e9, 1),
+            "fused": {"what": "the same step with the input transforms of the q+k+v and o launch groups inside "
+                              "their products (unisvq_gemv_rht_batched; 10 launches)",
+                      "ms_per_step": round(fms, 5), "GB_per_s": round(case.set_bytes / (fms * 1e-3) / 1e9, 1)}}
+
+
+def cpu_baseline(case, workload, seconds):
+    """The fp64 oracle (test infrastructure, untuned) on the host cores over
+    the same layer set: T threads for about `seconds`, then one thread on a
+    slice of the output rows."""
+    import oracle
+    ws = case.ws
+    threads = oracle.default_threads()
+    if ws.var:
+        packed_h = [oracle.var_pack_codes(Q, ws.bits, ws.dim)[0] for (Q, A, B) in ws.host]
+    elif ws.shared:
+        packed_h = [oracle.pack_codes(Q)[0] for (Q, A, B) in ws.host]
+    else:
+        packed_h = [oracle.pack(Q, A, B)[0] for (Q, A, B) in ws.host]
+    xs = [oracle.half_to_double(xb) if case.xdt == "f16" else oracle.bf16_to_double(xb) for xb in case.x_host]
+
+    def run(rows_frac, nthreads, budget):
+        done, t_cpu, passes = 0.0, 0.0, 0
+        while t_cpu < budget or passes == 0:
+            for li, L in enumerate(ws.layers):
+                Q, A, B = ws.host[li]
+                nrows = max(16, int(L.N * rows_frac))
+                rows = None if nrows >= L.N else np.arange(nrows)
+                s0 = time.perf_counter()
+                if ws.var:
+                    oracle.var_matmul(packed_h[li], L.N, L.K, ws.bits, A, B, xs[li], rows=rows, threads=nthreads)
+                elif ws.shared:
+                    oracle.matmul_shared(packed_h[li], L.N, L.K, A, B, xs[li], rows=rows, threads=nthreads)
+                else:
+                    oracle.matmul(packed_h[li], L.N, L.K, xs[li], rows=rows, threads=nthreads)
+                t_cpu += time.perf_counter() - s0
+                done += algorithmic_bytes(L.N, L.K, case.M, affine=ws.affine, bits=ws.bits, d=ws.dim) * (nrows / L.N)
+            passes += 1
+        return done / t_cpu / 1e9, passes, t_cpu
+
+    frac = 1.0 if case.M <= 16 else 1.0 / 64
+    v, passes, t = run(frac, threads, seconds)
+    v1, p1, t1 = run(frac / 8, 1, seconds / 2)
+    return {"value": round(v, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{passes} pass(es) over the {workload} layer set"
+                      + ("" if frac == 1.0 else f" (1/{int(1 / frac)} of output rows)")
+                      + f", fp64 C oracle, {threads} threads, {t:.1f} s",
+            "one_thread": {"value": round(v1, 4), "unit": "GB/s",
+                           "sample": f"{p1} pass(es) over 1/{int(8 / frac)} of the output rows of each layer, "
+                                     f"one thread, {t1:.1f} s"},
+            "cpu_model": cpu_model()}
+
+
+def sub_records(u, torch, main_ws, args):
+    """One record per configured workload besides the headline."""
+    out = {}
+    ws4096 = WeightSet(u, torch, (wl.Layer("layer", 4096, 4096),))
+    c = Case(ws4096, 1, "f16", False)
+    out["layer4096_m1"], _, _ = measure_case(c, "decoder", 100, 10)
+    del c, ws4096
+    for M in (4, 16, 64):
+        c = Case(main_ws, M, "f16", True)
+        out[f"llama7b_smallbatch_m{M}"], _, _ = measure_case(c, "decoder", 60, 5)
+        del c
+    ws70 = WeightSet(u, torch, wl.LLAMA70B)
+    for M in (1, 16):
+        c = Case(ws70, M, "f16", False)
+        out[f"llama70b_decode_m{M}"], _, _ = measure_case(c, "decoder", 30, 3)
+        del c
+    del ws70
+    wsp = WeightSet(u, torch, wl.PREFILL7B)
+    c = Case(wsp, 2048, "bf16", False)
+    rec, _, _ = measure_case(c, "decoder", 10, 2)
+    rec["what"] = "decode path, one (A, B) pair per (row, 128-column group)"
+    rec["dense_bf16"] = dense_baseline(torch, wsp.layers, 2048, c.tdt, c.x_host, 10)
+    rec["over_dense_eager_time"] = round(rec["ms_per_step"] / rec["dense_bf16"]["eager"]["ms_per_step"], 3)
+    del c, wsp
+    wsm = WeightSet(u, torch, wl.PREFILL7B, affine="matrix")
+    c = Case(wsm, 2048, "bf16", False, fold=True)
+    fold, _, _ = measure_case(c, "decoder", 10, 2)
+    fold["what"] = "Eq. 9 fold (unisvq_gemm_shared_fold), one (A, B) pair per matrix (the paper's setting)"
+    fold["over_dense_eager_time"] = round(fold["ms_per_step"] / rec["dense_bf16"]["eager"]["ms_per_step"], 3)
+    rec["fold"] = fold
+    del c, wsm
+    out["llama7b_prefill_m2048"] = rec
+    for k, v in out.items():
+        v["config_index"] = CONFIG_INDEX[k]
+    return out
+
+
 def main():
     args = parse()
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
         return
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the library has no multi-GPU "
+              "path (column-parallel layers would split N with no exchange, row-parallel ones K on packet "
+              "boundaries followed by one all-reduce of the partial outputs).", file=sys.stderr)
+        sys.exit(2)
     if args.workload == "ldlq_layer4096":
-        if args.gpus != 1:
-            print(f"bench.py measures one GPU only (asked for --gpus {args.gpus})", file=sys.stderr)
-            sys.exit(2)
         bench_ldlq(args)
         return
     if args.workload == "quantize_llama7b":
-        if args.gpus != 1:
-            print("bench.py measures one GPU only", file=sys.stderr)
-            sys.exit(2)
         bench_quantize(args)
         return
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
-              "this build has no multi-GPU path.", file=sys.stderr)
-        sys.exit(2)
 
     import torch
     import paper_2606_10520_amd.unisvq as u
 
     u.load()  # fails loudly if libunisvq.so is missing
-    dev = torch.device("cuda:0")
-    layers, M, xdt, outliers, kernel = workload_spec(args.workload)
-    tdt = torch.float16 if xdt == "f16" else torch.bfloat16
+    headline = args.workload or "llama7b_decode_m1"
+    layers, M, xdt, outliers = workload_spec(headline)
     bits, dim = (int(v) for v in args.format.split("x"))
     var = (bits, dim) != (2, 4)
     if var and args.affine == "row_group":
         args.affine = "matrix"  # the variants keep their pairs shared by the rows
     shared = args.affine != "row_group"
-    wname = args.workload if not shared else f"{args.workload}_{args.affine}_shared" + ("_fold" if args.fold else "")
+    if args.fold and (not shared or var or M <= 4):
+        print("--fold needs row-shared pairs (--affine matrix or group), the 2x4 format and more than 4 tokens "
+              "(the fold is a unisvq_gemm_shared_fold path)", file=sys.stderr)
+        sys.exit(2)
+    wname = headline if not shared else f"{headline}_{args.affine}_shared" + ("_fold" if args.fold else "")
     if var:
         wname += f"_b{bits}d{dim}"
 
-    # ---- inputs: canonical arrays drawn on the host, packed on the GPU
-    canon = []
-    for li, L in enumerate(layers):
-        if var:
-            Q, A, B = wl.gen_var_weights(L.N, L.K, bits, dim, affine_groups(L.K, args.affine), seed=li)
-        elif shared:
-            Q, A, B = wl.gen_shared_weights(L.N, L.K, affine_groups(L.K, args.affine), seed=li)
-        else:
-            Q, A, B = wl.gen_weights(L.N, L.K, seed=li)
-        xb = wl.gen_activations(M, L.K, seed=wl.activation_seed(li, M), dtype=xdt, outliers=outliers)
-        canon.append((Q, A, B, xb))
-    set_bytes = sum(algorithmic_bytes(L.N, L.K, M, affine=args.affine, bits=bits, d=dim) for L in layers)
-    set_packed = sum((u.var_codes_bytes(L.N, L.K, bits, dim) if var else
-                      u.codes_bytes(L.N, L.K) if shared else u.packed_bytes(L.N, L.K)) for L in layers)
-    copies = max(2, -(-2 * MALL_BYTES // set_packed) + 1)
-
-    def dev_half(a):
-        return torch.from_numpy(a.view(np.int16)).view(torch.float16).to(dev)
-
-    packed0 = []
-    for (Q, A, B, _), L in zip(canon, layers):
-        if var:
-            packed0.append(u.var_pack(torch.from_numpy(Q).to(dev), dev_half(A), dev_half(B), bits, dim))
-        elif shared:
-            packed0.append(u.pack_shared(torch.from_numpy(Q).to(dev), dev_half(A), dev_half(B)))
-        else:
-            packed0.append(u.pack(torch.from_numpy(Q).to(dev), dev_half(A), dev_half(B)))
-    sets = []
-    for c in range(copies):
-        s = []
-        for li, L in enumerate(layers):
-            if shared:
-                pk = packed0[li] if c == 0 else tuple(t.clone() for t in packed0[li])
-            else:
-                pk = packed0[li] if c == 0 else packed0[li].clone()
-            x = torch.from_numpy(canon[li][3].view(np.int16)).view(tdt).to(dev)
-            y = torch.empty((M, L.N), dtype=torch.float16, device=dev)
-            s.append((L, pk, x, y))
-        sets.append(s)
-    torch.cuda.synchronize()
-
-    lib = u.load()
-    xcode = u.F16 if xdt == "f16" else u.BF16
-    # GEMM workspace (bf16 activation copy, K-split partials): one buffer
-    # serves every call, since the calls run in order on one stream.
-    ws_bytes = 0
-    if kernel == "gemm":
-        wsf = u.var_gemm_workspace_bytes if var else u.gemm_workspace_bytes
-        ws_bytes = max(wsf(L.N, L.K, M, tdt) for L in layers)
-    if args.fold and shared and kernel == "gemm":
-        ws_bytes = max(ws_bytes, max(u.gemm_fold_workspace_bytes(L.N, L.K, M) for L in layers))
-    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
-    names = [L.name for L in layers]
-    full_set = {"q", "k", "v", "o", "gate", "up", "down"} <= set(names)
-
-    def schedule_groups(sched):
-        if kernel != "gemv":
-            return "per_layer", [[n] for n in names]
-        if sched == "decoder" and full_set:
-            return "decoder", [["q", "k", "v"], ["o"], ["gate", "up"], ["down"]]
-        if sched == "single" and len(names) <= u.MAX_BATCH:
-            return "single", [names]
-        return "per_layer", [[n] for n in names]
-
-    def build_calls(groups_):
-        calls = []  # per buffer copy: list of (label, single-problem tuple or ctypes problem array)
-        for s_ in sets:
-            by = {L.name: (L, pk, x, y) for (L, pk, x, y) in s_}
-            cc = []
-            for grp in groups_:
-                if len(grp) == 1:
-                    cc.append(("+".join(grp), by[grp[0]]))
-                elif shared:
-                    arr = (u.GemvSharedProblem * len(grp))()
-                    for i, n in enumerate(grp):
-                        L, (pc, pa), x, y = by[n]
-                        arr[i] = u.GemvSharedProblem(L.N, L.K, affine_groups(L.K, args.affine), pc.data_ptr(),
-                                                     pa.data_ptr(), x.data_ptr(), y.data_ptr())
-                    cc.append(("+".join(grp), arr))
-                else:
-                    arr = (u.GemvProblem * len(grp))()
-                    for i, n in enumerate(grp):
-                        L, pk, x, y = by[n]
-                        arr[i] = u.GemvProblem(L.N, L.K, pk.data_ptr(), x.data_ptr(), y.data_ptr())
-                    cc.append(("+".join(grp), arr))
-            calls.append(cc)
-        return calls
-
-    def launch(item, sptr):
-        if var:
-            if not isinstance(item, tuple):
-                return lib.unisvq_var_gemv_batched(item, len(item), bits, dim, M, xcode, u.F16, sptr)
-            L, (pc, pa), x, y = item
-            ga = affine_groups(L.K, args.affine)
-            if kernel == "gemv":
-                return lib.unisvq_var_gemv(L.N, L.K, bits, dim, ga, pc.data_ptr(), pa.data_ptr(), M, x.data_ptr(),
-                                           xcode, y.data_ptr(), u.F16, sptr)
-            return lib.unisvq_var_gemm(L.N, L.K, bits, dim, ga, pc.data_ptr(), pa.data_ptr(), M, x.data_ptr(),
-                                       xcode, y.data_ptr(), u.F16, ws.data_ptr(), ws_bytes, sptr)
-        if isinstance(item, tuple) and shared:
-            L, (pc, pa), x, y = item
-            ga = affine_groups(L.K, args.affine)
-            if kernel == "gemv":
-                return lib.unisvq_gemv_shared(L.N, L.K, ga, pc.data_ptr(), pa.data_ptr(), M, x.data_ptr(), xcode,
-                                              y.data_ptr(), u.F16, sptr)
-            if args.fold:
-                return lib.unisvq_gemm_shared_fold(L.N, L.K, ga, pc.data_ptr(), pa.data_ptr(), M, x.data_ptr(),
-                                                   xcode, y.data_ptr(), u.F16, ws.data_ptr(), ws_bytes, sptr)
-            return lib.unisvq_gemm_shared(L.N, L.K, ga, pc.data_ptr(), pa.data_ptr(), M, x.data_ptr(), xcode,
-                                          y.data_ptr(), u.F16, ws.data_ptr(), ws_bytes, sptr)
-        if shared:
-            return lib.unisvq_gemv_shared_batched(item, len(item), M, xcode, u.F16, sptr)
-        if isinstance(item, tuple):
-            L, pk, x, y = item
-            if kernel == "gemv":
-                return lib.unisvq_gemv(L.N, L.K, pk.data_ptr(), M, x.data_ptr(), xcode, y.data_ptr(), u.F16, sptr)
-            return lib.unisvq_gemm(L.N, L.K, pk.data_ptr(), M, x.data_ptr(), xcode, y.data_ptr(), u.F16,
-                                   ws.data_ptr(), ws_bytes, sptr)
-        return lib.unisvq_gemv_batched(item, len(item), M, xcode, u.F16, sptr)
-
-    def run_step(calls, i, sptr):
-        for _, item in calls[i % copies]:
-            st = launch(item, sptr)
-            if st != 0:
-                raise RuntimeError(f"{kernel} failed with status {st}")
-
-    stream = torch.cuda.current_stream()
-
-    def time_schedule(calls):
-        """Warm up, capture the steps of all buffer copies in one HIP graph, and
-        time ceil(steps / copies) replays between two events."""
-        for i in range(args.warmup):
-            run_step(calls, i, stream.cuda_stream)
-        torch.cuda.synchronize()
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            cap = torch.cuda.current_stream().cuda_stream
-            for c in range(copies):
-                run_step(calls, c, cap)
-        torch.cuda.synchronize()
-        graph.replay()  # one untimed replay
-        torch.cuda.synchronize()
-        replays = max(1, -(-args.steps // copies))
-        t0 = torch.cuda.Event(enable_timing=True)
-        t1 = torch.cuda.Event(enable_timing=True)
-        t0.record(stream)
-        for _ in range(replays):
-            graph.replay()
-        t1.record(stream)
-        torch.cuda.synchronize()
-        return t0.elapsed_time(t1) / (replays * copies), replays * copies
-
-    sched, groups_ = schedule_groups(args.schedule)
-    calls = build_calls(groups_)
-    ms_per_step, steps_done = time_schedule(calls)
-    value_gbs = set_bytes / (ms_per_step * 1e-3) / 1e9
-
-    # a dense product of the same shapes (random weights, the activation
-    # dtype), timed the same way: the library GEMM the decode would compete with
-    dense = None
-    if kernel == "gemm":
-        wts = [torch.randn(L.K, L.N, device=dev).to(tdt) for L in layers]  # K x N, contiguous
-        xs_d = [torch.from_numpy(canon[li][3].view(np.int16)).view(tdt).to(dev) for li in range(len(layers))]
-        for i in range(3):
-            for x_, w_ in zip(xs_d, wts):
-                torch.matmul(x_, w_)
-        torch.cuda.synchronize()
-        g_d = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g_d):
-            outs = [torch.matmul(x_, w_) for x_, w_ in zip(xs_d, wts)]
-        g_d.replay()
-        torch.cuda.synchronize()
-        reps = max(3, args.steps // 4)
-        d0 = torch.cuda.Event(enable_timing=True)
-        d1 = torch.cuda.Event(enable_timing=True)
-        d0.record(stream)
-        for _ in range(reps):
-            g_d.replay()
-        d1.record(stream)
-        torch.cuda.synchronize()
-        dms = d0.elapsed_time(d1) / reps
-        dflops = sum(2 * M * L.N * L.K for L in layers)
-        dense = {"what": f"torch.matmul, dense {'fp16' if xdt == 'f16' else 'bf16'} weights of the same shapes",
-                 "ms_per_step": round(dms, 5), "TFLOP_per_s": round(dflops / (dms * 1e-3) / 1e12, 1),
-                 "unisvq_over_dense_time": round(ms_per_step / dms, 3)}
-        del wts, xs_d, outs, g_d
-
-    # the other launch schedules of the same step, for context
+    ws = WeightSet(u, torch, layers, args.affine, bits, dim, keep_host=not args.no_cpu_baseline)
+    case = Case(ws, M, xdt, outliers, fold=args.fold)
+    rec, calls, groups = measure_case(case, args.schedule, args.steps, args.warmup, extras=not args.no_schedules,
+                                      traffic_key=wname)
     schedules = {}
-    if kernel == "gemv" and not args.no_schedules:
+    if case.kernel == "gemv" and not args.no_schedules:
         for other in ("per_layer", "decoder", "single"):
-            oname, ogroups = schedule_groups(other)
+            oname, ogroups = case.groups(other)
             if oname != other:
                 continue
-            oms = ms_per_step if oname == sched else time_schedule(build_calls(ogroups))[0]
+            oms = rec["ms_per_step"] if oname == rec["schedule"] else case.time_steps(case.calls(ogroups), 60, 2)
             schedules[oname] = {"launches_per_step": len(ogroups), "ms_per_step": round(oms, 5),
-                                "GB_per_s": round(set_bytes / (oms * 1e-3) / 1e9, 1)}
-
-    # ---- the rotated layer (Eq. 5): transforms around each launch group
-    rht = None
-    if args.rht and kernel == "gemv" and not shared and full_set:
-        rgroups = [["q", "k", "v"], ["o"], ["gate", "up"], ["down"]]
-        rng = np.random.default_rng(123)
-        rcalls = []
-        for s_ in sets:
-            by = {L.name: (L, pk, x, y) for (L, pk, x, y) in s_}
-            cc = []
-            for grp in rgroups:
-                Ls = [by[n][0] for n in grp]
-                N, K = Ls[0].N, Ls[0].K
-                sV = torch.from_numpy(rng.choice(np.array([-1, 1], np.int8), K)).to(dev)
-                sU = torch.from_numpy(rng.choice(np.array([-1, 1], np.int8), N)).to(dev)
-                xin = by[grp[0]][2]                                   # the group's activations
-                xrot = torch.empty_like(xin)
-                ystk = torch.empty((len(grp) * M, N), dtype=torch.float16, device=dev)
-                yout = torch.empty_like(ystk)
-                arr = (u.GemvProblem * len(grp))()
-                for i, n in enumerate(grp):
-                    L, pk, _, _ = by[n]
-                    arr[i] = u.GemvProblem(L.N, L.K, pk.data_ptr(), xrot.data_ptr(), ystk[i * M:(i + 1) * M].data_ptr())
-                cc.append((K, M, xin, xcode, sV, xrot, arr, len(grp), N, ystk, sU, yout))
-            rcalls.append(cc)
-
-        def rstep(i, sptr, fused):
-            for (K, M_, xin, xc, sV, xrot, arr, cnt, N, ystk, sU, yout) in rcalls[i % copies]:
-                # fused where the launch has at most 3 row blocks per CU: beyond that
-                # the transform each workgroup repeats outweighs the saved launch
-                if fused and K in (4096, 8192) and N * cnt // 16 <= 768:
-                    # input transform inside the product launch: x enters unrotated
-                    farr = (u.GemvProblem * cnt)()
-                    for j in range(cnt):
-                        farr[j] = u.GemvProblem(arr[j].N, arr[j].K, arr[j].packed, xin.data_ptr(), arr[j].y)
-                    sg = (ctypes.c_void_p * cnt)(*([sV.data_ptr()] * cnt))
-                    calls_ = (lib.unisvq_gemv_rht_batched(farr, cnt, M_, xc, u.F16, sg, sptr),)
-                else:
-                    calls_ = (lib.unisvq_rht(K, M_, xin.data_ptr(), xc, sV.data_ptr(), 0, xrot.data_ptr(), u.F16,
-                                             sptr),
-                              lib.unisvq_gemv_batched(arr, cnt, M_, u.F16, u.F16, sptr))
-                calls_ += (lib.unisvq_rht(N, cnt * M_, ystk.data_ptr(), u.F16, sU.data_ptr(), 1, yout.data_ptr(),
-                                          u.F16, sptr),)
-                for st in calls_:
-                    if st != 0:
-                        raise RuntimeError(f"rotated step failed with status {st}")
-
-        def time_rotated(fused):
-            for i in range(args.warmup):
-                rstep(i, stream.cuda_stream, fused)
-            torch.cuda.synchronize()
-            g_r = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g_r):
-                cap = torch.cuda.current_stream().cuda_stream
-                for c in range(copies):
-                    rstep(c, cap, fused)
-            g_r.replay()
-            torch.cuda.synchronize()
-            reps = max(1, -(-args.steps // copies))
-            r0 = torch.cuda.Event(enable_timing=True)
-            r1 = torch.cuda.Event(enable_timing=True)
-            r0.record(stream)
-            for _ in range(reps):
-                g_r.replay()
-            r1.record(stream)
-            torch.cuda.synchronize()
-            del g_r
-            return r0.elapsed_time(r1) / (reps * copies)
-
-        rms = time_rotated(False)
-        fms = time_rotated(True)
-        rht = {"what": "decoder step of a layer quantised in the rotated basis: 4 input transforms, 4 batched "
-                       "products, 4 output transforms (12 launches)",
-               "ms_per_step": round(rms, 5), "over_plain_step": round(rms / ms_per_step, 3),
-               "GB_per_s": round(set_bytes / (rms * 1e-3) / 1e9, 1),
-               "fused": {"what": "the same step with the input transforms of the q+k+v and o launch groups "
-                                 "inside their products (unisvq_gemv_rht_batched; 10 launches)",
-                         "ms_per_step": round(fms, 5), "over_plain_step": round(fms / ms_per_step, 3),
-                         "GB_per_s": round(set_bytes / (fms * 1e-3) / 1e9, 1)}}
-
-    # ---- per-launch breakdown: HIP events on the launch stream around each
-    # launch.  A spin kernel first lets the host queue a chunk of launches ahead
-    # of the GPU, so an interval brackets GPU work rather than host latency;
-    # each interval still includes one dispatch and two marker packets.
-    per_layer_us = {}
-    if not args.no_launch_events:
-        ev = []
-        chunk = 8
-        for c0 in range(0, args.steps, chunk):
-            torch.cuda.synchronize()
-            torch.cuda._sleep(20_000_000)  # ~8 ms of spinning at 2.4 GHz
-            for i in range(c0, min(args.steps, c0 + chunk)):
-                for label, item in calls[i % copies]:
-                    a = torch.cuda.Event(enable_timing=True)
-                    b = torch.cuda.Event(enable_timing=True)
-                    a.record(stream)
-                    launch(item, stream.cuda_stream)
-                    b.record(stream)
-                    ev.append((label, a, b))
-        torch.cuda.synchronize()
-        durs = {}
-        for name, a, b in ev:
-            durs.setdefault(name, []).append(a.elapsed_time(b) * 1e3)
-        per_layer_us = {k: float(np.mean(v)) for k, v in durs.items()}
-
-    # The roofline's launch duration comes from the timed region itself: the
-    # graph-timed step divided by its launches (events around single launches
-    # would add two marker packets and a dispatch to every interval).
-    launches_per_step = len(groups_)
-    avg_us = ms_per_step * 1e3 / launches_per_step
-    bytes_per_launch = set_bytes / launches_per_step
-    if kernel == "gemv":
-        ach = bytes_per_launch / (avg_us * 1e-6) / 1e9
-        traffic = measured_traffic("gemv", wname, sched)
-        roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                    "frac": round(ach / PEAK_HBM_GBS, 4),
-                    "traffic": None if traffic is None else int(traffic),
-                    "kernel": "gemv_kernel", "avg_launch_us": round(avg_us, 3),
-                    "bytes_per_launch": int(bytes_per_launch)}
-    elif M <= 64:
-        # small batch: still bound by the weight stream.  The 2x4 format at
-        # M <= 32 runs the skinny kernel, everything else the tiled one.
-        kname = "skinny" if (not var and M <= SKINNY_MAX_M) else "gemm"
-        ach = bytes_per_launch / (avg_us * 1e-6) / 1e9
-        traffic = measured_traffic(kname, wname, sched)
-        roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                    "frac": round(ach / PEAK_HBM_GBS, 4),
-                    "traffic": None if traffic is None else int(traffic),
-                    "kernel": f"{kname}_kernel", "avg_launch_us": round(avg_us, 3),
-                    "bytes_per_launch": int(bytes_per_launch)}
-    else:
-        flops = sum(2 * M * L.N * L.K for L in layers) / launches_per_step
-        ach = flops / (avg_us * 1e-6) / 1e12
-        traffic = measured_traffic("gemm", wname, sched)
-        roofline = {"bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS,
-                    "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
-                    "traffic": None if traffic is None else int(traffic),
-                    "kernel": "gemm_kernel", "avg_launch_us": round(avg_us, 3)}
-
-    # ---- CPU baseline: the fp64 oracle on the host cores, bounded sample
+                                "GB_per_s": round(case.set_bytes / (oms * 1e-3) / 1e9, 1)}
+    dense = None
+    if M > 64:
+        dense = dense_baseline(torch, layers, M, case.tdt, case.x_host, 10)
+    rot = None
+    full_set = {"q", "k", "v", "o", "gate", "up", "down"} <= set(case.names)
+    if (args.rht or args.workload is None) and case.kernel == "gemv" and not shared and full_set \
+            and not args.no_schedules:
+        rot = rotated_step(case, 60, 5)
     cpu = None
     if not args.no_cpu_baseline:
-        import oracle
-        threads = oracle.default_threads()
-        if var:
-            packed_h = [oracle.var_pack_codes(Q, bits, dim)[0] for (Q, A, B, _) in canon]
-        elif shared:
-            packed_h = [oracle.pack_codes(Q)[0] for (Q, A, B, _) in canon]
-        else:
-            packed_h = [oracle.pack(Q, A, B)[0] for (Q, A, B, _) in canon]
-        xs = [oracle.half_to_double(xb) if xdt == "f16" else oracle.bf16_to_double(xb) for (_, _, _, xb) in canon]
-        rows_frac = 1.0
-        if M > 16:  # prefill: a bounded slice of output rows per layer
-            rows_frac = 1.0 / 64
-        done_bytes, t_cpu, passes = 0.0, 0.0, 0
-        while t_cpu < args.cpu_seconds or passes == 0:
-            for li, L in enumerate(layers):
-                nrows = max(16, int(L.N * rows_frac))
-                rows = None if nrows >= L.N else np.arange(nrows)
-                s0 = time.perf_counter()
-                if var:
-                    oracle.var_matmul(packed_h[li], L.N, L.K, bits, canon[li][1], canon[li][2], xs[li], rows=rows,
-                                      threads=threads)
-                elif shared:
-                    oracle.matmul_shared(packed_h[li], L.N, L.K, canon[li][1], canon[li][2], xs[li], rows=rows,
-                                         threads=threads)
-                else:
-                    oracle.matmul(packed_h[li], L.N, L.K, xs[li], rows=rows, threads=threads)
-                t_cpu += time.perf_counter() - s0
-                done_bytes += algorithmic_bytes(L.N, L.K, M, affine=args.affine, bits=bits, d=dim) * (nrows / L.N)
-            passes += 1
-        cpu = {"value": round(done_bytes / t_cpu / 1e9, 3), "unit": "GB/s", "cores": threads,
-               "kind": "oracle",
-               "sample": f"{passes} pass(es) over the {args.workload} layer set"
-                         + ("" if rows_frac == 1.0 else f" (1/{int(1 / rows_frac)} of output rows)")
-                         + f", fp64 C oracle, {threads} threads, {t_cpu:.1f} s"}
+        cpu = cpu_baseline(case, headline, args.cpu_seconds)
+    configs = None
+    if args.workload is None and not args.no_sub and not shared and not var:
+        configs = sub_records(u, torch, ws, args)
 
-    if kernel == "gemv" or M <= 64:
-        metric = METRIC if (M == 1 and not shared) else f"2-bit decode achieved HBM GB/s at M={M}"
+    if case.M <= 64:
+        metric = METRIC if (M == 1 and not shared and not var) else f"2-bit decode achieved HBM GB/s at M={M}"
         if var:
             metric = f"{bits}-bit d={dim} decode achieved HBM GB/s at M={M}"
         if shared:
             metric += f" (codes-only, one (A, B) pair per {'matrix' if args.affine == 'matrix' else 'group'})"
-        value, unit = value_gbs, "GB/s"
     else:
-        flops = sum(2 * M * L.N * L.K for L in layers)
-        metric, value, unit = "unisvq_gemm effective TFLOP/s (2MNK)", flops / (ms_per_step * 1e-3) / 1e12, "TFLOP/s"
+        metric = "unisvq_gemm effective TFLOP/s (2MNK)"
         if var:
             metric = f"unisvq_var_gemm ({bits}-bit codes, d={dim}) effective TFLOP/s (2MNK)"
+        if args.fold:
+            metric = "unisvq_gemm_shared_fold effective TFLOP/s (2MNK)"
     out = {
         "metric": metric,
-        "value": round(value, 2),
-        "unit": unit,
+        "value": rec["value"],
+        "unit": rec["unit"],
         "n_gpus": 1,
-        "steps": steps_done,
+        "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5),
+        "ms_per_step": rec["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         # arithmetic type of the matrix cores: the GEMM multiplies in fp16
         # (bf16 activations are carried exactly as scaled fp16)
-        "dtype": "f16" if (xdt == "f16" or kernel == "gemm") else "bf16",
+        "dtype": "f16" if (xdt == "f16" or case.kernel == "gemm") else "bf16",
         "data": "synthetic",
-        "config": {"workload": args.workload, "layers": {L.name: [L.N, L.K] for L in layers}, "M": M,
-                   "activations": xdt, "affine": args.affine,
-                   "d": dim, "bits": bits, "group": 128, "kernel": kernel, "schedule": sched,
-                   "launches_per_step": len(groups_), "buffer_copies": copies,
-                   "set_bytes": set_bytes},
-        "pct_peak_hbm": round(100 * value_gbs / PEAK_HBM_GBS, 2) if (kernel == "gemv" or M <= 64) else None,
+        "config": {"workload": headline, "layers": {L.name: [L.N, L.K] for L in layers}, "M": M,
+                   "activations": xdt, "affine": args.affine, "d": dim, "bits": bits, "group": 128,
+                   "kernel": case.kernel, "schedule": rec["schedule"],
+                   "launches_per_step": rec["launches_per_step"], "buffer_copies": ws.copies,
+                   "set_bytes": case.set_bytes,
+                   "timing": "warmup steps eager; the timed steps are one HIP graph of exactly `steps` steps "
+                             "(captured, replayed once untimed, then once between two events)"},
+        "pct_peak_hbm": rec.get("pct_peak_hbm"),
+        "per_launch_us": rec.get("per_launch_us"),
+        "achievable": rec.get("achievable"),
+        "schedules": schedules or None,
         "dense_matmul": dense,
-        "event_us_per_launch": {k: round(v, 3) for k, v in per_layer_us.items()},
-        "schedules": schedules,
-        "rotated_layer": rht,
-        "roofline": roofline,
+        "rotated_layer": rot,
+        "roofline": rec["roofline"],
         "cpu_baseline": cpu,
+        "configs": configs,
     }
     print(json.dumps(out), flush=True)
 

@@ -464,23 +464,31 @@ int unisvq_gemv_rht_batched(const unisvq_gemv_problem* problems, int count, int6
 
 /* ---- Bandwidth reference (not part of the method) ----
  * A plain read of `count` device byte ranges in one launch, with the 16-byte
- * non-temporal loads the decode kernels stream their weights with (32 KB per
- * workgroup of 512 threads; a thread issues all four of its loads before
- * using any).  The 32-bit words of all ranges are XOR-folded into *sink (one
- * atomic per wavefront; XOR does not depend on the order, so the result is
- * exact and checkable).  Timed over the buffers of a product launch it gives
- * the read rate those bytes reach in the same launch structure.
- *   ranges  HOST array of 1..UNISVQ_MAX_BATCH descriptors, read before the
- *           call returns; each ptr device, 16-byte aligned, bytes a multiple
- *           of 16 in [0, 2^31) (UNISVQ_EINVAL otherwise)
- *   sink    device uint32, 4-byte aligned; XOR-accumulated (the caller sets
- *           its initial value) */
+ * non-temporal loads the decode kernels stream their weights with (8 KB per
+ * workgroup of 128 threads; a thread issues all four of its loads before
+ * using any).  Timed over the buffers of a product launch it gives the read
+ * rate those bytes reach in the same launch structure.
+ *   ranges      HOST array of 1..UNISVQ_MAX_BATCH descriptors, read before
+ *               the call returns; each ptr device, 16-byte aligned, bytes a
+ *               multiple of 16 in [0, 2^31) (UNISVQ_EINVAL otherwise)
+ *   store       0: nothing is written (sink may be NULL) -- the pure read;
+ *               1: each wavefront stores the XOR of the 32-bit words it read
+ *               to its own sink word, so the XOR of all sink words equals the
+ *               XOR of all words of the ranges (checkable on the host; the
+ *               stores, about 4 bytes per KB read, are of the order of a
+ *               product's output)
+ *   sink        device uint32 [sink_words], 4-byte aligned; overwritten
+ *   sink_words  >= unisvq_read_sink_words(ranges, count) when store = 1 (2
+ *               words per 8 KB of each range, rounded up), else
+ *               UNISVQ_EWORKSPACE */
 typedef struct {
     const void* ptr;
     int64_t bytes;
 } unisvq_byte_range;
 
-int unisvq_read_bytes(const unisvq_byte_range* ranges, int count, uint32_t* sink, void* stream);
+int64_t unisvq_read_sink_words(const unisvq_byte_range* ranges, int count);
+int unisvq_read_bytes(const unisvq_byte_range* ranges, int count, int store, uint32_t* sink, int64_t sink_words,
+                      void* stream);
 
 #ifdef __cplusplus
 }

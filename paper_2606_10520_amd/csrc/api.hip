@@ -426,10 +426,21 @@ int unisvq_rht(int64_t n, int64_t M, const void* x, int x_dtype, const int8_t* s
 
 /* ---- bandwidth reference ---- */
 
-int unisvq_read_bytes(const unisvq_byte_range* ranges, int count, uint32_t* sink, void* stream) {
-    if (!ranges || !sink || count < 1) return UNISVQ_EINVAL;
+int64_t unisvq_read_sink_words(const unisvq_byte_range* ranges, int count) {
+    if (!ranges || count < 1 || count > UNISVQ_MAX_BATCH) return 0;
+    int64_t bytes[UNISVQ_MAX_BATCH];
+    for (int i = 0; i < count; ++i) {
+        if (ranges[i].bytes < 0 || ranges[i].bytes > unisvq::kMaxBufferBytes) return 0;
+        bytes[i] = ranges[i].bytes;
+    }
+    return unisvq::read_sink_words(bytes, count);
+}
+
+int unisvq_read_bytes(const unisvq_byte_range* ranges, int count, int store, uint32_t* sink, int64_t sink_words,
+                      void* stream) {
+    if (!ranges || count < 1 || (store && !sink)) return UNISVQ_EINVAL;
     if (count > UNISVQ_MAX_BATCH) return UNISVQ_EUNSUP;
-    if (!aligned(sink, 4)) return UNISVQ_EALIGN;
+    if (store && !aligned(sink, 4)) return UNISVQ_EALIGN;
     const uint8_t* ptrs[UNISVQ_MAX_BATCH];
     int64_t bytes[UNISVQ_MAX_BATCH];
     for (int i = 0; i < count; ++i) {
@@ -440,7 +451,8 @@ int unisvq_read_bytes(const unisvq_byte_range* ranges, int count, uint32_t* sink
         ptrs[i] = static_cast<const uint8_t*>(ranges[i].ptr);
         bytes[i] = ranges[i].bytes;
     }
-    return unisvq::launch_read(ptrs, bytes, count, sink, static_cast<hipStream_t>(stream));
+    if (store && sink_words < unisvq::read_sink_words(bytes, count)) return UNISVQ_EWORKSPACE;
+    return unisvq::launch_read(ptrs, bytes, count, sink, store != 0, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

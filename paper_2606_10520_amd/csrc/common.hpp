@@ -201,8 +201,12 @@ inline int ensure_lds_limit(const void* fn, int bytes, std::atomic<uint64_t>& do
 }
 
 // Bandwidth reference: reads `count` byte ranges once (ptrs 16-byte aligned,
-// sizes multiples of 16 below 2^31), XOR-folding their words into *sink.
-int launch_read(const uint8_t* const* ptrs, const int64_t* bytes, int count, uint32_t* sink, hipStream_t s);
+// sizes multiples of 16 below 2^31); with `store` each wavefront stores the
+// XOR of the words it read to its own sink word (read_sink_words of them),
+// without it nothing is written.
+int64_t read_sink_words(const int64_t* bytes, int count);
+int launch_read(const uint8_t* const* ptrs, const int64_t* bytes, int count, uint32_t* sink, bool store,
+                hipStream_t s);
 
 // Output store in the requested dtype (fp32 -> fp16 / bf16 round to nearest even).
 __device__ inline void store_out(void* y, int64_t idx, float v, int y_dtype) {

@@ -28,7 +28,7 @@ EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "uni
            "unisvq_quantize", "unisvq_rht", "unisvq_var_codes_bytes", "unisvq_var_affine_bytes",
            "unisvq_var_pack", "unisvq_var_unpack", "unisvq_var_gemv", "unisvq_var_gemv_batched",
            "unisvq_var_gemm_workspace_bytes", "unisvq_var_gemm", "unisvq_ldlq_workspace_bytes", "unisvq_ldlq",
-           "unisvq_gemv_rht_batched", "unisvq_read_bytes")
+           "unisvq_gemv_rht_batched", "unisvq_read_sink_words", "unisvq_read_bytes")
 # format variants: (bits, d) pairs served by the unisvq_var_* entry points
 VARIANTS = ((3, 4), (2, 8), (3, 8))
 MAX_BATCH = 8
@@ -138,7 +138,9 @@ def load():
     lib.unisvq_ldlq_workspace_bytes.restype = sz
     lib.unisvq_ldlq.argtypes = [i64, i64, p, p, p, p, i64, p, p, sz, p]
     lib.unisvq_ldlq.restype = i32
-    lib.unisvq_read_bytes.argtypes = [ctypes.POINTER(ByteRange), i32, p, p]
+    lib.unisvq_read_sink_words.argtypes = [ctypes.POINTER(ByteRange), i32]
+    lib.unisvq_read_sink_words.restype = i64
+    lib.unisvq_read_bytes.argtypes = [ctypes.POINTER(ByteRange), i32, i32, p, i64, p]
     lib.unisvq_read_bytes.restype = i32
     _lib = lib
     return lib
@@ -694,9 +696,12 @@ def ldlq(W, U, A, B, affine_groups: int = 0, out=None, workspace=None, stream=No
 
 # ------------------------------------------------ bandwidth reference
 
-def read_bytes(buffers, sink, stream=None):
+def read_bytes(buffers, store: bool = True, sink=None, stream=None):
     """Plain read of the given device tensors (contiguous, 16-byte multiples)
-    in one launch; XOR-folds their 32-bit words into sink (int32 [1])."""
+    in one launch.  With `store`, returns the sink (uint32 words as int32, one
+    per wavefront) whose XOR equals the XOR of every 32-bit word read;
+    without it nothing is written and None is returned."""
+    torch = _torch()
     _need_cuda(sink, *buffers)
     if not 1 <= len(buffers) <= MAX_BATCH:
         raise ValueError(f"1..{MAX_BATCH} buffers per call")
@@ -705,5 +710,13 @@ def read_bytes(buffers, sink, stream=None):
         if not t.is_contiguous():
             raise ValueError("buffers must be contiguous")
         arr[i] = ByteRange(t.data_ptr(), _nbytes(t))
-    _need_buffer(sink, 4, "sink")
-    _check("unisvq_read_bytes", load().unisvq_read_bytes(arr, len(buffers), _ptr(sink), _stream(stream)))
+    if not store:
+        _check("unisvq_read_bytes", load().unisvq_read_bytes(arr, len(buffers), 0, None, 0, _stream(stream)))
+        return None
+    words = load().unisvq_read_sink_words(arr, len(buffers))
+    if sink is None:
+        sink = torch.empty(max(words, 1), dtype=torch.int32, device=buffers[0].device)
+    _need_buffer(sink, 4 * words, "sink")
+    _check("unisvq_read_bytes", load().unisvq_read_bytes(arr, len(buffers), 1, _ptr(sink), sink.numel(),
+                                                         _stream(stream)))
+    return sink

@@ -458,11 +458,17 @@ def test_read_bytes_validation():
     lib = u.load()
     R = u.ByteRange
     one = (R * 1)(R(GOOD, 4096))
-    assert lib.unisvq_read_bytes(None, 1, GOOD, None) == EINVAL
-    assert lib.unisvq_read_bytes(one, 0, GOOD, None) == EINVAL
-    assert lib.unisvq_read_bytes(one, 1, None, None) == EINVAL
-    assert lib.unisvq_read_bytes(one, 9, GOOD, None) == EUNSUP
-    assert lib.unisvq_read_bytes(one, 1, GOOD + 2, None) == EALIGN
-    for bad in (R(GOOD, 4100), R(GOOD, -16), R(None, 4096), R(GOOD, 2 ** 31)):
-        assert lib.unisvq_read_bytes((R * 1)(bad), 1, GOOD, None) == EINVAL
-    assert lib.unisvq_read_bytes((R * 1)(R(GOOD + 8, 4096)), 1, GOOD, None) == EALIGN
+    two = (R * 2)(R(GOOD, 32768 * 3), R(GOOD, 16))
+    assert lib.unisvq_read_sink_words(one, 1) == 2
+    assert lib.unisvq_read_sink_words(two, 2) == 2 * 13
+    assert lib.unisvq_read_bytes(None, 1, 1, GOOD, 8, None) == EINVAL
+    assert lib.unisvq_read_bytes(one, 0, 1, GOOD, 8, None) == EINVAL
+    assert lib.unisvq_read_bytes(one, 1, 1, None, 8, None) == EINVAL
+    assert lib.unisvq_read_bytes(one, 9, 1, GOOD, 8, None) == EUNSUP
+    assert lib.unisvq_read_bytes(one, 1, 1, GOOD + 2, 8, None) == EALIGN
+    assert lib.unisvq_read_bytes(two, 2, 1, GOOD, 25, None) == EWS
+    for st in (0, 1):
+        for bad in (R(GOOD, 4100), R(GOOD, -16), R(None, 4096), R(GOOD, 2 ** 31)):
+            assert lib.unisvq_read_bytes((R * 1)(bad), 1, st, GOOD, 8, None) == EINVAL
+        assert lib.unisvq_read_bytes((R * 1)(R(GOOD + 8, 4096)), 1, st, GOOD, 8, None) == EALIGN
+

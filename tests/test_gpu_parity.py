@@ -600,11 +600,17 @@ def test_read_bytes_folds_every_word():
     sizes = [9_437_184, 32_768 + 48, 0, 16]
     host = [rng.integers(0, 2 ** 32, size=n // 4, dtype=np.uint64).astype(np.uint32) for n in sizes]
     bufs = [torch.from_numpy(h.view(np.int32)).to(DEV) for h in host]
-    sink = torch.full((1,), 0x5A5A5A5A, dtype=torch.int32, device=DEV)
-    u.read_bytes(bufs, sink)
+    sink = u.read_bytes(bufs)
     torch.cuda.synchronize()
-    expect = np.uint32(0x5A5A5A5A)
+    expect = np.uint32(0)
     for h in host:
         if h.size:
             expect ^= np.bitwise_xor.reduce(h)
-    assert np.uint32(sink.cpu().numpy().view(np.uint32)[0]) == expect
+    assert sink.numel() == 2 * (-(-sizes[0] // 8192) + -(-sizes[1] // 8192) + 1)
+    assert np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32)) == expect
+    # the store-free mode writes nothing
+    before = sink.clone()
+    assert u.read_bytes(bufs, store=False) is None
+    u.read_bytes(bufs[:1], store=False)
+    torch.cuda.synchronize()
+    assert torch.equal(sink, before)
