@@ -131,7 +131,8 @@ typedef enum {
     UNISVQ_EUNSUP = -3,     /* valid but unsupported combination (dtype pair, M too large for gemv) */
     UNISVQ_EALIGN = -4,     /* a pointer lacks the alignment stated for it */
     UNISVQ_EHIP = -5,       /* the HIP runtime reported an error at launch */
-    UNISVQ_EWORKSPACE = -6  /* workspace smaller than unisvq_gemm_workspace_bytes() */
+    UNISVQ_EWORKSPACE = -6, /* workspace smaller than unisvq_gemm_workspace_bytes() */
+    UNISVQ_ESCRATCH = -7    /* the product needs more than the fixed scratch of unisvq_gemm_noalloc */
 } unisvq_status;
 
 typedef enum {
@@ -234,6 +235,25 @@ size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype)
  *              size is 0.  Overwritten; the caller owns it. */
 int unisvq_gemm(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype,
                 void* y, int y_dtype, void* workspace, size_t workspace_bytes, void* stream);
+
+/* unisvq_gemm for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same kernels, arguments (minus the workspace), results and errors, with the
+ * workspace taken from a scratch array of the library itself --
+ * unisvq_noalloc_scratch_bytes() (32 MiB) per device, held until the process
+ * ends; no call allocates or frees anything.  The first call on a device looks
+ * the array's device address up (with that device current).
+ *   UNISVQ_ESCRATCH (before any launch) when the product needs more than the
+ *   scratch, i.e. unisvq_gemm_workspace_bytes(N, K, M, x_dtype) exceeds it:
+ *   with bf16 activations the fp16 copy of x takes M*K*2 bytes (M rounded up
+ *   to 16 above 32 tokens), and a product split along K takes splits*M*N*4.
+ * Every call on a device shares that device's scratch, so calls that overlap
+ * on one device (different streams, different host threads) race; calls in
+ * order on one stream do not.  Nothing in the scratch needs to start at zero:
+ * each call writes every byte it reads. */
+size_t unisvq_noalloc_scratch_bytes(void);
+int unisvq_gemm_noalloc(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype, void* y,
+                        int y_dtype, void* stream);
 
 /* ---- Row-shared affine parameters (codes-only format block above) ---- */
 

@@ -82,6 +82,7 @@ const char* unisvq_status_string(int status) {
         case UNISVQ_EALIGN: return "misaligned pointer";
         case UNISVQ_EHIP: return "HIP runtime error";
         case UNISVQ_EWORKSPACE: return "workspace too small";
+        case UNISVQ_ESCRATCH: return "product needs more than the fixed scratch of unisvq_gemm_noalloc";
         default: return "unknown status";
     }
 }
@@ -422,6 +423,19 @@ int unisvq_rht(int64_t n, int64_t M, const void* x, int x_dtype, const int8_t* s
     if (x0 < y1 && y0 < x1) return UNISVQ_EINVAL;
     return unisvq::launch_rht(n, M, x, x_dtype, reinterpret_cast<const signed char*>(signs), mode, y, y_dtype,
                               static_cast<hipStream_t>(stream));
+}
+
+/* ---- the product without a caller workspace ---- */
+
+size_t unisvq_noalloc_scratch_bytes(void) { return unisvq::noalloc_scratch_bytes(); }
+
+int unisvq_gemm_noalloc(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype, void* y,
+                        int y_dtype, void* stream) {
+    const int st = check_product(N, K, packed, M, x, x_dtype, y, y_dtype);
+    if (st != UNISVQ_OK) return st;
+    if (x_dtype == UNISVQ_BF16 && K > 65536) return UNISVQ_EUNSUP;  // as unisvq_gemm
+    return unisvq::launch_gemm_noalloc(N, K, static_cast<const uint8_t*>(packed), M, x, x_dtype, y, y_dtype,
+                                       static_cast<hipStream_t>(stream));
 }
 
 /* ---- bandwidth reference ---- */

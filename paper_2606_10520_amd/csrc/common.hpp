@@ -164,6 +164,12 @@ int launch_gemv_var_batch(const GemvProblem* probs, int count, int64_t M, int x_
 size_t gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype);
 int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x,
                 int x_dtype, void* y, int y_dtype, void* workspace, hipStream_t s);
+// launch_gemm with the library's own fixed scratch array as the workspace
+// (noalloc_scratch_bytes() per device); UNISVQ_ESCRATCH when the product
+// needs more.
+size_t noalloc_scratch_bytes();
+int launch_gemm_noalloc(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const void* x, int x_dtype, void* y,
+                        int y_dtype, hipStream_t s);
 // The same with codes-only weights and a shared affine block.
 int launch_gemm_shared(int64_t N, int64_t K, const uint8_t* packed_codes, const uint8_t* affine,
                        int affine_one, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,

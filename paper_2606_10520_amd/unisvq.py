@@ -18,7 +18,7 @@ F16, BF16, F32 = 0, 1, 2
 GROUP, DIM, ROW_BLOCK = 128, 4, 16
 
 STATUS = {0: "UNISVQ_OK", -1: "UNISVQ_EINVAL", -2: "UNISVQ_ESHAPE", -3: "UNISVQ_EUNSUP",
-          -4: "UNISVQ_EALIGN", -5: "UNISVQ_EHIP", -6: "UNISVQ_EWORKSPACE"}
+          -4: "UNISVQ_EALIGN", -5: "UNISVQ_EHIP", -6: "UNISVQ_EWORKSPACE", -7: "UNISVQ_ESCRATCH"}
 
 EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "unisvq_pack",
            "unisvq_unpack", "unisvq_gemv", "unisvq_gemv_batched", "unisvq_gemm_workspace_bytes",
@@ -28,7 +28,8 @@ EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "uni
            "unisvq_quantize", "unisvq_rht", "unisvq_var_codes_bytes", "unisvq_var_affine_bytes",
            "unisvq_var_pack", "unisvq_var_unpack", "unisvq_var_gemv", "unisvq_var_gemv_batched",
            "unisvq_var_gemm_workspace_bytes", "unisvq_var_gemm", "unisvq_ldlq_workspace_bytes", "unisvq_ldlq",
-           "unisvq_gemv_rht_batched", "unisvq_read_sink_words", "unisvq_read_bytes")
+           "unisvq_gemv_rht_batched", "unisvq_read_sink_words", "unisvq_read_bytes", "unisvq_noalloc_scratch_bytes",
+           "unisvq_gemm_noalloc")
 # format variants: (bits, d) pairs served by the unisvq_var_* entry points
 VARIANTS = ((3, 4), (2, 8), (3, 8))
 MAX_BATCH = 8
@@ -138,6 +139,10 @@ def load():
     lib.unisvq_ldlq_workspace_bytes.restype = sz
     lib.unisvq_ldlq.argtypes = [i64, i64, p, p, p, p, i64, p, p, sz, p]
     lib.unisvq_ldlq.restype = i32
+    lib.unisvq_noalloc_scratch_bytes.argtypes = []
+    lib.unisvq_noalloc_scratch_bytes.restype = sz
+    lib.unisvq_gemm_noalloc.argtypes = [i64, i64, p, i64, p, i32, p, i32, p]
+    lib.unisvq_gemm_noalloc.restype = i32
     lib.unisvq_read_sink_words.argtypes = [ctypes.POINTER(ByteRange), i32]
     lib.unisvq_read_sink_words.restype = i64
     lib.unisvq_read_bytes.argtypes = [ctypes.POINTER(ByteRange), i32, i32, p, i64, p]
@@ -388,6 +393,17 @@ def gemm(packed, N: int, K: int, x, out=None, out_dtype=None, workspace=None, st
     workspace, ws_bytes = _workspace(workspace, gemm_workspace_bytes(N, K, M, x.dtype), x)
     return _product("unisvq_gemm", N, K, packed, x, out, out_dtype, stream,
                     extra=(_ptr(workspace), ws_bytes))
+
+
+def noalloc_scratch_bytes() -> int:
+    return int(load().unisvq_noalloc_scratch_bytes())
+
+
+def gemm_noalloc(packed, N: int, K: int, x, out=None, out_dtype=None, stream=None):
+    """unisvq_gemm with the library's fixed scratch as the workspace (the C
+    call allocates nothing; pass `out` to keep this wrapper from allocating
+    the output)."""
+    return _product("unisvq_gemm_noalloc", N, K, packed, x, out, out_dtype, stream)
 
 
 # ------------------------------------------------ row-shared affine parameters

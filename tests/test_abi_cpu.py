@@ -14,7 +14,7 @@ HEADER = os.path.join(ROOT, "include", "unisvq.h")
 
 pytestmark = pytest.mark.skipif(not os.path.exists(u.LIB_PATH), reason="libunisvq.so not built")
 
-OK, EINVAL, ESHAPE, EUNSUP, EALIGN, EHIP, EWS = 0, -1, -2, -3, -4, -5, -6
+OK, EINVAL, ESHAPE, EUNSUP, EALIGN, EHIP, EWS, ESCRATCH = 0, -1, -2, -3, -4, -5, -6, -7
 GOOD = 0x10000  # 16-byte aligned stand-in address; never dereferenced (validation fails first)
 
 
@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol():
 def test_version_and_status_strings():
     lib = u.load()
     assert lib.unisvq_version() == 1
-    for st in (OK, EINVAL, ESHAPE, EUNSUP, EALIGN, EHIP, EWS):
+    for st in (OK, EINVAL, ESHAPE, EUNSUP, EALIGN, EHIP, EWS, ESCRATCH):
         assert lib.unisvq_status_string(st)
     assert lib.unisvq_status_string(12345) == b"unknown status"
 
@@ -472,3 +472,22 @@ def test_read_bytes_validation():
             assert lib.unisvq_read_bytes((R * 1)(bad), 1, st, GOOD, 8, None) == EINVAL
         assert lib.unisvq_read_bytes((R * 1)(R(GOOD + 8, 4096)), 1, st, GOOD, 8, None) == EALIGN
 
+
+def test_gemm_noalloc_validation():
+    """The no-allocation product checks its arguments like unisvq_gemm and
+    refuses, before any HIP call, a product whose workspace exceeds the fixed
+    scratch."""
+    lib = u.load()
+    cap = lib.unisvq_noalloc_scratch_bytes()
+    assert cap == 32 << 20
+    f = lib.unisvq_gemm_noalloc
+    assert f(64, 256, None, 4, GOOD, u.F16, GOOD, u.F16, None) == EINVAL
+    assert f(64, 256, GOOD, 0, GOOD, u.F16, GOOD, u.F16, None) == EINVAL
+    assert f(60, 256, GOOD, 4, GOOD, u.F16, GOOD, u.F16, None) == ESHAPE
+    assert f(64, 256, GOOD + 8, 4, GOOD, u.F16, GOOD, u.F16, None) == EALIGN
+    assert f(64, 256, GOOD, 4, GOOD, 7, GOOD, u.F16, None) == EINVAL
+    assert f(64, 70016, GOOD, 4, GOOD, u.BF16, GOOD, u.F16, None) == EUNSUP
+    # bf16 activations: the fp16 copy alone (1024 x 16384 x 2 bytes) exceeds 32 MiB
+    assert lib.unisvq_gemm_workspace_bytes(4096, 16384, 1024, u.BF16) > cap
+    assert f(4096, 16384, GOOD, 1024, GOOD, u.BF16, GOOD, u.F16, None) == ESCRATCH
+    assert lib.unisvq_status_string(ESCRATCH).startswith(b"product needs more")
