@@ -451,6 +451,11 @@ class Case:
                              for L in layers)
         self.flops = sum(2 * M * L.N * L.K for L in layers)
         ws_bytes = 0
+        if self.kernel == "gemm" and M <= SKINNY_MAX_M and not ws.shared and not ws.var:
+            # batched launches (q+k+v, gate+up): the slices of all problems of a batch
+            for grp in (layers[:3], layers[4:6], layers):
+                arr = (u.GemvProblem * len(grp))(*[u.GemvProblem(L.N, L.K, None, None, None) for L in grp])
+                ws_bytes = max(ws_bytes, self.lib.unisvq_gemm_batched_workspace_bytes(arr, len(grp), M, self.xcode))
         if self.kernel == "gemm":
             for L in layers:
                 if ws.var:
@@ -469,9 +474,13 @@ class Case:
         torch.cuda.synchronize()
 
     # ---- schedules
+    def batched_gemm(self):
+        """The small-batch product takes batches (q+k+v, gate+up) in one launch."""
+        return self.kernel == "gemm" and self.M <= SKINNY_MAX_M and not self.ws.shared and not self.ws.var
+
     def groups(self, sched):
         full_set = {"q", "k", "v", "o", "gate", "up", "down"} <= set(self.names)
-        if self.kernel != "gemv":
+        if self.kernel != "gemv" and not self.batched_gemm():
             return "per_layer", [[n] for n in self.names]
         if sched == "decoder" and full_set:
             return "decoder", [["q", "k", "v"], ["o"], ["gate", "up"], ["down"]]
@@ -487,6 +496,14 @@ class Case:
     def launch(self, c, lis, sptr):
         u, lib, ws, M = self.u, self.lib, self.ws, self.M
         Ls = [ws.layers[i] for i in lis]
+        if len(lis) > 1 and self.kernel == "gemm":
+            arr = (u.GemvProblem * len(lis))()
+            for j, li in enumerate(lis):
+                L = ws.layers[li]
+                arr[j] = u.GemvProblem(L.N, L.K, ws.packed[c][li].data_ptr(), self.xs[c][li].data_ptr(),
+                                       self.ys[c][li].data_ptr())
+            return lib.unisvq_gemm_batched(arr, len(lis), M, self.xcode, u.F16, self.wsbuf.data_ptr(), self.ws_bytes,
+                                           sptr)
         if len(lis) > 1:
             if ws.shared or ws.var:
                 arr = (u.GemvSharedProblem * len(lis))()

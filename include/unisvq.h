@@ -236,6 +236,28 @@ size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype)
 int unisvq_gemm(int64_t N, int64_t K, const void* packed, int64_t M, const void* x, int x_dtype,
                 void* y, int y_dtype, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Device workspace unisvq_gemm_batched needs for these problems and M, in
+ * bytes: the 256-byte-aligned sum of unisvq_gemm_workspace_bytes of each
+ * problem (problem i uses its own slice, in order).  0 when none is needed or
+ * for invalid arguments.  problems: HOST array of `count` descriptors.
+ * Host-only. */
+size_t unisvq_gemm_batched_workspace_bytes(const unisvq_gemv_problem* problems, int count, int64_t M, int x_dtype);
+
+/* Several independent products y_i = x_i * W_hat_i^T of the same M and
+ * dtypes, with the results of unisvq_gemm on each (a decoder's query, key and
+ * value projections, or its gate and up projections, at a small batch).  For
+ * M <= 32 all of them run in ONE launch of the small-batch kernel (bf16
+ * activations first pass through the per-problem pre-pass into their
+ * workspace slice); above that each problem takes the tiled product.
+ *   problems   HOST array of `count` descriptors (1..UNISVQ_MAX_BATCH), read
+ *              before the call returns; packed format v1 weights; every
+ *              descriptor is validated before anything is enqueued
+ *   workspace  device, >= unisvq_gemm_batched_workspace_bytes(...) bytes,
+ *              16-byte aligned (UNISVQ_EWORKSPACE / UNISVQ_EALIGN); may be
+ *              NULL when that size is 0 */
+int unisvq_gemm_batched(const unisvq_gemv_problem* problems, int count, int64_t M, int x_dtype, int y_dtype,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
 /* unisvq_gemm for callers that cannot allocate device memory (code under HIP
  * graph capture, tight serving loops, harnesses that forbid allocation): the
  * same kernels, arguments (minus the workspace), results and errors, with the

@@ -178,6 +178,48 @@ int unisvq_gemm(int64_t N, int64_t K, const void* packed, int64_t M, const void*
                                workspace, static_cast<hipStream_t>(stream));
 }
 
+namespace {
+
+// Validate a batch of product descriptors and convert them (count checked by the caller).
+int batch_problems(const unisvq_gemv_problem* problems, int count, int64_t M, int x_dtype, int y_dtype,
+                   unisvq::GemmBatchProblem* out) {
+    for (int i = 0; i < count; ++i) {
+        const unisvq_gemv_problem& q = problems[i];
+        const int st = check_product(q.N, q.K, q.packed, M, q.x, x_dtype, q.y, y_dtype);
+        if (st != UNISVQ_OK) return st;
+        if (x_dtype == UNISVQ_BF16 && q.K > 65536) return UNISVQ_EUNSUP;
+        out[i] = unisvq::GemmBatchProblem{static_cast<const uint8_t*>(q.packed), q.x, q.y, q.N, q.K};
+    }
+    return UNISVQ_OK;
+}
+
+}  // namespace
+
+size_t unisvq_gemm_batched_workspace_bytes(const unisvq_gemv_problem* problems, int count, int64_t M, int x_dtype) {
+    if (!problems || count < 1 || count > UNISVQ_MAX_BATCH || M < 1 || !x_dtype_ok(x_dtype)) return 0;
+    unisvq::GemmBatchProblem probs[UNISVQ_MAX_BATCH];
+    for (int i = 0; i < count; ++i) {
+        if (!shape_ok(problems[i].N, problems[i].K)) return 0;
+        probs[i] = unisvq::GemmBatchProblem{nullptr, nullptr, nullptr, problems[i].N, problems[i].K};
+    }
+    return unisvq::gemm_batch_workspace_bytes(probs, count, M, x_dtype);
+}
+
+int unisvq_gemm_batched(const unisvq_gemv_problem* problems, int count, int64_t M, int x_dtype, int y_dtype,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+    if (!problems || count < 1) return UNISVQ_EINVAL;
+    if (count > UNISVQ_MAX_BATCH) return UNISVQ_EUNSUP;
+    unisvq::GemmBatchProblem probs[UNISVQ_MAX_BATCH];
+    const int st = batch_problems(problems, count, M, x_dtype, y_dtype, probs);
+    if (st != UNISVQ_OK) return st;
+    const size_t need = unisvq::gemm_batch_workspace_bytes(probs, count, M, x_dtype);
+    if (need) {
+        if (!workspace || workspace_bytes < need) return UNISVQ_EWORKSPACE;
+        if (!aligned(workspace, 16)) return UNISVQ_EALIGN;
+    }
+    return unisvq::launch_gemm_batch(probs, count, M, x_dtype, y_dtype, workspace, static_cast<hipStream_t>(stream));
+}
+
 /* ---- row-shared affine parameters ---- */
 
 size_t unisvq_codes_bytes(int64_t N, int64_t K) {

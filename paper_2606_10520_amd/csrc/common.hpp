@@ -192,6 +192,35 @@ constexpr int64_t kSkinnyMaxM = 32;
 hipError_t launch_skinny(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine, int affine_one,
                          int64_t M, const _Float16* x, const float* inv_scale, void* y, int y_dtype,
                          hipStream_t s);
+// Several independent small-batch products (same M, the same weight format)
+// in one launch.
+struct SkinnyProblem {
+    const uint8_t* packed;
+    const uint8_t* affine;
+    int affine_one;
+    const _Float16* x;
+    const float* inv_scale;
+    void* y;
+    int64_t N, K;
+};
+hipError_t launch_skinny_batch(const SkinnyProblem* probs, int count, int64_t M, int y_dtype, hipStream_t s);
+// The same with 64-row workgroups whose four row blocks share each step's
+// staged activations (for batches with many rows); workgroups it launches.
+int64_t skinny64_workgroups(const SkinnyProblem* probs, int count);
+hipError_t launch_skinny64_batch(const SkinnyProblem* probs, int count, int64_t M, int y_dtype, hipStream_t s);
+// unisvq_gemm over a batch of problems (same M and dtypes): one launch for
+// M <= kSkinnyMaxM (after the bf16 pre-passes), else one product per problem.
+// Problem i uses the workspace bytes [off_i, off_i + gemm_workspace_bytes(i)),
+// off_i the 256-aligned sum of the earlier ones (gemm_batch_workspace_bytes).
+struct GemmBatchProblem {
+    const uint8_t* packed;
+    const void* x;
+    void* y;
+    int64_t N, K;
+};
+size_t gemm_batch_workspace_bytes(const GemmBatchProblem* probs, int count, int64_t M, int x_dtype);
+int launch_gemm_batch(const GemmBatchProblem* probs, int count, int64_t M, int x_dtype, int y_dtype, void* workspace,
+                      hipStream_t s);
 
 // Raise a kernel's dynamic-LDS limit on the current device, once per
 // (kernel, device): `done` is the calling site's bitmask of devices already

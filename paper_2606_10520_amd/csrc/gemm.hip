@@ -796,6 +796,42 @@ int launch_gemm(int64_t N, int64_t K, const uint8_t* packed, int64_t M, const vo
     return gemm_common(N, K, packed, nullptr, 0, M, x, x_dtype, y, y_dtype, workspace, s);
 }
 
+size_t gemm_batch_workspace_bytes(const GemmBatchProblem* probs, int count, int64_t M, int x_dtype) {
+    size_t b = 0;
+    for (int i = 0; i < count; ++i) b += align256(gemm_workspace_bytes(probs[i].N, probs[i].K, M, x_dtype));
+    return b;
+}
+
+int launch_gemm_batch(const GemmBatchProblem* probs, int count, int64_t M, int x_dtype, int y_dtype, void* workspace,
+                      hipStream_t s) {
+    uint8_t* ws = static_cast<uint8_t*>(workspace);
+    if (M > kSkinnyMaxM) {
+        for (int i = 0; i < count; ++i) {
+            const GemmBatchProblem& q = probs[i];
+            const int st = gemm_common(q.N, q.K, q.packed, nullptr, 0, M, q.x, x_dtype, q.y, y_dtype, ws, s);
+            if (st != UNISVQ_OK) return st;
+            ws += align256(gemm_workspace_bytes(q.N, q.K, M, x_dtype));
+        }
+        return UNISVQ_OK;
+    }
+    SkinnyProblem sp[kMaxBatch];
+    for (int i = 0; i < count; ++i) {
+        const GemmBatchProblem& q = probs[i];
+        sp[i] = SkinnyProblem{q.packed, nullptr, 0, static_cast<const _Float16*>(q.x), nullptr, q.y, q.N, q.K};
+        if (x_dtype == UNISVQ_BF16) {
+            // the problem's own scaled fp16 copy (row-major at this size)
+            _Float16* wxh = reinterpret_cast<_Float16*>(ws);
+            float* winv = reinterpret_cast<float*>(ws + align256(static_cast<size_t>(M) * q.K * 2));
+            if (launch_scale<false>(q.K, M, static_cast<const uint16_t*>(q.x), wxh, winv, s) != hipSuccess)
+                return q.K > 65536 ? UNISVQ_EUNSUP : UNISVQ_EHIP;
+            sp[i].x = wxh;
+            sp[i].inv_scale = winv;
+        }
+        ws += align256(gemm_workspace_bytes(q.N, q.K, M, x_dtype));
+    }
+    return launch_skinny_batch(sp, count, M, y_dtype, s) == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+}
+
 int launch_gemm_shared(int64_t N, int64_t K, const uint8_t* packed_codes, const uint8_t* affine,
                        int affine_one, int64_t M, const void* x, int x_dtype, void* y, int y_dtype,
                        void* workspace, hipStream_t s) {

@@ -6,18 +6,28 @@
 namespace unisvq {
 namespace {
 
+// QX (packets per wavefront whose activations load up front): 1, 2, 4, 8
+// for one token, up to 4 for two, up to 2 for three or four (plan_qx).
 template <typename XT, bool SHARED, int WAVES, int MT, int PF>
-int launch_nx(const GemvBatch& b, int blocks, int maxK, int nx, hipStream_t s) {
-    if (nx == 1) return launch_cfg<XT, SHARED, WAVES, MT, PF, 1>(b, blocks, maxK, s);
-    if (nx == 2) return launch_cfg<XT, SHARED, WAVES, MT, PF, 2>(b, blocks, maxK, s);
-    if (nx == 4) return launch_cfg<XT, SHARED, WAVES, MT, PF, 4>(b, blocks, maxK, s);
-    return launch_cfg<XT, SHARED, WAVES, MT, PF, 8>(b, blocks, maxK, s);
+int launch_qx(const GemvBatch& b, int blocks, int maxK, int qx, hipStream_t s) {
+    if (qx <= 1) return launch_cfg<XT, SHARED, WAVES, MT, PF, 1>(b, blocks, maxK, s);
+    if constexpr (MT >= 3) {
+        return launch_cfg<XT, SHARED, WAVES, MT, PF, 2>(b, blocks, maxK, s);
+    } else {
+        if (qx == 2) return launch_cfg<XT, SHARED, WAVES, MT, PF, 2>(b, blocks, maxK, s);
+        if constexpr (MT == 2) {
+            return launch_cfg<XT, SHARED, WAVES, MT, PF, 4>(b, blocks, maxK, s);
+        } else {
+            if (qx == 4) return launch_cfg<XT, SHARED, WAVES, MT, PF, 4>(b, blocks, maxK, s);
+            return launch_cfg<XT, SHARED, WAVES, MT, PF, 8>(b, blocks, maxK, s);
+        }
+    }
 }
 
 template <typename XT, bool SHARED, int WAVES, int MT>
 int launch_pf(const GemvBatch& b, int blocks, int maxK, const GemvPlan& p, hipStream_t s) {
-    if (p.pf == 2) return launch_nx<XT, SHARED, WAVES, MT, 2>(b, blocks, maxK, p.nx, s);
-    return launch_nx<XT, SHARED, WAVES, MT, 4>(b, blocks, maxK, p.nx, s);
+    if (p.pf == 2) return launch_qx<XT, SHARED, WAVES, MT, 2>(b, blocks, maxK, p.qx, s);
+    return launch_qx<XT, SHARED, WAVES, MT, 4>(b, blocks, maxK, p.qx, s);
 }
 
 template <typename XT, bool SHARED, int MT>
@@ -27,10 +37,12 @@ int launch_waves(const GemvBatch& b, int blocks, int minK, int maxK, hipStream_t
     return launch_pf<XT, SHARED, 8, MT>(b, blocks, maxK, p, s);
 }
 
+// The token count is a template parameter (no per-token guards in the loop).
 template <typename XT, bool SHARED>
 int launch_tokens(const GemvBatch& b, int blocks, int minK, int maxK, hipStream_t s) {
     if (b.M == 1) return launch_waves<XT, SHARED, 1>(b, blocks, minK, maxK, s);
     if (b.M == 2) return launch_waves<XT, SHARED, 2>(b, blocks, minK, maxK, s);
+    if (b.M == 3) return launch_waves<XT, SHARED, 3>(b, blocks, minK, maxK, s);
     return launch_waves<XT, SHARED, 4>(b, blocks, minK, maxK, s);
 }
 

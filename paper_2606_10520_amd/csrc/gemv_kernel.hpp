@@ -204,11 +204,12 @@ constexpr int kXsPacketBytes = 64 * 8;
 constexpr int kXbarPacketBytes = 16 * 4;
 
 // One loaded activation word (lane's vector of packet P, token t) -> operand
-// order in LDS, plus the per-group sums.
-template <typename XT>
-__device__ inline void stage_packet(uint2 raw, int t, int P, int packets, int lane, uint2* xs, float* xbar) {
+// order in LDS, plus the per-group sums.  Packet-major layout: entry
+// P * MT + t, so a packet's tokens sit at constant offsets from each other.
+template <typename XT, int MT>
+__device__ inline void stage_packet(uint2 raw, int t, int P, int lane, uint2* xs, float* xbar) {
     const uint2 op = quad_transpose16(raw, lane & 3);
-    const size_t tp = static_cast<size_t>(t) * packets + P;
+    const size_t tp = static_cast<size_t>(P) * MT + t;
     xs[tp * 64 + lane] = op;
     // lane 4*(8 gi + s) + a holds component a of the 4 vectors of step s;
     // the 4 steps of one DPP row sum up in its lanes 12..15
@@ -247,19 +248,20 @@ __device__ inline void chain_step_half(typename XOps<XT>::vec4 xo, const typenam
 // One full packet P: groups 2P and 2P+1 of the row block.
 template <typename XT, int MT>
 __device__ inline void packet_step(const uint4& c, const uint4& a, uint32_t bw, int P, const uint2* xs,
-                                   const float* xbar, int packets, int M, int lane, float (&acc)[MT]) {
+                                   const float* xbar, int lane, float (&acc)[MT]) {
     typedef typename XOps<XT>::vec4 vec4;
     vec4 cop0[8], cop1[8];
     word_operands<XT>(c.x, cop0);
     word_operands<XT>(c.y, cop0 + 4);
     word_operands<XT>(c.z, cop1);
     word_operands<XT>(c.w, cop1 + 4);
+    const uint2* xp = xs + static_cast<size_t>(P) * MT * 64 + lane;
+    const float* bp = xbar + static_cast<size_t>(P) * MT * 16 + (lane & 3) * 4;
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
-        if (t < M) {
-            const size_t tp = static_cast<size_t>(t) * packets + P;
-            const vec4 xo = __builtin_bit_cast(vec4, xs[tp * 64 + lane]);
-            const f32x4 xb = *reinterpret_cast<const f32x4*>(xbar + tp * 16 + (lane & 3) * 4);
+        {
+            const vec4 xo = __builtin_bit_cast(vec4, xp[t * 64]);
+            const f32x4 xb = *reinterpret_cast<const f32x4*>(bp + t * 16);
             f32x4 d0 = {0.f, 0.f, 0.f, 0.f}, d1 = d0;
             chain_step<XT, 0>(xo, cop0, cop1, d0, d1);
             chain_step<XT, 1>(xo, cop0, cop1, d0, d1);
@@ -279,17 +281,18 @@ __device__ inline void packet_step(const uint4& c, const uint4& a, uint32_t bw, 
 // first group only).
 template <typename XT, int MT>
 __device__ inline void half_step(const uint2& c, const uint2& a, uint32_t bbits, int P, const uint2* xs,
-                                 const float* xbar, int packets, int M, int lane, float (&acc)[MT]) {
+                                 const float* xbar, int lane, float (&acc)[MT]) {
     typedef typename XOps<XT>::vec4 vec4;
     vec4 cop[8];
     word_operands<XT>(c.x, cop);
     word_operands<XT>(c.y, cop + 4);
+    const uint2* xp = xs + static_cast<size_t>(P) * MT * 64 + lane;
+    const float* bp = xbar + static_cast<size_t>(P) * MT * 16 + (lane & 3) * 4;
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
-        if (t < M) {
-            const size_t tp = static_cast<size_t>(t) * packets + P;
-            const vec4 xo = __builtin_bit_cast(vec4, xs[tp * 64 + lane]);
-            const f32x4 xb = *reinterpret_cast<const f32x4*>(xbar + tp * 16 + (lane & 3) * 4);
+        {
+            const vec4 xo = __builtin_bit_cast(vec4, xp[t * 64]);
+            const f32x4 xb = *reinterpret_cast<const f32x4*>(bp + t * 16);
             f32x4 d = {0.f, 0.f, 0.f, 0.f};
             chain_step_half<XT, 0>(xo, cop, d);
             chain_step_half<XT, 1>(xo, cop, d);
@@ -417,7 +420,7 @@ __device__ inline void var_group(typename XOps<XT>::vec4 xo, const f32x4& xb, co
 // A variant packet P: both groups (NG = 2) or the trailing half packet (NG = 1).
 template <typename XT, int MT, int BITS, int D, int NG>
 __device__ inline void var_packet_step(const LanePacket<BITS, D>& pk, int P, const uint2* xs, const float* xbar,
-                                       int packets, int M, int lane, float (&acc)[MT]) {
+                                       int lane, float (&acc)[MT]) {
     typedef typename XOps<XT>::vec4 vec4;
     vec4 lo0[8], lo1[8], hi0[8], hi1[8];
     word_operands<XT>(pk.c.x, lo0);
@@ -430,47 +433,48 @@ __device__ inline void var_packet_step(const LanePacket<BITS, D>& pk, int P, con
         high_operands<XT>(pk.h.x, hi0);
         if constexpr (NG == 2) high_operands<XT>(pk.h.y, hi1);
     }
+    const uint2* xp = xs + static_cast<size_t>(P) * MT * 64 + lane;
+    const float* bp = xbar + static_cast<size_t>(P) * MT * 16 + (lane & 3) * 4;
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
-        if (t < M) {
-            const size_t tp = static_cast<size_t>(t) * packets + P;
-            const vec4 xo = __builtin_bit_cast(vec4, xs[tp * 64 + lane]);
-            const f32x4 xb = *reinterpret_cast<const f32x4*>(xbar + tp * 16 + (lane & 3) * 4);
+        {
+            const vec4 xo = __builtin_bit_cast(vec4, xp[t * 64]);
+            const f32x4 xb = *reinterpret_cast<const f32x4*>(bp + t * 16);
             var_group<XT, BITS, D, 0>(xo, xb, lo0, hi0, pk, acc[t]);
             if constexpr (NG == 2) var_group<XT, BITS, D, 1>(xo, xb, lo1, hi1, pk, acc[t]);
         }
     }
 }
 
-// LDS of the matrix-vector kernel: staged operands xs [M][packets][64],
-// per-group sums xbar [M][packets][16], the cross-wavefront sums red
-// [waves][mt][16]; with the fused transform also the transformed rows
-// xt [M][K] (activation type) and the transform's exchange buffer z [K] (fp32),
-// which starts at offset 0 over xs (dead until the staging writes it) and,
-// for a single row, xt too.
-__host__ __device__ inline size_t gemv_lds_bytes(int K, int M, int waves, int mt) {
+// LDS of the matrix-vector kernel (M tokens): staged operands xs
+// [packets][M][64], per-group sums xbar [packets][M][16], the
+// cross-wavefront sums red [waves][M][16]; with the fused transform also the
+// transformed rows xt [M][K] (activation type) and the transform's exchange
+// buffer z [K] (fp32), which starts at offset 0 over xs (dead until the
+// staging writes it) and, for a single row, xt too.
+__host__ __device__ inline size_t gemv_lds_bytes(int K, int M, int waves) {
     const size_t packets = (K / kGroup + 1) / 2;
     return static_cast<size_t>(M) * packets * (kXsPacketBytes + kXbarPacketBytes) +
-           static_cast<size_t>(waves) * mt * 16 * 4;
+           static_cast<size_t>(waves) * M * 16 * 4;
 }
-__host__ __device__ inline size_t gemv_rht_xt_offset(int K, int M, int waves, int mt) {
-    return (gemv_lds_bytes(K, M, waves, mt) + 15) / 16 * 16;
+__host__ __device__ inline size_t gemv_rht_xt_offset(int K, int M, int waves) {
+    return (gemv_lds_bytes(K, M, waves) + 15) / 16 * 16;
 }
-__host__ __device__ inline size_t gemv_rht_z_offset(int K, int M, int waves, int mt) {
+__host__ __device__ inline size_t gemv_rht_z_offset(int K, int M, int waves) {
     // one row: z may overlap xt as well (the row's x' is written after the
     // last read of z); several rows: the next row's z must not overwrite x'
     if (M == 1) return 0;
-    const size_t base = gemv_lds_bytes(K, M, waves, mt);
-    return static_cast<size_t>(K) * 4 <= base ? 0 : gemv_rht_xt_offset(K, M, waves, mt) + static_cast<size_t>(M) * K * 2;
+    const size_t base = gemv_lds_bytes(K, M, waves);
+    return static_cast<size_t>(K) * 4 <= base ? 0 : gemv_rht_xt_offset(K, M, waves) + static_cast<size_t>(M) * K * 2;
 }
-__host__ __device__ inline size_t gemv_rht_lds_bytes(int K, int M, int waves, int mt) {
-    const size_t zo = gemv_rht_z_offset(K, M, waves, mt);
-    const size_t end_xt = gemv_rht_xt_offset(K, M, waves, mt) + static_cast<size_t>(M) * K * 2;
+__host__ __device__ inline size_t gemv_rht_lds_bytes(int K, int M, int waves) {
+    const size_t zo = gemv_rht_z_offset(K, M, waves);
+    const size_t end_xt = gemv_rht_xt_offset(K, M, waves) + static_cast<size_t>(M) * K * 2;
     const size_t end_z = zo + static_cast<size_t>(K) * 4;
     return end_xt > end_z ? end_xt : end_z;
 }
 
-// The input-side transform of M <= MT rows of K = 2^KLOG elements on eight
+// The input-side transform of MT rows of K = 2^KLOG elements on eight
 // wavefronts (512 threads; in a sixteen-wavefront workgroup the other eight
 // wait at the barriers), with the thread layout and the butterfly order of
 // the standalone transform for the same K (W = 3 wavefront bits, KLOG - 9
@@ -481,12 +485,12 @@ __host__ __device__ inline size_t gemv_rht_lds_bytes(int K, int M, int waves, in
 // the signs, both loaded by the caller.
 template <typename XT, int KLOG, int MT>
 __device__ inline void rht_prologue(const uint32_t (&xraw)[MT][1 << (KLOG - 9)], const float (&sraw)[1 << (KLOG - 9)],
-                                    int M, int lane, int wave, float norm, float* z, XT* xt) {
+                                    int lane, int wave, float norm, float* z, XT* xt) {
     constexpr int LR = KLOG - 9, R = 1 << LR, K = 1 << KLOG;
     const bool tw = wave < 8;  // a sixteen-wavefront workgroup's upper half only passes the barriers
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
-        if (t < M) {  // uniform
+        {
             float v[R];
 #pragma unroll
             for (int r = 0; r < R; ++r)
@@ -527,16 +531,17 @@ __device__ inline void rht_prologue(const uint32_t (&xraw)[MT][1 << (KLOG - 9)],
     __syncthreads();  // xt complete; z dead
 }
 
-// Template parameters: WAVES wavefronts per workgroup, MT the largest token
-// count, PF packets in flight per wavefront, NX activation load instructions
-// per wavefront (issued ahead of the packet loads), OCC the minimum
+// Template parameters: WAVES wavefronts per workgroup, MT the token count
+// (exactly; 1 to 4), PF packets in flight per wavefront, QX the packets per
+// wavefront whose activations (all MT tokens) are loaded ahead of the packet
+// loads (the rest are staged after them), OCC the minimum
 // wavefronts per SIMD the register allocation must allow; SHARED: codes-only
 // weights with row-shared pairs; BITS, D: the code width and vector
 // dimension (anything but 2, 4 is a variant, always SHARED).
 // RHTK > 0: the activations enter in the original basis and the workgroup
 // first applies the input-side transform x' = (x diag(s)) H / sqrt(K) of
 // Eq. 5 itself, K = 2^RHTK (see rht_prologue).
-template <typename XT, int WAVES, int MT, int PF, int NX, int OCC, bool SHARED, int BITS = 2, int D = 4, int RHTK = 0>
+template <typename XT, int WAVES, int MT, int PF, int QX, int OCC, bool SHARED, int BITS = 2, int D = 4, int RHTK = 0>
 __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch batch) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     constexpr bool kVar = BITS != 2 || D != 4;
@@ -565,7 +570,6 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
             if constexpr (RHTK > 0) sgn = batch.signs[i];
         }
     }
-    const int M = batch.M;
     const int rb = bid - rb0;
     const int groups = K >> 7;
     const int nfull = groups >> 1;
@@ -574,9 +578,9 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
 
-    uint2* xs = reinterpret_cast<uint2*>(smem);                                                    // [M][packets][64]
-    float* xbar = reinterpret_cast<float*>(smem + static_cast<size_t>(M) * packets * kXsPacketBytes);  // [M][packets][4][4]
-    float* red = xbar + static_cast<size_t>(M) * packets * 16;                                     // [WAVES][MT][16]
+    uint2* xs = reinterpret_cast<uint2*>(smem);                                                     // [packets][MT][64]
+    float* xbar = reinterpret_cast<float*>(smem + static_cast<size_t>(MT) * packets * kXsPacketBytes);  // [packets][MT][4][4]
+    float* red = xbar + static_cast<size_t>(MT) * packets * 16;                                     // [WAVES][MT][16]
 
     // This wavefront's run: full packets [p0, p0 + np), plus the trailing
     // half packet (packet nfull) for the last wavefront.
@@ -588,24 +592,20 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
     const int pbeg = do_half && np == 0 ? nfull : p0;
 
     // 1. Activation loads for exactly this wavefront's packets, before the
-    //    packet loads so that staging them waits for nothing else.  Load c
-    //    covers token c / npw, packet pbeg + c % npw; lane l reads the four
-    //    activations operand_unit<D>(l) of the packet.  Loads stay outside any
-    //    branch (a branch around a load makes the wait counters drain
-    //    completely at the join); an unneeded load, and the second group of
-    //    the half packet, get an offset past the end of the buffer and return
-    //    zeros without touching memory.
-    const int loads_w = M * npw;
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(M) * K * 2u);
+    //    packet loads so that staging them waits for nothing else: for each
+    //    token t and each of the first QX packets pbeg + q of the run, lane l
+    //    reads the four activations operand_unit<D>(l) of the packet.  Loads
+    //    stay outside any branch (a branch around a load makes the wait
+    //    counters drain completely at the join); a load past the run, and the
+    //    second group of the half packet, get an offset past the end of the
+    //    buffer and return zeros without touching memory.
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(MT) * K * 2u);
     const uint32_t vlane = operand_unit<D>(lane);
-    auto x_off = [&](int c) -> uint32_t {
-        const int t = MT == 1 || npw == 0 ? 0 : c / npw;
-        const int P = pbeg + (c - t * npw);
-        const uint32_t k = static_cast<uint32_t>(P) * 256u + 4u * vlane;
-        return c < loads_w && k < static_cast<uint32_t>(K) ? (static_cast<uint32_t>(t) * K + k) * 2u
-                                                           : kOutOfRange;
+    auto x_off = [&](int t, int q) -> uint32_t {
+        const uint32_t k = static_cast<uint32_t>(pbeg + q) * 256u + 4u * vlane;
+        return q < npw && k < static_cast<uint32_t>(K) ? (static_cast<uint32_t>(t) * K + k) * 2u : kOutOfRange;
     };
-    uint2 xr[NX];
+    uint2 xr[MT][QX];
     constexpr int kRR = RHTK > 0 ? 1 << (RHTK - 9) : 1;  // transform elements per thread and token
     uint32_t xraw[RHTK > 0 ? MT : 1][kRR];
     float sraw[kRR];
@@ -618,13 +618,15 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
             const bool tw = wave < 8;  // the transform's wavefronts
 #pragma unroll
             for (int t = 0; t < MT; ++t)
-                xraw[t][r] = ld16(rx, t < M && tw ? (static_cast<uint32_t>(t) * K + i) * 2u : kOutOfRange);
+                xraw[t][r] = ld16(rx, tw ? (static_cast<uint32_t>(t) * K + i) * 2u : kOutOfRange);
             sraw[r] = static_cast<float>(static_cast<signed char>(
                 __builtin_amdgcn_raw_buffer_load_b8(rsg, tw ? static_cast<uint32_t>(i) : kOutOfRange, 0, 0)));
         }
     } else {
 #pragma unroll
-        for (int i = 0; i < NX; ++i) xr[i] = ld64(rx, x_off(i));
+        for (int t = 0; t < MT; ++t)
+#pragma unroll
+            for (int q = 0; q < QX; ++q) xr[t][q] = ld64(rx, x_off(t, q));
     }
     __builtin_amdgcn_sched_barrier(0);  // keep the activation loads ahead of the packet loads
 
@@ -690,28 +692,30 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
     if constexpr (RHTK > 0) {
         // the transformed rows x' (rounded to the activation type, as a
         // standalone transform writing XT would) into LDS, then staged from there
-        XT* xt = reinterpret_cast<XT*>(smem + gemv_rht_xt_offset(K, M, WAVES, MT));
-        float* z = reinterpret_cast<float*>(smem + gemv_rht_z_offset(K, M, WAVES, MT));
-        rht_prologue<XT, RHTK, MT>(xraw, sraw, M, lane, wave, batch.rht_norm, z, xt);
-        for (int i = 0; i < loads_w; ++i) {
-            const uint32_t off = x_off(i);
-            const uint2 raw = off < kOutOfRange ? *reinterpret_cast<const uint2*>(
-                                                      reinterpret_cast<const unsigned char*>(xt) + off)
-                                                : uint2{0u, 0u};
-            const int t = MT == 1 ? 0 : i / npw;
-            stage_packet<XT>(raw, t, pbeg + (i - t * npw), packets, lane, xs, xbar);
+        XT* xt = reinterpret_cast<XT*>(smem + gemv_rht_xt_offset(K, MT, WAVES));
+        float* z = reinterpret_cast<float*>(smem + gemv_rht_z_offset(K, MT, WAVES));
+        rht_prologue<XT, RHTK, MT>(xraw, sraw, lane, wave, batch.rht_norm, z, xt);
+        for (int q = 0; q < npw; ++q) {
+#pragma unroll
+            for (int t = 0; t < MT; ++t) {
+                const uint32_t off = x_off(t, q);
+                const uint2 raw = off < kOutOfRange ? *reinterpret_cast<const uint2*>(
+                                                          reinterpret_cast<const unsigned char*>(xt) + off)
+                                                    : uint2{0u, 0u};
+                stage_packet<XT, MT>(raw, t, pbeg + q, lane, xs, xbar);
+            }
         }
     } else {
 #pragma unroll
-        for (int i = 0; i < NX; ++i) {
-            if (i < loads_w) {
-                const int t = MT == 1 ? 0 : i / npw;
-                stage_packet<XT>(xr[i], t, pbeg + (i - t * npw), packets, lane, xs, xbar);
+        for (int q = 0; q < QX; ++q) {
+            if (q < npw) {
+#pragma unroll
+                for (int t = 0; t < MT; ++t) stage_packet<XT, MT>(xr[t][q], t, pbeg + q, lane, xs, xbar);
             }
         }
-        for (int i = NX; i < loads_w; ++i) {  // more than NX loads: not overlapped with the packets
-            const int t = MT == 1 ? 0 : i / npw;
-            stage_packet<XT>(ld64(rx, x_off(i)), t, pbeg + (i - t * npw), packets, lane, xs, xbar);
+        for (int q = QX; q < npw; ++q) {  // more than QX packets: not overlapped with the packet loads
+#pragma unroll
+            for (int t = 0; t < MT; ++t) stage_packet<XT, MT>(ld64(rx, x_off(t, q)), t, pbeg + q, lane, xs, xbar);
         }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -728,13 +732,13 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
         if (np <= PF) {
 #pragma unroll
             for (int j = 0; j < PF; ++j)
-                if (j < np) var_packet_step<XT, MT, BITS, D, 2>(vbuf[j], p0 + j, xs, xbar, packets, M, lane, acc);
+                if (j < np) var_packet_step<XT, MT, BITS, D, 2>(vbuf[j], p0 + j, xs, xbar, lane, acc);
         } else {
             for (int i = 0; i < np; i += PF) {
 #pragma unroll
                 for (int j = 0; j < PF; ++j) {
                     if (i + j < np)
-                        var_packet_step<XT, MT, BITS, D, 2>(vbuf[j], p0 + i + j, xs, xbar, packets, M, lane, acc);
+                        var_packet_step<XT, MT, BITS, D, 2>(vbuf[j], p0 + i + j, xs, xbar, lane, acc);
                     const int nxt = i + j + PF;
                     load_var(p0 + nxt, nxt < np, vbuf[j]);
                 }
@@ -745,13 +749,13 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
 #pragma unroll
             for (int j = 0; j < PF; ++j)
                 if (j < np)
-                    packet_step<XT, MT>(cbuf[j], abuf[j], bbuf[j], p0 + j, xs, xbar, packets, M, lane, acc);
+                    packet_step<XT, MT>(cbuf[j], abuf[j], bbuf[j], p0 + j, xs, xbar, lane, acc);
         } else {
             for (int i = 0; i < np; i += PF) {
 #pragma unroll
                 for (int j = 0; j < PF; ++j) {
                     if (i + j < np)
-                        packet_step<XT, MT>(cbuf[j], abuf[j], bbuf[j], p0 + i + j, xs, xbar, packets, M, lane, acc);
+                        packet_step<XT, MT>(cbuf[j], abuf[j], bbuf[j], p0 + i + j, xs, xbar, lane, acc);
                     const int nxt = i + j + PF;
                     load_pkt(p0 + nxt, nxt < np, cbuf[j], abuf[j], bbuf[j]);
                 }
@@ -777,7 +781,7 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
                 hp.a[0] = uint4{a.x, a.y, 0u, 0u};
                 hp.b[0] = ld16(ra, R + kRecordBiasOff + 4 * jcol);
             }
-            var_packet_step<XT, MT, BITS, D, 1>(hp, nfull, xs, xbar, packets, M, lane, acc);
+            var_packet_step<XT, MT, BITS, D, 1>(hp, nfull, xs, xbar, lane, acc);
         } else {
             const uint2 hc = ld64_stream(rw, hoff + 8 * lane);
             uint2 ha;
@@ -790,7 +794,7 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
                 ha = ld64_stream(rw, hoff + kHalfAffineOff + 8 * lane);
                 hb = ld16_stream(rw, hoff + kHalfBiasOff + 2 * lane);
             }
-            half_step<XT, MT>(hc, ha, hb, nfull, xs, xbar, packets, M, lane, acc);
+            half_step<XT, MT>(hc, ha, hb, nfull, xs, xbar, lane, acc);
         }
     }
 
@@ -801,7 +805,7 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
         if ((lane & 3) == 0) red[(wave * MT + t) * 16 + (lane >> 2)] = v;
     }
     __syncthreads();
-    if (threadIdx.x < M * 16) {
+    if (threadIdx.x < MT * 16) {
         const int t = threadIdx.x >> 4, r = threadIdx.x & 15;
         float s = 0.f;
 #pragma unroll
@@ -814,25 +818,35 @@ __global__ __launch_bounds__(WAVES * 64, OCC) void gemv_kernel(const GemvBatch b
 constexpr size_t kMaxLds = 160 * 1024;
 
 
-template <typename XT, bool SHARED, int WAVES, int MT, int PF, int NX, int BITS = 2, int D = 4>
+template <typename XT, bool SHARED, int WAVES, int MT, int PF, int QX, int BITS = 2, int D = 4>
 int launch_cfg(const GemvBatch& b, int blocks, int maxK, hipStream_t s) {
-    const size_t lds = gemv_lds_bytes(maxK, b.M, WAVES, MT);
+    const size_t lds = gemv_lds_bytes(maxK, MT, WAVES);
     if (lds > kMaxLds) return UNISVQ_EUNSUP;
     // the dynamic-LDS limit, raised once per instantiation and device
     static std::atomic<uint64_t> attr_done{0};
-    const int st = ensure_lds_limit(reinterpret_cast<const void*>(&gemv_kernel<XT, WAVES, MT, PF, NX, 1, SHARED, BITS, D>),
+    const int st = ensure_lds_limit(reinterpret_cast<const void*>(&gemv_kernel<XT, WAVES, MT, PF, QX, 1, SHARED, BITS, D>),
                                     static_cast<int>(kMaxLds), attr_done);
     if (st != UNISVQ_OK) return st;
-    hipLaunchKernelGGL((gemv_kernel<XT, WAVES, MT, PF, NX, 1, SHARED, BITS, D>), dim3(static_cast<unsigned>(blocks)),
+    hipLaunchKernelGGL((gemv_kernel<XT, WAVES, MT, PF, QX, 1, SHARED, BITS, D>), dim3(static_cast<unsigned>(blocks)),
                        dim3(WAVES * 64), lds, s, b);
     return hipGetLastError() == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
 }
 
 // Launch geometry for a batch: WAVES wavefronts per 16-row block, PF packets
-// in flight per wavefront, NX activation loads per wavefront issued up front.
+// in flight per wavefront, QX packets per wavefront whose activations are
+// loaded up front.
 struct GemvPlan {
-    int waves, pf, nx;
+    int waves, pf, qx;
 };
+
+// Packets per wavefront whose activations load up front: the whole run (the
+// half packet included), as a power of two, at most 8 loads for all tokens.
+inline int plan_qx(int per_wave, int M) {
+    const int cap = M == 1 ? 8 : (M == 2 ? 4 : 2);
+    int q = 1;
+    while (q < per_wave && q < cap) q *= 2;
+    return q;
+}
 
 GemvPlan plan_gemv(int64_t blocks, int min_groups, int max_groups, int M) {
     (void)blocks;
@@ -852,9 +866,7 @@ GemvPlan plan_gemv(int64_t blocks, int min_groups, int max_groups, int M) {
     const int per = (packets + p.waves - 1) / p.waves;
     const int per_min = (min_groups / 2 + p.waves - 1) / p.waves;
     p.pf = M == 1 && per_min > 2 && per_min <= 4 ? 4 : 2;
-    // one activation load per packet and token (the half packet included)
-    const int loads = M * (per + (max_groups & 1));
-    p.nx = loads <= 1 ? 1 : (loads <= 2 ? 2 : (loads <= 4 ? 4 : 8));
+    p.qx = plan_qx(per + (max_groups & 1), M);
     return p;
 }
 

@@ -12,7 +12,7 @@ namespace {
 
 template <typename XT, int WAVES, int MT, int PF, int KLOG>
 int launch_rht_cfg(const GemvBatch& b, int blocks, hipStream_t s) {
-    const size_t lds = gemv_rht_lds_bytes(1 << KLOG, b.M, WAVES, MT);
+    const size_t lds = gemv_rht_lds_bytes(1 << KLOG, MT, WAVES);
     if (lds > kMaxLds) return UNISVQ_EUNSUP;
     static std::atomic<uint64_t> attr_done{0};
     const int st = ensure_lds_limit(reinterpret_cast<const void*>(&gemv_kernel<XT, WAVES, MT, PF, 1, 1, false, 2, 4, KLOG>),
@@ -36,6 +36,7 @@ int launch_rht_tokens(const GemvBatch& b, int blocks, hipStream_t s) {
         return p.pf == 4 ? launch_rht_cfg<XT, 8, 1, 4, KLOG>(b, blocks, s) : launch_rht_cfg<XT, 8, 1, 2, KLOG>(b, blocks, s);
     }
     if (b.M == 2) return launch_rht_cfg<XT, 8, 2, 2, KLOG>(b, blocks, s);
+    if (b.M == 3) return launch_rht_cfg<XT, 8, 3, 2, KLOG>(b, blocks, s);
     return launch_rht_cfg<XT, 8, 4, 2, KLOG>(b, blocks, s);
 }
 

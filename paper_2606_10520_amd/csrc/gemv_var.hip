@@ -9,21 +9,23 @@ namespace {
 
 // (b = 2, d = 4 is the codes-only format of the main path, not a variant.)
 // Geometry: 8 wavefronts per 16-row block and 2 packets in flight (a d = 8
-// packet holds 64 bytes of A columns per lane); the activation loads issued
-// up front cover the run when it is short (2) or up to 8 loads.
+// packet holds 64 bytes of A columns per lane); the activations of the run's
+// packets load up front (plan_qx).
 template <typename XT, int BITS, int D, int MT>
 int launch_var_mt(const GemvBatch& b, int blocks, int minK, int maxK, hipStream_t s) {
     (void)minK;
     const int per = (maxK / kGroup / 2 + 7) / 8;
-    const int loads = b.M * (per + ((maxK / kGroup) & 1));
-    if (loads <= 2) return launch_cfg<XT, true, 8, MT, 2, 2, BITS, D>(b, blocks, maxK, s);
-    return launch_cfg<XT, true, 8, MT, 2, 8, BITS, D>(b, blocks, maxK, s);
+    const int qx = plan_qx(per + ((maxK / kGroup) & 1), MT);
+    if (qx <= 1) return launch_cfg<XT, true, 8, MT, 2, 1, BITS, D>(b, blocks, maxK, s);
+    if (qx == 2) return launch_cfg<XT, true, 8, MT, 2, 2, BITS, D>(b, blocks, maxK, s);
+    return launch_cfg<XT, true, 8, MT, 2, (MT > 1 ? 4 : 8), BITS, D>(b, blocks, maxK, s);
 }
 
 template <typename XT, int BITS, int D>
 int launch_var_tokens(const GemvBatch& b, int blocks, int minK, int maxK, hipStream_t s) {
     if (b.M == 1) return launch_var_mt<XT, BITS, D, 1>(b, blocks, minK, maxK, s);
     if (b.M == 2) return launch_var_mt<XT, BITS, D, 2>(b, blocks, minK, maxK, s);
+    if (b.M == 3) return launch_var_mt<XT, BITS, D, 3>(b, blocks, minK, maxK, s);
     return launch_var_mt<XT, BITS, D, 4>(b, blocks, minK, maxK, s);
 }
 

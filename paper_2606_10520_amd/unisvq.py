@@ -29,7 +29,7 @@ EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "uni
            "unisvq_var_pack", "unisvq_var_unpack", "unisvq_var_gemv", "unisvq_var_gemv_batched",
            "unisvq_var_gemm_workspace_bytes", "unisvq_var_gemm", "unisvq_ldlq_workspace_bytes", "unisvq_ldlq",
            "unisvq_gemv_rht_batched", "unisvq_read_sink_words", "unisvq_read_bytes", "unisvq_noalloc_scratch_bytes",
-           "unisvq_gemm_noalloc")
+           "unisvq_gemm_noalloc", "unisvq_gemm_batched_workspace_bytes", "unisvq_gemm_batched")
 # format variants: (bits, d) pairs served by the unisvq_var_* entry points
 VARIANTS = ((3, 4), (2, 8), (3, 8))
 MAX_BATCH = 8
@@ -139,6 +139,10 @@ def load():
     lib.unisvq_ldlq_workspace_bytes.restype = sz
     lib.unisvq_ldlq.argtypes = [i64, i64, p, p, p, p, i64, p, p, sz, p]
     lib.unisvq_ldlq.restype = i32
+    lib.unisvq_gemm_batched_workspace_bytes.argtypes = [ctypes.POINTER(GemvProblem), i32, i64, i32]
+    lib.unisvq_gemm_batched_workspace_bytes.restype = sz
+    lib.unisvq_gemm_batched.argtypes = [ctypes.POINTER(GemvProblem), i32, i64, i32, i32, p, sz, p]
+    lib.unisvq_gemm_batched.restype = i32
     lib.unisvq_noalloc_scratch_bytes.argtypes = []
     lib.unisvq_noalloc_scratch_bytes.restype = sz
     lib.unisvq_gemm_noalloc.argtypes = [i64, i64, p, i64, p, i32, p, i32, p]
@@ -404,6 +408,36 @@ def gemm_noalloc(packed, N: int, K: int, x, out=None, out_dtype=None, stream=Non
     call allocates nothing; pass `out` to keep this wrapper from allocating
     the output)."""
     return _product("unisvq_gemm_noalloc", N, K, packed, x, out, out_dtype, stream)
+
+
+def gemm_batched(problems, out_dtype=None, workspace=None, stream=None):
+    """Several independent products (same M and dtypes), each as unisvq_gemm:
+    one launch for M <= 32.  problems: sequence of (packed, N, K, x, out-or-None).
+    Returns the list of outputs."""
+    if not 1 <= len(problems) <= MAX_BATCH:
+        raise ValueError(f"1..{MAX_BATCH} problems per call")
+    arr = (GemvProblem * len(problems))()
+    outs, M, xdt = [], None, None
+    for i, (packed, N, K, x, out) in enumerate(problems):
+        _need_cuda(packed, x, out)
+        _need_buffer(packed, packed_bytes(N, K), "packed", exact=True)
+        x2 = _activations(x, K)
+        if M is None:
+            M, xdt = x2.shape[0], x2.dtype
+        if x2.shape[0] != M or x2.dtype != xdt:
+            raise ValueError("all problems need the same token count and activation dtype")
+        out = _output(out, M, N, out_dtype, x2)
+        outs.append(out)
+        arr[i] = GemvProblem(N, K, packed.data_ptr(), x2.data_ptr(), out.data_ptr())
+    if len({o.dtype for o in outs}) != 1:
+        raise ValueError("all outputs need the same dtype")
+    lib = load()
+    need = lib.unisvq_gemm_batched_workspace_bytes(arr, len(problems), M, _dtype_code(xdt))
+    workspace, wb = _workspace(workspace, need, outs[0])
+    _check("unisvq_gemm_batched", lib.unisvq_gemm_batched(arr, len(problems), M, _dtype_code(xdt),
+                                                          _dtype_code(outs[0].dtype), _ptr(workspace), wb,
+                                                          _stream(stream)))
+    return outs
 
 
 # ------------------------------------------------ row-shared affine parameters

@@ -491,3 +491,27 @@ def test_gemm_noalloc_validation():
     assert lib.unisvq_gemm_workspace_bytes(4096, 16384, 1024, u.BF16) > cap
     assert f(4096, 16384, GOOD, 1024, GOOD, u.BF16, GOOD, u.F16, None) == ESCRATCH
     assert lib.unisvq_status_string(ESCRATCH).startswith(b"product needs more")
+
+
+def test_gemm_batched_validation():
+    lib = u.load()
+    P = u.GemvProblem
+    two = (P * 2)(P(4096, 4096, GOOD, GOOD, GOOD), P(1024, 4096, GOOD, GOOD, GOOD))
+    f = lib.unisvq_gemm_batched
+    assert f(None, 1, 16, u.F16, u.F16, None, 0, None) == EINVAL
+    assert f(two, 0, 16, u.F16, u.F16, None, 0, None) == EINVAL
+    assert f(two, 9, 16, u.F16, u.F16, None, 0, None) == EUNSUP
+    assert f(two, 2, 0, u.F16, u.F16, None, 0, None) == EINVAL
+    bad = (P * 2)(P(4096, 4096, GOOD, GOOD, GOOD), P(1000, 4096, GOOD, GOOD, GOOD))
+    assert f(bad, 2, 16, u.F16, u.F16, None, 0, None) == ESHAPE
+    mis = (P * 2)(P(4096, 4096, GOOD, GOOD, GOOD), P(1024, 4096, GOOD, GOOD + 8, GOOD))
+    assert f(mis, 2, 16, u.F16, u.F16, None, 0, None) == EALIGN
+    # fp16 activations at <= 32 tokens need no workspace; bf16 needs one slice per problem
+    assert lib.unisvq_gemm_batched_workspace_bytes(two, 2, 16, u.F16) == 0
+    need = lib.unisvq_gemm_batched_workspace_bytes(two, 2, 16, u.BF16)
+    singles = [lib.unisvq_gemm_workspace_bytes(N, 4096, 16, u.BF16) for N in (4096, 1024)]
+    assert need == sum(-(-s // 256) * 256 for s in singles) > 0
+    assert f(two, 2, 16, u.BF16, u.F16, None, need, None) == EWS
+    assert f(two, 2, 16, u.BF16, u.F16, GOOD, need - 1, None) == EWS
+    assert f(two, 2, 16, u.BF16, u.F16, GOOD + 8, need, None) == EALIGN
+    assert lib.unisvq_gemm_batched_workspace_bytes(two, 2, 16, 9) == 0

@@ -614,3 +614,80 @@ def test_read_bytes_folds_every_word():
     u.read_bytes(bufs[:1], store=False)
     torch.cuda.synchronize()
     assert torch.equal(sink, before)
+
+
+# ------------------------------------------- batched small-batch products
+
+@pytest.mark.parametrize("M", [5, 16, 17, 32, 40])
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_gemm_batched_matches_single_calls(M, dtype):
+    """q/k/v-style and gate/up-style batches (different N and K in one
+    launch, an odd group count): each output equals unisvq_gemm on that
+    problem alone bit for bit (the same kernel, workgroup and summation order),
+    and the single calls match the oracle."""
+    shapes = [(4096, 4096), (1024, 4096), (512, 11008), (64, 1152)]
+    probs, refs = [], []
+    for i, (N, K) in enumerate(shapes):
+        Q, A, B = wl.gen_weights(N, K, seed=90 + i)
+        xb = wl.gen_activations(M, K, seed=95 + i, dtype=dtype, outliers=True)
+        pk = upload_pack(Q, A, B)
+        probs.append((pk, N, K, dev_x(xb, dtype), None))
+        rows = np.arange(0, N, max(1, N // 64))
+        refs.append((rows, oracle.matmul(oracle.pack(Q, A, B)[0], N, K, x_as_f64(xb, dtype), rows=rows)))
+    outs = u.gemm_batched(probs, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    for (pk, N, K, x, _), y, (rows, ref) in zip(probs, outs, refs):
+        single = u.gemm(pk, N, K, x, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        assert torch.equal(y, single), (N, K)
+        assert rel_err(single.cpu().numpy()[:, rows], ref) <= 5e-4
+
+
+def test_gemm_batched_fp16_outputs_and_reruns():
+    M = 16
+    probs = []
+    for i, (N, K) in enumerate([(11008, 4096), (11008, 4096)]):
+        Q, A, B = wl.gen_weights(N, K, seed=70 + i)
+        probs.append((upload_pack(Q, A, B), N, K, dev_x(wl.gen_activations(M, K, seed=71, dtype="f16"), "f16"), None))
+    a = u.gemm_batched(probs, out_dtype=torch.float16)
+    b = u.gemm_batched(probs, out_dtype=torch.float16)
+    torch.cuda.synchronize()
+    for (pk, N, K, x, _), ya, yb in zip(probs, a, b):
+        assert torch.equal(ya, yb)
+        assert torch.equal(ya, u.gemm(pk, N, K, x, out_dtype=torch.float16))
+
+
+@pytest.mark.parametrize("M", [5, 16, 17, 32])
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_gemm_batched_64row_kernel(M, dtype):
+    """A batch with enough rows for the 64-row small-batch kernel (>= 160
+    workgroups): a partial last 64-row tile (2064 rows), an odd group count
+    (K = 1152: the last step holds a half packet) and K = 11008; every output
+    against the oracle on sampled rows incl. the last tile, and equal to single
+    calls where those take the same kernel."""
+    shapes = [(4096, 1152), (4096, 4096), (2064, 11008)]
+    probs, refs = [], []
+    for i, (N, K) in enumerate(shapes):
+        Q, A, B = wl.gen_weights(N, K, seed=110 + i)
+        xb = wl.gen_activations(M, K, seed=115 + i, dtype=dtype, outliers=True)
+        probs.append((upload_pack(Q, A, B), N, K, dev_x(xb, dtype), None))
+        rows = np.unique(np.concatenate([np.arange(0, N, 97), np.arange(N - 80, N)]))
+        refs.append((rows, oracle.matmul(oracle.pack(Q, A, B)[0], N, K, x_as_f64(xb, dtype), rows=rows)))
+    outs = u.gemm_batched(probs, out_dtype=torch.float32)
+    outs16 = u.gemm_batched(probs, out_dtype=torch.float16)
+    torch.cuda.synchronize()
+    for y, y16, (rows, ref) in zip(outs, outs16, refs):
+        assert rel_err(y.cpu().numpy()[:, rows], ref) <= 5e-4
+        assert torch.equal(y16, y.to(torch.float16))
+
+
+@pytest.mark.parametrize("per_group", [False, True])
+def test_gemm_shared_64row_kernel(per_group):
+    """Row-shared pairs through the 64-row kernel (a single problem with
+    11008 rows gives 172 workgroups)."""
+    N, K, M = 11008, 1152, 16
+    Ga = K // 128 if per_group else 1
+    y, (Q, A, B), xb = run_shared("gemm_shared", N, K, M, Ga, "f16", seed=120)
+    rows = np.unique(np.concatenate([np.arange(0, N, 101), np.arange(N - 64, N)]))
+    ref = oracle.matmul_shared(oracle.pack_codes(Q)[0], N, K, A, B, x_as_f64(xb, "f16"), rows=rows)
+    assert rel_err(y.cpu().numpy()[:, rows], ref) <= 5e-4
