@@ -190,8 +190,7 @@ int launch_gemm_var(int64_t N, int64_t K, int bits, int d, const uint8_t* packed
 // (per token, may be null) multiplies the results.
 constexpr int64_t kSkinnyMaxM = 32;
 hipError_t launch_skinny(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine, int affine_one,
-                         int64_t M, const _Float16* x, const float* inv_scale, void* y, int y_dtype,
-                         hipStream_t s);
+                         int64_t M, const _Float16* x, const float* inv_scale, void* y, int y_dtype, hipStream_t s);
 // Several independent small-batch products (same M, the same weight format)
 // in one launch.
 struct SkinnyProblem {
@@ -204,10 +203,6 @@ struct SkinnyProblem {
     int64_t N, K;
 };
 hipError_t launch_skinny_batch(const SkinnyProblem* probs, int count, int64_t M, int y_dtype, hipStream_t s);
-// The same with 64-row workgroups whose four row blocks share each step's
-// staged activations (for batches with many rows); workgroups it launches.
-int64_t skinny64_workgroups(const SkinnyProblem* probs, int count);
-hipError_t launch_skinny64_batch(const SkinnyProblem* probs, int count, int64_t M, int y_dtype, hipStream_t s);
 // unisvq_gemm over a batch of problems (same M and dtypes): one launch for
 // M <= kSkinnyMaxM (after the bf16 pre-passes), else one product per problem.
 // Problem i uses the workspace bytes [off_i, off_i + gemm_workspace_bytes(i)),
