@@ -210,15 +210,19 @@ int unisvq_gemv_batched(const unisvq_gemv_problem* problems, int count, int64_t 
  * for BF16 activations an fp16 copy of x (M*K*2 bytes, rounded up to 256;
  * above 32 tokens the copy is kept in 16-token tiles, so M counts rounded up
  * to a multiple of 16) and one fp32 scale per token (rounded up to 256);
- * for products with too
- * few output tiles to fill the GPU (small M), fp32 partial sums of a split
- * along K (splits*M*N*4 bytes).  0 also for an invalid shape, M < 1 or an
+ * above 32 tokens, for products with too few output tiles to fill the GPU,
+ * fp32 partial sums of a split along K (splits*M*N*4 bytes).  0 also for an invalid shape, M < 1 or an
  * unknown x_dtype.  Host-only, no GPU needed. */
 size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype);
 
 /* Prefill product y = x * W_hat^T for any M >= 1 (Eq. 1 with Eq. 4/8).
  * Arguments as unisvq_gemv; x_dtype F16 or BF16, y_dtype F16, BF16 or F32.
- * Each workgroup decodes a 128-row x 128-column weight tile at a time into
+ * Up to 32 tokens one launch of the small-batch kernel computes it: each
+ * wavefront decodes 16-row x 128-column tiles into its own LDS region and
+ * multiplies them with all tokens at once; the wavefronts of a workgroup
+ * split K and add their sums in a fixed order (no workspace beyond the bf16
+ * copy below).  Above 32 tokens each
+ * workgroup decodes a 128-row x 128-column weight tile at a time into
  * LDS (every vector A q + B in fp32 from the exact integer codes, rounded
  * once to fp16) and multiplies it with its tokens on the matrix cores
  * (fp16 x fp16, fp32 accumulation); decoded weights never reach global

@@ -1,6 +1,7 @@
 // Small-batch product y = x * W_hat^T for 4 < M <= 32 tokens on gfx950.
 //
-// A workgroup owns RB 16-row blocks (RB = 1, 2 or 4) of one problem over all
+// A workgroup owns RB 16-row blocks (RB = 1, 2 or 4; at most 2 above 16
+// tokens) of one problem over all
 // of K; several independent problems may share a launch (a decoder's query,
 // key and value projections).  Its sixteen wavefronts split the packets (two
 // 128-column groups each) round robin -- wavefront w takes packets w, w + 16,
@@ -77,14 +78,6 @@ constexpr int skinny_lds_bytes() {
     return tiles > red ? tiles : red;
 }
 
-// Operands of one packet: the activations of its two groups and the RB
-// row blocks' pieces.
-template <int MT, int RB>
-struct PacketSet {
-    f16x8 xa[2][MT][4];
-    Piece pc[RB];
-};
-
 // MT token tiles of 16 (M <= 16 MT), RB row blocks per workgroup; SHARED:
 // codes-only weights with the shared affine block.
 template <int MT, int RB, bool SHARED>
@@ -118,35 +111,22 @@ __global__ __launch_bounds__(kWavesS * 64, (RB * MT <= 1 ? 8 : 4)) void skinny_k
     // 8 (lane / 16) + 32 c of a group
     const uint32_t xlane = (static_cast<uint32_t>(lane & 15) * K + 8 * (lane >> 4)) * 2u;
 
-    // Requests for packet p in the order they are used: the activations of
-    // group 2p, the first row block's piece, the activations of group 2p + 1,
-    // the other pieces.  Past the last group (or N) everything reads zeros
-    // without memory traffic.
-    auto issue = [&](int p, PacketSet<MT, RB>& st) {
-        auto load_x = [&](int jj) {
-            const int g = 2 * p + jj;
-            const uint32_t base = g < groups ? xlane + static_cast<uint32_t>(g) * 256u : kOutOfRange;
+    auto load_x = [&](int g, f16x8 (&xa)[MT][4]) {
+        const uint32_t base = g < groups ? xlane + static_cast<uint32_t>(g) * 256u : kOutOfRange;
 #pragma unroll
-            for (int i = 0; i < MT; ++i)
+        for (int i = 0; i < MT; ++i)
 #pragma unroll
-                for (int c = 0; c < 4; ++c)
-                    st.xa[jj][i][c] = __builtin_bit_cast(
-                        f16x8, ld128(rx, base + static_cast<uint32_t>(i) * (16u * K * 2u) + 64u * c));
-        };
-        auto load = [&](int b) {
-            const int rb = rb0 + b;
-            const uint32_t rowblk = static_cast<uint32_t>(rb) * groups * kBlockBytes;
-            const int gend = rb < nrb ? groups : 0;
-            if constexpr (SHARED)
-                load_packet_shared<true>(rw, ra, rowblk, p, gend, pb.affine_one, lane, st.pc[b]);
-            else
-                load_packet<true>(rw, rowblk, p, gend, lane, st.pc[b]);
-        };
-        load_x(0);
-        load(0);
-        load_x(1);
-#pragma unroll
-        for (int b = 1; b < RB; ++b) load(b);
+            for (int c = 0; c < 4; ++c)
+                xa[i][c] = __builtin_bit_cast(f16x8, ld128(rx, base + static_cast<uint32_t>(i) * (16u * K * 2u) + 64u * c));
+    };
+    auto load = [&](int p, int b, Piece& pc) {
+        const int rb = rb0 + b;
+        const uint32_t rowblk = static_cast<uint32_t>(rb) * groups * kBlockBytes;
+        const int gend = rb < nrb ? groups : 0;
+        if constexpr (SHARED)
+            load_packet_shared<true>(rw, ra, rowblk, p, gend, pb.affine_one, lane, pc);
+        else
+            load_packet<true>(rw, rowblk, p, gend, lane, pc);
     };
 
     const int j = lane & 3;
@@ -157,21 +137,27 @@ __global__ __launch_bounds__(kWavesS * 64, (RB * MT <= 1 ? 8 : 4)) void skinny_k
     for (int b = 0; b < RB; ++b)
 #pragma unroll
         for (int i = 0; i < MT; ++i) acc[b][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    auto compute = [&](const PacketSet<MT, RB>& st) {
+
+    // Packets wave, wave + 16, ...: a 4096-column row is one round.  Requests
+    // go out in the order they are used: the activations of group 2p, the
+    // first row block's piece, the activations of group 2p + 1, the other
+    // pieces (past the last group, or N, everything reads zeros without
+    // memory traffic).
+    for (int p = wave; p < packets; p += kWavesS) {  // uniform
+        Piece pc[RB];
+        f16x8 x0[MT][4], x1[MT][4];
+        load_x(2 * p, x0);
+        load(p, 0, pc[0]);
+        load_x(2 * p + 1, x1);
+#pragma unroll
+        for (int b = 1; b < RB; ++b) load(p, b, pc[b]);
 #pragma unroll
         for (int b = 0; b < RB; ++b) {
             if (rb0 + b < nrb) {  // uniform
-                tile_product<MT>(st.pc[b], 0, j, wrow, wlane, st.xa[0], acc[b]);
-                tile_product<MT>(st.pc[b], 1, j, wrow, wlane, st.xa[1], acc[b]);
+                tile_product<MT>(pc[b], 0, j, wrow, wlane, x0, acc[b]);
+                tile_product<MT>(pc[b], 1, j, wrow, wlane, x1, acc[b]);
             }
         }
-    };
-
-    // Packets wave, wave + 16, ...: a 4096-column row is one round.
-    for (int p = wave; p < packets; p += kWavesS) {  // uniform
-        PacketSet<MT, RB> st;
-        issue(p, st);
-        compute(st);
     }
 
     // The sixteen wavefronts meet in LDS (over the decode tiles).  D lane
@@ -240,7 +226,7 @@ int pick_rb(const SkinnyProblem* probs, int count, int max_rb) {
 
 hipError_t launch_skinny_batch(const SkinnyProblem* probs, int count, int64_t M, int y_dtype, hipStream_t s) {
     if (count < 1 || count > kMaxBatch || M < 1 || M > kSkinnyMaxM) return hipErrorInvalidValue;
-    // 32-token tiles keep at most two row blocks (the reduction's LDS)
+    // two token tiles, at most two row blocks (the reduction's LDS)
     const int rb = pick_rb(probs, count, M > 16 ? 2 : 4);
     SkBatch b{};
     int blocks = 0;

@@ -162,6 +162,7 @@ def test_gemm_workspace():
     assert ws(4096, 4096, 2048, u.F16) == 0
     # above the small-batch range the fp16 copy is tiled (16-token tiles): 33 tokens take 48 rows
     assert ws(64, 256, 33, u.BF16) == 48 * 256 * 2 + 256
+    assert ws(64, 256, 32, u.BF16) == 32 * 256 * 2 + 256
     assert ws(16, 128, 1, u.BF16) == 256 + 256
     assert ws(16, 128, 1, u.F16) == 0
     assert ws(15, 128, 1, u.BF16) == 0

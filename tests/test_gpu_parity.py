@@ -193,7 +193,7 @@ def d4_inputs(N, K, M, seed):
     return Q, A, B, X
 
 
-@pytest.mark.parametrize("fn,M", [("gemv", 1), ("gemv", 4), ("gemm", 33)])
+@pytest.mark.parametrize("fn,M", [("gemv", 1), ("gemv", 4), ("gemm", 16), ("gemm", 32), ("gemm", 33)])
 def test_integer_inputs_bit_exact(fn, M):
     N, K = 512, 4096
     Q, A, B, X = d4_inputs(N, K, M, seed=M)
@@ -618,7 +618,7 @@ def test_read_bytes_folds_every_word():
 
 # ------------------------------------------- batched small-batch products
 
-@pytest.mark.parametrize("M", [5, 16, 17, 32, 40])
+@pytest.mark.parametrize("M", [5, 16, 17, 32, 33, 40])
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
 def test_gemm_batched_matches_single_calls(M, dtype):
     """q/k/v-style and gate/up-style batches (different N and K in one
@@ -659,8 +659,8 @@ def test_gemm_batched_fp16_outputs_and_reruns():
 
 # Small-batch launches by workgroup height (the launcher's choice for these
 # batches): four row blocks per workgroup (178 workgroups, one round), two
-# (4112 rows: 129 workgroups, the last one half full) and one (65 rows
-# blocks).  32-token launches take at most two.
+# (4112 rows: 129 workgroups, the last one half full) and one (65 row
+# blocks).  Launches of 17 to 32 tokens take at most two.
 SMALL_BATCH_SETS = {
     "rb4": [(4096, 1152), (4096, 4096), (2064, 11008), (1040, 2176)],
     "rb2": [(4112, 4224)],
