@@ -92,41 +92,58 @@ struct DecOps {
     f32x4 bvec;               // B[0..3]
 };
 
+// Lane permutation within each quad (DPP quad_perm): dest lane i reads lane
+// ((CTRL >> 2i) & 3).
+template <int CTRL>
+__device__ inline uint32_t quad_perm(uint32_t v) {
+    return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), CTRL, 0xf, 0xf, false));
+}
+
 // Gather, for group 2p + jj, the codes of vectors 4n+j, row j of A and all
 // of B from the four slots of the quad.
+//   Codes: lane b's word holds component b's 2-bit codes, field k of each
+//   byte for vector 4(byte) + k; lane j needs field j of every lane's word,
+//   as nibbles for the e2m1 converter: component 0 in the low nibble, 1 in
+//   the high one (p01), likewise 2 and 3 (p23).  The high nibble comes from a
+//   rotation of the other word by 2j - 4, which lands field j at bits 4-5 of
+//   each byte (bits that wrap around fall outside the mask).
+//   A: lane b holds column b (rows 0, 1 in word al, rows 2, 3 in ah); lane j
+//   needs row j.  A 4 x 4 transpose of 16-bit elements in two butterfly
+//   stages: the word pair across lanes j ^ 2, then the halves across j ^ 1.
+//   B: the word holds B[b] of both groups; each lane needs all four.
 // CODES_ONLY (the Eq. 9 fold, where A and B act on the activations): the
 // codes alone.
 template <bool CODES_ONLY = false>
 __device__ inline void prepare(const Piece& pc, int j, int jj, DecOps& d) {
     const uint32_t cl = jj ? pc.c.z : pc.c.x, ch = jj ? pc.c.w : pc.c.y;
     const uint32_t al = jj ? pc.a.z : pc.a.x, ah = jj ? pc.a.w : pc.a.y;
-    const uint32_t bv = jj ? pc.b >> 16 : pc.b & 0xffffu;
     const uint32_t cw[2][4] = {{quad_lane<0>(cl), quad_lane<1>(cl), quad_lane<2>(cl), quad_lane<3>(cl)},
                                {quad_lane<0>(ch), quad_lane<1>(ch), quad_lane<2>(ch), quad_lane<3>(ch)}};
     const int sh = 2 * j;
+    const int rot = (sh - 4) & 31;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-        uint32_t m[4];
-#pragma unroll
-        for (int b = 0; b < 4; ++b) m[b] = (cw[h][b] >> sh) & 0x03030303u;
-        d.p01[h] = m[0] | (m[1] << 4);
-        d.p23[h] = m[2] | (m[3] << 4);
+        d.p01[h] = ((cw[h][0] >> sh) & 0x03030303u) | (__builtin_amdgcn_alignbit(cw[h][1], cw[h][1], rot) & 0x30303030u);
+        d.p23[h] = ((cw[h][2] >> sh) & 0x03030303u) | (__builtin_amdgcn_alignbit(cw[h][3], cw[h][3], rot) & 0x30303030u);
     }
     if constexpr (CODES_ONLY) return;
-    // row j of A: half (j & 1) of word (j >> 1) of every column b
-    const uint32_t lo[4] = {quad_lane<0>(al), quad_lane<1>(al), quad_lane<2>(al), quad_lane<3>(al)};
-    const uint32_t hi[4] = {quad_lane<0>(ah), quad_lane<1>(ah), quad_lane<2>(ah), quad_lane<3>(ah)};
-    uint32_t w[4];
-#pragma unroll
-    for (int b = 0; b < 4; ++b) w[b] = j < 2 ? lo[b] : hi[b];
-    const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
-    const uint32_t a01 = __builtin_amdgcn_perm(w[1], w[0], sel);
-    const uint32_t a23 = __builtin_amdgcn_perm(w[3], w[2], sel);
+    const bool low = j < 2, odd = (j & 1) != 0;
+    // stage 1: lanes j < 2 keep rows 0, 1 of column j and receive those of
+    // column j + 2; lanes j >= 2 keep rows 2, 3 of column j, receive column j - 2
+    const uint32_t recv = quad_perm<0x4e>(low ? ah : al);  // [2, 3, 0, 1]
+    const uint32_t lowc = low ? al : recv;                 // column j & 1
+    const uint32_t highc = low ? recv : ah;                // column (j & 1) + 2
+    // stage 2: even lanes send their odd rows' halves, odd lanes their even
+    // rows'; each keeps its own row's halves
+    const uint32_t send2 = __builtin_amdgcn_perm(highc, lowc, odd ? 0x05040100u : 0x07060302u);
+    const uint32_t recv2 = quad_perm<0xb1>(send2);  // [1, 0, 3, 2]
+    const uint32_t a01 = __builtin_amdgcn_perm(recv2, lowc, odd ? 0x03020504u : 0x05040100u);
+    const uint32_t a23 = __builtin_amdgcn_perm(recv2, highc, odd ? 0x03020706u : 0x07060100u);
     d.arow = __builtin_bit_cast(f16x4, uint2{a01, a23});
-    d.bvec[0] = h2f(quad_lane<0>(bv));
-    d.bvec[1] = h2f(quad_lane<1>(bv));
-    d.bvec[2] = h2f(quad_lane<2>(bv));
-    d.bvec[3] = h2f(quad_lane<3>(bv));
+    // B of both groups per lane (the same four moves for either group)
+    const uint32_t bw[4] = {quad_lane<0>(pc.b), quad_lane<1>(pc.b), quad_lane<2>(pc.b), quad_lane<3>(pc.b)};
+#pragma unroll
+    for (int b = 0; b < 4; ++b) d.bvec[b] = h2f(jj ? bw[b] >> 16 : bw[b] & 0xffffu);
 }
 
 // Vectors 4N .. 4N+3 of the row block: one matrix-core instruction; lane
