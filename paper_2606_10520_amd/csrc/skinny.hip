@@ -1,6 +1,6 @@
 // Small-batch product y = x * W_hat^T for 4 < M <= 32 tokens on gfx950.
 //
-// A workgroup owns RB 16-row blocks (RB = 1, 2 or 4; at most 2 above 16
+// A workgroup owns RB 16-row blocks (RB = 1, 2, 3, 4 or 6; 1 above 16
 // tokens) of one problem over all
 // of K; several independent problems may share a launch (a decoder's query,
 // key and value projections).  Its sixteen wavefronts split the packets (two
@@ -143,20 +143,24 @@ __global__ __launch_bounds__(kWavesS * 64, (RB * MT <= 1 ? 8 : 4)) void skinny_k
     // first row block's piece, the activations of group 2p + 1, the other
     // pieces (past the last group, or N, everything reads zeros without
     // memory traffic).
+    // At most three pieces are in flight per wavefront (registers): row
+    // block b's piece is requested once row block b - 3 is done.
+    constexpr int kRing = RB < 3 ? RB : 3;
     for (int p = wave; p < packets; p += kWavesS) {  // uniform
-        Piece pc[RB];
+        Piece pc[kRing];
         f16x8 x0[MT][4], x1[MT][4];
         load_x(2 * p, x0);
         load(p, 0, pc[0]);
         load_x(2 * p + 1, x1);
 #pragma unroll
-        for (int b = 1; b < RB; ++b) load(p, b, pc[b]);
+        for (int b = 1; b < kRing; ++b) load(p, b, pc[b]);
 #pragma unroll
         for (int b = 0; b < RB; ++b) {
             if (rb0 + b < nrb) {  // uniform
-                tile_product<MT>(pc[b], 0, j, wrow, wlane, x0, acc[b]);
-                tile_product<MT>(pc[b], 1, j, wrow, wlane, x1, acc[b]);
+                tile_product<MT>(pc[b % kRing], 0, j, wrow, wlane, x0, acc[b]);
+                tile_product<MT>(pc[b % kRing], 1, j, wrow, wlane, x1, acc[b]);
             }
+            if (b + kRing < RB) load(p, b + kRing, pc[b % kRing]);
         }
     }
 
@@ -208,9 +212,11 @@ int pick_rb(const SkinnyProblem* probs, int count, int max_rb) {
         const int64_t w = (packets + kWavesS - 1) / kWavesS;
         ppw = w > ppw ? w : ppw;
     }
+    constexpr int kHeights[] = {6, 4, 3, 2, 1};
     int best = 1;
     int64_t best_cost = -1;
-    for (int rb = max_rb; rb >= 1; rb /= 2) {
+    for (const int rb : kHeights) {
+        if (rb > max_rb) continue;
         int64_t wgs = 0;
         for (int i = 0; i < count; ++i) wgs += (probs[i].N / kRowBlock + rb - 1) / rb;
         const int64_t cost = (wgs + 255) / 256 * (3 + rb * ppw);
@@ -226,8 +232,8 @@ int pick_rb(const SkinnyProblem* probs, int count, int max_rb) {
 
 hipError_t launch_skinny_batch(const SkinnyProblem* probs, int count, int64_t M, int y_dtype, hipStream_t s) {
     if (count < 1 || count > kMaxBatch || M < 1 || M > kSkinnyMaxM) return hipErrorInvalidValue;
-    // two token tiles, at most two row blocks (the reduction's LDS)
-    const int rb = pick_rb(probs, count, M > 16 ? 2 : 4);
+    // two token tiles: one row block per workgroup (registers)
+    const int rb = pick_rb(probs, count, M > 16 ? 1 : 6);
     SkBatch b{};
     int blocks = 0;
     for (int i = 0; i < count; ++i) {
@@ -240,10 +246,14 @@ hipError_t launch_skinny_batch(const SkinnyProblem* probs, int count, int64_t M,
     b.M = static_cast<int>(M);
     b.y_dtype = y_dtype;
     const bool shared = probs[0].affine != nullptr;
-    if (M > 16) return rb >= 2 ? launch_rb<2, 2>(b, blocks, shared, s) : launch_rb<2, 1>(b, blocks, shared, s);
-    return rb == 4   ? launch_rb<1, 4>(b, blocks, shared, s)
-           : rb == 2 ? launch_rb<1, 2>(b, blocks, shared, s)
-                     : launch_rb<1, 1>(b, blocks, shared, s);
+    if (M > 16) return launch_rb<2, 1>(b, blocks, shared, s);
+    switch (rb) {
+        case 6: return launch_rb<1, 6>(b, blocks, shared, s);
+        case 4: return launch_rb<1, 4>(b, blocks, shared, s);
+        case 3: return launch_rb<1, 3>(b, blocks, shared, s);
+        case 2: return launch_rb<1, 2>(b, blocks, shared, s);
+        default: return launch_rb<1, 1>(b, blocks, shared, s);
+    }
 }
 
 hipError_t launch_skinny(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine, int affine_one,

@@ -658,11 +658,17 @@ def test_gemm_batched_fp16_outputs_and_reruns():
 
 
 # Small-batch launches by workgroup height (the launcher's choice for these
-# batches): four row blocks per workgroup (178 workgroups, one round), two
-# (4112 rows: 129 workgroups, the last one half full) and one (65 row
-# blocks).  Launches of 17 to 32 tokens take at most two.
+# batches at up to 16 tokens; above 16 tokens every workgroup has one row
+# block): six row blocks per workgroup (two 11008-row problems, 230
+# workgroups, the last of each with four), four (1024 row blocks), three
+# (a 70B-q+k+v-like batch, 215 workgroups, the last of the first problem with
+# two row blocks), three again for a mix with multi-packet wavefronts, two (4112 rows: 129
+# workgroups, the last one half full) and one (65 row blocks).
 SMALL_BATCH_SETS = {
-    "rb4": [(4096, 1152), (4096, 4096), (2064, 11008), (1040, 2176)],
+    "rb6": [(11008, 4096), (11008, 2176)],
+    "rb4": [(16384, 1152)],
+    "rb3": [(8192, 2176), (1024, 2176), (1024, 2176)],
+    "mixed": [(4096, 1152), (4096, 4096), (2064, 11008), (1040, 2176)],
     "rb2": [(4112, 4224)],
     "rb1": [(1040, 2176)],
 }
@@ -672,13 +678,13 @@ SMALL_BATCH_SETS = {
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
 @pytest.mark.parametrize("which", sorted(SMALL_BATCH_SETS))
 def test_gemm_batched_edges(which, M, dtype):
-    """Small-batch workgroups at their edges: a partial last workgroup
-    (2064 = 129 x 16 rows, 4112 = 257 x 16), K = 1152 (five packets, the last
-    a half packet: eleven wavefronts have none), K = 2176 (nine packets),
-    K = 4224 (seventeen: wavefront 0 takes two, the second a half packet),
-    K = 11008 (43 packets: two or three per wavefront) and K = 4096; every
-    output element against the oracle, fp16 outputs equal to the rounded
-    fp32 ones."""
+    """Small-batch workgroups at their edges: partial last workgroups
+    (2064 = 129 x 16 rows, 4112 = 257 x 16, 11008 = 688 x 16), K = 1152 (five
+    packets, the last a half packet: eleven wavefronts have none), K = 2176
+    (nine packets), K = 4224 (seventeen: wavefront 0 takes two, the second a
+    half packet), K = 11008 (43 packets: two or three per wavefront) and
+    K = 4096; every output element against the oracle, fp16 outputs equal to
+    the rounded fp32 ones."""
     shapes = SMALL_BATCH_SETS[which]
     probs, refs = [], []
     for i, (N, K) in enumerate(shapes):
