@@ -451,7 +451,7 @@ class Case:
                              for L in layers)
         self.flops = sum(2 * M * L.N * L.K for L in layers)
         ws_bytes = 0
-        if self.kernel == "gemm" and M <= SKINNY_MAX_M and not ws.shared and not ws.var:
+        if self.kernel == "gemm" and not ws.shared and not ws.var and not fold:
             # batched launches (q+k+v, gate+up): the slices of all problems of a batch
             for grp in (layers[:3], layers[4:6], layers):
                 arr = (u.GemvProblem * len(grp))(*[u.GemvProblem(L.N, L.K, None, None, None) for L in grp])
@@ -475,8 +475,8 @@ class Case:
 
     # ---- schedules
     def batched_gemm(self):
-        """The small-batch product takes batches (q+k+v, gate+up) in one launch."""
-        return self.kernel == "gemm" and self.M <= SKINNY_MAX_M and not self.ws.shared and not self.ws.var
+        """unisvq_gemm_batched takes batches (q+k+v, gate+up) in one launch."""
+        return self.kernel == "gemm" and not self.ws.shared and not self.ws.var and not self.fold
 
     def groups(self, sched):
         full_set = {"q", "k", "v", "o", "gate", "up", "down"} <= set(self.names)

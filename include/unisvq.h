@@ -248,11 +248,16 @@ int unisvq_gemm(int64_t N, int64_t K, const void* packed, int64_t M, const void*
 size_t unisvq_gemm_batched_workspace_bytes(const unisvq_gemv_problem* problems, int count, int64_t M, int x_dtype);
 
 /* Several independent products y_i = x_i * W_hat_i^T of the same M and
- * dtypes, with the results of unisvq_gemm on each (a decoder's query, key and
- * value projections, or its gate and up projections, at a small batch).  For
- * M <= 32 all of them run in ONE launch of the small-batch kernel (bf16
- * activations first pass through the per-problem pre-pass into their
- * workspace slice); above that each problem takes the tiled product.
+ * dtypes (a decoder's query, key and value projections, or its gate and up
+ * projections, at a small batch).  For M <= 32 all of them run in ONE launch
+ * of the small-batch kernel, with the results of unisvq_gemm on each bit for
+ * bit; above that in ONE launch of the tiled product, planned over the whole
+ * batch, plus one reduction launch when the batch's tiles leave CUs idle and
+ * K is split -- the same arithmetic as unisvq_gemm, but the K split (and so
+ * the grouping of the fp32 partial sums) follows the batch, so results can
+ * differ from single calls in the last bits (bf16 activations first pass
+ * through the per-problem pre-pass into their workspace slice; activations
+ * above 2 GiB fall back to one product at a time, as single calls).
  *   problems   HOST array of `count` descriptors (1..UNISVQ_MAX_BATCH), read
  *              before the call returns; packed format v1 weights; every
  *              descriptor is validated before anything is enqueued

@@ -203,8 +203,9 @@ struct SkinnyProblem {
     int64_t N, K;
 };
 hipError_t launch_skinny_batch(const SkinnyProblem* probs, int count, int64_t M, int y_dtype, hipStream_t s);
-// unisvq_gemm over a batch of problems (same M and dtypes): one launch for
-// M <= kSkinnyMaxM (after the bf16 pre-passes), else one product per problem.
+// unisvq_gemm over a batch of problems (same M and dtypes): one launch of the
+// small-batch kernel for M <= kSkinnyMaxM, else one tiled launch (and one
+// reduction) for the batch, after the bf16 pre-passes.
 // Problem i uses the workspace bytes [off_i, off_i + gemm_workspace_bytes(i)),
 // off_i the 256-aligned sum of the earlier ones (gemm_batch_workspace_bytes).
 struct GemmBatchProblem {

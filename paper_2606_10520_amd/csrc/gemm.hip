@@ -38,6 +38,34 @@ constexpr int kBN = 16 * kNI;         // output rows per workgroup
 constexpr int kLdsRow = kGroup + 16;  // halves per decoded row in LDS (32-byte pad: no bank conflicts)
 constexpr int kWBuf = kBN * kLdsRow;  // halves per decoded-weight buffer
 
+// One product of a (possibly batched) tiled launch; the products of a batch
+// share M, the token tiling and the output dtype.
+struct TileProb {
+    const uint8_t* packed;
+    const uint8_t* affine;
+    const _Float16* x;
+    const float* inv_scale;  // per token, or null
+    const float* bias;       // per token (fold), or null
+    float* partial;          // [splits][M][N] fp32 when splits > 1, else null
+    void* y;
+    int affine_one, N, K, n_tiles, splits, gps, wg_begin;
+};
+
+struct TileBatch {
+    TileProb p[kMaxBatch];
+    int count, M, m_tiles, y_dtype;
+};
+
+// The K-split products of a batch: their partial sums and outputs.
+struct ReduceBatch {
+    const float* partial[kMaxBatch];
+    const float* inv_scale[kMaxBatch];
+    const float* bias[kMaxBatch];
+    void* y[kMaxBatch];
+    int N[kMaxBatch], splits[kMaxBatch], wg_begin[kMaxBatch];
+    int count, M, y_dtype;
+};
+
 // One 32-column step of the tile product: MI x kNI matrix-core tiles.
 template <int MI>
 __device__ inline void mma(const f16x8 (&xa)[MI], const f16x8 (&wb)[kNI], f32x4 (&acc)[MI][kNI]) {
@@ -171,14 +199,23 @@ __device__ inline void group_step_var(const GemmState<MI>& st, int g, const VarP
 // multiplied by A (fold pre-pass), so the weights are the bare codes, and
 // the per-token bias term sum_v x_v . B is added in the epilogue.
 template <int MI, bool SHARED, int BITS = 2, int D = 4, bool TX = false, bool FOLD = false>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restrict__ packed,
-                                                        const uint8_t* __restrict__ affine, int affine_one,
-                                                        const _Float16* __restrict__ x,
-                                                        const float* __restrict__ inv_scale, void* y, int N,
-                                                        int K, int M, int y_dtype, int m_tiles, int n_tiles,
-                                                        int splits, int gps, float* __restrict__ partial,
-                                                        const float* __restrict__ bias) {
+__global__ __launch_bounds__(kThreads) void gemm_kernel(const TileBatch tb) {
     __shared__ __attribute__((aligned(16))) _Float16 wsh[2 * kWBuf];
+    // problem of this workgroup (uniform scalar selection)
+    TileProb prob = tb.p[0];
+#pragma unroll
+    for (int i = 1; i < kMaxBatch; ++i)
+        if (i < tb.count && static_cast<int>(blockIdx.x) >= tb.p[i].wg_begin) prob = tb.p[i];
+    const uint8_t* packed = prob.packed;
+    const uint8_t* affine = prob.affine;
+    const _Float16* x = prob.x;
+    const float* inv_scale = prob.inv_scale;
+    const float* bias = prob.bias;
+    float* partial = prob.partial;
+    void* y = prob.y;
+    const int affine_one = prob.affine_one, N = prob.N, K = prob.K, n_tiles = prob.n_tiles, splits = prob.splits,
+              gps = prob.gps;
+    const int M = tb.M, y_dtype = tb.y_dtype, m_tiles = tb.m_tiles;
     static_assert(!FOLD || (SHARED && TX && BITS == 2 && D == 4), "the fold runs on the tiled shared-pair kernel");
     constexpr int BM = kWaves * 16 * MI;
     constexpr bool kVar = BITS != 2 || D != 4;
@@ -192,7 +229,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     // them so that each XCD gets a contiguous run of tiles makes the tiles
     // that share activation rows share that XCD's L2.
     const int T = m_tiles * n_tiles * splits;
-    int L = blockIdx.x;
+    int L = static_cast<int>(blockIdx.x) - prob.wg_begin;
     if ((T & 7) == 0) L = (L & 7) * (T >> 3) + (L >> 3);
     const int nt = L % n_tiles;
     const int mt = (L / n_tiles) % m_tiles;
@@ -358,28 +395,44 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
     }
 }
 
-// y = (sum over the K splits of the partial sums) * per-token scale, four
-// outputs per thread (N is a multiple of 16).
-__global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ partial, int splits, int M,
-                                                            int N, const float* __restrict__ inv_scale, void* y,
-                                                            int y_dtype, const float* __restrict__ bias) {
-    const int64_t total4 = static_cast<int64_t>(M) * N / 4;
-    const int64_t i4 = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+// y = (sum over the K splits of the partial sums, in split order) *
+// per-token scale (+ bias), four outputs per thread (N is a multiple of 16),
+// for every split product of a batch; the loads of eight splits are in
+// flight at once.
+constexpr int kReduceChunk = 8;
+
+__global__ __launch_bounds__(256) void reduce_splits_kernel(const ReduceBatch r) {
+    const int bid = blockIdx.x;
+    int pi = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxBatch; ++i)
+        if (i < r.count && bid >= r.wg_begin[i]) pi = i;
+    const int N = r.N[pi], splits = r.splits[pi];
+    const int64_t total4 = static_cast<int64_t>(r.M) * N / 4;
+    const int64_t i4 = static_cast<int64_t>(bid - r.wg_begin[pi]) * 256 + threadIdx.x;
     if (i4 >= total4) return;
-    const f32x4* p = reinterpret_cast<const f32x4*>(partial);
-    f32x4 s = p[i4];
-    for (int k = 1; k < splits; ++k) s += p[k * total4 + i4];
+    const f32x4* p = reinterpret_cast<const f32x4*>(r.partial[pi]) + i4;
+    f32x4 s = {0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < splits; k0 += kReduceChunk) {
+        f32x4 q[kReduceChunk];
+#pragma unroll
+        for (int k = 0; k < kReduceChunk; ++k) q[k] = k0 + k < splits ? p[(k0 + k) * total4] : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k = 0; k < kReduceChunk; ++k)
+            if (k0 + k < splits) s += q[k];
+    }
     const int64_t e0 = 4 * i4;
     const int t = static_cast<int>(e0 / N);
-    const float sc = inv_scale ? inv_scale[t] : 1.0f;
-    if (bias) {
-        const float bt = bias[t];
+    const float sc = r.inv_scale[pi] ? r.inv_scale[pi][t] : 1.0f;
+    void* y = r.y[pi];
+    if (r.bias[pi]) {
+        const float bt = r.bias[pi][t];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) store_out(y, e0 + c, s[c] * sc + bt, y_dtype);
+        for (int c = 0; c < 4; ++c) store_out(y, e0 + c, s[c] * sc + bt, r.y_dtype);
         return;
     }
 #pragma unroll
-    for (int c = 0; c < 4; ++c) store_out(y, e0 + c, s[c] * sc, y_dtype);
+    for (int c = 0; c < 4; ++c) store_out(y, e0 + c, s[c] * sc, r.y_dtype);
 }
 
 // bf16 activations -> fp16 with a power-of-two scale per token (see the top
@@ -666,23 +719,54 @@ size_t partial_bytes(int64_t N, int64_t K, int64_t M) {
     return p.splits > 1 ? static_cast<size_t>(p.splits) * M * N * 4 : 0;
 }
 
+// Launch a batch of products (one kernel, plus one reduction kernel for
+// those split along K).
+template <int MI, bool SHARED, int BITS = 2, int D = 4, bool TX = false, bool FOLD = false>
+hipError_t launch_tile_batch(TileBatch& b, hipStream_t s) {
+    ReduceBatch r{};
+    int blocks = 0, rblocks = 0, nred = 0;
+    for (int i = 0; i < b.count; ++i) {
+        TileProb& q = b.p[i];
+        if (q.splits > 1 && q.partial == nullptr) return hipErrorInvalidValue;  // never launch without the partials
+        if (q.splits <= 1) q.partial = nullptr;
+        q.wg_begin = blocks;
+        blocks += b.m_tiles * q.n_tiles * q.splits;
+        if (q.splits > 1) {
+            r.partial[nred] = q.partial;
+            r.inv_scale[nred] = q.inv_scale;
+            r.bias[nred] = q.bias;
+            r.y[nred] = q.y;
+            r.N[nred] = q.N;
+            r.splits[nred] = q.splits;
+            r.wg_begin[nred] = rblocks;
+            rblocks += static_cast<int>((static_cast<int64_t>(b.M) * q.N / 4 + 255) / 256);
+            ++nred;
+        }
+    }
+    hipLaunchKernelGGL((gemm_kernel<MI, SHARED, BITS, D, TX, FOLD>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(kThreads), 0, s, b);
+    if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
+    if (nred > 0) {
+        r.count = nred;
+        r.M = b.M;
+        r.y_dtype = b.y_dtype;
+        hipLaunchKernelGGL(reduce_splits_kernel, dim3(static_cast<unsigned>(rblocks)), dim3(256), 0, s, r);
+    }
+    return hipGetLastError();
+}
+
 template <int MI, bool SHARED, int BITS = 2, int D = 4, bool TX = false, bool FOLD = false>
 hipError_t launch_tiles(const GemmPlan& p, int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine,
                         int affine_one, int64_t M, const _Float16* x, const float* inv_scale, void* y,
                         int y_dtype, float* partial, hipStream_t s, const float* bias = nullptr) {
-    if (p.splits > 1 && partial == nullptr) return hipErrorInvalidValue;  // never launch without the partials
-    const unsigned blocks = static_cast<unsigned>(p.m_tiles) * p.n_tiles * p.splits;
-    hipLaunchKernelGGL((gemm_kernel<MI, SHARED, BITS, D, TX, FOLD>), dim3(blocks), dim3(kThreads), 0, s, packed, affine, affine_one,
-                       x, inv_scale, y,
-                       static_cast<int>(N), static_cast<int>(K), static_cast<int>(M), y_dtype, p.m_tiles,
-                       p.n_tiles, p.splits, p.gps, p.splits > 1 ? partial : nullptr, bias);
-    if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
-    if (p.splits > 1) {
-        const int64_t total4 = M * N / 4;
-        hipLaunchKernelGGL(reduce_splits_kernel, dim3(static_cast<unsigned>((total4 + 255) / 256)), dim3(256), 0, s,
-                           partial, p.splits, static_cast<int>(M), static_cast<int>(N), inv_scale, y, y_dtype, bias);
-    }
-    return hipGetLastError();
+    TileBatch b{};
+    b.p[0] = TileProb{packed, affine, x, inv_scale, bias, partial, y, affine_one, static_cast<int>(N),
+                      static_cast<int>(K), p.n_tiles, p.splits, p.gps, 0};
+    b.count = 1;
+    b.M = static_cast<int>(M);
+    b.m_tiles = p.m_tiles;
+    b.y_dtype = y_dtype;
+    return launch_tile_batch<MI, SHARED, BITS, D, TX, FOLD>(b, s);
 }
 
 }  // namespace
@@ -805,7 +889,10 @@ size_t gemm_batch_workspace_bytes(const GemmBatchProblem* probs, int count, int6
 int launch_gemm_batch(const GemmBatchProblem* probs, int count, int64_t M, int x_dtype, int y_dtype, void* workspace,
                       hipStream_t s) {
     uint8_t* ws = static_cast<uint8_t*>(workspace);
-    if (M > kSkinnyMaxM) {
+    bool sliced = false;
+    for (int i = 0; i < count; ++i) sliced = sliced || M > kMaxBufferBytes / (2 * probs[i].K) / 256 * 256;
+    if (M > kSkinnyMaxM && sliced) {
+        // activations above 2 GiB: one product at a time, in token slices
         for (int i = 0; i < count; ++i) {
             const GemmBatchProblem& q = probs[i];
             const int st = gemm_common(q.N, q.K, q.packed, nullptr, 0, M, q.x, x_dtype, q.y, y_dtype, ws, s);
@@ -813,6 +900,58 @@ int launch_gemm_batch(const GemmBatchProblem* probs, int count, int64_t M, int x
             ws += align256(gemm_workspace_bytes(q.N, q.K, M, x_dtype));
         }
         return UNISVQ_OK;
+    }
+    if (M > kSkinnyMaxM) {
+        // one tiled launch (and one reduction) for the whole batch: the bf16
+        // pre-pass of each problem into its slice, then the tiles planned
+        // over the batch (a K split only as far as the batch's tiles leave
+        // CUs idle; never more splits than the problem alone would take, so
+        // the partials fit its slice)
+        const GemmPlan p0 = plan_gemm(probs[0].N, probs[0].K, M);
+        TileBatch b{};
+        b.count = count;
+        b.M = static_cast<int>(M);
+        b.m_tiles = p0.m_tiles;
+        b.y_dtype = y_dtype;
+        int64_t tiles = 0;
+        for (int i = 0; i < count; ++i) tiles += static_cast<int64_t>(p0.m_tiles) * ((probs[i].N + kBN - 1) / kBN);
+        for (int i = 0; i < count; ++i) {
+            const GemmBatchProblem& q = probs[i];
+            uint8_t* slice = ws;
+            ws += align256(gemm_workspace_bytes(q.N, q.K, M, x_dtype));
+            const _Float16* xh = static_cast<const _Float16*>(q.x);
+            const float* inv = nullptr;
+            if (x_dtype == UNISVQ_BF16) {
+                _Float16* wxh = reinterpret_cast<_Float16*>(slice);
+                slice += align256(static_cast<size_t>((M + 15) / 16 * 16) * q.K * 2);
+                float* winv = reinterpret_cast<float*>(slice);
+                slice += align256(static_cast<size_t>(M) * 4);
+                if (launch_scale<true>(q.K, M, static_cast<const uint16_t*>(q.x), wxh, winv, s) != hipSuccess)
+                    return q.K > 65536 ? UNISVQ_EUNSUP : UNISVQ_EHIP;
+                xh = wxh;
+                inv = winv;
+            }
+            const int groups = static_cast<int>(q.K / kGroup);
+            const int packets = (groups + 1) / 2;
+            int splits = 1, gps = groups;
+            if (tiles < 256 && groups >= 4) {
+                const int fill = static_cast<int>((256 + tiles - 1) / tiles);
+                const int want = fill > (packets + 3) / 4 ? fill : (packets + 3) / 4;
+                const int sp = want < packets ? want : packets;
+                gps = 2 * ((packets + sp - 1) / sp);
+                splits = (groups + gps - 1) / gps;
+            }
+            b.p[i] = TileProb{q.packed, nullptr, xh, inv, nullptr, reinterpret_cast<float*>(slice), q.y, 0,
+                              static_cast<int>(q.N), static_cast<int>(q.K),
+                              static_cast<int>((q.N + kBN - 1) / kBN), splits, gps, 0};
+        }
+        const bool tx = x_dtype == UNISVQ_BF16;
+        hipError_t e;
+        if (p0.mi == 2)
+            e = tx ? launch_tile_batch<2, false, 2, 4, true>(b, s) : launch_tile_batch<2, false>(b, s);
+        else
+            e = tx ? launch_tile_batch<1, false, 2, 4, true>(b, s) : launch_tile_batch<1, false>(b, s);
+        return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
     }
     SkinnyProblem sp[kMaxBatch];
     for (int i = 0; i < count; ++i) {

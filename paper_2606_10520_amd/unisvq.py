@@ -412,7 +412,8 @@ def gemm_noalloc(packed, N: int, K: int, x, out=None, out_dtype=None, stream=Non
 
 def gemm_batched(problems, out_dtype=None, workspace=None, stream=None):
     """Several independent products (same M and dtypes), each as unisvq_gemm:
-    one launch for M <= 32.  problems: sequence of (packed, N, K, x, out-or-None).
+    one launch (plus one reduction launch above 32 tokens when K is split).
+    problems: sequence of (packed, N, K, x, out-or-None).
     Returns the list of outputs."""
     if not 1 <= len(problems) <= MAX_BATCH:
         raise ValueError(f"1..{MAX_BATCH} problems per call")

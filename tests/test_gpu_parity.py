@@ -618,13 +618,15 @@ def test_read_bytes_folds_every_word():
 
 # ------------------------------------------- batched small-batch products
 
-@pytest.mark.parametrize("M", [5, 16, 17, 32, 33, 40])
+@pytest.mark.parametrize("M", [5, 16, 17, 32, 33, 40, 64, 100])
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
 def test_gemm_batched_matches_single_calls(M, dtype):
     """q/k/v-style and gate/up-style batches (different N and K in one
-    launch, an odd group count): each output equals unisvq_gemm on that
-    problem alone bit for bit (the same kernel, workgroup and summation order),
-    and the single calls match the oracle."""
+    launch, an odd group count), every output element against the oracle.
+    Up to 32 tokens each output equals unisvq_gemm on that problem alone bit
+    for bit (the same kernel, workgroup and summation order); above, the
+    batch plans its own K split, so the outputs equal single calls to within
+    the fp32 regrouping of the partial sums, and repeat bit for bit."""
     shapes = [(4096, 4096), (1024, 4096), (512, 11008), (64, 1152)]
     probs, refs = [], []
     for i, (N, K) in enumerate(shapes):
@@ -632,15 +634,20 @@ def test_gemm_batched_matches_single_calls(M, dtype):
         xb = wl.gen_activations(M, K, seed=95 + i, dtype=dtype, outliers=True)
         pk = upload_pack(Q, A, B)
         probs.append((pk, N, K, dev_x(xb, dtype), None))
-        rows = np.arange(0, N, max(1, N // 64))
-        refs.append((rows, oracle.matmul(oracle.pack(Q, A, B)[0], N, K, x_as_f64(xb, dtype), rows=rows)))
+        refs.append(oracle.matmul(oracle.pack(Q, A, B)[0], N, K, x_as_f64(xb, dtype)))
     outs = u.gemm_batched(probs, out_dtype=torch.float32)
+    again = u.gemm_batched(probs, out_dtype=torch.float32)
     torch.cuda.synchronize()
-    for (pk, N, K, x, _), y, (rows, ref) in zip(probs, outs, refs):
+    for (pk, N, K, x, _), y, y2, ref in zip(probs, outs, again, refs):
         single = u.gemm(pk, N, K, x, out_dtype=torch.float32)
         torch.cuda.synchronize()
-        assert torch.equal(y, single), (N, K)
-        assert rel_err(single.cpu().numpy()[:, rows], ref) <= 5e-4
+        assert torch.equal(y, y2), (N, K)
+        if M <= 32:
+            assert torch.equal(y, single), (N, K)
+        else:
+            assert rel_err(y.cpu().numpy(), single.cpu().numpy().astype(np.float64)) <= 1e-6, (N, K)
+        assert rel_err(y.cpu().numpy(), ref) <= 5e-4
+        assert rel_err(single.cpu().numpy(), ref) <= 5e-4
 
 
 def test_gemm_batched_fp16_outputs_and_reruns():
