@@ -80,7 +80,7 @@ def parse():
                    help="time this workload only (default: the 7B M = 1 headline plus a sub-record per "
                         "configured workload)")
     p.add_argument("--fold", action="store_true",
-                   help="with --affine matrix/group and a workload above 4 tokens: the Eq. 9 fold "
+                   help="with --affine matrix/group and a workload above 3 tokens: the Eq. 9 fold "
                         "(unisvq_gemm_shared_fold) instead of the decode path")
     p.add_argument("--affine", default="row_group", choices=["row_group", "matrix", "group"],
                    help="row_group: one (A, B) pair per (row, 128-column group), stored with the codes (the "
@@ -438,7 +438,7 @@ class Case:
         self.lib = u.load()
         self.tdt = torch.float16 if xdt == "f16" else torch.bfloat16
         self.xcode = u.F16 if xdt == "f16" else u.BF16
-        self.kernel = "gemv" if M <= 4 else "gemm"
+        self.kernel = "gemv" if M <= 3 else "gemm"
         dev = torch.device("cuda:0")
         layers = ws.layers
         self.x_host = [wl.gen_activations(M, L.K, seed=wl.activation_seed(li, M), dtype=xdt, outliers=outliers)
@@ -913,7 +913,7 @@ def main():
     if var and args.affine == "row_group":
         args.affine = "matrix"  # the variants keep their pairs shared by the rows
     shared = args.affine != "row_group"
-    if args.fold and (not shared or var or M <= 4):
+    if args.fold and (not shared or var or M <= 3):
         print("--fold needs row-shared pairs (--affine matrix or group), the 2x4 format and more than 4 tokens "
               "(the fold is a unisvq_gemm_shared_fold path)", file=sys.stderr)
         sys.exit(2)

@@ -217,7 +217,10 @@ size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype)
 
 /* Prefill product y = x * W_hat^T for any M >= 1 (Eq. 1 with Eq. 4/8).
  * Arguments as unisvq_gemv; x_dtype F16 or BF16, y_dtype F16, BF16 or F32.
- * Up to 32 tokens one launch of the small-batch kernel computes it: each
+ * Up to 3 tokens the matrix-vector kernel of unisvq_gemv computes it (its
+ * faster range; the workspace then goes unused), unless K is too long for
+ * that kernel's LDS.  Up to 32 tokens one launch of the small-batch kernel
+ * computes it: each
  * wavefront decodes 16-row x 128-column tiles into its own LDS region and
  * multiplies them with all tokens at once; the wavefronts of a workgroup
  * split K and add their sums in a fixed order (no workspace beyond the bf16
@@ -250,7 +253,8 @@ size_t unisvq_gemm_batched_workspace_bytes(const unisvq_gemv_problem* problems, 
 /* Several independent products y_i = x_i * W_hat_i^T of the same M and
  * dtypes (a decoder's query, key and value projections, or its gate and up
  * projections, at a small batch).  For M <= 32 all of them run in ONE launch
- * of the small-batch kernel, with the results of unisvq_gemm on each bit for
+ * (of the matrix-vector kernel up to 3 tokens, as unisvq_gemm does, else of
+ * the small-batch kernel), with the results of unisvq_gemm on each bit for
  * bit; above that in ONE launch of the tiled product, planned over the whole
  * batch, plus one reduction launch when the batch's tiles leave CUs idle and
  * K is split -- the same arithmetic as unisvq_gemm, but the K split (and so

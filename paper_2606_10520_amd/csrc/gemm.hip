@@ -805,6 +805,11 @@ int gemm_common(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affi
                 const void* x, int x_dtype, void* y, int y_dtype, void* workspace, hipStream_t s, int bits = 2,
                 int d = 4) {
     const bool var = bits != 2 || d != 4;
+    if (!var && M <= kGemvMaxM) {
+        GemvProblem g{packed, x, y, static_cast<int>(N), static_cast<int>(K), 0, affine, affine_one};
+        const int st = launch_gemv_batch(&g, 1, M, x_dtype, y_dtype, s);
+        if (st != UNISVQ_EUNSUP) return st;  // else K too long for its LDS: the small-batch kernel
+    }
     const _Float16* xh = static_cast<const _Float16*>(x);
     const float* inv = nullptr;
     uint8_t* ws = static_cast<uint8_t*>(workspace);
@@ -952,6 +957,14 @@ int launch_gemm_batch(const GemmBatchProblem* probs, int count, int64_t M, int x
         else
             e = tx ? launch_tile_batch<1, false, 2, 4, true>(b, s) : launch_tile_batch<1, false>(b, s);
         return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+    }
+    if (M <= kGemvMaxM) {
+        GemvProblem g[kMaxBatch];
+        for (int i = 0; i < count; ++i)
+            g[i] = GemvProblem{probs[i].packed, probs[i].x, probs[i].y, static_cast<int>(probs[i].N),
+                               static_cast<int>(probs[i].K), 0, nullptr, 0};
+        const int st = launch_gemv_batch(g, count, M, x_dtype, y_dtype, s);
+        if (st != UNISVQ_EUNSUP) return st;  // else K too long for its LDS: the small-batch kernel
     }
     SkinnyProblem sp[kMaxBatch];
     for (int i = 0; i < count; ++i) {
