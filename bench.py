@@ -914,7 +914,7 @@ def main():
         args.affine = "matrix"  # the variants keep their pairs shared by the rows
     shared = args.affine != "row_group"
     if args.fold and (not shared or var or M <= 3):
-        print("--fold needs row-shared pairs (--affine matrix or group), the 2x4 format and more than 4 tokens "
+        print("--fold needs row-shared pairs (--affine matrix or group), the 2x4 format and more than 3 tokens "
               "(the fold is a unisvq_gemm_shared_fold path)", file=sys.stderr)
         sys.exit(2)
     wname = headline if not shared else f"{headline}_{args.affine}_shared" + ("_fold" if args.fold else "")
