@@ -79,6 +79,46 @@ __device__ inline void load_packet_shared(__amdgpu_buffer_rsrc_t rc, __amdgpu_bu
     }
 }
 
+// load_packet without branches: both shapes issue the same three loads, so
+// the compiler's wait counts for the code that follows stay exact.  A half
+// packet's 8-byte slots are read 16 bytes at a time and the upper halves
+// dropped; its 2-byte B values come from the aligned word that holds them.
+// (The tiled GEMM keeps the branching form: this one costs it registers.)
+template <bool STREAM = false>
+__device__ inline void load_packet_flat(__amdgpu_buffer_rsrc_t rw, uint32_t rowblk, int p, int gend, int lane,
+                                   Piece& pc) {
+    const bool full = 2 * p + 1 < gend;
+    const bool half = 2 * p + 1 == gend;
+    const uint32_t P = full || half ? rowblk + static_cast<uint32_t>(p) * kPacketBytes : kOutOfRange;
+    const uint32_t slot = (half ? 8u : 16u) * static_cast<uint32_t>(lane);
+    const uint32_t aoff = P + (half ? kHalfAffineOff : kPacketAffineOff) + slot;
+    const uint32_t boff = P + (half ? kHalfBiasOff + 4 * (lane >> 1) : kPacketBiasOff + 4 * lane);
+    const uint4 c = STREAM ? ld128_stream(rw, P + slot) : ld128(rw, P + slot);
+    const uint4 a = STREAM ? ld128_stream(rw, aoff) : ld128(rw, aoff);
+    const uint32_t b = STREAM ? ld32_stream(rw, boff) : ld32(rw, boff);
+    pc.c = half ? uint4{c.x, c.y, 0u, 0u} : c;
+    pc.a = half ? uint4{a.x, a.y, 0u, 0u} : a;
+    pc.b = half ? (lane & 1 ? b >> 16 : b & 0xffffu) : b;
+}
+
+// load_packet_shared without branches (same three loads for both shapes).
+template <bool STREAM = false>
+__device__ inline void load_packet_shared_flat(__amdgpu_buffer_rsrc_t rc, __amdgpu_buffer_rsrc_t ra, uint32_t rowblk,
+                                          int p, int gend, int affine_one, int lane, Piece& pc) {
+    const bool full = 2 * p + 1 < gend;
+    const bool half = 2 * p + 1 == gend;
+    const uint32_t P = full || half ? rowblk + static_cast<uint32_t>(p) * kCodePacketBytes : kOutOfRange;
+    const uint32_t R = full || half ? static_cast<uint32_t>(affine_one ? 0 : p) * kAffineRecordBytes : kOutOfRange;
+    const int j = lane & 3;
+    const uint32_t slot = (half ? 8u : 16u) * static_cast<uint32_t>(lane);
+    const uint4 c = STREAM ? ld128_stream(rc, P + slot) : ld128(rc, P + slot);
+    const uint4 a = ld128(ra, R + 16 * j);
+    const uint32_t b = ld32(ra, R + kRecordBiasOff + 4 * j);
+    pc.c = half ? uint4{c.x, c.y, 0u, 0u} : c;
+    pc.a = half ? uint4{a.x, a.y, 0u, 0u} : a;
+    pc.b = half ? b & 0xffffu : b;
+}
+
 // Value of lane b of this lane's quad.
 template <int B>
 __device__ inline uint32_t quad_lane(uint32_t v) {

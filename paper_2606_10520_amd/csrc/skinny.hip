@@ -7,11 +7,16 @@
 // 128-column groups each) round robin -- wavefront w takes packets w, w + 16,
 // ... -- so a 4096-column row is a single round: every wavefront requests all
 // it needs at once and no wavefront waits for another until they meet in LDS
-// at the end.  Per packet a wavefront loads the activation operands of the
-// two groups first (tokens in tiles of 16, fp16; reused from registers by the
-// RB row blocks), then the RB packets, each a coalesced 16-byte-per-lane read
-// of the packet slots, and computes row block by row block as the packets
-// arrive.  Per row block and group it decodes the 16 x 128 weight tile on the
+// at the end.  Per packet a wavefront loads the activations of the two groups
+// first (tokens in tiles of 16, fp16; reused from registers by the RB row
+// blocks), then the RB packets, each a coalesced 16-byte-per-lane read of the
+// packet slots, and computes row block by row block as the packets arrive.
+// With one token tile the activations travel through LDS: each load
+// instruction reads four whole token rows of a group (256 contiguous bytes
+// each) straight into the wavefront's LDS area, laid out so that the
+// operand reads that follow are free of bank conflicts.  Loading the operand
+// layout directly from memory would touch sixteen token rows, 64 bytes each,
+// per instruction, and every workgroup reads all of the activations.  Per row block and group it decodes the 16 x 128 weight tile on the
 // matrix cores (A q + B exactly in fp32 from the integer codes, Eq. 4; one
 // rounding to fp16) into its own LDS tile, reads it back as the B operand and
 // multiplies it with the activations on v_mfma_f32_16x16x32_f16.  One kernel,
@@ -30,6 +35,17 @@ namespace {
 constexpr int kWavesS = 16;         // wavefronts per workgroup
 constexpr int kTRow = kGroup + 16;  // halves per decoded row of a wavefront tile (32-byte pad)
 constexpr int kTile = 16 * kTRow;
+// Staged activations of one group (16 tokens x 128 columns, fp16): four
+// load instructions of four token rows each, 1 KB per instruction plus a
+// 64-byte pad.  Lane l of instruction q reads token 4q + r (r = l / 16),
+// 16-byte chunk k = (l % 16) ^ r of the group's row, and the load puts it at
+// q * kXInst + 16 l.  The operand read of lane L (token t = L % 16, chunk
+// 4c + L / 16) then finds it at kXInst (t / 4) + 256 (t % 4) + 16 ((L / 16) ^
+// (t % 4)) + 64 c: sixteen lanes of one read hit sixteen distinct 16-byte
+// bank groups.
+constexpr int kXInst = 1024 + 64;
+constexpr int kXStage = 4 * kXInst;
+static_assert(kXStage <= kTile * 2, "a group's activations fit in a decode tile");
 
 struct SkProblem {
     const uint8_t* packed;   // full format, or codes only when `affine` is set
@@ -71,9 +87,17 @@ __device__ inline void tile_product(const Piece& pc, int jj, int j, _Float16* wr
         for (int i = 0; i < MT; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa[i][c], wb[c], acc[i], 0, 0, 0);
 }
 
+// Per wavefront: its decode tile, and with one token tile an activation
+// area (group 2p; group 2p + 1 is staged in the tile, which is free until
+// the first decode of the packet).
+template <int MT>
+constexpr int skinny_area_bytes() {
+    return kTile * 2 + (MT == 1 ? kXStage : 0);
+}
+
 template <int MT, int RB>
 constexpr int skinny_lds_bytes() {
-    constexpr int tiles = kWavesS * kTile * 2;
+    constexpr int tiles = kWavesS * skinny_area_bytes<MT>();
     constexpr int red = kWavesS * RB * 16 * MT * 16 * 4;
     return tiles > red ? tiles : red;
 }
@@ -83,7 +107,8 @@ constexpr int skinny_lds_bytes() {
 template <int MT, int RB, bool SHARED>
 __global__ __launch_bounds__(kWavesS * 64, (RB * MT <= 1 ? 8 : 4)) void skinny_kernel(const SkBatch batch) {
     __shared__ __attribute__((aligned(16))) unsigned char lds[skinny_lds_bytes<MT, RB>()];
-    _Float16* wtile = reinterpret_cast<_Float16*>(lds);
+    constexpr bool kStage = MT == 1;  // activations through LDS
+    constexpr int kArea = skinny_area_bytes<MT>();
 
     // problem and row tile of this workgroup (uniform scalar selection)
     const int bid = blockIdx.x;
@@ -110,6 +135,15 @@ __global__ __launch_bounds__(kWavesS * 64, (RB * MT <= 1 ? 8 : 4)) void skinny_k
     // activation operand of this lane: token lane % 16 + 16 i, columns
     // 8 (lane / 16) + 32 c of a group
     const uint32_t xlane = (static_cast<uint32_t>(lane & 15) * K + 8 * (lane >> 4)) * 2u;
+    // staged: the lane's load offset (token lane / 16 of each instruction,
+    // swizzled chunk) and its operand read offset within a staging area
+    const int xr = lane >> 4, xt = lane & 15;
+    const uint32_t xload = static_cast<uint32_t>(xr) * K * 2u + 16u * static_cast<uint32_t>((lane & 15) ^ xr);
+    const int xread = kXInst * (xt >> 2) + 256 * (xt & 3) + 16 * ((lane >> 4) ^ (xt & 3));
+    // the wavefront's LDS area (a wave-uniform address: the loads' LDS base)
+    const int wu = __builtin_amdgcn_readfirstlane(wave);
+    unsigned char* const uarea = lds + wu * kArea;
+    unsigned char* const warea = lds + wave * kArea;
 
     auto load_x = [&](int g, f16x8 (&xa)[MT][4]) {
         const uint32_t base = g < groups ? xlane + static_cast<uint32_t>(g) * 256u : kOutOfRange;
@@ -119,19 +153,37 @@ __global__ __launch_bounds__(kWavesS * 64, (RB * MT <= 1 ? 8 : 4)) void skinny_k
             for (int c = 0; c < 4; ++c)
                 xa[i][c] = __builtin_bit_cast(f16x8, ld128(rx, base + static_cast<uint32_t>(i) * (16u * K * 2u) + 64u * c));
     };
+    // group g's activations into the staging area at byte `at` of the
+    // wavefront's area (past the last group or token: zeros).  Token
+    // quads at or past M are not loaded: their rows hold stale values, which
+    // reach only the discarded outputs of those tokens.
+    auto stage_x = [&](int g, int at) {
+        const uint32_t base = g < groups ? xload + static_cast<uint32_t>(g) * 256u : kOutOfRange;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (4 * q < M)  // uniform
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rx, (__attribute__((address_space(3))) void*)(uarea + at + q * kXInst), 16,
+                    base + static_cast<uint32_t>(q) * (4u * K * 2u), 0, 0, 0);
+    };
+    auto read_x = [&](int at, f16x8 (&xa)[MT][4]) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) xa[0][c] = *reinterpret_cast<const f16x8*>(warea + at + xread + 64 * c);
+    };
     auto load = [&](int p, int b, Piece& pc) {
         const int rb = rb0 + b;
         const uint32_t rowblk = static_cast<uint32_t>(rb) * groups * kBlockBytes;
         const int gend = rb < nrb ? groups : 0;
         if constexpr (SHARED)
-            load_packet_shared<true>(rw, ra, rowblk, p, gend, pb.affine_one, lane, pc);
+            load_packet_shared_flat<true>(rw, ra, rowblk, p, gend, pb.affine_one, lane, pc);
         else
-            load_packet<true>(rw, rowblk, p, gend, lane, pc);
+            load_packet_flat<true>(rw, rowblk, p, gend, lane, pc);
     };
 
     const int j = lane & 3;
-    _Float16* wrow = wtile + wave * kTile + (lane >> 2) * kTRow;
-    const _Float16* wlane = wtile + wave * kTile + (lane & 15) * kTRow + 8 * (lane >> 4);
+    _Float16* const wtile = reinterpret_cast<_Float16*>(warea);
+    _Float16* wrow = wtile + (lane >> 2) * kTRow;
+    const _Float16* wlane = wtile + (lane & 15) * kTRow + 8 * (lane >> 4);
     f32x4 acc[RB][MT];
 #pragma unroll
     for (int b = 0; b < RB; ++b)
@@ -149,11 +201,28 @@ __global__ __launch_bounds__(kWavesS * 64, (RB * MT <= 1 ? 8 : 4)) void skinny_k
     for (int p = wave; p < packets; p += kWavesS) {  // uniform
         Piece pc[kRing];
         f16x8 x0[MT][4], x1[MT][4];
-        load_x(2 * p, x0);
-        load(p, 0, pc[0]);
-        load_x(2 * p + 1, x1);
+        if constexpr (kStage) {
+            // Every read of the previous packet's tile is complete (its
+            // products consumed the values), so the tile may be loaded into.
+            // The compiler does not order these LDS-bound loads against the
+            // LDS reads below: the piece loads stay behind them (memory
+            // clobbers) and an explicit count waits for them -- the loads
+            // retire in order and exactly 3 per piece follow.
+            stage_x(2 * p, kTile * 2);
+            stage_x(2 * p + 1, 0);
+            asm volatile("" ::: "memory");
 #pragma unroll
-        for (int b = 1; b < kRing; ++b) load(p, b, pc[b]);
+            for (int b = 0; b < kRing; ++b) load(p, b, pc[b]);
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * kRing) : "memory");
+            read_x(kTile * 2, x0);
+            read_x(0, x1);
+        } else {
+            load_x(2 * p, x0);
+            load(p, 0, pc[0]);
+            load_x(2 * p + 1, x1);
+#pragma unroll
+            for (int b = 1; b < kRing; ++b) load(p, b, pc[b]);
+        }
 #pragma unroll
         for (int b = 0; b < RB; ++b) {
             if (rb0 + b < nrb) {  // uniform
