@@ -98,7 +98,7 @@ constexpr int skinny_area_bytes() {
 template <int MT, int RB>
 constexpr int skinny_lds_bytes() {
     constexpr int tiles = kWavesS * skinny_area_bytes<MT>();
-    constexpr int red = kWavesS * RB * 16 * MT * 16 * 4;
+    constexpr int red = kWavesS * RB * MT * 64 * 16;
     return tiles > red ? tiles : red;
 }
 
@@ -233,27 +233,33 @@ __global__ __launch_bounds__(kWavesS * 64, (RB * MT <= 1 ? 8 : 4)) void skinny_k
         }
     }
 
-    // The sixteen wavefronts meet in LDS (over the decode tiles).  D lane
-    // layout: row lane % 16, tokens 16 i + 4 (lane / 16) + e.
+    // The sixteen wavefronts meet in LDS (over the decode tiles and staging
+    // areas): each stores its accumulators as they are (lane order, 16
+    // bytes per lane), and one thread per (row block, token tile, lane) sums
+    // the sixteen in wavefront order.  D lane layout: row lane % 16, tokens
+    // 16 i + 4 (lane / 16) + e.
     __syncthreads();
-    float* red = reinterpret_cast<float*>(lds);  // [wave][row block][16 MT tokens][16 rows]
+    f32x4* red = reinterpret_cast<f32x4*>(lds);  // [wave][row block][token tile][lane]
 #pragma unroll
     for (int b = 0; b < RB; ++b)
 #pragma unroll
-        for (int i = 0; i < MT; ++i)
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                red[((wave * RB + b) * 16 * MT + 16 * i + 4 * (lane >> 4) + e) * 16 + (lane & 15)] = acc[b][i][e];
+        for (int i = 0; i < MT; ++i) red[((wave * RB + b) * MT + i) * 64 + lane] = acc[b][i];
     __syncthreads();
     constexpr int kRows = RB * kRowBlock;
-    for (int o = threadIdx.x; o < M * kRows; o += kWavesS * 64) {
-        const int t = o / kRows, rr = o % kRows, b = rr >> 4, r = rr & 15;
-        const int row = rtile * kRows + rr;
-        if (row >= N) continue;
-        float v = 0.f;
+    for (int q = threadIdx.x; q < RB * MT * 64; q += kWavesS * 64) {
+        f32x4 v = red[q];
 #pragma unroll
-        for (int w = 0; w < kWavesS; ++w) v += red[((w * RB + b) * 16 * MT + t) * 16 + r];
-        store_out(pb.y, static_cast<int64_t>(t) * N + row, pb.inv_scale ? v * pb.inv_scale[t] : v, batch.y_dtype);
+        for (int w = 1; w < kWavesS; ++w) v += red[w * RB * MT * 64 + q];
+        const int ln = q & 63, bi = q >> 6, b = bi / MT, i = bi % MT;
+        const int row = rtile * kRows + b * kRowBlock + (ln & 15);
+        if (row >= N) continue;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int t = 16 * i + 4 * (ln >> 4) + e;
+            if (t < M)
+                store_out(pb.y, static_cast<int64_t>(t) * N + row, pb.inv_scale ? v[e] * pb.inv_scale[t] : v[e],
+                          batch.y_dtype);
+        }
     }
 }
 
