@@ -1,6 +1,8 @@
-// Small-batch product y = x * W_hat^T for 4 < M <= 32 tokens on gfx950.
+// Small-batch product y = x * W_hat^T for up to 32 tokens on gfx950 (the
+// product routes 1 to 3 tokens to the matrix-vector kernel where its LDS
+// allows).
 //
-// A workgroup owns RB 16-row blocks (RB = 1, 2, 3, 4 or 6; 1 above 16
+// A workgroup owns RB 16-row blocks (RB = 1, 2, 3, 4, 6 or 7; 1 above 16
 // tokens) of one problem over all
 // of K; several independent problems may share a launch (a decoder's query,
 // key and value projections).  Its sixteen wavefronts split the packets (two
@@ -287,7 +289,7 @@ int pick_rb(const SkinnyProblem* probs, int count, int max_rb) {
         const int64_t w = (packets + kWavesS - 1) / kWavesS;
         ppw = w > ppw ? w : ppw;
     }
-    constexpr int kHeights[] = {6, 4, 3, 2, 1};
+    constexpr int kHeights[] = {7, 6, 4, 3, 2, 1};
     int best = 1;
     int64_t best_cost = -1;
     for (const int rb : kHeights) {
@@ -308,7 +310,7 @@ int pick_rb(const SkinnyProblem* probs, int count, int max_rb) {
 hipError_t launch_skinny_batch(const SkinnyProblem* probs, int count, int64_t M, int y_dtype, hipStream_t s) {
     if (count < 1 || count > kMaxBatch || M < 1 || M > kSkinnyMaxM) return hipErrorInvalidValue;
     // two token tiles: one row block per workgroup (registers)
-    const int rb = pick_rb(probs, count, M > 16 ? 1 : 6);
+    const int rb = pick_rb(probs, count, M > 16 ? 1 : 7);
     SkBatch b{};
     int blocks = 0;
     for (int i = 0; i < count; ++i) {
@@ -323,6 +325,7 @@ hipError_t launch_skinny_batch(const SkinnyProblem* probs, int count, int64_t M,
     const bool shared = probs[0].affine != nullptr;
     if (M > 16) return launch_rb<2, 1>(b, blocks, shared, s);
     switch (rb) {
+        case 7: return launch_rb<1, 7>(b, blocks, shared, s);
         case 6: return launch_rb<1, 6>(b, blocks, shared, s);
         case 4: return launch_rb<1, 4>(b, blocks, shared, s);
         case 3: return launch_rb<1, 3>(b, blocks, shared, s);

@@ -672,6 +672,7 @@ def test_gemm_batched_fp16_outputs_and_reruns():
 # two row blocks), three again for a mix with multi-packet wavefronts, two (4112 rows: 129
 # workgroups, the last one half full) and one (65 row blocks).
 SMALL_BATCH_SETS = {
+    "rb7": [(25600, 2176)],
     "rb6": [(11008, 4096), (11008, 2176)],
     "rb4": [(16384, 1152)],
     "rb3": [(8192, 2176), (1024, 2176), (1024, 2176)],
@@ -686,7 +687,8 @@ SMALL_BATCH_SETS = {
 @pytest.mark.parametrize("which", sorted(SMALL_BATCH_SETS))
 def test_gemm_batched_edges(which, M, dtype):
     """Small-batch workgroups at their edges: partial last workgroups
-    (2064 = 129 x 16 rows, 4112 = 257 x 16, 11008 = 688 x 16), K = 1152 (five
+    (2064 = 129 x 16 rows, 4112 = 257 x 16, 11008 = 688 x 16, 25600 = 1600 x
+    16: seven-row-block workgroups, the last with four), K = 1152 (five
     packets, the last a half packet: eleven wavefronts have none), K = 2176
     (nine packets), K = 4224 (seventeen: wavefront 0 takes two, the second a
     half packet), K = 11008 (43 packets: two or three per wavefront) and
