@@ -441,11 +441,23 @@ class Case:
         self.kernel = "gemv" if M <= 3 else "gemm"
         dev = torch.device("cuda:0")
         layers = ws.layers
+        # a decoder's query, key and value projections read one activation
+        # matrix (the normalised hidden state), and so do gate and up: those
+        # layers share the rows of the first of them, in one device buffer
+        names = [L.name for L in layers]
+        lead = list(range(len(layers)))
+        for grp in (("q", "k", "v"), ("gate", "up")):
+            if set(grp) <= set(names):
+                for n in grp[1:]:
+                    lead[names.index(n)] = names.index(grp[0])
         self.x_host = [wl.gen_activations(M, L.K, seed=wl.activation_seed(li, M), dtype=xdt, outliers=outliers)
-                       for li, L in enumerate(layers)]
+                       if lead[li] == li else None for li, L in enumerate(layers)]
+        self.x_host = [self.x_host[lead[li]] for li in range(len(layers))]
         self.xs, self.ys = [], []
         for c in range(ws.copies):
-            self.xs.append([torch.from_numpy(xb.view(np.int16)).view(self.tdt).to(dev) for xb in self.x_host])
+            xc = [torch.from_numpy(xb.view(np.int16)).view(self.tdt).to(dev) if lead[li] == li else None
+                  for li, xb in enumerate(self.x_host)]
+            self.xs.append([xc[lead[li]] for li in range(len(layers))])
             self.ys.append([torch.empty((M, L.N), dtype=torch.float16, device=dev) for L in layers])
         self.set_bytes = sum(algorithmic_bytes(L.N, L.K, M, affine=ws.affine, bits=ws.bits, d=ws.dim)
                              for L in layers)

@@ -46,16 +46,24 @@ constexpr int kTile = 16 * kTRow;
 // (t % 4)) + 64 c: sixteen lanes of one read hit sixteen distinct 16-byte
 // bank groups.
 constexpr int kXInst = 1024 + 64;
+// Workgroups of up to this many row blocks may run across two problems.
+constexpr int kSkinnySpanMax = 3;
 constexpr int kXStage = 4 * kXInst;
 static_assert(kXStage <= kTile * 2, "a group's activations fit in a decode tile");
 
+// Row blocks of a batch are numbered globally: problem i's start at
+// rb_begin; workgroup w owns global row blocks w RB .. w RB + RB - 1.  When
+// the problems share their activations (and K), the numbering is packed and a
+// workgroup may run on into the next problem (at most one more: every problem
+// then has at least RB row blocks); otherwise each problem starts on a
+// multiple of RB and the row blocks in between exist in no problem.
 struct SkProblem {
     const uint8_t* packed;   // full format, or codes only when `affine` is set
     const uint8_t* affine;   // shared affine block (codes-only format), else null
     const _Float16* x;       // [M][K] fp16 (bf16 activations arrive as their scaled fp16 copy)
     const float* inv_scale;  // per token (scaled bf16 copies), else null
     void* y;                 // [M][N]
-    int N, K, wg_begin, affine_one;
+    int N, K, rb_begin, affine_one;
 };
 
 struct SkBatch {
@@ -112,26 +120,45 @@ __global__ __launch_bounds__(kWavesS * 64, (RB * MT <= 1 ? 8 : 4)) void skinny_k
     constexpr bool kStage = MT == 1;  // activations through LDS
     constexpr int kArea = skinny_area_bytes<MT>();
 
-    // problem and row tile of this workgroup (uniform scalar selection)
+    // problems of this workgroup (uniform scalar selection): `pb` holds its
+    // first row block, `pn` the next problem; row blocks b >= bsplit are pn's
     const int bid = blockIdx.x;
-    SkProblem pb = batch.p[0];
+    const int g0 = bid * RB;
+    int ia = 0;
 #pragma unroll
     for (int i = 1; i < kMaxBatch; ++i)
-        if (i < batch.count && bid >= batch.p[i].wg_begin) pb = batch.p[i];
+        if (i < batch.count && g0 >= batch.p[i].rb_begin) ia = i;
+    SkProblem pb = batch.p[0], pn = batch.p[0];
+#pragma unroll
+    for (int i = 1; i < kMaxBatch; ++i) {
+        if (i == ia) pb = batch.p[i];
+        if (i == ia + 1) pn = batch.p[i];
+    }
+    // (taller workgroups never span: their scalar registers would spill)
+    const int bsplit = kSkinnySpanMax >= RB && ia + 1 < batch.count ? min(max(pn.rb_begin - g0, 0), RB) : RB;
     const int M = batch.M;
-    const int N = pb.N, K = pb.K;
-    const int rtile = bid - pb.wg_begin;
+    const int K = pb.K;  // (pn, if reached, has the same K and activations)
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int groups = K >> 7;
     const int packets = (groups + 1) >> 1;
-    const int rb0 = rtile * RB;
-    const int nrb = N / kRowBlock;
+    const int rb0 = g0 - pb.rb_begin;  // pb's local row block of b = 0
+    const int rbn = g0 - pn.rb_begin;  // pn's local row block of b = 0 (used for b >= bsplit)
+    const int nrb = pb.N / kRowBlock, nrbn = pn.N / kRowBlock;
+    // row block b: its problem's local index, or -1 where no problem has it
+    auto local_rb = [&](int b) {
+        const int r = b < bsplit ? rb0 + b : rbn + b;
+        return r < (b < bsplit ? nrb : nrbn) ? r : -1;
+    };
 
     constexpr uint32_t kBlockBytes = SHARED ? kCodeGroupBlockBytes : kGroupBlockBytes;
+    auto affine_bytes = [&](const SkProblem& q) {
+        return SHARED ? static_cast<uint32_t>(q.affine_one ? 1 : (groups + 1) / 2) * kAffineRecordBytes : 0u;
+    };
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(pb.packed, static_cast<uint32_t>(nrb) * groups * kBlockBytes);
-    const __amdgpu_buffer_rsrc_t ra = make_rsrc(
-        pb.affine, SHARED ? static_cast<uint32_t>(pb.affine_one ? 1 : (groups + 1) / 2) * kAffineRecordBytes : 0u);
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(pb.affine, affine_bytes(pb));
+    const __amdgpu_buffer_rsrc_t rwn = make_rsrc(pn.packed, static_cast<uint32_t>(nrbn) * groups * kBlockBytes);
+    const __amdgpu_buffer_rsrc_t ran = make_rsrc(pn.affine, affine_bytes(pn));
     // tokens at or past M lie past the end of the buffer: they read zeros
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(pb.x, static_cast<uint32_t>(M) * K * 2u);
     // activation operand of this lane: token lane % 16 + 16 i, columns
@@ -173,13 +200,15 @@ __global__ __launch_bounds__(kWavesS * 64, (RB * MT <= 1 ? 8 : 4)) void skinny_k
         for (int c = 0; c < 4; ++c) xa[0][c] = *reinterpret_cast<const f16x8*>(warea + at + xread + 64 * c);
     };
     auto load = [&](int p, int b, Piece& pc) {
-        const int rb = rb0 + b;
-        const uint32_t rowblk = static_cast<uint32_t>(rb) * groups * kBlockBytes;
-        const int gend = rb < nrb ? groups : 0;
+        const int rb = local_rb(b);
+        const uint32_t rowblk = static_cast<uint32_t>(rb < 0 ? 0 : rb) * groups * kBlockBytes;
+        const int gend = rb >= 0 ? groups : 0;
+        const bool first = b < bsplit;
         if constexpr (SHARED)
-            load_packet_shared_flat<true>(rw, ra, rowblk, p, gend, pb.affine_one, lane, pc);
+            load_packet_shared_flat<true>(first ? rw : rwn, first ? ra : ran, rowblk, p, gend,
+                                          first ? pb.affine_one : pn.affine_one, lane, pc);
         else
-            load_packet_flat<true>(rw, rowblk, p, gend, lane, pc);
+            load_packet_flat<true>(first ? rw : rwn, rowblk, p, gend, lane, pc);
     };
 
     const int j = lane & 3;
@@ -227,7 +256,7 @@ __global__ __launch_bounds__(kWavesS * 64, (RB * MT <= 1 ? 8 : 4)) void skinny_k
         }
 #pragma unroll
         for (int b = 0; b < RB; ++b) {
-            if (rb0 + b < nrb) {  // uniform
+            if (local_rb(b) >= 0) {  // uniform
                 tile_product<MT>(pc[b % kRing], 0, j, wrow, wlane, x0, acc[b]);
                 tile_product<MT>(pc[b % kRing], 1, j, wrow, wlane, x1, acc[b]);
             }
@@ -247,19 +276,22 @@ __global__ __launch_bounds__(kWavesS * 64, (RB * MT <= 1 ? 8 : 4)) void skinny_k
 #pragma unroll
         for (int i = 0; i < MT; ++i) red[((wave * RB + b) * MT + i) * 64 + lane] = acc[b][i];
     __syncthreads();
-    constexpr int kRows = RB * kRowBlock;
     for (int q = threadIdx.x; q < RB * MT * 64; q += kWavesS * 64) {
         f32x4 v = red[q];
 #pragma unroll
         for (int w = 1; w < kWavesS; ++w) v += red[w * RB * MT * 64 + q];
         const int ln = q & 63, bi = q >> 6, b = bi / MT, i = bi % MT;
-        const int row = rtile * kRows + b * kRowBlock + (ln & 15);
-        if (row >= N) continue;
+        const int rb = local_rb(b);
+        if (rb < 0) continue;
+        const bool first = b < bsplit;
+        void* const y = first ? pb.y : pn.y;
+        const int N = first ? pb.N : pn.N;
+        const int row = rb * kRowBlock + (ln & 15);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int t = 16 * i + 4 * (ln >> 4) + e;
             if (t < M)
-                store_out(pb.y, static_cast<int64_t>(t) * N + row, pb.inv_scale ? v[e] * pb.inv_scale[t] : v[e],
+                store_out(y, static_cast<int64_t>(t) * N + row, pb.inv_scale ? v[e] * pb.inv_scale[t] : v[e],
                           batch.y_dtype);
         }
     }
@@ -277,12 +309,24 @@ hipError_t launch_rb(const SkBatch& b, int blocks, bool shared, hipStream_t s) {
     return shared ? launch_k<MT, RB, true>(b, blocks, s) : launch_k<MT, RB, false>(b, blocks, s);
 }
 
+// Workgroups of height rb for a batch (row blocks packed across problems when
+// `span` and rb allows it).
+int64_t skinny_wgs(const SkinnyProblem* probs, int count, int rb, bool span) {
+    span = span && rb <= kSkinnySpanMax;
+    int64_t wgs = 0, rbs = 0;
+    for (int i = 0; i < count; ++i) {
+        rbs += probs[i].N / kRowBlock;
+        wgs += (probs[i].N / kRowBlock + rb - 1) / rb;
+    }
+    return span ? (rbs + rb - 1) / rb : wgs;
+}
+
 // Row blocks per workgroup for a batch: the fewest rounds of workgroups
 // over the 256 CUs (one resident workgroup each) times the time of one, taken
 // as 3 + RB * (packets per wavefront) in units of one packet's work -- the
 // fixed part is the wait for the first loads and the final reduction.  Ties go
 // to the taller workgroup (activation operands reused more).
-int pick_rb(const SkinnyProblem* probs, int count, int max_rb) {
+int pick_rb(const SkinnyProblem* probs, int count, int max_rb, bool span) {
     int64_t ppw = 1;
     for (int i = 0; i < count; ++i) {
         const int64_t packets = (probs[i].K / kGroup + 1) / 2;
@@ -294,8 +338,7 @@ int pick_rb(const SkinnyProblem* probs, int count, int max_rb) {
     int64_t best_cost = -1;
     for (const int rb : kHeights) {
         if (rb > max_rb) continue;
-        int64_t wgs = 0;
-        for (int i = 0; i < count; ++i) wgs += (probs[i].N / kRowBlock + rb - 1) / rb;
+        const int64_t wgs = skinny_wgs(probs, count, rb, span);
         const int64_t cost = (wgs + 255) / 256 * (3 + rb * ppw);
         if (best_cost < 0 || cost < best_cost) {
             best = rb;
@@ -310,15 +353,24 @@ int pick_rb(const SkinnyProblem* probs, int count, int max_rb) {
 hipError_t launch_skinny_batch(const SkinnyProblem* probs, int count, int64_t M, int y_dtype, hipStream_t s) {
     if (count < 1 || count > kMaxBatch || M < 1 || M > kSkinnyMaxM) return hipErrorInvalidValue;
     // two token tiles: one row block per workgroup (registers)
-    const int rb = pick_rb(probs, count, M > 16 ? 1 : 7);
+    const int max_rb = M > 16 ? 1 : 7;
+    // workgroups may run across problems that share activations and K, when
+    // every problem has at least max_rb row blocks (so at most two meet)
+    bool span = count > 1;
+    for (int i = 0; i < count && span; ++i)
+        span = probs[i].x == probs[0].x && probs[i].inv_scale == probs[0].inv_scale && probs[i].K == probs[0].K &&
+               probs[i].N / kRowBlock >= max_rb;
+    const int rb = pick_rb(probs, count, max_rb, span);
     SkBatch b{};
-    int blocks = 0;
+    int64_t start = 0;
     for (int i = 0; i < count; ++i) {
         const SkinnyProblem& q = probs[i];
         b.p[i] = SkProblem{q.packed, q.affine, q.x, q.inv_scale, q.y, static_cast<int>(q.N), static_cast<int>(q.K),
-                           blocks, q.affine_one};
-        blocks += static_cast<int>((q.N / kRowBlock + rb - 1) / rb);
+                           static_cast<int>(start), q.affine_one};
+        const int64_t nrb = q.N / kRowBlock;
+        start += span && rb <= kSkinnySpanMax ? nrb : (nrb + rb - 1) / rb * rb;
     }
+    const int blocks = static_cast<int>((start + rb - 1) / rb);
     b.count = count;
     b.M = static_cast<int>(M);
     b.y_dtype = y_dtype;

@@ -650,6 +650,41 @@ def test_gemm_batched_matches_single_calls(M, dtype):
         assert rel_err(single.cpu().numpy(), ref) <= 5e-4
 
 
+SPAN_SETS = {
+    # 65, 129 and 65 row blocks: three-block workgroups, two of them across
+    # a problem boundary (row blocks 63-65 and 192-194)
+    "small": [(1040, 2176), (2064, 2176), (1040, 2176)],
+    # the 7B query/key/value launch: 768 row blocks in 256 workgroups
+    "qkv7b": [(4096, 4096)] * 3,
+}
+
+
+@pytest.mark.parametrize("M", [4, 5, 16])
+@pytest.mark.parametrize("which", sorted(SPAN_SETS))
+def test_gemm_batched_shared_activations(which, M):
+    """Problems of a batch reading one activation buffer (a decoder's q/k/v)
+    share workgroups across their boundaries: every output element against
+    the oracle, and equal bit for bit to each problem alone."""
+    shapes = SPAN_SETS[which]
+    K = shapes[0][1]
+    xb = wl.gen_activations(M, K, seed=131, dtype="f16", outliers=True)
+    x = dev_x(xb, "f16")
+    probs, refs = [], []
+    for i, (N, _) in enumerate(shapes):
+        Q, A, B = wl.gen_weights(N, K, seed=132 + i)
+        probs.append((upload_pack(Q, A, B), N, K, x, None))
+        refs.append(oracle.matmul(oracle.pack(Q, A, B)[0], N, K, x_as_f64(xb, "f16")))
+    outs = u.gemm_batched(probs, out_dtype=torch.float32)
+    outs16 = u.gemm_batched(probs, out_dtype=torch.float16)
+    torch.cuda.synchronize()
+    for (pk, N, _, _, _), y, y16, ref in zip(probs, outs, outs16, refs):
+        single = u.gemm(pk, N, K, x, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        assert torch.equal(y, single), N
+        assert torch.equal(y16, y.to(torch.float16))
+        assert rel_err(y.cpu().numpy(), ref) <= 5e-4
+
+
 def test_gemm_batched_fp16_outputs_and_reruns():
     M = 16
     probs = []
