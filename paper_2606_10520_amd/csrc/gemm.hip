@@ -971,13 +971,23 @@ int launch_gemm_batch(const GemmBatchProblem* probs, int count, int64_t M, int x
         const GemmBatchProblem& q = probs[i];
         sp[i] = SkinnyProblem{q.packed, nullptr, 0, static_cast<const _Float16*>(q.x), nullptr, q.y, q.N, q.K};
         if (x_dtype == UNISVQ_BF16) {
-            // the problem's own scaled fp16 copy (row-major at this size)
-            _Float16* wxh = reinterpret_cast<_Float16*>(ws);
-            float* winv = reinterpret_cast<float*>(ws + align256(static_cast<size_t>(M) * q.K * 2));
-            if (launch_scale<false>(q.K, M, static_cast<const uint16_t*>(q.x), wxh, winv, s) != hipSuccess)
-                return q.K > 65536 ? UNISVQ_EUNSUP : UNISVQ_EHIP;
-            sp[i].x = wxh;
-            sp[i].inv_scale = winv;
+            // the problem's own scaled fp16 copy (row-major at this size), or
+            // that of an earlier problem with the same activations (one copy
+            // keeps them shared, so that workgroups may span the problems)
+            int same = -1;
+            for (int j = 0; j < i && same < 0; ++j)
+                if (probs[j].x == q.x && probs[j].K == q.K) same = j;
+            if (same >= 0) {
+                sp[i].x = sp[same].x;
+                sp[i].inv_scale = sp[same].inv_scale;
+            } else {
+                _Float16* wxh = reinterpret_cast<_Float16*>(ws);
+                float* winv = reinterpret_cast<float*>(ws + align256(static_cast<size_t>(M) * q.K * 2));
+                if (launch_scale<false>(q.K, M, static_cast<const uint16_t*>(q.x), wxh, winv, s) != hipSuccess)
+                    return q.K > 65536 ? UNISVQ_EUNSUP : UNISVQ_EHIP;
+                sp[i].x = wxh;
+                sp[i].inv_scale = winv;
+            }
         }
         ws += align256(gemm_workspace_bytes(q.N, q.K, M, x_dtype));
     }

@@ -660,20 +660,22 @@ SPAN_SETS = {
 
 
 @pytest.mark.parametrize("M", [4, 5, 16])
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
 @pytest.mark.parametrize("which", sorted(SPAN_SETS))
-def test_gemm_batched_shared_activations(which, M):
+def test_gemm_batched_shared_activations(which, dtype, M):
     """Problems of a batch reading one activation buffer (a decoder's q/k/v)
-    share workgroups across their boundaries: every output element against
-    the oracle, and equal bit for bit to each problem alone."""
+    share workgroups across their boundaries (bf16: one scaled copy for all):
+    every output element against the oracle, and equal bit for bit to each
+    problem alone."""
     shapes = SPAN_SETS[which]
     K = shapes[0][1]
-    xb = wl.gen_activations(M, K, seed=131, dtype="f16", outliers=True)
-    x = dev_x(xb, "f16")
+    xb = wl.gen_activations(M, K, seed=131, dtype=dtype, outliers=True)
+    x = dev_x(xb, dtype)
     probs, refs = [], []
     for i, (N, _) in enumerate(shapes):
         Q, A, B = wl.gen_weights(N, K, seed=132 + i)
         probs.append((upload_pack(Q, A, B), N, K, x, None))
-        refs.append(oracle.matmul(oracle.pack(Q, A, B)[0], N, K, x_as_f64(xb, "f16")))
+        refs.append(oracle.matmul(oracle.pack(Q, A, B)[0], N, K, x_as_f64(xb, dtype)))
     outs = u.gemm_batched(probs, out_dtype=torch.float32)
     outs16 = u.gemm_batched(probs, out_dtype=torch.float16)
     torch.cuda.synchronize()
