@@ -576,8 +576,9 @@ class Case:
 
     def run_step(self, calls, i, sptr, fn=None):
         fn = fn or self.launch
-        for _, lis in calls[i % self.ws.copies]:
-            st = fn(i % self.ws.copies, lis, sptr)
+        n = len(calls)  # one entry per buffer copy
+        for _, lis in calls[i % n]:
+            st = fn(i % n, lis, sptr)
             if st != 0:
                 raise RuntimeError(f"{self.kernel} launch failed with status {st}")
 
@@ -609,11 +610,29 @@ class Case:
 
     def per_launch_us(self, groups, reps):
         """Graph-timed duration of each launch of the schedule: `reps`
-        back-to-back launches of that launch alone (rotating over the copies)."""
+        back-to-back launches of that launch alone, rotating over enough
+        copies of its own weights (> 2x the 256 MB Infinity Cache; extra
+        copies are cloned for the measurement) that every launch streams them
+        from HBM, as in the step."""
+        ws, torch = self.ws, self.torch
+        idx = {n: i for i, n in enumerate(self.names)}
         out = {}
         for g in groups:
-            one = self.calls([g])
-            out["+".join(g)] = round(self.time_steps(one, reps, 2) * 1e3, 3)
+            lis = [idx[n] for n in g]
+            gbytes = sum(sum(t.numel() for t in ws.weight_buffers(0, li)) for li in lis)
+            need = max(ws.copies, -(-2 * MALL_BYTES // max(gbytes, 1)) + 1)
+            base = ws.copies
+            for c in range(base, need):
+                ws.packed.append([(tuple(t.clone() for t in pk) if isinstance(pk, tuple) else pk.clone())
+                                  if li in lis else pk for li, pk in enumerate(ws.packed[0])])
+                self.xs.append(self.xs[c % base])
+                self.ys.append(self.ys[c % base])
+            one = [[("+".join(g), lis)] for _ in range(need)]
+            try:
+                out["+".join(g)] = round(self.time_steps(one, max(reps, need), 2) * 1e3, 3)
+            finally:
+                del ws.packed[base:], self.xs[base:], self.ys[base:]
+                torch.cuda.synchronize()
         return out
 
 
