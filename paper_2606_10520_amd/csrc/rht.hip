@@ -20,6 +20,7 @@
 // each of those blocks of 2^k.  fp32 throughout, one rounding to the output
 // dtype.
 #include <cmath>
+#include <type_traits>
 
 #include "common.hpp"
 #include "fwht.hpp"
@@ -541,6 +542,133 @@ __global__ __launch_bounds__(kRhtThreads) void rht_paley_kernel(const XT* __rest
     }
 }
 
+// The Paley factor for 16-bit rows (fp16, bf16; blocks of 2^k >= 16): a
+// row's values times +-1 signs and the +-1 Paley entries are exact in the
+// row's own type, so the product runs on v_mfma_f32_16x16x32_{f16,bf16} with
+// fp32 sums.  Both operands sit transposed in LDS, k (the Paley index) fastest
+// and rows padded by 8 halves, so that each operand is one conflict-free
+// 16-byte read per lane: zt[c][im] = z[im][c] (the row, zero past m),
+// pt[jl][im] = P[im][jb0 + jl].  The workgroup's Paley columns are built while
+// the row is in flight; one wavefront per 16-column tile, the k range in
+// steps of 32.  The Sylvester factor and the store are as above.
+constexpr int kP16Pad = 8;
+
+__host__ __device__ inline int paley16_kp(const HadSpec& h) { return (h.m + 31) / 32 * 32; }
+__host__ __device__ inline int paley16_pitch(const HadSpec& h) { return paley16_kp(h) + kP16Pad; }
+__host__ __device__ inline size_t paley16_lds_bytes(const HadSpec& h, const PaleyPlan& pl) {
+    const size_t half = size_t{1} << h.k, pitch = static_cast<size_t>(paley16_pitch(h));
+    return half * pitch * 2 + 16 * pitch * 2 + static_cast<size_t>(pl.cnt) * half * 4 + static_cast<size_t>(h.q) * 5;
+}
+
+template <typename XT>
+__global__ __launch_bounds__(kRhtThreads) void rht_paley16_kernel(const XT* __restrict__ x,
+                                                                  const signed char* __restrict__ signs, int mode,
+                                                                  void* __restrict__ y, int y_dtype, int n, HadSpec h,
+                                                                  PaleyPlan pl, float norm) {
+    typedef XT xt8 __attribute__((ext_vector_type(8)));
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    const int half = 1 << h.k;
+    const int m = h.m;
+    const int kp = paley16_kp(h), pitch = paley16_pitch(h);
+    XT* zt = reinterpret_cast<XT*>(smem);                          // [half][pitch]
+    XT* pt = zt + half * pitch;                                     // [16][pitch]
+    float* w = reinterpret_cast<float*>(pt + 16 * pitch);          // [cnt][half]
+    int* dig = reinterpret_cast<int*>(w + pl.cnt * half);           // [q]
+    signed char* chi = reinterpret_cast<signed char*>(dig + h.q);   // [q]
+    const int64_t row = blockIdx.y;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int jb0 = blockIdx.x * pl.cnt;
+    const int cnt = min(m, jb0 + pl.cnt) - jb0;
+
+    // 1. the row's loads go out first, raw into registers
+    constexpr int C = kRhtMaxN / (8 * kRhtThreads);
+    RowChunk<XT> rc[C];
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + row * n, static_cast<uint32_t>(n) * sizeof(XT));
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(signs, static_cast<uint32_t>(n));
+#pragma unroll
+    for (int u = 0; u < C; ++u) fetch_chunk<XT>(rx, rs, 8 * (tid + u * kRhtThreads), rc[u]);
+    float so[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) so[u] = ld_sign(rs, jb0 * half + tid + u * kRhtThreads);
+    // 2. digit and character tables, then this workgroup's Paley columns
+    //    (pt rows past cnt and columns past m are zero)
+    for (int i = tid; i < h.q; i += kRhtThreads) {
+        chi[i] = i == 0 ? 0 : -1;
+        dig[i] = gf_packed(i, h.p, h.e);
+    }
+    __syncthreads();
+    for (int v = 1 + tid; v < h.q; v += kRhtThreads) chi[gf_square(v, h)] = 1;
+    __syncthreads();
+    for (int t = tid; t < 16 * kp; t += kRhtThreads) {
+        const int jl = t & 15, im = t >> 4;
+        const int j = jb0 + jl;
+        const int a = dig[min(max(im - 1, 0), h.q - 1)];
+        const int b = dig[min(max(j - 1, 0), h.q - 1)];
+        const float c = static_cast<float>(chi[gf_sub_index(a, b, h.p, h.e)]);
+        float v = im == j ? 1.f : (j == 0 ? -1.f : c);
+        v = im == 0 ? 1.f : v;
+        pt[jl * pitch + im] = static_cast<XT>((jl < cnt && im < m) ? v : 0.f);
+    }
+    // 3. the row, transposed (signs applied on the input side), and zero
+    //    Paley rows m .. kp - 1
+#pragma unroll
+    for (int u = 0; u < C; ++u) {
+        const int i0 = 8 * (tid + u * kRhtThreads);
+        const uint32_t wd[4] = {rc[u].a.x, rc[u].a.y, rc[u].a.z, rc[u].a.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int i = i0 + e;
+            if (i < n) {
+                float v = static_cast<float>(__builtin_bit_cast(XT, static_cast<uint16_t>(wd[e >> 1] >> (16 * (e & 1)))));
+                if (mode == 0) {
+                    const uint32_t sw = e < 4 ? rc[u].s.x : rc[u].s.y;
+                    v *= static_cast<float>(static_cast<signed char>((sw >> (8 * (e & 3))) & 0xffu));
+                }
+                zt[(i & (half - 1)) * pitch + (i >> h.k)] = static_cast<XT>(v);
+            }
+        }
+    }
+    for (int t = tid; t < (kp - m) * half; t += kRhtThreads) {
+        const int c = t % half, im = m + t / half;
+        zt[c * pitch + im] = static_cast<XT>(0.f);
+    }
+    __syncthreads();
+    // 4. the product: wavefront item nt = one 16-column tile; D lane: column
+    //    16 nt + lane % 16, blocks 4 (lane / 16) + e
+    const int ntiles = half >> 4;
+    for (int nt = wave; nt < ntiles; nt += kRhtThreads / 64) {
+        const XT* pa = pt + (lane & 15) * pitch + 8 * (lane >> 4);
+        const XT* pb = zt + (16 * nt + (lane & 15)) * pitch + 8 * (lane >> 4);
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int k0 = 0; k0 < kp; k0 += 32) {
+            const xt8 av = *reinterpret_cast<const xt8*>(pa + k0);
+            const xt8 bv = *reinterpret_cast<const xt8*>(pb + k0);
+            if constexpr (sizeof(XT) == 2 && std::is_same<XT, _Float16>::value)
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, bv, acc, 0, 0, 0);
+            else
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int jl = 4 * (lane >> 4) + e;
+            if (jl < cnt) w[jl * half + 16 * nt + (lane & 15)] = acc[e];
+        }
+    }
+    __syncthreads();
+    // 5. Sylvester factor inside each of this workgroup's blocks
+    sylvester_blocks(w, cnt * half, h.k, tid);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int o = tid + u * kRhtThreads;
+        if (o < cnt * half) {
+            const float v = w[o] * norm;
+            store_out(y, row * n + jb0 * half + o, mode == 1 ? v * so[u] : v, y_dtype);
+        }
+    }
+}
+
 bool is_prime(int v) {
     if (v < 2) return false;
     for (int d = 2; d * d <= v; ++d)
@@ -670,14 +798,16 @@ int launch_rht(int64_t n, int64_t M, const void* x, int x_dtype, const signed ch
     const size_t lds = rht_lds_bytes(h, static_cast<int>(n), per);
     if (lds > kRhtMaxLds) return UNISVQ_EUNSUP;
     // the dynamic-LDS limits, raised once per kernel and device
-    static std::atomic<uint64_t> attr_done[6];
-    const void* fns[6] = {reinterpret_cast<const void*>(&rht_kernel<_Float16>),
+    static std::atomic<uint64_t> attr_done[8];
+    const void* fns[8] = {reinterpret_cast<const void*>(&rht_kernel<_Float16>),
                           reinterpret_cast<const void*>(&rht_kernel<__bf16>),
                           reinterpret_cast<const void*>(&rht_kernel<float>),
                           reinterpret_cast<const void*>(&rht_paley_kernel<_Float16>),
                           reinterpret_cast<const void*>(&rht_paley_kernel<__bf16>),
-                          reinterpret_cast<const void*>(&rht_paley_kernel<float>)};
-    for (int i = 0; i < 6; ++i) {
+                          reinterpret_cast<const void*>(&rht_paley_kernel<float>),
+                          reinterpret_cast<const void*>(&rht_paley16_kernel<_Float16>),
+                          reinterpret_cast<const void*>(&rht_paley16_kernel<__bf16>)};
+    for (int i = 0; i < 8; ++i) {
         const int st = ensure_lds_limit(fns[i], static_cast<int>(kRhtMaxLds), attr_done[i]);
         if (st != UNISVQ_OK) return st;
     }
@@ -694,6 +824,23 @@ int launch_rht(int64_t n, int64_t M, const void* x, int x_dtype, const signed ch
             default: st = launch_fwht<4, 5>(x, x_dtype, signs, mode, y, y_dtype, norm, fgrid, s); break;
         }
         return st;
+    }
+    if (h.m > 1 && h.k >= 4 && (x_dtype == UNISVQ_F16 || x_dtype == UNISVQ_BF16)) {
+        // 16-bit rows: the Paley factor on the 16-bit matrix cores
+        const PaleyPlan pl = paley_plan(h);
+        const size_t plds = paley16_lds_bytes(h, pl);
+        if (plds <= kRhtMaxLds && pl.cnt << h.k <= 2 * kRhtThreads) {  // at most two outputs per thread
+            const dim3 pgrid(static_cast<unsigned>((h.m + pl.cnt - 1) / pl.cnt), static_cast<unsigned>(M));
+            if (x_dtype == UNISVQ_F16)
+                hipLaunchKernelGGL(rht_paley16_kernel<_Float16>, pgrid, dim3(kRhtThreads), plds, s,
+                                   static_cast<const _Float16*>(x), signs, mode, y, y_dtype, static_cast<int>(n), h,
+                                   pl, norm);
+            else
+                hipLaunchKernelGGL(rht_paley16_kernel<__bf16>, pgrid, dim3(kRhtThreads), plds, s,
+                                   static_cast<const __bf16*>(x), signs, mode, y, y_dtype, static_cast<int>(n), h,
+                                   pl, norm);
+            return hipGetLastError() == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+        }
     }
     if (h.m > 1) {
         // matrix-core Paley factor whenever its tables fit the LDS

@@ -557,6 +557,24 @@ def test_rht_matches_dense_oracle(n, mode):
     assert rel_err(y.cpu().numpy(), ref) <= 2e-6
 
 
+# 16-bit rows with a Paley factor and blocks of 2^k >= 16 take the 16-bit
+# matrix-core kernel: q = 11 (192, blocks of 16), q = 7^3 (5504, 11008,
+# 22016: blocks of 16 to 64), q = 3^3 (28672: blocks of 1024, one per
+# workgroup).
+@pytest.mark.parametrize("n", [192, 5504, 11008, 22016, 28672])
+@pytest.mark.parametrize("mode", ["in", "out"])
+@pytest.mark.parametrize("xdt", ["f16", "bf16"])
+def test_rht_16bit_rows_match_dense_oracle(n, mode, xdt):
+    M = 2
+    xb = wl.gen_activations(M, n, seed=n + 3, dtype=xdt)
+    s = np.random.default_rng(n + 5).choice(np.array([-1, 1], np.int8), n)
+    y = u.rht(dev_x(xb, xdt), torch.from_numpy(s).to(DEV), mode, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = oracle.rht(x_as_f64(xb, xdt), s, mode)
+    # the products with +-1 are exact in the 16-bit type; fp32 sums
+    assert rel_err(y.cpu().numpy(), ref) <= 2e-6
+
+
 @pytest.mark.parametrize("xdt,ydt", [("f16", torch.float16), ("bf16", torch.bfloat16), ("f16", torch.float32)])
 def test_rht_dtypes(xdt, ydt):
     n, M = 11008, 3
