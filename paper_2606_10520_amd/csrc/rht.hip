@@ -552,6 +552,14 @@ __global__ __launch_bounds__(kRhtThreads) void rht_paley_kernel(const XT* __rest
 // the row is in flight; one wavefront per 16-column tile, the k range in
 // steps of 32.  The Sylvester factor and the store are as above.
 constexpr int kP16Pad = 8;
+// The quadratic character of GF(q), bit i = 1 when element i is a nonzero
+// square, computed on the host for q <= kChiBitsMax (it rides in the kernel
+// arguments; the workgroups would otherwise each rebuild it).
+constexpr int kChiBitsMax = 2048;
+struct ChiBits {
+    uint64_t w[kChiBitsMax / 64];
+    int given;
+};
 
 __host__ __device__ inline int paley16_kp(const HadSpec& h) { return (h.m + 31) / 32 * 32; }
 __host__ __device__ inline int paley16_pitch(const HadSpec& h) { return paley16_kp(h) + kP16Pad; }
@@ -564,7 +572,7 @@ template <typename XT>
 __global__ __launch_bounds__(kRhtThreads) void rht_paley16_kernel(const XT* __restrict__ x,
                                                                   const signed char* __restrict__ signs, int mode,
                                                                   void* __restrict__ y, int y_dtype, int n, HadSpec h,
-                                                                  PaleyPlan pl, float norm) {
+                                                                  PaleyPlan pl, float norm, const ChiBits cb) {
     typedef XT xt8 __attribute__((ext_vector_type(8)));
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     const int half = 1 << h.k;
@@ -592,15 +600,29 @@ __global__ __launch_bounds__(kRhtThreads) void rht_paley16_kernel(const XT* __re
     float so[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) so[u] = ld_sign(rs, jb0 * half + tid + u * kRhtThreads);
-    // 2. digit and character tables, then this workgroup's Paley columns
-    //    (pt rows past cnt and columns past m are zero)
-    for (int i = tid; i < h.q; i += kRhtThreads) {
-        chi[i] = i == 0 ? 0 : -1;
-        dig[i] = gf_packed(i, h.p, h.e);
+    // 2. digit and character tables (the character from the arguments when
+    //    given: wavefront w reads word w of each 1024-element stretch), then
+    //    this workgroup's Paley columns (pt rows past cnt and columns past m
+    //    are zero)
+    if (cb.given) {
+        for (int i0 = 0; i0 < h.q; i0 += kRhtThreads) {
+            const uint64_t word = cb.w[__builtin_amdgcn_readfirstlane((i0 + tid) >> 6)];
+            const int i = i0 + tid;
+            if (i < h.q) {
+                chi[i] = i == 0 ? 0 : ((word >> (i & 63)) & 1u ? 1 : -1);
+                dig[i] = gf_packed(i, h.p, h.e);
+            }
+        }
+        __syncthreads();
+    } else {
+        for (int i = tid; i < h.q; i += kRhtThreads) {
+            chi[i] = i == 0 ? 0 : -1;
+            dig[i] = gf_packed(i, h.p, h.e);
+        }
+        __syncthreads();
+        for (int v = 1 + tid; v < h.q; v += kRhtThreads) chi[gf_square(v, h)] = 1;
+        __syncthreads();
     }
-    __syncthreads();
-    for (int v = 1 + tid; v < h.q; v += kRhtThreads) chi[gf_square(v, h)] = 1;
-    __syncthreads();
     for (int t = tid; t < 16 * kp; t += kRhtThreads) {
         const int jl = t & 15, im = t >> 4;
         const int j = jb0 + jl;
@@ -736,6 +758,28 @@ bool hadamard_spec(int64_t n, HadSpec* out) {
 
 constexpr size_t kRhtMaxLds = 160 * 1024;
 
+// Bit i set when field element i (digits base p, constant term first) is a
+// nonzero square of GF(p^e) modulo f: x^2 for every x != 0, the product's
+// degrees e .. 2e - 2 removed from the top with x^e = -(f[e-1] x^(e-1) + ...
+// + f[0]).  Host side of the character the transform kernels build from the
+// same definition (q <= kChiBitsMax).
+static void square_bits(const HadSpec& h, uint64_t* w) {
+    const int p = h.p, e = h.e;
+    for (int i = 0; i < kChiBitsMax / 64; ++i) w[i] = 0;
+    for (int x = 1; x < h.q; ++x) {
+        int a[3] = {0, 0, 0};
+        for (int i = 0, v = x; i < e; ++i, v /= p) a[i] = v % p;
+        int64_t c[5] = {0, 0, 0, 0, 0};
+        for (int i = 0; i < e; ++i)
+            for (int j = 0; j < e; ++j) c[i + j] += static_cast<int64_t>(a[i]) * a[j];
+        for (int d = 2 * e - 2; d >= e; --d)
+            for (int i = 0; i < e; ++i) c[d - e + i] -= c[d] * h.f[i];
+        int idx = 0;
+        for (int i = e - 1; i >= 0; --i) idx = idx * p + static_cast<int>(((c[i] % p) + p) % p);
+        w[idx >> 6] |= uint64_t{1} << (idx & 63);
+    }
+}
+
 size_t rht_lds_bytes(const HadSpec& h, int n, int per) {
     size_t b = static_cast<size_t>(n) * 4;
     if (h.m > 1)
@@ -831,14 +875,19 @@ int launch_rht(int64_t n, int64_t M, const void* x, int x_dtype, const signed ch
         const size_t plds = paley16_lds_bytes(h, pl);
         if (plds <= kRhtMaxLds && pl.cnt << h.k <= 2 * kRhtThreads) {  // at most two outputs per thread
             const dim3 pgrid(static_cast<unsigned>((h.m + pl.cnt - 1) / pl.cnt), static_cast<unsigned>(M));
+            ChiBits cb{};
+            if (h.q <= kChiBitsMax) {
+                square_bits(h, cb.w);
+                cb.given = 1;
+            }
             if (x_dtype == UNISVQ_F16)
                 hipLaunchKernelGGL(rht_paley16_kernel<_Float16>, pgrid, dim3(kRhtThreads), plds, s,
                                    static_cast<const _Float16*>(x), signs, mode, y, y_dtype, static_cast<int>(n), h,
-                                   pl, norm);
+                                   pl, norm, cb);
             else
                 hipLaunchKernelGGL(rht_paley16_kernel<__bf16>, pgrid, dim3(kRhtThreads), plds, s,
                                    static_cast<const __bf16*>(x), signs, mode, y, y_dtype, static_cast<int>(n), h,
-                                   pl, norm);
+                                   pl, norm, cb);
             return hipGetLastError() == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
         }
     }
