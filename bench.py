@@ -582,10 +582,11 @@ class Case:
             if st != 0:
                 raise RuntimeError(f"{self.kernel} launch failed with status {st}")
 
-    def time_steps(self, calls, nsteps, warmup, fn=None):
+    def time_steps(self, calls, nsteps, warmup, fn=None, replays=1):
         """Warm up eagerly, capture exactly `nsteps` steps (rotating over the
-        copies) in one HIP graph, replay it once untimed and once between two
-        events; returns ms per step."""
+        copies) in one HIP graph, replay it once untimed and then `replays`
+        times, each between two events; returns ms per step (the median over
+        the timed replays)."""
         torch = self.torch
         stream = torch.cuda.current_stream()
         for i in range(warmup):
@@ -599,14 +600,17 @@ class Case:
         torch.cuda.synchronize()
         graph.replay()
         torch.cuda.synchronize()
-        t0 = torch.cuda.Event(enable_timing=True)
-        t1 = torch.cuda.Event(enable_timing=True)
-        t0.record(stream)
-        graph.replay()
-        t1.record(stream)
-        torch.cuda.synchronize()
+        times = []
+        for _ in range(replays):
+            t0 = torch.cuda.Event(enable_timing=True)
+            t1 = torch.cuda.Event(enable_timing=True)
+            t0.record(stream)
+            graph.replay()
+            t1.record(stream)
+            torch.cuda.synchronize()
+            times.append(t0.elapsed_time(t1) / nsteps)
         del graph
-        return t0.elapsed_time(t1) / nsteps
+        return sorted(times)[len(times) // 2]
 
     def per_launch_us(self, groups, reps):
         """Graph-timed duration of each launch of the schedule: `reps`
@@ -689,12 +693,13 @@ def measure_case(case, sched_name, nsteps, warmup, extras=True, traffic_key=None
     if extras:
         rec["per_launch_us"] = case.per_launch_us(groups, max(8, min(nsteps, 60)))
         if bandwidth_bound:
-            rms = case.time_steps(calls, nsteps, 2, fn=case.read_only)
-            sms = case.time_steps(calls, nsteps, 2, fn=case.read_store)
+            rms = case.time_steps(calls, nsteps, 2, fn=case.read_only, replays=3)
+            sms = case.time_steps(calls, nsteps, 2, fn=case.read_store, replays=3)
             rec["achievable"] = {
                 "what": "plain read (unisvq_read_bytes) of the same weight and activation buffers, one launch per "
                         "launch of the schedule; read_only writes nothing, read_and_store also stores one word per "
-                        "wavefront (a kernel that writes any output pays a fixed end-of-launch cost)",
+                        "wavefront (a kernel that writes any output pays a fixed end-of-launch cost); the median "
+                        "of three timed replays of the graph of the same steps",
                 "read_only": {"ms_per_step": round(rms, 5), "GB_per_s": round(case.set_bytes / (rms * 1e-3) / 1e9, 1),
                               "product_over_read_time": round(ms / rms, 4)},
                 "read_and_store": {"ms_per_step": round(sms, 5),
