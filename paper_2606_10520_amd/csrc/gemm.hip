@@ -37,6 +37,11 @@ constexpr int kNI = 8;                // 16-row output tiles per wavefront
 constexpr int kBN = 16 * kNI;         // output rows per workgroup
 constexpr int kLdsRow = kGroup + 16;  // halves per decoded row in LDS (32-byte pad: no bank conflicts)
 constexpr int kWBuf = kBN * kLdsRow;  // halves per decoded-weight buffer
+// LDS bytes per token row when a wavefront's outputs are staged for the
+// stores (kBN values and 16 bytes of pad; multiples of 16 for 16-byte reads)
+constexpr int kStagePitch16 = kBN * 2 + 16;
+constexpr int kStagePitch32 = kBN * 4 + 16;
+static_assert(kWaves * 32 * kStagePitch32 <= 2 * kWBuf * 2, "the staged outputs fit the decode buffers");
 
 // One product of a (possibly batched) tiled launch; the products of a batch
 // share M, the token tiling and the output dtype.
@@ -372,7 +377,54 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const TileBatch tb) {
 
     // Epilogue.  D lane layout: output row 16 n + lane % 16, tokens
     // 16 i + 4 (lane / 16) + e.  With a K split the fp32 partial sums go to
-    // partial[split][M][N] and a second kernel adds them up.
+    // partial[split][M][N] and a second kernel adds them up.  Two- and
+    // four-byte stores of that layout scatter a token's rows over four
+    // segments per instruction; so the outputs (not the partial sums: staging
+    // their sixteen-lane runs of 64 bytes measured slower) go through LDS: each
+    // wavefront puts its 16 MI tokens x 128 rows there, converted (the
+    // buffers are free after the last group's barrier), and writes them back
+    // as 16-byte pieces of token rows.  An output not 16-byte aligned takes
+    // the element stores.
+    if (partial == nullptr && (reinterpret_cast<uintptr_t>(y) & 15) == 0) {  // uniform
+        const int esz = y_dtype == UNISVQ_F32 ? 4 : 2;
+        unsigned char* const dst = static_cast<unsigned char*>(y);
+        const int pitch = esz == 2 ? kStagePitch16 : kStagePitch32;  // bytes per token row in LDS
+        unsigned char* const stage = reinterpret_cast<unsigned char*>(wsh) + wave * 16 * MI * pitch;
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int tl = 16 * i + 4 * (lane >> 4) + e;  // token of the wavefront's tile
+                const int t = tok0 + tl;
+                const float sc = inv_scale && t < M ? inv_scale[t] : 1.0f;
+                const float bt = bias && t < M ? bias[t] : 0.0f;
+#pragma unroll
+                for (int n = 0; n < kNI; ++n) {
+                    unsigned char* const at = stage + tl * pitch + (16 * n + (lane & 15)) * esz;
+                    const float v = bias ? acc[i][n][e] * sc + bt : acc[i][n][e] * sc;
+                    if (y_dtype == UNISVQ_F32)
+                        *reinterpret_cast<float*>(at) = v;
+                    else if (y_dtype == UNISVQ_F16)
+                        *reinterpret_cast<_Float16*>(at) = static_cast<_Float16>(v);
+                    else
+                        *reinterpret_cast<__bf16*>(at) = static_cast<__bf16>(v);
+                }
+            }
+        }
+        __syncthreads();
+        // 16-byte pieces: kBN * esz / 16 per token row; rows come in whole
+        // pieces (N and the row tiles are multiples of 16)
+        const int per = kBN * esz / 16;
+        for (int k = lane; k < 16 * MI * per; k += 64) {
+            const int tl = k / per, c = k - tl * per;
+            const int t = tok0 + tl;
+            const int row = n0 + c * (16 / esz);
+            if (t < M && row < N)
+                *reinterpret_cast<uint4*>(dst + (static_cast<int64_t>(t) * N + row) * esz) =
+                    *reinterpret_cast<const uint4*>(stage + tl * pitch + 16 * c);
+        }
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
 #pragma unroll

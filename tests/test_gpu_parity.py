@@ -245,6 +245,29 @@ def test_output_is_overwritten_and_guard_bytes_untouched():
         assert rel_err(out.cpu().numpy(), ref) <= 5e-4
 
 
+@pytest.mark.parametrize("N,K,M", [(80, 384, 40), (256, 384, 130)])
+@pytest.mark.parametrize("ydt", [torch.float16, torch.bfloat16, torch.float32])
+def test_gemm_output_store_paths_agree(N, K, M, ydt):
+    """The tiled product writes a 16-byte aligned output through LDS in
+    16-byte pieces and any other output element by element: both give the
+    same bits (three groups: no K split, so both shapes take the direct
+    epilogue; 80 rows and 130 tokens leave parts of tiles past the ends)."""
+    Q, A, B = wl.gen_weights(N, K, seed=N + M)
+    pk = upload_pack(Q, A, B)
+    xb = wl.gen_activations(M, K, seed=M)
+    x = dev_x(xb, "f16")
+    aligned = u.gemm(pk, N, K, x, out_dtype=ydt)
+    buf = torch.zeros(M * N + 1, dtype=ydt, device=DEV)
+    shifted = buf[1:].view(M, N)  # one element past a 256-byte boundary
+    assert shifted.data_ptr() % 16 != 0
+    u.gemm(pk, N, K, x, out=shifted)
+    torch.cuda.synchronize()
+    assert torch.equal(aligned.view(torch.int16 if ydt != torch.float32 else torch.int32),
+                       shifted.view(torch.int16 if ydt != torch.float32 else torch.int32))
+    ref = oracle.matmul(oracle.pack(Q, A, B)[0], N, K, x_as_f64(xb, "f16"))
+    assert rel_err(aligned.float().cpu().numpy(), ref) <= (5e-4 if ydt == torch.float32 else 4e-3)
+
+
 def test_repeatable_and_linear_in_x():
     N, K = 1024, 4096
     Q, A, B = wl.gen_weights(N, K, seed=6)
