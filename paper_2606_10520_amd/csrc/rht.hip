@@ -590,7 +590,9 @@ __global__ __launch_bounds__(kRhtThreads) void rht_paley16_kernel(const XT* __re
     const int jb0 = blockIdx.x * pl.cnt;
     const int cnt = min(m, jb0 + pl.cnt) - jb0;
 
-    // 1. the row's loads go out first, raw into registers
+    // 1. the row's loads go out first, raw into registers (with the first
+    //    word of the character a wavefront needs, see 2.)
+    const uint64_t cw0 = cb.given ? cb.w[__builtin_amdgcn_readfirstlane(tid >> 6)] : 0;
     constexpr int C = kRhtMaxN / (8 * kRhtThreads);
     RowChunk<XT> rc[C];
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + row * n, static_cast<uint32_t>(n) * sizeof(XT));
@@ -601,12 +603,12 @@ __global__ __launch_bounds__(kRhtThreads) void rht_paley16_kernel(const XT* __re
 #pragma unroll
     for (int u = 0; u < 2; ++u) so[u] = ld_sign(rs, jb0 * half + tid + u * kRhtThreads);
     // 2. digit and character tables (the character from the arguments when
-    //    given: wavefront w reads word w of each 1024-element stretch), then
+    //    given: wavefront w reads word w of each 512-element stretch), then
     //    this workgroup's Paley columns (pt rows past cnt and columns past m
     //    are zero)
     if (cb.given) {
         for (int i0 = 0; i0 < h.q; i0 += kRhtThreads) {
-            const uint64_t word = cb.w[__builtin_amdgcn_readfirstlane((i0 + tid) >> 6)];
+            const uint64_t word = i0 == 0 ? cw0 : cb.w[__builtin_amdgcn_readfirstlane((i0 + tid) >> 6)];
             const int i = i0 + tid;
             if (i < h.q) {
                 chi[i] = i == 0 ? 0 : ((word >> (i & 63)) & 1u ? 1 : -1);
@@ -623,37 +625,44 @@ __global__ __launch_bounds__(kRhtThreads) void rht_paley16_kernel(const XT* __re
         for (int v = 1 + tid; v < h.q; v += kRhtThreads) chi[gf_square(v, h)] = 1;
         __syncthreads();
     }
-    for (int t = tid; t < 16 * kp; t += kRhtThreads) {
-        const int jl = t & 15, im = t >> 4;
-        const int j = jb0 + jl;
-        const int a = dig[min(max(im - 1, 0), h.q - 1)];
+    {
+        // a thread keeps one column (the stride is a multiple of 16)
+        const int jl = tid & 15, j = jb0 + jl;
         const int b = dig[min(max(j - 1, 0), h.q - 1)];
-        const float c = static_cast<float>(chi[gf_sub_index(a, b, h.p, h.e)]);
-        float v = im == j ? 1.f : (j == 0 ? -1.f : c);
-        v = im == 0 ? 1.f : v;
-        pt[jl * pitch + im] = static_cast<XT>((jl < cnt && im < m) ? v : 0.f);
+#pragma unroll 4
+        for (int t = tid; t < 16 * kp; t += kRhtThreads) {
+            const int im = t >> 4;
+            const int a = dig[min(max(im - 1, 0), h.q - 1)];
+            const float c = static_cast<float>(chi[gf_sub_index(a, b, h.p, h.e)]);
+            float v = im == j ? 1.f : (j == 0 ? -1.f : c);
+            v = im == 0 ? 1.f : v;
+            pt[jl * pitch + im] = static_cast<XT>((jl < cnt && im < m) ? v : 0.f);
+        }
     }
-    // 3. the row, transposed (signs applied on the input side), and zero
-    //    Paley rows m .. kp - 1
+    // 3. the row, transposed, and zero Paley rows m .. kp - 1.  A chunk's 8
+    //    elements share one Paley index and take 8 consecutive block
+    //    positions (8 divides the block, and n is a multiple of 16); the sign
+    //    of the input side flips the 16-bit value's sign bit (exact: the
+    //    stored value is x times +-1), the byte of -1 having its top bit set.
 #pragma unroll
     for (int u = 0; u < C; ++u) {
         const int i0 = 8 * (tid + u * kRhtThreads);
-        const uint32_t wd[4] = {rc[u].a.x, rc[u].a.y, rc[u].a.z, rc[u].a.w};
+        if (i0 < n) {
+            const uint32_t wd[4] = {rc[u].a.x, rc[u].a.y, rc[u].a.z, rc[u].a.w};
+            uint16_t* const dst = reinterpret_cast<uint16_t*>(zt + (i0 & (half - 1)) * pitch + (i0 >> h.k));
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int i = i0 + e;
-            if (i < n) {
-                float v = static_cast<float>(__builtin_bit_cast(XT, static_cast<uint16_t>(wd[e >> 1] >> (16 * (e & 1)))));
+            for (int e = 0; e < 8; ++e) {
+                uint32_t bits = (wd[e >> 1] >> (16 * (e & 1))) & 0xffffu;
                 if (mode == 0) {
                     const uint32_t sw = e < 4 ? rc[u].s.x : rc[u].s.y;
-                    v *= static_cast<float>(static_cast<signed char>((sw >> (8 * (e & 3))) & 0xffu));
+                    bits ^= ((sw >> (8 * (e & 3) + 7)) & 1u) << 15;
                 }
-                zt[(i & (half - 1)) * pitch + (i >> h.k)] = static_cast<XT>(v);
+                dst[e * pitch] = static_cast<uint16_t>(bits);
             }
         }
     }
     for (int t = tid; t < (kp - m) * half; t += kRhtThreads) {
-        const int c = t % half, im = m + t / half;
+        const int c = t & (half - 1), im = m + (t >> h.k);
         zt[c * pitch + im] = static_cast<XT>(0.f);
     }
     __syncthreads();
