@@ -268,19 +268,6 @@ def decoded_rows(u, q, Ad, Bd):
     return y.t().double().cpu().numpy()
 
 
-def ldl_factor(H, d=4):
-    """H = U D U^T with U unit upper block triangular (the caller's factorisation
-    that unisvq_ldlq takes): Cholesky of H with its index order reversed."""
-    C = np.linalg.cholesky(H[::-1, ::-1])
-    R = np.ascontiguousarray(C[::-1, ::-1])
-    U = np.empty_like(R)
-    for j in range(H.shape[0] // d):
-        sl = slice(d * j, d * (j + 1))
-        U[:, sl] = np.linalg.solve(R[sl, sl].T, R[:, sl].T).T
-        U[sl, sl] = np.eye(d)
-    return U
-
-
 LDLQ_FLOP_PER_FEEDBACK = 2  # one fma per (row, earlier column, column)
 
 
@@ -288,9 +275,10 @@ def bench_ldlq(args):
     """LDLQ (Eq. 7) on one 4096 x 4096 layer: W ~ N(0, 1) fp32, the paper's
     initial grid (Eq. 6) with one pair per (row, group), and a synthetic
     Hessian with coupled columns (X^T X / S, S = 2K activations sharing a
-    common component, + mu I, mu = 0.01, Sec. 4.2) factorised on the host.
-    Reports vectors per second, the fp64 rate, and the Hessian proxy loss
-    tr(E H E^T) against plain nearest-codeword rounding on a slice of rows."""
+    common component, + mu I, mu = 0.01, Sec. 4.2) factorised H = U D U^T by
+    unisvq_ldl (timed on its own).  Reports vectors per second, the fp64 rate,
+    and the Hessian proxy loss tr(E H E^T) against plain nearest-codeword
+    rounding on a slice of rows."""
     import torch
     import paper_2606_10520_amd.unisvq as u
 
@@ -306,14 +294,37 @@ def bench_ldlq(args):
     X = np.sqrt(0.1) * rng.standard_normal((S, K)) + np.sqrt(0.9) * rng.standard_normal((S, 1)) * rng.standard_normal((1, K))
     H = X.T @ X / S + 0.01 * np.eye(K)
     del X
-    U = ldl_factor(H)
+    # the factorisation on the GPU (timed separately from the quantiser)
+    Hd = torch.from_numpy(H).to(dev)
+    Ud = torch.empty_like(Hd)
+    info = torch.zeros(1, dtype=torch.int32, device=dev)
+    ws_ldl = torch.empty(u.ldl_workspace_bytes(K), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def factor():
+        st = lib.unisvq_ldl(K, Hd.data_ptr(), Ud.data_ptr(), None, info.data_ptr(), ws_ldl.data_ptr(),
+                            ws_ldl.numel(), stream.cuda_stream)
+        if st != 0:
+            raise RuntimeError(f"unisvq_ldl failed with status {st}")
+
+    factor()
+    torch.cuda.synchronize()
+    if int(info.item()) != 0:
+        raise RuntimeError(f"the synthetic Hessian is not positive definite (info {int(info.item())})")
+    f0 = torch.cuda.Event(enable_timing=True)
+    f1 = torch.cuda.Event(enable_timing=True)
+    f0.record(stream)
+    for _ in range(3):
+        factor()
+    f1.record(stream)
+    torch.cuda.synchronize()
+    ldl_ms = f0.elapsed_time(f1) / 3
+    U = Ud.cpu().numpy()
     W = torch.randn(N, K, device=dev, generator=torch.Generator(device=dev).manual_seed(1))
     Ad = torch.from_numpy(A.view(np.int16)).view(torch.float16).to(dev)
     Bd = torch.from_numpy(B.view(np.int16)).view(torch.float16).to(dev)
-    Ud = torch.from_numpy(U).to(dev)
     q = torch.empty((N, K), dtype=torch.uint8, device=dev)
     ws = torch.empty(u.ldlq_workspace_bytes(N, K), dtype=torch.uint8, device=dev)
-    stream = torch.cuda.current_stream()
 
     def step():
         st = lib.unisvq_ldlq(N, K, W.data_ptr(), Ud.data_ptr(), Ad.data_ptr(), Bd.data_ptr(), 0, q.data_ptr(),
@@ -368,6 +379,9 @@ def bench_ldlq(args):
                    "grid": "Eq. 6 initial grid, one pair per (row, group)",
                    "hessian": "X^T X / S, S = 2K, X = sqrt(0.1) Z + sqrt(0.9) common component, + 0.01 I",
                    "launches": 1 + 2 * (K // 128) - 1},
+        "factorisation": {"what": "unisvq_ldl, H = U D U^T with 4 x 4 pivot blocks, fp64",
+                          "ms": round(ldl_ms, 3), "launches": 1 + 3 * (K // 64) - 2,
+                          "fp64_TFLOP_s": round(K ** 3 / 3 / (ldl_ms * 1e-3) / 1e12, 2)},
         "proxy_loss_over_nearest": round(loss(E_l) / loss(E_r), 4),
         "weight_mse": {"ldlq": round(mse(E_l), 5), "nearest": round(mse(E_r), 5)},
         "roofline": {"bound": "alu", "achieved": round(ach, 2), "peak": PEAK_FP64_TFLOPS, "unit": "TFLOP/s",

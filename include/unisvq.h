@@ -457,7 +457,7 @@ int unisvq_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, con
  * same operation order, ties to the lowest index).  U is the unit upper
  * block-triangular factor of H = U D U^T (4 x 4 identity blocks on the
  * diagonal, D block diagonal; H the layer's input Hessian, regularised by
- * mu I with mu = 0.01 in Sec. 4.2); the caller factorises H.  Each sum is
+ * mu I with mu = 0.01 in Sec. 4.2), e.g. from unisvq_ldl.  Each sum is
  * evaluated as one fma chain in increasing k from 0, then u = W + sum, so the
  * codes are those of a plain sequential evaluation bit for bit.
  *   W          device fp32 [N][K], 16-byte aligned
@@ -473,6 +473,35 @@ int unisvq_quantize(int64_t N, int64_t K, const float* W, const uint16_t* A, con
 size_t unisvq_ldlq_workspace_bytes(int64_t N, int64_t K);
 int unisvq_ldlq(int64_t N, int64_t K, const float* W, const double* U, const uint16_t* A, const uint16_t* B,
                 int64_t affine_groups, uint8_t* codes, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---- Block LDL^T factorisation of the Hessian for LDLQ (Sec. 3.2.2, Eq. 7) ----
+ * The factor unisvq_ldlq takes: H = U D U^T with U unit upper
+ * block-triangular (4 x 4 identity blocks on the diagonal, zeros below them)
+ * and D block diagonal (4 x 4 blocks), U's off-diagonal entries being Eq. 7's
+ * feedback coefficients.  Computed in fp64 from the last pivot block to the
+ * first (D_j = S_jj, U[0:j, j] = S[0:j, j] D_j^-1, S[0:j, 0:j] -= U[0:j, j] D_j
+ * U[0:j, j]^T, S the part not yet factorised), blocked over 64-column panels;
+ * results differ from another LDL^T or Cholesky-based factorisation only by
+ * rounding.
+ *   K          128 <= K <= 32768, K % 128 == 0 (UNISVQ_ESHAPE otherwise)
+ *   H          device fp64 [K][K] row-major, 16-byte aligned, symmetric
+ *              positive definite (e.g. regularised by mu I); only the upper
+ *              triangle H[a][b], a <= b, is read
+ *   U          device fp64 [K][K] row-major, 16-byte aligned, written in full;
+ *              U == H factorises in place (H is then overwritten), any other
+ *              overlap is UNISVQ_EINVAL
+ *   D          device fp64 [K/4][4][4], or NULL
+ *   info       device int32, or NULL: set to 0, or to 1 + the index of the
+ *              first pivot block found not positive definite (blocks are taken
+ *              last to first), after which U and D are meaningless.  The launches
+ *              are asynchronous: read it after synchronising the stream.
+ *   workspace  device, >= unisvq_ldl_workspace_bytes(K) bytes (K x 64 fp64 and
+ *              the panel's pivot inverses), 16-byte aligned; overwritten
+ * Work: one set-up launch and 3 K/64 - 2 launches of the panel steps.
+ * unisvq_ldl_workspace_bytes returns 0 for a K outside the range above. */
+size_t unisvq_ldl_workspace_bytes(int64_t K);
+int unisvq_ldl(int64_t K, const double* H, double* U, double* D, int32_t* info, void* workspace,
+               size_t workspace_bytes, void* stream);
 
 /* ---- Randomized Hadamard transform around the product (Sec. 3.2.1, Eq. 5) ----
  * The weights are quantised in the rotated basis W_rot = U S_U W S_V V (S_U,

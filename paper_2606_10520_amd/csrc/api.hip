@@ -450,6 +450,35 @@ int unisvq_ldlq(int64_t N, int64_t K, const float* W, const double* U, const uin
     return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
 }
 
+/* ---- block LDL^T factorisation of the Hessian ---- */
+
+size_t unisvq_ldl_workspace_bytes(int64_t K) {
+    if (K < unisvq::kGroup || K % unisvq::kGroup || K > 32768) return 0;
+    return unisvq::ldl_workspace_bytes(K);
+}
+
+int unisvq_ldl(int64_t K, const double* H, double* U, double* D, int32_t* info, void* workspace,
+               size_t workspace_bytes, void* stream) {
+    if (!H || !U) return UNISVQ_EINVAL;
+    if (K < unisvq::kGroup || K % unisvq::kGroup || K > 32768) return UNISVQ_ESHAPE;
+    if (!aligned(H, 16) || !aligned(U, 16) || (D && !aligned(D, 8)) || (info && !aligned(info, 4)))
+        return UNISVQ_EALIGN;
+    // U may be H itself (in place) but must not overlap it otherwise; D and
+    // info must not overlap either of them
+    const uintptr_t bytes = static_cast<uintptr_t>(K) * static_cast<uintptr_t>(K) * 8;
+    const uintptr_t h0 = reinterpret_cast<uintptr_t>(H), u0 = reinterpret_cast<uintptr_t>(U);
+    if (h0 != u0 && h0 < u0 + bytes && u0 < h0 + bytes) return UNISVQ_EINVAL;
+    auto clash = [&](const void* p, uintptr_t n) {
+        const uintptr_t q = reinterpret_cast<uintptr_t>(p);
+        return (q < h0 + bytes && h0 < q + n) || (q < u0 + bytes && u0 < q + n);
+    };
+    if ((D && clash(D, static_cast<uintptr_t>(K) * 4 * 8)) || (info && clash(info, 4))) return UNISVQ_EINVAL;
+    if (!workspace || workspace_bytes < unisvq::ldl_workspace_bytes(K)) return UNISVQ_EWORKSPACE;
+    if (!aligned(workspace, 16)) return UNISVQ_EALIGN;
+    const hipError_t e = unisvq::launch_ldl(K, H, U, D, info, workspace, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? UNISVQ_OK : UNISVQ_EHIP;
+}
+
 /* ---- randomized Hadamard transform ---- */
 
 int unisvq_rht(int64_t n, int64_t M, const void* x, int x_dtype, const int8_t* signs, int mode, void* y, int y_dtype,

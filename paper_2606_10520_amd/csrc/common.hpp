@@ -127,6 +127,12 @@ size_t ldlq_workspace_bytes(int64_t N, int64_t K);
 hipError_t launch_ldlq(int64_t N, int64_t K, const float* W, const double* U, const uint16_t* A, const uint16_t* B,
                        int64_t affine_groups, uint8_t* codes, void* workspace, hipStream_t s);
 
+// Block LDL^T factorisation H = U D U^T (4 x 4 pivot blocks, fp64 [K][K]);
+// workspace of ldl_workspace_bytes(K) bytes.
+size_t ldl_workspace_bytes(int64_t K);
+hipError_t launch_ldl(int64_t K, const double* H, double* U, double* D, int32_t* info, void* workspace,
+                      hipStream_t s);
+
 // Randomized Hadamard transform of M rows of length n (mode 0: input side,
 // signs first; mode 1: output side, signs last); UNISVQ_EUNSUP when n has no
 // supported Hadamard construction or exceeds the LDS row.

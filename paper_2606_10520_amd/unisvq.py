@@ -28,6 +28,7 @@ EXPORTS = ("unisvq_version", "unisvq_status_string", "unisvq_packed_bytes", "uni
            "unisvq_quantize", "unisvq_rht", "unisvq_var_codes_bytes", "unisvq_var_affine_bytes",
            "unisvq_var_pack", "unisvq_var_unpack", "unisvq_var_gemv", "unisvq_var_gemv_batched",
            "unisvq_var_gemm_workspace_bytes", "unisvq_var_gemm", "unisvq_ldlq_workspace_bytes", "unisvq_ldlq",
+           "unisvq_ldl_workspace_bytes", "unisvq_ldl",
            "unisvq_gemv_rht_batched", "unisvq_read_sink_words", "unisvq_read_bytes", "unisvq_noalloc_scratch_bytes",
            "unisvq_gemm_noalloc", "unisvq_gemm_batched_workspace_bytes", "unisvq_gemm_batched")
 # format variants: (bits, d) pairs served by the unisvq_var_* entry points
@@ -139,6 +140,10 @@ def load():
     lib.unisvq_ldlq_workspace_bytes.restype = sz
     lib.unisvq_ldlq.argtypes = [i64, i64, p, p, p, p, i64, p, p, sz, p]
     lib.unisvq_ldlq.restype = i32
+    lib.unisvq_ldl_workspace_bytes.argtypes = [i64]
+    lib.unisvq_ldl_workspace_bytes.restype = sz
+    lib.unisvq_ldl.argtypes = [i64, p, p, p, p, p, sz, p]
+    lib.unisvq_ldl.restype = i32
     lib.unisvq_gemm_batched_workspace_bytes.argtypes = [ctypes.POINTER(GemvProblem), i32, i64, i32]
     lib.unisvq_gemm_batched_workspace_bytes.restype = sz
     lib.unisvq_gemm_batched.argtypes = [ctypes.POINTER(GemvProblem), i32, i64, i32, i32, p, sz, p]
@@ -719,6 +724,36 @@ def var_gemm(packed_codes, packed_affine, N: int, K: int, bits: int, d: int, aff
 
 
 # ------------------------------------------------ LDLQ (Eq. 7)
+
+def ldl_workspace_bytes(K: int) -> int:
+    return load().unisvq_ldl_workspace_bytes(K)
+
+
+def ldl(H, out=None, with_d: bool = True, workspace=None, stream=None):
+    """H = U D U^T (fp64 [K][K], symmetric positive definite; the upper
+    triangle is read) with U unit upper block triangular and D block diagonal
+    (4 x 4 blocks): the factor ldlq() takes.  `out` may be H itself (in place).
+    Returns (U, D [K/4][4][4] or None, info): info is a device int32 [1], 0 or
+    1 + the first pivot block found not positive definite."""
+    torch = _torch()
+    _need_cuda(H, out, workspace)
+    if H.dtype != torch.float64 or H.dim() != 2 or H.shape[0] != H.shape[1]:
+        raise ValueError("H must be fp64 [K][K]")
+    if not H.is_contiguous():
+        raise ValueError("H must be contiguous")
+    K = H.shape[0]
+    if out is None:
+        out = torch.empty((K, K), dtype=torch.float64, device=H.device)
+    if out.dtype != torch.float64:
+        raise ValueError("out must be fp64")
+    _need_buffer(out, K * K * 8, "out", exact=True)
+    D = torch.empty((K // 4, 4, 4), dtype=torch.float64, device=H.device) if with_d else None
+    info = torch.empty(1, dtype=torch.int32, device=H.device)
+    workspace, wb = _workspace(workspace, ldl_workspace_bytes(K), H)
+    _check("unisvq_ldl", load().unisvq_ldl(K, _ptr(H), _ptr(out), _ptr(D), _ptr(info), _ptr(workspace), wb,
+                                            _stream(stream)))
+    return out, D, info
+
 
 def ldlq_workspace_bytes(N: int, K: int) -> int:
     return load().unisvq_ldlq_workspace_bytes(N, K)

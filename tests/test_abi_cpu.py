@@ -388,6 +388,39 @@ def test_ldlq_validation():
     assert lib.unisvq_ldlq(16, 256, GOOD, GOOD, GOOD, GOOD, 0, GOOD, GOOD + 8, need, None) == EALIGN
 
 
+def test_ldl_validation():
+    lib = u.load()
+    K = 256
+    need = lib.unisvq_ldl_workspace_bytes(K)
+    assert need == K * 64 * 8 + 256 * 8
+    for bad in (0, 64, 200, 32768 + 128):
+        assert lib.unisvq_ldl_workspace_bytes(bad) == 0
+    H = GOOD
+    U = H + K * K * 8
+    D = U + K * K * 8
+    info = D + K * 4 * 8
+    ws = info + 256
+
+    def call(K=K, H=H, U=U, D=D, info=info, ws=ws, wb=need):
+        return lib.unisvq_ldl(K, H, U, D, info, ws, wb, None)
+
+    assert call(H=None) == EINVAL
+    assert call(U=None) == EINVAL
+    for bad in (0, 64, 200, 32768 + 128):
+        assert call(K=bad) == ESHAPE
+    assert call(H=H + 8) == EALIGN
+    assert call(U=U + 8) == EALIGN
+    assert call(D=D + 4) == EALIGN
+    assert call(info=info + 2) == EALIGN
+    assert call(U=H + 128) == EINVAL  # overlaps H without being H
+    assert call(D=H + 64) == EINVAL
+    assert call(D=U + K * K * 8 - 8) == EINVAL
+    assert call(info=U + 4) == EINVAL
+    assert call(ws=None) == EWS
+    assert call(wb=need - 8) == EWS
+    assert call(ws=ws + 8) == EALIGN
+
+
 def test_fold_workspace_and_validation():
     lib = u.load()
     ws = lib.unisvq_gemm_fold_workspace_bytes
