@@ -19,9 +19,9 @@
 //     per row, lane c = panel column c;
 //  3. trailing: S[a][b] -= sum_k W[a][k] U[b][k] over the panel's 64
 //     columns, for a <= b above the panel (64 x 64 tiles of the upper
-//     triangle, 4 x 4 outputs per thread).
-// Every pivot block is checked for positive definiteness (its 4 x 4
-// Cholesky factor); the first failure is reported through `info`.
+//     triangle on the fp64 matrix cores).
+// Every pivot block is checked for positive definiteness (its leading
+// principal minors); the first failure is reported through `info`.
 #include "common.hpp"
 
 namespace unisvq {
@@ -29,7 +29,6 @@ namespace {
 
 constexpr int kLdlP = 64;          // panel width (16 pivot blocks of 4)
 constexpr int kLdlPitch = kLdlP + 1;  // LDS row pitch (doubles) of the diagonal block
-constexpr int kLdlTPitch = kLdlP + 2;  // LDS pitch of the transposed trailing operands
 
 __device__ inline double lane_f64(double v, int src) {
     const uint2 u = __builtin_bit_cast(uint2, v);
@@ -49,9 +48,47 @@ __global__ __launch_bounds__(256) void ldl_init_kernel(const double* H, double* 
     *reinterpret_cast<double2*>(U + e) = double2{a <= b ? h.x : 0.0, a <= b + 1 ? h.y : 0.0};
 }
 
-// Panel [c0, c0 + 64): its diagonal block factorised in LDS.  Writes the
-// block's U (identity pivot blocks, zeros below them), D (when given) and
-// the 16 inverses D_j^-1 to dinv[16][4][4].
+// Inverse of a 4 x 4 matrix by Laplace expansion along its first two rows
+// (complementary 2 x 2 minors: s_ of rows 0, 1, c_ of rows 2, 3), every
+// index fixed at compile time; returns the determinant.
+__device__ inline double inverse4(const double (&m)[4][4], double (&b)[4][4]) {
+    const double s0 = m[0][0] * m[1][1] - m[1][0] * m[0][1], s1 = m[0][0] * m[1][2] - m[1][0] * m[0][2];
+    const double s2 = m[0][0] * m[1][3] - m[1][0] * m[0][3], s3 = m[0][1] * m[1][2] - m[1][1] * m[0][2];
+    const double s4 = m[0][1] * m[1][3] - m[1][1] * m[0][3], s5 = m[0][2] * m[1][3] - m[1][2] * m[0][3];
+    const double c5 = m[2][2] * m[3][3] - m[3][2] * m[2][3], c4 = m[2][1] * m[3][3] - m[3][1] * m[2][3];
+    const double c3 = m[2][1] * m[3][2] - m[3][1] * m[2][2], c2 = m[2][0] * m[3][3] - m[3][0] * m[2][3];
+    const double c1 = m[2][0] * m[3][2] - m[3][0] * m[2][2], c0 = m[2][0] * m[3][1] - m[3][0] * m[2][1];
+    const double det = s0 * c5 - s1 * c4 + s2 * c3 + s3 * c2 - s4 * c1 + s5 * c0;
+    const double r = 1.0 / det;
+    b[0][0] = (m[1][1] * c5 - m[1][2] * c4 + m[1][3] * c3) * r;
+    b[0][1] = (-m[0][1] * c5 + m[0][2] * c4 - m[0][3] * c3) * r;
+    b[0][2] = (m[3][1] * s5 - m[3][2] * s4 + m[3][3] * s3) * r;
+    b[0][3] = (-m[2][1] * s5 + m[2][2] * s4 - m[2][3] * s3) * r;
+    b[1][0] = (-m[1][0] * c5 + m[1][2] * c2 - m[1][3] * c1) * r;
+    b[1][1] = (m[0][0] * c5 - m[0][2] * c2 + m[0][3] * c1) * r;
+    b[1][2] = (-m[3][0] * s5 + m[3][2] * s2 - m[3][3] * s1) * r;
+    b[1][3] = (m[2][0] * s5 - m[2][2] * s2 + m[2][3] * s1) * r;
+    b[2][0] = (m[1][0] * c4 - m[1][1] * c2 + m[1][3] * c0) * r;
+    b[2][1] = (-m[0][0] * c4 + m[0][1] * c2 - m[0][3] * c0) * r;
+    b[2][2] = (m[3][0] * s4 - m[3][1] * s2 + m[3][3] * s0) * r;
+    b[2][3] = (-m[2][0] * s4 + m[2][1] * s2 - m[2][3] * s0) * r;
+    b[3][0] = (-m[1][0] * c3 + m[1][1] * c1 - m[1][2] * c0) * r;
+    b[3][1] = (m[0][0] * c3 - m[0][1] * c1 + m[0][2] * c0) * r;
+    b[3][2] = (-m[3][0] * s3 + m[3][1] * s1 - m[3][2] * s0) * r;
+    b[3][3] = (m[2][0] * s3 - m[2][1] * s1 + m[2][2] * s0) * r;
+    return det;
+}
+
+// Panel [c0, c0 + 64): its diagonal block factorised in LDS, pivot block by
+// pivot block (a = 4 jb, the last first).  Per pivot, two phases:
+//  A. every thread t < max(1, a) inverts D_j itself (inverse4) and forms
+//     row t of u = S[0:a, a:a+4] D_j^-1; thread 0 also writes D_j, D_j^-1 and
+//     checks positive definiteness (the leading principal minors);
+//  B. S[r][c] -= u[r] . S[c][a:a+4] for r <= c < a (thread: column c = t % 64,
+//     rows t / 64 + 4k; computed for the whole block, without branches),
+//     and u and the identity pivot block go to U.
+// Entries below the pivot blocks keep the zeros written by the set-up, so
+// the LDS block is never written back.  The 16 inverses go to dinv.
 __global__ __launch_bounds__(256) void ldl_diag_kernel(double* U, int64_t K, int64_t c0, double* D, int32_t* info,
                                                        double* dinv) {
     __shared__ double B[kLdlP * kLdlPitch];
@@ -59,91 +96,74 @@ __global__ __launch_bounds__(256) void ldl_diag_kernel(double* U, int64_t K, int
     __shared__ double uu[kLdlP * 4];
     const int t = threadIdx.x;
     double* const blk = U + c0 * K + c0;
-    for (int i = t; i < kLdlP * kLdlP; i += 256) {
-        const int r = i / kLdlP, c = i % kLdlP;
-        B[r * kLdlPitch + c] = r <= c ? blk[r * K + c] : 0.0;
+    const int c = t & 63, rq = t >> 6;
+    {
+        // all 16 loads of a thread in flight at once (row rq + 4k, column c)
+        double v[kLdlP / 4];
+#pragma unroll
+        for (int k = 0; k < kLdlP / 4; ++k) v[k] = blk[(rq + 4 * k) * K + c];
+#pragma unroll
+        for (int k = 0; k < kLdlP / 4; ++k) B[(rq + 4 * k) * kLdlPitch + c] = v[k];
     }
     __syncthreads();
     for (int jb = kLdlP / 4 - 1; jb >= 0; --jb) {
         const int a = 4 * jb;
-        if (t == 0) {
-            // D_j from the upper triangle, its Cholesky factor L, then
-            // D_j^-1 = L^-T L^-1
-            double d[4][4], L[4][4] = {}, Li[4][4] = {};
+        // A.
+        if (t == 0 || t < a) {
+            double d[4][4], inv[4][4];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) d[i][j] = B[(a + (i < j ? i : j)) * kLdlPitch + a + (i < j ? j : i)];
-            if (D) {
+            const double det = inverse4(d, inv);
+            if (t == 0) {
 #pragma unroll
-                for (int i = 0; i < 16; ++i) D[(c0 / 4 + jb) * 16 + i] = d[i >> 2][i & 3];
-            }
-            bool ok = true;
+                for (int i = 0; i < 16; ++i) Di[jb * 16 + i] = inv[i >> 2][i & 3];
+                if (D) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                double s = d[j][j];
-#pragma unroll
-                for (int k = 0; k < j; ++k) s -= L[j][k] * L[j][k];
-                if (!(s > 0.0)) ok = false;  // also NaN
-                L[j][j] = sqrt(s);
-#pragma unroll
-                for (int i = j + 1; i < 4; ++i) {
-                    double v = d[i][j];
-#pragma unroll
-                    for (int k = 0; k < j; ++k) v -= L[i][k] * L[j][k];
-                    L[i][j] = v / L[j][j];
+                    for (int i = 0; i < 16; ++i) D[(c0 / 4 + jb) * 16 + i] = d[i >> 2][i & 3];
                 }
+                const double m2 = d[0][0] * d[1][1] - d[1][0] * d[0][1];
+                const double m3 = d[0][0] * (d[1][1] * d[2][2] - d[1][2] * d[2][1]) -
+                                  d[0][1] * (d[1][0] * d[2][2] - d[1][2] * d[2][0]) +
+                                  d[0][2] * (d[1][0] * d[2][1] - d[1][1] * d[2][0]);
+                const bool ok = d[0][0] > 0.0 && m2 > 0.0 && m3 > 0.0 && det > 0.0;  // false on NaN
+                if (!ok && info && *info == 0) *info = static_cast<int32_t>(c0 / 4 + jb + 1);
             }
-            if (!ok && info && *info == 0) *info = static_cast<int32_t>(c0 / 4 + jb + 1);
+            if (t < a) {
+                double x[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                Li[i][i] = 1.0 / L[i][i];
+                for (int n = 0; n < 4; ++n) x[n] = B[t * kLdlPitch + a + n];
 #pragma unroll
-                for (int j = 0; j < i; ++j) {
-                    double s = 0.0;
+                for (int m = 0; m < 4; ++m) {
+                    double v = 0.0;
 #pragma unroll
-                    for (int k = j; k < i; ++k) s += L[i][k] * Li[k][j];
-                    Li[i][j] = -s / L[i][i];
+                    for (int n = 0; n < 4; ++n) v = fma(x[n], inv[n][m], v);
+                    uu[t * 4 + m] = v;
                 }
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    double s = 0.0;
-#pragma unroll
-                    for (int k = (i > j ? i : j); k < 4; ++k) s += Li[k][i] * Li[k][j];
-                    Di[jb * 16 + i * 4 + j] = s;
-                }
-        }
-        __syncthreads();
-        // the rows above the pivot: u = S[0:a, a:a+4] D_j^-1
-        if (t < 4 * a) {
-            const int r = t >> 2, m = t & 3;
-            double s = 0.0;
-#pragma unroll
-            for (int n = 0; n < 4; ++n) s = fma(B[r * kLdlPitch + a + n], Di[jb * 16 + n * 4 + m], s);
-            uu[r * 4 + m] = s;
-        }
-        __syncthreads();
-        // S[r][c] -= u[r] . S[c][a:a+4] for r <= c < a
-        for (int i = t; i < a * a; i += 256) {
-            const int r = i / a, c = i - r * a;
-            if (r <= c) {
-                double s = 0.0;
-#pragma unroll
-                for (int m = 0; m < 4; ++m) s = fma(uu[r * 4 + m], B[c * kLdlPitch + a + m], s);
-                B[r * kLdlPitch + c] -= s;
             }
         }
         __syncthreads();
-        if (t < 4 * a) B[(t >> 2) * kLdlPitch + a + (t & 3)] = uu[t];
-        if (t < 16) B[(a + (t >> 2)) * kLdlPitch + a + (t & 3)] = (t >> 2) == (t & 3) ? 1.0 : 0.0;
+        // B.  Only S[r][c] with r <= c < a is live: the LDS entries below the
+        // diagonal and those of columns a and beyond are never read again
+        // (the factor goes straight to U), so the whole block is updated
+        // without branches; the dead entries take whatever they get.
+        {
+            double bc[4];
+#pragma unroll
+            for (int n = 0; n < 4; ++n) bc[n] = B[c * kLdlPitch + a + n];
+#pragma unroll
+            for (int k = 0; k < kLdlP / 4; ++k) {
+                const int r = rq + 4 * k;
+                double v = 0.0;
+#pragma unroll
+                for (int n = 0; n < 4; ++n) v = fma(uu[r * 4 + n], bc[n], v);
+                B[r * kLdlPitch + c] -= v;
+            }
+        }
+        if (t < 4 * a) blk[(t >> 2) * K + a + (t & 3)] = uu[t];
+        if (t < 16) blk[(a + (t >> 2)) * K + a + (t & 3)] = (t >> 2) == (t & 3) ? 1.0 : 0.0;
         __syncthreads();
-    }
-    for (int i = t; i < kLdlP * kLdlP; i += 256) {
-        const int r = i / kLdlP, c = i % kLdlP;
-        blk[r * K + c] = B[r * kLdlPitch + c];
     }
     dinv[t] = Di[t];  // 256 threads, 16 x 16 values
 }
@@ -157,11 +177,15 @@ __global__ __launch_bounds__(256) void ldl_strip_kernel(double* U, int64_t K, in
     __shared__ double Di[16 * 16];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const double* const blk = U + c0 * K + c0;
-    for (int i = t; i < kLdlP * kLdlP; i += 256) {
-        const int r = i / kLdlP, c = i % kLdlP;
-        Up[r * kLdlPitch + c] = blk[r * K + c];
+    {
+        double v[kLdlP / 4];
+#pragma unroll
+        for (int k = 0; k < kLdlP / 4; ++k) v[k] = blk[(wave + 4 * k) * K + lane];
+        const double di = dinv[t];
+#pragma unroll
+        for (int k = 0; k < kLdlP / 4; ++k) Up[(wave + 4 * k) * kLdlPitch + lane] = v[k];
+        Di[t] = di;
     }
-    Di[t] = dinv[t];
     __syncthreads();
     const int b = lane >> 2;  // the lane's pivot block
     for (int64_t r = static_cast<int64_t>(blockIdx.x) * 4 + wave; r < c0; r += static_cast<int64_t>(gridDim.x) * 4) {
@@ -190,43 +214,81 @@ __global__ __launch_bounds__(256) void ldl_strip_kernel(double* U, int64_t K, in
 
 // S[a][b] -= sum_k W[a][k] U[b][c0 + k] for a <= b < c0: workgroup (tb, ta)
 // takes the 64 x 64 tile of rows 64 ta, columns 64 tb (tiles below the
-// diagonal return at once); thread (ty, tx) 4 x 4 outputs.
+// diagonal return at once) on the fp64 matrix cores.  Both 64 x 64 operands
+// are staged row-major in LDS (pitch 68 doubles: an operand read touches
+// every bank the minimum number of times); wavefront w computes the 32 x 32
+// quarter (rows 32 (w / 2), columns 32 (w % 2)) as 2 x 2 blocks of
+// v_mfma_f64_16x16x4f64 over 16 steps of 4 columns of k.  Operand lanes:
+// A[i][k] at lane i + 16 k, B[k][j] at lane j + 16 k; result D[i][j] at
+// lane j + 16 (i % 4), item i / 4.
+constexpr int kLdlMPitch = kLdlP + 4;
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
 __global__ __launch_bounds__(256) void ldl_trailing_kernel(double* U, int64_t K, int64_t c0, const double* W) {
     const int ta = blockIdx.y, tb = blockIdx.x;
     if (ta > tb) return;  // uniform
-    __shared__ double Wt[kLdlP * kLdlTPitch];  // [k][row]
-    __shared__ double Ut[kLdlP * kLdlTPitch];  // [k][column]
-    const int t = threadIdx.x;
+    __shared__ double Ws[kLdlP * kLdlMPitch];  // [row][k]
+    __shared__ double Us[kLdlP * kLdlMPitch];  // [column][k]
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int64_t a0 = static_cast<int64_t>(ta) * kLdlP, b0 = static_cast<int64_t>(tb) * kLdlP;
-    for (int e = t; e < kLdlP * kLdlP; e += 256) {
-        const int i = e >> 6, k = e & 63;
-        Wt[k * kLdlTPitch + i] = W[(a0 + i) * kLdlP + k];
-        Ut[k * kLdlTPitch + i] = U[(b0 + i) * K + c0 + k];
+    const int wr = 32 * (wave >> 1), wc = 32 * (wave & 1);
+    const int li = lane & 15, lk = lane >> 4;
+    // this lane's 16 outputs, read now (every one in bounds: the tile lies
+    // above row c0) and written back after the products
+    double old[2][2][4];
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                old[bi][bj][v] = U[(a0 + wr + 16 * bi + lk + 4 * v) * K + b0 + wc + 16 * bj + li];
+    {
+        // the operands, 16 + 16 coalesced loads per thread in flight at once
+        // (row rq + 4k, column c of each 64 x 64 operand)
+        const int c = t & 63, rq = t >> 6;
+        double wv[kLdlP / 4], uv[kLdlP / 4];
+#pragma unroll
+        for (int k = 0; k < kLdlP / 4; ++k) {
+            wv[k] = W[(a0 + rq + 4 * k) * kLdlP + c];
+            uv[k] = U[(b0 + rq + 4 * k) * K + c0 + c];
+        }
+#pragma unroll
+        for (int k = 0; k < kLdlP / 4; ++k) {
+            Ws[(rq + 4 * k) * kLdlMPitch + c] = wv[k];
+            Us[(rq + 4 * k) * kLdlMPitch + c] = uv[k];
+        }
     }
     __syncthreads();
-    const int ty = t >> 4, tx = t & 15;
-    double acc[4][4] = {};
-    for (int k = 0; k < kLdlP; ++k) {
-        double wv[4], uv[4];
+    f64x4 acc[2][2];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            wv[i] = Wt[k * kLdlTPitch + 4 * ty + i];
-            uv[i] = Ut[k * kLdlTPitch + 4 * tx + i];
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj) acc[bi][bj] = f64x4{0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int s = 0; s < kLdlP / 4; ++s) {
+        double av[2], bv[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            av[q] = Ws[(wr + 16 * q + li) * kLdlMPitch + 4 * s + lk];
+            bv[q] = Us[(wc + 16 * q + li) * kLdlMPitch + 4 * s + lk];
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = fma(wv[i], uv[j], acc[i][j]);
+            for (int bj = 0; bj < 2; ++bj)
+                acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[bi], bv[bj], acc[bi][bj], 0, 0, 0);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int64_t a = a0 + 4 * ty + i;
+    for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t bcol = b0 + 4 * tx + j;
-            if (a <= bcol) U[a * K + bcol] -= acc[i][j];
-        }
-    }
+        for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int64_t a = a0 + wr + 16 * bi + lk + 4 * v;
+                const int64_t bcol = b0 + wc + 16 * bj + li;
+                if (a <= bcol) U[a * K + bcol] = old[bi][bj][v] - acc[bi][bj][v];
+            }
 }
 
 }  // namespace
