@@ -676,11 +676,14 @@ def product_kernel_name(case):
         return "gemv_kernel"
     if not case.ws.var and not case.fold and case.M <= SKINNY_MAX_M:
         return "skinny_kernel"
+    if not case.ws.var and not case.fold and case.M <= 32:
+        return "skinny_kernel or gemm_kernel (by launch width)"
     return "gemm_kernel"
 
 
-# Largest batch the 2x4 product sends to the small-batch kernel.
-SKINNY_MAX_M = 32
+# Largest batch the 2x4 product always sends to the small-batch kernel (from
+# 17 to 32 tokens only launches of fewer than 64 tiles of 128 rows go there).
+SKINNY_MAX_M = 16
 
 
 def measure_case(case, sched_name, nsteps, warmup, extras=True, traffic_key=None):

@@ -208,10 +208,11 @@ int unisvq_gemv_batched(const unisvq_gemv_problem* problems, int count, int64_t 
 
 /* Device workspace unisvq_gemm needs for this product, in bytes (0: none):
  * for BF16 activations an fp16 copy of x (M*K*2 bytes, rounded up to 256;
- * above 32 tokens the copy is kept in 16-token tiles, so M counts rounded up
- * to a multiple of 16) and one fp32 scale per token (rounded up to 256);
- * above 32 tokens, for products with too few output tiles to fill the GPU,
- * fp32 partial sums of a split along K (splits*M*N*4 bytes).  0 also for an invalid shape, M < 1 or an
+ * above 16 tokens sized for the copy in 16-token tiles, so M counts rounded
+ * up to a multiple of 16) and one fp32 scale per token (rounded up to 256);
+ * above 16 tokens, for products with too few output tiles to fill the GPU,
+ * fp32 partial sums of a split along K (splits*M*N*4 bytes).  From 17 to 32
+ * tokens the size covers either kernel below (the one taken may use less).  0 also for an invalid shape, M < 1 or an
  * unknown x_dtype.  Host-only, no GPU needed. */
 size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype);
 
@@ -219,12 +220,13 @@ size_t unisvq_gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype)
  * Arguments as unisvq_gemv; x_dtype F16 or BF16, y_dtype F16, BF16 or F32.
  * Up to 3 tokens the matrix-vector kernel of unisvq_gemv computes it (its
  * faster range; the workspace then goes unused), unless K is too long for
- * that kernel's LDS.  Up to 32 tokens one launch of the small-batch kernel
- * computes it: each
+ * that kernel's LDS.  Up to 16 tokens -- and up to 32 when the product has
+ * fewer than 64 tiles of 128 output rows, where the alternative would split
+ * K many ways -- one launch of the small-batch kernel computes it: each
  * wavefront decodes 16-row x 128-column tiles into its own LDS region and
  * multiplies them with all tokens at once; the wavefronts of a workgroup
  * split K and add their sums in a fixed order (no workspace beyond the bf16
- * copy below).  Above 32 tokens each
+ * copy below).  Otherwise each
  * workgroup decodes a 128-row x 128-column weight tile at a time into
  * LDS (every vector A q + B in fp32 from the exact integer codes, rounded
  * once to fp16) and multiplies it with its tokens on the matrix cores
@@ -252,10 +254,12 @@ size_t unisvq_gemm_batched_workspace_bytes(const unisvq_gemv_problem* problems, 
 
 /* Several independent products y_i = x_i * W_hat_i^T of the same M and
  * dtypes (a decoder's query, key and value projections, or its gate and up
- * projections, at a small batch).  For M <= 32 all of them run in ONE launch
+ * projections, at a small batch).  For M <= 16 all of them run in ONE launch
  * (of the matrix-vector kernel up to 3 tokens, as unisvq_gemm does, else of
  * the small-batch kernel), with the results of unisvq_gemm on each bit for
- * bit; above that in ONE launch of the tiled product, planned over the whole
+ * bit; so also from 17 to 32 tokens when all the batch's rows make fewer than
+ * 64 tiles of 128 (unisvq_gemm's rule applied to the whole batch); otherwise
+ * in ONE launch of the tiled product, planned over the whole
  * batch, plus one reduction launch when the batch's tiles leave CUs idle and
  * K is split -- the same arithmetic as unisvq_gemm, but the K split (and so
  * the grouping of the fp32 partial sums) follows the batch, so results can
@@ -281,7 +285,7 @@ int unisvq_gemm_batched(const unisvq_gemv_problem* problems, int count, int64_t 
  *   UNISVQ_ESCRATCH (before any launch) when the product needs more than the
  *   scratch, i.e. unisvq_gemm_workspace_bytes(N, K, M, x_dtype) exceeds it:
  *   with bf16 activations the fp16 copy of x takes M*K*2 bytes (M rounded up
- *   to 16 above 32 tokens), and a product split along K takes splits*M*N*4.
+ *   to 16 above 16 tokens), and a product split along K takes splits*M*N*4.
  * Every call on a device shares that device's scratch, so calls that overlap
  * on one device (different streams, different host threads) race; calls in
  * order on one stream do not.  Nothing in the scratch needs to start at zero:

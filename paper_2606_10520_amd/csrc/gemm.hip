@@ -766,7 +766,7 @@ GemmPlan plan_gemm(int64_t N, int64_t K, int64_t M) {
 size_t align256(size_t b) { return (b + 255) & ~size_t{255}; }
 
 size_t partial_bytes(int64_t N, int64_t K, int64_t M) {
-    if (M <= kSkinnyMaxM) return 0;  // the small-batch kernel needs no partials
+    if (M <= 16) return 0;  // the small-batch kernel needs no partials (above: either kernel, see use_skinny)
     const GemmPlan p = plan_gemm(N, K, M);
     return p.splits > 1 ? static_cast<size_t>(p.splits) * M * N * 4 : 0;
 }
@@ -825,8 +825,8 @@ hipError_t launch_tiles(const GemmPlan& p, int64_t N, int64_t K, const uint8_t* 
 
 size_t gemm_workspace_bytes(int64_t N, int64_t K, int64_t M, int x_dtype) {
     size_t b = 0;
-    // (above the small-batch range the fp16 copy is tiled: tokens padded to 16)
-    const int64_t mx = M > kSkinnyMaxM ? (M + 15) / 16 * 16 : M;
+    // (above 16 tokens the fp16 copy may be the tiled one: tokens padded to 16)
+    const int64_t mx = M > 16 ? (M + 15) / 16 * 16 : M;
     if (x_dtype == UNISVQ_BF16) b += align256(static_cast<size_t>(mx) * K * 2) + align256(static_cast<size_t>(M) * 4);
     return b + partial_bytes(N, K, M);
 }
@@ -867,7 +867,8 @@ int gemm_common(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affi
     uint8_t* ws = static_cast<uint8_t*>(workspace);
     // bf16 activations for the tiled kernel (2-bit d = 4, M above the
     // small-batch range) go through the pre-pass that writes the tiled layout
-    const bool tiled = x_dtype == UNISVQ_BF16 && !var && M > kSkinnyMaxM;
+    const bool skinny = !var && use_skinny(M, N);
+    const bool tiled = x_dtype == UNISVQ_BF16 && !var && !skinny;
     if (x_dtype == UNISVQ_BF16) {
         _Float16* wxh = reinterpret_cast<_Float16*>(ws);
         ws += align256(static_cast<size_t>(tiled ? (M + 15) / 16 * 16 : M) * K * 2);
@@ -879,7 +880,7 @@ int gemm_common(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affi
         xh = wxh;
         inv = winv;
     }
-    if (!var && M <= kSkinnyMaxM)
+    if (skinny)
         return launch_skinny(N, K, packed, affine, affine_one, M, xh, inv, y, y_dtype, s) == hipSuccess
                    ? UNISVQ_OK
                    : UNISVQ_EHIP;
@@ -948,7 +949,10 @@ int launch_gemm_batch(const GemmBatchProblem* probs, int count, int64_t M, int x
     uint8_t* ws = static_cast<uint8_t*>(workspace);
     bool sliced = false;
     for (int i = 0; i < count; ++i) sliced = sliced || M > kMaxBufferBytes / (2 * probs[i].K) / 256 * 256;
-    if (M > kSkinnyMaxM && sliced) {
+    int64_t rows = 0;
+    for (int i = 0; i < count; ++i) rows += probs[i].N;
+    const bool skinny = use_skinny(M, rows);
+    if (!skinny && sliced) {
         // activations above 2 GiB: one product at a time, in token slices
         for (int i = 0; i < count; ++i) {
             const GemmBatchProblem& q = probs[i];
@@ -958,7 +962,7 @@ int launch_gemm_batch(const GemmBatchProblem* probs, int count, int64_t M, int x
         }
         return UNISVQ_OK;
     }
-    if (M > kSkinnyMaxM) {
+    if (!skinny) {
         // one tiled launch (and one reduction) for the whole batch: the bf16
         // pre-pass of each problem into its slice, then the tiles planned
         // over the batch (a K split only as far as the batch's tiles leave

@@ -160,18 +160,23 @@ def test_gemm_workspace():
     # M = 2048 fills the GPU with output tiles, so there is no split along K
     assert ws(4096, 4096, 2048, u.BF16) == 2048 * 4096 * 2 + 2048 * 4
     assert ws(4096, 4096, 2048, u.F16) == 0
-    # above the small-batch range the fp16 copy is tiled (16-token tiles): 33 tokens take 48 rows
+    # above 16 tokens the size covers the tiled fp16 copy (16-token tiles): 33 tokens take 48 rows,
+    # 17 take 32; up to 16 the row-major copy of the small-batch kernel
     assert ws(64, 256, 33, u.BF16) == 48 * 256 * 2 + 256
     assert ws(64, 256, 32, u.BF16) == 32 * 256 * 2 + 256
+    assert ws(64, 256, 17, u.BF16) == 32 * 256 * 2 + 256
+    assert ws(64, 256, 15, u.BF16) == 15 * 256 * 2 + 256
     assert ws(16, 128, 1, u.BF16) == 256 + 256
     assert ws(16, 128, 1, u.F16) == 0
     assert ws(15, 128, 1, u.BF16) == 0
     assert ws(16, 128, 0, u.BF16) == 0
     assert ws(16, 128, 1, u.F32) == 0
-    # up to 32 tokens the small-batch kernel needs nothing; a 100-token product
-    # with few output tiles is split along K: fp32 partials for every split
-    assert ws(64, 1024, 32, u.F16) == 0
-    assert ws(64, 1024, 33, u.F16) > 0
+    # up to 16 tokens the small-batch kernel needs nothing; from 17 to 32 the
+    # size also covers the tiled product (the launch's width picks the kernel);
+    # a product with few output tiles is split along K: fp32 partials for every split
+    assert ws(64, 1024, 16, u.F16) == 0
+    for m in (17, 32, 33):
+        assert ws(64, 1024, m, u.F16) > 0 and ws(64, 1024, m, u.F16) % (m * 64 * 4) == 0
     split = ws(64, 1024, 100, u.F16)
     assert split > 0 and split % (100 * 64 * 4) == 0
     # (the bf16 pre-pass's fp16 copy for the tiled kernel: 100 tokens padded to 112)

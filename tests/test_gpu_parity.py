@@ -664,10 +664,12 @@ def test_read_bytes_folds_every_word():
 def test_gemm_batched_matches_single_calls(M, dtype):
     """q/k/v-style and gate/up-style batches (different N and K in one
     launch, an odd group count), every output element against the oracle.
-    Up to 32 tokens each output equals unisvq_gemm on that problem alone bit
-    for bit (the same kernel, workgroup and summation order); above, the
-    batch plans its own K split, so the outputs equal single calls to within
-    the fp32 regrouping of the partial sums, and repeat bit for bit."""
+    Up to 32 tokens this batch (45 tiles of 128 rows, as each of its problems
+    alone) runs on the small-batch kernel, and each output equals unisvq_gemm
+    on that problem alone bit for bit (the same kernel, workgroup and
+    summation order); above, the batch plans its own K split, so the outputs
+    equal single calls to within the fp32 regrouping of the partial sums, and
+    repeat bit for bit."""
     shapes = [(4096, 4096), (1024, 4096), (512, 11008), (64, 1152)]
     probs, refs = [], []
     for i, (N, K) in enumerate(shapes):
@@ -689,6 +691,34 @@ def test_gemm_batched_matches_single_calls(M, dtype):
             assert rel_err(y.cpu().numpy(), single.cpu().numpy().astype(np.float64)) <= 1e-6, (N, K)
         assert rel_err(y.cpu().numpy(), ref) <= 5e-4
         assert rel_err(single.cpu().numpy(), ref) <= 5e-4
+
+
+@pytest.mark.parametrize("M", [17, 24, 32])
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_gemm_batched_wide_batch_above_16_tokens(M, dtype):
+    """From 17 to 32 tokens a batch of 64 or more tiles of 128 rows (here the
+    7B q+k+v shape, 96 tiles) runs on the tiled product while each problem
+    alone (32 tiles) stays on the small-batch kernel: both against the oracle
+    over every element, and against each other within the fp32 regrouping of
+    their sums."""
+    N, K = 4096, 4096
+    xb = wl.gen_activations(M, K, seed=141, dtype=dtype, outliers=True)
+    x = dev_x(xb, dtype)
+    probs, refs = [], []
+    for i in range(3):
+        Q, A, B = wl.gen_weights(N, K, seed=142 + i)
+        probs.append((upload_pack(Q, A, B), N, K, x, None))
+        refs.append(oracle.matmul(oracle.pack(Q, A, B)[0], N, K, x_as_f64(xb, dtype)))
+    outs = u.gemm_batched(probs, out_dtype=torch.float32)
+    again = u.gemm_batched(probs, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    for (pk, _, _, _, _), y, y2, ref in zip(probs, outs, again, refs):
+        single = u.gemm(pk, N, K, x, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        assert torch.equal(y, y2)
+        assert rel_err(y.cpu().numpy(), ref) <= 5e-4
+        assert rel_err(single.cpu().numpy(), ref) <= 5e-4
+        assert rel_err(y.cpu().numpy(), single.cpu().numpy().astype(np.float64)) <= 1e-5
 
 
 SPAN_SETS = {
