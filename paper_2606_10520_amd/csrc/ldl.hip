@@ -4,10 +4,10 @@
 // blocks -- the factor whose off-diagonal entries are LDLQ's feedback
 // coefficients.  All arithmetic in fp64.
 //
-// The factorisation runs from the last column block to the first, the way
-// the feedback runs from the later columns' point of view.  With S the part
-// of H not yet factorised (its upper triangle held in U's own buffer), one
-// 4 x 4 pivot block j gives
+// With U unit upper triangular the factorisation runs from the last column
+// block to the first (the last pivot is H's own last diagonal block).  With
+// S the part of H not yet factorised (its upper triangle held in U's own
+// buffer), one 4 x 4 pivot block j gives
 //     D_j = S_jj,   U[0:j, j] = S[0:j, j] D_j^-1,
 //     S[0:j, 0:j] -= U[0:j, j] D_j U[0:j, j]^T.
 // Blocked over panels of 64 columns (16 pivot blocks), right to left:
