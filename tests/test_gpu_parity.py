@@ -394,6 +394,78 @@ def test_graph_replays_match_eager():
         assert torch.equal(junk, u.gemv(pk, N, K, x1 * 2))
 
 
+def test_graph_replays_cover_every_launch_family():
+    """Every other launch family captured in one HIP graph, with eager work
+    (fills and launches of the same kernels on other inputs) between the
+    replays; each replay reproduces the eager results bit for bit: batched
+    small-batch launches (16 tokens, workgroups across problems; 24 tokens,
+    two token tiles), a wide 24-token batch (tiled, K split and reduction),
+    bf16 activations (row-major and tiled pre-passes), row-shared pairs with the Eq. 9 fold (its pre-pass),
+    the input transform fused into the matrix-vector product, standalone
+    transforms (fast Walsh-Hadamard and Paley orders) and a 3-bit d = 8
+    variant product."""
+    K = 4096
+    probs = []
+    for i in range(3):
+        Q, A, B = wl.gen_weights(1024, K, seed=150 + i)
+        probs.append(upload_pack(Q, A, B))
+    wide = []  # 3 x 4096 rows: 96 tiles of 128, the tiled product at 24 tokens
+    for i in range(3):
+        Q, A, B = wl.gen_weights(4096, K, seed=170 + i)
+        wide.append(upload_pack(Q, A, B))
+    x16 = dev_x(wl.gen_activations(16, K, seed=151, outliers=True), "f16")
+    x24 = dev_x(wl.gen_activations(24, K, seed=152), "f16")
+    xb16 = dev_x(wl.gen_activations(16, K, seed=153, dtype="bf16"), "bf16")
+    xb64 = dev_x(wl.gen_activations(64, K, seed=154, dtype="bf16"), "bf16")
+    Qs, As, Bs = wl.gen_shared_weights(1024, K, 1, seed=155)
+    pc, pa = upload_shared(Qs, As, Bs)
+    signs = torch.from_numpy(np.random.default_rng(156).choice(np.array([-1, 1], dtype=np.int8), K)).to(DEV)
+    x1 = dev_x(wl.gen_activations(1, K, seed=157), "f16")
+    xr = dev_x(wl.gen_activations(2, 11008, seed=158), "f16")
+    sr = torch.from_numpy(np.random.default_rng(159).choice(np.array([-1, 1], dtype=np.int8), 11008)).to(DEV)
+    Qv, Av, Bv = wl.gen_var_weights(1024, K, 3, 8, 1, seed=160)
+    vc, va = u.var_pack(torch.from_numpy(Qv).to(DEV), dev_u16_as_half(Av), dev_u16_as_half(Bv), 3, 8)
+    torch.cuda.synchronize()
+
+    def run(outs=None):
+        o = outs or {}
+        r = {}
+        r["b16"] = u.gemm_batched([(pk, 1024, K, x16, o.get("b16", [None] * 3)[i]) for i, pk in enumerate(probs)])
+        r["b24"] = u.gemm_batched([(pk, 1024, K, x24, o.get("b24", [None] * 3)[i]) for i, pk in enumerate(probs)],
+                                  out_dtype=torch.float32)
+        r["w24"] = u.gemm_batched([(pk, 4096, K, x24, o.get("w24", [None] * 3)[i]) for i, pk in enumerate(wide)],
+                                  out_dtype=torch.float32)
+        r["bf16"] = [u.gemm(probs[0], 1024, K, xb16, out=o.get("bf16", [None])[0], out_dtype=torch.float32)]
+        r["bf64"] = [u.gemm(probs[1], 1024, K, xb64, out=o.get("bf64", [None])[0], out_dtype=torch.float32)]
+        r["fold"] = [u.gemm_shared_fold(pc, pa, 1024, K, 1, xb64, out=o.get("fold", [None])[0],
+                                        out_dtype=torch.float32)]
+        r["rht"] = u.gemv_rht_batched([(probs[2], 1024, K, x1, signs, o.get("rht", [None])[0])])
+        r["fwht"] = [u.rht(x16, signs, "out", out=o.get("fwht", [None])[0])]
+        r["paley"] = [u.rht(xr, sr, "in", out=o.get("paley", [None])[0])]
+        r["var"] = [u.var_gemv(vc, va, 1024, K, 3, 8, 1, x1, out=o.get("var", [None])[0])]
+        return r
+
+    eager = {k: [t.clone() for t in v] for k, v in run().items()}
+    outs = run()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run(outs)
+    for rep in range(3):
+        for v in outs.values():
+            for t in v:
+                t.fill_(7.0)                                       # eager work between replays
+        junk = u.gemm_batched([(pk, 1024, K, x16 * 2, None) for pk in probs])  # the same kernels, eagerly
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k in eager:
+            for a, b in zip(outs[k], eager[k]):
+                assert torch.equal(a, b), (k, rep)
+        assert all(torch.equal(a, b) for a, b in zip(junk, u.gemm_batched([(pk, 1024, K, x16 * 2, None)
+                                                                            for pk in probs])))
+
+
 # ------------------------------------------- row-shared affine parameters
 
 def upload_shared(Q, A, B):
