@@ -200,19 +200,6 @@ int launch_gemm_var(int64_t N, int64_t K, int bits, int d, const uint8_t* packed
 // matrix-vector kernel's LDS cannot hold the activations.
 constexpr int64_t kSkinnyMaxM = 32;
 constexpr int64_t kGemvMaxM = 3;
-// Above 16 tokens the small-batch kernel takes two token tiles and one row
-// block per workgroup, and beats the tiled product only on narrow batches:
-// 7B decoder step at 20 / 24 / 32 tokens, per launch, small-batch against
-// tiled: o (4096 rows) 10.0 / 10.6 / 11.9 against 15.3 / 15.5 / 16.1 us, down
-// (4096 rows) 21.6 / 22.8 / 26.3 against 24.8 / 25.3 / 25.7, q+k+v (12288)
-// 25.2 / 27.2 / 31.1 against 24.3 / 24.5 / 24.8, gate+up (22016) 47.9 / 51.9 /
-// 59.9 against 37.2 / 38.7 / 39.0.  So from 17 to 32 tokens a batch goes to
-// the small-batch kernel only when it has fewer than this many 128-row tiles.
-constexpr int64_t kSkinnyWideMaxTiles = 64;
-// The small-batch kernel for M tokens over a batch of `rows` output rows in all.
-inline bool use_skinny(int64_t M, int64_t rows) {
-    return M <= 16 || (M <= kSkinnyMaxM && (rows + 127) / 128 < kSkinnyWideMaxTiles);
-}
 hipError_t launch_skinny(int64_t N, int64_t K, const uint8_t* packed, const uint8_t* affine, int affine_one,
                          int64_t M, const _Float16* x, const float* inv_scale, void* y, int y_dtype, hipStream_t s);
 // Several independent small-batch products (same M, the same weight format)
